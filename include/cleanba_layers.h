@@ -1,0 +1,76 @@
+/*
+ * cleanba_layers.h -- layer-level entry points of the learner-update library.
+ *
+ * Each call runs one step of the IMPALA-ResNet forward or backward pass (the network the
+ * paper trains with, Section 5) on activations in the library's storage type:
+ * IMPALA_PREC_BF16 stores activations as bf16 bit patterns (uint16, round to nearest even)
+ * and computes on bf16 matrix cores with float32 accumulation; IMPALA_PREC_FP32 stores
+ * and computes in float32. Weights and weight gradients are float32 HWIO [3,3,cin,cout].
+ * Conventions (memory, streams, errors, determinism) are those of cleanba_learner.h.
+ * Supported channel pairs are those the network uses: cin == 4 for uint8 frames, else
+ * cin, cout in {16, 32, 64} with cin <= cout (cin == cout when x_mode is IMPALA_X_RELU).
+ */
+#ifndef CLEANBA_LAYERS_H
+#define CLEANBA_LAYERS_H
+
+#include "cleanba_learner.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    IMPALA_X_PLAIN = 0,  /* x as stored */
+    IMPALA_X_RELU = 1,   /* relu(x), applied while loading */
+    IMPALA_X_U8 = 2      /* uint8 frames obs[row_idx[i]] (row_idx may be NULL), cin == 4;
+                            the convolution sum is scaled by 1/255 */
+} impala_x_mode_t;
+
+/* y = conv3x3_same(X, w) + bias [+ add], X = x, relu(x) or frames/255 per x_mode.
+ * x: [n, H, W, cin]; bias: float [cout] or NULL; add: [n, H, W, cout] or NULL;
+ * y: [n, H, W, cout]. */
+impala_status_t impala_conv3x3_fwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W,
+                                   int32_t cin, int32_t cout, const void* x, int32_t x_mode,
+                                   const int32_t* row_idx, const float* w, const float* bias,
+                                   const void* add, void* y, hipStream_t stream);
+
+/* Input gradient of y = conv3x3_same(x, w): dx = conv3x3_same^T(dy, w), then
+ * dx *= (mask > 0) if mask is not NULL, then dx += add if add is not NULL.
+ * dy: [n, H, W, cout]; mask, add, dx: [n, H, W, cin]. */
+impala_status_t impala_conv3x3_dgrad(impala_prec_t prec, int64_t n, int32_t H, int32_t W,
+                                     int32_t cin, int32_t cout, const void* dy, const float* w,
+                                     const void* mask, const void* add, void* dx,
+                                     hipStream_t stream);
+
+/* Weight and bias gradient: dw[ky][kx][ci][co] = sum over pixels of X_pad[h+ky][w+kx][ci]
+ * dy[h][w][co] (X per x_mode; with uint8 frames the sum is scaled by 1/255), db[co] = sum dy.
+ * dw: float [3,3,cin,cout]; db: float [cout]; ws: device scratch of
+ * impala_conv3x3_wgrad_workspace_bytes() bytes. */
+size_t impala_conv3x3_wgrad_workspace_bytes(impala_prec_t prec, int32_t H, int32_t W, int32_t cin,
+                                            int32_t cout);
+impala_status_t impala_conv3x3_wgrad(impala_prec_t prec, int64_t n, int32_t H, int32_t W,
+                                     int32_t cin, int32_t cout, const void* x, int32_t x_mode,
+                                     const int32_t* row_idx, const void* dy, float* dw, float* db,
+                                     void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* 3x3 stride-2 SAME max-pool with XLA's padding split (pad_lo = P/2) and -inf padding.
+ * x: [n, H, W, C]; y: [n, ceil(H/2), ceil(W/2), C]; arg: uint8, same shape as y, the
+ * row-major window index 0..8 of the first maximum. C % 4 == 0. */
+impala_status_t impala_maxpool_fwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t C,
+                                   const void* x, void* y, uint8_t* arg, hipStream_t stream);
+
+/* Max-pool input gradient: dx[cell] = sum of dy over the windows whose argmax is the cell. */
+impala_status_t impala_maxpool_bwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t C,
+                                   const uint8_t* arg, const void* dy, void* dx,
+                                   hipStream_t stream);
+
+/* Gumbel-max sampling on given logits: actions[i] = argmax_j (logits[i][j] + gumbel[i][j])
+ * (float32 sums, ties to the lowest index) and logp[i] = log_softmax(logits[i])[actions[i]]. */
+impala_status_t impala_gumbel_sample(int64_t n, int32_t A, const float* logits,
+                                     const float* gumbel, int32_t* actions, float* logp,
+                                     hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CLEANBA_LAYERS_H */

@@ -1,0 +1,528 @@
+// C-ABI of the learner-update library: argument validation on the host (before any HIP
+// call), workspace planning, and the learning-phase orchestration of Algorithm 1.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "../../include/cleanba_layers.h"
+#include "../../include/cleanba_learner.h"
+#include "kernels.h"
+#include "plan.h"
+
+using namespace cb;
+
+namespace {
+
+thread_local std::string g_err;
+
+impala_status_t fail(impala_status_t code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+impala_status_t ok() {
+    g_err.clear();
+    return IMPALA_OK;
+}
+
+impala_status_t hip_status(hipError_t e, const char* where) {
+    if (e == hipSuccess) return ok();
+    return fail(IMPALA_EHIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+#define CHECK_PTR(p) \
+    if (!(p)) return fail(IMPALA_EINVAL, "%s: argument '%s' is NULL", __func__, #p)
+
+bool valid_prec(int p) { return p == IMPALA_PREC_BF16 || p == IMPALA_PREC_FP32; }
+
+// Learner workspace layout (bytes from the start of ws).
+struct LearnerLayout {
+    NetPlan plan;
+    size_t cnn, adv, ret, tlogp, logits, value, dlogits, dvalue, grads, apart;
+    size_t total;
+    int64_t fwd_rows, mb;
+};
+
+size_t a256(size_t x) { return (x + 255) / 256 * 256; }
+
+std::string check_cfg(const learner_cfg_t* c) {
+    if (!c) return "cfg is NULL";
+    if (c->algo != LEARNER_PPO && c->algo != LEARNER_IMPALA) return "cfg.algo must be PPO or IMPALA";
+    if (!valid_prec(c->prec)) return "cfg.prec must be BF16 or FP32";
+    if (c->T < 1 || c->E < 1) return "cfg.T and cfg.E must be >= 1";
+    if (int64_t(c->T) * c->E > (int64_t(1) << 26)) return "cfg.T * cfg.E too large";
+    if (c->algo == LEARNER_PPO) {
+        if (c->update_epochs < 1 || c->num_minibatches < 1 || c->minibatch_size < 1)
+            return "PPO needs update_epochs, num_minibatches, minibatch_size >= 1";
+        if (int64_t(c->num_minibatches) * c->minibatch_size > int64_t(c->T) * c->E)
+            return "num_minibatches * minibatch_size exceeds T * E";
+    }
+    if (!(c->lr >= 0.f) || !(c->adam_eps >= 0.f) || !(c->beta1 >= 0.f && c->beta1 < 1.f) ||
+        !(c->beta2 >= 0.f && c->beta2 < 1.f))
+        return "cfg Adam hyperparameters out of range";
+    return "";
+}
+
+LearnerLayout learner_layout(const impala_net_t& net, const learner_cfg_t& c) {
+    LearnerLayout L;
+    const int64_t TE = int64_t(c.T) * c.E;
+    const int A = net.num_actions;
+    L.mb = c.algo == LEARNER_PPO ? c.minibatch_size : TE;
+    L.fwd_rows = c.algo == LEARNER_PPO ? c.minibatch_size : TE + c.E;
+    L.plan = make_plan(net, c.prec, L.fwd_rows, 1);
+    size_t off = 0;
+    auto take = [&](size_t bytes) { const size_t o = off; off += a256(bytes); return o; };
+    L.cnn = take(L.plan.total);
+    L.adv = take(TE * sizeof(float));
+    L.ret = take(TE * sizeof(float));
+    L.tlogp = take(TE * sizeof(float));
+    L.logits = take(size_t(L.fwd_rows) * A * sizeof(float));
+    L.value = take(size_t(L.fwd_rows) * sizeof(float));
+    L.dlogits = take(size_t(L.mb) * A * sizeof(float));
+    L.dvalue = take(size_t(L.mb) * sizeof(float));
+    L.grads = take(size_t(L.plan.po.total) * sizeof(float));
+    L.apart = take(adam_partial_floats(L.plan.po.total) * sizeof(float));
+    L.total = off;
+    return L;
+}
+
+}  // namespace
+
+namespace cb {
+
+__global__ void fill_zero_kernel(float* p, int64_t n) {
+    const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    if (i < n) p[i] = 0.f;
+}
+
+size_t lds_limit() {
+    static thread_local int dev_cached = -1;
+    static thread_local size_t bytes = 64 * 1024;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 64 * 1024;
+    if (dev != dev_cached) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess && v > 0)
+            bytes = size_t(v);
+        dev_cached = dev;
+    }
+    return bytes;
+}
+
+hipError_t fill_zero(float* p, int64_t n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_zero_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, p, n);
+    return hipGetLastError();
+}
+
+}  // namespace cb
+
+extern "C" {
+
+const char* impala_last_error(void) { return g_err.c_str(); }
+
+int64_t impala_param_count(const impala_net_t* net) {
+    const std::string e = check_net(net);
+    if (!e.empty()) { fail(IMPALA_EINVAL, "impala_param_count: %s", e.c_str()); return -1; }
+    ok();
+    return param_offsets(*net).total;
+}
+
+int impala_param_layout(const impala_net_t* net, impala_tensor_desc_t* out, int cap) {
+    const std::string e = check_net(net);
+    if (!e.empty()) return fail(IMPALA_EINVAL, "impala_param_layout: %s", e.c_str());
+    if (!out && cap > 0) return fail(IMPALA_EINVAL, "impala_param_layout: out is NULL");
+    const ParamOffsets po = param_offsets(*net);
+    int k = 0;
+    auto put = [&](const char* name, int64_t off, int nd, int s0, int s1, int s2, int s3) {
+        if (k < cap) {
+            impala_tensor_desc_t& d = out[k];
+            std::memset(&d, 0, sizeof(d));
+            std::snprintf(d.name, sizeof(d.name), "%s", name);
+            d.offset = off; d.ndim = nd;
+            d.shape[0] = s0; d.shape[1] = s1; d.shape[2] = s2; d.shape[3] = s3;
+        }
+        ++k;
+    };
+    int cin = net->in_c;
+    char nm[32];
+    for (int s = 0; s < 3; ++s) {
+        const int c = net->ch[s];
+        std::snprintf(nm, sizeof(nm), "s%d.conv.w", s); put(nm, po.conv_w[s][0], 4, 3, 3, cin, c);
+        std::snprintf(nm, sizeof(nm), "s%d.conv.b", s); put(nm, po.conv_b[s][0], 1, c, 0, 0, 0);
+        for (int r = 0; r < 2; ++r)
+            for (int q = 0; q < 2; ++q) {
+                std::snprintf(nm, sizeof(nm), "s%d.res%d.conv%d.w", s, r, q);
+                put(nm, po.conv_w[s][1 + 2 * r + q], 4, 3, 3, c, c);
+                std::snprintf(nm, sizeof(nm), "s%d.res%d.conv%d.b", s, r, q);
+                put(nm, po.conv_b[s][1 + 2 * r + q], 1, c, 0, 0, 0);
+            }
+        cin = c;
+    }
+    const int flat = int((po.dense_b - po.dense_w) / net->hidden);
+    put("dense.w", po.dense_w, 2, flat, net->hidden, 0, 0);
+    put("dense.b", po.dense_b, 1, net->hidden, 0, 0, 0);
+    put("logits.w", po.logits_w, 2, net->hidden, net->num_actions, 0, 0);
+    put("logits.b", po.logits_b, 1, net->num_actions, 0, 0, 0);
+    put("value.w", po.value_w, 2, net->hidden, 1, 0, 0);
+    put("value.b", po.value_b, 1, 1, 0, 0, 0);
+    ok();
+    return k;
+}
+
+size_t impala_workspace_bytes(const impala_net_t* net, int64_t n_frames, impala_prec_t prec,
+                              int training) {
+    const std::string e = check_net(net);
+    if (!e.empty()) { fail(IMPALA_EINVAL, "impala_workspace_bytes: %s", e.c_str()); return 0; }
+    if (!valid_prec(prec) || n_frames < 0) { fail(IMPALA_EINVAL, "impala_workspace_bytes: bad prec or n"); return 0; }
+    ok();
+    return make_plan(*net, prec, n_frames > 0 ? n_frames : 1, training ? 1 : 0).total;
+}
+
+impala_status_t impala_cnn_fwd(const impala_net_t* net, impala_prec_t prec, const float* params,
+                               const uint8_t* obs, const int32_t* row_idx, int64_t n, void* ws,
+                               size_t ws_bytes, int training, float* logits, float* value,
+                               hipStream_t stream) {
+    const std::string e = check_net(net);
+    if (!e.empty()) return fail(IMPALA_EINVAL, "impala_cnn_fwd: %s", e.c_str());
+    if (!valid_prec(prec)) return fail(IMPALA_EINVAL, "impala_cnn_fwd: bad prec %d", int(prec));
+    if (n < 0 || n > (int64_t(1) << 24)) return fail(IMPALA_EINVAL, "impala_cnn_fwd: n out of range");
+    if (n == 0) return ok();
+    CHECK_PTR(params); CHECK_PTR(obs); CHECK_PTR(ws); CHECK_PTR(logits); CHECK_PTR(value);
+    const NetPlan p = make_plan(*net, prec, n, training ? 1 : 0);
+    if (ws_bytes < p.total)
+        return fail(IMPALA_EWORKSPACE, "impala_cnn_fwd: workspace %zu < %zu bytes", ws_bytes, p.total);
+    return hip_status(run_forward(p, params, obs, row_idx, n, static_cast<char*>(ws), logits, value, stream),
+                      "impala_cnn_fwd");
+}
+
+impala_status_t impala_cnn_bwd(const impala_net_t* net, impala_prec_t prec, const float* params,
+                               const uint8_t* obs, const int32_t* row_idx, int64_t n, void* ws,
+                               size_t ws_bytes, const float* dlogits, const float* dvalue,
+                               float* grads, hipStream_t stream) {
+    const std::string e = check_net(net);
+    if (!e.empty()) return fail(IMPALA_EINVAL, "impala_cnn_bwd: %s", e.c_str());
+    if (!valid_prec(prec)) return fail(IMPALA_EINVAL, "impala_cnn_bwd: bad prec %d", int(prec));
+    if (n < 0 || n > (int64_t(1) << 24)) return fail(IMPALA_EINVAL, "impala_cnn_bwd: n out of range");
+    CHECK_PTR(params); CHECK_PTR(grads);
+    const NetPlan p = make_plan(*net, prec, n > 0 ? n : 1, 1);
+    if (n == 0) return hip_status(fill_zero(grads, p.po.total, stream), "impala_cnn_bwd");
+    CHECK_PTR(obs); CHECK_PTR(ws); CHECK_PTR(dlogits); CHECK_PTR(dvalue);
+    if (ws_bytes < p.total)
+        return fail(IMPALA_EWORKSPACE, "impala_cnn_bwd: workspace %zu < %zu bytes", ws_bytes, p.total);
+    return hip_status(run_backward(p, params, obs, row_idx, n, static_cast<char*>(ws), dlogits, dvalue,
+                                   grads, stream),
+                      "impala_cnn_bwd");
+}
+
+impala_status_t gae_advantages(int32_t T, int32_t E, const float* rewards, const float* values,
+                               const uint8_t* dones, const float* next_value,
+                               const uint8_t* next_done, float gamma, float lambda, float* adv,
+                               float* ret, hipStream_t stream) {
+    if (T < 0 || E < 0) return fail(IMPALA_EINVAL, "gae_advantages: T and E must be >= 0");
+    if (T == 0 || E == 0) return ok();
+    CHECK_PTR(rewards); CHECK_PTR(values); CHECK_PTR(dones); CHECK_PTR(next_value);
+    CHECK_PTR(next_done); CHECK_PTR(adv); CHECK_PTR(ret);
+    return hip_status(gae(T, E, rewards, values, dones, next_value, next_done, gamma, lambda, adv, ret, stream),
+                      "gae_advantages");
+}
+
+impala_status_t vtrace_targets(int32_t T, int32_t E, const float* behav_logp,
+                               const float* target_logp, const float* rewards, const float* values,
+                               const uint8_t* dones, const float* bootstrap_value,
+                               const uint8_t* next_done, float gamma, float lambda, float rho_bar,
+                               float c_bar, float pg_rho_bar, float* vs, float* pg_adv,
+                               hipStream_t stream) {
+    if (T < 0 || E < 0) return fail(IMPALA_EINVAL, "vtrace_targets: T and E must be >= 0");
+    if (T == 0 || E == 0) return ok();
+    CHECK_PTR(behav_logp); CHECK_PTR(target_logp); CHECK_PTR(rewards); CHECK_PTR(values);
+    CHECK_PTR(dones); CHECK_PTR(bootstrap_value); CHECK_PTR(next_done); CHECK_PTR(vs); CHECK_PTR(pg_adv);
+    return hip_status(vtrace(T, E, behav_logp, target_logp, rewards, values, dones, bootstrap_value,
+                             next_done, gamma, lambda, rho_bar, c_bar, pg_rho_bar, vs, pg_adv, stream),
+                      "vtrace_targets");
+}
+
+impala_status_t ppo_loss_grad(int64_t m, int32_t A, const float* logits, const float* value,
+                              const int32_t* actions, const float* old_logp, const float* adv,
+                              const float* ret, int32_t norm_adv, float clip_eps, float vf_coef,
+                              float ent_coef, float* dlogits, float* dvalue, float* stats,
+                              hipStream_t stream) {
+    if (m < 1 || m > (int64_t(1) << 26)) return fail(IMPALA_EINVAL, "ppo_loss_grad: m out of range");
+    if (A < 1 || A > 64) return fail(IMPALA_EINVAL, "ppo_loss_grad: A must be in [1, 64]");
+    CHECK_PTR(logits); CHECK_PTR(value); CHECK_PTR(actions); CHECK_PTR(old_logp); CHECK_PTR(adv);
+    CHECK_PTR(ret); CHECK_PTR(dlogits); CHECK_PTR(dvalue); CHECK_PTR(stats);
+    return hip_status(ppo_loss(m, A, logits, value, actions, old_logp, adv, ret, nullptr, norm_adv,
+                               clip_eps, vf_coef, ent_coef, dlogits, dvalue, stats, stream),
+                      "ppo_loss_grad");
+}
+
+impala_status_t impala_loss_grad(int64_t m, int32_t A, const float* logits, const float* value,
+                                 const int32_t* actions, const float* vs, const float* pg_adv,
+                                 float pg_coef, float vf_coef, float ent_coef, float* dlogits,
+                                 float* dvalue, float* stats, hipStream_t stream) {
+    if (m < 1 || m > (int64_t(1) << 26)) return fail(IMPALA_EINVAL, "impala_loss_grad: m out of range");
+    if (A < 1 || A > 64) return fail(IMPALA_EINVAL, "impala_loss_grad: A must be in [1, 64]");
+    CHECK_PTR(logits); CHECK_PTR(value); CHECK_PTR(actions); CHECK_PTR(vs); CHECK_PTR(pg_adv);
+    CHECK_PTR(dlogits); CHECK_PTR(dvalue); CHECK_PTR(stats);
+    return hip_status(impala_loss(m, A, logits, value, actions, vs, pg_adv, pg_coef, vf_coef, ent_coef,
+                                  dlogits, dvalue, stats, stream),
+                      "impala_loss_grad");
+}
+
+namespace {
+struct AdamConsts { float omb1, omb2, bc1, bc2; };
+
+// 1 - beta and the bias corrections 1 - beta^t of the caller's float betas, formed in double
+// (in float, 1 - beta would lose the low bits of beta: for 0.999f about 1e-5 relative).
+AdamConsts adam_consts(int32_t step, float b1, float b2) {
+    AdamConsts c;
+    c.omb1 = float(1.0 - double(b1));
+    c.omb2 = float(1.0 - double(b2));
+    c.bc1 = float(1.0 - std::pow(double(b1), double(step)));
+    c.bc2 = float(1.0 - std::pow(double(b2), double(step)));
+    return c;
+}
+}  // namespace
+
+size_t adam_workspace_bytes(int64_t n_params) {
+    return adam_partial_floats(n_params > 0 ? n_params : 1) * sizeof(float);
+}
+
+impala_status_t adam_step(int64_t n_params, float* params, const float* grads, float* m, float* v,
+                          int32_t step, float lr, float beta1, float beta2, float eps,
+                          float max_grad_norm, float* stats, void* ws, size_t ws_bytes,
+                          hipStream_t stream) {
+    if (n_params < 0) return fail(IMPALA_EINVAL, "adam_step: n_params < 0");
+    if (step < 1) return fail(IMPALA_EINVAL, "adam_step: step is 1-based");
+    if (!(beta1 >= 0.f && beta1 < 1.f && beta2 >= 0.f && beta2 < 1.f))
+        return fail(IMPALA_EINVAL, "adam_step: betas must be in [0, 1)");
+    if (n_params == 0) return ok();
+    CHECK_PTR(params); CHECK_PTR(grads); CHECK_PTR(m); CHECK_PTR(v); CHECK_PTR(ws);
+    const size_t need = adam_workspace_bytes(n_params);
+    if (ws_bytes < need) return fail(IMPALA_EWORKSPACE, "adam_step: workspace %zu < %zu bytes", ws_bytes, need);
+    const AdamConsts ac = adam_consts(step, beta1, beta2);
+    return hip_status(adam(n_params, params, grads, m, v, lr, beta1, beta2, ac.omb1, ac.omb2, ac.bc1, ac.bc2,
+                           eps, max_grad_norm, stats, static_cast<float*>(ws), stream),
+                      "adam_step");
+}
+
+size_t learner_workspace_bytes(const impala_net_t* net, const learner_cfg_t* cfg) {
+    std::string e = check_net(net);
+    if (e.empty()) e = check_cfg(cfg);
+    if (!e.empty()) { fail(IMPALA_EINVAL, "learner_workspace_bytes: %s", e.c_str()); return 0; }
+    ok();
+    return learner_layout(*net, *cfg).total;
+}
+
+impala_status_t learner_step(const impala_net_t* net, const learner_cfg_t* cfg,
+                             const rollout_t* ro, float* params, float* m, float* v,
+                             int32_t* step, const int32_t* perm, void* ws, size_t ws_bytes,
+                             float* stats, hipStream_t stream) {
+    std::string e = check_net(net);
+    if (e.empty()) e = check_cfg(cfg);
+    if (!e.empty()) return fail(IMPALA_EINVAL, "learner_step: %s", e.c_str());
+    CHECK_PTR(ro); CHECK_PTR(params); CHECK_PTR(m); CHECK_PTR(v); CHECK_PTR(step); CHECK_PTR(ws);
+    CHECK_PTR(stats);
+    CHECK_PTR(ro->obs); CHECK_PTR(ro->actions); CHECK_PTR(ro->behav_logp); CHECK_PTR(ro->rewards);
+    CHECK_PTR(ro->dones); CHECK_PTR(ro->next_done);
+    if (*step < 0) return fail(IMPALA_EINVAL, "learner_step: *step must be >= 0");
+    const learner_cfg_t& c = *cfg;
+    if (c.algo == LEARNER_PPO) {
+        CHECK_PTR(ro->values); CHECK_PTR(ro->next_value); CHECK_PTR(perm);
+    }
+    const LearnerLayout L = learner_layout(*net, c);
+    if (ws_bytes < L.total)
+        return fail(IMPALA_EWORKSPACE, "learner_step: workspace %zu < %zu bytes", ws_bytes, L.total);
+    char* w = static_cast<char*>(ws);
+    const NetPlan& P = L.plan;
+    const int A = net->num_actions;
+    const int64_t TE = int64_t(c.T) * c.E;
+    float* grads = reinterpret_cast<float*>(w + L.grads);
+    float* apart = reinterpret_cast<float*>(w + L.apart);
+    float* logits = reinterpret_cast<float*>(w + L.logits);
+    float* value = reinterpret_cast<float*>(w + L.value);
+    float* dlogits = reinterpret_cast<float*>(w + L.dlogits);
+    float* dvalue = reinterpret_cast<float*>(w + L.dvalue);
+    char* cnn = w + L.cnn;
+    hipError_t he;
+#define LS_TRY(x, what) \
+    if ((he = (x)) != hipSuccess) return hip_status(he, what)
+
+    if (c.algo == LEARNER_PPO) {
+        float* adv = reinterpret_cast<float*>(w + L.adv);
+        float* ret = reinterpret_cast<float*>(w + L.ret);
+        LS_TRY(gae(c.T, c.E, ro->rewards, ro->values, ro->dones, ro->next_value, ro->next_done, c.gamma,
+                   c.lambda, adv, ret, stream), "learner_step: gae");
+        int u = 0;
+        for (int j = 0; j < c.update_epochs; ++j) {
+            for (int k = 0; k < c.num_minibatches; ++k, ++u) {
+                const int32_t* rows = perm + int64_t(j) * TE + int64_t(k) * c.minibatch_size;
+                const int64_t mb = c.minibatch_size;
+                LS_TRY(run_forward(P, params, ro->obs, rows, mb, cnn, logits, value, stream),
+                       "learner_step: forward");
+                LS_TRY(ppo_loss(mb, A, logits, value, ro->actions, ro->behav_logp, adv, ret, rows,
+                                c.norm_adv, c.clip_eps, c.vf_coef, c.ent_coef, dlogits, dvalue,
+                                stats + 8 * u, stream), "learner_step: ppo loss");
+                LS_TRY(run_backward(P, params, ro->obs, rows, mb, cnn, dlogits, dvalue, grads, stream),
+                       "learner_step: backward");
+                *step += 1;
+                const AdamConsts ac = adam_consts(*step, c.beta1, c.beta2);
+                LS_TRY(adam(P.po.total, params, grads, m, v, c.lr, c.beta1, c.beta2, ac.omb1, ac.omb2, ac.bc1,
+                            ac.bc2, c.adam_eps, c.max_grad_norm, stats + 8 * u + 6, apart, stream),
+                       "learner_step: adam");
+            }
+        }
+    } else {
+        float* tlogp = reinterpret_cast<float*>(w + L.tlogp);
+        float* vs = reinterpret_cast<float*>(w + L.adv);
+        float* pg = reinterpret_cast<float*>(w + L.ret);
+        const int64_t n1 = TE + c.E;
+        LS_TRY(run_forward(P, params, ro->obs, nullptr, n1, cnn, logits, value, stream),
+               "learner_step: forward");
+        LS_TRY(action_logp(TE, A, logits, ro->actions, tlogp, stream), "learner_step: logp");
+        LS_TRY(vtrace(c.T, c.E, ro->behav_logp, tlogp, ro->rewards, value, ro->dones, value + TE,
+                      ro->next_done, c.gamma, c.lambda, c.rho_bar, c.c_bar, c.pg_rho_bar, vs, pg, stream),
+               "learner_step: vtrace");
+        LS_TRY(impala_loss(TE, A, logits, value, ro->actions, vs, pg, c.pg_coef, c.vf_coef, c.ent_coef,
+                           dlogits, dvalue, stats, stream), "learner_step: impala loss");
+        LS_TRY(run_backward(P, params, ro->obs, nullptr, TE, cnn, dlogits, dvalue, grads, stream),
+               "learner_step: backward");
+        *step += 1;
+        const AdamConsts ac = adam_consts(*step, c.beta1, c.beta2);
+        LS_TRY(adam(P.po.total, params, grads, m, v, c.lr, c.beta1, c.beta2, ac.omb1, ac.omb2, ac.bc1, ac.bc2,
+                    c.adam_eps, c.max_grad_norm, stats + 6, apart, stream), "learner_step: adam");
+    }
+#undef LS_TRY
+    return ok();
+}
+
+impala_status_t impala_actor_step(const impala_net_t* net, impala_prec_t prec, const float* params,
+                                  const uint8_t* obs, int64_t n, const float* gumbel, void* ws,
+                                  size_t ws_bytes, int32_t* actions, float* logp, float* value,
+                                  float* logits, hipStream_t stream) {
+    const std::string e = check_net(net);
+    if (!e.empty()) return fail(IMPALA_EINVAL, "impala_actor_step: %s", e.c_str());
+    if (!valid_prec(prec)) return fail(IMPALA_EINVAL, "impala_actor_step: bad prec");
+    if (n < 0 || n > (int64_t(1) << 24)) return fail(IMPALA_EINVAL, "impala_actor_step: n out of range");
+    if (n == 0) return ok();
+    CHECK_PTR(params); CHECK_PTR(obs); CHECK_PTR(gumbel); CHECK_PTR(ws); CHECK_PTR(actions);
+    CHECK_PTR(logp); CHECK_PTR(value);
+    const NetPlan p = make_plan(*net, prec, n, 0);
+    const size_t extra = logits ? 0 : a256(size_t(n) * net->num_actions * sizeof(float));
+    if (ws_bytes < p.total + extra)
+        return fail(IMPALA_EWORKSPACE, "impala_actor_step: workspace %zu < %zu bytes (add n*A*4 when logits is NULL)",
+                    ws_bytes, p.total + extra);
+    float* z = logits ? logits : reinterpret_cast<float*>(static_cast<char*>(ws) + p.total);
+    hipError_t he = run_forward(p, params, obs, nullptr, n, static_cast<char*>(ws), z, value, stream);
+    if (he != hipSuccess) return hip_status(he, "impala_actor_step: forward");
+    return hip_status(gumbel_max(n, net->num_actions, z, gumbel, actions, logp, stream),
+                      "impala_actor_step: sample");
+}
+
+// ------------------------------------------------------------------ layer-level entry points
+
+static impala_status_t check_layer(const char* fn, int prec, int64_t n, int H, int W, int cin, int cout) {
+    if (!valid_prec(prec)) return fail(IMPALA_EINVAL, "%s: bad prec", fn);
+    if (n < 0 || n > (int64_t(1) << 24) || H < 1 || W < 1 || H > 256 || W > 256)
+        return fail(IMPALA_EINVAL, "%s: shape out of range", fn);
+    (void)cin; (void)cout;
+    return IMPALA_OK;
+}
+
+impala_status_t impala_conv3x3_fwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t cin,
+                                   int32_t cout, const void* x, int32_t x_mode,
+                                   const int32_t* row_idx, const float* w, const float* bias,
+                                   const void* add, void* y, hipStream_t stream) {
+    impala_status_t st = check_layer(__func__, prec, n, H, W, cin, cout);
+    if (st) return st;
+    if (x_mode < 0 || x_mode > 2 || !conv3x3_supported(cin, cout, x_mode, 0))
+        return fail(IMPALA_EUNSUPPORTED, "impala_conv3x3_fwd: unsupported cin=%d cout=%d x_mode=%d", cin, cout, x_mode);
+    if (n == 0) return ok();
+    CHECK_PTR(x); CHECK_PTR(w); CHECK_PTR(y);
+    ConvArgs a{};
+    a.x = x; a.row_idx = x_mode == IN_U8 ? row_idx : nullptr; a.w = w; a.bias = bias; a.add = add;
+    a.y = y; a.n = int(n); a.H = H; a.W = W; a.scale = x_mode == IN_U8 ? 1.f / 255.f : 1.f;
+    return hip_status(conv3x3(prec, cin, cout, x_mode, 0, a, stream), "impala_conv3x3_fwd");
+}
+
+impala_status_t impala_conv3x3_dgrad(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t cin,
+                                     int32_t cout, const void* dy, const float* w, const void* mask,
+                                     const void* add, void* dx, hipStream_t stream) {
+    impala_status_t st = check_layer(__func__, prec, n, H, W, cin, cout);
+    if (st) return st;
+    if (!conv3x3_supported(cin, cout, IN_PLAIN, 1))
+        return fail(IMPALA_EUNSUPPORTED, "impala_conv3x3_dgrad: unsupported cin=%d cout=%d", cin, cout);
+    if (n == 0) return ok();
+    CHECK_PTR(dy); CHECK_PTR(w); CHECK_PTR(dx);
+    ConvArgs a{};
+    a.x = dy; a.w = w; a.mask = mask; a.add = add; a.y = dx;
+    a.n = int(n); a.H = H; a.W = W; a.scale = 1.f;
+    return hip_status(conv3x3(prec, cin, cout, IN_PLAIN, 1, a, stream), "impala_conv3x3_dgrad");
+}
+
+size_t impala_conv3x3_wgrad_workspace_bytes(impala_prec_t prec, int32_t H, int32_t W, int32_t cin,
+                                            int32_t cout) {
+    if (!valid_prec(prec) || H < 1 || W < 1) return 0;
+    return wgrad_partial_floats(prec, cin, cout, H, W) * sizeof(float);
+}
+
+impala_status_t impala_conv3x3_wgrad(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t cin,
+                                     int32_t cout, const void* x, int32_t x_mode,
+                                     const int32_t* row_idx, const void* dy, float* dw, float* db,
+                                     void* ws, size_t ws_bytes, hipStream_t stream) {
+    impala_status_t st = check_layer(__func__, prec, n, H, W, cin, cout);
+    if (st) return st;
+    if (x_mode < 0 || x_mode > 2 || !wgrad_supported(cin, cout, x_mode))
+        return fail(IMPALA_EUNSUPPORTED, "impala_conv3x3_wgrad: unsupported cin=%d cout=%d x_mode=%d", cin, cout, x_mode);
+    CHECK_PTR(dw); CHECK_PTR(db);
+    if (n == 0) {
+        hipError_t he = fill_zero(dw, int64_t(9) * cin * cout, stream);
+        if (he == hipSuccess) he = fill_zero(db, cout, stream);
+        return hip_status(he, "impala_conv3x3_wgrad");
+    }
+    CHECK_PTR(x); CHECK_PTR(dy); CHECK_PTR(ws);
+    const size_t need = wgrad_partial_floats(prec, cin, cout, H, W) * sizeof(float);
+    if (ws_bytes < need) return fail(IMPALA_EWORKSPACE, "impala_conv3x3_wgrad: workspace %zu < %zu", ws_bytes, need);
+    WgradArgs a{};
+    a.x = x; a.row_idx = x_mode == IN_U8 ? row_idx : nullptr; a.dy = dy; a.dw = dw; a.db = db;
+    a.partial = static_cast<float*>(ws); a.n = int(n); a.H = H; a.W = W;
+    a.scale = x_mode == IN_U8 ? 1.f / 255.f : 1.f;
+    return hip_status(conv3x3_wgrad(prec, cin, cout, x_mode, a, stream), "impala_conv3x3_wgrad");
+}
+
+impala_status_t impala_maxpool_fwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t C,
+                                   const void* x, void* y, uint8_t* arg, hipStream_t stream) {
+    impala_status_t st = check_layer(__func__, prec, n, H, W, C, C);
+    if (st) return st;
+    if (C < 4 || C % 4) return fail(IMPALA_EUNSUPPORTED, "impala_maxpool_fwd: C must be a multiple of 4");
+    if (n == 0) return ok();
+    CHECK_PTR(x); CHECK_PTR(y); CHECK_PTR(arg);
+    return hip_status(maxpool_fwd(prec, int(n), H, W, C, x, y, arg, stream), "impala_maxpool_fwd");
+}
+
+impala_status_t impala_maxpool_bwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t C,
+                                   const uint8_t* arg, const void* dy, void* dx, hipStream_t stream) {
+    impala_status_t st = check_layer(__func__, prec, n, H, W, C, C);
+    if (st) return st;
+    if (C < 4 || C % 4) return fail(IMPALA_EUNSUPPORTED, "impala_maxpool_bwd: C must be a multiple of 4");
+    if (n == 0) return ok();
+    CHECK_PTR(arg); CHECK_PTR(dy); CHECK_PTR(dx);
+    return hip_status(maxpool_bwd(prec, int(n), H, W, C, arg, dy, dx, stream), "impala_maxpool_bwd");
+}
+
+impala_status_t impala_gumbel_sample(int64_t n, int32_t A, const float* logits, const float* gumbel,
+                                     int32_t* actions, float* logp, hipStream_t stream) {
+    if (n < 0 || A < 1 || A > 64) return fail(IMPALA_EINVAL, "impala_gumbel_sample: bad n or A");
+    if (n == 0) return ok();
+    CHECK_PTR(logits); CHECK_PTR(gumbel); CHECK_PTR(actions); CHECK_PTR(logp);
+    return hip_status(gumbel_max(n, A, logits, gumbel, actions, logp, stream), "impala_gumbel_sample");
+}
+
+}  // extern "C"

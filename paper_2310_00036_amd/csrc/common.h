@@ -1,0 +1,99 @@
+// Device-side helpers shared by the gfx950 kernels: bf16 storage, MFMA wrappers and
+// the two precision traits (bf16 matrix-core operands or float32 validation mode).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define CB_DEV __device__ __forceinline__
+
+typedef __bf16 cb_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float cb_f32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- bf16 storage
+// Activations in bf16 mode are stored as raw 16-bit patterns (uint16_t).
+
+CB_DEV float bf2f(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
+
+// float -> bf16, round to nearest even; NaN stays NaN.
+CB_DEV uint16_t f2bf(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return uint16_t((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return uint16_t(u >> 16);
+}
+
+CB_DEV uint32_t pack2bf(float a, float b) { return uint32_t(f2bf(a)) | (uint32_t(f2bf(b)) << 16); }
+
+// ---------------------------------------------------------------- precision traits
+//
+// A 16x16 MFMA tile computes D[i][n] += sum_k A[i][k] * B[k][n]. Lane l supplies A row
+// (l % 16) and B column (l % 16) for its KPL consecutive k values starting at KPL*(l/16),
+// and receives D rows 4*(l/16) .. +3 of column (l % 16). A and B use the same k
+// assignment, so the sum covers each k exactly once.
+
+struct PrecBF16 {
+    using T = uint16_t;                  // storage element
+    static constexpr int KPL = 8;        // k values per lane per MFMA
+    static constexpr int KSTEP = 32;     // k per MFMA (v_mfma_f32_16x16x32_bf16)
+    using Frag = uint4;                  // 8 bf16
+    static CB_DEV float load(T v) { return bf2f(v); }
+    static CB_DEV T store(float f) { return f2bf(f); }
+    static CB_DEV cb_f32x4 mma(Frag a, Frag b, cb_f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(cb_bf16x8, a),
+                                                       __builtin_bit_cast(cb_bf16x8, b), c, 0, 0, 0);
+    }
+    static CB_DEV Frag zero() { return make_uint4(0, 0, 0, 0); }
+    static CB_DEV Frag lds_frag(const T* p) { return *reinterpret_cast<const uint4*>(p); }
+};
+
+struct PrecF32 {
+    using T = float;
+    static constexpr int KPL = 1;
+    static constexpr int KSTEP = 4;      // v_mfma_f32_16x16x4_f32
+    using Frag = float;
+    static CB_DEV float load(T v) { return v; }
+    static CB_DEV T store(float f) { return f; }
+    static CB_DEV cb_f32x4 mma(Frag a, Frag b, cb_f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+    }
+    static CB_DEV Frag zero() { return 0.f; }
+    static CB_DEV Frag lds_frag(const T* p) { return *p; }
+};
+
+// Store / load 4 consecutive channels of one pixel.
+CB_DEV void store4(uint16_t* p, float a, float b, float c, float d) {
+    *reinterpret_cast<uint2*>(p) = make_uint2(pack2bf(a, b), pack2bf(c, d));
+}
+CB_DEV void store4(float* p, float a, float b, float c, float d) {
+    *reinterpret_cast<float4*>(p) = make_float4(a, b, c, d);
+}
+CB_DEV void load4(const uint16_t* p, float* o) {
+    uint2 v = *reinterpret_cast<const uint2*>(p);
+    o[0] = __uint_as_float(v.x << 16);
+    o[1] = __uint_as_float(v.x & 0xffff0000u);
+    o[2] = __uint_as_float(v.y << 16);
+    o[3] = __uint_as_float(v.y & 0xffff0000u);
+}
+CB_DEV void load4(const float* p, float* o) {
+    float4 v = *reinterpret_cast<const float4*>(p);
+    o[0] = v.x; o[1] = v.y; o[2] = v.z; o[3] = v.w;
+}
+
+CB_DEV float relu_f(float x) { return x < 0.f ? 0.f : x; }   // keeps NaN
+
+// Block-wide reduction of a double over 256 threads (fixed order -> deterministic).
+template <int NT>
+CB_DEV double block_sum(double v, double* sh) {
+    const int t = threadIdx.x;
+    sh[t] = v;
+    __syncthreads();
+#pragma unroll
+    for (int s = NT / 2; s > 0; s >>= 1) {
+        if (t < s) sh[t] += sh[t + s];
+        __syncthreads();
+    }
+    double r = sh[0];
+    __syncthreads();
+    return r;
+}

@@ -1,0 +1,256 @@
+// Dense-layer and head GEMMs on gfx950 MFMA: D[m][n] = sum_k A(m,k) B(k,n), written to
+// out[n*ld + m] (m contiguous, so a lane's 4 accumulator rows are 4 adjacent outputs).
+//
+// A and B are read from global memory in either orientation (k-contiguous or
+// m/n-contiguous), converted to the compute type and staged k-contiguous in LDS; float32
+// weights are rounded to bf16 on the way in when the compute type is bf16. A 64x64 output
+// tile per workgroup, 4 waves of 32x32. Split-K writes float32 partials that a second
+// kernel sums in a fixed order before applying the epilogue (bias, ReLU, mask, store).
+#include "common.h"
+#include "kernels.h"
+
+namespace cb {
+
+template <class P>
+struct GemmTile {
+    static constexpr int BM = 64, BN = 64;
+    static constexpr int BK = P::KSTEP * (sizeof(typename P::T) == 2 ? 2 : 4);
+    static constexpr int LDK = BK + (sizeof(typename P::T) == 2 ? 8 : 1);
+};
+
+template <class P>
+CB_DEV float ld_elem(const void* base, int is_f32, int64_t idx) {
+    if (is_f32) return static_cast<const float*>(base)[idx];
+    return P::load(static_cast<const typename P::T*>(base)[idx]);
+}
+
+template <class P>
+CB_DEV void gemm_epilogue(const GemmArgs& a, int m, int n, float v) {
+    using T = typename P::T;
+    if (m >= a.M || n >= a.N) return;
+    const bool hi = m >= a.msplit;
+    const float* bias = hi ? a.bias2 : a.bias1;
+    v = v * a.alpha + (bias ? bias[hi ? m - a.msplit : m] : 0.f);
+    if (a.relu) v = relu_f(v);
+    if (a.mask && !(P::load(static_cast<const T*>(a.mask)[int64_t(n) * a.ldmask + m]) > 0.f)) v = 0.f;
+    if (!hi) {
+        const int64_t o = int64_t(n) * a.ld1 + m;
+        if (a.out1_f32) static_cast<float*>(a.out1)[o] = v;
+        else static_cast<T*>(a.out1)[o] = P::store(v);
+    } else {
+        const int64_t o = int64_t(n) * a.ld2 + (m - a.msplit);
+        if (a.out2_f32) static_cast<float*>(a.out2)[o] = v;
+        else static_cast<T*>(a.out2)[o] = P::store(v);
+    }
+}
+
+template <class P>
+__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a, int kchunk) {
+    using T = typename P::T;
+    using G = GemmTile<P>;
+    using Frag = typename P::Frag;
+    constexpr int BM = G::BM, BN = G::BN, BK = G::BK, LDK = G::LDK;
+    __shared__ __align__(16) T As[BM * LDK];
+    __shared__ __align__(16) T Bs[BN * LDK];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, r16 = lane & 15;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+    const int k_begin = blockIdx.z * kchunk;
+    const int k_end = min(a.K, k_begin + kchunk);
+
+    cb_f32x4 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int k0 = k_begin; k0 < k_end; k0 += BK) {
+        __syncthreads();
+        for (int e = tid; e < BM * BK; e += 256) {
+            int mm, kk;
+            if (a.a_kcontig) { mm = e / BK; kk = e % BK; } else { mm = e % BM; kk = e / BM; }
+            const int m = m0 + mm, k = k0 + kk;
+            float v = 0.f;
+            if (m < a.M && k < k_end)
+                v = ld_elem<P>(a.a, a.a_f32, a.a_kcontig ? int64_t(m) * a.lda + k : int64_t(k) * a.lda + m);
+            As[mm * LDK + kk] = P::store(v);
+        }
+        for (int e = tid; e < BN * BK; e += 256) {
+            int nn, kk;
+            if (a.b_kcontig) { nn = e / BK; kk = e % BK; } else { nn = e % BN; kk = e / BN; }
+            const int n = n0 + nn, k = k0 + kk;
+            float v = 0.f;
+            if (n < a.N && k < k_end)
+                v = ld_elem<P>(a.b, a.b_f32, a.b_kcontig ? int64_t(n) * a.ldb + k : int64_t(k) * a.ldb + n);
+            if (a.b_relu) v = relu_f(v);
+            Bs[nn * LDK + kk] = P::store(v);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int ks = 0; ks < BK; ks += P::KSTEP) {
+            Frag af[2], bf[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) af[i] = P::lds_frag(As + (wm * 32 + i * 16 + r16) * LDK + ks + g * P::KPL);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) bf[j] = P::lds_frag(Bs + (wn * 32 + j * 16 + r16) * LDK + ks + g * P::KPL);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) acc[i][j] = P::mma(af[i], bf[j], acc[i][j]);
+        }
+    }
+
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = m0 + wm * 32 + i * 16 + 4 * g + r;
+                const int n = n0 + wn * 32 + j * 16 + r16;
+                if (gridDim.z == 1) {
+                    gemm_epilogue<P>(a, m, n, acc[i][j][r]);
+                } else if (m < a.M && n < a.N) {
+                    a.partial[(int64_t(blockIdx.z) * a.N + n) * a.M + m] = acc[i][j][r];
+                }
+            }
+}
+
+template <class P>
+__global__ __launch_bounds__(256) void gemm_finish_kernel(GemmArgs a, int splits) {
+    const int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    const int64_t total = int64_t(a.M) * a.N;
+    if (e >= total) return;
+    float s = 0.f;
+    for (int z = 0; z < splits; ++z) s += a.partial[z * total + e];
+    gemm_epilogue<P>(a, int(e % a.M), int(e / a.M), s);
+}
+
+size_t gemm_partial_floats(int M, int N, int splits) {
+    return splits > 1 ? size_t(M) * N * splits : 0;
+}
+
+template <class P>
+static hipError_t gemm_launch(const GemmArgs& a, int splits, hipStream_t s) {
+    using G = GemmTile<P>;
+    if (a.M <= 0 || a.N <= 0) return hipSuccess;
+    int kchunk = (a.K + splits - 1) / splits;
+    kchunk = (kchunk + G::BK - 1) / G::BK * G::BK;
+    if (kchunk <= 0) kchunk = G::BK;
+    const int z = (a.K + kchunk - 1) / kchunk > 0 ? (a.K + kchunk - 1) / kchunk : 1;
+    dim3 grid((a.M + G::BM - 1) / G::BM, (a.N + G::BN - 1) / G::BN, z);
+    hipLaunchKernelGGL(gemm_kernel<P>, grid, dim3(256), 0, s, a, kchunk);
+    if (z > 1) {
+        const int64_t total = int64_t(a.M) * a.N;
+        hipLaunchKernelGGL(gemm_finish_kernel<P>, dim3(unsigned((total + 255) / 256)), dim3(256), 0,
+                           s, a, z);
+    }
+    return hipGetLastError();
+}
+
+hipError_t gemm(int prec, const GemmArgs& a, int splits, hipStream_t s) {
+    if (splits < 1) splits = 1;
+    return prec == BF16 ? gemm_launch<PrecBF16>(a, splits, s) : gemm_launch<PrecF32>(a, splits, s);
+}
+
+// ------------------------------------------------------------------ column sums
+// out[c] = sum_r x[r*ld + c], two passes with a fixed order: 64 columns x 4 row lanes per
+// block and up to 64 row slabs, then one pass over the slabs.
+template <class T>
+__global__ __launch_bounds__(256) void colsum_kernel(const T* __restrict__ x, int64_t rows, int cols,
+                                                     int64_t ld, float* __restrict__ partial,
+                                                     int slabs) {
+    __shared__ float sh[4][64];
+    const int c = blockIdx.x * 64 + (threadIdx.x & 63);
+    const int rl = threadIdx.x >> 6;
+    const int64_t per = (rows + slabs - 1) / slabs;
+    const int64_t r0 = int64_t(blockIdx.y) * per, r1 = r0 + per < rows ? r0 + per : rows;
+    float s = 0.f;
+    if (c < cols)
+        for (int64_t r = r0 + rl; r < r1; r += 4) {
+            if constexpr (sizeof(T) == 2) s += bf2f(x[r * ld + c]);
+            else s += x[r * ld + c];
+        }
+    sh[rl][threadIdx.x & 63] = s;
+    __syncthreads();
+    if (rl == 0 && c < cols)
+        partial[int64_t(blockIdx.y) * cols + c] = ((sh[0][threadIdx.x] + sh[1][threadIdx.x]) + sh[2][threadIdx.x]) + sh[3][threadIdx.x];
+}
+
+__global__ void colsum_finish_kernel(const float* __restrict__ partial, int cols, int slabs,
+                                     float* __restrict__ out) {
+    const int c = blockIdx.x * 256 + threadIdx.x;
+    if (c >= cols) return;
+    float s = 0.f;
+    for (int z = 0; z < slabs; ++z) s += partial[int64_t(z) * cols + c];
+    out[c] = s;
+}
+
+constexpr int kColSlabs = 64;
+
+size_t colsum_partial_floats(int cols) { return size_t(kColSlabs) * cols; }
+
+hipError_t colsum(int prec_storage, const void* x, int64_t rows, int cols, int64_t ld, float* out,
+                  float* partial, hipStream_t s) {
+    if (cols <= 0) return hipSuccess;
+    int slabs = int(rows < kColSlabs ? (rows > 0 ? rows : 1) : kColSlabs);
+    dim3 grid((cols + 63) / 64, slabs);
+    if (prec_storage == BF16)
+        hipLaunchKernelGGL(colsum_kernel<uint16_t>, grid, dim3(256), 0, s,
+                           static_cast<const uint16_t*>(x), rows, cols, ld, partial, slabs);
+    else
+        hipLaunchKernelGGL(colsum_kernel<float>, grid, dim3(256), 0, s, static_cast<const float*>(x),
+                           rows, cols, ld, partial, slabs);
+    hipLaunchKernelGGL(colsum_finish_kernel, dim3((cols + 255) / 256), dim3(256), 0, s, partial, cols,
+                       slabs, out);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ head packing
+// out[a][j]: rows 0..A-1 are the logit weights' columns, row A is the value weights.
+__global__ void pack_heads_w_kernel(const float* __restrict__ wl, const float* __restrict__ wv,
+                                    int hidden, int A, float* __restrict__ out) {
+    const int e = blockIdx.x * 256 + threadIdx.x;
+    if (e >= (A + 1) * hidden) return;
+    const int a = e / hidden, j = e % hidden;
+    out[e] = a < A ? wl[int64_t(j) * A + a] : wv[j];
+}
+
+hipError_t pack_heads_w(const float* wl, const float* wv, int hidden, int A, float* out,
+                        hipStream_t s) {
+    const int total = (A + 1) * hidden;
+    hipLaunchKernelGGL(pack_heads_w_kernel, dim3((total + 255) / 256), dim3(256), 0, s, wl, wv,
+                       hidden, A, out);
+    return hipGetLastError();
+}
+
+// out[i][a] = dlogits[i][a] (a < A), dvalue[i] (a == A), in the storage type.
+template <class T>
+__global__ void pack_dz_kernel(const float* __restrict__ dl, const float* __restrict__ dv,
+                               int64_t n, int A, T* __restrict__ out) {
+    const int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    if (e >= n * (A + 1)) return;
+    const int64_t i = e / (A + 1);
+    const int a = int(e % (A + 1));
+    const float v = a < A ? dl[i * A + a] : dv[i];
+    if constexpr (sizeof(T) == 2) out[e] = f2bf(v);
+    else out[e] = v;
+}
+
+hipError_t pack_dz(int prec, const float* dlogits, const float* dvalue, int64_t n, int A, void* out,
+                   hipStream_t s) {
+    const int64_t total = n * (A + 1);
+    if (total <= 0) return hipSuccess;
+    const dim3 grid(unsigned((total + 255) / 256));
+    if (prec == BF16)
+        hipLaunchKernelGGL(pack_dz_kernel<uint16_t>, grid, dim3(256), 0, s, dlogits, dvalue, n, A,
+                           static_cast<uint16_t*>(out));
+    else
+        hipLaunchKernelGGL(pack_dz_kernel<float>, grid, dim3(256), 0, s, dlogits, dvalue, n, A,
+                           static_cast<float*>(out));
+    return hipGetLastError();
+}
+
+}  // namespace cb

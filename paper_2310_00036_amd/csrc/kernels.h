@@ -1,0 +1,109 @@
+// Internal launch interface between the host orchestration and the gfx950 kernels.
+// Every launcher validates nothing (the C-ABI layer does) and returns hipGetLastError().
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cb {
+
+enum Prec { BF16 = 0, FP32 = 1 };
+enum InMode { IN_PLAIN = 0, IN_RELU = 1, IN_U8 = 2 };
+
+// ---- 3x3 SAME convolution as implicit GEMM (forward, and input-gradient with flip=1)
+struct ConvArgs {
+    const void* x;          // input activations [n, H, W, cin] (storage type) or uint8 frames
+    const int32_t* row_idx; // uint8 mode: frame i reads obs row row_idx[i] (NULL: i)
+    const float* w;         // float32 HWIO weights of the forward conv
+    const float* bias;      // [cout] or NULL
+    const void* add;        // [n, H, W, cout] added after the mask, or NULL
+    const void* mask;       // [n, H, W, cout]: output kept where mask > 0, or NULL
+    void* y;                // [n, H, W, cout]
+    int n, H, W;
+    float scale;            // multiplies the sum before the bias (1/255 for uint8 frames)
+};
+// flip = 0: y = conv(x, w) (cin, cout are the forward conv's channels).
+// flip = 1: y = conv^T(x, w), the adjoint w.r.t. the forward input; here x has the forward
+//           conv's output channels (cin argument = forward cout) and y its input channels.
+hipError_t conv3x3(int prec, int cin, int cout, int mode, int flip, const ConvArgs& a,
+                   hipStream_t s);
+bool conv3x3_supported(int cin, int cout, int mode, int flip);
+
+// ---- weight gradient of a 3x3 SAME conv (deterministic split over pixels)
+struct WgradArgs {
+    const void* x;          // forward input (storage type or uint8 frames)
+    const int32_t* row_idx;
+    const void* dy;         // [n, H, W, cout] gradient at the conv output
+    float* dw;              // float32 HWIO [3,3,cin,cout]
+    float* db;              // float32 [cout]
+    float* partial;         // workspace, wgrad_partial_floats() floats
+    int n, H, W;
+    float scale;            // applied to dw (1/255 for uint8 frames)
+};
+size_t wgrad_partial_floats(int prec, int cin, int cout, int H, int W);
+hipError_t conv3x3_wgrad(int prec, int cin, int cout, int mode, const WgradArgs& a,
+                         hipStream_t s);
+bool wgrad_supported(int cin, int cout, int mode);
+
+// ---- 3x3 stride-2 SAME max-pool (XLA padding split), first-max argmax in 0..8
+hipError_t maxpool_fwd(int prec, int n, int H, int W, int C, const void* x, void* y,
+                       uint8_t* arg, hipStream_t s);
+hipError_t maxpool_bwd(int prec, int n, int H, int W, int C, const uint8_t* arg, const void* dy,
+                       void* dx, hipStream_t s);
+
+// ---- GEMM D[m][n] = sum_k A(m,k) B(k,n) on MFMA, output out[n*ld + m]
+struct GemmArgs {
+    const void* a; int a_f32; int a_kcontig; int64_t lda;   // A(m,k) = a[m*lda+k] or a[k*lda+m]
+    const void* b; int b_f32; int b_kcontig; int64_t ldb;   // B(k,n) = b[n*ldb+k] or b[k*ldb+n]
+    int b_relu;                                             // relu(B) on load
+    int M, N, K;
+    // epilogue (applied after the split-K sum): v = sum*alpha + bias; relu; mask; store
+    float alpha;
+    const float* bias1; const float* bias2;                 // bias for m < msplit / m >= msplit
+    int relu;
+    const void* mask; int64_t ldmask;                       // storage type, keep where > 0
+    void* out1; int64_t ld1; int out1_f32;                  // rows m < msplit
+    void* out2; int64_t ld2; int out2_f32;                  // rows m >= msplit (index m - msplit)
+    int msplit;
+    float* partial;                                         // split-K workspace
+};
+size_t gemm_partial_floats(int M, int N, int splits);
+hipError_t gemm(int prec, const GemmArgs& a, int splits, hipStream_t s);
+
+// ---- small helpers
+hipError_t colsum(int prec_storage, const void* x, int64_t rows, int cols, int64_t ld,
+                  float* out, float* partial, hipStream_t s);   // out[c] = sum_r x[r*ld + c]
+size_t colsum_partial_floats(int cols);
+hipError_t pack_heads_w(const float* wl, const float* wv, int hidden, int A, float* out,
+                        hipStream_t s);   // out [A+1][hidden]
+hipError_t pack_dz(int prec, const float* dlogits, const float* dvalue, int64_t n, int A,
+                   void* out, hipStream_t s);   // out [n][A+1] storage type
+
+// ---- loss, targets, optimiser
+hipError_t gae(int T, int E, const float* r, const float* v, const uint8_t* d, const float* nv,
+               const uint8_t* nd, float gamma, float lam, float* adv, float* ret, hipStream_t s);
+hipError_t vtrace(int T, int E, const float* mu, const float* pi, const float* r, const float* v,
+                  const uint8_t* d, const float* bv, const uint8_t* nd, float gamma, float lam,
+                  float rho_bar, float c_bar, float pg_rho_bar, float* vs, float* pg,
+                  hipStream_t s);
+// stats [8] doubles as the advantage-statistics scratch (entries 6, 7) of ppo_loss.
+hipError_t ppo_loss(int64_t m, int A, const float* z, const float* v, const int32_t* act,
+                    const float* old_logp, const float* adv, const float* ret,
+                    const int32_t* rows, int norm_adv, float clip, float vf, float ent,
+                    float* dz, float* dv, float* stats, hipStream_t s);
+hipError_t impala_loss(int64_t m, int A, const float* z, const float* v, const int32_t* act,
+                       const float* vs, const float* pg, float pgc, float vf, float ent,
+                       float* dz, float* dv, float* stats, hipStream_t s);
+hipError_t action_logp(int64_t m, int A, const float* z, const int32_t* act, float* logp,
+                       hipStream_t s);
+hipError_t gumbel_max(int64_t m, int A, const float* z, const float* g, int32_t* act,
+                      float* logp, hipStream_t s);
+size_t adam_partial_floats(int64_t n);
+// omb1 = 1 - b1, omb2 = 1 - b2, bc1 = 1 - b1^t, bc2 = 1 - b2^t, all formed in double.
+hipError_t adam(int64_t n, float* p, const float* g, float* m, float* v, float lr, float b1,
+                float b2, float omb1, float omb2, float bc1, float bc2, float eps, float max_norm,
+                float* stats, float* partial, hipStream_t s);
+// Largest dynamic LDS allocation per workgroup on the current device (bytes).
+size_t lds_limit();
+
+}  // namespace cb

@@ -1,0 +1,253 @@
+// Fused policy / value / entropy losses and their logit and value gradients, one thread per
+// minibatch row (A <= 64 logits per row), plus the actor's Gumbel-max sampler.
+//
+// PPO runs three launches: (1) one block computes the minibatch advantage mean and
+// population std (float64 sums) into the caller's stats vector, (2) one thread per row
+// computes log-softmax, ratio, clipped surrogate, entropy and value terms and writes
+// dlogits / dvalue, (3) one block re-derives the row terms and sums them (float64, fixed
+// order) into the stats vector. No scratch memory is needed and every reduction has a
+// fixed order, so results are bit-reproducible.
+#include "common.h"
+#include "kernels.h"
+
+namespace cb {
+
+constexpr int kLossRows = 256;   // rows per block in the gradient kernels
+constexpr int kStatThreads = 1024;
+
+// ---- (1) advantage statistics over the minibatch (single block, fixed order), written to
+//          stats[6] (mean) and stats[7] (population std)
+__global__ __launch_bounds__(256) void adv_stats_kernel(int64_t m, const float* __restrict__ adv,
+                                                        const int32_t* __restrict__ rows,
+                                                        float* __restrict__ stats) {
+    __shared__ double sh[256];
+    double s = 0.0, s2 = 0.0;
+    for (int64_t i = threadIdx.x; i < m; i += 256) {
+        const double a = adv[rows ? rows[i] : i];
+        s += a;
+        s2 += a * a;
+    }
+    const double tot = block_sum<256>(s, sh);
+    const double tot2 = block_sum<256>(s2, sh);
+    if (threadIdx.x == 0) {
+        const double mean = tot / double(m);
+        const double var = tot2 / double(m) - mean * mean;
+        stats[6] = float(mean);
+        stats[7] = float(sqrt(var > 0.0 ? var : 0.0));
+    }
+}
+
+// Log-softmax of one row: writes l[j] = z_j - logsumexp(z); returns the entropy.
+CB_DEV float row_log_softmax(const float* z, int A, float* l) {
+    float zmax = z[0];
+    for (int j = 1; j < A; ++j) zmax = fmaxf(zmax, z[j]);
+    float se = 0.f;
+    for (int j = 0; j < A; ++j) se += expf(z[j] - zmax);
+    const float lse = logf(se);
+    float H = 0.f;
+    for (int j = 0; j < A; ++j) {
+        l[j] = (z[j] - zmax) - lse;
+        H -= expf(l[j]) * l[j];
+    }
+    return H;
+}
+
+struct PpoRow {
+    float H, ratio, A_hat, pg, kappa;
+    int a;
+};
+
+CB_DEV PpoRow ppo_row(int64_t i, int64_t src, int A, const float* z, const int32_t* act,
+                      const float* old_logp, const float* adv, int norm_adv, float clip,
+                      float mean, float std, float* l) {
+    PpoRow r;
+    r.H = row_log_softmax(z + i * A, A, l);
+    r.a = act[src];
+    r.A_hat = adv[src];
+    if (norm_adv) r.A_hat = (r.A_hat - mean) / (std + 1e-8f);
+    // an action outside [0, A) poisons the row with NaN instead of reading past l[]
+    const float la = (r.a >= 0 && r.a < A) ? l[r.a] : __builtin_nanf("");
+    r.ratio = expf(la - old_logp[src]);
+    const float pg1 = -r.A_hat * r.ratio;
+    const float pg2 = -r.A_hat * fminf(fmaxf(r.ratio, 1.f - clip), 1.f + clip);
+    r.pg = fmaxf(pg1, pg2);
+    r.kappa = pg2 > pg1 ? 0.f : 1.f;   // clipped branch strictly larger: no ratio gradient
+    return r;
+}
+
+// ---- (2) per-row PPO gradients
+__global__ __launch_bounds__(kLossRows) void ppo_rows_kernel(
+    int64_t m, int A, const float* __restrict__ z, const float* __restrict__ val,
+    const int32_t* __restrict__ act, const float* __restrict__ old_logp,
+    const float* __restrict__ adv, const float* __restrict__ ret, const int32_t* __restrict__ rows,
+    int norm_adv, float clip, float vf, float ent, float* __restrict__ dz, float* __restrict__ dv,
+    const float* __restrict__ stats) {
+    const int64_t i = int64_t(blockIdx.x) * kLossRows + threadIdx.x;
+    if (i >= m) return;
+    const int64_t src = rows ? rows[i] : i;
+    float l[64];
+    const PpoRow r = ppo_row(i, src, A, z, act, old_logp, adv, norm_adv, clip, stats[6], stats[7], l);
+    const float inv_m = 1.f / float(m);
+    const float coef = -r.kappa * r.A_hat * r.ratio;
+    for (int j = 0; j < A; ++j) {
+        const float p = expf(l[j]);
+        dz[i * A + j] = (coef * ((j == r.a ? 1.f : 0.f) - p) + ent * p * (l[j] + r.H)) * inv_m;
+    }
+    dv[i] = vf * (val[i] - ret[src]) * inv_m;
+}
+
+// ---- (3) PPO stats: one block re-derives the row terms and sums them in a fixed order
+__global__ __launch_bounds__(kStatThreads) void ppo_stats_kernel(
+    int64_t m, int A, const float* __restrict__ z, const float* __restrict__ val,
+    const int32_t* __restrict__ act, const float* __restrict__ old_logp,
+    const float* __restrict__ adv, const float* __restrict__ ret, const int32_t* __restrict__ rows,
+    int norm_adv, float clip, float vf, float ent, float* __restrict__ stats) {
+    __shared__ double sh[kStatThreads];
+    const float mean = stats[6], std = stats[7];
+    double st[5] = {0, 0, 0, 0, 0};
+    float l[64];
+    for (int64_t i = threadIdx.x; i < m; i += kStatThreads) {
+        const int64_t src = rows ? rows[i] : i;
+        const PpoRow r = ppo_row(i, src, A, z, act, old_logp, adv, norm_adv, clip, mean, std, l);
+        const double dvl = double(val[i]) - double(ret[src]);
+        st[0] += r.pg;
+        st[1] += dvl * dvl;
+        st[2] += r.H;
+        st[3] += double(r.ratio - 1.f) - double(logf(r.ratio));
+        st[4] += fabsf(r.ratio - 1.f) > clip ? 1.0 : 0.0;
+    }
+    double tot[5];
+    for (int k = 0; k < 5; ++k) tot[k] = block_sum<kStatThreads>(st[k], sh);
+    if (threadIdx.x == 0) {
+        const double inv = 1.0 / double(m);
+        const double pg = tot[0] * inv, vl = 0.5 * tot[1] * inv, H = tot[2] * inv;
+        stats[0] = float(pg + vf * vl - ent * H);
+        stats[1] = float(pg); stats[2] = float(vl); stats[3] = float(H);
+        stats[4] = float(tot[3] * inv); stats[5] = float(tot[4] * inv);
+    }
+}
+
+// ---- IMPALA: per-row gradients, then one stats block
+__global__ __launch_bounds__(kLossRows) void impala_rows_kernel(
+    int64_t m, int A, const float* __restrict__ z, const float* __restrict__ val,
+    const int32_t* __restrict__ act, const float* __restrict__ vs, const float* __restrict__ pgadv,
+    float pgc, float vf, float ent, float* __restrict__ dz, float* __restrict__ dv) {
+    const int64_t i = int64_t(blockIdx.x) * kLossRows + threadIdx.x;
+    if (i >= m) return;
+    float l[64];
+    const float H = row_log_softmax(z + i * A, A, l);
+    const int a = act[i];
+    const float adv = pgadv[i];
+    const float inv_m = 1.f / float(m);
+    const bool a_ok = a >= 0 && a < A;
+    for (int j = 0; j < A; ++j) {
+        const float p = expf(l[j]);
+        dz[i * A + j] = a_ok ? (-pgc * adv * ((j == a ? 1.f : 0.f) - p) + ent * p * (l[j] + H)) * inv_m
+                             : __builtin_nanf("");
+    }
+    dv[i] = vf * (val[i] - vs[i]) * inv_m;
+}
+
+__global__ __launch_bounds__(kStatThreads) void impala_stats_kernel(
+    int64_t m, int A, const float* __restrict__ z, const float* __restrict__ val,
+    const int32_t* __restrict__ act, const float* __restrict__ vs, const float* __restrict__ pgadv,
+    float pgc, float vf, float ent, float* __restrict__ stats) {
+    __shared__ double sh[kStatThreads];
+    double st[5] = {0, 0, 0, 0, 0};
+    float l[64];
+    for (int64_t i = threadIdx.x; i < m; i += kStatThreads) {
+        const float H = row_log_softmax(z + i * A, A, l);
+        const double dvl = double(val[i]) - double(vs[i]);
+        const int a = act[i];
+        st[0] += -double(pgadv[i]) * ((a >= 0 && a < A) ? double(l[a]) : double(__builtin_nanf("")));
+        st[1] += dvl * dvl;
+        st[2] += H;
+        st[3] += pgadv[i];
+        st[4] += vs[i];
+    }
+    double tot[5];
+    for (int k = 0; k < 5; ++k) tot[k] = block_sum<kStatThreads>(st[k], sh);
+    if (threadIdx.x == 0) {
+        const double inv = 1.0 / double(m);
+        const double pg = tot[0] * inv, vl = 0.5 * tot[1] * inv, H = tot[2] * inv;
+        stats[0] = float(pgc * pg + vf * vl - ent * H);
+        stats[1] = float(pg); stats[2] = float(vl); stats[3] = float(H);
+        stats[4] = float(tot[3] * inv); stats[5] = float(tot[4] * inv);
+        stats[6] = 0.f; stats[7] = 0.f;
+    }
+}
+
+hipError_t ppo_loss(int64_t m, int A, const float* z, const float* v, const int32_t* act,
+                    const float* old_logp, const float* adv, const float* ret, const int32_t* rows,
+                    int norm_adv, float clip, float vf, float ent, float* dz, float* dv, float* stats,
+                    hipStream_t s) {
+    if (m <= 0) return hipSuccess;
+    const int nb = int((m + kLossRows - 1) / kLossRows);
+    hipLaunchKernelGGL(adv_stats_kernel, dim3(1), dim3(256), 0, s, m, adv, rows, stats);
+    hipLaunchKernelGGL(ppo_rows_kernel, dim3(nb), dim3(kLossRows), 0, s, m, A, z, v, act, old_logp,
+                       adv, ret, rows, norm_adv, clip, vf, ent, dz, dv, stats);
+    hipLaunchKernelGGL(ppo_stats_kernel, dim3(1), dim3(kStatThreads), 0, s, m, A, z, v, act, old_logp,
+                       adv, ret, rows, norm_adv, clip, vf, ent, stats);
+    return hipGetLastError();
+}
+
+hipError_t impala_loss(int64_t m, int A, const float* z, const float* v, const int32_t* act,
+                       const float* vs, const float* pg, float pgc, float vf, float ent, float* dz,
+                       float* dv, float* stats, hipStream_t s) {
+    if (m <= 0) return hipSuccess;
+    const int nb = int((m + kLossRows - 1) / kLossRows);
+    hipLaunchKernelGGL(impala_rows_kernel, dim3(nb), dim3(kLossRows), 0, s, m, A, z, v, act, vs, pg,
+                       pgc, vf, ent, dz, dv);
+    hipLaunchKernelGGL(impala_stats_kernel, dim3(1), dim3(kStatThreads), 0, s, m, A, z, v, act, vs, pg,
+                       pgc, vf, ent, stats);
+    return hipGetLastError();
+}
+
+// ---- log pi(a) per row (IMPALA target log-probs for V-trace)
+__global__ void action_logp_kernel(int64_t m, int A, const float* __restrict__ z,
+                                   const int32_t* __restrict__ act, float* __restrict__ logp) {
+    const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= m) return;
+    float l[64];
+    row_log_softmax(z + i * A, A, l);
+    const int a = act[i];
+    logp[i] = (a >= 0 && a < A) ? l[a] : __builtin_nanf("");
+}
+
+hipError_t action_logp(int64_t m, int A, const float* z, const int32_t* act, float* logp,
+                       hipStream_t s) {
+    if (m <= 0) return hipSuccess;
+    hipLaunchKernelGGL(action_logp_kernel, dim3(unsigned((m + 255) / 256)), dim3(256), 0, s, m, A, z,
+                       act, logp);
+    return hipGetLastError();
+}
+
+// ---- Gumbel-max sampling: a = argmax_j (z_j + g_j), ties to the lowest index
+__global__ void gumbel_max_kernel(int64_t m, int A, const float* __restrict__ z,
+                                  const float* __restrict__ g, int32_t* __restrict__ act,
+                                  float* __restrict__ logp) {
+    const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= m) return;
+    const float* zr = z + i * A;
+    const float* gr = g + i * A;
+    int best = 0;
+    float bv = zr[0] + gr[0];
+    for (int j = 1; j < A; ++j) {
+        const float v = zr[j] + gr[j];
+        if (v > bv) { bv = v; best = j; }
+    }
+    float l[64];
+    row_log_softmax(zr, A, l);
+    act[i] = best;
+    logp[i] = l[best];
+}
+
+hipError_t gumbel_max(int64_t m, int A, const float* z, const float* g, int32_t* act, float* logp,
+                      hipStream_t s) {
+    if (m <= 0) return hipSuccess;
+    hipLaunchKernelGGL(gumbel_max_kernel, dim3(unsigned((m + 255) / 256)), dim3(256), 0, s, m, A, z, g,
+                       act, logp);
+    return hipGetLastError();
+}
+
+}  // namespace cb

@@ -1,0 +1,289 @@
+// IMPALA-ResNet forward / backward launch sequences on one stream.
+//
+// Network (the "IMPALA's ResNet" the paper trains with, Section 5): for each of three
+// stages, conv3x3 -> maxpool3x3/2 -> 2 x [x + conv(relu(conv(relu(x))))]; then relu,
+// flatten (H, W, C), dense + relu, and the policy-logit / value heads.
+//
+// Saved for the backward pass (all frame-major, `cap` frames): every stage's pre-pool
+// conv output (only its pool argmax is read back), the pool argmax, the three residual
+// stream tensors x0..x2 and the two inner activations t0, t1 per stage, and the dense
+// output h. The backward pass reads the residual inputs with relu applied on load, so no
+// relu'd copies are stored.
+#include <algorithm>
+#include <cstring>
+
+#include "kernels.h"
+#include "plan.h"
+
+namespace cb {
+
+static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+std::string check_net(const impala_net_t* net) {
+    if (!net) return "net is NULL";
+    if (net->in_c != 4) return "in_c must be 4 (stacked uint8 frames)";
+    if (net->in_h < 1 || net->in_h > 128 || net->in_w < 1 || net->in_w > 128)
+        return "in_h and in_w must be in [1, 128]";
+    for (int i = 0; i < 3; ++i) {
+        const int c = net->ch[i];
+        if (c != 16 && c != 32 && c != 64) return "stage channels must be 16, 32 or 64";
+        if (i > 0 && c < net->ch[i - 1]) return "stage channels must be non-decreasing";
+    }
+    if (net->hidden < 1 || net->hidden > 4096) return "hidden must be in [1, 4096]";
+    if (net->num_actions < 1 || net->num_actions > 64) return "num_actions must be in [1, 64]";
+    return "";
+}
+
+ParamOffsets param_offsets(const impala_net_t& net) {
+    ParamOffsets o;
+    int64_t off = 0;
+    int cin = net.in_c, h = net.in_h, w = net.in_w;
+    for (int s = 0; s < 3; ++s) {
+        const int c = net.ch[s];
+        for (int k = 0; k < 5; ++k) {
+            const int ci = k == 0 ? cin : c;
+            o.conv_w[s][k] = off; off += int64_t(9) * ci * c;
+            o.conv_b[s][k] = off; off += c;
+        }
+        cin = c;
+        h = (h + 1) / 2;
+        w = (w + 1) / 2;
+    }
+    const int64_t flat = int64_t(h) * w * net.ch[2];
+    o.dense_w = off; off += flat * net.hidden;
+    o.dense_b = off; off += net.hidden;
+    o.logits_w = off; off += int64_t(net.hidden) * net.num_actions;
+    o.logits_b = off; off += net.num_actions;
+    o.value_w = off; off += net.hidden;
+    o.value_b = off; off += 1;
+    o.total = off;
+    return o;
+}
+
+static int dense_wgrad_splits(int M, int N, int64_t K) {
+    const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
+    int s = std::max(1, std::min(8, 1024 / std::max(1, tiles)));
+    while (s > 1 && K / s < 256) --s;
+    return s;
+}
+
+static int heads_wgrad_splits(int64_t K) {
+    int s = int(std::min<int64_t>(32, std::max<int64_t>(1, K / 256)));
+    return s;
+}
+
+NetPlan make_plan(const impala_net_t& net, int prec, int64_t cap, int training) {
+    NetPlan p;
+    std::memset(&p, 0, sizeof(p));
+    p.net = net;
+    p.prec = prec;
+    p.es = prec == BF16 ? 2 : 4;
+    p.cap = cap;
+    p.training = training;
+    p.H[0] = net.in_h; p.W[0] = net.in_w; p.C[0] = net.in_c;
+    for (int s = 0; s < 3; ++s) {
+        p.H[s + 1] = (p.H[s] + 1) / 2;
+        p.W[s + 1] = (p.W[s] + 1) / 2;
+        p.C[s + 1] = net.ch[s];
+    }
+    p.flat = p.H[3] * p.W[3] * p.C[3];
+    p.hidden = net.hidden;
+    p.A = net.num_actions;
+    p.po = param_offsets(net);
+
+    size_t off = 0;
+    auto take = [&](size_t bytes) { const size_t o = off; off += align256(bytes); return o; };
+    int64_t maxact = std::max<int64_t>(p.hidden, p.flat);
+    for (int s = 0; s < 3; ++s) {
+        const int64_t conv_el = int64_t(p.H[s]) * p.W[s] * p.C[s + 1];
+        const int64_t pool_el = int64_t(p.H[s + 1]) * p.W[s + 1] * p.C[s + 1];
+        maxact = std::max(maxact, conv_el);
+        p.c[s] = take(size_t(cap * conv_el) * p.es);
+        p.idx[s] = take(size_t(cap * pool_el));
+        for (int k = 0; k < 3; ++k) p.x[s][k] = take(size_t(cap * pool_el) * p.es);
+        for (int k = 0; k < 2; ++k) p.t[s][k] = take(size_t(cap * pool_el) * p.es);
+    }
+    p.h = take(size_t(cap) * p.hidden * p.es);
+    p.whp = take(size_t(p.A + 1) * p.hidden * sizeof(float));
+    if (training) {
+        for (int k = 0; k < 3; ++k) p.g[k] = take(size_t(cap * maxact) * p.es);
+        p.dz = take(size_t(cap) * (p.A + 1) * p.es);
+        size_t sc = 0;
+        for (int s = 0; s < 3; ++s) {
+            sc = std::max(sc, wgrad_partial_floats(prec, p.C[s], p.C[s + 1], p.H[s], p.W[s]));
+            sc = std::max(sc, wgrad_partial_floats(prec, p.C[s + 1], p.C[s + 1], p.H[s + 1], p.W[s + 1]));
+        }
+        sc = std::max(sc, gemm_partial_floats(p.hidden, p.flat, dense_wgrad_splits(p.hidden, p.flat, cap)));
+        sc = std::max(sc, gemm_partial_floats(p.A + 1, p.hidden, heads_wgrad_splits(cap)));
+        sc = std::max(sc, colsum_partial_floats(std::max(p.hidden, p.A + 1)));
+        p.scratch_bytes = sc * sizeof(float);
+        p.scratch = take(p.scratch_bytes);
+    }
+    p.total = off;
+    return p;
+}
+
+#define CB_TRY(x)                          \
+    do {                                   \
+        hipError_t e_ = (x);               \
+        if (e_ != hipSuccess) return e_;   \
+    } while (0)
+
+hipError_t run_forward(const NetPlan& p, const float* params, const uint8_t* obs,
+                       const int32_t* row_idx, int64_t n, char* ws, float* logits, float* value,
+                       hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    const ParamOffsets& po = p.po;
+    for (int st = 0; st < 3; ++st) {
+        ConvArgs a{};
+        a.x = st == 0 ? static_cast<const void*>(obs) : static_cast<const void*>(ws + p.x[st - 1][2]);
+        a.row_idx = st == 0 ? row_idx : nullptr;
+        a.w = params + po.conv_w[st][0];
+        a.bias = params + po.conv_b[st][0];
+        a.y = ws + p.c[st];
+        a.n = int(n); a.H = p.H[st]; a.W = p.W[st];
+        a.scale = st == 0 ? 1.f / 255.f : 1.f;
+        CB_TRY(conv3x3(p.prec, p.C[st], p.C[st + 1], st == 0 ? IN_U8 : IN_PLAIN, 0, a, s));
+        CB_TRY(maxpool_fwd(p.prec, int(n), p.H[st], p.W[st], p.C[st + 1], ws + p.c[st], ws + p.x[st][0],
+                           reinterpret_cast<uint8_t*>(ws + p.idx[st]), s));
+        const int C = p.C[st + 1];
+        for (int r = 0; r < 2; ++r) {
+            ConvArgs b{};
+            b.x = ws + p.x[st][r]; b.w = params + po.conv_w[st][1 + 2 * r];
+            b.bias = params + po.conv_b[st][1 + 2 * r]; b.y = ws + p.t[st][r];
+            b.n = int(n); b.H = p.H[st + 1]; b.W = p.W[st + 1]; b.scale = 1.f;
+            CB_TRY(conv3x3(p.prec, C, C, IN_RELU, 0, b, s));
+            ConvArgs c{};
+            c.x = ws + p.t[st][r]; c.w = params + po.conv_w[st][2 + 2 * r];
+            c.bias = params + po.conv_b[st][2 + 2 * r]; c.add = ws + p.x[st][r];
+            c.y = ws + p.x[st][r + 1];
+            c.n = int(n); c.H = p.H[st + 1]; c.W = p.W[st + 1]; c.scale = 1.f;
+            CB_TRY(conv3x3(p.prec, C, C, IN_RELU, 0, c, s));
+        }
+    }
+    // dense: h[i][j] = relu(b[j] + sum_k relu(x)[i][k] W[k][j])
+    GemmArgs d{};
+    d.a = params + po.dense_w; d.a_f32 = 1; d.a_kcontig = 0; d.lda = p.hidden;
+    d.b = ws + p.x[2][2]; d.b_f32 = p.prec == FP32; d.b_kcontig = 1; d.ldb = p.flat; d.b_relu = 1;
+    d.M = p.hidden; d.N = int(n); d.K = p.flat;
+    d.alpha = 1.f; d.bias1 = params + po.dense_b; d.relu = 1;
+    d.out1 = ws + p.h; d.ld1 = p.hidden; d.out1_f32 = p.prec == FP32; d.msplit = p.hidden;
+    CB_TRY(gemm(p.prec, d, 1, s));
+    // heads: logits[i][a] = bl[a] + sum_j h[i][j] Wl[j][a]; value[i] = bv + sum_j h[i][j] Wv[j]
+    float* whp = reinterpret_cast<float*>(ws + p.whp);
+    CB_TRY(pack_heads_w(params + po.logits_w, params + po.value_w, p.hidden, p.A, whp, s));
+    GemmArgs hd{};
+    hd.a = whp; hd.a_f32 = 1; hd.a_kcontig = 1; hd.lda = p.hidden;
+    hd.b = ws + p.h; hd.b_f32 = p.prec == FP32; hd.b_kcontig = 1; hd.ldb = p.hidden;
+    hd.M = p.A + 1; hd.N = int(n); hd.K = p.hidden; hd.alpha = 1.f;
+    hd.bias1 = params + po.logits_b; hd.bias2 = params + po.value_b;
+    hd.out1 = logits; hd.ld1 = p.A; hd.out1_f32 = 1;
+    hd.out2 = value; hd.ld2 = 1; hd.out2_f32 = 1; hd.msplit = p.A;
+    CB_TRY(gemm(p.prec, hd, 1, s));
+    return hipSuccess;
+}
+
+hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* obs,
+                        const int32_t* row_idx, int64_t n, char* ws, const float* dlogits,
+                        const float* dvalue, float* grads, hipStream_t s) {
+    const ParamOffsets& po = p.po;
+    if (n <= 0) return fill_zero(grads, po.total, s);
+    const int es = p.es, A = p.A;
+    const int st_f32 = p.prec == FP32;
+    float* scratch = reinterpret_cast<float*>(ws + p.scratch);
+    char* dz = ws + p.dz;
+    char* G[3] = {ws + p.g[0], ws + p.g[1], ws + p.g[2]};
+
+    CB_TRY(pack_dz(p.prec, dlogits, dvalue, n, A, dz, s));
+    // head weight gradients: dWl[j][a] = sum_i h[i][j] dz[i][a] (value column a == A)
+    GemmArgs hw{};
+    hw.a = dz; hw.a_f32 = st_f32; hw.a_kcontig = 0; hw.lda = A + 1;
+    hw.b = ws + p.h; hw.b_f32 = st_f32; hw.b_kcontig = 0; hw.ldb = p.hidden;
+    hw.M = A + 1; hw.N = p.hidden; hw.K = int(n); hw.alpha = 1.f;
+    hw.out1 = grads + po.logits_w; hw.ld1 = A; hw.out1_f32 = 1;
+    hw.out2 = grads + po.value_w; hw.ld2 = 1; hw.out2_f32 = 1; hw.msplit = A;
+    hw.partial = scratch;
+    CB_TRY(gemm(p.prec, hw, heads_wgrad_splits(n), s));
+    CB_TRY(colsum(p.prec, dz, n, A, A + 1, grads + po.logits_b, scratch, s));
+    CB_TRY(colsum(p.prec, dz + size_t(A) * es, n, 1, A + 1, grads + po.value_b, scratch, s));
+    // dh = (dz Wh^T) * (h > 0)
+    float* whp = reinterpret_cast<float*>(ws + p.whp);
+    CB_TRY(pack_heads_w(params + po.logits_w, params + po.value_w, p.hidden, A, whp, s));
+    GemmArgs hg{};
+    hg.a = whp; hg.a_f32 = 1; hg.a_kcontig = 0; hg.lda = p.hidden;
+    hg.b = dz; hg.b_f32 = st_f32; hg.b_kcontig = 1; hg.ldb = A + 1;
+    hg.M = p.hidden; hg.N = int(n); hg.K = A + 1; hg.alpha = 1.f;
+    hg.mask = ws + p.h; hg.ldmask = p.hidden;
+    hg.out1 = G[0]; hg.ld1 = p.hidden; hg.out1_f32 = st_f32; hg.msplit = p.hidden;
+    CB_TRY(gemm(p.prec, hg, 1, s));
+    // dense weight gradient: dWd[k][j] = sum_i relu(x)[i][k] dh[i][j]; bias: column sums of dh
+    GemmArgs dw{};
+    dw.a = G[0]; dw.a_f32 = st_f32; dw.a_kcontig = 0; dw.lda = p.hidden;
+    dw.b = ws + p.x[2][2]; dw.b_f32 = st_f32; dw.b_kcontig = 0; dw.ldb = p.flat; dw.b_relu = 1;
+    dw.M = p.hidden; dw.N = p.flat; dw.K = int(n); dw.alpha = 1.f;
+    dw.out1 = grads + po.dense_w; dw.ld1 = p.hidden; dw.out1_f32 = 1; dw.msplit = p.hidden;
+    dw.partial = scratch;
+    CB_TRY(gemm(p.prec, dw, dense_wgrad_splits(p.hidden, p.flat, n), s));
+    CB_TRY(colsum(p.prec, G[0], n, p.hidden, p.hidden, grads + po.dense_b, scratch, s));
+    // dense input gradient: dx[i][k] = (sum_j Wd[k][j] dh[i][j]) * (x[i][k] > 0)
+    GemmArgs dg{};
+    dg.a = params + po.dense_w; dg.a_f32 = 1; dg.a_kcontig = 1; dg.lda = p.hidden;
+    dg.b = G[0]; dg.b_f32 = st_f32; dg.b_kcontig = 1; dg.ldb = p.hidden;
+    dg.M = p.flat; dg.N = int(n); dg.K = p.hidden; dg.alpha = 1.f;
+    dg.mask = ws + p.x[2][2]; dg.ldmask = p.flat;
+    dg.out1 = G[1]; dg.ld1 = p.flat; dg.out1_f32 = st_f32; dg.msplit = p.flat;
+    CB_TRY(gemm(p.prec, dg, 1, s));
+
+    int gy = 1;
+    auto others = [](int k, int& a, int& b) { a = (k + 1) % 3; b = (k + 2) % 3; };
+    for (int st = 2; st >= 0; --st) {
+        const int C = p.C[st + 1], Hs = p.H[st + 1], Ws = p.W[st + 1];
+        for (int r = 1; r >= 0; --r) {
+            int fa, fb;
+            others(gy, fa, fb);
+            const int k0 = 1 + 2 * r, k1 = 2 + 2 * r;
+            // y = x + conv1(relu(t)) + b1 with t = conv0(relu(x)) + b0
+            WgradArgs w1{};
+            w1.x = ws + p.t[st][r]; w1.dy = G[gy]; w1.dw = grads + po.conv_w[st][k1];
+            w1.db = grads + po.conv_b[st][k1]; w1.partial = scratch;
+            w1.n = int(n); w1.H = Hs; w1.W = Ws; w1.scale = 1.f;
+            CB_TRY(conv3x3_wgrad(p.prec, C, C, IN_RELU, w1, s));
+            ConvArgs d1{};
+            d1.x = G[gy]; d1.w = params + po.conv_w[st][k1]; d1.mask = ws + p.t[st][r]; d1.y = G[fa];
+            d1.n = int(n); d1.H = Hs; d1.W = Ws; d1.scale = 1.f;
+            CB_TRY(conv3x3(p.prec, C, C, IN_PLAIN, 1, d1, s));
+            WgradArgs w0{};
+            w0.x = ws + p.x[st][r]; w0.dy = G[fa]; w0.dw = grads + po.conv_w[st][k0];
+            w0.db = grads + po.conv_b[st][k0]; w0.partial = scratch;
+            w0.n = int(n); w0.H = Hs; w0.W = Ws; w0.scale = 1.f;
+            CB_TRY(conv3x3_wgrad(p.prec, C, C, IN_RELU, w0, s));
+            ConvArgs d0{};
+            d0.x = G[fa]; d0.w = params + po.conv_w[st][k0]; d0.mask = ws + p.x[st][r];
+            d0.add = G[gy]; d0.y = G[fb];
+            d0.n = int(n); d0.H = Hs; d0.W = Ws; d0.scale = 1.f;
+            CB_TRY(conv3x3(p.prec, C, C, IN_PLAIN, 1, d0, s));
+            gy = fb;
+        }
+        int fa, fb;
+        others(gy, fa, fb);
+        CB_TRY(maxpool_bwd(p.prec, int(n), p.H[st], p.W[st], C,
+                           reinterpret_cast<const uint8_t*>(ws + p.idx[st]), G[gy], G[fa], s));
+        WgradArgs we{};
+        we.x = st == 0 ? static_cast<const void*>(obs) : static_cast<const void*>(ws + p.x[st - 1][2]);
+        we.row_idx = st == 0 ? row_idx : nullptr;
+        we.dy = G[fa]; we.dw = grads + po.conv_w[st][0]; we.db = grads + po.conv_b[st][0];
+        we.partial = scratch; we.n = int(n); we.H = p.H[st]; we.W = p.W[st];
+        we.scale = st == 0 ? 1.f / 255.f : 1.f;
+        CB_TRY(conv3x3_wgrad(p.prec, p.C[st], C, st == 0 ? IN_U8 : IN_PLAIN, we, s));
+        if (st > 0) {
+            ConvArgs de{};
+            de.x = G[fa]; de.w = params + po.conv_w[st][0]; de.y = G[fb];
+            de.n = int(n); de.H = p.H[st]; de.W = p.W[st]; de.scale = 1.f;
+            CB_TRY(conv3x3(p.prec, p.C[st], C, IN_PLAIN, 1, de, s));
+            gy = fb;
+        }
+    }
+    return hipSuccess;
+}
+
+}  // namespace cb

@@ -1,0 +1,112 @@
+"""CPU tests of the C-ABI boundary: the library loads, exports every declared symbol, agrees
+with the oracle's parameter layout, and rejects bad arguments before any HIP call."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+P = pytest.importorskip("paper_2310_00036_amd")
+
+from oracle import net as onet  # noqa: E402
+from synth import NetShape, WORKLOADS  # noqa: E402
+
+
+def _declared_functions():
+    names = set()
+    for h in ("cleanba_learner.h", "cleanba_layers.h"):
+        src = open(os.path.join(ROOT, "include", h)).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        for m in re.finditer(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\*?\s*([a-z_][a-z0-9_]*)\s*\(",
+                             src, flags=re.M):
+            names.add(m.group(1))
+    return names
+
+
+def test_exports_every_declared_symbol():
+    names = _declared_functions()
+    for want in ("impala_cnn_fwd", "impala_cnn_bwd", "gae_advantages", "vtrace_targets",
+                 "ppo_loss_grad", "impala_loss_grad", "adam_step", "learner_step"):
+        assert want in names
+    lib = C.CDLL(P._lib.LIB_PATH)
+    missing = [n for n in sorted(names) if not hasattr(lib, n)]
+    assert not missing, missing
+    assert names <= set(P._lib._SIGS), sorted(names - set(P._lib._SIGS))
+
+
+@pytest.mark.parametrize("net", [NetShape(), NetShape(num_actions=6), NetShape(ch=(32, 64, 64), hidden=512),
+                                 NetShape(in_h=12, in_w=10, ch=(16, 16, 32), hidden=8, num_actions=3)])
+def test_param_layout_matches_oracle(net):
+    got = P.impala_param_layout(net)
+    want = [(n, tuple(s), o) for n, s, o in onet.param_layout(net)]
+    assert got == want
+    assert P.impala_param_count(net) == onet.param_count(net)
+
+
+def test_invalid_nets_are_rejected():
+    for bad in (NetShape(in_c=3), NetShape(ch=(16, 24, 32)), NetShape(ch=(32, 16, 16)),
+                NetShape(num_actions=65), NetShape(hidden=0), NetShape(in_h=0)):
+        with pytest.raises(P.LibraryError) as e:
+            P.impala_param_count(bad)
+        assert e.value.status == -1
+
+
+def _net():
+    return C.byref(P.net_struct(NetShape()))
+
+
+def test_null_pointers_and_small_workspace_fail_before_hip():
+    lib = P.lib
+    # forward with NULL params
+    st = lib.impala_cnn_fwd(_net(), 0, None, 1, None, 4, 1, 1 << 40, 1, 1, 1, None)
+    assert st == -1 and b"params" in lib.impala_last_error()
+    # workspace too small
+    need = lib.impala_workspace_bytes(_net(), 4, 0, 1)
+    st = lib.impala_cnn_fwd(_net(), 0, 1, 1, None, 4, 1, need - 1, 1, 1, 1, None)
+    assert st == -2
+    st = lib.impala_cnn_bwd(_net(), 1, 1, 1, None, 4, 1, 16, 1, 1, 1, None)
+    assert st == -2
+    # bad precision
+    assert lib.impala_cnn_fwd(_net(), 7, 1, 1, None, 4, 1, 1 << 40, 1, 1, 1, None) == -1
+    # scans and losses
+    assert lib.gae_advantages(-1, 4, 1, 1, 1, 1, 1, 0.99, 0.95, 1, 1, None) == -1
+    assert lib.gae_advantages(8, 4, None, 1, 1, 1, 1, 0.99, 0.95, 1, 1, None) == -1
+    assert lib.vtrace_targets(8, 4, 1, 1, 1, 1, 1, 1, None, .99, 1, 1, 1, 1, 1, 1, None) == -1
+    assert lib.ppo_loss_grad(16, 0, 1, 1, 1, 1, 1, 1, 1, .1, .5, .01, 1, 1, 1, None) == -1
+    assert lib.ppo_loss_grad(16, 65, 1, 1, 1, 1, 1, 1, 1, .1, .5, .01, 1, 1, 1, None) == -1
+    assert lib.impala_loss_grad(0, 6, 1, 1, 1, 1, 1, 1., .5, .01, 1, 1, 1, None) == -1
+    # adam
+    assert lib.adam_step(10, 1, 1, 1, 1, 0, 1e-3, .9, .999, 1e-5, .5, None, 1, 1 << 20, None) == -1
+    assert lib.adam_step(10, 1, 1, 1, 1, 1, 1e-3, 1.0, .999, 1e-5, .5, None, 1, 1 << 20, None) == -1
+    assert lib.adam_step(10, 1, 1, 1, 1, 1, 1e-3, .9, .999, 1e-5, .5, None, 1, 8, None) == -2
+    # layers
+    assert lib.impala_conv3x3_fwd(0, 4, 84, 84, 4, 24, 1, 2, None, 1, None, None, 1, None) == -3
+    assert lib.impala_conv3x3_dgrad(0, 4, 42, 42, 32, 16, 1, 1, None, None, 1, None) == -3
+    assert lib.impala_maxpool_fwd(0, 4, 42, 42, 6, 1, 1, 1, None) == -3
+    # zero-size work is a no-op success
+    assert lib.gae_advantages(0, 4, None, None, None, None, None, .99, .95, None, None, None) == 0
+    assert lib.impala_cnn_fwd(_net(), 0, None, None, None, 0, None, 0, 1, None, None, None) == 0
+
+
+def test_learner_cfg_validation():
+    wl = WORKLOADS[1]
+    cfg = P.learner_cfg(wl, P.PREC_BF16)
+    assert P.learner_workspace_bytes(wl.net, cfg) > 0
+    bad = P.learner_cfg(wl.replace(minibatch_size=5000), P.PREC_BF16)   # 4 * 5000 > 8192
+    assert P.lib.learner_workspace_bytes(C.byref(P.net_struct(wl.net)), C.byref(bad)) == 0
+    assert b"exceeds" in P.lib.impala_last_error()
+    ro = P.Rollout()
+    st = C.c_int32(0)
+    r = P.lib.learner_step(C.byref(P.net_struct(wl.net)), C.byref(cfg), C.byref(ro), 1, 1, 1,
+                           C.byref(st), 1, 1, 1 << 40, 1, None)
+    assert r == -1 and b"obs" in P.lib.impala_last_error()
+
+
+def test_workspace_grows_with_frames_and_precision():
+    net = NetShape()
+    a = P.impala_workspace_bytes(net, 256, P.PREC_BF16, 1)
+    b = P.impala_workspace_bytes(net, 512, P.PREC_BF16, 1)
+    c = P.impala_workspace_bytes(net, 256, P.PREC_FP32, 1)
+    d = P.impala_workspace_bytes(net, 256, P.PREC_BF16, 0)
+    assert b > 1.9 * a and c > 1.8 * a and d < a

@@ -1,0 +1,272 @@
+"""GPU parity of every kernel against the oracle on identical inputs (via the C-ABI).
+
+bf16 mode: inputs are bf16-representable, so the only difference from the exact result is
+float32 accumulation order and the final rounding of stored outputs (checked to 1 bf16 ulp
+for stored activations, 1e-5 relative for float32 outputs). fp32 mode: 1e-5 relative.
+Shapes span several tiles and ragged tails (widths and heights that are not multiples of
+the tile, frame counts that are not multiples of the frames per workgroup).
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+from oracle import losses as olosses, net as onet, optim as ooptim, targets as otargets  # noqa: E402
+from tests import gpu_util as G  # noqa: E402
+
+P = pytest.importorskip("paper_2310_00036_amd")
+
+PRECS = [G.BF16, G.FP32]
+PNAME = {G.BF16: "bf16", G.FP32: "fp32"}
+
+
+def _relu(x):
+    return np.maximum(x, 0)
+
+
+# (n, H, W, cin, cout, mode): the network's conv shapes (base and wide) plus ragged ones
+CONV_CASES = [
+    (3, 84, 84, 4, 16, P.X_U8), (2, 84, 84, 4, 32, P.X_U8), (2, 13, 9, 4, 64, P.X_U8),
+    (3, 42, 42, 16, 16, P.X_RELU), (3, 42, 42, 16, 32, P.X_PLAIN), (2, 21, 21, 32, 32, P.X_PLAIN),
+    (5, 21, 21, 32, 32, P.X_RELU), (7, 11, 11, 32, 32, P.X_RELU), (3, 42, 42, 32, 64, P.X_PLAIN),
+    (3, 21, 21, 64, 64, P.X_RELU), (5, 11, 11, 64, 64, P.X_PLAIN), (2, 17, 23, 16, 64, P.X_PLAIN),
+]
+
+
+def _conv_inputs(n, H, W, cin, cout, mode, prec, seed):
+    rng = np.random.default_rng(seed)
+    if mode == P.X_U8:
+        x = rng.integers(0, 256, size=(n + 2, H, W, cin), dtype=np.uint8)
+        rows = rng.permutation(n + 2)[:n].astype(np.int32)
+        xin = x[rows].astype(np.float64) / 255.0
+    else:
+        x = G.q(rng.standard_normal((n, H, W, cin)), prec)
+        rows = None
+        xin = _relu(x) if mode == P.X_RELU else x
+    w = rng.standard_normal((3, 3, cin, cout)).astype(np.float32) * np.sqrt(2.0 / (9 * cin))
+    b = (0.1 * rng.standard_normal(cout)).astype(np.float32)
+    return x, rows, xin, w, b
+
+
+@pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
+@pytest.mark.parametrize("case", CONV_CASES, ids=lambda c: "n%d_%dx%d_%d-%d_m%d" % c)
+def test_conv_forward(case, prec):
+    n, H, W, cin, cout, mode = case
+    x, rows, xin, w, b = _conv_inputs(n, H, W, cin, cout, mode, prec, 11)
+    wq = G.q(w, prec)
+    add = G.q(np.random.default_rng(5).standard_normal((n, H, W, cout)), prec) if mode == P.X_RELU else None
+    want = onet.conv3x3(xin, wq, b.astype(np.float64)) + (add if add is not None else 0)
+    absum = onet.conv3x3(np.abs(xin), np.abs(wq), np.abs(b).astype(np.float64)) + \
+        (np.abs(add) if add is not None else 0)
+    dx = G.dev_u8(x) if mode == P.X_U8 else G.dev_act(x, prec)
+    y = G.empty_act((n, H, W, cout), prec)
+    P.impala_conv3x3_fwd(prec, n, H, W, cin, cout, dx, mode, G.dev_i32(rows) if rows is not None else None,
+                         G.dev_f32(w), G.dev_f32(b), G.dev_act(add, prec) if add is not None else None, y)
+    G.sync()
+    got = G.host(y)
+    if prec == G.BF16:
+        G.assert_bf16_ulp(got, want, absum, "conv fwd")
+    else:
+        G.assert_sum_close(got, want, absum, 1e-5, "conv fwd")
+
+
+DGRAD_CASES = [(3, 42, 42, 16, 16), (3, 42, 42, 16, 32), (4, 21, 21, 32, 32), (7, 11, 11, 32, 32),
+               (2, 42, 42, 32, 64), (3, 21, 21, 64, 64), (2, 17, 23, 16, 64)]
+
+
+@pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
+@pytest.mark.parametrize("case", DGRAD_CASES, ids=lambda c: "n%d_%dx%d_%d-%d" % c)
+@pytest.mark.parametrize("epi", ["plain", "mask_add"])
+def test_conv_input_gradient(case, prec, epi):
+    n, H, W, cin, cout = case
+    rng = np.random.default_rng(21)
+    dy = G.q(rng.standard_normal((n, H, W, cout)), prec)
+    w = (rng.standard_normal((3, 3, cin, cout)) * np.sqrt(2.0 / (9 * cin))).astype(np.float32)
+    mask = G.q(rng.standard_normal((n, H, W, cin)), prec) if epi == "mask_add" else None
+    add = G.q(rng.standard_normal((n, H, W, cin)), prec) if epi == "mask_add" else None
+    want = onet.conv3x3_dgrad(dy, G.q(w, prec))
+    absum = onet.conv3x3_dgrad(np.abs(dy), np.abs(G.q(w, prec)))
+    if mask is not None:
+        want = want * (mask > 0) + add
+        absum = absum * (mask > 0) + np.abs(add)
+    out = G.empty_act((n, H, W, cin), prec)
+    P.impala_conv3x3_dgrad(prec, n, H, W, cin, cout, G.dev_act(dy, prec), G.dev_f32(w),
+                           G.dev_act(mask, prec) if mask is not None else None,
+                           G.dev_act(add, prec) if add is not None else None, out)
+    G.sync()
+    if prec == G.BF16:
+        G.assert_bf16_ulp(G.host(out), want, absum, "dgrad")
+    else:
+        G.assert_sum_close(G.host(out), want, absum, 1e-5, "dgrad")
+
+
+@pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
+@pytest.mark.parametrize("case", CONV_CASES, ids=lambda c: "n%d_%dx%d_%d-%d_m%d" % c)
+def test_conv_weight_gradient(case, prec):
+    n, H, W, cin, cout, mode = case
+    x, rows, xin, _, _ = _conv_inputs(n, H, W, cin, cout, mode, prec, 31)
+    dy = G.q(np.random.default_rng(32).standard_normal((n, H, W, cout)), prec)
+    want_w, want_b = onet.conv3x3_wgrad(xin, dy)
+    abs_w, abs_b = onet.conv3x3_wgrad(np.abs(xin), np.abs(dy))
+    dw = G.dev_f32(np.zeros((3, 3, cin, cout)))
+    db = G.dev_f32(np.zeros(cout))
+    ws = G.ws_bytes(P.impala_conv3x3_wgrad_workspace_bytes(prec, H, W, cin, cout))
+    dx = G.dev_u8(x) if mode == P.X_U8 else G.dev_act(x, prec)
+    P.impala_conv3x3_wgrad(prec, n, H, W, cin, cout, dx, mode,
+                           G.dev_i32(rows) if rows is not None else None, G.dev_act(dy, prec), dw, db, ws)
+    G.sync()
+    G.assert_sum_close(G.host(dw), want_w, abs_w, 1e-5, "wgrad w")
+    G.assert_sum_close(G.host(db), want_b, abs_b, 1e-5, "wgrad b")
+
+
+@pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
+@pytest.mark.parametrize("shape", [(3, 84, 84, 16), (2, 42, 42, 32), (5, 21, 21, 32), (2, 11, 11, 64),
+                                   (3, 7, 9, 16)], ids=lambda s: "n%d_%dx%dx%d" % s)
+def test_maxpool_forward_backward(shape, prec):
+    n, H, W, C = shape
+    rng = np.random.default_rng(41)
+    # small integers: many exact ties, so the first-max rule is exercised
+    x = rng.integers(-4, 5, size=shape).astype(np.float64) * 0.25
+    y_want, arg_want = onet.maxpool(x)
+    OH, OW = y_want.shape[1:3]
+    y = G.empty_act((n, OH, OW, C), prec)
+    torch = G.torch()
+    arg = torch.empty((n, OH, OW, C), dtype=torch.uint8, device="cuda:0")
+    P.impala_maxpool_fwd(prec, n, H, W, C, G.dev_act(x, prec), y, arg)
+    dy = G.q(rng.standard_normal(y_want.shape), prec)
+    dx = G.empty_act(shape, prec)
+    P.impala_maxpool_bwd(prec, n, H, W, C, arg, G.dev_act(dy, prec), dx)
+    G.sync()
+    np.testing.assert_array_equal(G.host(y), y_want)
+    np.testing.assert_array_equal(arg.cpu().numpy(), arg_want)
+    want_dx = onet.maxpool_backward(arg_want, dy, shape)
+    abs_dx = onet.maxpool_backward(arg_want, np.abs(dy), shape)
+    if prec == G.BF16:
+        G.assert_bf16_ulp(G.host(dx), want_dx, abs_dx, "pool bwd")
+    else:
+        G.assert_sum_close(G.host(dx), want_dx, abs_dx, 1e-6, "pool bwd")
+
+
+@pytest.mark.parametrize("T,E", [(128, 64), (20, 64), (37, 100), (1, 3), (8, 4), (128, 128), (65, 257)])
+def test_gae_matches_oracle(T, E):
+    rng = np.random.default_rng(T * 1000 + E)
+    r = rng.choice([-1.0, 0.0, 1.0], size=(T, E), p=[.05, .9, .05]).astype(np.float32)
+    v = rng.standard_normal((T, E)).astype(np.float32)
+    d = (rng.random((T, E)) < 0.05).astype(np.uint8)
+    nv = rng.standard_normal(E).astype(np.float32)
+    nd = (rng.random(E) < 0.05).astype(np.uint8)
+    adv_w, ret_w = otargets.gae(r, v, d, nv, nd, 0.99, 0.95)
+    adv, ret = G.dev_f32(np.zeros((T, E))), G.dev_f32(np.zeros((T, E)))
+    P.gae_advantages(T, E, G.dev_f32(r), G.dev_f32(v), G.dev_u8(d), G.dev_f32(nv), G.dev_u8(nd),
+                     0.99, 0.95, adv, ret)
+    G.sync()
+    G.assert_close(G.host(adv), adv_w, 1e-5, "adv")
+    G.assert_close(G.host(ret), ret_w, 1e-5, "ret")
+
+
+@pytest.mark.parametrize("T,E,lam,rho,cbar", [(20, 64, 1.0, 1.0, 1.0), (128, 70, 0.95, 1.0, 1.0),
+                                              (33, 5, 1.0, 0.8, 1.2), (1, 1, 1.0, 1.0, 1.0)])
+def test_vtrace_matches_oracle(T, E, lam, rho, cbar):
+    rng = np.random.default_rng(7 * T + E)
+    r = rng.choice([-1.0, 0.0, 1.0], size=(T, E), p=[.05, .9, .05]).astype(np.float32)
+    v = rng.standard_normal((T, E)).astype(np.float32)
+    d = (rng.random((T, E)) < 0.05).astype(np.uint8)
+    bv = rng.standard_normal(E).astype(np.float32)
+    nd = (rng.random(E) < 0.05).astype(np.uint8)
+    mu = (rng.standard_normal((T, E)) * 0.5 - 2).astype(np.float32)
+    pi = (mu + 0.3 * rng.standard_normal((T, E))).astype(np.float32)
+    vs_w, pg_w = otargets.vtrace(mu, pi, r, v, d, bv, nd, 0.99, lam, rho, cbar, 1.0)
+    vs, pg = G.dev_f32(np.zeros((T, E))), G.dev_f32(np.zeros((T, E)))
+    P.vtrace_targets(T, E, G.dev_f32(mu), G.dev_f32(pi), G.dev_f32(r), G.dev_f32(v), G.dev_u8(d),
+                     G.dev_f32(bv), G.dev_u8(nd), 0.99, lam, rho, cbar, 1.0, vs, pg)
+    G.sync()
+    G.assert_close(G.host(vs), vs_w, 1e-5, "vs")
+    G.assert_close(G.host(pg), pg_w, 1e-5, "pg_adv")
+
+
+def _loss_batch(m, A, seed):
+    rng = np.random.default_rng(seed)
+    z = (rng.standard_normal((m, A)) * 3).astype(np.float32)
+    a = rng.integers(0, A, m).astype(np.int32)
+    lp = olosses.log_softmax(z.astype(np.float64))[np.arange(m), a]
+    return dict(z=z, v=rng.standard_normal(m).astype(np.float32), a=a,
+                old=(lp + 0.1 * rng.standard_normal(m)).astype(np.float32),
+                adv=(rng.standard_normal(m) * 2 + 0.3).astype(np.float32),
+                ret=rng.standard_normal(m).astype(np.float32),
+                vs=rng.standard_normal(m).astype(np.float32),
+                pg=rng.standard_normal(m).astype(np.float32))
+
+
+@pytest.mark.parametrize("m,A,norm", [(2048, 18, 1), (32, 6, 1), (8192, 18, 1), (1000, 7, 0), (1, 18, 0)])
+def test_ppo_loss_matches_oracle(m, A, norm):
+    b = _loss_batch(m, A, m + A)
+    L, dz_w, dv_w, st_w = olosses.ppo_loss_grad(b["z"], b["v"], b["a"], b["old"], b["adv"], b["ret"],
+                                                0.1, 0.5, 0.01, bool(norm))
+    dz, dv, st = G.dev_f32(np.zeros((m, A))), G.dev_f32(np.zeros(m)), G.dev_f32(np.zeros(8))
+    P.ppo_loss_grad(m, A, G.dev_f32(b["z"]), G.dev_f32(b["v"]), G.dev_i32(b["a"]), G.dev_f32(b["old"]),
+                    G.dev_f32(b["adv"]), G.dev_f32(b["ret"]), norm, 0.1, 0.5, 0.01, dz, dv, st)
+    G.sync()
+    G.assert_close(G.host(dz), dz_w, 1e-5, "dlogits")
+    G.assert_close(G.host(dv), dv_w, 1e-5, "dvalue")
+    got = G.host(st)
+    idx = [0, 1, 2, 3, 4, 6, 7] if m > 1 else [0, 1, 2, 3, 4, 6]
+    G.assert_close(got[idx], st_w[idx], 1e-5, "stats")
+    assert abs(got[5] - st_w[5]) <= 1.0 / m   # clip fraction: a count over rows
+
+
+@pytest.mark.parametrize("m,A", [(1280, 18), (37, 6), (4096, 64)])
+def test_impala_loss_matches_oracle(m, A):
+    b = _loss_batch(m, A, 3 * m + A)
+    L, dz_w, dv_w, st_w = olosses.impala_loss_grad(b["z"], b["v"], b["a"], b["vs"], b["pg"], 1.0, 0.5, 0.01)
+    dz, dv, st = G.dev_f32(np.zeros((m, A))), G.dev_f32(np.zeros(m)), G.dev_f32(np.zeros(8))
+    P.impala_loss_grad(m, A, G.dev_f32(b["z"]), G.dev_f32(b["v"]), G.dev_i32(b["a"]), G.dev_f32(b["vs"]),
+                       G.dev_f32(b["pg"]), 1.0, 0.5, 0.01, dz, dv, st)
+    G.sync()
+    G.assert_close(G.host(dz), dz_w, 1e-5, "dlogits")
+    G.assert_close(G.host(dv), dv_w, 1e-5, "dvalue")
+    G.assert_close(G.host(st)[:6], st_w[:6], 1e-5, "stats")
+
+
+@pytest.mark.parametrize("n,scale,max_norm,step", [(1_094_115, 1e-3, 0.5, 1), (1_094_115, 10.0, 0.5, 7),
+                                                    (4_364_211, 1.0, 40.0, 3), (1001, 1.0, 0.0, 2),
+                                                    (3, 1.0, 0.5, 1)])
+def test_adam_matches_oracle(n, scale, max_norm, step):
+    rng = np.random.default_rng(n + step)
+    p = rng.standard_normal(n).astype(np.float32)
+    g = (rng.standard_normal(n) * scale / np.sqrt(n) * 30).astype(np.float32)
+    m = (rng.standard_normal(n) * 1e-3).astype(np.float32)
+    v = (rng.random(n) * 1e-5).astype(np.float32)
+    # the library receives float32 hyperparameters; the oracle gets the same values
+    f = lambda x: float(np.float32(x))  # noqa: E731
+    gc, norm = ooptim.clip_by_global_norm(g, f(max_norm))
+    pw, mw, vw = ooptim.adam(p, gc, m, v, step, f(2.5e-4), f(0.9), f(0.999), f(1e-5))
+    dp, dg, dm, dv = G.dev_f32(p), G.dev_f32(g), G.dev_f32(m), G.dev_f32(v)
+    st = G.dev_f32(np.zeros(2))
+    ws = G.ws_bytes(P.adam_workspace_bytes(n))
+    P.adam_step(n, dp, dg, dm, dv, step, 2.5e-4, 0.9, 0.999, 1e-5, max_norm, st, ws)
+    G.sync()
+    G.assert_close(G.host(dm), mw, 1e-5, "m")
+    G.assert_close(G.host(dv), vw, 1e-5, "v")
+    # the new float32 parameter can only be as exact as its own rounding: within 2 ulps
+    # of the oracle's value, plus 1e-5 of the update
+    got_p = G.host(dp)
+    ulp = np.spacing(np.abs(pw).astype(np.float32)).astype(np.float64)
+    assert (np.abs(got_p - pw) <= 2 * ulp + 1e-5 * np.abs(pw - p)).all()
+    G.assert_close(got_p - p, pw - p, 1e-3, "param update")
+    s = G.host(st)
+    assert abs(s[0] - norm) <= 1e-5 * norm and s[1] == 0
+
+
+@pytest.mark.parametrize("n,A", [(128, 18), (1000, 6), (7, 64)])
+def test_gumbel_sample_bit_exact(n, A):
+    rng = np.random.default_rng(n)
+    z = (rng.standard_normal((n, A)) * 2).astype(np.float32)
+    z[::5, 1] = z[::5, 0]                           # exact ties in the logits
+    g = rng.gumbel(size=(n, A)).astype(np.float32)
+    g[::7] = 0.0                                     # ties in z + g, resolved to the lowest index
+    a_w, lp_w = olosses.gumbel_max(z, g)
+    act, lp = G.dev_i32(np.zeros(n)), G.dev_f32(np.zeros(n))
+    P.impala_gumbel_sample(n, A, G.dev_f32(z), G.dev_f32(g), act, lp)
+    G.sync()
+    np.testing.assert_array_equal(act.cpu().numpy(), a_w)
+    G.assert_close(G.host(lp), olosses.log_softmax(z.astype(np.float64))[np.arange(n), a_w], 1e-5, "logp")

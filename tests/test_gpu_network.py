@@ -1,0 +1,432 @@
+"""GPU parity of the whole network, the learner step and the actor step against the oracle.
+
+Tier A -- exact parity in float32 (1e-4 per tensor against the float64 oracle) on inputs
+the oracle certifies to have every max-pool top-2 gap, ReLU input and PPO clip test at
+least 1e-6..2e-6 (relative) away from switching (tests/certify.py). There every decision
+is the same on both sides and only summation order differs.
+
+Tier B -- the workload shapes as specified (He-normal init, 84x84 frames, tens of frames):
+there some decisions sit within float32 rounding of switching, and one switched max-pool
+argmax moves a conv-weight gradient by ~1e-3..1e-2 relative (the oracle's own float32 vs
+float64 evaluation shows up to 6e-3 on these inputs). float32 is held to FP32_FLIP_TOL per
+tensor. bf16 is compared with the oracle's bf16-emulating mode (logits and values to 2e-2);
+its gradients are held to statistical bounds: a global relative L2 and cosine over all
+parameters, and a per-tensor bound far below what any indexing error produces (~1.0).
+The bf16 kernels themselves are pinned to 1 bf16 ulp in test_gpu_kernels.py.
+
+Tier C -- full-size shapes (2048-frame minibatches): sampled forward rows, a sparse-row
+backward the oracle can recompute frame by frame, bit-exact determinism, and bit-exact
+equality of learner_step with the composition of its ABI calls.
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+from oracle import learner as olearner, losses as olosses, net as onet  # noqa: E402
+from synth import NetShape, Workload, WORKLOADS, draw_params, draw_rollout, draw_actor_batch  # noqa: E402
+from tests import certify, gpu_util as G  # noqa: E402
+
+P = pytest.importorskip("paper_2310_00036_amd")
+
+PNAME = {G.BF16: "bf16", G.FP32: "fp32"}
+FP32_TOL = 1e-4              # tier A
+FP32_FLIP_TOL = 2e-2         # tier B, float32
+BF16_OUT_TOL = 2e-2          # logits / values, bf16 vs bf16 emulation
+# tier B, bf16: error(GPU vs float64) <= K * error(bf16-emulating oracle vs float64) + slack
+BF16_K_TENSOR, BF16_SLACK_TENSOR = 3.0, 0.05
+BF16_K_GLOBAL, BF16_SLACK_GLOBAL = 2.0, 0.02
+
+
+def _tensor_errs(got, want, net):
+    errs = {}
+    for name, shape, off in onet.param_layout(net):
+        sl = slice(off, off + int(np.prod(shape)))
+        errs[name] = G.rel_l2(got[sl], want[sl])
+    return errs
+
+
+def _check_grads(got, want, net, prec, label="", tier="A", emu=None):
+    """got vs want (float64 oracle), tensor by tensor: ||d_t|| <= tol_t ||g_t|| + slack ||g||.
+
+    The slack, a share of the whole gradient's norm, covers tensors whose true gradient is
+    itself below the arithmetic's resolution (a saturated softmax makes the policy-logit
+    gradient ~1e-20 of the value gradient; a bias gradient can be a cancelling sum).
+    float32: tol_t = the tier's tolerance, slack = 2^-20. bf16: emu is the bf16-emulating
+    oracle's result; tol_t = 3 x its own error on the tensor + 0.05 and slack = 5% of its
+    global error (module docstring)."""
+    glob = G.rel_l2(got, want)
+    gnorm = np.linalg.norm(want)
+    errs = _tensor_errs(got, want, net)
+    print(f"\n[{label} {PNAME[prec]} tier {tier}] gradient error vs float64: worst tensor "
+          f"{max(errs.values()):.3e} ({max(errs, key=errs.get)}), global {glob:.3e}", flush=True)
+    if prec == G.FP32:
+        tol = {k: FP32_TOL if tier == "A" else FP32_FLIP_TOL for k in errs}
+        slack = 2.0 ** -20
+    else:
+        floor = _tensor_errs(emu, want, net)
+        gfloor = G.rel_l2(emu, want)
+        print(f"    bf16-emulation floor: worst tensor {max(floor.values()):.3e}, global {gfloor:.3e}", flush=True)
+        assert glob <= BF16_K_GLOBAL * gfloor + BF16_SLACK_GLOBAL, (glob, gfloor)
+        tol = {k: BF16_K_TENSOR * floor[k] + BF16_SLACK_TENSOR for k in errs}
+        slack = 0.05 * gfloor
+    bad = {}
+    for name, shape, off in onet.param_layout(net):
+        sl = slice(off, off + int(np.prod(shape)))
+        d, gt = np.linalg.norm(got[sl] - want[sl]), np.linalg.norm(want[sl])
+        if d > tol[name] * gt + slack * gnorm:
+            bad[name] = (errs[name], float(gt / gnorm))
+    assert not bad, bad
+
+
+def _run_fwd_bwd(net, prec, params, obs, rows, n, dz, dv):
+    torch = G.torch()
+    ws = G.ws_bytes(P.impala_workspace_bytes(net, n, prec, 1))
+    logits = torch.empty((n, net.num_actions), dtype=torch.float32, device="cuda:0")
+    value = torch.empty(n, dtype=torch.float32, device="cuda:0")
+    grads = torch.empty(onet.param_count(net), dtype=torch.float32, device="cuda:0")
+    P.impala_cnn_fwd(net, prec, G.dev_f32(params), G.dev_u8(obs), G.dev_i32(rows) if rows is not None else None,
+                     n, ws, 1, logits, value)
+    if dz is not None:
+        P.impala_cnn_bwd(net, prec, G.dev_f32(params), G.dev_u8(obs), G.dev_i32(rows) if rows is not None else None,
+                         n, ws, G.dev_f32(dz), G.dev_f32(dv), grads)
+    G.sync()
+    return G.host(logits), G.host(value), G.host(grads)
+
+
+NETS = {"base_a6": NetShape(num_actions=6), "base": NetShape(), "wide": NetShape(ch=(32, 64, 64), hidden=512)}
+# certified frames per net: (frames, margin threshold); see tests/certify.py
+CERT = {"base_a6": (2, 2e-6), "base": (2, 2e-6), "wide": (1, 1e-6)}
+
+
+@pytest.mark.parametrize("netname", ["base_a6", "base", "wide"])
+def test_cnn_fp32_exact_on_certified_frames(netname):
+    """Tier A: float32 forward and backward, gathering the certified frames from a larger
+    uint8 buffer by row index, against the float64 oracle to 1e-4 per tensor."""
+    net = NETS[netname]
+    params = draw_params(net, 7)
+    k, thr = CERT[netname]
+    seed, frames, margin = certify.certified_frames(net, params, k, threshold=thr)
+    print(f"\ncertified seed {seed} margin {margin:.2e}", flush=True)
+    rng = np.random.default_rng(seed)
+    obs = rng.integers(0, 256, size=(k + 5, 84, 84, 4), dtype=np.uint8)
+    rows = rng.permutation(k + 5)[:k].astype(np.int32)
+    obs[rows] = frames
+    dz = (rng.standard_normal((k, net.num_actions)) * 0.1).astype(np.float32)
+    dv = rng.standard_normal(k).astype(np.float32)
+    z_w, v_w, cache = onet.forward(net, params, frames, "fp64")
+    g_w = onet.backward(net, cache, dz, dv)
+    z, v, g = _run_fwd_bwd(net, G.FP32, params, obs, rows, k, dz, dv)
+    G.assert_close(z, z_w, FP32_TOL, "logits")
+    G.assert_close(v, v_w, FP32_TOL, "value")
+    _check_grads(g, g_w, net, G.FP32, netname, "A")
+
+
+@pytest.mark.parametrize("prec", [G.BF16, G.FP32], ids=lambda p: PNAME[p])
+@pytest.mark.parametrize("netname", ["base_a6", "base", "wide"])
+def test_cnn_forward_backward_with_gather(prec, netname):
+    """Tier B: 5 gathered frames, uncertified."""
+    net = NETS[netname]
+    rng = np.random.default_rng(3)
+    params = draw_params(net, 7)
+    obs = rng.integers(0, 256, size=(9, 84, 84, 4), dtype=np.uint8)
+    rows = np.array([4, 0, 7, 2, 8], np.int32)
+    n = len(rows)
+    dz = (rng.standard_normal((n, net.num_actions)) * 0.1).astype(np.float32)
+    dv = rng.standard_normal(n).astype(np.float32)
+    z_w, v_w, cache = onet.forward(net, params, obs[rows], "fp64")
+    g_w = onet.backward(net, cache, dz, dv)
+    emu = None
+    if prec == G.BF16:
+        z_e, v_e, cache_e = onet.forward(net, params, obs[rows], "bf16")
+        emu = onet.backward(net, cache_e, dz, dv)
+        z_w, v_w = z_e, v_e                      # outputs compared with the emulation
+    z, v, g = _run_fwd_bwd(net, prec, params, obs, rows, n, dz, dv)
+    tol = FP32_TOL if prec == G.FP32 else BF16_OUT_TOL
+    G.assert_close(z, z_w, tol, "logits")
+    G.assert_close(v, v_w, tol, "value")
+    _check_grads(g, g_w, net, prec, netname, "B", emu)
+
+
+@pytest.mark.parametrize("prec", [G.BF16, G.FP32], ids=lambda p: PNAME[p])
+def test_cnn_full_minibatch_sampled_rows(prec):
+    """At the PPO minibatch size (2048 frames) in the launch configuration the learner uses:
+    forward outputs on sampled rows, and the backward pass with the upstream gradient
+    non-zero on 3 sampled rows only (the gradient is then that of those rows alone), which
+    the oracle computes frame by frame."""
+    net = NetShape()
+    n = 2048
+    rng = np.random.default_rng(11)
+    params = draw_params(net, 1)
+    obs = rng.integers(0, 256, size=(n, 84, 84, 4), dtype=np.uint8)
+    rows = rng.permutation(n).astype(np.int32)
+    pick = np.array([0, 1337, n - 1])
+    if prec == G.FP32:   # tier A on the rows that carry gradient
+        _, frames, _ = certify.certified_frames(net, params, 3, threshold=1e-6)
+        obs[rows[pick]] = frames
+    dz = np.zeros((n, net.num_actions), np.float32)
+    dv = np.zeros(n, np.float32)
+    dz[pick] = rng.standard_normal((3, net.num_actions)) * 0.1
+    dv[pick] = rng.standard_normal(3)
+    z, v, g = _run_fwd_bwd(net, prec, params, obs, rows, n, dz, dv)
+    sample = np.array([0, 5, 1337, 2000, n - 1])
+    z_w, v_w, _ = onet.forward(net, params, obs[rows[sample]], "fp64" if prec == G.FP32 else "bf16")
+    tol = FP32_TOL if prec == G.FP32 else BF16_OUT_TOL
+    G.assert_close(z[sample], z_w, tol, "logits")
+    G.assert_close(v[sample], v_w, tol, "value")
+    _, _, cache = onet.forward(net, params, obs[rows[pick]], "fp64")
+    g_w = onet.backward(net, cache, dz[pick], dv[pick])
+    emu = None
+    if prec == G.BF16:
+        _, _, cache_e = onet.forward(net, params, obs[rows[pick]], "bf16")
+        emu = onet.backward(net, cache_e, dz[pick], dv[pick])
+    _check_grads(g, g_w, net, prec, "mb2048-sparse", "A" if prec == G.FP32 else "B", emu)
+
+
+def _gpu_rollout(ro, wl):
+    return dict(obs=G.dev_u8(ro["obs"]), actions=G.dev_i32(ro["actions"]), logp=G.dev_f32(ro["logp"]),
+                rewards=G.dev_f32(ro["rewards"]), dones=G.dev_u8(ro["dones"]),
+                values=G.dev_f32(ro["values"]) if "values" in ro else None,
+                next_value=G.dev_f32(ro["next_value"]) if "next_value" in ro else None,
+                next_done=G.dev_u8(ro["next_done"]))
+
+
+def _learner_gpu(wl, prec, params, ro, perm, n_calls=1, state=None):
+    torch = G.torch()
+    net = wl.net
+    cfg = P.learner_cfg(wl, prec)
+    ws = G.ws_bytes(P.learner_workspace_bytes(net, cfg))
+    d = _gpu_rollout(ro, wl)
+    rs = P.rollout_struct(d["obs"], d["actions"], d["logp"], d["rewards"], d["dones"], d["values"],
+                          d["next_value"], d["next_done"])
+    if state is None:
+        p = G.dev_f32(params)
+        m = torch.zeros_like(p)
+        v = torch.zeros_like(p)
+        step = 0
+    else:
+        p, m, v, step = state
+    stats = torch.zeros((wl.n_updates, 8), dtype=torch.float32, device="cuda:0")
+    dperm = G.dev_i32(perm) if perm is not None else None
+    for _ in range(n_calls):
+        step = P.learner_step(net, cfg, rs, p, m, v, step, dperm, ws, stats)
+    G.sync()
+    return p, m, v, step, stats, (d, rs, ws)
+
+
+def _compare_learner(wl, prec, p0, out_gpu, want, label, tier, emu=None):
+    """want: float64 oracle (params, m, v, step, stats); emu: bf16-emulating oracle."""
+    p, m, v, step, stats = out_gpu[:5]
+    assert step == want[3]
+    net = wl.net
+    got_m, got_v, got_p = G.host(m), G.host(v), G.host(p)
+    # m after the updates is a weighted sum of the (clipped) gradients: per-tensor parity
+    _check_grads(got_m, want[1], net, prec, label + " adam-m", tier, None if emu is None else emu[1])
+    if prec == G.FP32:
+        tol = FP32_TOL if tier == "A" else FP32_FLIP_TOL
+        assert G.rel_l2(got_v, want[2]) <= 2 * tol
+        assert G.rel_l2(got_p - p0, want[0] - p0) <= 2 * tol
+    else:
+        assert G.rel_l2(got_v, want[2]) <= 2 * BF16_K_GLOBAL * G.rel_l2(emu[2], want[2]) + 2 * BF16_SLACK_GLOBAL
+        assert G.rel_l2(got_p - p0, want[0] - p0) <= \
+            BF16_K_GLOBAL * G.rel_l2(emu[0] - p0, want[0] - p0) + BF16_SLACK_GLOBAL
+    s_, sw = G.host(stats), np.asarray(want[4])
+    for col in (0, 1, 2, 3, 6):   # loss, policy, value, entropy, grad norm
+        scale = abs(sw[:, col]).max() + 1e-3
+        if prec == G.FP32:
+            tol = (1e-4 if tier == "A" else FP32_FLIP_TOL) * scale
+        else:   # within 3x the bf16 emulation's own deviation (free-running over the updates)
+            tol = 3 * abs(np.asarray(emu[4])[:, col] - sw[:, col]).max() + 0.05 * scale
+        assert abs(s_[:, col] - sw[:, col]).max() <= tol, (col, s_[:, col], sw[:, col])
+    assert (s_[:, 7] == 0).all()
+
+
+def _oracle_learner(wl, params, ro, perm, prec):
+    z = np.zeros_like(params, dtype=np.float64)
+    if wl.algo == "ppo":
+        run = lambda mode: olearner.ppo_learner_step(wl.net, wl, ro, params, z, z, 0, perm, mode)  # noqa: E731
+    else:
+        run = lambda mode: olearner.impala_learner_step(wl.net, wl, ro, params, z, z, 0, mode)  # noqa: E731
+    return run("fp64"), (run("bf16") if prec == G.BF16 else None)
+
+
+def _certified_rollout(wl, params, threshold=1e-6, max_seeds=300):
+    """First workload seed whose learner frames are certified and, for PPO, whose clip tests
+    are at least 1e-4 away from switching."""
+    T, E = wl.T, wl.E
+    for seed in range(max_seeds):
+        w = wl.replace(seed=seed)
+        raw = draw_rollout(w)
+        frames = raw["obs"][:T].reshape(T * E, 84, 84, 4)
+        if certify.decision_margin(wl.net, params, frames) <= threshold:
+            continue
+        ro = olearner.behaviour_rollout(w, params, raw)
+        if w.algo == "ppo":
+            z, _, _ = onet.forward(w.net, params, ro["obs"])
+            if certify.ppo_clip_margin(z, ro["actions"], ro["logp"], w.clip_eps) < 1e-4:
+                continue
+        return w, raw, ro
+    raise RuntimeError("no certified rollout")
+
+
+@pytest.mark.parametrize("algo", ["ppo", "impala"])
+def test_learner_step_fp32_exact_on_certified_rollout(algo):
+    """Tier A: a whole learning phase (targets, loss, backward, clip, Adam) in float32 on a
+    2-step, 1-env rollout whose decisions the oracle certifies, to 1e-4."""
+    base = WORKLOADS[0] if algo == "ppo" else WORKLOADS[2]
+    wl = base.replace(T=2, E=1, net=NetShape(num_actions=6))
+    params = draw_params(wl.net, 5)
+    wl, raw, ro = _certified_rollout(wl, params)
+    want, _ = _oracle_learner(wl, params, ro, raw["perm"], G.FP32)
+    got = _learner_gpu(wl, G.FP32, params, ro, raw["perm"] if algo == "ppo" else None)
+    _compare_learner(wl, G.FP32, params.astype(np.float64), got, want, f"{algo}-certified", "A")
+
+
+@pytest.mark.parametrize("prec", [G.BF16, G.FP32], ids=lambda p: PNAME[p])
+def test_learner_step_ppo_tiny(prec):
+    """Tier B: PPO, 4 envs x 8 steps, 6 actions, one full-batch update (the tiny workload)."""
+    wl = WORKLOADS[0]
+    params = draw_params(wl.net, wl.seed)
+    raw = draw_rollout(wl)
+    ro = olearner.behaviour_rollout(wl, params, raw)
+    want, emu = _oracle_learner(wl, params, ro, raw["perm"], prec)
+    got = _learner_gpu(wl, prec, params, ro, raw["perm"])
+    _compare_learner(wl, prec, params.astype(np.float64), got, want, "ppo-tiny", "B", emu)
+
+
+@pytest.mark.parametrize("prec", [G.BF16, G.FP32], ids=lambda p: PNAME[p])
+def test_learner_step_ppo_multi_minibatch(prec):
+    """Tier B: PPO with 2 epochs x 3 minibatches of 8 over a 6 x 4 rollout (6 updates,
+    advantage normalisation per minibatch, permuted rows)."""
+    wl = Workload("ppo_small", "ppo", T=4, E=6, net=NetShape(num_actions=5), epochs=2,
+                  num_minibatches=3, seed=21)
+    params = draw_params(wl.net, wl.seed)
+    raw = draw_rollout(wl)
+    ro = olearner.behaviour_rollout(wl, params, raw)
+    want, emu = _oracle_learner(wl, params, ro, raw["perm"], prec)
+    got = _learner_gpu(wl, prec, params, ro, raw["perm"])
+    _compare_learner(wl, prec, params.astype(np.float64), got, want, "ppo-6upd", "B", emu)
+
+
+@pytest.mark.parametrize("prec", [G.BF16, G.FP32], ids=lambda p: PNAME[p])
+def test_learner_step_impala_small(prec):
+    """Tier B: IMPALA / V-trace with off-policy behaviour logits, 8 envs x 5 steps + bootstrap."""
+    wl = WORKLOADS[2].replace(T=5, E=8, seed=22)
+    params = draw_params(wl.net, wl.seed)
+    raw = draw_rollout(wl)
+    ro = olearner.behaviour_rollout(wl, params, raw)
+    want, emu = _oracle_learner(wl, params, ro, None, prec)
+    got = _learner_gpu(wl, prec, params, ro, None)
+    _compare_learner(wl, prec, params.astype(np.float64), got, want, "impala", "B", emu)
+
+
+def _c1_like_inputs(seed=1):
+    """PPO 64 x 128 rollout with minibatches of 2048 (Cleanba-like shape); behaviour data
+    are drawn without the network (this test compares GPU against GPU)."""
+    wl = WORKLOADS[1]
+    raw = draw_rollout(wl)
+    rng = np.random.default_rng(seed)
+    T, E, A = wl.T, wl.E, wl.net.num_actions
+    ro = dict(obs=raw["obs"][:T].reshape(T * E, 84, 84, 4), actions=rng.integers(0, A, T * E).astype(np.int32),
+              logp=(np.log(1.0 / A) + 0.05 * rng.standard_normal(T * E)).astype(np.float32),
+              rewards=raw["rewards"], dones=raw["dones"], values=(0.1 * rng.standard_normal((T, E))).astype(np.float32),
+              next_value=(0.1 * rng.standard_normal(E)).astype(np.float32), next_done=raw["next_done"])
+    return wl, draw_params(wl.net, wl.seed), ro, raw["perm"]
+
+
+def test_learner_step_is_deterministic_and_resumable():
+    """Bit-identical results when a learning phase is repeated from the same state (no
+    atomics), and two phases in a row equal one phase, a copy of the state, and another."""
+    torch = G.torch()
+    wl, params, ro, perm = _c1_like_inputs()
+    wl = wl.replace(epochs=1, num_minibatches=2)
+    a = _learner_gpu(wl, G.BF16, params, ro, perm)
+    b = _learner_gpu(wl, G.BF16, params, ro, perm)
+    for x, y in zip(a[:3], b[:3]):
+        assert torch.equal(x, y)
+    assert torch.equal(a[4], b[4])
+    two = _learner_gpu(wl, G.BF16, params, ro, perm, n_calls=2)
+    saved = (a[0].clone(), a[1].clone(), a[2].clone(), a[3])
+    resumed = _learner_gpu(wl, G.BF16, params, ro, perm, state=saved)
+    assert two[3] == resumed[3] == 4
+    for x, y in zip(two[:3], resumed[:3]):
+        assert torch.equal(x, y)
+
+
+def test_learner_step_equals_its_abi_calls():
+    """learner_step (PPO) is exactly GAE, then per minibatch impala_cnn_fwd with the permuted
+    rows, ppo_loss_grad on the gathered rows, impala_cnn_bwd and adam_step."""
+    torch = G.torch()
+    wl, params, ro, perm = _c1_like_inputs()
+    wl = wl.replace(epochs=1, num_minibatches=2)
+    net, prec = wl.net, G.BF16
+    got = _learner_gpu(wl, prec, params, ro, perm)
+    d = _gpu_rollout(ro, wl)
+    T, E, A, mb = wl.T, wl.E, net.num_actions, wl.mb
+    adv = torch.empty((T, E), dtype=torch.float32, device="cuda:0")
+    ret = torch.empty_like(adv)
+    P.gae_advantages(T, E, d["rewards"], d["values"], d["dones"], d["next_value"], d["next_done"],
+                     wl.gamma, wl.lam, adv, ret)
+    p = G.dev_f32(params)
+    m, v = torch.zeros_like(p), torch.zeros_like(p)
+    ws = G.ws_bytes(P.impala_workspace_bytes(net, mb, prec, 1))
+    aws = G.ws_bytes(P.adam_workspace_bytes(p.numel()))
+    grads = torch.empty_like(p)
+    logits = torch.empty((mb, A), dtype=torch.float32, device="cuda:0")
+    value = torch.empty(mb, dtype=torch.float32, device="cuda:0")
+    dz, dv = torch.empty_like(logits), torch.empty_like(value)
+    stats = torch.zeros((wl.n_updates, 8), dtype=torch.float32, device="cuda:0")
+    dperm = G.dev_i32(perm)
+    u = 0
+    for j in range(wl.epochs):
+        for k in range(wl.num_minibatches):
+            rows = dperm[j, k * mb:(k + 1) * mb].contiguous()
+            P.impala_cnn_fwd(net, prec, p, d["obs"], rows, mb, ws, 1, logits, value)
+            rl = rows.long()
+            P.ppo_loss_grad(mb, A, logits, value, d["actions"][rl].contiguous(), d["logp"][rl].contiguous(),
+                            adv.view(-1)[rl].contiguous(), ret.view(-1)[rl].contiguous(), 1, wl.clip_eps,
+                            wl.vf_coef, wl.ent_coef, dz, dv, stats[u])
+            P.impala_cnn_bwd(net, prec, p, d["obs"], rows, mb, ws, dz, dv, grads)
+            P.adam_step(p.numel(), p, grads, m, v, u + 1, wl.lr, wl.beta1, wl.beta2, wl.adam_eps,
+                        wl.max_grad_norm, stats[u, 6:], aws)
+            u += 1
+    G.sync()
+    assert torch.equal(got[0], p) and torch.equal(got[1], m) and torch.equal(got[2], v)
+    assert torch.equal(got[4], stats)
+
+
+@pytest.mark.parametrize("prec", [G.BF16, G.FP32], ids=lambda p: PNAME[p])
+def test_actor_step_matches_oracle(prec):
+    """128 frames per call with Gumbel-max sampling. Actions must equal the oracle's wherever
+    the top-2 gap of z + g exceeds the logit error bound; logp / value to the tolerances."""
+    wl = WORKLOADS[3]
+    net = wl.net
+    batch = draw_actor_batch(wl)
+    params = draw_params(net, wl.seed)
+    n = wl.T
+    torch = G.torch()
+    ws = G.ws_bytes(P.impala_workspace_bytes(net, n, prec, 0))
+    act = torch.empty(n, dtype=torch.int32, device="cuda:0")
+    logp = torch.empty(n, dtype=torch.float32, device="cuda:0")
+    value = torch.empty(n, dtype=torch.float32, device="cuda:0")
+    logits = torch.empty((n, net.num_actions), dtype=torch.float32, device="cuda:0")
+    P.impala_actor_step(net, prec, G.dev_f32(params), G.dev_u8(batch["obs"]), n, G.dev_f32(batch["gumbel"]),
+                        ws, act, logp, value, logits)
+    G.sync()
+    a_w, lp_w, v_w, z_w = olearner.actor_step(net, params, batch["obs"], batch["gumbel"],
+                                              "fp64" if prec == G.FP32 else "bf16")
+    tol = FP32_TOL if prec == G.FP32 else BF16_OUT_TOL
+    G.assert_close(G.host(value), v_w, tol, "value")
+    z = G.host(logits)
+    G.assert_close(z, z_w, tol, "logits")
+    a = act.cpu().numpy()
+    err = np.abs(z - z_w).max(axis=1) * 2
+    s = np.sort(z_w + batch["gumbel"], axis=1)
+    gap = s[:, -1] - s[:, -2]
+    mismatch = a != a_w
+    assert not (mismatch & (gap > err)).any(), np.nonzero(mismatch & (gap > err))
+    # log pi(a) = z_a - logsumexp(z) moves by at most 2 max_j |dz_j|: bound it by the
+    # observed logit error (large He-normal logits make logp ill-conditioned)
+    same = ~mismatch
+    dlp = np.abs(G.host(logp) - lp_w)[same]
+    assert (dlp <= 2 * np.abs(z - z_w).max(axis=1)[same] + 1e-6 * (1 + np.abs(lp_w[same]))).all()
