@@ -74,6 +74,10 @@ _SIGS = {
     "impala_maxpool_fwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _P, _P, _P, _P]),
     "impala_maxpool_bwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _P, _P, _P, _P]),
     "impala_gumbel_sample": (C.c_int, [_I64, _I32, _P, _P, _P, _P, _P]),
+    "impala_profile_begin": (C.c_int, [C.c_char_p, _I32]),
+    "impala_profile_end": (C.c_int, []),
+    "impala_profile_key": (C.c_int, [_I32, C.c_char_p, _SZ, C.POINTER(C.c_double), C.POINTER(_I32)]),
+    "impala_profile_dropped": (_I32, []),
 }
 
 
@@ -291,3 +295,22 @@ def impala_maxpool_bwd(prec, n, H, W, C_, arg, dy, dx, stream=None):
 def impala_gumbel_sample(n, A, logits, gumbel, actions, logp, stream=None):
     _check("impala_gumbel_sample", lib.impala_gumbel_sample(n, A, ptr(logits), ptr(gumbel), ptr(actions),
                                                             ptr(logp), stream_handle(stream)))
+
+
+def impala_profile_begin(only_key: str | None = None, max_launches: int = 1 << 16) -> None:
+    _check("impala_profile_begin", lib.impala_profile_begin(
+        only_key.encode() if only_key else None, max_launches))
+
+
+def impala_profile_end() -> list:
+    """Close the profile; returns [(key, total_ms, launches)] sorted by total time."""
+    k = lib.impala_profile_end()
+    if k < 0:
+        raise LibraryError("impala_profile_end", k)
+    out = []
+    buf = C.create_string_buffer(128)
+    ms, cnt = C.c_double(), C.c_int32()
+    for i in range(k):
+        _check("impala_profile_key", lib.impala_profile_key(i, buf, 128, C.byref(ms), C.byref(cnt)))
+        out.append((buf.value.decode(), ms.value, cnt.value))
+    return sorted(out, key=lambda r: -r[1])

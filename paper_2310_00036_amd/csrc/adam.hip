@@ -86,7 +86,11 @@ hipError_t adam(int64_t n, float* p, const float* g, float* m, float* v, float l
     int64_t blocks = (n / 4 + 255) / 256;
     if (blocks < 1) blocks = 1;
     if (blocks > kAdamBlocks) blocks = kAdamBlocks;
-    hipLaunchKernelGGL(sumsq_kernel, dim3(unsigned(blocks)), dim3(256), 0, s, n, g, part);
+    {
+        ProfScope ps(s, [&] { return "grad_sumsq/" + std::to_string(n); });
+        hipLaunchKernelGGL(sumsq_kernel, dim3(unsigned(blocks)), dim3(256), 0, s, n, g, part);
+    }
+    ProfScope ps(s, [&] { return "adam/" + std::to_string(n); });
     hipLaunchKernelGGL(adam_kernel, dim3(unsigned(blocks)), dim3(256), 0, s, n, p, g, m, v, lr, b1, b2,
                        omb1, omb2, bc1, bc2, eps, max_norm, part, int(blocks), stats);
     return hipGetLastError();

@@ -118,6 +118,7 @@ size_t lds_limit() {
 
 hipError_t fill_zero(float* p, int64_t n, hipStream_t s) {
     if (n <= 0) return hipSuccess;
+    ProfScope ps(s, [&] { return "fill_zero/" + std::to_string(n); });
     hipLaunchKernelGGL(fill_zero_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, p, n);
     return hipGetLastError();
 }

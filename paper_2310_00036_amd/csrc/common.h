@@ -7,6 +7,14 @@
 
 #define CB_DEV __device__ __forceinline__
 
+#include <string>
+
+// Profiling key of a launch: family/precision/shape (see include/cleanba_profile.h).
+inline std::string cb_key(const char* family, int prec, const std::string& shape) {
+    return std::string(family) + (prec == 0 ? "/bf16/" : "/fp32/") + shape;
+}
+inline std::string cb_dims(int a, int b) { return std::to_string(a) + "x" + std::to_string(b); }
+
 typedef __bf16 cb_bf16x8 __attribute__((ext_vector_type(8)));
 typedef float cb_f32x4 __attribute__((ext_vector_type(4)));
 

@@ -253,6 +253,10 @@ hipError_t launch(const ConvArgs& a, int cout_total, hipStream_t s) {
     const int nfg = (a.n + FR - 1) / FR;
     const size_t lds = conv_lds_bytes<P, CIN, COUT>(TH, FR, W);
     dim3 grid(unsigned(nbands * nfg), unsigned(cout_total / COUT));
+    ProfScope ps(s, [&] {
+        return cb_key(FLIP ? "conv_dgrad" : "conv_fwd", sizeof(typename P::T) == 2 ? 0 : 1,
+                      cb_dims(CIN, cout_total) + "/" + cb_dims(H, W));
+    });
     hipLaunchKernelGGL((conv3x3_kernel<P, CIN, COUT, MODE, FLIP>), grid, dim3(256), lds, s, a, TH,
                        FR, nbands, cout_total);
     return hipGetLastError();

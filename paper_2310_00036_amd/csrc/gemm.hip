@@ -141,8 +141,14 @@ static hipError_t gemm_launch(const GemmArgs& a, int splits, hipStream_t s) {
     if (kchunk <= 0) kchunk = G::BK;
     const int z = (a.K + kchunk - 1) / kchunk > 0 ? (a.K + kchunk - 1) / kchunk : 1;
     dim3 grid((a.M + G::BM - 1) / G::BM, (a.N + G::BN - 1) / G::BN, z);
-    hipLaunchKernelGGL(gemm_kernel<P>, grid, dim3(256), 0, s, a, kchunk);
+    const int pr = sizeof(typename P::T) == 2 ? 0 : 1;
+    const std::string shape = cb_dims(a.M, a.N) + "x" + std::to_string(a.K);
+    {
+        ProfScope ps(s, [&] { return cb_key("gemm", pr, shape); });
+        hipLaunchKernelGGL(gemm_kernel<P>, grid, dim3(256), 0, s, a, kchunk);
+    }
     if (z > 1) {
+        ProfScope ps(s, [&] { return cb_key("gemm_finish", pr, shape); });
         const int64_t total = int64_t(a.M) * a.N;
         hipLaunchKernelGGL(gemm_finish_kernel<P>, dim3(unsigned((total + 255) / 256)), dim3(256), 0,
                            s, a, z);
@@ -196,6 +202,7 @@ hipError_t colsum(int prec_storage, const void* x, int64_t rows, int cols, int64
                   float* partial, hipStream_t s) {
     if (cols <= 0) return hipSuccess;
     int slabs = int(rows < kColSlabs ? (rows > 0 ? rows : 1) : kColSlabs);
+    ProfScope ps(s, [&] { return cb_key("colsum", prec_storage, std::to_string(cols)); });
     dim3 grid((cols + 63) / 64, slabs);
     if (prec_storage == BF16)
         hipLaunchKernelGGL(colsum_kernel<uint16_t>, grid, dim3(256), 0, s,
@@ -221,6 +228,7 @@ __global__ void pack_heads_w_kernel(const float* __restrict__ wl, const float* _
 hipError_t pack_heads_w(const float* wl, const float* wv, int hidden, int A, float* out,
                         hipStream_t s) {
     const int total = (A + 1) * hidden;
+    ProfScope ps(s, [&] { return std::string("pack_heads_w"); });
     hipLaunchKernelGGL(pack_heads_w_kernel, dim3((total + 255) / 256), dim3(256), 0, s, wl, wv,
                        hidden, A, out);
     return hipGetLastError();
@@ -244,6 +252,7 @@ hipError_t pack_dz(int prec, const float* dlogits, const float* dvalue, int64_t 
     const int64_t total = n * (A + 1);
     if (total <= 0) return hipSuccess;
     const dim3 grid(unsigned((total + 255) / 256));
+    ProfScope ps(s, [&] { return cb_key("pack_dz", prec, std::to_string(A)); });
     if (prec == BF16)
         hipLaunchKernelGGL(pack_dz_kernel<uint16_t>, grid, dim3(256), 0, s, dlogits, dvalue, n, A,
                            static_cast<uint16_t*>(out));

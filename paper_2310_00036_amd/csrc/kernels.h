@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "prof.h"
+
 namespace cb {
 
 enum Prec { BF16 = 0, FP32 = 1 };

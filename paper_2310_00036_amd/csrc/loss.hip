@@ -183,6 +183,7 @@ hipError_t ppo_loss(int64_t m, int A, const float* z, const float* v, const int3
                     hipStream_t s) {
     if (m <= 0) return hipSuccess;
     const int nb = int((m + kLossRows - 1) / kLossRows);
+    ProfScope ps(s, [&] { return "ppo_loss/" + cb_dims(int(m), A); });
     hipLaunchKernelGGL(adv_stats_kernel, dim3(1), dim3(256), 0, s, m, adv, rows, stats);
     hipLaunchKernelGGL(ppo_rows_kernel, dim3(nb), dim3(kLossRows), 0, s, m, A, z, v, act, old_logp,
                        adv, ret, rows, norm_adv, clip, vf, ent, dz, dv, stats);
@@ -196,6 +197,7 @@ hipError_t impala_loss(int64_t m, int A, const float* z, const float* v, const i
                        float* dv, float* stats, hipStream_t s) {
     if (m <= 0) return hipSuccess;
     const int nb = int((m + kLossRows - 1) / kLossRows);
+    ProfScope ps(s, [&] { return "impala_loss/" + cb_dims(int(m), A); });
     hipLaunchKernelGGL(impala_rows_kernel, dim3(nb), dim3(kLossRows), 0, s, m, A, z, v, act, vs, pg,
                        pgc, vf, ent, dz, dv);
     hipLaunchKernelGGL(impala_stats_kernel, dim3(1), dim3(kStatThreads), 0, s, m, A, z, v, act, vs, pg,
@@ -217,6 +219,7 @@ __global__ void action_logp_kernel(int64_t m, int A, const float* __restrict__ z
 hipError_t action_logp(int64_t m, int A, const float* z, const int32_t* act, float* logp,
                        hipStream_t s) {
     if (m <= 0) return hipSuccess;
+    ProfScope ps(s, [&] { return "action_logp/" + cb_dims(int(m), A); });
     hipLaunchKernelGGL(action_logp_kernel, dim3(unsigned((m + 255) / 256)), dim3(256), 0, s, m, A, z,
                        act, logp);
     return hipGetLastError();
@@ -245,6 +248,7 @@ __global__ void gumbel_max_kernel(int64_t m, int A, const float* __restrict__ z,
 hipError_t gumbel_max(int64_t m, int A, const float* z, const float* g, int32_t* act, float* logp,
                       hipStream_t s) {
     if (m <= 0) return hipSuccess;
+    ProfScope ps(s, [&] { return "gumbel_max/" + cb_dims(int(m), A); });
     hipLaunchKernelGGL(gumbel_max_kernel, dim3(unsigned((m + 255) / 256)), dim3(256), 0, s, m, A, z, g,
                        act, logp);
     return hipGetLastError();

@@ -102,6 +102,7 @@ hipError_t maxpool_fwd(int prec, int n, int H, int W, int C, const void* x, void
     const int64_t total4 = int64_t(n) * g.OH * g.OW * (C / 4);
     if (total4 <= 0) return hipSuccess;
     const dim3 grid(unsigned((total4 + 255) / 256));
+    ProfScope ps(s, [&] { return cb_key("pool_fwd", prec, std::to_string(C) + "/" + cb_dims(H, W)); });
     if (prec == BF16)
         hipLaunchKernelGGL(maxpool_fwd_kernel<uint16_t>, grid, dim3(256), 0, s,
                            static_cast<const uint16_t*>(x), static_cast<uint16_t*>(y), arg, g, total4);
@@ -117,6 +118,7 @@ hipError_t maxpool_bwd(int prec, int n, int H, int W, int C, const uint8_t* arg,
     const int64_t total4 = int64_t(n) * H * W * (C / 4);
     if (total4 <= 0) return hipSuccess;
     const dim3 grid(unsigned((total4 + 255) / 256));
+    ProfScope ps(s, [&] { return cb_key("pool_bwd", prec, std::to_string(C) + "/" + cb_dims(H, W)); });
     if (prec == BF16)
         hipLaunchKernelGGL(maxpool_bwd_kernel<uint16_t>, grid, dim3(256), 0, s, arg,
                            static_cast<const uint16_t*>(dy), static_cast<uint16_t*>(dx), g, total4);

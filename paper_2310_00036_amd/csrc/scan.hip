@@ -124,6 +124,7 @@ __global__ __launch_bounds__(256) void vtrace_kernel(int T, int E, const float* 
 hipError_t gae(int T, int E, const float* r, const float* v, const uint8_t* d, const float* nv,
                const uint8_t* nd, float gamma, float lam, float* adv, float* ret, hipStream_t s) {
     if (T <= 0 || E <= 0) return hipSuccess;
+    ProfScope ps(s, [&] { return "gae/" + cb_dims(T, E); });
     hipLaunchKernelGGL(gae_kernel, dim3((E + kSE - 1) / kSE), dim3(256), 0, s, T, E, r, v, d, nv, nd,
                        gamma, lam, adv, ret);
     return hipGetLastError();
@@ -134,6 +135,7 @@ hipError_t vtrace(int T, int E, const float* mu, const float* pi, const float* r
                   float rho_bar, float c_bar, float pg_rho_bar, float* vs, float* pg,
                   hipStream_t s) {
     if (T <= 0 || E <= 0) return hipSuccess;
+    ProfScope ps(s, [&] { return "vtrace/" + cb_dims(T, E); });
     hipLaunchKernelGGL(vtrace_kernel, dim3((E + kSE - 1) / kSE), dim3(256), 0, s, T, E, mu, pi, r, v,
                        d, bv, nd, gamma, lam, rho_bar, c_bar, pg_rho_bar, vs, pg);
     return hipGetLastError();

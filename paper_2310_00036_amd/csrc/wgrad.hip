@@ -253,9 +253,17 @@ hipError_t wg_launch(const WgradArgs& a, hipStream_t s) {
     const int parts = r.nchunks < kWgradParts ? r.nchunks : kWgradParts;
     size_t lds = size_t(CIN * r.XP + 3 * COUT * r.GP) * sizeof(typename P::T);
     if (lds < 256 * 8 * sizeof(float)) lds = 256 * 8 * sizeof(float);
-    hipLaunchKernelGGL((wgrad_kernel<P, CIN, COUT, MODE>), dim3(parts), dim3(256), lds, s, a, r);
-    hipLaunchKernelGGL((wgrad_reduce_kernel<CIN, COUT>), dim3((G::PSTRIDE + 63) / 64), dim3(256), 0,
-                       s, a.partial, parts, a.dw, a.db, a.scale);
+    const int pr = sizeof(typename P::T) == 2 ? 0 : 1;
+    const std::string shape = cb_dims(CIN, COUT) + "/" + cb_dims(a.H, a.W);
+    {
+        ProfScope ps(s, [&] { return cb_key("wgrad", pr, shape); });
+        hipLaunchKernelGGL((wgrad_kernel<P, CIN, COUT, MODE>), dim3(parts), dim3(256), lds, s, a, r);
+    }
+    {
+        ProfScope ps(s, [&] { return cb_key("wgrad_reduce", pr, shape); });
+        hipLaunchKernelGGL((wgrad_reduce_kernel<CIN, COUT>), dim3((G::PSTRIDE + 63) / 64), dim3(256), 0,
+                           s, a.partial, parts, a.dw, a.db, a.scale);
+    }
     return hipGetLastError();
 }
 
