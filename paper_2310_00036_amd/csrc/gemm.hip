@@ -44,8 +44,83 @@ CB_DEV void gemm_epilogue(const GemmArgs& a, int m, int n, float v) {
     }
 }
 
+// Loads one BM(or BN) x BK tile of an operand into LDS as tile[row][k] (k contiguous).
+// src(row, k) = base[row*ld + k] (kcontig) or base[k*ld + row]; 16-byte vector loads along
+// the contiguous dimension when `vec` (aligned leading dimension and base), with a scalar
+// fallback for ragged edges.
+template <class P, int ROWS, int BK, int LDK>
+CB_DEV void gemm_load_tile(typename P::T* tile, const void* base, int is_f32, int kcontig, int64_t ld,
+                           int vec, int relu, int row0, int nrows, int k0, int kend, int tid) {
+    using T = typename P::T;
+    const int V = is_f32 ? 4 : (sizeof(T) == 2 ? 8 : 4);     // elements per 16 bytes
+    if (kcontig) {
+        const int nch = ROWS * (BK / V);
+        for (int e = tid; e < nch; e += 256) {
+            const int rr = e / (BK / V), kc = (e % (BK / V)) * V;
+            const int row = row0 + rr, k = k0 + kc;
+            float v[8];
+            if (vec && row < nrows && k + V <= kend) {
+                const int64_t off = int64_t(row) * ld + k;
+                if (is_f32) {
+                    const float4 f = *reinterpret_cast<const float4*>(static_cast<const float*>(base) + off);
+                    v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+                } else if (sizeof(T) == 2) {
+                    const uint4 u = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(base) + off);
+                    const uint32_t* uu = reinterpret_cast<const uint32_t*>(&u);
+                    for (int j = 0; j < 4; ++j) {
+                        v[2 * j] = __uint_as_float(uu[j] << 16);
+                        v[2 * j + 1] = __uint_as_float(uu[j] & 0xffff0000u);
+                    }
+                } else {
+                    const float4 f = *reinterpret_cast<const float4*>(static_cast<const float*>(base) + off);
+                    v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+                }
+            } else {
+                for (int j = 0; j < V; ++j) {
+                    v[j] = 0.f;
+                    if (row < nrows && k + j < kend) {
+                        const int64_t off = int64_t(row) * ld + k + j;
+                        v[j] = is_f32 ? static_cast<const float*>(base)[off] : P::load(static_cast<const T*>(base)[off]);
+                    }
+                }
+            }
+            for (int j = 0; j < V; ++j) tile[rr * LDK + kc + j] = P::store(relu ? relu_f(v[j]) : v[j]);
+        }
+    } else {
+        const int nch = BK * (ROWS / V);
+        for (int e = tid; e < nch; e += 256) {
+            const int kk = e / (ROWS / V), rc = (e % (ROWS / V)) * V;
+            const int row = row0 + rc, k = k0 + kk;
+            float v[8];
+            if (vec && k < kend && row + V <= nrows) {
+                const int64_t off = int64_t(k) * ld + row;
+                if (is_f32 || sizeof(T) == 4) {
+                    const float4 f = *reinterpret_cast<const float4*>(static_cast<const float*>(base) + off);
+                    v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+                } else {
+                    const uint4 u = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(base) + off);
+                    const uint32_t* uu = reinterpret_cast<const uint32_t*>(&u);
+                    for (int j = 0; j < 4; ++j) {
+                        v[2 * j] = __uint_as_float(uu[j] << 16);
+                        v[2 * j + 1] = __uint_as_float(uu[j] & 0xffff0000u);
+                    }
+                }
+            } else {
+                for (int j = 0; j < V; ++j) {
+                    v[j] = 0.f;
+                    if (k < kend && row + j < nrows) {
+                        const int64_t off = int64_t(k) * ld + row + j;
+                        v[j] = is_f32 ? static_cast<const float*>(base)[off] : P::load(static_cast<const T*>(base)[off]);
+                    }
+                }
+            }
+            for (int j = 0; j < V; ++j) tile[(rc + j) * LDK + kk] = P::store(relu ? relu_f(v[j]) : v[j]);
+        }
+    }
+}
+
 template <class P>
-__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a, int kchunk) {
+__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a, int kchunk, int avec, int bvec) {
     using T = typename P::T;
     using G = GemmTile<P>;
     using Frag = typename P::Frag;
@@ -68,25 +143,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a, int kchunk) {
 
     for (int k0 = k_begin; k0 < k_end; k0 += BK) {
         __syncthreads();
-        for (int e = tid; e < BM * BK; e += 256) {
-            int mm, kk;
-            if (a.a_kcontig) { mm = e / BK; kk = e % BK; } else { mm = e % BM; kk = e / BM; }
-            const int m = m0 + mm, k = k0 + kk;
-            float v = 0.f;
-            if (m < a.M && k < k_end)
-                v = ld_elem<P>(a.a, a.a_f32, a.a_kcontig ? int64_t(m) * a.lda + k : int64_t(k) * a.lda + m);
-            As[mm * LDK + kk] = P::store(v);
-        }
-        for (int e = tid; e < BN * BK; e += 256) {
-            int nn, kk;
-            if (a.b_kcontig) { nn = e / BK; kk = e % BK; } else { nn = e % BN; kk = e / BN; }
-            const int n = n0 + nn, k = k0 + kk;
-            float v = 0.f;
-            if (n < a.N && k < k_end)
-                v = ld_elem<P>(a.b, a.b_f32, a.b_kcontig ? int64_t(n) * a.ldb + k : int64_t(k) * a.ldb + n);
-            if (a.b_relu) v = relu_f(v);
-            Bs[nn * LDK + kk] = P::store(v);
-        }
+        gemm_load_tile<P, BM, BK, LDK>(As, a.a, a.a_f32, a.a_kcontig, a.lda, avec, 0, m0, a.M, k0, k_end, tid);
+        gemm_load_tile<P, BN, BK, LDK>(Bs, a.b, a.b_f32, a.b_kcontig, a.ldb, bvec, a.b_relu, n0, a.N, k0, k_end, tid);
         __syncthreads();
 #pragma unroll
         for (int ks = 0; ks < BK; ks += P::KSTEP) {
@@ -128,24 +186,45 @@ __global__ __launch_bounds__(256) void gemm_finish_kernel(GemmArgs a, int splits
     gemm_epilogue<P>(a, int(e % a.M), int(e / a.M), s);
 }
 
-size_t gemm_partial_floats(int M, int N, int splits) {
-    return splits > 1 ? size_t(M) * N * splits : 0;
+// Split-K so the grid covers the chip (about two workgroups per CU), never below 256 k per
+// split and never above the caller's partial-buffer allowance `max_splits`.
+static int auto_splits(int M, int N, int K, int max_splits, int bm, int bn) {
+    const int tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+    int s = (512 + tiles - 1) / tiles;
+    if (s > max_splits) s = max_splits;
+    while (s > 1 && K / s < 256) --s;
+    return s < 1 ? 1 : s;
+}
+
+static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+constexpr int kMaxSplits = 8;
+
+size_t gemm_partial_floats(int M, int N, int K) {
+    const int sp = auto_splits(M, N, K, kMaxSplits, 64, 64);
+    return sp > 1 ? size_t(M) * N * sp : 0;
 }
 
 template <class P>
-static hipError_t gemm_launch(const GemmArgs& a, int splits, hipStream_t s) {
+static hipError_t gemm_launch(const GemmArgs& a, hipStream_t s) {
     using G = GemmTile<P>;
     if (a.M <= 0 || a.N <= 0) return hipSuccess;
+    int splits = a.partial ? auto_splits(a.M, a.N, a.K, kMaxSplits, G::BM, G::BN) : 1;
+    while (splits > 1 && size_t(a.M) * a.N * splits > a.partial_floats) --splits;
     int kchunk = (a.K + splits - 1) / splits;
     kchunk = (kchunk + G::BK - 1) / G::BK * G::BK;
     if (kchunk <= 0) kchunk = G::BK;
     const int z = (a.K + kchunk - 1) / kchunk > 0 ? (a.K + kchunk - 1) / kchunk : 1;
+    const int va = (a.a_f32 || sizeof(typename P::T) == 4) ? 4 : 8;
+    const int vb = (a.b_f32 || sizeof(typename P::T) == 4) ? 4 : 8;
+    const int avec = aligned16(a.a) && a.lda % va == 0;
+    const int bvec = aligned16(a.b) && a.ldb % vb == 0;
     dim3 grid((a.M + G::BM - 1) / G::BM, (a.N + G::BN - 1) / G::BN, z);
     const int pr = sizeof(typename P::T) == 2 ? 0 : 1;
     const std::string shape = cb_dims(a.M, a.N) + "x" + std::to_string(a.K);
     {
         ProfScope ps(s, [&] { return cb_key("gemm", pr, shape); });
-        hipLaunchKernelGGL(gemm_kernel<P>, grid, dim3(256), 0, s, a, kchunk);
+        hipLaunchKernelGGL(gemm_kernel<P>, grid, dim3(256), 0, s, a, kchunk, avec, bvec);
     }
     if (z > 1) {
         ProfScope ps(s, [&] { return cb_key("gemm_finish", pr, shape); });
@@ -156,9 +235,8 @@ static hipError_t gemm_launch(const GemmArgs& a, int splits, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t gemm(int prec, const GemmArgs& a, int splits, hipStream_t s) {
-    if (splits < 1) splits = 1;
-    return prec == BF16 ? gemm_launch<PrecBF16>(a, splits, s) : gemm_launch<PrecF32>(a, splits, s);
+hipError_t gemm(int prec, const GemmArgs& a, hipStream_t s) {
+    return prec == BF16 ? gemm_launch<PrecBF16>(a, s) : gemm_launch<PrecF32>(a, s);
 }
 
 // ------------------------------------------------------------------ column sums

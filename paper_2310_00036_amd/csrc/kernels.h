@@ -67,10 +67,13 @@ struct GemmArgs {
     void* out1; int64_t ld1; int out1_f32;                  // rows m < msplit
     void* out2; int64_t ld2; int out2_f32;                  // rows m >= msplit (index m - msplit)
     int msplit;
-    float* partial;                                         // split-K workspace
+    float* partial;                                         // split-K workspace (or NULL)
+    size_t partial_floats;                                  // its capacity
 };
-size_t gemm_partial_floats(int M, int N, int splits);
-hipError_t gemm(int prec, const GemmArgs& a, int splits, hipStream_t s);
+// Floats of split-K workspace a GEMM of this shape uses at most.
+size_t gemm_partial_floats(int M, int N, int K);
+// The launcher splits K so the grid covers the chip, within a.partial_floats.
+hipError_t gemm(int prec, const GemmArgs& a, hipStream_t s);
 
 // ---- small helpers
 hipError_t colsum(int prec_storage, const void* x, int64_t rows, int cols, int64_t ld,

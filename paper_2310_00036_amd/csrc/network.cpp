@@ -60,18 +60,6 @@ ParamOffsets param_offsets(const impala_net_t& net) {
     return o;
 }
 
-static int dense_wgrad_splits(int M, int N, int64_t K) {
-    const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
-    int s = std::max(1, std::min(8, 1024 / std::max(1, tiles)));
-    while (s > 1 && K / s < 256) --s;
-    return s;
-}
-
-static int heads_wgrad_splits(int64_t K) {
-    int s = int(std::min<int64_t>(32, std::max<int64_t>(1, K / 256)));
-    return s;
-}
-
 NetPlan make_plan(const impala_net_t& net, int prec, int64_t cap, int training) {
     NetPlan p;
     std::memset(&p, 0, sizeof(p));
@@ -105,20 +93,30 @@ NetPlan make_plan(const impala_net_t& net, int prec, int64_t cap, int training) 
     }
     p.h = take(size_t(cap) * p.hidden * p.es);
     p.whp = take(size_t(p.A + 1) * p.hidden * sizeof(float));
+    // split-K / column-sum / weight-gradient partials, shared by the launches in turn. The
+    // GEMM launcher never splits beyond this capacity, so the sizing only affects speed.
+    size_t sc = 0;
+    for (int64_t nn = cap; nn >= 1; nn = nn > 64 ? nn / 2 : 0) {
+        sc = std::max(sc, gemm_partial_floats(p.hidden, int(nn), p.flat));
+        sc = std::max(sc, gemm_partial_floats(p.A + 1, int(nn), p.hidden));
+        if (training) {
+            sc = std::max(sc, gemm_partial_floats(p.A + 1, p.hidden, int(nn)));
+            sc = std::max(sc, gemm_partial_floats(p.hidden, int(nn), p.A + 1));
+            sc = std::max(sc, gemm_partial_floats(p.hidden, p.flat, int(nn)));
+            sc = std::max(sc, gemm_partial_floats(p.flat, int(nn), p.hidden));
+        }
+    }
     if (training) {
         for (int k = 0; k < 3; ++k) p.g[k] = take(size_t(cap * maxact) * p.es);
         p.dz = take(size_t(cap) * (p.A + 1) * p.es);
-        size_t sc = 0;
         for (int s = 0; s < 3; ++s) {
             sc = std::max(sc, wgrad_partial_floats(prec, p.C[s], p.C[s + 1], p.H[s], p.W[s]));
             sc = std::max(sc, wgrad_partial_floats(prec, p.C[s + 1], p.C[s + 1], p.H[s + 1], p.W[s + 1]));
         }
-        sc = std::max(sc, gemm_partial_floats(p.hidden, p.flat, dense_wgrad_splits(p.hidden, p.flat, cap)));
-        sc = std::max(sc, gemm_partial_floats(p.A + 1, p.hidden, heads_wgrad_splits(cap)));
         sc = std::max(sc, colsum_partial_floats(std::max(p.hidden, p.A + 1)));
-        p.scratch_bytes = sc * sizeof(float);
-        p.scratch = take(p.scratch_bytes);
     }
+    p.scratch_bytes = sc * sizeof(float);
+    p.scratch = take(p.scratch_bytes);
     p.total = off;
     return p;
 }
@@ -168,7 +166,8 @@ hipError_t run_forward(const NetPlan& p, const float* params, const uint8_t* obs
     d.M = p.hidden; d.N = int(n); d.K = p.flat;
     d.alpha = 1.f; d.bias1 = params + po.dense_b; d.relu = 1;
     d.out1 = ws + p.h; d.ld1 = p.hidden; d.out1_f32 = p.prec == FP32; d.msplit = p.hidden;
-    CB_TRY(gemm(p.prec, d, 1, s));
+    d.partial = reinterpret_cast<float*>(ws + p.scratch); d.partial_floats = p.scratch_bytes / sizeof(float);
+    CB_TRY(gemm(p.prec, d, s));
     // heads: logits[i][a] = bl[a] + sum_j h[i][j] Wl[j][a]; value[i] = bv + sum_j h[i][j] Wv[j]
     float* whp = reinterpret_cast<float*>(ws + p.whp);
     CB_TRY(pack_heads_w(params + po.logits_w, params + po.value_w, p.hidden, p.A, whp, s));
@@ -179,7 +178,8 @@ hipError_t run_forward(const NetPlan& p, const float* params, const uint8_t* obs
     hd.bias1 = params + po.logits_b; hd.bias2 = params + po.value_b;
     hd.out1 = logits; hd.ld1 = p.A; hd.out1_f32 = 1;
     hd.out2 = value; hd.ld2 = 1; hd.out2_f32 = 1; hd.msplit = p.A;
-    CB_TRY(gemm(p.prec, hd, 1, s));
+    hd.partial = reinterpret_cast<float*>(ws + p.scratch); hd.partial_floats = p.scratch_bytes / sizeof(float);
+    CB_TRY(gemm(p.prec, hd, s));
     return hipSuccess;
 }
 
@@ -202,8 +202,8 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
     hw.M = A + 1; hw.N = p.hidden; hw.K = int(n); hw.alpha = 1.f;
     hw.out1 = grads + po.logits_w; hw.ld1 = A; hw.out1_f32 = 1;
     hw.out2 = grads + po.value_w; hw.ld2 = 1; hw.out2_f32 = 1; hw.msplit = A;
-    hw.partial = scratch;
-    CB_TRY(gemm(p.prec, hw, heads_wgrad_splits(n), s));
+    hw.partial = scratch; hw.partial_floats = p.scratch_bytes / sizeof(float);
+    CB_TRY(gemm(p.prec, hw, s));
     CB_TRY(colsum(p.prec, dz, n, A, A + 1, grads + po.logits_b, scratch, s));
     CB_TRY(colsum(p.prec, dz + size_t(A) * es, n, 1, A + 1, grads + po.value_b, scratch, s));
     // dh = (dz Wh^T) * (h > 0)
@@ -215,15 +215,16 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
     hg.M = p.hidden; hg.N = int(n); hg.K = A + 1; hg.alpha = 1.f;
     hg.mask = ws + p.h; hg.ldmask = p.hidden;
     hg.out1 = G[0]; hg.ld1 = p.hidden; hg.out1_f32 = st_f32; hg.msplit = p.hidden;
-    CB_TRY(gemm(p.prec, hg, 1, s));
+    hg.partial = scratch; hg.partial_floats = p.scratch_bytes / sizeof(float);
+    CB_TRY(gemm(p.prec, hg, s));
     // dense weight gradient: dWd[k][j] = sum_i relu(x)[i][k] dh[i][j]; bias: column sums of dh
     GemmArgs dw{};
     dw.a = G[0]; dw.a_f32 = st_f32; dw.a_kcontig = 0; dw.lda = p.hidden;
     dw.b = ws + p.x[2][2]; dw.b_f32 = st_f32; dw.b_kcontig = 0; dw.ldb = p.flat; dw.b_relu = 1;
     dw.M = p.hidden; dw.N = p.flat; dw.K = int(n); dw.alpha = 1.f;
     dw.out1 = grads + po.dense_w; dw.ld1 = p.hidden; dw.out1_f32 = 1; dw.msplit = p.hidden;
-    dw.partial = scratch;
-    CB_TRY(gemm(p.prec, dw, dense_wgrad_splits(p.hidden, p.flat, n), s));
+    dw.partial = scratch; dw.partial_floats = p.scratch_bytes / sizeof(float);
+    CB_TRY(gemm(p.prec, dw, s));
     CB_TRY(colsum(p.prec, G[0], n, p.hidden, p.hidden, grads + po.dense_b, scratch, s));
     // dense input gradient: dx[i][k] = (sum_j Wd[k][j] dh[i][j]) * (x[i][k] > 0)
     GemmArgs dg{};
@@ -232,7 +233,8 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
     dg.M = p.flat; dg.N = int(n); dg.K = p.hidden; dg.alpha = 1.f;
     dg.mask = ws + p.x[2][2]; dg.ldmask = p.flat;
     dg.out1 = G[1]; dg.ld1 = p.flat; dg.out1_f32 = st_f32; dg.msplit = p.flat;
-    CB_TRY(gemm(p.prec, dg, 1, s));
+    dg.partial = scratch; dg.partial_floats = p.scratch_bytes / sizeof(float);
+    CB_TRY(gemm(p.prec, dg, s));
 
     int gy = 1;
     auto others = [](int k, int& a, int& b) { a = (k + 1) % 3; b = (k + 2) % 3; };

@@ -32,9 +32,19 @@ struct WgGeom {
 
 struct WgRun {
     int TH, nbands, nchunks, PITCH, KLEN, XP, GP;
+    int nx, ng;   // load items per chunk: (TH+2)*W*NCI input items, TH*W*NCO gradient items
 };
 
 static inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
+
+constexpr int kWgItems = 4;   // load items per thread per operand (register prefetch depth)
+
+// One 16-byte (8 channels; 4 for uint8 frames) load item kept in registers between the
+// global load and the LDS store, so the next chunk's loads overlap this chunk's MFMAs.
+template <class P, int VEC>
+struct WgItem {
+    uint4 raw[sizeof(typename P::T) == 4 && VEC == 8 ? 2 : 1];
+};
 
 template <class P, int CIN, int COUT, int MODE>
 __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, WgRun g_) {
@@ -42,8 +52,9 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, WgRun g_) {
     using Frag = typename P::Frag;
     using G = WgGeom<P, CIN, COUT>;
     constexpr int KPL = P::KPL, KSTEP = P::KSTEP;
-    constexpr int VEC = MODE == IN_U8 ? 4 : 8;        // channels per global load
+    constexpr int VEC = MODE == IN_U8 ? 4 : 8;        // channels per input load item
     constexpr int NCI = CIN / VEC, NCO = COUT / 8;
+    constexpr bool BF = sizeof(T) == 2;
 
     extern __shared__ __align__(16) unsigned char smem[];
     T* xT = reinterpret_cast<T*>(smem);               // [CIN][XP]
@@ -53,6 +64,14 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, WgRun g_) {
     const int g = lane >> 4, r16 = lane & 15;
     const int H = a.H, W = a.W, TH = g_.TH, PITCH = g_.PITCH, KLEN = g_.KLEN;
     const int XP = g_.XP, GP = g_.GP;
+
+    // Zero both tiles once: cells outside the image (halo columns, rows past the image,
+    // k padding) are never written again, so they stay zero for every chunk.
+    {
+        const int words = (CIN * XP + 3 * COUT * GP) * int(sizeof(T)) / 4;
+        uint32_t* z = reinterpret_cast<uint32_t*>(smem);
+        for (int i = tid; i < words; i += 256) z[i] = 0u;
+    }
 
     // Per-tile fragment bases (fixed for the whole kernel).
     int a_off[G::TPW], b_off[G::TPW];
@@ -75,80 +94,109 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, WgRun g_) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) bsum[j] = 0.f;
 
+    WgItem<P, VEC> xr[kWgItems];
+    WgItem<P, 8> gr[kWgItems];
     const T* dy = static_cast<const T*>(a.dy);
-    for (int ch = blockIdx.x; ch < g_.nchunks; ch += gridDim.x) {
-        const int band = ch % g_.nbands, frame = ch / g_.nbands;
-        const int h0 = band * TH;
-        __syncthreads();   // previous chunk's MFMA reads are done
 
-        // ---- input window, channel-major: xT[ci][r*PITCH + c'] = x[h0 + r - 1][c' - 1][ci]
-        for (int e = tid; e < NCI * XP; e += 256) {
-            const int cg = e % NCI, kk = e / NCI;
-            const int r = kk / PITCH, cc = kk % PITCH;
-            const int h = h0 + r - 1, w = cc - 1;
-            const bool in = r < TH + 2 && h >= 0 && h < H && w >= 0 && w < W;
-            float v[VEC];
-            if constexpr (MODE == IN_U8) {
-                uint32_t u = 0;
-                if (in) {
-                    const int64_t row = a.row_idx ? a.row_idx[frame] : frame;
-                    u = *reinterpret_cast<const uint32_t*>(static_cast<const uint8_t*>(a.x) +
-                                                           ((row * H + h) * W + w) * 4);
-                }
+    // Global -> registers for chunk ch (zeros outside the image).
+    auto load = [&](int ch) {
+        const int band = ch % g_.nbands, frame = ch / g_.nbands, h0 = band * TH;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) v[j] = float((u >> (8 * j)) & 0xff);
-            } else {
-                const T* src = static_cast<const T*>(a.x) + ((int64_t(frame) * H + h) * W + w) * CIN + cg * VEC;
-                if constexpr (sizeof(T) == 2) {
-                    uint4 u = in ? *reinterpret_cast<const uint4*>(src) : make_uint4(0, 0, 0, 0);
-                    const uint32_t* uu = reinterpret_cast<const uint32_t*>(&u);
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        v[2 * j] = __uint_as_float(uu[j] << 16);
-                        v[2 * j + 1] = __uint_as_float(uu[j] & 0xffff0000u);
+        for (int i = 0; i < kWgItems; ++i) {
+            const int idx = tid + 256 * i;
+            xr[i].raw[0] = make_uint4(0, 0, 0, 0);
+            if constexpr (sizeof(xr[i].raw) > 16) xr[i].raw[1] = make_uint4(0, 0, 0, 0);
+            if (idx < g_.nx) {
+                const int cg = idx % NCI, pos = idx / NCI;
+                const int r = pos / W, w = pos % W, h = h0 + r - 1;
+                if (h >= 0 && h < H) {
+                    if constexpr (MODE == IN_U8) {
+                        const int64_t row = a.row_idx ? a.row_idx[frame] : frame;
+                        xr[i].raw[0].x = *reinterpret_cast<const uint32_t*>(
+                            static_cast<const uint8_t*>(a.x) + ((row * H + h) * W + w) * 4);
+                    } else {
+                        const uint4* src = reinterpret_cast<const uint4*>(
+                            static_cast<const T*>(a.x) + ((int64_t(frame) * H + h) * W + w) * CIN + cg * VEC);
+                        xr[i].raw[0] = src[0];
+                        if constexpr (sizeof(xr[i].raw) > 16) xr[i].raw[1] = src[1];
                     }
-                } else {
-#pragma unroll
-                    for (int j = 0; j < VEC; ++j) v[j] = in ? src[j] : 0.f;
-                }
-                if (MODE == IN_RELU) {
-#pragma unroll
-                    for (int j = 0; j < VEC; ++j) v[j] = relu_f(v[j]);
                 }
             }
-#pragma unroll
-            for (int j = 0; j < VEC; ++j) xT[(cg * VEC + j) * XP + kk] = P::store(v[j]);
+            gr[i].raw[0] = make_uint4(0, 0, 0, 0);
+            if constexpr (sizeof(gr[i].raw) > 16) gr[i].raw[1] = make_uint4(0, 0, 0, 0);
+            if (idx < g_.ng) {
+                const int cg = idx % NCO, pos = idx / NCO;
+                const int r = pos / W, w = pos % W;
+                if (h0 + r < H) {
+                    const uint4* src = reinterpret_cast<const uint4*>(
+                        dy + ((int64_t(frame) * H + h0 + r) * W + w) * COUT + cg * 8);
+                    gr[i].raw[0] = src[0];
+                    if constexpr (sizeof(gr[i].raw) > 16) gr[i].raw[1] = src[1];
+                }
+            }
         }
+    };
 
-        // ---- output gradient, three column-shifted channel-major copies
-        for (int e = tid; e < 3 * GP * NCO; e += 256) {
-            const int cg = e % NCO, kk = (e / NCO) % GP, kx = e / (NCO * GP);
-            const int r = kk / PITCH, w = kk % PITCH - kx;
-            const bool in = kk < KLEN && r < TH && h0 + r < H && w >= 0 && w < W;
-            float v[8];
-            const T* src = dy + ((int64_t(frame) * H + h0 + r) * W + w) * COUT + cg * 8;
-            if constexpr (sizeof(T) == 2) {
-                uint4 u = in ? *reinterpret_cast<const uint4*>(src) : make_uint4(0, 0, 0, 0);
-                const uint32_t* uu = reinterpret_cast<const uint32_t*>(&u);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    v[2 * j] = __uint_as_float(uu[j] << 16);
-                    v[2 * j + 1] = __uint_as_float(uu[j] & 0xffff0000u);
-                }
-            } else {
-#pragma unroll
-                for (int j = 0; j < 8; ++j) v[j] = in ? src[j] : 0.f;
+    auto unpack = [&](const uint4* raw, int n, float* v) {
+        if constexpr (BF) {
+            const uint32_t* u = reinterpret_cast<const uint32_t*>(raw);
+            for (int j = 0; j < n / 2; ++j) {
+                v[2 * j] = __uint_as_float(u[j] << 16);
+                v[2 * j + 1] = __uint_as_float(u[j] & 0xffff0000u);
             }
-            if (kx == 0) {
+        } else {
+            const float* f = reinterpret_cast<const float*>(raw);
+            for (int j = 0; j < n; ++j) v[j] = f[j];
+        }
+    };
+
+    // Registers -> LDS: input channel-major, gradient in three column-shifted copies.
+    auto store = [&]() {
+#pragma unroll
+        for (int i = 0; i < kWgItems; ++i) {
+            const int idx = tid + 256 * i;
+            if (idx < g_.nx) {
+                const int cg = idx % NCI, pos = idx / NCI;
+                const int r = pos / W, w = pos % W;
+                float v[VEC];
+                if constexpr (MODE == IN_U8) {
+                    const uint32_t u = xr[i].raw[0].x;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) v[j] = float((u >> (8 * j)) & 0xff);
+                } else {
+                    unpack(xr[i].raw, VEC, v);
+                    if (MODE == IN_RELU) {
+#pragma unroll
+                        for (int j = 0; j < VEC; ++j) v[j] = relu_f(v[j]);
+                    }
+                }
+                T* dst = xT + (cg * VEC) * XP + r * PITCH + w + 1;
+#pragma unroll
+                for (int j = 0; j < VEC; ++j) dst[j * XP] = P::store(v[j]);
+            }
+            if (idx < g_.ng) {
+                const int cg = idx % NCO, pos = idx / NCO;
+                const int r = pos / W, w = pos % W;
+                float v[8];
+                unpack(gr[i].raw, 8, v);
 #pragma unroll
                 for (int j = 0; j < 8; ++j) bsum[j] += v[j];
-            }
+                T* dst = gS + (cg * 8) * GP + r * PITCH + w;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) gS[(kx * COUT + cg * 8 + j) * GP + kk] = P::store(v[j]);
+                for (int kx = 0; kx < 3; ++kx)
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) dst[(kx * COUT + j) * GP + kx] = P::store(v[j]);
+            }
         }
-        __syncthreads();
+    };
 
-        // ---- MFMA over the band's pixels
+    int ch = blockIdx.x;
+    if (ch < g_.nchunks) load(ch);
+    for (; ch < g_.nchunks; ch += gridDim.x) {
+        __syncthreads();   // zero fill / previous chunk's MFMA reads are done
+        store();
+        __syncthreads();
+        if (ch + int(gridDim.x) < g_.nchunks) load(ch + gridDim.x);   // overlaps the MFMAs
         for (int k0 = 0; k0 < KLEN; k0 += KSTEP) {
 #pragma unroll
             for (int j = 0; j < G::TPW; ++j) {
@@ -190,22 +238,25 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, WgRun g_) {
 }
 
 // Sum the partials of all workgroups in a fixed order and scatter to HWIO / bias.
+// Block: 64 consecutive partial entries x 16 interleaved slices of the partials.
 template <int CIN, int COUT>
-__global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restrict__ partial,
-                                                           int nparts, float* dw, float* db,
-                                                           float scale) {
+__global__ __launch_bounds__(1024) void wgrad_reduce_kernel(const float* __restrict__ partial,
+                                                            int nparts, float* dw, float* db,
+                                                            float scale) {
     using G = WgGeom<PrecF32, CIN, COUT>;
-    __shared__ float sh[4][64];
+    __shared__ float sh[16][64];
     const int e = blockIdx.x * 64 + (threadIdx.x & 63);
     const int sp = threadIdx.x >> 6;
     float s = 0.f;
     if (e < G::PSTRIDE) {
-        for (int p = sp; p < nparts; p += 4) s += partial[int64_t(p) * G::PSTRIDE + e];
+        for (int p = sp; p < nparts; p += 16) s += partial[int64_t(p) * G::PSTRIDE + e];
     }
     sh[sp][threadIdx.x & 63] = s;
     __syncthreads();
     if (sp == 0 && e < G::PSTRIDE) {
-        const float tot = ((sh[0][threadIdx.x] + sh[1][threadIdx.x]) + sh[2][threadIdx.x]) + sh[3][threadIdx.x];
+        float tot = 0.f;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) tot += sh[k][threadIdx.x];
         constexpr int WSZ = 3 * COUT * G::NTN * 16;
         if (e < WSZ) {
             const int col = e % (G::NTN * 16), co = (e / (G::NTN * 16)) % COUT, kx = e / (COUT * G::NTN * 16);
@@ -221,37 +272,55 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restri
 
 namespace {
 
-constexpr int kWgradParts = 256;
-constexpr size_t kWgLds = 64 * 1024;
+constexpr int kWgradParts = 1024;        // upper bound on workgroups (and partials)
+constexpr size_t kWgLds = 40 * 1024;      // aim for four workgroups per CU
 
 template <class P, int CIN, int COUT>
+size_t wg_lds(const WgRun& r) {
+    return size_t(CIN * r.XP + 3 * COUT * r.GP) * sizeof(typename P::T);
+}
+
+template <class P, int CIN, int COUT, int MODE>
 WgRun wg_plan(int n, int H, int W) {
+    constexpr int VEC = MODE == IN_U8 ? 4 : 8;
+    constexpr int NCI = CIN / VEC, NCO = COUT / 8;
     WgRun r;
-    const int es = sizeof(typename P::T);
     r.PITCH = round_up(W + 2, 8);
-    int TH = H;
-    for (;;) {
+    for (int TH = H; TH >= 1; --TH) {
         r.TH = TH;
         r.KLEN = round_up(TH * r.PITCH, P::KSTEP);
         r.XP = round_up(r.KLEN + 2 * r.PITCH, 16) + 8;
         r.GP = round_up(r.KLEN, 16) + 8;
-        const size_t lds = size_t(CIN * r.XP + 3 * COUT * r.GP) * es;
-        if ((lds <= kWgLds && TH * r.PITCH <= 512) || TH == 1) break;
-        const int nb = (H + TH - 1) / TH + 1;
-        const int next = (H + nb - 1) / nb;
-        TH = next < TH ? next : TH - 1;
+        r.nx = (TH + 2) * W * NCI;
+        r.ng = TH * W * NCO;
+        const bool fits = r.nx <= 256 * kWgItems && r.ng <= 256 * kWgItems;
+        if (fits && (wg_lds<P, CIN, COUT>(r) <= kWgLds || TH == 1)) break;
     }
     r.nbands = (H + r.TH - 1) / r.TH;
     r.nchunks = n * r.nbands;
     return r;
 }
 
+// Workgroups (= partials): up to 1024 (four per CU), fewer when the partials would exceed
+// ~40 MB (the fixed-order reduction reads them all once).
+static int wg_parts_cap(int pstride) {
+    int cap = int((40u << 20) / (sizeof(float) * size_t(pstride)));
+    return cap < 256 ? 256 : (cap > kWgradParts ? kWgradParts : cap);
+}
+
+template <int CIN, int COUT>
+int wg_parts(int nchunks) {
+    const int cap = wg_parts_cap(WgGeom<PrecF32, CIN, COUT>::PSTRIDE);
+    return nchunks < cap ? nchunks : cap;
+}
+
 template <class P, int CIN, int COUT, int MODE>
 hipError_t wg_launch(const WgradArgs& a, hipStream_t s) {
     using G = WgGeom<P, CIN, COUT>;
-    const WgRun r = wg_plan<P, CIN, COUT>(a.n, a.H, a.W);
-    const int parts = r.nchunks < kWgradParts ? r.nchunks : kWgradParts;
-    size_t lds = size_t(CIN * r.XP + 3 * COUT * r.GP) * sizeof(typename P::T);
+    const WgRun r = wg_plan<P, CIN, COUT, MODE>(a.n, a.H, a.W);
+    if (r.nx > 256 * kWgItems || r.ng > 256 * kWgItems) return hipErrorInvalidValue;
+    const int parts = wg_parts<CIN, COUT>(r.nchunks);
+    size_t lds = wg_lds<P, CIN, COUT>(r);
     if (lds < 256 * 8 * sizeof(float)) lds = 256 * 8 * sizeof(float);
     const int pr = sizeof(typename P::T) == 2 ? 0 : 1;
     const std::string shape = cb_dims(CIN, COUT) + "/" + cb_dims(a.H, a.W);
@@ -261,7 +330,7 @@ hipError_t wg_launch(const WgradArgs& a, hipStream_t s) {
     }
     {
         ProfScope ps(s, [&] { return cb_key("wgrad_reduce", pr, shape); });
-        hipLaunchKernelGGL((wgrad_reduce_kernel<CIN, COUT>), dim3((G::PSTRIDE + 63) / 64), dim3(256), 0,
+        hipLaunchKernelGGL((wgrad_reduce_kernel<CIN, COUT>), dim3((G::PSTRIDE + 63) / 64), dim3(1024), 0,
                            s, a.partial, parts, a.dw, a.db, a.scale);
     }
     return hipGetLastError();
@@ -294,7 +363,8 @@ bool wgrad_supported(int cin, int cout, int mode) {
 size_t wgrad_partial_floats(int prec, int cin, int cout, int H, int W) {
     (void)prec; (void)H; (void)W;
     const size_t ncol = size_t(3 * cin + 15) / 16 * 16;
-    return size_t(kWgradParts) * (3 * size_t(cout) * ncol + cout);
+    const size_t pst = 3 * size_t(cout) * ncol + cout;
+    return size_t(wg_parts_cap(int(pst))) * pst;
 }
 
 hipError_t conv3x3_wgrad(int prec, int cin, int cout, int mode, const WgradArgs& a,
