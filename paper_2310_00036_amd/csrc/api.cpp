@@ -4,7 +4,9 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
+#include <vector>
 
 #include "../../include/cleanba_layers.h"
 #include "../../include/cleanba_learner.h"
@@ -114,6 +116,25 @@ size_t lds_limit() {
         dev_cached = dev;
     }
     return bytes;
+}
+
+int resident_blocks(const void* fn, int threads, size_t lds) {
+    struct Entry { int dev; const void* fn; int threads; size_t lds; int blocks; };
+    static std::mutex mu;
+    static std::vector<Entry> cache;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+    std::lock_guard<std::mutex> lock(mu);
+    for (const Entry& e : cache)
+        if (e.dev == dev && e.fn == fn && e.threads == threads && e.lds == lds) return e.blocks;
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, threads, lds) != hipSuccess || per_cu < 1)
+        per_cu = 1;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+        cus = 1;
+    (void)hipGetLastError();   // a failed query must not be reported by the next launch
+    cache.push_back(Entry{dev, fn, threads, lds, per_cu * cus});
+    return per_cu * cus;
 }
 
 hipError_t fill_zero(float* p, int64_t n, hipStream_t s) {

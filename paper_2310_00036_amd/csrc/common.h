@@ -23,13 +23,8 @@ typedef float cb_f32x4 __attribute__((ext_vector_type(4)));
 
 CB_DEV float bf2f(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
 
-// float -> bf16, round to nearest even; NaN stays NaN.
-CB_DEV uint16_t f2bf(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return uint16_t((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return uint16_t(u >> 16);
-}
+// float -> bf16, round to nearest even (NaN stays NaN): gfx950 converts natively.
+CB_DEV uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f)); }
 
 CB_DEV uint32_t pack2bf(float a, float b) { return uint32_t(f2bf(a)) | (uint32_t(f2bf(b)) << 16); }
 

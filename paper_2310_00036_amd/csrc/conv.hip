@@ -15,6 +15,7 @@
 #include "kernels.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace cb {
 
@@ -29,14 +30,22 @@ struct ConvGeom {
     static constexpr int CP = sizeof(T) == 2 ? (CIN >= 8 ? CIN + 8 : CIN) : CIN + 1;
 };
 
+constexpr int kConvItems = 6;   // 16-byte input load items per thread (register prefetch)
+
 template <class P, int CIN, int COUT, int MODE, int FLIP>
 __global__ __launch_bounds__(256) void conv3x3_kernel(ConvArgs a, int TH, int FR, int nbands,
-                                                      int cout_total) {
+                                                      int ntiles, int cout_total) {
     using T = typename P::T;
     using G = ConvGeom<P, CIN>;
     using Frag = typename P::Frag;
     constexpr int KPL = P::KPL, KSTEP = P::KSTEP, KSTEPS = G::KSTEPS, KP = G::KP;
     constexpr int KPITCH = G::KPITCH, CP = G::CP, MT = COUT / 16;
+    constexpr bool BF = sizeof(T) == 2;
+    // input load items: one pixel of uint8 frames, else 16 bytes of channels
+    constexpr int VEC = MODE == IN_U8 ? 4 : (BF ? 8 : 4);
+    constexpr int NCH = CIN / VEC;
+    // keep the weight fragments in registers when they are few
+    constexpr bool HOIST = BF && MT * KSTEPS <= 10;
     static_assert(MODE != IN_U8 || CIN == 4, "uint8 frames carry 4 stacked channels");
     static_assert(COUT % 16 == 0, "output channels in 16-wide MFMA tiles");
 
@@ -46,13 +55,12 @@ __global__ __launch_bounds__(256) void conv3x3_kernel(ConvArgs a, int TH, int FR
     T* xs = wl + WL_ELEMS;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int band = blockIdx.x % nbands, fg = blockIdx.x / nbands;
     const int og = blockIdx.y * COUT;                  // first output channel of this group
     const int H = a.H, W = a.W;
-    const int h0 = band * TH, f0 = fg * FR;
     const int TW = W + 2, TR = TH + 2;
+    const int nitems = FR * TR * W * NCH;
 
-    // ---- weights -> LDS: wl[o][tap*CIN + i], zero in the k padding
+    // ---- weights -> LDS once: wl[o][tap*CIN + i], zero in the k padding
     if (FLIP) {
         // forward HWIO [9][cout_total(=our out channels)][CIN(=forward out)]; rotate taps.
         for (int e = tid; e < 9 * COUT * CIN; e += 256) {
@@ -71,139 +79,471 @@ __global__ __launch_bounds__(256) void conv3x3_kernel(ConvArgs a, int TH, int FR
         for (int e = tid; e < COUT * PADK; e += 256)
             wl[(e / PADK) * KPITCH + G::K + e % PADK] = P::store(0.f);
     }
+    // The two padding columns of the window (image columns -1 and W) are zero for every
+    // tile: write them once.
+    for (int e = tid; e < FR * TR * 2 * CP; e += 256) {
+        const int c = e % CP, side = (e / CP) % 2, rowi = e / (2 * CP);
+        xs[(rowi * TW + (side ? W + 1 : 0)) * CP + c] = P::store(0.f);
+    }
 
-    // ---- zero-padded input window -> LDS: xs[f][r][c][i]
-    const int npix = FR * TR * TW;
-    if constexpr (MODE == IN_U8) {
-        const uint8_t* obs = static_cast<const uint8_t*>(a.x);
-        for (int p = tid; p < npix; p += 256) {
-            const int col = p % TW, rr = (p / TW) % TR, f = p / (TW * TR);
-            const int h = h0 + rr - 1, w = col - 1, frame = f0 + f;
-            uint32_t v = 0;
-            if (h >= 0 && h < H && w >= 0 && w < W && frame < a.n) {
-                const int64_t row = a.row_idx ? a.row_idx[frame] : frame;
-                v = *reinterpret_cast<const uint32_t*>(obs + ((row * H + h) * W + w) * 4);
-            }
-            T* dst = xs + p * CP;
-            if constexpr (sizeof(T) == 2) {
-                const uint32_t lo = pack2bf(float(v & 0xff), float((v >> 8) & 0xff));
-                const uint32_t hi = pack2bf(float((v >> 16) & 0xff), float(v >> 24));
-                *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
-            } else {
-                dst[0] = float(v & 0xff); dst[1] = float((v >> 8) & 0xff);
-                dst[2] = float((v >> 16) & 0xff); dst[3] = float(v >> 24);
-            }
-        }
-    } else {
-        constexpr int VEC = sizeof(T) == 2 ? 8 : 4;   // channels per 16-byte chunk
-        constexpr int NCH = CIN / VEC;
-        const T* x = static_cast<const T*>(a.x);
-        for (int e = tid; e < npix * NCH; e += 256) {
-            const int ch = e % NCH, p = e / NCH;
-            const int col = p % TW, rr = (p / TW) % TR, f = p / (TW * TR);
-            const int h = h0 + rr - 1, w = col - 1, frame = f0 + f;
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (h >= 0 && h < H && w >= 0 && w < W && frame < a.n)
-                v = *reinterpret_cast<const uint4*>(x + ((int64_t(frame) * H + h) * W + w) * CIN + ch * VEC);
-            T* dst = xs + p * CP + ch * VEC;
-            if constexpr (sizeof(T) == 2) {
-                if (MODE == IN_RELU) {
-                    uint32_t* u = reinterpret_cast<uint32_t*>(&v);
+    // ---- register prefetch of one tile's window (zeros outside the image / past n).
+    // Windows larger than the prefetch capacity are loaded directly, kConvItems items per
+    // thread at a time, without overlap.
+    const bool prefetch = nitems <= 256 * kConvItems;
+    uint4 pre[kConvItems];
+    auto load = [&](int tile, int base) {
+        const int band = tile % nbands, fg = tile / nbands;
+        const int h0 = band * TH, f0 = fg * FR;
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        uint32_t lo = u[j] & 0xffffu, hi = u[j] >> 16;
-                        if ((lo & 0x8000u) && (lo & 0x7fffu) <= 0x7f80u) lo = 0;   // negative, not NaN
-                        if ((hi & 0x8000u) && (hi & 0x7fffu) <= 0x7f80u) hi = 0;
-                        u[j] = lo | (hi << 16);
+        for (int i = 0; i < kConvItems; ++i) {
+            pre[i] = make_uint4(0, 0, 0, 0);
+            const int idx = base + tid + 256 * i;
+            if (idx < nitems) {
+                const int ch = idx % NCH, pix = idx / NCH;
+                const int w = pix % W, rr = (pix / W) % TR, f = pix / (W * TR);
+                const int h = h0 + rr - 1, frame = f0 + f;
+                if (h >= 0 && h < H && frame < a.n) {
+                    if constexpr (MODE == IN_U8) {
+                        const int64_t row = a.row_idx ? a.row_idx[frame] : frame;
+                        pre[i].x = *reinterpret_cast<const uint32_t*>(static_cast<const uint8_t*>(a.x) +
+                                                                      ((row * H + h) * W + w) * 4);
+                    } else {
+                        pre[i] = *reinterpret_cast<const uint4*>(static_cast<const T*>(a.x) +
+                                                                 ((int64_t(frame) * H + h) * W + w) * CIN + ch * VEC);
                     }
                 }
-                *reinterpret_cast<uint4*>(dst) = v;
-            } else {
-                const float* fv = reinterpret_cast<const float*>(&v);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) dst[j] = MODE == IN_RELU ? relu_f(fv[j]) : fv[j];
             }
         }
-    }
-    __syncthreads();
+    };
+    auto store = [&](int base) {
+#pragma unroll
+        for (int i = 0; i < kConvItems; ++i) {
+            const int idx = base + tid + 256 * i;
+            if (idx < nitems) {
+                const int ch = idx % NCH, pix = idx / NCH;
+                const int w = pix % W, rr = (pix / W) % TR, f = pix / (W * TR);
+                T* dst = xs + ((f * TR + rr) * TW + w + 1) * CP + ch * VEC;
+                uint4 v = pre[i];
+                if constexpr (MODE == IN_U8) {
+                    const uint32_t u = v.x;
+                    if constexpr (BF) {
+                        *reinterpret_cast<uint2*>(dst) = make_uint2(pack2bf(float(u & 0xff), float((u >> 8) & 0xff)),
+                                                                    pack2bf(float((u >> 16) & 0xff), float(u >> 24)));
+                    } else {
+                        dst[0] = float(u & 0xff); dst[1] = float((u >> 8) & 0xff);
+                        dst[2] = float((u >> 16) & 0xff); dst[3] = float(u >> 24);
+                    }
+                } else if constexpr (BF) {
+                    if (MODE == IN_RELU) {
+                        uint32_t* u = reinterpret_cast<uint32_t*>(&v);
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            uint32_t lo = u[j] & 0xffffu, hi = u[j] >> 16;
+                            if ((lo & 0x8000u) && (lo & 0x7fffu) <= 0x7f80u) lo = 0;   // negative, not NaN
+                            if ((hi & 0x8000u) && (hi & 0x7fffu) <= 0x7f80u) hi = 0;
+                            u[j] = lo | (hi << 16);
+                        }
+                    }
+                    *reinterpret_cast<uint4*>(dst) = v;
+                } else {
+                    const float* fv = reinterpret_cast<const float*>(&v);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) dst[j] = MODE == IN_RELU ? relu_f(fv[j]) : fv[j];
+                }
+            }
+        }
+    };
 
-    // ---- MFMA main loop over 16-pixel tiles
     const int g = lane >> 4, r16 = lane & 15;
     const int npx = FR * TH * W;
-    const int ntiles = (npx + 15) / 16;
+    const int ntl = (npx + 15) / 16;
 
     // Per-lane LDS offset of its B fragment within the 3x3 window, per k-step.
     auto b_off = [&](int ks, int half) -> int {
-        // k of this lane's first element (for CIN == 4 bf16: each half covers one tap)
         const int k0 = ks * KSTEP + g * KPL + half * 4;
         const int tap = k0 / CIN, i = k0 % CIN;
         if (tap >= 9) return -1;
         return ((tap / 3) * TW + (tap % 3)) * CP + i;
     };
 
-    for (int nt = wave; nt < ntiles; nt += 4) {
-        const int q = nt * 16 + r16;
-        const int qc = q < npx ? q : npx - 1;
-        const int c = qc % W, rr = (qc / W) % TH, f = qc / (W * TH);
-        const T* xb = xs + ((f * TR + rr) * TW + c) * CP;
-        cb_f32x4 acc[MT];
+    int tile = blockIdx.x;
+    if (prefetch && tile < ntiles) load(tile, 0);
+    __syncthreads();   // weights and padding columns visible
+    Frag wreg[HOIST ? MT * KSTEPS : 1];
+    if constexpr (HOIST) {
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) acc[mt] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int ks = 0; ks < KSTEPS; ++ks)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+                wreg[ks * MT + mt] = P::lds_frag(wl + (mt * 16 + r16) * KPITCH + ks * KSTEP + g * KPL);
+    }
 
-        if constexpr (sizeof(T) == 2) {
+    for (; tile < ntiles; tile += gridDim.x) {
+        const int band = tile % nbands, fg = tile / nbands;
+        const int h0 = band * TH, f0 = fg * FR;
+        __syncthreads();   // previous tile's MFMA reads are done
+        if (prefetch) {
+            store(0);
+        } else {
+            for (int base = 0; base < nitems; base += 256 * kConvItems) {
+                load(tile, base);
+                store(base);
+            }
+        }
+        __syncthreads();
+        if (prefetch && tile + int(gridDim.x) < ntiles) load(tile + gridDim.x, 0);   // overlaps the MFMAs
+
+        for (int nt = wave; nt < ntl; nt += 4) {
+            const int q = nt * 16 + r16;
+            const int qc = q < npx ? q : npx - 1;
+            const int c = qc % W, rr = (qc / W) % TH, f = qc / (W * TH);
+            const T* xb = xs + ((f * TR + rr) * TW + c) * CP;
+            cb_f32x4 acc[MT];
 #pragma unroll
-            for (int ks = 0; ks < KSTEPS; ++ks) {
-                Frag b;
-                if constexpr (CIN == 4) {
-                    const int o0 = b_off(ks, 0), o1 = b_off(ks, 1);
-                    const uint2 lo = o0 >= 0 ? *reinterpret_cast<const uint2*>(xb + o0) : make_uint2(0, 0);
-                    const uint2 hi = o1 >= 0 ? *reinterpret_cast<const uint2*>(xb + o1) : make_uint2(0, 0);
-                    b = make_uint4(lo.x, lo.y, hi.x, hi.y);
-                } else {
-                    const int o0 = b_off(ks, 0);
-                    b = o0 >= 0 ? P::lds_frag(xb + o0) : P::zero();
+            for (int mt = 0; mt < MT; ++mt) acc[mt] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+
+            if constexpr (BF) {
+#pragma unroll
+                for (int ks = 0; ks < KSTEPS; ++ks) {
+                    Frag b;
+                    if constexpr (CIN == 4) {
+                        const int o0 = b_off(ks, 0), o1 = b_off(ks, 1);
+                        const uint2 lo = o0 >= 0 ? *reinterpret_cast<const uint2*>(xb + o0) : make_uint2(0, 0);
+                        const uint2 hi = o1 >= 0 ? *reinterpret_cast<const uint2*>(xb + o1) : make_uint2(0, 0);
+                        b = make_uint4(lo.x, lo.y, hi.x, hi.y);
+                    } else {
+                        const int o0 = b_off(ks, 0);
+                        b = o0 >= 0 ? P::lds_frag(xb + o0) : P::zero();
+                    }
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) {
+                        Frag af;
+                        if constexpr (HOIST) af = wreg[ks * MT + mt];
+                        else af = P::lds_frag(wl + (mt * 16 + r16) * KPITCH + ks * KSTEP + g * KPL);
+                        acc[mt] = P::mma(af, b, acc[mt]);
+                    }
                 }
+            } else {
+                for (int ks = 0; ks < KSTEPS; ++ks) {
+                    const int o0 = b_off(ks, 0);
+                    const Frag b = o0 >= 0 ? P::lds_frag(xb + o0) : P::zero();
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    const Frag af = P::lds_frag(wl + (mt * 16 + r16) * KPITCH + ks * KSTEP + g * KPL);
-                    acc[mt] = P::mma(af, b, acc[mt]);
+                    for (int mt = 0; mt < MT; ++mt) {
+                        const Frag af = P::lds_frag(wl + (mt * 16 + r16) * KPITCH + ks * KSTEP + g * KPL);
+                        acc[mt] = P::mma(af, b, acc[mt]);
+                    }
                 }
             }
-        } else {
-            for (int ks = 0; ks < KSTEPS; ++ks) {
-                const int o0 = b_off(ks, 0);
-                const Frag b = o0 >= 0 ? P::lds_frag(xb + o0) : P::zero();
+
+            // ---- fused epilogue
+            const int hh = h0 + rr, frame = f0 + f;
+            if (q < npx && hh < H && frame < a.n) {
+                const int64_t pix = (int64_t(frame) * H + hh) * W + c;
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
-                    const Frag af = P::lds_frag(wl + (mt * 16 + r16) * KPITCH + ks * KSTEP + g * KPL);
-                    acc[mt] = P::mma(af, b, acc[mt]);
+                    const int co = og + mt * 16 + g * 4;
+                    float v[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) v[j] = acc[mt][j] * a.scale + (a.bias ? a.bias[co + j] : 0.f);
+                    if (a.mask) {
+                        float mk[4];
+                        load4(static_cast<const T*>(a.mask) + pix * cout_total + co, mk);
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) v[j] = mk[j] > 0.f ? v[j] : 0.f;
+                    }
+                    if (a.add) {
+                        float ad[4];
+                        load4(static_cast<const T*>(a.add) + pix * cout_total + co, ad);
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) v[j] += ad[j];
+                    }
+                    store4(static_cast<T*>(a.y) + pix * cout_total + co, v[0], v[1], v[2], v[3]);
                 }
             }
         }
+    }
+}
 
-        // ---- fused epilogue
-        const int hh = h0 + rr, frame = f0 + f;
-        if (q < npx && hh < H && frame < a.n) {
-            const int64_t pix = (int64_t(frame) * H + hh) * W + c;
+// ------------------------------------------------------------------ bf16 streaming kernel
+//
+// At these channel counts a bf16 conv does about 70 flops per byte it must move, so it is
+// bound by HBM, not by the matrix cores; this kernel is organised around keeping enough
+// bytes in flight. Each tile (FR frames x TH output rows x all W columns) is staged with
+// direct buffer->LDS loads, which need no registers: the zero-padded input window and, when
+// present, the epilogue's mask and residual operands for exactly the tile's output pixels.
+// Padding (image borders, frames past n) comes from offsets past the end of the buffer
+// resource, which read as zeros. The waves then run the implicit GEMM out of LDS and store
+// straight from the MFMA accumulators. Several workgroups per CU interleave their staging
+// and compute phases.
+//
+// LDS layout (bytes): weights [COUT][KPITCH] bf16 | window [FR][TH+2][W+2] pixels |
+// mask [FR*TH*W][COUT] bf16 | residual [FR*TH*W][COUT] bf16. A bf16 window pixel holds CIN/8
+// 16-byte slots plus one slot that stays zero: the odd slot pitch spreads the 16 lanes of a
+// fragment read (consecutive pixels) over distinct banks, and the zero slot doubles as the
+// source of empty fragments. A uint8 window pixel is its 4 frame bytes.
+
+namespace {
+
+typedef __attribute__((address_space(3))) void lds_t;
+
+// Raw buffer resource over [base, base + bytes); loads at offsets >= bytes return zero.
+CB_DEV __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, int(bytes), 0x00020000);
+}
+constexpr uint32_t kOOB = 0x80000000u;   // past every resource the launcher allows
+
+// floor(q / d) for 0 <= q < 2^20, given inv = 1.0f / d: the error of the product stays below
+// the distance from (q + 0.5) / d to the nearest integer.
+CB_DEV int qdiv(int q, float inv) { return int((float(q) + 0.5f) * inv); }
+
+typedef short cb_s16x2 __attribute__((ext_vector_type(2)));
+// relu on two bf16 patterns: every pattern with the sign bit set becomes +0.
+CB_DEV uint32_t relu_bf16x2(uint32_t u) {
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(cb_s16x2, u),
+                                                                  cb_s16x2{0, 0}));
+}
+
+// One DMA lane: 4 or 16 bytes at byte offset off of the resource -> LDS at lds + lane * size
+// (lds is the same for the whole wave).
+CB_DEV void dma4_to_lds(__amdgpu_buffer_rsrc_t r, unsigned char* lds, uint32_t off) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_t*)(lds), 4, off, 0, 0, 0);
+}
+CB_DEV void dma16_to_lds(__amdgpu_buffer_rsrc_t r, unsigned char* lds, uint32_t off) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_t*)(lds), 16, off, 0, 0, 0);
+}
+
+CB_DEV uint2 u8x4_to_bf16(uint32_t u) {
+    return make_uint2(pack2bf(float(u & 0xffu), float((u >> 8) & 0xffu)),
+                      pack2bf(float((u >> 16) & 0xffu), float(u >> 24)));
+}
+
+}  // namespace
+
+struct DmaTile {
+    int TH, FR, nbands, ntiles, cout_total;
+    int win_off, mask_off, add_off;   // LDS byte offsets of the regions
+    float inv_W, inv_TW, inv_TH, inv_TR;
+};
+
+template <int CIN, int COUT, int MODE>
+struct DmaGeom {
+    using G = ConvGeom<PrecBF16, CIN>;
+    static constexpr bool U8 = MODE == IN_U8;
+    static constexpr int SPP = U8 ? 1 : CIN / 8 + 1;   // LDS slots per window pixel
+    static constexpr int SB = U8 ? 4 : 16;             // bytes per slot (one DMA lane)
+    static constexpr int PB = SPP * SB;                // bytes per window pixel
+    static constexpr int OCH = COUT / 8;               // 16-byte operand slots per pixel
+    static constexpr int WLB = (COUT * G::KPITCH * 2 + 15) / 16 * 16;
+    static int blocks(int slots) { return (slots + 63) / 64; }
+    static int win_bytes(int TH, int FR, int W) { return blocks(FR * (TH + 2) * (W + 2) * SPP) * 64 * SB; }
+    static int op_bytes(int TH, int FR, int W) { return blocks(FR * TH * W * OCH) * 64 * 16; }
+};
+
+template <int CIN, int COUT, int MODE, int FLIP>
+__global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t) {
+    using D = DmaGeom<CIN, COUT, MODE>;
+    using G = ConvGeom<PrecBF16, CIN>;
+    using P = PrecBF16;
+    constexpr int KSTEPS = G::KSTEPS, KPITCH = G::KPITCH, MT = COUT / 16;
+    constexpr int SPP = D::SPP, PB = D::PB, OCH = D::OCH;
+    constexpr bool U8 = D::U8;
+    constexpr bool HOIST = MT * KSTEPS <= 10;
+    static_assert(!U8 || CIN == 4, "uint8 frames carry 4 stacked channels");
+    static_assert(U8 || CIN % 16 == 0, "bf16 inputs in 16-channel multiples");
+
+    extern __shared__ __align__(16) unsigned char smem[];
+    uint16_t* wl = reinterpret_cast<uint16_t*>(smem);
+    unsigned char* win = smem + t.win_off;
+    unsigned char* opm = smem + t.mask_off;
+    unsigned char* opa = smem + t.add_off;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, r16 = lane & 15;
+    const int og = blockIdx.y * COUT;
+    const int H = a.H, W = a.W, TH = t.TH, FR = t.FR;
+    const int TW = W + 2, TR = TH + 2;
+    const bool has_mask = a.mask != nullptr, has_add = a.add != nullptr;
+
+    // ---- weights -> LDS once: wl[o][tap*CIN + i], zero in the k padding
+    if (FLIP) {
+        for (int e = tid; e < 9 * COUT * CIN; e += 256) {
+            const int i = e % CIN, o = (e / CIN) % COUT, tap = e / (CIN * COUT);
+            wl[o * KPITCH + (8 - tap) * CIN + i] = P::store(a.w[(int64_t(tap) * t.cout_total + og + o) * CIN + i]);
+        }
+    } else {
+        for (int e = tid; e < 9 * CIN * COUT; e += 256) {
+            const int o = e % COUT, k = e / COUT;
+            wl[o * KPITCH + k] = P::store(a.w[int64_t(k) * t.cout_total + og + o]);
+        }
+    }
+    if constexpr (G::KP > G::K) {
+        constexpr int PADK = G::KP - G::K;
+        for (int e = tid; e < COUT * PADK; e += 256)
+            wl[(e / PADK) * KPITCH + G::K + e % PADK] = 0;
+    }
+    float bias[MT][4];
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                const int co = og + mt * 16 + g * 4;
-                float v[4];
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) v[j] = acc[mt][j] * a.scale + (a.bias ? a.bias[co + j] : 0.f);
-                if (a.mask) {
-                    float mk[4];
-                    load4(static_cast<const T*>(a.mask) + pix * cout_total + co, mk);
+        for (int j = 0; j < 4; ++j) bias[mt][j] = a.bias ? a.bias[og + mt * 16 + g * 4 + j] : 0.f;
+    __syncthreads();
+    uint4 wreg[HOIST ? MT * KSTEPS : 1];
+    if constexpr (HOIST) {
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) v[j] = mk[j] > 0.f ? v[j] : 0.f;
+        for (int ks = 0; ks < KSTEPS; ++ks)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+                wreg[ks * MT + mt] = P::lds_frag(wl + (mt * 16 + r16) * KPITCH + ks * 32 + g * 8);
+    }
+
+    // ---- per-lane B-fragment offsets from the lane's tap-(0,0) window pixel (bytes).
+    // k = ks*32 + g*8 .. +7 covers taps k / CIN; past the 9 taps the fragment is zero.
+    auto tap_off = [&](int tap) { return ((tap / 3) * TW + tap % 3) * PB; };
+    int boff[KSTEPS];
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+        if constexpr (U8) {
+            boff[ks] = 0;   // uint8 fragments are read per tap below
+        } else {
+            const int k0 = ks * 32 + g * 8, tap = k0 / CIN, c = (k0 % CIN) / 8;
+            boff[ks] = tap < 9 ? tap_off(tap) + c * 16 : (SPP - 1) * 16;   // zero slot
+        }
+    }
+    // uint8: lane g holds taps 2g, 2g+1 in k-step 0 and tap 8 (g == 0) in k-step 1
+    const int u0 = tap_off(U8 ? 2 * g : 0), u1 = tap_off(U8 ? 2 * g + 1 : 0), u2 = tap_off(8);
+
+    int lg = blockIdx.x;   // neighbouring tiles (which share halo rows) on one XCD
+    if ((gridDim.x & 7) == 0) lg = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+
+    for (int tile = lg; tile < t.ntiles; tile += gridDim.x) {
+        const int band = tile % t.nbands, fg = tile / t.nbands;
+        const int h0 = band * TH, f0 = fg * FR;
+        const int nf = a.n - f0 < FR ? a.n - f0 : FR;
+        const int the = H - h0 < TH ? H - h0 : TH;
+        const int npx = nf * the * W;   // FR > 1 only when a band is the whole frame
+        __syncthreads();   // the previous tile's LDS reads are done
+
+        // ---- stage window (and operands) HBM -> LDS
+        if constexpr (U8) {
+            const uint32_t fb = uint32_t(H) * W * 4;
+            const int64_t row = a.row_idx ? a.row_idx[f0] : f0;
+            const auto rx = buf_rsrc(static_cast<const uint8_t*>(a.x) + row * fb, fb);
+            const int ns = TR * TW;
+            for (int b = wave; b * 64 < ns; b += 4) {
+                const int j = b * 64 + lane;
+                uint32_t off = kOOB;
+                if (j < ns) {
+                    const int rr = qdiv(j, t.inv_TW), col = j - rr * TW, h = h0 + rr - 1;
+                    if (col >= 1 && col <= W && h >= 0 && h < H) off = (uint32_t(h) * W + col - 1) * 4;
                 }
-                if (a.add) {
-                    float ad[4];
-                    load4(static_cast<const T*>(a.add) + pix * cout_total + co, ad);
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) v[j] += ad[j];
+                dma4_to_lds(rx, win + b * 256, off);
+            }
+        } else {
+            const uint32_t fb = uint32_t(H) * W * CIN * 2;
+            const auto rx = buf_rsrc(static_cast<const uint16_t*>(a.x) + int64_t(f0) * H * W * CIN, uint32_t(nf) * fb);
+            const int ns = FR * TR * TW * SPP;
+            for (int b = wave; b * 64 < ns; b += 4) {
+                const int j = b * 64 + lane;
+                uint32_t off = kOOB;
+                if (j < ns) {
+                    const int p = j / SPP, c = j - p * SPP;
+                    const int rowi = qdiv(p, t.inv_TW), col = p - rowi * TW;
+                    const int f = qdiv(rowi, t.inv_TR), rr = rowi - f * TR, h = h0 + rr - 1;
+                    if (c < SPP - 1 && col >= 1 && col <= W && h >= 0 && h < H)
+                        off = ((uint32_t(f) * H + h) * W + col - 1) * (CIN * 2) + c * 16;
                 }
-                store4(static_cast<T*>(a.y) + pix * cout_total + co, v[0], v[1], v[2], v[3]);
+                dma16_to_lds(rx, win + b * 1024, off);
+            }
+        }
+        if (has_mask || has_add) {
+            const uint32_t ob = uint32_t(H) * W * t.cout_total * 2;
+            const int64_t fo = int64_t(f0) * H * W * t.cout_total;
+            const auto rm = buf_rsrc(has_mask ? static_cast<const uint16_t*>(a.mask) + fo : nullptr, has_mask ? uint32_t(nf) * ob : 0);
+            const auto ra = buf_rsrc(has_add ? static_cast<const uint16_t*>(a.add) + fo : nullptr, has_add ? uint32_t(nf) * ob : 0);
+            const int ns = npx * OCH;
+            for (int b = wave; b * 64 < ns; b += 4) {
+                const int j = b * 64 + lane;
+                uint32_t off = kOOB;
+                if (j < ns) {
+                    const int q = j / OCH, c = j - q * OCH;
+                    const int rowi = qdiv(q, t.inv_W), col = q - rowi * W;
+                    const int f = qdiv(rowi, t.inv_TH), rr = rowi - f * TH;
+                    off = ((uint32_t(f) * H + h0 + rr) * W + col) * (t.cout_total * 2) + (og + c * 8) * 2;
+                }
+                if (has_mask) dma16_to_lds(rm, opm + b * 1024, off);
+                if (has_add) dma16_to_lds(ra, opa + b * 1024, off);
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0);   // this wave's loads have landed in LDS
+        __syncthreads();                 // ... and everyone else's
+        if constexpr (MODE == IN_RELU) {
+            uint4* w4 = reinterpret_cast<uint4*>(win);
+            const int ns = FR * TR * TW * SPP;
+            for (int j = tid; j < ns; j += 256) {
+                uint4 v = w4[j];
+                v.x = relu_bf16x2(v.x); v.y = relu_bf16x2(v.y); v.z = relu_bf16x2(v.z); v.w = relu_bf16x2(v.w);
+                w4[j] = v;
+            }
+            __syncthreads();
+        }
+
+        // ---- implicit GEMM over the tile's output pixels, 16 per MFMA column tile
+        const int ntl = (npx + 15) >> 4;
+        for (int nt = wave; nt < ntl; nt += 4) {
+            const int q = nt * 16 + r16;
+            const int qc = q < npx ? q : npx - 1;
+            const int rowi = qdiv(qc, t.inv_W), col = qc - rowi * W;
+            const int f = qdiv(rowi, t.inv_TH), r = rowi - f * TH;
+            const unsigned char* xb = win + ((f * TR + r) * TW + col) * PB;
+            cb_f32x4 acc[MT];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) acc[mt] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KSTEPS; ++ks) {
+                uint4 b;
+                if constexpr (U8) {
+                    if (ks == 0) {
+                        const uint2 lo = u8x4_to_bf16(*reinterpret_cast<const uint32_t*>(xb + u0));
+                        const uint2 hi = u8x4_to_bf16(*reinterpret_cast<const uint32_t*>(xb + u1));
+                        b = make_uint4(lo.x, lo.y, hi.x, hi.y);
+                    } else {
+                        const uint2 lo = u8x4_to_bf16(*reinterpret_cast<const uint32_t*>(xb + u2));
+                        b = g == 0 ? make_uint4(lo.x, lo.y, 0, 0) : make_uint4(0, 0, 0, 0);
+                    }
+                } else {
+                    b = *reinterpret_cast<const uint4*>(xb + boff[ks]);
+                }
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    uint4 af;
+                    if constexpr (HOIST) af = wreg[ks * MT + mt];
+                    else af = P::lds_frag(wl + (mt * 16 + r16) * KPITCH + ks * 32 + g * 8);
+                    acc[mt] = P::mma(af, b, acc[mt]);
+                }
+            }
+            if (q < npx) {
+                const int64_t pix = (int64_t(f0 + f) * H + h0 + r) * W + col;
+                uint16_t* yp = static_cast<uint16_t*>(a.y) + pix * t.cout_total + og + g * 4;
+                const int oq = (q * COUT + g * 4) * 2;
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    float v[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) v[j] = acc[mt][j] * a.scale + bias[mt][j];
+                    if (has_mask) {
+                        float mk[4];
+                        load4(reinterpret_cast<const uint16_t*>(opm + oq + mt * 32), mk);
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) v[j] = mk[j] > 0.f ? v[j] : 0.f;
+                    }
+                    if (has_add) {
+                        float ad[4];
+                        load4(reinterpret_cast<const uint16_t*>(opa + oq + mt * 32), ad);
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) v[j] += ad[j];
+                    }
+                    store4(yp + mt * 16, v[0], v[1], v[2], v[3]);
+                }
             }
         }
     }
@@ -215,7 +555,7 @@ namespace {
 
 // Tiles aim at 64 KB of LDS (two or more workgroups per CU); layers whose weights alone
 // need more may use up to the device's per-workgroup maximum.
-constexpr size_t kLdsTarget = 64 * 1024;
+constexpr size_t kLdsTarget = 40 * 1024;
 
 template <class P, int CIN, int COUT>
 size_t conv_lds_bytes(int TH, int FR, int W) {
@@ -226,39 +566,49 @@ size_t conv_lds_bytes(int TH, int FR, int W) {
 
 template <class P, int CIN, int COUT, int MODE, int FLIP>
 hipError_t launch(const ConvArgs& a, int cout_total, hipStream_t s) {
-    // Tile: about 512 output pixels per workgroup, bands of equal height, within the LDS budget.
+    // Tile: bands of about 640 output pixels (whole frames when small), as many input load
+    // items as the register prefetch holds, within the LDS budget.
+    constexpr int VEC = MODE == IN_U8 ? 4 : (sizeof(typename P::T) == 2 ? 8 : 4);
+    constexpr int NCH = CIN / VEC;
     const int H = a.H, W = a.W;
     int TH, FR = 1;
-    if (H * W >= 512) {
-        const int target = (512 + W - 1) / W;
+    if (H * W >= 640) {
+        const int target = (640 + W - 1) / W;
         const int nb = (H + target - 1) / target;
         TH = (H + nb - 1) / nb;
     } else {
         TH = H;
-        FR = 512 / (H * W);
+        FR = 640 / (H * W);
         if (FR < 1) FR = 1;
         if (FR > a.n) FR = a.n;
     }
+    auto items = [&](int th, int fr) { return fr * (th + 2) * W * NCH; };
     const size_t budget = std::max(kLdsTarget, std::min<size_t>(lds_limit(), 160 * 1024));
-    while (conv_lds_bytes<P, CIN, COUT>(TH, FR, W) > (FR > 1 || TH > 4 ? kLdsTarget : budget)) {
+    while ((items(TH, FR) > 256 * kConvItems && (FR > 1 || TH > 1)) ||
+           conv_lds_bytes<P, CIN, COUT>(TH, FR, W) > (FR > 1 || TH > 4 ? kLdsTarget : budget)) {
         if (FR > 1) --FR;
         else if (TH > 1) {
             const int nb = (H + TH - 1) / TH + 1;
             const int next = (H + nb - 1) / nb;
             TH = next < TH ? next : TH - 1;
-        }
-        else return hipErrorInvalidValue;
+        } else return hipErrorInvalidValue;
     }
     const int nbands = (H + TH - 1) / TH;
     const int nfg = (a.n + FR - 1) / FR;
+    const int ntiles = nbands * nfg;
     const size_t lds = conv_lds_bytes<P, CIN, COUT>(TH, FR, W);
-    dim3 grid(unsigned(nbands * nfg), unsigned(cout_total / COUT));
+    const int groups = cout_total / COUT;
+    // persistent grid: as many workgroups as are resident at once, over the channel groups
+    const void* fn = reinterpret_cast<const void*>(&conv3x3_kernel<P, CIN, COUT, MODE, FLIP>);
+    int gx = std::max(1, resident_blocks(fn, 256, lds) / groups);
+    if (gx > ntiles) gx = ntiles;
+    const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(groups));
     ProfScope ps(s, [&] {
         return cb_key(FLIP ? "conv_dgrad" : "conv_fwd", sizeof(typename P::T) == 2 ? 0 : 1,
                       cb_dims(CIN, cout_total) + "/" + cb_dims(H, W));
     });
     hipLaunchKernelGGL((conv3x3_kernel<P, CIN, COUT, MODE, FLIP>), grid, dim3(256), lds, s, a, TH,
-                       FR, nbands, cout_total);
+                       FR, nbands, ntiles, cout_total);
     return hipGetLastError();
 }
 
@@ -270,9 +620,62 @@ constexpr int conv_group() {
     return cg;
 }
 
+// bf16 tiles: a band height that keeps a workgroup within kDmaLdsTarget (four per CU) and
+// stages the fewest window rows per frame; whole frames batch up to kDmaPixMax pixels.
+constexpr int kDmaLdsTarget = 40 * 1024;
+constexpr int kDmaPixMax = 2048;
+
+template <int CIN, int COUT, int MODE, int FLIP>
+hipError_t launch_bf16(const ConvArgs& a, int cout_total, hipStream_t s) {
+    using D = DmaGeom<CIN, COUT, MODE>;
+    const int H = a.H, W = a.W;
+    const int nops = (a.mask ? 1 : 0) + (a.add ? 1 : 0);
+    auto lds = [&](int th, int fr) {
+        return size_t(D::WLB) + size_t(D::win_bytes(th, fr, W)) + size_t(nops) * D::op_bytes(th, fr, W);
+    };
+    const size_t limit = std::min<size_t>(lds_limit(), 160 * 1024);
+    int thmax = std::min(H, std::max(1, kDmaPixMax / W));
+    while (thmax > 1 && lds(thmax, 1) > size_t(kDmaLdsTarget)) --thmax;
+    if (lds(thmax, 1) > limit) return hipErrorInvalidValue;
+    int TH = 1, best = 1 << 30;
+    for (int th = 1; th <= thmax; ++th) {
+        const int rows = (H + th - 1) / th * (th + 2);
+        if (rows <= best) { best = rows; TH = th; }
+    }
+    const int nbands = (H + TH - 1) / TH;
+    int FR = 1;
+    if (nbands == 1 && MODE != IN_U8)
+        while (FR < a.n && lds(TH, FR + 1) <= size_t(kDmaLdsTarget) && (FR + 1) * H * W <= kDmaPixMax) ++FR;
+    // 32-bit buffer offsets cover FR frames of input and of each operand
+    if (int64_t(FR) * H * W * std::max(MODE == IN_U8 ? 2 : CIN, cout_total) * 2 >= (int64_t(1) << 31))
+        return hipErrorInvalidValue;
+    const int ntiles = nbands * ((a.n + FR - 1) / FR);
+    const size_t L = lds(TH, FR);
+    DmaTile t{};
+    t.TH = TH; t.FR = FR; t.nbands = nbands; t.ntiles = ntiles; t.cout_total = cout_total;
+    t.win_off = D::WLB;
+    t.mask_off = t.win_off + D::win_bytes(TH, FR, W);
+    t.add_off = t.mask_off + (a.mask ? D::op_bytes(TH, FR, W) : 0);
+    t.inv_W = 1.f / float(W); t.inv_TW = 1.f / float(W + 2);
+    t.inv_TH = 1.f / float(TH); t.inv_TR = 1.f / float(TH + 2);
+    const int groups = cout_total / COUT;
+    const void* fn = reinterpret_cast<const void*>(&conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP>);
+    int gx = std::max(1, resident_blocks(fn, 256, L) / groups);
+    if (gx > ntiles) gx = ntiles;
+    const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(groups));
+    ProfScope ps(s, [&] {
+        return cb_key(FLIP ? "conv_dgrad" : "conv_fwd", 0, cb_dims(CIN, cout_total) + "/" + cb_dims(H, W));
+    });
+    hipLaunchKernelGGL((conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP>), grid, dim3(256), L, s, a, t);
+    return hipGetLastError();
+}
+
 template <class P, int CIN, int COUT, int MODE, int FLIP>
 hipError_t launch_split(const ConvArgs& a, hipStream_t s) {
-    return launch<P, CIN, conv_group<P, CIN, COUT>(), MODE, FLIP>(a, COUT, s);
+    if constexpr (std::is_same_v<P, PrecBF16>)
+        return launch_bf16<CIN, conv_group<P, CIN, COUT>(), MODE, FLIP>(a, COUT, s);
+    else
+        return launch<P, CIN, conv_group<P, CIN, COUT>(), MODE, FLIP>(a, COUT, s);
 }
 
 template <class P>

@@ -110,5 +110,8 @@ hipError_t adam(int64_t n, float* p, const float* g, float* m, float* v, float l
                 float* stats, float* partial, hipStream_t s);
 // Largest dynamic LDS allocation per workgroup on the current device (bytes).
 size_t lds_limit();
+// Workgroups of kernel `fn` (with `threads` threads and `lds` bytes of dynamic LDS) that are
+// resident at once on the whole current device; sizes persistent grids (cached).
+int resident_blocks(const void* fn, int threads, size_t lds);
 
 }  // namespace cb
