@@ -85,6 +85,53 @@ CB_DEV void load4(const float* p, float* o) {
 
 CB_DEV float relu_f(float x) { return x < 0.f ? 0.f : x; }   // keeps NaN
 
+// ---------------------------------------------------------------- direct HBM -> LDS staging
+// buffer_load ... lds writes each lane's 4 or 16 bytes to LDS at a wave-uniform base plus
+// lane * size, without passing through registers.
+
+typedef __attribute__((address_space(3))) void lds_t;
+
+// Raw buffer resource over [base, base + bytes); loads at offsets >= bytes return zero.
+CB_DEV __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, int(bytes), 0x00020000);
+}
+constexpr uint32_t kOOB = 0x80000000u;   // past every resource the launcher allows
+
+// floor(q / d) for 0 <= q < 2^20, given inv = 1.0f / d: the error of the product stays below
+// the distance from (q + 0.5) / d to the nearest integer.
+CB_DEV int qdiv(int q, float inv) { return int((float(q) + 0.5f) * inv); }
+
+typedef short cb_s16x2 __attribute__((ext_vector_type(2)));
+// relu on two bf16 patterns: every pattern with the sign bit set becomes +0.
+CB_DEV uint32_t relu_bf16x2(uint32_t u) {
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(cb_s16x2, u),
+                                                                  cb_s16x2{0, 0}));
+}
+
+// One DMA lane: 4 or 16 bytes at byte offset off of the resource -> LDS at lds + lane * size
+// (lds is the same for the whole wave).
+CB_DEV void dma4_to_lds(__amdgpu_buffer_rsrc_t r, unsigned char* lds, uint32_t off) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_t*)(lds), 4, off, 0, 0, 0);
+}
+CB_DEV void dma16_to_lds(__amdgpu_buffer_rsrc_t r, unsigned char* lds, uint32_t off) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_t*)(lds), 16, off, 0, 0, 0);
+}
+
+typedef short cb_s16x4 __attribute__((ext_vector_type(4)));
+// LDS transpose read of 16-bit data (ds_read_b64_tr_b16). Every lane addresses an 8-byte
+// chunk (4 elements); within each group of 16 lanes, lane i receives as its element j
+// element (i % 4) of the chunk addressed by lane 4*j + i/4 of the group.
+CB_DEV uint2 lds_read_tr16(const unsigned char* p) {
+    typedef __attribute__((address_space(3))) cb_s16x4 lds_s16x4;
+    return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p)));
+}
+
+CB_DEV uint2 u8x4_to_bf16(uint32_t u) {
+    return make_uint2(pack2bf(float(u & 0xffu), float((u >> 8) & 0xffu)),
+                      pack2bf(float((u >> 16) & 0xffu), float(u >> 24)));
+}
+
+
 // Block-wide reduction of a double over 256 threads (fixed order -> deterministic).
 template <int NT>
 CB_DEV double block_sum(double v, double* sh) {

@@ -282,42 +282,6 @@ __global__ __launch_bounds__(256) void conv3x3_kernel(ConvArgs a, int TH, int FR
 // fragment read (consecutive pixels) over distinct banks, and the zero slot doubles as the
 // source of empty fragments. A uint8 window pixel is its 4 frame bytes.
 
-namespace {
-
-typedef __attribute__((address_space(3))) void lds_t;
-
-// Raw buffer resource over [base, base + bytes); loads at offsets >= bytes return zero.
-CB_DEV __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, int(bytes), 0x00020000);
-}
-constexpr uint32_t kOOB = 0x80000000u;   // past every resource the launcher allows
-
-// floor(q / d) for 0 <= q < 2^20, given inv = 1.0f / d: the error of the product stays below
-// the distance from (q + 0.5) / d to the nearest integer.
-CB_DEV int qdiv(int q, float inv) { return int((float(q) + 0.5f) * inv); }
-
-typedef short cb_s16x2 __attribute__((ext_vector_type(2)));
-// relu on two bf16 patterns: every pattern with the sign bit set becomes +0.
-CB_DEV uint32_t relu_bf16x2(uint32_t u) {
-    return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(cb_s16x2, u),
-                                                                  cb_s16x2{0, 0}));
-}
-
-// One DMA lane: 4 or 16 bytes at byte offset off of the resource -> LDS at lds + lane * size
-// (lds is the same for the whole wave).
-CB_DEV void dma4_to_lds(__amdgpu_buffer_rsrc_t r, unsigned char* lds, uint32_t off) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_t*)(lds), 4, off, 0, 0, 0);
-}
-CB_DEV void dma16_to_lds(__amdgpu_buffer_rsrc_t r, unsigned char* lds, uint32_t off) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_t*)(lds), 16, off, 0, 0, 0);
-}
-
-CB_DEV uint2 u8x4_to_bf16(uint32_t u) {
-    return make_uint2(pack2bf(float(u & 0xffu), float((u >> 8) & 0xffu)),
-                      pack2bf(float((u >> 16) & 0xffu), float(u >> 24)));
-}
-
-}  // namespace
 
 struct DmaTile {
     int TH, FR, nbands, ntiles, cout_total;

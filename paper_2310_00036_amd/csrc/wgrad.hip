@@ -18,6 +18,9 @@
 #include "common.h"
 #include "kernels.h"
 
+#include <algorithm>
+#include <type_traits>
+
 namespace cb {
 
 template <class P, int CIN, int COUT>
@@ -270,6 +273,247 @@ __global__ __launch_bounds__(1024) void wgrad_reduce_kernel(const float* __restr
     }
 }
 
+// ------------------------------------------------------------------ bf16: transpose reads
+//
+// The contraction runs over output pixels q, which an MFMA fragment wants consecutive in a
+// lane, while NHWC tiles keep channels consecutive. Here both operands are staged in NHWC as
+// they are, with direct buffer->LDS loads, and the fragments come from the LDS transpose
+// read: in a group of 16 lanes, lane 4j+m addresses 4 channels (4m..4m+3 of a 16-channel
+// block) of pixel q_j and lane i receives channel i of the four pixels q_0..q_3; two reads
+// give a fragment's 8 pixels. A = dy^T (rows: output channels). B = the input window shifted
+// by one tap (columns: 16 input channels of that tap; for uint8 frames, 4 taps x 4 channels).
+// The bias gradient is one more column block whose B fragment is all ones, so it is summed
+// in the same order as the weights. Waves split the column blocks, and when there are few
+// blocks also the k-steps (summed across waves in a fixed order at the end). Each workgroup
+// writes one float32 partial; a second kernel adds the partials in a fixed order.
+
+template <int CIN, int COUT, int MODE>
+struct WgTr {
+    static constexpr bool U8 = MODE == IN_U8;
+    // pixel pitches in bytes; 8 pixels x 32 bytes then cover distinct banks
+    static constexpr int XPB = U8 ? 8 : CIN * 2 + (CIN >= 32 ? 32 : 0);
+    static constexpr int DPB = COUT * 2 + (COUT >= 32 ? 32 : 0);
+    static constexpr int MT = COUT / 16;
+    static constexpr int NB = U8 ? 3 : 9 * CIN / 16;                  // weight column blocks
+    static constexpr int NBB = NB + 1;                                 // + the bias block
+    static constexpr int TILES = MT * NBB;
+    // waves splitting k: as many as leave each wave at most 12 accumulator tiles
+    static constexpr int kw_fits(int kw) { return (4 / kw) % MT == 0 && (NBB + (4 / kw) / MT - 1) / ((4 / kw) / MT) <= 12; }
+    static constexpr int KW = kw_fits(4) ? 4 : (kw_fits(2) ? 2 : 1);
+    static constexpr int TG = 4 / KW;                                  // waves splitting tiles
+    static constexpr int NPW = TG / MT;                                // waves per row block
+    static constexpr int TPW = (NBB + NPW - 1) / NPW;                  // column blocks per wave
+    static constexpr int PSTRIDE = TILES * 256;                        // floats per partial
+    static_assert(TG % MT == 0, "row blocks spread over whole wave groups");
+};
+
+struct WgTrRun {
+    int TH, FR, nbands, ntiles;
+    int raw_off, win_off, dy_off;   // LDS byte offsets; 16 zero bytes at offset 0
+    float inv_W, inv_TW, inv_TH, inv_TR;
+};
+
+template <int CIN, int COUT, int MODE>
+__global__ __launch_bounds__(256) void wgrad_tr_kernel(WgradArgs a, WgTrRun t) {
+    using D = WgTr<CIN, COUT, MODE>;
+    constexpr int XPB = D::XPB, DPB = D::DPB, MT = D::MT, NB = D::NB, NBB = D::NBB;
+    constexpr int KW = D::KW, TG = D::TG, NPW = D::NPW, TPW = D::TPW;
+    constexpr bool U8 = D::U8;
+    constexpr int XSL = XPB / 16, DSL = DPB / 16;   // 16-byte DMA slots per pixel
+
+    extern __shared__ __align__(16) unsigned char smem[];
+    unsigned char* zero = smem;
+    unsigned char* raw = smem + t.raw_off;   // uint8 frames: [TR*TW] x 4 bytes
+    unsigned char* win = smem + t.win_off;   // [FR][TR][TW] x XPB, bf16
+    unsigned char* dyt = smem + t.dy_off;    // [FR*TH*W] x DPB, bf16
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, r16 = lane & 15, jj = r16 >> 2, m = r16 & 3;
+    const int kgrp = wave % KW, tgrp = wave / KW;
+    const int mt = tgrp % MT, nbw = tgrp / MT;
+    const int H = a.H, W = a.W, TH = t.TH, FR = t.FR;
+    const int TW = W + 2, TR = TH + 2;
+
+    if (tid < 4) reinterpret_cast<uint32_t*>(zero)[tid] = 0u;
+
+    // Per-lane byte offset of each column block's chunk from the lane's tap-(0,0) window
+    // pixel; -1 where the k values lie past the 9 taps (read as zero).
+    int boff[TPW];
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+        const int nb = nbw + NPW * i;
+        const int tap = U8 ? nb * 4 + m : nb / (CIN / 16 > 0 ? CIN / 16 : 1);
+        const int ci = U8 ? 0 : (nb % (CIN / 16 > 0 ? CIN / 16 : 1)) * 16 + 4 * m;
+        boff[i] = (nb < NB && tap < 9) ? ((tap / 3) * TW + tap % 3) * XPB + ci * 2 : -1;
+    }
+    cb_f32x4 acc[TPW];
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) acc[i] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+    const uint4 ones = make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
+
+    int lg = blockIdx.x;   // neighbouring tiles (which share halo rows) on one XCD
+    if ((gridDim.x & 7) == 0) lg = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+
+    for (int tile = lg; tile < t.ntiles; tile += gridDim.x) {
+        const int band = tile % t.nbands, fg = tile / t.nbands;
+        const int h0 = band * TH, f0 = fg * FR;
+        const int nf = a.n - f0 < FR ? a.n - f0 : FR;
+        const int the = H - h0 < TH ? H - h0 : TH;
+        const int npx = nf * the * W;   // FR > 1 only when a band is the whole frame
+        __syncthreads();   // the previous tile's LDS reads are done
+
+        // ---- stage the input window and the output-gradient tile, HBM -> LDS
+        if constexpr (U8) {
+            const uint32_t fb = uint32_t(H) * W * 4;
+            const int64_t row = a.row_idx ? a.row_idx[f0] : f0;
+            const auto rx = buf_rsrc(static_cast<const uint8_t*>(a.x) + row * fb, fb);
+            const int ns = TR * TW;
+            for (int b = wave; b * 64 < ns; b += 4) {
+                const int j = b * 64 + lane;
+                uint32_t off = kOOB;
+                if (j < ns) {
+                    const int rr = qdiv(j, t.inv_TW), col = j - rr * TW, h = h0 + rr - 1;
+                    if (col >= 1 && col <= W && h >= 0 && h < H) off = (uint32_t(h) * W + col - 1) * 4;
+                }
+                dma4_to_lds(rx, raw + b * 256, off);
+            }
+        } else {
+            const uint32_t fb = uint32_t(H) * W * CIN * 2;
+            const auto rx = buf_rsrc(static_cast<const uint16_t*>(a.x) + int64_t(f0) * H * W * CIN, uint32_t(nf) * fb);
+            const int ns = FR * TR * TW * XSL;
+            for (int b = wave; b * 64 < ns; b += 4) {
+                const int j = b * 64 + lane;
+                uint32_t off = kOOB;
+                if (j < ns) {
+                    const int p = j / XSL, c = j - p * XSL;
+                    const int rowi = qdiv(p, t.inv_TW), col = p - rowi * TW;
+                    const int f = qdiv(rowi, t.inv_TR), rr = rowi - f * TR, h = h0 + rr - 1;
+                    if (c < CIN / 8 && col >= 1 && col <= W && h >= 0 && h < H)
+                        off = ((uint32_t(f) * H + h) * W + col - 1) * (CIN * 2) + c * 16;
+                }
+                dma16_to_lds(rx, win + b * 1024, off);
+            }
+        }
+        {
+            const uint32_t gb = uint32_t(H) * W * COUT * 2;
+            const auto rg = buf_rsrc(static_cast<const uint16_t*>(a.dy) + int64_t(f0) * H * W * COUT, uint32_t(nf) * gb);
+            const int ns = npx * DSL;
+            for (int b = wave; b * 64 < ns; b += 4) {
+                const int j = b * 64 + lane;
+                uint32_t off = kOOB;
+                if (j < ns) {
+                    const int q = j / DSL, c = j - q * DSL;
+                    const int rowi = qdiv(q, t.inv_W), col = q - rowi * W;
+                    const int f = qdiv(rowi, t.inv_TH), rr = rowi - f * TH;
+                    if (c < COUT / 8) off = ((uint32_t(f) * H + h0 + rr) * W + col) * (COUT * 2) + c * 16;
+                }
+                dma16_to_lds(rg, dyt + b * 1024, off);
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0);   // this wave's loads have landed in LDS
+        __syncthreads();                 // ... and everyone else's
+        if constexpr (U8) {
+            for (int p = tid; p < TR * TW; p += 256)
+                *reinterpret_cast<uint2*>(win + p * 8) = u8x4_to_bf16(*reinterpret_cast<const uint32_t*>(raw + p * 4));
+            __syncthreads();
+        } else if constexpr (MODE == IN_RELU) {
+            uint4* w4 = reinterpret_cast<uint4*>(win);
+            for (int j = tid; j < FR * TR * TW * XSL; j += 256) {
+                uint4 v = w4[j];
+                v.x = relu_bf16x2(v.x); v.y = relu_bf16x2(v.y); v.z = relu_bf16x2(v.z); v.w = relu_bf16x2(v.w);
+                w4[j] = v;
+            }
+            __syncthreads();
+        }
+
+        // ---- k-steps of 32 pixels: lane (g, 4j+m) addresses pixels ks*32 + 16*half + 4g + j
+        const int nks = (npx + 31) >> 5;
+#pragma unroll 2
+        for (int ks = kgrp; ks < nks; ks += KW) {
+            uint2 av[2];
+            int bp[2];
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                const int q = ks * 32 + half * 16 + 4 * g + jj;
+                const bool ok = q < npx;
+                const int qc = ok ? q : 0;
+                const int rowi = qdiv(qc, t.inv_W), col = qc - rowi * W;
+                const int f = qdiv(rowi, t.inv_TH), r = rowi - f * TH;
+                bp[half] = ((f * TR + r) * TW + col) * XPB;
+                av[half] = lds_read_tr16(ok ? dyt + q * DPB + (mt * 16 + 4 * m) * 2 : zero);
+            }
+            const uint4 af = make_uint4(av[0].x, av[0].y, av[1].x, av[1].y);
+#pragma unroll
+            for (int i = 0; i < TPW; ++i) {
+                const int nb = nbw + NPW * i;
+                if (nb >= NBB) continue;
+                uint4 bf = ones;
+                if (nb < NB) {
+                    const uint2 lo = lds_read_tr16(boff[i] >= 0 ? win + bp[0] + boff[i] : zero);
+                    const uint2 hi = lds_read_tr16(boff[i] >= 0 ? win + bp[1] + boff[i] : zero);
+                    bf = make_uint4(lo.x, lo.y, hi.x, hi.y);
+                }
+                acc[i] = PrecBF16::mma(af, bf, acc[i]);
+            }
+        }
+    }
+
+    // ---- this workgroup's partial: [mt*NBB + nb][row 16][col 16]
+    if constexpr (KW > 1) {
+        __syncthreads();   // tile LDS is free
+        cb_f32x4* red = reinterpret_cast<cb_f32x4*>(smem);   // [KW][TG][TPW][64]
+#pragma unroll
+        for (int i = 0; i < TPW; ++i) red[((kgrp * TG + tgrp) * TPW + i) * 64 + lane] = acc[i];
+        __syncthreads();
+        if (kgrp == 0) {
+#pragma unroll
+            for (int i = 0; i < TPW; ++i)
+                for (int k = 1; k < KW; ++k) acc[i] += red[((k * TG + tgrp) * TPW + i) * 64 + lane];
+        }
+    }
+    if (kgrp == 0) {
+        float* part = a.partial + int64_t(blockIdx.x) * D::PSTRIDE;
+#pragma unroll
+        for (int i = 0; i < TPW; ++i) {
+            const int nb = nbw + NPW * i;
+            if (nb < NBB) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) part[(mt * NBB + nb) * 256 + (4 * g + e) * 16 + r16] = acc[i][e];
+            }
+        }
+    }
+}
+
+// Fixed-order sum of the partials, scattered to HWIO weights (times scale) and the bias.
+template <int CIN, int COUT, int MODE>
+__global__ __launch_bounds__(1024) void wgrad_tr_reduce_kernel(const float* __restrict__ partial,
+                                                               int nparts, float* dw, float* db,
+                                                               float scale) {
+    using D = WgTr<CIN, COUT, MODE>;
+    __shared__ float sh[16][64];
+    const int e = blockIdx.x * 64 + (threadIdx.x & 63);
+    const int sp = threadIdx.x >> 6;
+    float s = 0.f;
+    if (e < D::PSTRIDE)
+        for (int p = sp; p < nparts; p += 16) s += partial[int64_t(p) * D::PSTRIDE + e];
+    sh[sp][threadIdx.x & 63] = s;
+    __syncthreads();
+    if (sp == 0 && e < D::PSTRIDE) {
+        float tot = 0.f;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) tot += sh[k][threadIdx.x];
+        const int tile = e >> 8, row = (e >> 4) & 15, col = e & 15;
+        const int mt = tile / D::NBB, nb = tile % D::NBB, co = mt * 16 + row;
+        if (nb == D::NB) {
+            if (col == 0) db[co] = tot;
+        } else {
+            const int tap = D::U8 ? nb * 4 + col / 4 : nb / (CIN / 16 > 0 ? CIN / 16 : 1);
+            const int ci = D::U8 ? col % 4 : (nb % (CIN / 16 > 0 ? CIN / 16 : 1)) * 16 + col;
+            if (tap < 9) dw[(tap * CIN + ci) * COUT + co] = tot * scale;
+        }
+    }
+}
+
 namespace {
 
 constexpr int kWgradParts = 1024;        // upper bound on workgroups (and partials)
@@ -336,8 +580,92 @@ hipError_t wg_launch(const WgradArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
+// ---- transpose-read kernel (bf16): band height that stages the fewest window rows within
+// kWgTrLds of LDS; workgroups (= partials, summed afterwards) up to the resident count, with
+// at most kWgTrPartBytes of partials.
+constexpr int kWgTrLds = 40 * 1024;
+constexpr size_t kWgTrPartBytes = 24u << 20;
+constexpr int kWgTrPixMax = 2048;
+
+static int wg_tr_parts_cap(size_t pstride) {
+    const size_t cap = kWgTrPartBytes / (pstride * sizeof(float));
+    return int(cap < 256 ? 256 : (cap > 1024 ? 1024 : cap));
+}
+
+// Channel pairs the transpose-read kernel takes (its accumulators fit in registers).
+static bool wg_tr_ok(int cin, int cout) {
+    return cin == 4 || (cin == 16 && (cout == 16 || cout == 32 || cout == 64)) || (cin == 32 && cout == 32);
+}
+static size_t wg_tr_pstride(int cin, int cout) {
+    const int nb = cin == 4 ? 3 : 9 * cin / 16;
+    return size_t(cout / 16) * (nb + 1) * 256;
+}
+
+template <int CIN, int COUT, int MODE>
+hipError_t wg_tr_launch(const WgradArgs& a, hipStream_t s) {
+    using D = WgTr<CIN, COUT, MODE>;
+    const int H = a.H, W = a.W;
+    auto blk = [](int slots) { return (slots + 63) / 64; };
+    auto regions = [&](int th, int fr, int& raw, int& win, int& dyb) {
+        const int wp = fr * (th + 2) * (W + 2);
+        raw = D::U8 ? blk(wp) * 256 : 0;
+        win = D::U8 ? (wp * 8 + 15) / 16 * 16 : blk(wp * (D::XPB / 16)) * 1024;
+        dyb = blk(fr * th * W * (D::DPB / 16)) * 1024;
+    };
+    auto lds = [&](int th, int fr) {
+        int raw, win, dyb;
+        regions(th, fr, raw, win, dyb);
+        return size_t(16 + raw + win + dyb);
+    };
+    const size_t limit = std::min<size_t>(lds_limit(), 160 * 1024);
+    int thmax = std::min(H, std::max(1, kWgTrPixMax / W));
+    while (thmax > 1 && lds(thmax, 1) > size_t(kWgTrLds)) --thmax;
+    if (lds(thmax, 1) > limit) return hipErrorInvalidValue;
+    int TH = 1, best = 1 << 30;
+    for (int th = 1; th <= thmax; ++th) {
+        const int rows = (H + th - 1) / th * (th + 2);
+        if (rows <= best) { best = rows; TH = th; }
+    }
+    const int nbands = (H + TH - 1) / TH;
+    int FR = 1;
+    if (nbands == 1 && !D::U8)
+        while (FR < a.n && lds(TH, FR + 1) <= size_t(kWgTrLds) && (FR + 1) * H * W <= kWgTrPixMax) ++FR;
+    if (int64_t(FR) * H * W * std::max(CIN, COUT) * 2 >= (int64_t(1) << 31)) return hipErrorInvalidValue;
+    WgTrRun r{};
+    r.TH = TH; r.FR = FR; r.nbands = nbands; r.ntiles = nbands * ((a.n + FR - 1) / FR);
+    int raw, win, dyb;
+    regions(TH, FR, raw, win, dyb);
+    r.raw_off = 16; r.win_off = 16 + raw; r.dy_off = r.win_off + win;
+    r.inv_W = 1.f / float(W); r.inv_TW = 1.f / float(W + 2);
+    r.inv_TH = 1.f / float(TH); r.inv_TR = 1.f / float(TH + 2);
+    size_t L = lds(TH, FR);
+    if (D::KW > 1) L = std::max<size_t>(L, size_t(4) * D::TPW * 64 * 16);   // cross-wave sums
+    const void* fn = reinterpret_cast<const void*>(&wgrad_tr_kernel<CIN, COUT, MODE>);
+    int parts = std::min(resident_blocks(fn, 256, L), wg_tr_parts_cap(D::PSTRIDE));
+    if (parts > r.ntiles) parts = r.ntiles;
+    const std::string shape = cb_dims(CIN, COUT) + "/" + cb_dims(H, W);
+    {
+        ProfScope ps(s, [&] { return cb_key("wgrad", 0, shape); });
+        hipLaunchKernelGGL((wgrad_tr_kernel<CIN, COUT, MODE>), dim3(parts), dim3(256), L, s, a, r);
+    }
+    {
+        ProfScope ps(s, [&] { return cb_key("wgrad_reduce", 0, shape); });
+        hipLaunchKernelGGL((wgrad_tr_reduce_kernel<CIN, COUT, MODE>), dim3((D::PSTRIDE + 63) / 64), dim3(1024),
+                           0, s, a.partial, parts, a.dw, a.db, a.scale);
+    }
+    return hipGetLastError();
+}
+
 template <class P>
 hipError_t wg_dispatch(int cin, int cout, int mode, const WgradArgs& a, hipStream_t s) {
+    if constexpr (std::is_same_v<P, PrecBF16>) {
+#define CB_WGT(CI, CO, MD) \
+        if (cin == CI && cout == CO && mode == MD) return wg_tr_launch<CI, CO, MD>(a, s);
+        CB_WGT(4, 16, IN_U8) CB_WGT(4, 32, IN_U8) CB_WGT(4, 64, IN_U8)
+        CB_WGT(16, 16, IN_PLAIN) CB_WGT(16, 32, IN_PLAIN) CB_WGT(16, 64, IN_PLAIN) CB_WGT(32, 32, IN_PLAIN)
+        CB_WGT(16, 16, IN_RELU) CB_WGT(32, 32, IN_RELU)
+#undef CB_WGT
+    }
 #define CB_WG(CI, CO, MD) \
     if (cin == CI && cout == CO && mode == MD) return wg_launch<P, CI, CO, MD>(a, s);
     CB_WG(4, 16, IN_U8) CB_WG(4, 32, IN_U8) CB_WG(4, 64, IN_U8)
@@ -361,7 +689,11 @@ bool wgrad_supported(int cin, int cout, int mode) {
 }
 
 size_t wgrad_partial_floats(int prec, int cin, int cout, int H, int W) {
-    (void)prec; (void)H; (void)W;
+    (void)H; (void)W;
+    if (prec == BF16 && wg_tr_ok(cin, cout)) {
+        const size_t ps = wg_tr_pstride(cin, cout);
+        return size_t(wg_tr_parts_cap(ps)) * ps;
+    }
     const size_t ncol = size_t(3 * cin + 15) / 16 * 16;
     const size_t pst = 3 * size_t(cout) * ncol + cout;
     return size_t(wg_parts_cap(int(pst))) * pst;
