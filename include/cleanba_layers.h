@@ -34,6 +34,17 @@ impala_status_t impala_conv3x3_fwd(impala_prec_t prec, int64_t n, int32_t H, int
                                    const int32_t* row_idx, const float* w, const float* bias,
                                    const void* add, void* y, hipStream_t stream);
 
+/* A stage's entry (conv, then max-pool; Section 5's IMPALA-ResNet) in one pass, bf16 only:
+ * y = maxpool3x3s2_same(conv3x3_same(X, w) + bias), arg as impala_maxpool_fwd. The
+ * full-resolution conv output is rounded to bf16 and pooled without being stored, so y and
+ * arg equal those of impala_conv3x3_fwd followed by impala_maxpool_fwd.
+ * x_mode: IMPALA_X_PLAIN or IMPALA_X_U8. x: [n, H, W, cin]; y (bf16) and arg (uint8):
+ * [n, ceil(H/2), ceil(W/2), cout]. IMPALA_PREC_FP32 returns IMPALA_EUNSUPPORTED. */
+impala_status_t impala_conv3x3_pool_fwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W,
+                                        int32_t cin, int32_t cout, const void* x, int32_t x_mode,
+                                        const int32_t* row_idx, const float* w, const float* bias,
+                                        void* y, uint8_t* arg, hipStream_t stream);
+
 /* Input gradient of y = conv3x3_same(x, w): dx = conv3x3_same^T(dy, w), then
  * dx *= (mask > 0) if mask is not NULL, then dx += add if add is not NULL.
  * dy: [n, H, W, cout]; mask, add, dx: [n, H, W, cin]. */
@@ -55,7 +66,7 @@ impala_status_t impala_conv3x3_wgrad(impala_prec_t prec, int64_t n, int32_t H, i
 
 /* 3x3 stride-2 SAME max-pool with XLA's padding split (pad_lo = P/2) and -inf padding.
  * x: [n, H, W, C]; y: [n, ceil(H/2), ceil(W/2), C]; arg: uint8, same shape as y, the
- * row-major window index 0..8 of the first maximum. C % 4 == 0. */
+ * row-major window index 0..8 of the first maximum. C % 4 == 0, C <= 256. */
 impala_status_t impala_maxpool_fwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t C,
                                    const void* x, void* y, uint8_t* arg, hipStream_t stream);
 

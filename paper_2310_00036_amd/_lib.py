@@ -67,6 +67,8 @@ _SIGS = {
                                C.POINTER(_I32), _P, _P, _SZ, _P, _P]),
     "impala_actor_step": (C.c_int, [_NETP, C.c_int, _P, _P, _I64, _P, _P, _SZ, _P, _P, _P, _P, _P]),
     "impala_conv3x3_fwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _I32, _P, _I32, _P, _P, _P, _P, _P, _P]),
+    "impala_conv3x3_pool_fwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _I32, _P, _I32, _P, _P, _P, _P, _P,
+                                          _P]),
     "impala_conv3x3_dgrad": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P]),
     "impala_conv3x3_wgrad_workspace_bytes": (_SZ, [C.c_int, _I32, _I32, _I32, _I32]),
     "impala_conv3x3_wgrad": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _I32, _P, _I32, _P, _P, _P, _P,
@@ -264,6 +266,12 @@ def impala_actor_step(net, prec, params, obs, n, gumbel, ws, actions, logp, valu
 def impala_conv3x3_fwd(prec, n, H, W, cin, cout, x, x_mode, row_idx, w, bias, add, y, stream=None):
     _check("impala_conv3x3_fwd", lib.impala_conv3x3_fwd(
         prec, n, H, W, cin, cout, ptr(x), x_mode, ptr(row_idx), ptr(w), ptr(bias), ptr(add), ptr(y),
+        stream_handle(stream)))
+
+
+def impala_conv3x3_pool_fwd(prec, n, H, W, cin, cout, x, x_mode, row_idx, w, bias, y, arg, stream=None):
+    _check("impala_conv3x3_pool_fwd", lib.impala_conv3x3_pool_fwd(
+        prec, n, H, W, cin, cout, ptr(x), x_mode, ptr(row_idx), ptr(w), ptr(bias), ptr(y), ptr(arg),
         stream_handle(stream)))
 
 

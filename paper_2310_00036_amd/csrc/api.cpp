@@ -474,6 +474,24 @@ impala_status_t impala_conv3x3_fwd(impala_prec_t prec, int64_t n, int32_t H, int
     return hip_status(conv3x3(prec, cin, cout, x_mode, 0, a, stream), "impala_conv3x3_fwd");
 }
 
+impala_status_t impala_conv3x3_pool_fwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t cin,
+                                        int32_t cout, const void* x, int32_t x_mode,
+                                        const int32_t* row_idx, const float* w, const float* bias,
+                                        void* y, uint8_t* arg, hipStream_t stream) {
+    impala_status_t st = check_layer(__func__, prec, n, H, W, cin, cout);
+    if (st) return st;
+    if (prec != IMPALA_PREC_BF16)
+        return fail(IMPALA_EUNSUPPORTED, "impala_conv3x3_pool_fwd: bf16 only (float32: conv, then max-pool)");
+    if ((x_mode != IN_U8 && x_mode != IN_PLAIN) || !conv3x3_supported(cin, cout, x_mode, 0))
+        return fail(IMPALA_EUNSUPPORTED, "impala_conv3x3_pool_fwd: unsupported cin=%d cout=%d x_mode=%d", cin, cout, x_mode);
+    if (n == 0) return ok();
+    CHECK_PTR(x); CHECK_PTR(w); CHECK_PTR(y); CHECK_PTR(arg);
+    ConvArgs a{};
+    a.x = x; a.row_idx = x_mode == IN_U8 ? row_idx : nullptr; a.w = w; a.bias = bias;
+    a.y = y; a.arg = arg; a.n = int(n); a.H = H; a.W = W; a.scale = x_mode == IN_U8 ? 1.f / 255.f : 1.f;
+    return hip_status(conv3x3_pool(cin, cout, x_mode, a, stream), "impala_conv3x3_pool_fwd");
+}
+
 impala_status_t impala_conv3x3_dgrad(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t cin,
                                      int32_t cout, const void* dy, const float* w, const void* mask,
                                      const void* add, void* dx, hipStream_t stream) {
@@ -523,7 +541,7 @@ impala_status_t impala_maxpool_fwd(impala_prec_t prec, int64_t n, int32_t H, int
                                    const void* x, void* y, uint8_t* arg, hipStream_t stream) {
     impala_status_t st = check_layer(__func__, prec, n, H, W, C, C);
     if (st) return st;
-    if (C < 4 || C % 4) return fail(IMPALA_EUNSUPPORTED, "impala_maxpool_fwd: C must be a multiple of 4");
+    if (C < 4 || C % 4 || C > 256) return fail(IMPALA_EUNSUPPORTED, "impala_maxpool_fwd: C must be a multiple of 4 up to 256");
     if (n == 0) return ok();
     CHECK_PTR(x); CHECK_PTR(y); CHECK_PTR(arg);
     return hip_status(maxpool_fwd(prec, int(n), H, W, C, x, y, arg, stream), "impala_maxpool_fwd");
@@ -533,7 +551,7 @@ impala_status_t impala_maxpool_bwd(impala_prec_t prec, int64_t n, int32_t H, int
                                    const uint8_t* arg, const void* dy, void* dx, hipStream_t stream) {
     impala_status_t st = check_layer(__func__, prec, n, H, W, C, C);
     if (st) return st;
-    if (C < 4 || C % 4) return fail(IMPALA_EUNSUPPORTED, "impala_maxpool_bwd: C must be a multiple of 4");
+    if (C < 4 || C % 4 || C > 256) return fail(IMPALA_EUNSUPPORTED, "impala_maxpool_bwd: C must be a multiple of 4 up to 256");
     if (n == 0) return ok();
     CHECK_PTR(arg); CHECK_PTR(dy); CHECK_PTR(dx);
     return hip_status(maxpool_bwd(prec, int(n), H, W, C, arg, dy, dx, stream), "impala_maxpool_bwd");

@@ -26,7 +26,12 @@ CB_DEV float bf2f(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
 // float -> bf16, round to nearest even (NaN stays NaN): gfx950 converts natively.
 CB_DEV uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f)); }
 
-CB_DEV uint32_t pack2bf(float a, float b) { return uint32_t(f2bf(a)) | (uint32_t(f2bf(b)) << 16); }
+typedef __bf16 cb_bf16x2 __attribute__((ext_vector_type(2)));
+typedef float cb_f32x2 __attribute__((ext_vector_type(2)));
+// Two floats -> two bf16 (a in the low half) in one packed conversion.
+CB_DEV uint32_t pack2bf(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(cb_f32x2{a, b}, cb_bf16x2));
+}
 
 // ---------------------------------------------------------------- precision traits
 //
@@ -97,8 +102,8 @@ CB_DEV __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint32_t bytes) {
 }
 constexpr uint32_t kOOB = 0x80000000u;   // past every resource the launcher allows
 
-// floor(q / d) for 0 <= q < 2^20, given inv = 1.0f / d: the error of the product stays below
-// the distance from (q + 0.5) / d to the nearest integer.
+// floor(q / d) for 0 <= q < 2^22, given inv = 1.0f / d: the relative error of the product
+// (at most 2^-23) stays below the distance from (q + 0.5) / d to the nearest integer.
 CB_DEV int qdiv(int q, float inv) { return int((float(q) + 0.5f) * inv); }
 
 typedef short cb_s16x2 __attribute__((ext_vector_type(2)));
@@ -116,6 +121,11 @@ CB_DEV void dma4_to_lds(__amdgpu_buffer_rsrc_t r, unsigned char* lds, uint32_t o
 CB_DEV void dma16_to_lds(__amdgpu_buffer_rsrc_t r, unsigned char* lds, uint32_t off) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_t*)(lds), 16, off, 0, 0, 0);
 }
+
+// Order-preserving 16-bit keys of two packed bf16 values: as unsigned integers the keys
+// compare like the values (-0 sorts just below +0; NaNs sort beyond the infinities).
+CB_DEV uint32_t bf16x2_key(uint32_t u) { return u ^ ((((u >> 15) & 0x10001u) * 0x7fffu) | 0x80008000u); }
+CB_DEV uint32_t bf16x2_unkey(uint32_t k) { return k ^ (((((~k) >> 15) & 0x10001u) * 0x7fffu) | 0x80008000u); }
 
 typedef short cb_s16x4 __attribute__((ext_vector_type(4)));
 // LDS transpose read of 16-bit data (ds_read_b64_tr_b16). Every lane addresses an 8-byte

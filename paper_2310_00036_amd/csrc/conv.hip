@@ -287,23 +287,32 @@ struct DmaTile {
     int TH, FR, nbands, ntiles, cout_total;
     int win_off, mask_off, add_off;   // LDS byte offsets of the regions
     float inv_W, inv_TW, inv_TH, inv_TR;
+    // fused max-pool: PTH pooled rows per band, pooled size OH x OW, pads ph/pw, conv tile
+    int PTH, OH, OW, ph, pw, ct_off;
+    float inv_OW, inv_ppf;   // 1/OW, 1/(OH*OW)
 };
 
 template <int CIN, int COUT, int MODE>
 struct DmaGeom {
     using G = ConvGeom<PrecBF16, CIN>;
     static constexpr bool U8 = MODE == IN_U8;
-    static constexpr int SPP = U8 ? 1 : CIN / 8 + 1;   // LDS slots per window pixel
-    static constexpr int SB = U8 ? 4 : 16;             // bytes per slot (one DMA lane)
-    static constexpr int PB = SPP * SB;                // bytes per window pixel
+    static constexpr int SPP = U8 ? 1 : CIN / 8 + 1;   // 16-byte LDS slots per bf16 window pixel
+    static constexpr int PB = U8 ? 8 : SPP * 16;       // bytes per (bf16) window pixel
     static constexpr int OCH = COUT / 8;               // 16-byte operand slots per pixel
     static constexpr int WLB = (COUT * G::KPITCH * 2 + 15) / 16 * 16;
-    static int blocks(int slots) { return (slots + 63) / 64; }
-    static int win_bytes(int TH, int FR, int W) { return blocks(FR * (TH + 2) * (W + 2) * SPP) * 64 * SB; }
-    static int op_bytes(int TH, int FR, int W) { return blocks(FR * TH * W * OCH) * 64 * 16; }
+    __host__ __device__ static int blocks(int slots) { return (slots + 63) / 64; }
+    // bf16 window; uint8 frames also stage their raw bytes (4 per pixel) right after it
+    __host__ __device__ static int bf_bytes(int TH, int FR, int W) {
+        const int wp = FR * (TH + 2) * (W + 2);
+        return U8 ? (wp * 8 + 15) / 16 * 16 : blocks(wp * SPP) * 1024;
+    }
+    __host__ __device__ static int win_bytes(int TH, int FR, int W) {
+        return bf_bytes(TH, FR, W) + (U8 ? blocks(FR * (TH + 2) * (W + 2)) * 256 : 0);
+    }
+    __host__ __device__ static int op_bytes(int TH, int FR, int W) { return blocks(FR * TH * W * OCH) * 64 * 16; }
 };
 
-template <int CIN, int COUT, int MODE, int FLIP>
+template <int CIN, int COUT, int MODE, int FLIP, int POOL>
 __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t) {
     using D = DmaGeom<CIN, COUT, MODE>;
     using G = ConvGeom<PrecBF16, CIN>;
@@ -318,6 +327,7 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
     extern __shared__ __align__(16) unsigned char smem[];
     uint16_t* wl = reinterpret_cast<uint16_t*>(smem);
     unsigned char* win = smem + t.win_off;
+    unsigned char* raw = win + D::bf_bytes(t.TH, t.FR, a.W);   // uint8 frames only
     unsigned char* opm = smem + t.mask_off;
     unsigned char* opa = smem + t.add_off;
 
@@ -381,10 +391,23 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
 
     for (int tile = lg; tile < t.ntiles; tile += gridDim.x) {
         const int band = tile % t.nbands, fg = tile / t.nbands;
-        const int h0 = band * TH, f0 = fg * FR;
+        const int f0 = fg * FR;
         const int nf = a.n - f0 < FR ? a.n - f0 : FR;
-        const int the = H - h0 < TH ? H - h0 : TH;
+        // conv rows [h0, h0 + the): a band of TH rows, or (fused pool) exactly the rows the
+        // band's pooled rows [p0, p1) read
+        int h0, the, p0 = 0, p1 = 0;
+        if constexpr (POOL) {
+            p0 = band * t.PTH;
+            p1 = p0 + t.PTH < t.OH ? p0 + t.PTH : t.OH;
+            h0 = 2 * p0 - t.ph > 0 ? 2 * p0 - t.ph : 0;
+            const int h1 = 2 * (p1 - 1) - t.ph + 3;
+            the = (h1 < H ? h1 : H) - h0;
+        } else {
+            h0 = band * TH;
+            the = H - h0 < TH ? H - h0 : TH;
+        }
         const int npx = nf * the * W;   // FR > 1 only when a band is the whole frame
+        uint16_t* ybase = static_cast<uint16_t*>(a.y) + (int64_t(f0) * H + h0) * W * t.cout_total + og;
         __syncthreads();   // the previous tile's LDS reads are done
 
         // ---- stage window (and operands) HBM -> LDS
@@ -400,7 +423,7 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
                     const int rr = qdiv(j, t.inv_TW), col = j - rr * TW, h = h0 + rr - 1;
                     if (col >= 1 && col <= W && h >= 0 && h < H) off = (uint32_t(h) * W + col - 1) * 4;
                 }
-                dma4_to_lds(rx, win + b * 256, off);
+                dma4_to_lds(rx, raw + b * 256, off);
             }
         } else {
             const uint32_t fb = uint32_t(H) * W * CIN * 2;
@@ -440,7 +463,12 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
         }
         __builtin_amdgcn_s_waitcnt(0);   // this wave's loads have landed in LDS
         __syncthreads();                 // ... and everyone else's
-        if constexpr (MODE == IN_RELU) {
+        if constexpr (U8) {
+            // frames -> bf16 once per pixel (4 channels, exact for 0..255)
+            for (int p = tid; p < TR * TW; p += 256)
+                *reinterpret_cast<uint2*>(win + p * 8) = u8x4_to_bf16(*reinterpret_cast<const uint32_t*>(raw + p * 4));
+            __syncthreads();
+        } else if constexpr (MODE == IN_RELU) {
             uint4* w4 = reinterpret_cast<uint4*>(win);
             const int ns = FR * TR * TW * SPP;
             for (int j = tid; j < ns; j += 256) {
@@ -457,7 +485,8 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
             const int q = nt * 16 + r16;
             const int qc = q < npx ? q : npx - 1;
             const int rowi = qdiv(qc, t.inv_W), col = qc - rowi * W;
-            const int f = qdiv(rowi, t.inv_TH), r = rowi - f * TH;
+            int f = 0, r = rowi;
+            if (FR > 1) { f = qdiv(rowi, t.inv_TH); r = rowi - f * TH; }
             const unsigned char* xb = win + ((f * TR + r) * TW + col) * PB;
             cb_f32x4 acc[MT];
 #pragma unroll
@@ -467,11 +496,11 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
                 uint4 b;
                 if constexpr (U8) {
                     if (ks == 0) {
-                        const uint2 lo = u8x4_to_bf16(*reinterpret_cast<const uint32_t*>(xb + u0));
-                        const uint2 hi = u8x4_to_bf16(*reinterpret_cast<const uint32_t*>(xb + u1));
+                        const uint2 lo = *reinterpret_cast<const uint2*>(xb + u0);
+                        const uint2 hi = *reinterpret_cast<const uint2*>(xb + u1);
                         b = make_uint4(lo.x, lo.y, hi.x, hi.y);
                     } else {
-                        const uint2 lo = u8x4_to_bf16(*reinterpret_cast<const uint32_t*>(xb + u2));
+                        const uint2 lo = *reinterpret_cast<const uint2*>(xb + u2);
                         b = g == 0 ? make_uint4(lo.x, lo.y, 0, 0) : make_uint4(0, 0, 0, 0);
                     }
                 } else {
@@ -485,9 +514,20 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
                     acc[mt] = P::mma(af, b, acc[mt]);
                 }
             }
-            if (q < npx) {
-                const int64_t pix = (int64_t(f0 + f) * H + h0 + r) * W + col;
-                uint16_t* yp = static_cast<uint16_t*>(a.y) + pix * t.cout_total + og + g * 4;
+            if (POOL && q < npx) {
+                // the bf16 conv value as an order-preserving 16-bit key (pool compares keys)
+                unsigned char* cp = smem + t.ct_off + (q * COUT + g * 4) * 2;
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    float v[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) v[j] = acc[mt][j] * a.scale + bias[mt][j];
+                    *reinterpret_cast<uint2*>(cp + mt * 32) =
+                        make_uint2(bf16x2_key(pack2bf(v[0], v[1])), bf16x2_key(pack2bf(v[2], v[3])));
+                }
+            } else if (q < npx) {
+                // 32-bit offset from the tile's first output element (the launcher bounds FR frames)
+                uint16_t* yp = ybase + ((uint32_t(f) * H + r) * W + col) * uint32_t(t.cout_total) + g * 4;
                 const int oq = (q * COUT + g * 4) * 2;
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
@@ -508,6 +548,58 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
                     }
                     store4(yp + mt * 16, v[0], v[1], v[2], v[3]);
                 }
+            }
+        }
+
+        if constexpr (POOL) {
+            // ---- 3x3 stride-2 max-pool of the conv tile, 8 channels per item. Per channel the
+            // candidate (key << 16) | (15 - k) of window cell k (row-major 0..8) is maximised as an
+            // integer: the largest key wins and, among equal keys, the first cell. Padded cells
+            // are skipped, so they never win.
+            __syncthreads();
+            constexpr int C8 = COUT / 8;
+            const int prows = p1 - p0;
+            const int ppf = prows * t.OW;
+            const int items = nf * ppf * C8;
+            const unsigned char* ct = smem + t.ct_off;
+            uint16_t* pbase = static_cast<uint16_t*>(a.y) + (int64_t(f0) * t.OH + p0) * t.OW * t.cout_total + og;
+            uint8_t* abase = a.arg + (int64_t(f0) * t.OH + p0) * t.OW * t.cout_total + og;
+            for (int it = tid; it < items; it += 256) {
+                const int c8 = it % C8, pp = it / C8;
+                const int f = FR > 1 ? qdiv(pp, t.inv_ppf) : 0;
+                const int rem = pp - f * ppf;
+                const int ohl = qdiv(rem, t.inv_OW), ow = rem - ohl * t.OW, oh = p0 + ohl;
+                uint32_t best[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) best[j] = 0u;
+#pragma unroll
+                for (int dy = 0; dy < 3; ++dy) {
+                    const int h = 2 * oh + dy - t.ph;
+                    if (h < 0 || h >= H) continue;
+#pragma unroll
+                    for (int dx = 0; dx < 3; ++dx) {
+                        const int w = 2 * ow + dx - t.pw;
+                        if (w < 0 || w >= W) continue;
+                        const uint4 k4 = *reinterpret_cast<const uint4*>(ct + (((f * TH + h - h0) * W + w) * COUT + c8 * 8) * 2);
+                        const uint32_t tag = 15u - uint32_t(dy * 3 + dx);
+                        const uint32_t kk[4] = {k4.x, k4.y, k4.z, k4.w};
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            best[2 * j] = max(best[2 * j], (kk[j] << 16) | tag);
+                            best[2 * j + 1] = max(best[2 * j + 1], (kk[j] & 0xffff0000u) | tag);
+                        }
+                    }
+                }
+                uint32_t vals[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    vals[j] = bf16x2_unkey((best[2 * j] >> 16) | (best[2 * j + 1] & 0xffff0000u));
+                uint32_t idx[2] = {0u, 0u};
+#pragma unroll
+                for (int j = 0; j < 8; ++j) idx[j >> 2] |= (15u - (best[j] & 15u)) << (8 * (j & 3));
+                const uint32_t o = ((uint32_t(f) * t.OH + ohl) * t.OW + ow) * uint32_t(t.cout_total) + c8 * 8;
+                *reinterpret_cast<uint4*>(pbase + o) = make_uint4(vals[0], vals[1], vals[2], vals[3]);
+                *reinterpret_cast<uint2*>(abase + o) = make_uint2(idx[0], idx[1]);
             }
         }
     }
@@ -623,14 +715,62 @@ hipError_t launch_bf16(const ConvArgs& a, int cout_total, hipStream_t s) {
     t.inv_W = 1.f / float(W); t.inv_TW = 1.f / float(W + 2);
     t.inv_TH = 1.f / float(TH); t.inv_TR = 1.f / float(TH + 2);
     const int groups = cout_total / COUT;
-    const void* fn = reinterpret_cast<const void*>(&conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP>);
+    const void* fn = reinterpret_cast<const void*>(&conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP, 0>);
     int gx = std::max(1, resident_blocks(fn, 256, L) / groups);
     if (gx > ntiles) gx = ntiles;
     const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(groups));
     ProfScope ps(s, [&] {
         return cb_key(FLIP ? "conv_dgrad" : "conv_fwd", 0, cb_dims(CIN, cout_total) + "/" + cb_dims(H, W));
     });
-    hipLaunchKernelGGL((conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP>), grid, dim3(256), L, s, a, t);
+    hipLaunchKernelGGL((conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP, 0>), grid, dim3(256), L, s, a, t);
+    return hipGetLastError();
+}
+
+// Conv + fused max-pool (bf16): bands of PTH pooled rows; each computes the 2*PTH+1 conv
+// rows they read into LDS. Whole frames batch as in launch_bf16.
+template <int CIN, int COUT, int MODE>
+hipError_t launch_bf16_pool(const ConvArgs& a, int cout_total, hipStream_t s) {
+    using D = DmaGeom<CIN, COUT, MODE>;
+    const int H = a.H, W = a.W;
+    const int OH = (H + 1) / 2, OW = (W + 1) / 2;
+    const int PH = (OH - 1) * 2 + 3 - H, PW = (OW - 1) * 2 + 3 - W;
+    auto cap = [&](int pth, int fr) { return fr > 1 || pth >= OH ? H : std::min(2 * pth + 1, H); };
+    auto lds = [&](int pth, int fr) {
+        const int th = cap(pth, fr);
+        return size_t(D::WLB) + size_t(D::win_bytes(th, fr, W)) + size_t(fr) * th * W * COUT * 2;
+    };
+    const size_t limit = std::min<size_t>(lds_limit(), 160 * 1024);
+    int pmax = OH;
+    while (pmax > 1 && (lds(pmax, 1) > size_t(kDmaLdsTarget) || cap(pmax, 1) * W > kDmaPixMax)) --pmax;
+    if (lds(pmax, 1) > limit) return hipErrorInvalidValue;
+    const int nbands0 = (OH + pmax - 1) / pmax;
+    const int PTH = (OH + nbands0 - 1) / nbands0;
+    const int nbands = (OH + PTH - 1) / PTH;
+    int FR = 1;
+    if (nbands == 1 && MODE != IN_U8)
+        while (FR < a.n && lds(PTH, FR + 1) <= size_t(kDmaLdsTarget) && (FR + 1) * H * W <= kDmaPixMax) ++FR;
+    const int TH = cap(PTH, FR);
+    if (int64_t(FR) * H * W * std::max(MODE == IN_U8 ? 2 : CIN, cout_total) * 2 >= (int64_t(1) << 31))
+        return hipErrorInvalidValue;
+    DmaTile t{};
+    t.TH = TH; t.FR = FR; t.nbands = nbands; t.ntiles = nbands * ((a.n + FR - 1) / FR);
+    t.cout_total = cout_total;
+    t.win_off = D::WLB;
+    t.ct_off = t.win_off + D::win_bytes(TH, FR, W);
+    t.mask_off = t.add_off = t.ct_off;
+    t.inv_W = 1.f / float(W); t.inv_TW = 1.f / float(W + 2);
+    t.inv_TH = 1.f / float(TH); t.inv_TR = 1.f / float(TH + 2);
+    t.PTH = PTH; t.OH = OH; t.OW = OW;
+    t.ph = (PH > 0 ? PH : 0) / 2; t.pw = (PW > 0 ? PW : 0) / 2;
+    t.inv_OW = 1.f / float(OW); t.inv_ppf = 1.f / float(OH * OW);
+    const size_t L = lds(PTH, FR);
+    const int groups = cout_total / COUT;
+    const void* fn = reinterpret_cast<const void*>(&conv3x3_bf16_kernel<CIN, COUT, MODE, 0, 1>);
+    int gx = std::max(1, resident_blocks(fn, 256, L) / groups);
+    if (gx > t.ntiles) gx = t.ntiles;
+    const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(groups));
+    ProfScope ps(s, [&] { return cb_key("conv_pool", 0, cb_dims(CIN, cout_total) + "/" + cb_dims(H, W)); });
+    hipLaunchKernelGGL((conv3x3_bf16_kernel<CIN, COUT, MODE, 0, 1>), grid, dim3(256), L, s, a, t);
     return hipGetLastError();
 }
 
@@ -671,6 +811,18 @@ bool conv3x3_supported(int cin, int cout, int mode, int flip) {
     if (mode == IN_U8) return cin == 4 && ch_ok(cout);
     if (mode == IN_RELU) return cin == cout && ch_ok(cin);
     return ch_ok(cin) && ch_ok(cout) && cin <= cout;
+}
+
+hipError_t conv3x3_pool(int cin, int cout, int mode, const ConvArgs& a, hipStream_t s) {
+    if (a.n <= 0) return hipSuccess;
+#define CB_CP(CI, CO, MD) \
+    if (cin == CI && cout == CO && mode == MD) \
+        return launch_bf16_pool<CI, conv_group<PrecBF16, CI, CO>(), MD>(a, CO, s);
+    CB_CP(4, 16, IN_U8) CB_CP(4, 32, IN_U8) CB_CP(4, 64, IN_U8)
+    CB_CP(16, 16, IN_PLAIN) CB_CP(16, 32, IN_PLAIN) CB_CP(16, 64, IN_PLAIN)
+    CB_CP(32, 32, IN_PLAIN) CB_CP(32, 64, IN_PLAIN) CB_CP(64, 64, IN_PLAIN)
+#undef CB_CP
+    return hipErrorInvalidValue;
 }
 
 hipError_t conv3x3(int prec, int cin, int cout, int mode, int flip, const ConvArgs& a,

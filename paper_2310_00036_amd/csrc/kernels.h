@@ -20,7 +20,8 @@ struct ConvArgs {
     const float* bias;      // [cout] or NULL
     const void* add;        // [n, H, W, cout] added after the mask, or NULL
     const void* mask;       // [n, H, W, cout]: output kept where mask > 0, or NULL
-    void* y;                // [n, H, W, cout]
+    void* y;                // [n, H, W, cout] (conv3x3_pool: the pooled [n, OH, OW, cout])
+    uint8_t* arg;           // conv3x3_pool: argmax of each pooled value (0..8), else unused
     int n, H, W;
     float scale;            // multiplies the sum before the bias (1/255 for uint8 frames)
 };
@@ -30,6 +31,9 @@ struct ConvArgs {
 hipError_t conv3x3(int prec, int cin, int cout, int mode, int flip, const ConvArgs& a,
                    hipStream_t s);
 bool conv3x3_supported(int cin, int cout, int mode, int flip);
+// bf16 only: y = maxpool3x3s2(conv(x, w) + b) with its argmax (as maxpool_fwd), the conv
+// output kept in LDS; OH = (H+1)/2, OW = (W+1)/2. Modes IN_U8 and IN_PLAIN.
+hipError_t conv3x3_pool(int cin, int cout, int mode, const ConvArgs& a, hipStream_t s);
 
 // ---- weight gradient of a 3x3 SAME conv (deterministic split over pixels)
 struct WgradArgs {

@@ -86,7 +86,7 @@ NetPlan make_plan(const impala_net_t& net, int prec, int64_t cap, int training) 
         const int64_t conv_el = int64_t(p.H[s]) * p.W[s] * p.C[s + 1];
         const int64_t pool_el = int64_t(p.H[s + 1]) * p.W[s + 1] * p.C[s + 1];
         maxact = std::max(maxact, conv_el);
-        p.c[s] = take(size_t(cap * conv_el) * p.es);
+        p.c[s] = take(prec == BF16 ? 0 : size_t(cap * conv_el) * p.es);   // bf16 pools on chip
         p.idx[s] = take(size_t(cap * pool_el));
         for (int k = 0; k < 3; ++k) p.x[s][k] = take(size_t(cap * pool_el) * p.es);
         for (int k = 0; k < 2; ++k) p.t[s][k] = take(size_t(cap * pool_el) * p.es);
@@ -138,12 +138,19 @@ hipError_t run_forward(const NetPlan& p, const float* params, const uint8_t* obs
         a.row_idx = st == 0 ? row_idx : nullptr;
         a.w = params + po.conv_w[st][0];
         a.bias = params + po.conv_b[st][0];
-        a.y = ws + p.c[st];
         a.n = int(n); a.H = p.H[st]; a.W = p.W[st];
         a.scale = st == 0 ? 1.f / 255.f : 1.f;
-        CB_TRY(conv3x3(p.prec, p.C[st], p.C[st + 1], st == 0 ? IN_U8 : IN_PLAIN, 0, a, s));
-        CB_TRY(maxpool_fwd(p.prec, int(n), p.H[st], p.W[st], p.C[st + 1], ws + p.c[st], ws + p.x[st][0],
-                           reinterpret_cast<uint8_t*>(ws + p.idx[st]), s));
+        if (p.prec == BF16) {
+            // conv and pool in one pass: the full-resolution output stays on chip
+            a.y = ws + p.x[st][0];
+            a.arg = reinterpret_cast<uint8_t*>(ws + p.idx[st]);
+            CB_TRY(conv3x3_pool(p.C[st], p.C[st + 1], st == 0 ? IN_U8 : IN_PLAIN, a, s));
+        } else {
+            a.y = ws + p.c[st];
+            CB_TRY(conv3x3(p.prec, p.C[st], p.C[st + 1], st == 0 ? IN_U8 : IN_PLAIN, 0, a, s));
+            CB_TRY(maxpool_fwd(p.prec, int(n), p.H[st], p.W[st], p.C[st + 1], ws + p.c[st], ws + p.x[st][0],
+                               reinterpret_cast<uint8_t*>(ws + p.idx[st]), s));
+        }
         const int C = p.C[st + 1];
         for (int r = 0; r < 2; ++r) {
             ConvArgs b{};

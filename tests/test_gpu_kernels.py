@@ -70,6 +70,64 @@ def test_conv_forward(case, prec):
         G.assert_sum_close(got, want, absum, 1e-5, "conv fwd")
 
 
+POOL_CASES = [(3, 84, 84, 4, 16, P.X_U8), (2, 84, 84, 4, 32, P.X_U8), (2, 13, 9, 4, 64, P.X_U8),
+              (3, 42, 42, 16, 32, P.X_PLAIN), (2, 42, 42, 16, 16, P.X_PLAIN), (4, 21, 21, 32, 32, P.X_PLAIN),
+              (5, 11, 11, 32, 64, P.X_PLAIN), (2, 17, 23, 16, 64, P.X_PLAIN), (3, 21, 21, 64, 64, P.X_PLAIN)]
+
+
+def _pool_windows(x, fill):
+    """[9, n, OH, OW, C]: the 3x3 stride-2 SAME windows of x, padded cells = fill."""
+    n, h, w, c = x.shape
+    oh, ph0, ph1 = onet.same_pool_pads(h)
+    ow, pw0, pw1 = onet.same_pool_pads(w)
+    xp = np.full((n, h + ph0 + ph1, w + pw0 + pw1, c), fill, np.float64)
+    xp[:, ph0:ph0 + h, pw0:pw0 + w] = x
+    return np.stack(onet._pool_views(xp, oh, ow))
+
+
+@pytest.mark.parametrize("case", POOL_CASES, ids=lambda c: "n%d_%dx%d_%d-%d_m%d" % c)
+def test_conv_pool_forward(case):
+    """Fused conv + max-pool (bf16): the conv output is never stored, so the check works on
+    the exact conv: the pooled value is within 1 bf16 ulp of the exact conv at the chosen
+    cell, that cell is a maximum up to rounding, and wherever the window's maximum is clear
+    by more than 4 ulps the argmax is the oracle's."""
+    n, H, W, cin, cout, mode = case
+    x, rows, xin, w, b = _conv_inputs(n, H, W, cin, cout, mode, G.BF16, 13)
+    wq = G.q(w, G.BF16)
+    conv = onet.conv3x3(xin, wq, b.astype(np.float64))
+    absum = onet.conv3x3(np.abs(xin), np.abs(wq), np.abs(b).astype(np.float64))
+    win, wabs = _pool_windows(conv, -np.inf), _pool_windows(absum, 0.0)
+    OH, OW = win.shape[2:4]
+    torch = G.torch()
+    y = G.empty_act((n, OH, OW, cout), G.BF16)
+    arg = torch.empty((n, OH, OW, cout), dtype=torch.uint8, device="cuda:0")
+    dx = G.dev_u8(x) if mode == P.X_U8 else G.dev_act(x, G.BF16)
+    P.impala_conv3x3_pool_fwd(G.BF16, n, H, W, cin, cout, dx, mode, G.dev_i32(rows) if rows is not None else None,
+                              G.dev_f32(w), G.dev_f32(b), y, arg)
+    G.sync()
+    got_arg = arg.cpu().numpy().astype(np.int64)
+    assert got_arg.max() <= 8
+    sel = np.take_along_axis(win, got_arg[None], 0)[0]
+    assert np.isfinite(sel).all(), "argmax points at a padded cell"
+    G.assert_bf16_ulp(G.host(y), sel, np.take_along_axis(wabs, got_arg[None], 0)[0], "pooled value")
+    best = win.max(0)
+    amax = wabs.max(0)
+    spacing = np.maximum(np.abs(best), 1e-30) * 2.0 ** -7
+    assert (sel >= best - 2 * spacing - 2.0 ** -19 * amax).all(), "argmax is not a maximum"
+    top2 = np.sort(win, 0)[-2:]
+    clear = top2[1] - top2[0] > 4 * spacing + 2.0 ** -18 * amax
+    assert clear.mean() > 0.5
+    np.testing.assert_array_equal(got_arg[clear], win.argmax(0)[clear])
+
+
+@pytest.mark.parametrize("prec", [G.FP32])
+def test_conv_pool_rejects_fp32(prec):
+    with pytest.raises(P.LibraryError):
+        P.impala_conv3x3_pool_fwd(prec, 1, 8, 8, 16, 16, G.dev_act(np.zeros((1, 8, 8, 16)), prec), P.X_PLAIN, None,
+                                  G.dev_f32(np.zeros((3, 3, 16, 16))), None, G.empty_act((1, 4, 4, 16), prec),
+                                  G.torch().empty((1, 4, 4, 16), dtype=G.torch().uint8, device="cuda:0"))
+
+
 DGRAD_CASES = [(3, 42, 42, 16, 16), (3, 42, 42, 16, 32), (4, 21, 21, 32, 32), (7, 11, 11, 32, 32),
                (2, 42, 42, 32, 64), (3, 21, 21, 64, 64), (2, 17, 23, 16, 64)]
 
