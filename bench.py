@@ -39,7 +39,90 @@ def parse():
     ap.add_argument("--prec", default="bf16", choices=["bf16", "fp32"])
     ap.add_argument("--cpu-sample-frames", type=int, default=1024,
                     help="frames in the oracle's timed CPU update (0 skips the CPU baseline)")
+    ap.add_argument("--layer", default=None,
+                    help="replay one profiling key's launch (e.g. conv_dgrad/bf16/32x32/21x21/mask/add) "
+                         "--steps times through the C-ABI on the minibatch size, for counter runs")
+    ap.add_argument("--copy-mb", type=int, default=0,
+                    help="time a plain device copy of this many MiB --steps times (counter calibration)")
     return ap.parse_args()
+
+
+def run_layer(P, key, n, steps):
+    """Launch the layer a profiling key names, `steps` times, on synthetic bf16/uint8 data of
+    the minibatch's shape; prints the average launch time."""
+    import torch
+    parts = key.split("/")
+    fam, prec = parts[0], (P.PREC_BF16 if parts[1] == "bf16" else P.PREC_FP32)
+    dt = torch.bfloat16 if prec == P.PREC_BF16 else torch.float32
+    g = torch.Generator(device="cuda").manual_seed(7)
+    act = lambda h, w, c: (torch.randn(n, h, w, c, device="cuda", generator=g) * 0.5).to(dt)  # noqa: E731
+    if fam in ("pool_fwd", "pool_bwd"):
+        c = int(parts[2])
+        h, w = map(int, parts[3].split("x"))
+        oh, ow = (h + 1) // 2, (w + 1) // 2
+        x, y = act(h, w, c), act(oh, ow, c)
+        arg = torch.randint(0, 9, (n, oh, ow, c), dtype=torch.uint8, device="cuda", generator=g)
+        fn = ((lambda: P.impala_maxpool_fwd(prec, n, h, w, c, x, y, arg)) if fam == "pool_fwd"
+              else (lambda: P.impala_maxpool_bwd(prec, n, h, w, c, arg, y, x)))
+    else:
+        ci, co = map(int, parts[2].split("x"))
+        h, w = map(int, parts[3].split("x"))
+        flags = set(parts[4:])
+        mode = P.X_U8 if "u8" in flags else (P.X_RELU if "relu" in flags else P.X_PLAIN)
+        x = (torch.randint(0, 256, (n, h, w, 4), dtype=torch.uint8, device="cuda", generator=g)
+             if mode == P.X_U8 else act(h, w, ci))
+        if fam == "conv_dgrad":   # key channels: dy (forward cout) x dx (forward cin)
+            wt = torch.randn(3, 3, co, ci, device="cuda", generator=g) * 0.1
+            mask = act(h, w, co) if "mask" in flags else None
+            add = act(h, w, co) if "add" in flags else None
+            out = act(h, w, co)
+            fn = lambda: P.impala_conv3x3_dgrad(prec, n, h, w, co, ci, x, wt, mask, add, out)  # noqa: E731
+        else:
+            wt = torch.randn(3, 3, ci, co, device="cuda", generator=g) * 0.1
+            b = torch.zeros(co, device="cuda")
+            if fam == "conv_fwd":
+                add = act(h, w, co) if "add" in flags else None
+                out = act(h, w, co)
+                fn = lambda: P.impala_conv3x3_fwd(prec, n, h, w, ci, co, x, mode, None, wt, b, add, out)  # noqa: E731
+            elif fam == "conv_pool":
+                oh, ow = (h + 1) // 2, (w + 1) // 2
+                out = act(oh, ow, co)
+                arg = torch.empty((n, oh, ow, co), dtype=torch.uint8, device="cuda")
+                fn = lambda: P.impala_conv3x3_pool_fwd(prec, n, h, w, ci, co, x, mode, None, wt, b, out, arg)  # noqa: E731
+            elif fam == "wgrad":
+                dy = act(h, w, co)
+                dw = torch.empty(3, 3, ci, co, device="cuda")
+                db = torch.empty(co, device="cuda")
+                ws = torch.empty(P.impala_conv3x3_wgrad_workspace_bytes(prec, h, w, ci, co), dtype=torch.uint8,
+                                 device="cuda")
+                fn = lambda: P.impala_conv3x3_wgrad(prec, n, h, w, ci, co, x, mode, None, dy, dw, db, ws)  # noqa: E731
+            else:
+                raise SystemExit(f"--layer: no replay for {key}")
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / steps * 1e3
+    print(json.dumps({"layer": key, "n": n, "launches": steps + 1, "avg_launch_us": round(us, 2)}), flush=True)
+
+
+def run_copy(mb, steps):
+    import torch
+    a = torch.empty(mb << 18, dtype=torch.float32, device="cuda").fill_(1.0)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    print(json.dumps({"copy_mib": mb, "launches": steps + 1, "bytes_read": a.numel() * 4,
+                      "bytes_written": a.numel() * 4, "avg_s": dt}), flush=True)
 
 
 def build_inputs(P, wl, prec):
@@ -86,27 +169,50 @@ def build_inputs(P, wl, prec):
 
 
 def kernel_work(key, n, prec):
-    """(bound, algorithmic amount per launch, unit) for a profiling key.
-    conv_fwd / conv_dgrad / wgrad: 2 * n * H * W * 9 * Cin * Cout FLOP (a 3x3 conv's MACs);
-    gemm: 2 * M * N * K FLOP; adam: 28 bytes per parameter."""
-    fam, _, shape = key.split("/", 2) if key.count("/") >= 2 else (key.split("/")[0], "", key.split("/", 1)[1])
-    if fam in ("conv_fwd", "conv_dgrad", "wgrad"):
-        ch, hw = shape.split("/")
-        cin, cout = map(int, ch.split("x"))
-        h, w = map(int, hw.split("x"))
-        return "mfma", 2.0 * n * h * w * 9 * cin * cout, "FLOP"
+    """(bound, algorithmic amount per launch, unit, flop) for a profiling key.
+
+    The convolution family is bound by HBM at these channel counts (9 * Cin * Cout * 2 flop
+    per pixel against (Cin + Cout) * 2 bytes: 72-144 flop/byte, below the bf16 ridge of
+    2500 / 8 = 312), so its amount is the bytes it must move once: the input (1 byte per
+    channel for uint8 frames), the output and any mask / residual operand; a fused conv +
+    pool stores the pooled output and its uint8 argmax; a weight gradient reads x and dy.
+    Pools move their input, output and argmax; adam 28 bytes per parameter. gemm is counted
+    in flop against the matrix-core peak. `flop` is the MFMA work (None if none)."""
+    parts = key.split("/")
+    fam = parts[0]
+    es = 2 if len(parts) > 1 and parts[1] == "bf16" else 4
+    if fam in ("conv_fwd", "conv_dgrad", "wgrad", "conv_pool"):
+        ci, co = map(int, parts[2].split("x"))
+        h, w = map(int, parts[3].split("x"))
+        flags = set(parts[4:])
+        xb = 1 if "u8" in flags else es
+        px = n * h * w
+        flop = 2.0 * px * 9 * ci * co
+        if fam == "wgrad":
+            b = px * (ci * xb + co * es)
+        elif fam == "conv_pool":
+            oh, ow = (h + 1) // 2, (w + 1) // 2
+            b = px * ci * xb + n * oh * ow * co * (es + 1)
+        else:
+            b = px * (ci * xb + co * es * (1 + ("mask" in flags) + ("add" in flags)))
+        return "hbm", float(b), "B", flop
+    if fam in ("pool_fwd", "pool_bwd"):
+        c = int(parts[2])
+        h, w = map(int, parts[3].split("x"))
+        oh, ow = (h + 1) // 2, (w + 1) // 2
+        return "hbm", float(n * (h * w * c * es + oh * ow * c * (es + 1))), "B", None
     if fam == "gemm":
-        m, nn, k = map(int, shape.split("x"))
-        return "mfma", 2.0 * m * nn * k, "FLOP"
+        m, nn, k = map(int, parts[2].split("x"))
+        return "mfma", 2.0 * m * nn * k, "FLOP", 2.0 * m * nn * k
     if fam == "adam":
-        return "hbm", 28.0 * int(shape), "B"
-    return None, None, None
+        return "hbm", 28.0 * int(parts[2]), "B", None
+    return None, None, None, None
 
 
 def source_digest(key):
     fam = key.split("/")[0]
-    src = {"conv_fwd": "conv.hip", "conv_dgrad": "conv.hip", "wgrad": "wgrad.hip", "gemm": "gemm.hip",
-           "adam": "adam.hip"}.get(fam)
+    src = {"conv_fwd": "conv.hip", "conv_dgrad": "conv.hip", "conv_pool": "conv.hip", "wgrad": "wgrad.hip",
+           "gemm": "gemm.hip", "adam": "adam.hip", "pool_fwd": "pool.hip", "pool_bwd": "pool.hip"}.get(fam)
     if not src:
         return None
     path = os.path.join(ROOT, "paper_2310_00036_amd", "csrc", src)
@@ -167,6 +273,10 @@ def main():
     from synth import WORKLOADS
 
     wl = WORKLOADS[args.workload]
+    if args.copy_mb:
+        return run_copy(args.copy_mb, args.steps)
+    if args.layer:
+        return run_layer(P, args.layer, wl.mb, args.steps)
     prec = P.PREC_BF16 if args.prec == "bf16" else P.PREC_FP32
     net = wl.net
     params, ro, perm = build_inputs(P, wl, prec)
@@ -213,7 +323,7 @@ def main():
     ms_per_step = gpu_ms / args.steps
     value = frames_per_step * args.steps / (gpu_ms / 1e3)
 
-    bound, work, unit = kernel_work(dominant[0], mb, args.prec)
+    bound, work, unit, flop = kernel_work(dominant[0], mb, args.prec)
     avg_s = kms / kcnt / 1e3
     if bound == "mfma":
         achieved = work / avg_s / 1e12
@@ -221,6 +331,7 @@ def main():
     else:
         achieved = work / avg_s / 1e9
         peak, punit = PEAK["hbm"]
+    mfma_tflops = flop / avg_s / 1e12 if flop else None
     traffic = traffic_for(dominant[0], dominant[2])
     line = {
         "metric": "learner frames/sec (fwd+bwd+loss+Adam), IMPALA-CNN; % MFMA peak",
@@ -245,7 +356,9 @@ def main():
                      "unit": punit, "frac": round(achieved / peak, 4),
                      "avg_launch_us": round(avg_s * 1e6, 2), "launches_timed": kcnt,
                      "share_of_step": round(dominant[1] / profiled_total, 3) if profiled_total else None,
-                     "traffic": traffic},
+                     "traffic": traffic, "algorithmic_bytes": work if unit == "B" else None,
+                     "mfma_tflops": round(mfma_tflops, 2) if mfma_tflops else None,
+                     "mfma_frac": round(mfma_tflops / PEAK[args.prec][0], 4) if mfma_tflops else None},
         "kernels_top": [{"key": k, "ms_per_step": round(t, 3), "launches": c} for k, t, c in table[:8]],
     }
     if args.cpu_sample_frames > 0:

@@ -14,6 +14,16 @@ inline std::string cb_key(const char* family, int prec, const std::string& shape
     return std::string(family) + (prec == 0 ? "/bf16/" : "/fp32/") + shape;
 }
 inline std::string cb_dims(int a, int b) { return std::to_string(a) + "x" + std::to_string(b); }
+// Key suffix naming what a conv-family launch moves besides x and y: uint8 frames or a relu
+// on load (mode 2 / 1), and the mask / residual operands of its epilogue.
+inline std::string cb_flags(int mode, bool mask, bool add) {
+    std::string f;
+    if (mode == 2) f += "/u8";
+    if (mode == 1) f += "/relu";
+    if (mask) f += "/mask";
+    if (add) f += "/add";
+    return f;
+}
 
 typedef __bf16 cb_bf16x8 __attribute__((ext_vector_type(8)));
 typedef float cb_f32x4 __attribute__((ext_vector_type(4)));

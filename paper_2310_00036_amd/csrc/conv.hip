@@ -661,7 +661,7 @@ hipError_t launch(const ConvArgs& a, int cout_total, hipStream_t s) {
     const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(groups));
     ProfScope ps(s, [&] {
         return cb_key(FLIP ? "conv_dgrad" : "conv_fwd", sizeof(typename P::T) == 2 ? 0 : 1,
-                      cb_dims(CIN, cout_total) + "/" + cb_dims(H, W));
+                      cb_dims(CIN, cout_total) + "/" + cb_dims(H, W) + cb_flags(MODE, a.mask, a.add));
     });
     hipLaunchKernelGGL((conv3x3_kernel<P, CIN, COUT, MODE, FLIP>), grid, dim3(256), lds, s, a, TH,
                        FR, nbands, ntiles, cout_total);
@@ -720,7 +720,8 @@ hipError_t launch_bf16(const ConvArgs& a, int cout_total, hipStream_t s) {
     if (gx > ntiles) gx = ntiles;
     const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(groups));
     ProfScope ps(s, [&] {
-        return cb_key(FLIP ? "conv_dgrad" : "conv_fwd", 0, cb_dims(CIN, cout_total) + "/" + cb_dims(H, W));
+        return cb_key(FLIP ? "conv_dgrad" : "conv_fwd", 0,
+                      cb_dims(CIN, cout_total) + "/" + cb_dims(H, W) + cb_flags(MODE, a.mask, a.add));
     });
     hipLaunchKernelGGL((conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP, 0>), grid, dim3(256), L, s, a, t);
     return hipGetLastError();
@@ -769,7 +770,9 @@ hipError_t launch_bf16_pool(const ConvArgs& a, int cout_total, hipStream_t s) {
     int gx = std::max(1, resident_blocks(fn, 256, L) / groups);
     if (gx > t.ntiles) gx = t.ntiles;
     const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(groups));
-    ProfScope ps(s, [&] { return cb_key("conv_pool", 0, cb_dims(CIN, cout_total) + "/" + cb_dims(H, W)); });
+    ProfScope ps(s, [&] {
+        return cb_key("conv_pool", 0, cb_dims(CIN, cout_total) + "/" + cb_dims(H, W) + cb_flags(MODE, false, false));
+    });
     hipLaunchKernelGGL((conv3x3_bf16_kernel<CIN, COUT, MODE, 0, 1>), grid, dim3(256), L, s, a, t);
     return hipGetLastError();
 }

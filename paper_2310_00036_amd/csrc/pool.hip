@@ -6,8 +6,8 @@
 // 2x2) windows whose argmax it is, in a fixed order -- no atomics.
 //
 // One thread handles VEC consecutive channels (8 in bf16 when the channel count allows, else
-// 4) of one output (forward) or input (backward) cell; grid rows are frames, so in-frame
-// indices stay 32-bit and divide exactly by a reciprocal multiply. These kernels are bound by
+// 4) of one output cell (forward) or of a 2x2 block of input cells (backward); grid rows are
+// frames, so in-frame indices stay 32-bit and divide exactly by a reciprocal multiply. These kernels are bound by
 // vector-ALU issue as much as by HBM, so the index math is kept minimal.
 #include "common.h"
 #include "kernels.h"
@@ -16,7 +16,7 @@ namespace cb {
 
 struct PoolGeom {
     int H, W, C, OH, OW, ph, pw, CG;   // CG = C / VEC channel groups
-    float inv_CG, inv_W, inv_OW;
+    float inv_CG, inv_W, inv_OW, inv_BW;   // inv_BW = 1 / ceil((W + pw) / 2)
 };
 
 static inline PoolGeom pool_geom(int H, int W, int C, int vec) {
@@ -28,6 +28,7 @@ static inline PoolGeom pool_geom(int H, int W, int C, int vec) {
     g.pw = (PW > 0 ? PW : 0) / 2;
     g.CG = C / vec;
     g.inv_CG = 1.f / float(g.CG); g.inv_W = 1.f / float(W); g.inv_OW = 1.f / float(g.OW);
+    g.inv_BW = 1.f / float((W + g.pw + 1) / 2);
     return g;
 }
 
@@ -93,40 +94,75 @@ __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const T* __restrict__ 
     else *reinterpret_cast<uint32_t*>(arg + fo + o) = a[0];
 }
 
+// Backward as a gather over 2x2 input blocks: block (i, j) holds the cells with padded
+// coordinates (2i + a, 2j + b), a, b in {0, 1}, and only the windows (i-1 | i, j-1 | j) reach
+// it (window (oh, ow) covers padded rows 2oh..2oh+2 and columns 2ow..2ow+2). Every lane runs
+// the same four windows, so nothing diverges; each cell adds its windows in (oh, ow) order.
 template <class T, int VEC>
 __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const uint8_t* __restrict__ arg,
                                                           const T* __restrict__ dy,
                                                           T* __restrict__ dx, PoolGeom g) {
+    const int BH = (g.H + g.ph + 1) >> 1, BW = (g.W + g.pw + 1) >> 1;
     const int t = blockIdx.x * 256 + threadIdx.x;
-    if (t >= g.H * g.W * g.CG) return;
-    const int q = qdiv(t, g.inv_CG), c = (t - q * g.CG) * VEC;
-    const int h = qdiv(q, g.inv_W), w = q - h * g.W;
+    if (t >= BH * BW * g.CG) return;
+    const int blk = qdiv(t, g.inv_CG), c = (t - blk * g.CG) * VEC;
+    const int i = qdiv(blk, g.inv_BW), j = blk - i * BW;
     const int64_t n = blockIdx.y;
-    const int64_t fo = n * g.OH * g.OW * g.C;
-    const uint8_t* af = arg + fo + c;
-    const T* df = dy + fo + c;
-    float acc[VEC];
+    const uint8_t* af = arg + n * g.OH * g.OW * g.C + c;
+    const T* df = dy + n * g.OH * g.OW * g.C + c;
+    float a00[VEC], a01[VEC], a10[VEC], a11[VEC];
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
-    // windows oh with oh*2 - ph <= h <= oh*2 - ph + 2 (one or two per axis)
-    const int hp = h + g.ph, wp = w + g.pw;
-    const int oh_lo = hp >= 2 ? (hp - 1) >> 1 : 0, oh_hi = (hp >> 1) < g.OH - 1 ? hp >> 1 : g.OH - 1;
-    const int ow_lo = wp >= 2 ? (wp - 1) >> 1 : 0, ow_hi = (wp >> 1) < g.OW - 1 ? wp >> 1 : g.OW - 1;
-    for (int oh = oh_lo; oh <= oh_hi; ++oh) {
-        for (int ow = ow_lo; ow <= ow_hi; ++ow) {
-            const uint32_t k = uint32_t((hp - oh * 2) * 3 + (wp - ow * 2));
-            const uint32_t o = uint32_t(oh * g.OW + ow) * g.C;
-            uint32_t a4[VEC / 4];
-            if constexpr (VEC == 8) { const uint2 u = *reinterpret_cast<const uint2*>(af + o); a4[0] = u.x; a4[1] = u.y; }
-            else a4[0] = *reinterpret_cast<const uint32_t*>(af + o);
-            float v[VEC];
-            loadv<T, VEC>(df + o, v);
+    for (int e = 0; e < VEC; ++e) { a00[e] = 0.f; a01[e] = 0.f; a10[e] = 0.f; a11[e] = 0.f; }
+    auto window = [&](int oh, int ow, uint8_t* k, float* v) {
+        const uint32_t o = uint32_t(oh * g.OW + ow) * g.C;
+        if constexpr (VEC == 8) {
+            const uint2 u = *reinterpret_cast<const uint2*>(af + o);
+            const uint32_t w2[2] = {u.x, u.y};
 #pragma unroll
-            for (int j = 0; j < VEC; ++j)
-                if (((a4[j >> 2] >> (8 * (j & 3))) & 0xffu) == k) acc[j] += v[j];
+            for (int e = 0; e < 8; ++e) k[e] = uint8_t(w2[e >> 2] >> (8 * (e & 3)));
+        } else {
+            const uint32_t u = *reinterpret_cast<const uint32_t*>(af + o);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) k[e] = uint8_t(u >> (8 * e));
+        }
+        loadv<T, VEC>(df + o, v);
+    };
+    uint8_t k[VEC];
+    float v[VEC];
+    const bool up = i >= 1, left = j >= 1, down = i < g.OH, right = j < g.OW;
+    if (up && left) {
+        window(i - 1, j - 1, k, v);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) a00[e] += k[e] == 8 ? v[e] : 0.f;
+    }
+    if (up && right) {
+        window(i - 1, j, k, v);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) { a00[e] += k[e] == 6 ? v[e] : 0.f; a01[e] += k[e] == 7 ? v[e] : 0.f; }
+    }
+    if (down && left) {
+        window(i, j - 1, k, v);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) { a00[e] += k[e] == 2 ? v[e] : 0.f; a10[e] += k[e] == 5 ? v[e] : 0.f; }
+    }
+    if (down && right) {
+        window(i, j, k, v);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            a00[e] += k[e] == 0 ? v[e] : 0.f; a01[e] += k[e] == 1 ? v[e] : 0.f;
+            a10[e] += k[e] == 3 ? v[e] : 0.f; a11[e] += k[e] == 4 ? v[e] : 0.f;
         }
     }
-    storev<T, VEC>(dx + n * g.H * g.W * g.C + uint32_t(q) * g.C + c, acc);
+    T* xf = dx + n * g.H * g.W * g.C + c;
+    const int h0 = 2 * i - g.ph, w0 = 2 * j - g.pw;
+    const bool r0 = h0 >= 0, r1 = h0 + 1 < g.H, c0 = w0 >= 0, c1 = w0 + 1 < g.W;
+    const int o = (h0 * g.W + w0) * g.C;   // negative at a top / left border; each sum below is
+                                           // formed before it offsets the pointer, and only
+                                           // for cells inside the frame
+    if (r0 && c0) storev<T, VEC>(xf + o, a00);
+    if (r0 && c1) storev<T, VEC>(xf + (o + g.C), a01);
+    if (r1 && c0) storev<T, VEC>(xf + (o + g.W * g.C), a10);
+    if (r1 && c1) storev<T, VEC>(xf + (o + (g.W + 1) * g.C), a11);
 }
 
 // Frames per launch: grid rows are frames (at most 65535 per launch).
@@ -150,7 +186,7 @@ template <class T, int VEC>
 static hipError_t pool_bwd_launch(int64_t n, int H, int W, int C, const uint8_t* arg, const T* dy, T* dx,
                                   hipStream_t s) {
     const PoolGeom g = pool_geom(H, W, C, VEC);
-    const int per = H * W * g.CG;
+    const int per = ((H + g.ph + 1) / 2) * ((W + g.pw + 1) / 2) * g.CG;
     for (int64_t n0 = 0; n0 < n; n0 += kPoolFrames) {
         const int64_t nn = n - n0 < kPoolFrames ? n - n0 : kPoolFrames;
         const int64_t in0 = n0 * H * W * C, out0 = n0 * g.OH * g.OW * C;

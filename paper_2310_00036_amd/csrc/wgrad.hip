@@ -567,7 +567,7 @@ hipError_t wg_launch(const WgradArgs& a, hipStream_t s) {
     size_t lds = wg_lds<P, CIN, COUT>(r);
     if (lds < 256 * 8 * sizeof(float)) lds = 256 * 8 * sizeof(float);
     const int pr = sizeof(typename P::T) == 2 ? 0 : 1;
-    const std::string shape = cb_dims(CIN, COUT) + "/" + cb_dims(a.H, a.W);
+    const std::string shape = cb_dims(CIN, COUT) + "/" + cb_dims(a.H, a.W) + cb_flags(MODE, false, false);
     {
         ProfScope ps(s, [&] { return cb_key("wgrad", pr, shape); });
         hipLaunchKernelGGL((wgrad_kernel<P, CIN, COUT, MODE>), dim3(parts), dim3(256), lds, s, a, r);
@@ -643,7 +643,7 @@ hipError_t wg_tr_launch(const WgradArgs& a, hipStream_t s) {
     const void* fn = reinterpret_cast<const void*>(&wgrad_tr_kernel<CIN, COUT, MODE>);
     int parts = std::min(resident_blocks(fn, 256, L), wg_tr_parts_cap(D::PSTRIDE));
     if (parts > r.ntiles) parts = r.ntiles;
-    const std::string shape = cb_dims(CIN, COUT) + "/" + cb_dims(H, W);
+    const std::string shape = cb_dims(CIN, COUT) + "/" + cb_dims(H, W) + cb_flags(MODE, false, false);
     {
         ProfScope ps(s, [&] { return cb_key("wgrad", 0, shape); });
         hipLaunchKernelGGL((wgrad_tr_kernel<CIN, COUT, MODE>), dim3(parts), dim3(256), L, s, a, r);
