@@ -359,7 +359,7 @@ def main():
                      "traffic": traffic, "algorithmic_bytes": work if unit == "B" else None,
                      "mfma_tflops": round(mfma_tflops, 2) if mfma_tflops else None,
                      "mfma_frac": round(mfma_tflops / PEAK[args.prec][0], 4) if mfma_tflops else None},
-        "kernels_top": [{"key": k, "ms_per_step": round(t, 3), "launches": c} for k, t, c in table[:8]],
+        "kernels_top": [{"key": k, "ms_per_step": round(t, 3), "launches": c} for k, t, c in table[:24]],
     }
     if args.cpu_sample_frames > 0:
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_frames)

@@ -288,7 +288,7 @@ struct DmaTile {
     int win_off, mask_off, add_off;   // LDS byte offsets of the regions
     float inv_W, inv_TW, inv_TH, inv_TR;
     // fused max-pool: PTH pooled rows per band, pooled size OH x OW, pads ph/pw, conv tile
-    int PTH, OH, OW, ph, pw, ct_off;
+    int PTH, OH, OW, ph, pw, ct_off, zero_off;   // zero_off: 16 zero bytes
     float inv_OW, inv_ppf;   // 1/OW, 1/(OH*OW)
 };
 
@@ -355,6 +355,7 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
         for (int e = tid; e < COUT * PADK; e += 256)
             wl[(e / PADK) * KPITCH + G::K + e % PADK] = 0;
     }
+    if (POOL && tid < 4) reinterpret_cast<uint32_t*>(smem + t.zero_off)[tid] = 0u;
     float bias[MT][4];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -562,6 +563,7 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
             const int ppf = prows * t.OW;
             const int items = nf * ppf * C8;
             const unsigned char* ct = smem + t.ct_off;
+            const unsigned char* zero16 = smem + t.zero_off;
             uint16_t* pbase = static_cast<uint16_t*>(a.y) + (int64_t(f0) * t.OH + p0) * t.OW * t.cout_total + og;
             uint8_t* abase = a.arg + (int64_t(f0) * t.OH + p0) * t.OW * t.cout_total + og;
             for (int it = tid; it < items; it += 256) {
@@ -572,15 +574,24 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
                 uint32_t best[8];
 #pragma unroll
                 for (int j = 0; j < 8; ++j) best[j] = 0u;
+                // cell (dy, dx) of the window; padded cells read the zero keys (never win), so
+                // all nine loads go out without branches
+                const int hc = 2 * oh - t.ph, wc = 2 * ow - t.pw;
+                const unsigned char* cb = ct + (((f * TH + hc - h0) * W + wc) * COUT + c8 * 8) * 2;
+                const bool rv[3] = {hc >= 0, true, hc + 2 < H};
+                const bool cv[3] = {wc >= 0, true, wc + 2 < W};
+                uint4 cell[9];
+#pragma unroll
+                for (int dy = 0; dy < 3; ++dy)
+#pragma unroll
+                    for (int dx = 0; dx < 3; ++dx)
+                        cell[dy * 3 + dx] = *reinterpret_cast<const uint4*>(
+                            rv[dy] && cv[dx] ? cb + (dy * W + dx) * COUT * 2 : zero16);
 #pragma unroll
                 for (int dy = 0; dy < 3; ++dy) {
-                    const int h = 2 * oh + dy - t.ph;
-                    if (h < 0 || h >= H) continue;
 #pragma unroll
                     for (int dx = 0; dx < 3; ++dx) {
-                        const int w = 2 * ow + dx - t.pw;
-                        if (w < 0 || w >= W) continue;
-                        const uint4 k4 = *reinterpret_cast<const uint4*>(ct + (((f * TH + h - h0) * W + w) * COUT + c8 * 8) * 2);
+                        const uint4 k4 = cell[dy * 3 + dx];
                         const uint32_t tag = 15u - uint32_t(dy * 3 + dx);
                         const uint32_t kk[4] = {k4.x, k4.y, k4.z, k4.w};
 #pragma unroll
@@ -738,7 +749,7 @@ hipError_t launch_bf16_pool(const ConvArgs& a, int cout_total, hipStream_t s) {
     auto cap = [&](int pth, int fr) { return fr > 1 || pth >= OH ? H : std::min(2 * pth + 1, H); };
     auto lds = [&](int pth, int fr) {
         const int th = cap(pth, fr);
-        return size_t(D::WLB) + size_t(D::win_bytes(th, fr, W)) + size_t(fr) * th * W * COUT * 2;
+        return size_t(D::WLB) + size_t(D::win_bytes(th, fr, W)) + size_t(fr) * th * W * COUT * 2 + 16;
     };
     const size_t limit = std::min<size_t>(lds_limit(), 160 * 1024);
     int pmax = OH;
@@ -759,6 +770,7 @@ hipError_t launch_bf16_pool(const ConvArgs& a, int cout_total, hipStream_t s) {
     t.win_off = D::WLB;
     t.ct_off = t.win_off + D::win_bytes(TH, FR, W);
     t.mask_off = t.add_off = t.ct_off;
+    t.zero_off = t.ct_off + FR * TH * W * COUT * 2;
     t.inv_W = 1.f / float(W); t.inv_TW = 1.f / float(W + 2);
     t.inv_TH = 1.f / float(TH); t.inv_TR = 1.f / float(TH + 2);
     t.PTH = PTH; t.OH = OH; t.OW = OW;

@@ -9,6 +9,8 @@
 #include "common.h"
 #include "kernels.h"
 
+#include <type_traits>
+
 namespace cb {
 
 template <class P>
@@ -176,6 +178,147 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a, int kchunk, int a
             }
 }
 
+// ------------------------------------------------------------------ bf16 operands: DMA path
+//
+// When both operands are bf16 in memory (the dense layer, its weights cast once per pass), the
+// tiles are staged straight from HBM into LDS with buffer->LDS loads in the layout they have
+// in memory, double-buffered: the next k-block's loads are issued before this block's MFMAs.
+// A k-contiguous tile is [128 rows][64 k] with 144-byte rows and is read as 16-byte
+// fragments; a rows-contiguous tile is [64 k][128 rows] with 288-byte rows and is read with
+// the LDS transpose read, which hands each lane 4 consecutive k of its row. The padding (one
+// 16-byte slot per row, two for the k-major tile) keeps the 16-lane reads on distinct banks
+// and is filled by out-of-range (zero) loads, as are the tails past M, N and K.
+// 128x128 output tile per workgroup, 4 waves of 64x64 (4x4 MFMA 16x16x32 tiles).
+
+namespace {
+constexpr int kGB = 128, kGK = 64;
+constexpr int kPK = 144, kPM = 288;            // row pitches (bytes) of the two tile layouts
+constexpr int kGTile = kGB * kPK;              // bytes per operand tile (== kGK * kPM)
+constexpr int kGStage = 2 * kGTile;            // A and B
+static_assert(kGK * kPM == kGTile, "both layouts fill the same tile");
+}  // namespace
+
+// DMA one operand tile: rows [r0, r0+128) of `nrows`, k [k0, k0+64) of `kend`.
+template <int KC>
+CB_DEV void gemm_stage(__amdgpu_buffer_rsrc_t rs, unsigned char* __restrict__ dst, int ld, int r0, int nrows,
+                       int k0, int kend, int wave, int lane) {
+    constexpr int SPR = KC ? kPK / 16 : kPM / 16;   // slots per LDS row
+    constexpr int DATA = KC ? 8 : 16;               // data slots per row
+    constexpr int NS = (KC ? kGB : kGK) * SPR;      // slots per tile (multiple of 64)
+    static_assert(NS % 64 == 0, "whole DMA blocks");
+    for (int b = wave; b < NS / 64; b += 4) {
+        const int j = b * 64 + lane;
+        const int row = j / SPR, c = j - row * SPR;
+        uint32_t off = kOOB;
+        if (KC) {
+            if (c < DATA && r0 + row < nrows && k0 + c * 8 < kend)
+                off = (uint32_t(r0 + row) * uint32_t(ld) + uint32_t(k0 + c * 8)) * 2u;
+        } else {
+            if (c < DATA && k0 + row < kend && r0 + c * 8 < nrows)
+                off = (uint32_t(k0 + row) * uint32_t(ld) + uint32_t(r0 + c * 8)) * 2u;
+        }
+        dma16_to_lds(rs, dst + b * 1024, off);
+    }
+}
+
+// Fragment of 8 consecutive k (k-step ks, lane group g) of tile row `row`.
+template <int KC>
+CB_DEV uint4 gemm_frag(const unsigned char* __restrict__ t, int row, int ks, int g, int lane) {
+    if constexpr (KC) {
+        return *reinterpret_cast<const uint4*>(t + row * kPK + ks * 64 + g * 16);
+    } else {
+        // transpose read: lane 4j+m of the 16-lane group addresses k = base + j, rows 4m..4m+3
+        const int r16 = lane & 15, j = r16 >> 2, m = r16 & 3;
+        const int rb = row - r16 + 4 * m;   // first row of this lane's 4-row chunk
+        const uint2 lo = lds_read_tr16(t + (ks * 32 + g * 8 + j) * kPM + rb * 2);
+        const uint2 hi = lds_read_tr16(t + (ks * 32 + g * 8 + 4 + j) * kPM + rb * 2);
+        return make_uint4(lo.x, lo.y, hi.x, hi.y);
+    }
+}
+
+// One k-block: issue the next block's loads into `nxt`, then the MFMAs on `cur`. Both buffers
+// are restrict parameters of the one call, so the compiler knows the loads in flight do not
+// write what the MFMAs read and does not wait for them.
+template <int AKC, int BKC, int BRELU>
+CB_DEV void gemm_block(const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt, bool more,
+                       __amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb, const GemmArgs& a, int m0, int n0,
+                       int k1, int k_end, int wave, int lane, cb_f32x4 (&acc)[4][4]) {
+    if (more) {
+        gemm_stage<AKC>(ra, nxt, int(a.lda), m0, a.M, k1, k_end, wave, lane);
+        gemm_stage<BKC>(rb, nxt + kGTile, int(a.ldb), n0, a.N, k1, k_end, wave, lane);
+    }
+    const int g = (lane >> 4) & 3, r16 = lane & 15;
+    const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+        uint4 af[4], bf[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) af[i] = gemm_frag<AKC>(cur, wm * 64 + i * 16 + r16, ks, g, lane);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            bf[j] = gemm_frag<BKC>(cur + kGTile, wn * 64 + j * 16 + r16, ks, g, lane);
+            if constexpr (BRELU) {
+                bf[j].x = relu_bf16x2(bf[j].x); bf[j].y = relu_bf16x2(bf[j].y);
+                bf[j].z = relu_bf16x2(bf[j].z); bf[j].w = relu_bf16x2(bf[j].w);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = PrecBF16::mma(af[i], bf[j], acc[i][j]);
+    }
+}
+
+template <int AKC, int BKC, int BRELU>
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a, int kchunk) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, r16 = lane & 15;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int m0 = blockIdx.x * kGB, n0 = blockIdx.y * kGB;
+    const int k_begin = blockIdx.z * kchunk;
+    const int k_end = min(a.K, k_begin + kchunk);
+    const auto ra = buf_rsrc(a.a, uint32_t((AKC ? int64_t(a.M) : int64_t(a.K)) * a.lda * 2));
+    const auto rb = buf_rsrc(a.b, uint32_t((BKC ? int64_t(a.N) : int64_t(a.K)) * a.ldb * 2));
+
+    cb_f32x4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+
+    gemm_stage<AKC>(ra, smem, int(a.lda), m0, a.M, k_begin, k_end, wave, lane);
+    gemm_stage<BKC>(rb, smem + kGTile, int(a.ldb), n0, a.N, k_begin, k_end, wave, lane);
+    int it = 0;
+    for (int k0 = k_begin; k0 < k_end; k0 += kGK, ++it) {
+        __builtin_amdgcn_s_waitcnt(0);   // this block's loads (this wave's) are in LDS
+        __syncthreads();                 // all waves' loads in; the other buffer is free
+        unsigned char* cur = smem + (it & 1) * kGStage;
+        unsigned char* nxt = smem + ((it + 1) & 1) * kGStage;
+        gemm_block<AKC, BKC, BRELU>(cur, nxt, k0 + kGK < k_end, ra, rb, a, m0, n0, k0 + kGK, k_end, wave, lane, acc);
+    }
+
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int mb = m0 + wm * 64 + i * 16 + 4 * g;
+            const int n = n0 + wn * 64 + j * 16 + r16;
+            if (gridDim.z == 1) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) gemm_epilogue<PrecBF16>(a, mb + r, n, acc[i][j][r]);
+            } else if (n < a.N && mb < a.M) {
+                float* pp = a.partial + (int64_t(blockIdx.z) * a.N + n) * a.M + mb;
+                if (mb + 4 <= a.M && (a.M & 3) == 0) {
+                    *reinterpret_cast<float4*>(pp) = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) if (mb + r < a.M) pp[r] = acc[i][j][r];
+                }
+            }
+        }
+}
+
 template <class P>
 __global__ __launch_bounds__(256) void gemm_finish_kernel(GemmArgs a, int splits) {
     const int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x;
@@ -202,13 +345,77 @@ constexpr int kMaxSplits = 8;
 
 size_t gemm_partial_floats(int M, int N, int K) {
     const int sp = auto_splits(M, N, K, kMaxSplits, 64, 64);
-    return sp > 1 ? size_t(M) * N * sp : 0;
+    // the bf16 DMA path: about two 128x128 workgroups per CU, at least 256 k per split
+    const int tiles = ((M + 127) / 128) * ((N + 127) / 128);
+    int sd = (512 + tiles - 1) / tiles;
+    while (sd > 1 && K / sd < 256) --sd;
+    const int spm = sp > sd ? sp : sd;
+    return spm > 1 ? size_t(M) * N * spm : 0;
+}
+
+// ------------------------------------------------------------------ float32 -> bf16
+__global__ void cast_bf16_kernel(const float* __restrict__ x, uint16_t* __restrict__ y, int64_t n) {
+    const int64_t i = (int64_t(blockIdx.x) * 256 + threadIdx.x) * 2;
+    if (i + 1 < n) *reinterpret_cast<uint32_t*>(y + i) = pack2bf(x[i], x[i + 1]);
+    else if (i < n) y[i] = f2bf(x[i]);
+}
+
+hipError_t cast_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    ProfScope ps(s, [&] { return "cast_bf16/" + std::to_string(n); });
+    hipLaunchKernelGGL(cast_bf16_kernel, dim3(unsigned((n + 511) / 512)), dim3(256), 0, s, x, y, n);
+    return hipGetLastError();
+}
+
+// Whether the DMA path takes this GEMM: bf16 operands with 16-byte aligned rows, multiples of
+// 8 where a tile row is cut along the contiguous dimension, tiles worth filling, operands
+// addressable with 32-bit offsets.
+static bool gemm_dma_ok(const GemmArgs& a) {
+    auto al = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+    if (a.a_f32 || a.b_f32 || a.M < 64 || a.N < 64 || a.K % 8) return false;
+    if (!al(a.a) || !al(a.b) || a.lda % 8 || a.ldb % 8) return false;
+    if (!a.a_kcontig && a.M % 8) return false;
+    if (!a.b_kcontig && a.N % 8) return false;
+    const int64_t abytes = (a.a_kcontig ? int64_t(a.M) : int64_t(a.K)) * a.lda * 2;
+    const int64_t bbytes = (a.b_kcontig ? int64_t(a.N) : int64_t(a.K)) * a.ldb * 2;
+    return abytes < (int64_t(1) << 31) && bbytes < (int64_t(1) << 31);
+}
+
+static hipError_t gemm_dma_launch(const GemmArgs& a, hipStream_t s) {
+    const int tiles = ((a.M + kGB - 1) / kGB) * ((a.N + kGB - 1) / kGB);
+    int splits = a.partial ? (512 + tiles - 1) / tiles : 1;   // about two workgroups per CU
+    while (splits > 1 && a.K / splits < 256) --splits;
+    while (splits > 1 && size_t(a.M) * a.N * splits > a.partial_floats) --splits;
+    if (splits < 1) splits = 1;
+    int kchunk = (a.K + splits - 1) / splits;
+    kchunk = (kchunk + kGK - 1) / kGK * kGK;
+    const int z = (a.K + kchunk - 1) / kchunk > 0 ? (a.K + kchunk - 1) / kchunk : 1;
+    const dim3 grid((a.M + kGB - 1) / kGB, (a.N + kGB - 1) / kGB, z);
+    const size_t lds = 2 * kGStage;
+    const std::string shape = cb_dims(a.M, a.N) + "x" + std::to_string(a.K);
+    {
+        ProfScope ps(s, [&] { return cb_key("gemm", 0, shape); });
+#define CB_GB(AK, BK, BR) \
+        if (a.a_kcontig == AK && a.b_kcontig == BK && (a.b_relu != 0) == BR) \
+            hipLaunchKernelGGL((gemm_bf16_kernel<AK, BK, BR>), grid, dim3(256), lds, s, a, kchunk);
+        CB_GB(1, 1, 0) CB_GB(1, 0, 0) CB_GB(0, 1, 0) CB_GB(0, 0, 0)
+        CB_GB(1, 1, 1) CB_GB(1, 0, 1) CB_GB(0, 1, 1) CB_GB(0, 0, 1)
+#undef CB_GB
+    }
+    if (z > 1) {
+        ProfScope ps(s, [&] { return cb_key("gemm_finish", 0, shape); });
+        const int64_t total = int64_t(a.M) * a.N;
+        hipLaunchKernelGGL(gemm_finish_kernel<PrecBF16>, dim3(unsigned((total + 255) / 256)), dim3(256), 0,
+                           s, a, z);
+    }
+    return hipGetLastError();
 }
 
 template <class P>
 static hipError_t gemm_launch(const GemmArgs& a, hipStream_t s) {
     using G = GemmTile<P>;
     if (a.M <= 0 || a.N <= 0) return hipSuccess;
+    if (std::is_same_v<P, PrecBF16> && gemm_dma_ok(a)) return gemm_dma_launch(a, s);
     int splits = a.partial ? auto_splits(a.M, a.N, a.K, kMaxSplits, G::BM, G::BN) : 1;
     while (splits > 1 && size_t(a.M) * a.N * splits > a.partial_floats) --splits;
     int kchunk = (a.K + splits - 1) / splits;

@@ -79,6 +79,9 @@ size_t gemm_partial_floats(int M, int N, int K);
 // The launcher splits K so the grid covers the chip, within a.partial_floats.
 hipError_t gemm(int prec, const GemmArgs& a, hipStream_t s);
 
+// y[i] = bf16(x[i]) (round to nearest even); y 4-byte aligned.
+hipError_t cast_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t s);
+
 // ---- small helpers
 hipError_t colsum(int prec_storage, const void* x, int64_t rows, int cols, int64_t ld,
                   float* out, float* partial, hipStream_t s);   // out[c] = sum_r x[r*ld + c]

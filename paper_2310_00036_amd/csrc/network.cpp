@@ -93,6 +93,7 @@ NetPlan make_plan(const impala_net_t& net, int prec, int64_t cap, int training) 
     }
     p.h = take(size_t(cap) * p.hidden * p.es);
     p.whp = take(size_t(p.A + 1) * p.hidden * sizeof(float));
+    p.wdb = take(prec == BF16 ? size_t(p.flat) * p.hidden * 2 : 0);
     // split-K / column-sum / weight-gradient partials, shared by the launches in turn. The
     // GEMM launcher never splits beyond this capacity, so the sizing only affects speed.
     size_t sc = 0;
@@ -167,8 +168,13 @@ hipError_t run_forward(const NetPlan& p, const float* params, const uint8_t* obs
         }
     }
     // dense: h[i][j] = relu(b[j] + sum_k relu(x)[i][k] W[k][j])
+    // bf16: the dense weights are cast once per pass, so both dense GEMMs read bf16 operands
+    const bool wbf = p.prec == BF16;
+    if (wbf) CB_TRY(cast_bf16(params + po.dense_w, reinterpret_cast<uint16_t*>(ws + p.wdb),
+                              int64_t(p.flat) * p.hidden, s));
     GemmArgs d{};
-    d.a = params + po.dense_w; d.a_f32 = 1; d.a_kcontig = 0; d.lda = p.hidden;
+    d.a = wbf ? static_cast<const void*>(ws + p.wdb) : static_cast<const void*>(params + po.dense_w);
+    d.a_f32 = !wbf; d.a_kcontig = 0; d.lda = p.hidden;
     d.b = ws + p.x[2][2]; d.b_f32 = p.prec == FP32; d.b_kcontig = 1; d.ldb = p.flat; d.b_relu = 1;
     d.M = p.hidden; d.N = int(n); d.K = p.flat;
     d.alpha = 1.f; d.bias1 = params + po.dense_b; d.relu = 1;
@@ -234,8 +240,12 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
     CB_TRY(gemm(p.prec, dw, s));
     CB_TRY(colsum(p.prec, G[0], n, p.hidden, p.hidden, grads + po.dense_b, scratch, s));
     // dense input gradient: dx[i][k] = (sum_j Wd[k][j] dh[i][j]) * (x[i][k] > 0)
+    const bool wbf = p.prec == BF16;
+    if (wbf) CB_TRY(cast_bf16(params + po.dense_w, reinterpret_cast<uint16_t*>(ws + p.wdb),
+                              int64_t(p.flat) * p.hidden, s));
     GemmArgs dg{};
-    dg.a = params + po.dense_w; dg.a_f32 = 1; dg.a_kcontig = 1; dg.lda = p.hidden;
+    dg.a = wbf ? static_cast<const void*>(ws + p.wdb) : static_cast<const void*>(params + po.dense_w);
+    dg.a_f32 = !wbf; dg.a_kcontig = 1; dg.lda = p.hidden;
     dg.b = G[0]; dg.b_f32 = st_f32; dg.b_kcontig = 1; dg.ldb = p.hidden;
     dg.M = p.flat; dg.N = int(n); dg.K = p.hidden; dg.alpha = 1.f;
     dg.mask = ws + p.x[2][2]; dg.ldmask = p.flat;

@@ -113,45 +113,43 @@ __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const uint8_t* __restr
     float a00[VEC], a01[VEC], a10[VEC], a11[VEC];
 #pragma unroll
     for (int e = 0; e < VEC; ++e) { a00[e] = 0.f; a01[e] = 0.f; a10[e] = 0.f; a11[e] = 0.f; }
-    auto window = [&](int oh, int ow, uint8_t* k, float* v) {
-        const uint32_t o = uint32_t(oh * g.OW + ow) * g.C;
+    // The four windows; one outside the pooled grid reads a clamped window with its argmax
+    // bytes forced to 0xff, which matches no cell. No branches, so the loads overlap.
+    const bool up = i >= 1, left = j >= 1, down = i < g.OH, right = j < g.OW;
+    const int ohs[2] = {up ? i - 1 : 0, down ? i : g.OH - 1};
+    const int ows[2] = {left ? j - 1 : 0, right ? j : g.OW - 1};
+    const bool ok[4] = {up && left, up && right, down && left, down && right};
+    uint32_t ka[4][VEC / 4];
+    float v[4][VEC];
+#pragma unroll
+    for (int wdw = 0; wdw < 4; ++wdw) {
+        const uint32_t o = uint32_t(ohs[wdw >> 1] * g.OW + ows[wdw & 1]) * g.C;
         if constexpr (VEC == 8) {
             const uint2 u = *reinterpret_cast<const uint2*>(af + o);
-            const uint32_t w2[2] = {u.x, u.y};
-#pragma unroll
-            for (int e = 0; e < 8; ++e) k[e] = uint8_t(w2[e >> 2] >> (8 * (e & 3)));
+            ka[wdw][0] = ok[wdw] ? u.x : 0xffffffffu;
+            ka[wdw][1] = ok[wdw] ? u.y : 0xffffffffu;
         } else {
             const uint32_t u = *reinterpret_cast<const uint32_t*>(af + o);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) k[e] = uint8_t(u >> (8 * e));
+            ka[wdw][0] = ok[wdw] ? u : 0xffffffffu;
         }
-        loadv<T, VEC>(df + o, v);
-    };
-    uint8_t k[VEC];
-    float v[VEC];
-    const bool up = i >= 1, left = j >= 1, down = i < g.OH, right = j < g.OW;
-    if (up && left) {
-        window(i - 1, j - 1, k, v);
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) a00[e] += k[e] == 8 ? v[e] : 0.f;
+        loadv<T, VEC>(df + o, v[wdw]);
     }
-    if (up && right) {
-        window(i - 1, j, k, v);
+    // cell <- window: a00 <- (i-1,j-1):8, (i-1,j):6, (i,j-1):2, (i,j):0; a01 <- (i-1,j):7, (i,j):1;
+    // a10 <- (i,j-1):5, (i,j):3; a11 <- (i,j):4 -- each in (oh, ow) order
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) { a00[e] += k[e] == 6 ? v[e] : 0.f; a01[e] += k[e] == 7 ? v[e] : 0.f; }
-    }
-    if (down && left) {
-        window(i, j - 1, k, v);
+    for (int e = 0; e < VEC; ++e) {
+        uint32_t k[4];
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) { a00[e] += k[e] == 2 ? v[e] : 0.f; a10[e] += k[e] == 5 ? v[e] : 0.f; }
-    }
-    if (down && right) {
-        window(i, j, k, v);
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-            a00[e] += k[e] == 0 ? v[e] : 0.f; a01[e] += k[e] == 1 ? v[e] : 0.f;
-            a10[e] += k[e] == 3 ? v[e] : 0.f; a11[e] += k[e] == 4 ? v[e] : 0.f;
-        }
+        for (int wdw = 0; wdw < 4; ++wdw) k[wdw] = (ka[wdw][e >> 2] >> (8 * (e & 3))) & 0xffu;
+        a00[e] += k[0] == 8 ? v[0][e] : 0.f;
+        a00[e] += k[1] == 6 ? v[1][e] : 0.f;
+        a00[e] += k[2] == 2 ? v[2][e] : 0.f;
+        a00[e] += k[3] == 0 ? v[3][e] : 0.f;
+        a01[e] += k[1] == 7 ? v[1][e] : 0.f;
+        a01[e] += k[3] == 1 ? v[3][e] : 0.f;
+        a10[e] += k[2] == 5 ? v[2][e] : 0.f;
+        a10[e] += k[3] == 3 ? v[3][e] : 0.f;
+        a11[e] += k[3] == 4 ? v[3][e] : 0.f;
     }
     T* xf = dx + n * g.H * g.W * g.C + c;
     const int h0 = 2 * i - g.ph, w0 = 2 * j - g.pw;
