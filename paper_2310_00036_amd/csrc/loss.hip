@@ -37,36 +37,46 @@ __global__ __launch_bounds__(256) void adv_stats_kernel(int64_t m, const float* 
     }
 }
 
-// Log-softmax of one row: writes l[j] = z_j - logsumexp(z); returns the entropy.
-CB_DEV float row_log_softmax(const float* z, int A, float* l) {
-    float zmax = z[0];
-    for (int j = 1; j < A; ++j) zmax = fmaxf(zmax, z[j]);
+// Log-softmax of one row, kept as (zmax, lse): log pi_j = (z_j - zmax) - lse, recomputed from
+// the logits where needed (no per-row array, so nothing spills to scratch). Also the entropy.
+struct RowLsm {
+    float zmax, lse, H;
+    CB_DEV float l(float zj) const { return (zj - zmax) - lse; }
+};
+
+CB_DEV RowLsm row_log_softmax(const float* z, int A) {
+    RowLsm r;
+    r.zmax = z[0];
+    for (int j = 1; j < A; ++j) r.zmax = fmaxf(r.zmax, z[j]);
     float se = 0.f;
-    for (int j = 0; j < A; ++j) se += expf(z[j] - zmax);
-    const float lse = logf(se);
-    float H = 0.f;
+    for (int j = 0; j < A; ++j) se += expf(z[j] - r.zmax);
+    r.lse = logf(se);
+    r.H = 0.f;
     for (int j = 0; j < A; ++j) {
-        l[j] = (z[j] - zmax) - lse;
-        H -= expf(l[j]) * l[j];
+        const float l = r.l(z[j]);
+        r.H -= expf(l) * l;
     }
-    return H;
+    return r;
 }
 
 struct PpoRow {
+    RowLsm s;
     float H, ratio, A_hat, pg, kappa;
     int a;
 };
 
 CB_DEV PpoRow ppo_row(int64_t i, int64_t src, int A, const float* z, const int32_t* act,
                       const float* old_logp, const float* adv, int norm_adv, float clip,
-                      float mean, float std, float* l) {
+                      float mean, float std) {
     PpoRow r;
-    r.H = row_log_softmax(z + i * A, A, l);
+    const float* zr = z + i * A;
+    r.s = row_log_softmax(zr, A);
+    r.H = r.s.H;
     r.a = act[src];
     r.A_hat = adv[src];
     if (norm_adv) r.A_hat = (r.A_hat - mean) / (std + 1e-8f);
-    // an action outside [0, A) poisons the row with NaN instead of reading past l[]
-    const float la = (r.a >= 0 && r.a < A) ? l[r.a] : __builtin_nanf("");
+    // an action outside [0, A) poisons the row with NaN instead of reading past the row
+    const float la = (r.a >= 0 && r.a < A) ? r.s.l(zr[r.a]) : __builtin_nanf("");
     r.ratio = expf(la - old_logp[src]);
     const float pg1 = -r.A_hat * r.ratio;
     const float pg2 = -r.A_hat * fminf(fmaxf(r.ratio, 1.f - clip), 1.f + clip);
@@ -85,13 +95,14 @@ __global__ __launch_bounds__(kLossRows) void ppo_rows_kernel(
     const int64_t i = int64_t(blockIdx.x) * kLossRows + threadIdx.x;
     if (i >= m) return;
     const int64_t src = rows ? rows[i] : i;
-    float l[64];
-    const PpoRow r = ppo_row(i, src, A, z, act, old_logp, adv, norm_adv, clip, stats[6], stats[7], l);
+    const PpoRow r = ppo_row(i, src, A, z, act, old_logp, adv, norm_adv, clip, stats[6], stats[7]);
     const float inv_m = 1.f / float(m);
     const float coef = -r.kappa * r.A_hat * r.ratio;
+    const float* zr = z + i * A;
     for (int j = 0; j < A; ++j) {
-        const float p = expf(l[j]);
-        dz[i * A + j] = (coef * ((j == r.a ? 1.f : 0.f) - p) + ent * p * (l[j] + r.H)) * inv_m;
+        const float l = r.s.l(zr[j]);
+        const float p = expf(l);
+        dz[i * A + j] = (coef * ((j == r.a ? 1.f : 0.f) - p) + ent * p * (l + r.H)) * inv_m;
     }
     dv[i] = vf * (val[i] - ret[src]) * inv_m;
 }
@@ -105,10 +116,9 @@ __global__ __launch_bounds__(kStatThreads) void ppo_stats_kernel(
     __shared__ double sh[kStatThreads];
     const float mean = stats[6], std = stats[7];
     double st[5] = {0, 0, 0, 0, 0};
-    float l[64];
     for (int64_t i = threadIdx.x; i < m; i += kStatThreads) {
         const int64_t src = rows ? rows[i] : i;
-        const PpoRow r = ppo_row(i, src, A, z, act, old_logp, adv, norm_adv, clip, mean, std, l);
+        const PpoRow r = ppo_row(i, src, A, z, act, old_logp, adv, norm_adv, clip, mean, std);
         const double dvl = double(val[i]) - double(ret[src]);
         st[0] += r.pg;
         st[1] += dvl * dvl;
@@ -134,15 +144,17 @@ __global__ __launch_bounds__(kLossRows) void impala_rows_kernel(
     float pgc, float vf, float ent, float* __restrict__ dz, float* __restrict__ dv) {
     const int64_t i = int64_t(blockIdx.x) * kLossRows + threadIdx.x;
     if (i >= m) return;
-    float l[64];
-    const float H = row_log_softmax(z + i * A, A, l);
+    const float* zr = z + i * A;
+    const RowLsm rs = row_log_softmax(zr, A);
+    const float H = rs.H;
     const int a = act[i];
     const float adv = pgadv[i];
     const float inv_m = 1.f / float(m);
     const bool a_ok = a >= 0 && a < A;
     for (int j = 0; j < A; ++j) {
-        const float p = expf(l[j]);
-        dz[i * A + j] = a_ok ? (-pgc * adv * ((j == a ? 1.f : 0.f) - p) + ent * p * (l[j] + H)) * inv_m
+        const float l = rs.l(zr[j]);
+        const float p = expf(l);
+        dz[i * A + j] = a_ok ? (-pgc * adv * ((j == a ? 1.f : 0.f) - p) + ent * p * (l + H)) * inv_m
                              : __builtin_nanf("");
     }
     dv[i] = vf * (val[i] - vs[i]) * inv_m;
@@ -154,12 +166,13 @@ __global__ __launch_bounds__(kStatThreads) void impala_stats_kernel(
     float pgc, float vf, float ent, float* __restrict__ stats) {
     __shared__ double sh[kStatThreads];
     double st[5] = {0, 0, 0, 0, 0};
-    float l[64];
     for (int64_t i = threadIdx.x; i < m; i += kStatThreads) {
-        const float H = row_log_softmax(z + i * A, A, l);
+        const float* zr = z + i * A;
+        const RowLsm rs = row_log_softmax(zr, A);
+        const float H = rs.H;
         const double dvl = double(val[i]) - double(vs[i]);
         const int a = act[i];
-        st[0] += -double(pgadv[i]) * ((a >= 0 && a < A) ? double(l[a]) : double(__builtin_nanf("")));
+        st[0] += -double(pgadv[i]) * ((a >= 0 && a < A) ? double(rs.l(zr[a])) : double(__builtin_nanf("")));
         st[1] += dvl * dvl;
         st[2] += H;
         st[3] += pgadv[i];
@@ -210,10 +223,10 @@ __global__ void action_logp_kernel(int64_t m, int A, const float* __restrict__ z
                                    const int32_t* __restrict__ act, float* __restrict__ logp) {
     const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
     if (i >= m) return;
-    float l[64];
-    row_log_softmax(z + i * A, A, l);
+    const float* zr = z + i * A;
+    const RowLsm rs = row_log_softmax(zr, A);
     const int a = act[i];
-    logp[i] = (a >= 0 && a < A) ? l[a] : __builtin_nanf("");
+    logp[i] = (a >= 0 && a < A) ? rs.l(zr[a]) : __builtin_nanf("");
 }
 
 hipError_t action_logp(int64_t m, int A, const float* z, const int32_t* act, float* logp,
@@ -239,10 +252,9 @@ __global__ void gumbel_max_kernel(int64_t m, int A, const float* __restrict__ z,
         const float v = zr[j] + gr[j];
         if (v > bv) { bv = v; best = j; }
     }
-    float l[64];
-    row_log_softmax(zr, A, l);
+    const RowLsm rs = row_log_softmax(zr, A);
     act[i] = best;
-    logp[i] = l[best];
+    logp[i] = rs.l(zr[best]);
 }
 
 hipError_t gumbel_max(int64_t m, int A, const float* z, const float* g, int32_t* act, float* logp,

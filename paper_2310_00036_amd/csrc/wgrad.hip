@@ -240,26 +240,34 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, WgRun g_) {
     }
 }
 
+// Fixed-order sum of `nparts` partials of `pstride` floats, 16 consecutive entries per
+// 1024-thread block: slice s (of 64) adds partials s, s+64, ..., then a fixed pairwise tree
+// over the slices. emit(entry, total) gets each entry's sum.
+template <class F>
+CB_DEV void sum_partials16(const float* __restrict__ partial, int nparts, int pstride, F&& emit) {
+    __shared__ float sh[64][17];
+    const int el = threadIdx.x & 15, sp = threadIdx.x >> 4;
+    const int e = blockIdx.x * 16 + el;
+    float s = 0.f;
+    if (e < pstride)
+        for (int p = sp; p < nparts; p += 64) s += partial[int64_t(p) * pstride + e];
+    sh[sp][el] = s;
+    __syncthreads();
+#pragma unroll
+    for (int w = 32; w >= 1; w >>= 1) {
+        if (sp < w) sh[sp][el] += sh[sp + w][el];
+        __syncthreads();
+    }
+    if (sp == 0 && e < pstride) emit(e, sh[0][el]);
+}
+
 // Sum the partials of all workgroups in a fixed order and scatter to HWIO / bias.
-// Block: 64 consecutive partial entries x 16 interleaved slices of the partials.
 template <int CIN, int COUT>
 __global__ __launch_bounds__(1024) void wgrad_reduce_kernel(const float* __restrict__ partial,
                                                             int nparts, float* dw, float* db,
                                                             float scale) {
     using G = WgGeom<PrecF32, CIN, COUT>;
-    __shared__ float sh[16][64];
-    const int e = blockIdx.x * 64 + (threadIdx.x & 63);
-    const int sp = threadIdx.x >> 6;
-    float s = 0.f;
-    if (e < G::PSTRIDE) {
-        for (int p = sp; p < nparts; p += 16) s += partial[int64_t(p) * G::PSTRIDE + e];
-    }
-    sh[sp][threadIdx.x & 63] = s;
-    __syncthreads();
-    if (sp == 0 && e < G::PSTRIDE) {
-        float tot = 0.f;
-#pragma unroll
-        for (int k = 0; k < 16; ++k) tot += sh[k][threadIdx.x];
+    sum_partials16(partial, nparts, G::PSTRIDE, [&](int e, float tot) {
         constexpr int WSZ = 3 * COUT * G::NTN * 16;
         if (e < WSZ) {
             const int col = e % (G::NTN * 16), co = (e / (G::NTN * 16)) % COUT, kx = e / (COUT * G::NTN * 16);
@@ -270,7 +278,7 @@ __global__ __launch_bounds__(1024) void wgrad_reduce_kernel(const float* __restr
         } else {
             db[e - WSZ] = tot;
         }
-    }
+    });
 }
 
 // ------------------------------------------------------------------ bf16: transpose reads
@@ -490,18 +498,7 @@ __global__ __launch_bounds__(1024) void wgrad_tr_reduce_kernel(const float* __re
                                                                int nparts, float* dw, float* db,
                                                                float scale) {
     using D = WgTr<CIN, COUT, MODE>;
-    __shared__ float sh[16][64];
-    const int e = blockIdx.x * 64 + (threadIdx.x & 63);
-    const int sp = threadIdx.x >> 6;
-    float s = 0.f;
-    if (e < D::PSTRIDE)
-        for (int p = sp; p < nparts; p += 16) s += partial[int64_t(p) * D::PSTRIDE + e];
-    sh[sp][threadIdx.x & 63] = s;
-    __syncthreads();
-    if (sp == 0 && e < D::PSTRIDE) {
-        float tot = 0.f;
-#pragma unroll
-        for (int k = 0; k < 16; ++k) tot += sh[k][threadIdx.x];
+    sum_partials16(partial, nparts, D::PSTRIDE, [&](int e, float tot) {
         const int tile = e >> 8, row = (e >> 4) & 15, col = e & 15;
         const int mt = tile / D::NBB, nb = tile % D::NBB, co = mt * 16 + row;
         if (nb == D::NB) {
@@ -511,7 +508,7 @@ __global__ __launch_bounds__(1024) void wgrad_tr_reduce_kernel(const float* __re
             const int ci = D::U8 ? col % 4 : (nb % (CIN / 16 > 0 ? CIN / 16 : 1)) * 16 + col;
             if (tap < 9) dw[(tap * CIN + ci) * COUT + co] = tot * scale;
         }
-    }
+    });
 }
 
 namespace {
@@ -574,7 +571,7 @@ hipError_t wg_launch(const WgradArgs& a, hipStream_t s) {
     }
     {
         ProfScope ps(s, [&] { return cb_key("wgrad_reduce", pr, shape); });
-        hipLaunchKernelGGL((wgrad_reduce_kernel<CIN, COUT>), dim3((G::PSTRIDE + 63) / 64), dim3(1024), 0,
+        hipLaunchKernelGGL((wgrad_reduce_kernel<CIN, COUT>), dim3((G::PSTRIDE + 15) / 16), dim3(1024), 0,
                            s, a.partial, parts, a.dw, a.db, a.scale);
     }
     return hipGetLastError();
@@ -650,7 +647,7 @@ hipError_t wg_tr_launch(const WgradArgs& a, hipStream_t s) {
     }
     {
         ProfScope ps(s, [&] { return cb_key("wgrad_reduce", 0, shape); });
-        hipLaunchKernelGGL((wgrad_tr_reduce_kernel<CIN, COUT, MODE>), dim3((D::PSTRIDE + 63) / 64), dim3(1024),
+        hipLaunchKernelGGL((wgrad_tr_reduce_kernel<CIN, COUT, MODE>), dim3((D::PSTRIDE + 15) / 16), dim3(1024),
                            0, s, a.partial, parts, a.dw, a.db, a.scale);
     }
     return hipGetLastError();
