@@ -312,8 +312,8 @@ struct DmaGeom {
     __host__ __device__ static int op_bytes(int TH, int FR, int W) { return blocks(FR * TH * W * OCH) * 64 * 16; }
 };
 
-template <int CIN, int COUT, int MODE, int FLIP, int POOL>
-__global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t) {
+template <int CIN, int COUT, int MODE, int FLIP, int POOL, int NW>
+__global__ __launch_bounds__(64 * NW) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t) {
     using D = DmaGeom<CIN, COUT, MODE>;
     using G = ConvGeom<PrecBF16, CIN>;
     using P = PrecBF16;
@@ -331,6 +331,7 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
     unsigned char* opm = smem + t.mask_off;
     unsigned char* opa = smem + t.add_off;
 
+    constexpr int NT = 64 * NW;   // threads per workgroup
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, r16 = lane & 15;
     const int og = blockIdx.y * COUT;
@@ -340,19 +341,19 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
 
     // ---- weights -> LDS once: wl[o][tap*CIN + i], zero in the k padding
     if (FLIP) {
-        for (int e = tid; e < 9 * COUT * CIN; e += 256) {
+        for (int e = tid; e < 9 * COUT * CIN; e += NT) {
             const int i = e % CIN, o = (e / CIN) % COUT, tap = e / (CIN * COUT);
             wl[o * KPITCH + (8 - tap) * CIN + i] = P::store(a.w[(int64_t(tap) * t.cout_total + og + o) * CIN + i]);
         }
     } else {
-        for (int e = tid; e < 9 * CIN * COUT; e += 256) {
+        for (int e = tid; e < 9 * CIN * COUT; e += NT) {
             const int o = e % COUT, k = e / COUT;
             wl[o * KPITCH + k] = P::store(a.w[int64_t(k) * t.cout_total + og + o]);
         }
     }
     if constexpr (G::KP > G::K) {
         constexpr int PADK = G::KP - G::K;
-        for (int e = tid; e < COUT * PADK; e += 256)
+        for (int e = tid; e < COUT * PADK; e += NT)
             wl[(e / PADK) * KPITCH + G::K + e % PADK] = 0;
     }
     if (POOL && tid < 4) reinterpret_cast<uint32_t*>(smem + t.zero_off)[tid] = 0u;
@@ -417,7 +418,7 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
             const int64_t row = a.row_idx ? a.row_idx[f0] : f0;
             const auto rx = buf_rsrc(static_cast<const uint8_t*>(a.x) + row * fb, fb);
             const int ns = TR * TW;
-            for (int b = wave; b * 64 < ns; b += 4) {
+            for (int b = wave; b * 64 < ns; b += NW) {
                 const int j = b * 64 + lane;
                 uint32_t off = kOOB;
                 if (j < ns) {
@@ -430,7 +431,7 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
             const uint32_t fb = uint32_t(H) * W * CIN * 2;
             const auto rx = buf_rsrc(static_cast<const uint16_t*>(a.x) + int64_t(f0) * H * W * CIN, uint32_t(nf) * fb);
             const int ns = FR * TR * TW * SPP;
-            for (int b = wave; b * 64 < ns; b += 4) {
+            for (int b = wave; b * 64 < ns; b += NW) {
                 const int j = b * 64 + lane;
                 uint32_t off = kOOB;
                 if (j < ns) {
@@ -449,7 +450,7 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
             const auto rm = buf_rsrc(has_mask ? static_cast<const uint16_t*>(a.mask) + fo : nullptr, has_mask ? uint32_t(nf) * ob : 0);
             const auto ra = buf_rsrc(has_add ? static_cast<const uint16_t*>(a.add) + fo : nullptr, has_add ? uint32_t(nf) * ob : 0);
             const int ns = npx * OCH;
-            for (int b = wave; b * 64 < ns; b += 4) {
+            for (int b = wave; b * 64 < ns; b += NW) {
                 const int j = b * 64 + lane;
                 uint32_t off = kOOB;
                 if (j < ns) {
@@ -466,13 +467,13 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
         __syncthreads();                 // ... and everyone else's
         if constexpr (U8) {
             // frames -> bf16 once per pixel (4 channels, exact for 0..255)
-            for (int p = tid; p < TR * TW; p += 256)
+            for (int p = tid; p < TR * TW; p += NT)
                 *reinterpret_cast<uint2*>(win + p * 8) = u8x4_to_bf16(*reinterpret_cast<const uint32_t*>(raw + p * 4));
             __syncthreads();
         } else if constexpr (MODE == IN_RELU) {
             uint4* w4 = reinterpret_cast<uint4*>(win);
             const int ns = FR * TR * TW * SPP;
-            for (int j = tid; j < ns; j += 256) {
+            for (int j = tid; j < ns; j += NT) {
                 uint4 v = w4[j];
                 v.x = relu_bf16x2(v.x); v.y = relu_bf16x2(v.y); v.z = relu_bf16x2(v.z); v.w = relu_bf16x2(v.w);
                 w4[j] = v;
@@ -482,7 +483,7 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
 
         // ---- implicit GEMM over the tile's output pixels, 16 per MFMA column tile
         const int ntl = (npx + 15) >> 4;
-        for (int nt = wave; nt < ntl; nt += 4) {
+        for (int nt = wave; nt < ntl; nt += NW) {
             const int q = nt * 16 + r16;
             const int qc = q < npx ? q : npx - 1;
             const int rowi = qdiv(qc, t.inv_W), col = qc - rowi * W;
@@ -566,7 +567,7 @@ __global__ __launch_bounds__(256) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t
             const unsigned char* zero16 = smem + t.zero_off;
             uint16_t* pbase = static_cast<uint16_t*>(a.y) + (int64_t(f0) * t.OH + p0) * t.OW * t.cout_total + og;
             uint8_t* abase = a.arg + (int64_t(f0) * t.OH + p0) * t.OW * t.cout_total + og;
-            for (int it = tid; it < items; it += 256) {
+            for (int it = tid; it < items; it += NT) {
                 const int c8 = it % C8, pp = it / C8;
                 const int f = FR > 1 ? qdiv(pp, t.inv_ppf) : 0;
                 const int rem = pp - f * ppf;
@@ -726,7 +727,7 @@ hipError_t launch_bf16(const ConvArgs& a, int cout_total, hipStream_t s) {
     t.inv_W = 1.f / float(W); t.inv_TW = 1.f / float(W + 2);
     t.inv_TH = 1.f / float(TH); t.inv_TR = 1.f / float(TH + 2);
     const int groups = cout_total / COUT;
-    const void* fn = reinterpret_cast<const void*>(&conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP, 0>);
+    const void* fn = reinterpret_cast<const void*>(&conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP, 0, 4>);
     int gx = std::max(1, resident_blocks(fn, 256, L) / groups);
     if (gx > ntiles) gx = ntiles;
     const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(groups));
@@ -734,12 +735,18 @@ hipError_t launch_bf16(const ConvArgs& a, int cout_total, hipStream_t s) {
         return cb_key(FLIP ? "conv_dgrad" : "conv_fwd", 0,
                       cb_dims(CIN, cout_total) + "/" + cb_dims(H, W) + cb_flags(MODE, a.mask, a.add));
     });
-    hipLaunchKernelGGL((conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP, 0>), grid, dim3(256), L, s, a, t);
+    hipLaunchKernelGGL((conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP, 0, 4>), grid, dim3(256), L, s, a, t);
     return hipGetLastError();
 }
 
 // Conv + fused max-pool (bf16): bands of PTH pooled rows; each computes the 2*PTH+1 conv
-// rows they read into LDS. Whole frames batch as in launch_bf16.
+// rows they read into LDS. Whole frames batch as in launch_bf16. The conv tile has to sit
+// in LDS beside the window, so these workgroups take 8 waves and twice the LDS of the plain
+// conv's: twice the rows per tile for the same waves per CU, halving the per-tile latency
+// that small tiles leave exposed.
+constexpr int kPoolWaves = 8;
+constexpr int kPoolLdsTarget = 80 * 1024;
+constexpr int kPoolPixMax = 4096;
 template <int CIN, int COUT, int MODE>
 hipError_t launch_bf16_pool(const ConvArgs& a, int cout_total, hipStream_t s) {
     using D = DmaGeom<CIN, COUT, MODE>;
@@ -753,14 +760,14 @@ hipError_t launch_bf16_pool(const ConvArgs& a, int cout_total, hipStream_t s) {
     };
     const size_t limit = std::min<size_t>(lds_limit(), 160 * 1024);
     int pmax = OH;
-    while (pmax > 1 && (lds(pmax, 1) > size_t(kDmaLdsTarget) || cap(pmax, 1) * W > kDmaPixMax)) --pmax;
+    while (pmax > 1 && (lds(pmax, 1) > size_t(kPoolLdsTarget) || cap(pmax, 1) * W > kPoolPixMax)) --pmax;
     if (lds(pmax, 1) > limit) return hipErrorInvalidValue;
     const int nbands0 = (OH + pmax - 1) / pmax;
     const int PTH = (OH + nbands0 - 1) / nbands0;
     const int nbands = (OH + PTH - 1) / PTH;
     int FR = 1;
     if (nbands == 1 && MODE != IN_U8)
-        while (FR < a.n && lds(PTH, FR + 1) <= size_t(kDmaLdsTarget) && (FR + 1) * H * W <= kDmaPixMax) ++FR;
+        while (FR < a.n && lds(PTH, FR + 1) <= size_t(kPoolLdsTarget) && (FR + 1) * H * W <= kPoolPixMax) ++FR;
     const int TH = cap(PTH, FR);
     if (int64_t(FR) * H * W * std::max(MODE == IN_U8 ? 2 : CIN, cout_total) * 2 >= (int64_t(1) << 31))
         return hipErrorInvalidValue;
@@ -778,14 +785,14 @@ hipError_t launch_bf16_pool(const ConvArgs& a, int cout_total, hipStream_t s) {
     t.inv_OW = 1.f / float(OW); t.inv_ppf = 1.f / float(OH * OW);
     const size_t L = lds(PTH, FR);
     const int groups = cout_total / COUT;
-    const void* fn = reinterpret_cast<const void*>(&conv3x3_bf16_kernel<CIN, COUT, MODE, 0, 1>);
-    int gx = std::max(1, resident_blocks(fn, 256, L) / groups);
+    const void* fn = reinterpret_cast<const void*>(&conv3x3_bf16_kernel<CIN, COUT, MODE, 0, 1, kPoolWaves>);
+    int gx = std::max(1, resident_blocks(fn, 64 * kPoolWaves, L) / groups);
     if (gx > t.ntiles) gx = t.ntiles;
     const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(groups));
     ProfScope ps(s, [&] {
         return cb_key("conv_pool", 0, cb_dims(CIN, cout_total) + "/" + cb_dims(H, W) + cb_flags(MODE, false, false));
     });
-    hipLaunchKernelGGL((conv3x3_bf16_kernel<CIN, COUT, MODE, 0, 1>), grid, dim3(256), L, s, a, t);
+    hipLaunchKernelGGL((conv3x3_bf16_kernel<CIN, COUT, MODE, 0, 1, kPoolWaves>), grid, dim3(64 * kPoolWaves), L, s, a, t);
     return hipGetLastError();
 }
 
