@@ -45,6 +45,16 @@ impala_status_t impala_conv3x3_pool_fwd(impala_prec_t prec, int64_t n, int32_t H
                                         const int32_t* row_idx, const float* w, const float* bias,
                                         void* y, uint8_t* arg, hipStream_t stream);
 
+/* One residual block of Section 5's IMPALA-ResNet in one pass, bf16 only (C = 16 or 32):
+ * t = conv3x3_same(relu(x), w1) + b1 and y = x + conv3x3_same(relu(t), w2) + b2. t is
+ * rounded to bf16 before conv2 reads it, so t and y equal those of two impala_conv3x3_fwd
+ * calls (IMPALA_X_RELU, the second with add = x); t is returned for the backward pass.
+ * x, t, y: [n, H, W, C] bf16; w1, w2: float HWIO [3,3,C,C]; b1, b2: float [C] or NULL.
+ * Other precisions or channel counts return IMPALA_EUNSUPPORTED. */
+impala_status_t impala_resblock_fwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t C,
+                                   const void* x, const float* w1, const float* b1, const float* w2,
+                                   const float* b2, void* t, void* y, hipStream_t stream);
+
 /* Input gradient of y = conv3x3_same(x, w): dx = conv3x3_same^T(dy, w), then
  * dx *= (mask > 0) if mask is not NULL, then dx += add if add is not NULL.
  * dy: [n, H, W, cout]; mask, add, dx: [n, H, W, cin]. */

@@ -69,6 +69,7 @@ _SIGS = {
     "impala_conv3x3_fwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _I32, _P, _I32, _P, _P, _P, _P, _P, _P]),
     "impala_conv3x3_pool_fwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _I32, _P, _I32, _P, _P, _P, _P, _P,
                                           _P]),
+    "impala_resblock_fwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P]),
     "impala_conv3x3_dgrad": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P]),
     "impala_conv3x3_wgrad_workspace_bytes": (_SZ, [C.c_int, _I32, _I32, _I32, _I32]),
     "impala_conv3x3_wgrad": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _I32, _P, _I32, _P, _P, _P, _P,
@@ -273,6 +274,11 @@ def impala_conv3x3_pool_fwd(prec, n, H, W, cin, cout, x, x_mode, row_idx, w, bia
     _check("impala_conv3x3_pool_fwd", lib.impala_conv3x3_pool_fwd(
         prec, n, H, W, cin, cout, ptr(x), x_mode, ptr(row_idx), ptr(w), ptr(bias), ptr(y), ptr(arg),
         stream_handle(stream)))
+
+
+def impala_resblock_fwd(prec, n, H, W, C_, x, w1, b1, w2, b2, t, y, stream=None):
+    _check("impala_resblock_fwd", lib.impala_resblock_fwd(
+        prec, n, H, W, C_, ptr(x), ptr(w1), ptr(b1), ptr(w2), ptr(b2), ptr(t), ptr(y), stream_handle(stream)))
 
 
 def impala_conv3x3_dgrad(prec, n, H, W, cin, cout, dy, w, mask, add, dx, stream=None):

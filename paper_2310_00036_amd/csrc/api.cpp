@@ -492,6 +492,21 @@ impala_status_t impala_conv3x3_pool_fwd(impala_prec_t prec, int64_t n, int32_t H
     return hip_status(conv3x3_pool(cin, cout, x_mode, a, stream), "impala_conv3x3_pool_fwd");
 }
 
+impala_status_t impala_resblock_fwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t C,
+                                   const void* x, const float* w1, const float* b1, const float* w2,
+                                   const float* b2, void* t, void* y, hipStream_t stream) {
+    impala_status_t st = check_layer(__func__, prec, n, H, W, C, C);
+    if (st) return st;
+    if (prec != IMPALA_PREC_BF16 || !resblock_fwd_supported(C))
+        return fail(IMPALA_EUNSUPPORTED, "impala_resblock_fwd: bf16 with C = 16 or 32 only (got prec=%d C=%d)", int(prec), C);
+    if (n == 0) return ok();
+    CHECK_PTR(x); CHECK_PTR(w1); CHECK_PTR(w2); CHECK_PTR(t); CHECK_PTR(y);
+    ResBlockArgs a{};
+    a.x = x; a.w1 = w1; a.b1 = b1; a.w2 = w2; a.b2 = b2; a.t = t; a.y = y;
+    a.n = int(n); a.H = H; a.W = W;
+    return hip_status(resblock_fwd(C, a, stream), "impala_resblock_fwd");
+}
+
 impala_status_t impala_conv3x3_dgrad(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t cin,
                                      int32_t cout, const void* dy, const float* w, const void* mask,
                                      const void* add, void* dx, hipStream_t stream) {

@@ -35,6 +35,16 @@ bool conv3x3_supported(int cin, int cout, int mode, int flip);
 // output kept in LDS; OH = (H+1)/2, OW = (W+1)/2. Modes IN_U8 and IN_PLAIN.
 hipError_t conv3x3_pool(int cin, int cout, int mode, const ConvArgs& a, hipStream_t s);
 
+// ---- a whole residual block, bf16 forward: t = conv1(relu(x)) + b1 (stored),
+//      y = x + conv2(relu(t)) + b2; all tensors [n, H, W, C], weights float32 HWIO [3,3,C,C].
+struct ResBlockArgs {
+    const void* x; const float* w1; const float* b1; const float* w2; const float* b2;
+    void* t; void* y;
+    int n, H, W;
+};
+bool resblock_fwd_supported(int C);
+hipError_t resblock_fwd(int C, const ResBlockArgs& a, hipStream_t s);
+
 // ---- weight gradient of a 3x3 SAME conv (deterministic split over pixels)
 struct WgradArgs {
     const void* x;          // forward input (storage type or uint8 frames)

@@ -154,6 +154,17 @@ hipError_t run_forward(const NetPlan& p, const float* params, const uint8_t* obs
         }
         const int C = p.C[st + 1];
         for (int r = 0; r < 2; ++r) {
+            if (p.prec == BF16 && resblock_fwd_supported(C)) {
+                // the whole block in one pass: t and y written, x read once
+                ResBlockArgs rb{};
+                rb.x = ws + p.x[st][r];
+                rb.w1 = params + po.conv_w[st][1 + 2 * r]; rb.b1 = params + po.conv_b[st][1 + 2 * r];
+                rb.w2 = params + po.conv_w[st][2 + 2 * r]; rb.b2 = params + po.conv_b[st][2 + 2 * r];
+                rb.t = ws + p.t[st][r]; rb.y = ws + p.x[st][r + 1];
+                rb.n = int(n); rb.H = p.H[st + 1]; rb.W = p.W[st + 1];
+                CB_TRY(resblock_fwd(C, rb, s));
+                continue;
+            }
             ConvArgs b{};
             b.x = ws + p.x[st][r]; b.w = params + po.conv_w[st][1 + 2 * r];
             b.bias = params + po.conv_b[st][1 + 2 * r]; b.y = ws + p.t[st][r];

@@ -128,6 +128,48 @@ def test_conv_pool_rejects_fp32(prec):
                                   G.torch().empty((1, 4, 4, 16), dtype=G.torch().uint8, device="cuda:0"))
 
 
+RES_CASES = [(3, 42, 42, 16), (4, 21, 21, 32), (5, 11, 11, 32), (2, 17, 23, 16), (3, 9, 7, 32), (2, 84, 84, 16)]
+
+
+@pytest.mark.parametrize("case", RES_CASES, ids=lambda c: "n%d_%dx%d_c%d" % c)
+def test_resblock_forward(case):
+    """Fused residual block (bf16): t against the exact conv1 of relu(x), y against the exact
+    conv2 of relu(t) using the t the kernel returned (so t's rounding does not propagate)."""
+    n, H, W, C = case
+    rng = np.random.default_rng(17)
+    x = G.q(rng.standard_normal((n, H, W, C)), G.BF16)
+    w1, w2 = (rng.standard_normal((2, 3, 3, C, C)) * np.sqrt(2.0 / (9 * C))).astype(np.float32)
+    b1, b2 = (0.1 * rng.standard_normal((2, C))).astype(np.float32)
+    w1q, w2q = G.q(w1, G.BF16), G.q(w2, G.BF16)
+    t = G.empty_act((n, H, W, C), G.BF16)
+    y = G.empty_act((n, H, W, C), G.BF16)
+    P.impala_resblock_fwd(G.BF16, n, H, W, C, G.dev_act(x, G.BF16), G.dev_f32(w1), G.dev_f32(b1), G.dev_f32(w2),
+                          G.dev_f32(b2), t, y)
+    G.sync()
+    rx = _relu(x)
+    t_want = onet.conv3x3(rx, w1q, b1.astype(np.float64))
+    t_abs = onet.conv3x3(np.abs(rx), np.abs(w1q), np.abs(b1).astype(np.float64))
+    got_t = G.host(t)
+    G.assert_bf16_ulp(got_t, t_want, t_abs, "resblock t")
+    rt = _relu(got_t)
+    y_want = onet.conv3x3(rt, w2q, b2.astype(np.float64)) + x
+    y_abs = onet.conv3x3(np.abs(rt), np.abs(w2q), np.abs(b2).astype(np.float64)) + np.abs(x)
+    G.assert_bf16_ulp(G.host(y), y_want, y_abs, "resblock y")
+
+
+def test_resblock_rejects_unsupported():
+    x = G.dev_act(np.zeros((1, 8, 8, 64)), G.BF16)
+    w = G.dev_f32(np.zeros((3, 3, 64, 64)))
+    with pytest.raises(P.LibraryError):
+        P.impala_resblock_fwd(G.BF16, 1, 8, 8, 64, x, w, None, w, None, G.empty_act((1, 8, 8, 64), G.BF16),
+                              G.empty_act((1, 8, 8, 64), G.BF16))
+    x16 = G.dev_act(np.zeros((1, 8, 8, 16)), G.FP32)
+    w16 = G.dev_f32(np.zeros((3, 3, 16, 16)))
+    with pytest.raises(P.LibraryError):
+        P.impala_resblock_fwd(G.FP32, 1, 8, 8, 16, x16, w16, None, w16, None, G.empty_act((1, 8, 8, 16), G.FP32),
+                              G.empty_act((1, 8, 8, 16), G.FP32))
+
+
 DGRAD_CASES = [(3, 42, 42, 16, 16), (3, 42, 42, 16, 32), (4, 21, 21, 32, 32), (7, 11, 11, 32, 32),
                (2, 42, 42, 32, 64), (3, 21, 21, 64, 64), (2, 17, 23, 16, 64)]
 
