@@ -312,8 +312,16 @@ struct DmaGeom {
     __host__ __device__ static int op_bytes(int TH, int FR, int W) { return blocks(FR * TH * W * OCH) * 64 * 16; }
 };
 
+// Waves per SIMD the register allocation must allow: four (four 4-wave or two 8-wave
+// workgroups per CU, as the LDS budgets are sized), except the 64-output-channel tiles that
+// read their weights from LDS, whose accumulators need the registers of two.
+template <int CIN, int COUT, int MODE>
+constexpr int conv_min_waves() {
+    return (COUT >= 64 && (COUT / 16) * ((9 * CIN + 31) / 32) > 10) ? 2 : 4;
+}
+
 template <int CIN, int COUT, int MODE, int FLIP, int POOL, int NW>
-__global__ __launch_bounds__(64 * NW) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t) {
+__global__ __launch_bounds__(64 * NW, (conv_min_waves<CIN, COUT, MODE>())) void conv3x3_bf16_kernel(ConvArgs a, DmaTile t) {
     using D = DmaGeom<CIN, COUT, MODE>;
     using G = ConvGeom<PrecBF16, CIN>;
     using P = PrecBF16;
@@ -375,16 +383,32 @@ __global__ __launch_bounds__(64 * NW) void conv3x3_bf16_kernel(ConvArgs a, DmaTi
     // ---- per-lane B-fragment offsets from the lane's tap-(0,0) window pixel (bytes).
     // k = ks*32 + g*8 .. +7 covers taps k / CIN; past the 9 taps the fragment is zero.
     auto tap_off = [&](int tap) { return ((tap / 3) * TW + tap % 3) * PB; };
-    int boff[KSTEPS];
+    // With 16 input channels a k-step spans two taps, chosen by the lane group: a per-lane
+    // table. From 32 channels on the tap is the k-step's and only the channel slot is the
+    // lane's, so the offset is computed in place (no registers held across the loop).
+    constexpr bool BTAB = U8 || CIN < 32;
+    int boff[BTAB ? KSTEPS : 1];
+    if constexpr (BTAB) {
 #pragma unroll
-    for (int ks = 0; ks < KSTEPS; ++ks) {
-        if constexpr (U8) {
-            boff[ks] = 0;   // uint8 fragments are read per tap below
-        } else {
-            const int k0 = ks * 32 + g * 8, tap = k0 / CIN, c = (k0 % CIN) / 8;
-            boff[ks] = tap < 9 ? tap_off(tap) + c * 16 : (SPP - 1) * 16;   // zero slot
+        for (int ks = 0; ks < KSTEPS; ++ks) {
+            if constexpr (U8) {
+                boff[ks] = 0;   // uint8 fragments are read per tap below
+            } else {
+                const int k0 = ks * 32 + g * 8, tap = k0 / CIN, c = (k0 % CIN) / 8;
+                boff[ks] = tap < 9 ? tap_off(tap) + c * 16 : (SPP - 1) * 16;   // zero slot
+            }
         }
     }
+    const int twpb = TW * PB;
+    auto b_offset = [&](int ks) -> int {
+        if constexpr (BTAB) {
+            return boff[ks];
+        } else {
+            constexpr int TPK = CIN / 32;   // k-steps per tap
+            const int tap = ks / TPK, cs = (ks % TPK) * 4;
+            return (tap / 3) * twpb + (tap % 3) * PB + (cs + g) * 16;
+        }
+    };
     // uint8: lane g holds taps 2g, 2g+1 in k-step 0 and tap 8 (g == 0) in k-step 1
     const int u0 = tap_off(U8 ? 2 * g : 0), u1 = tap_off(U8 ? 2 * g + 1 : 0), u2 = tap_off(8);
 
@@ -481,41 +505,12 @@ __global__ __launch_bounds__(64 * NW) void conv3x3_bf16_kernel(ConvArgs a, DmaTi
             __syncthreads();
         }
 
-        // ---- implicit GEMM over the tile's output pixels, 16 per MFMA column tile
-        const int ntl = (npx + 15) >> 4;
-        for (int nt = wave; nt < ntl; nt += NW) {
-            const int q = nt * 16 + r16;
-            const int qc = q < npx ? q : npx - 1;
-            const int rowi = qdiv(qc, t.inv_W), col = qc - rowi * W;
-            int f = 0, r = rowi;
-            if (FR > 1) { f = qdiv(rowi, t.inv_TH); r = rowi - f * TH; }
-            const unsigned char* xb = win + ((f * TR + r) * TW + col) * PB;
-            cb_f32x4 acc[MT];
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) acc[mt] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int ks = 0; ks < KSTEPS; ++ks) {
-                uint4 b;
-                if constexpr (U8) {
-                    if (ks == 0) {
-                        const uint2 lo = *reinterpret_cast<const uint2*>(xb + u0);
-                        const uint2 hi = *reinterpret_cast<const uint2*>(xb + u1);
-                        b = make_uint4(lo.x, lo.y, hi.x, hi.y);
-                    } else {
-                        const uint2 lo = *reinterpret_cast<const uint2*>(xb + u2);
-                        b = g == 0 ? make_uint4(lo.x, lo.y, 0, 0) : make_uint4(0, 0, 0, 0);
-                    }
-                } else {
-                    b = *reinterpret_cast<const uint4*>(xb + boff[ks]);
-                }
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    uint4 af;
-                    if constexpr (HOIST) af = wreg[ks * MT + mt];
-                    else af = P::lds_frag(wl + (mt * 16 + r16) * KPITCH + ks * 32 + g * 8);
-                    acc[mt] = P::mma(af, b, acc[mt]);
-                }
-            }
+        // ---- implicit GEMM over the tile's output pixels, 16 per MFMA column tile. When the
+        // weight fragments come from LDS, each wave of the 8-wave variant takes NP = 2 column
+        // tiles per pass so every A-fragment read feeds two MFMAs (the 4-wave variant keeps
+        // one: the extra registers would cost it a resident workgroup per CU).
+        constexpr int NP = (HOIST || U8 || NW < 8) ? 1 : 2;
+        auto epilogue = [&](int q, int f, int r, int col, const cb_f32x4* acc) {
             if (POOL && q < npx) {
                 // the bf16 conv value as an order-preserving 16-bit key (pool compares keys)
                 unsigned char* cp = smem + t.ct_off + (q * COUT + g * 4) * 2;
@@ -551,6 +546,55 @@ __global__ __launch_bounds__(64 * NW) void conv3x3_bf16_kernel(ConvArgs a, DmaTi
                     store4(yp + mt * 16, v[0], v[1], v[2], v[3]);
                 }
             }
+        };
+        const int ntl = (npx + 15) >> 4;
+        for (int nt0 = wave; nt0 < ntl; nt0 += NW * NP) {
+            int qv[NP], fv[NP], rv[NP], cv[NP];
+            const unsigned char* xb[NP];
+#pragma unroll
+            for (int p = 0; p < NP; ++p) {
+                qv[p] = (nt0 + p * NW) * 16 + r16;   // past npx: clamped, computed, not stored
+                const int qc = qv[p] < npx ? qv[p] : npx - 1;
+                const int rowi = qdiv(qc, t.inv_W);
+                cv[p] = qc - rowi * W;
+                fv[p] = 0; rv[p] = rowi;
+                if (FR > 1) { fv[p] = qdiv(rowi, t.inv_TH); rv[p] = rowi - fv[p] * TH; }
+                xb[p] = win + ((fv[p] * TR + rv[p]) * TW + cv[p]) * PB;
+            }
+            cb_f32x4 acc[NP][MT];
+#pragma unroll
+            for (int p = 0; p < NP; ++p)
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) acc[p][mt] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KSTEPS; ++ks) {
+                uint4 b[NP];
+#pragma unroll
+                for (int p = 0; p < NP; ++p) {
+                    if constexpr (U8) {
+                        if (ks == 0) {
+                            const uint2 lo = *reinterpret_cast<const uint2*>(xb[p] + u0);
+                            const uint2 hi = *reinterpret_cast<const uint2*>(xb[p] + u1);
+                            b[p] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+                        } else {
+                            const uint2 lo = *reinterpret_cast<const uint2*>(xb[p] + u2);
+                            b[p] = g == 0 ? make_uint4(lo.x, lo.y, 0, 0) : make_uint4(0, 0, 0, 0);
+                        }
+                    } else {
+                        b[p] = *reinterpret_cast<const uint4*>(xb[p] + b_offset(ks));
+                    }
+                }
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    uint4 af;
+                    if constexpr (HOIST) af = wreg[ks * MT + mt];
+                    else af = P::lds_frag(wl + (mt * 16 + r16) * KPITCH + ks * 32 + g * 8);
+#pragma unroll
+                    for (int p = 0; p < NP; ++p) acc[p][mt] = P::mma(af, b[p], acc[p][mt]);
+                }
+            }
+#pragma unroll
+            for (int p = 0; p < NP; ++p) epilogue(qv[p], fv[p], rv[p], cv[p], acc[p]);
         }
 
         if constexpr (POOL) {

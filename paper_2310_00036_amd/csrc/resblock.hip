@@ -47,20 +47,26 @@ struct RbTile {
     float inv_W, inv_TW;
 };
 
-// The MFMAs of one 16-pixel column tile: acc[mt] += W[mt rows] * window(taps at xb).
-template <int C>
-CB_DEV void rb_mma(const unsigned char* xb, const int* boff, const uint16_t* wl, const uint4* wreg,
-                   int r16, int g, cb_f32x4* acc) {
+// The MFMAs of NP 16-pixel column tiles: acc[p][mt] += W[mt rows] * window(taps at xb[p]);
+// each A fragment read from LDS feeds all NP tiles.
+template <int C, int NP>
+CB_DEV void rb_mma(const unsigned char* const* xb, const int* boff, int twpb, const uint16_t* wl,
+                   const uint4* wreg, int r16, int g, cb_f32x4 (*acc)[C / 16]) {
     using G = RbGeom<C>;
 #pragma unroll
     for (int ks = 0; ks < G::KSTEPS; ++ks) {
-        const uint4 b = *reinterpret_cast<const uint4*>(xb + boff[ks]);
+        // 16 channels: per-lane table (a k-step spans two taps); 32: tap ks, lane's slot g
+        const int bo = C < 32 ? boff[ks] : (ks / 3) * twpb + (ks % 3) * G::PB + g * 16;
+        uint4 b[NP];
+#pragma unroll
+        for (int p = 0; p < NP; ++p) b[p] = *reinterpret_cast<const uint4*>(xb[p] + bo);
 #pragma unroll
         for (int mt = 0; mt < G::MT; ++mt) {
             uint4 af;
             if constexpr (G::HOIST) af = wreg[ks * G::MT + mt];
             else af = PrecBF16::lds_frag(wl + (mt * 16 + r16) * G::KPITCH + ks * 32 + g * 8);
-            acc[mt] = PrecBF16::mma(af, b, acc[mt]);
+#pragma unroll
+            for (int p = 0; p < NP; ++p) acc[p][mt] = PrecBF16::mma(af, b[p], acc[p][mt]);
         }
     }
 }
@@ -70,6 +76,7 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_fwd_kernel(ResBlockArgs a
     using G = RbGeom<C>;
     constexpr int NT = 64 * NW, KSTEPS = G::KSTEPS, KPITCH = G::KPITCH, MT = G::MT;
     constexpr int SPP = G::SPP, PB = G::PB, OCH = G::OCH;
+    constexpr int NP = 1;   // column tiles per pass (two would spill at 32 channels)
 
     extern __shared__ __align__(16) unsigned char smem[];
     uint16_t* wl1 = reinterpret_cast<uint16_t*>(smem);
@@ -110,13 +117,17 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_fwd_kernel(ResBlockArgs a
                 wr2[ks * MT + mt] = PrecBF16::lds_frag(wl2 + (mt * 16 + r16) * KPITCH + ks * 32 + g * 8);
             }
     }
-    // per-lane B-fragment offsets from the tap-(0,0) pixel (both windows share the pitch)
-    int boff[KSTEPS];
+    // per-lane B-fragment offsets from the tap-(0,0) pixel (both windows share the pitch);
+    // only 16 channels need the table
+    int boff[C < 32 ? KSTEPS : 1];
+    if constexpr (C < 32) {
 #pragma unroll
-    for (int ks = 0; ks < KSTEPS; ++ks) {
-        const int k0 = ks * 32 + g * 8, tap = k0 / C, c = (k0 % C) / 8;
-        boff[ks] = tap < 9 ? ((tap / 3) * TW + tap % 3) * PB + c * 16 : (SPP - 1) * 16;
+        for (int ks = 0; ks < KSTEPS; ++ks) {
+            const int k0 = ks * 32 + g * 8, tap = k0 / C, c = (k0 % C) / 8;
+            boff[ks] = tap < 9 ? ((tap / 3) * TW + tap % 3) * PB + c * 16 : (SPP - 1) * 16;
+        }
     }
+    const int twpb = TW * PB;
 
     int lg = blockIdx.x;   // neighbouring bands on one XCD
     if ((gridDim.x & 7) == 0) lg = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
@@ -178,14 +189,27 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_fwd_kernel(ResBlockArgs a
         // ---- conv1: t on rows [tr0, tr1)
         uint16_t* tbase = static_cast<uint16_t*>(a.t) + fo;
         const int npx1 = (tr1 - tr0) * W;
-        for (int nt = wave; nt * 16 < npx1; nt += NW) {
-            const int q = nt * 16 + r16;
-            const int qc = q < npx1 ? q : npx1 - 1;
-            const int rowi = qdiv(qc, t.inv_W), col = qc - rowi * W, tr = tr0 + rowi;
-            cb_f32x4 acc[MT];
+        for (int nt0 = wave; nt0 * 16 < npx1; nt0 += NW * NP) {
+          int qv[NP], trv[NP], cv[NP];
+          const unsigned char* xb[NP];
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) acc[mt] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
-            rb_mma<C>(xw + (tr * TW + col) * PB, boff, wl1, wr1, r16, g, acc);
+          for (int p = 0; p < NP; ++p) {
+              qv[p] = (nt0 + p * NW) * 16 + r16;
+              const int qc = qv[p] < npx1 ? qv[p] : npx1 - 1;
+              const int rowi = qdiv(qc, t.inv_W);
+              cv[p] = qc - rowi * W; trv[p] = tr0 + rowi;
+              xb[p] = xw + (trv[p] * TW + cv[p]) * PB;
+          }
+          cb_f32x4 accs[NP][MT];
+#pragma unroll
+          for (int p = 0; p < NP; ++p)
+#pragma unroll
+              for (int mt = 0; mt < MT; ++mt) accs[p][mt] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+          rb_mma<C, NP>(xb, boff, twpb, wl1, wr1, r16, g, accs);
+#pragma unroll
+          for (int p = 0; p < NP; ++p) {
+            const int q = qv[p], tr = trv[p], col = cv[p];
+            const cb_f32x4* acc = accs[p];
             if (q < npx1) {
                 const int h = h0 - 1 + tr;
                 const bool own = h >= h0 && h < h0 + the;
@@ -200,20 +224,33 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_fwd_kernel(ResBlockArgs a
                     *reinterpret_cast<uint2*>(twp + mt * 32) = make_uint2(relu_bf16x2(u0), relu_bf16x2(u1));
                 }
             }
+          }
         }
         __syncthreads();
 
         // ---- conv2 + residual: y on the band's rows
         uint16_t* ybase = static_cast<uint16_t*>(a.y) + fo;
         const int npx2 = the * W;
-        for (int nt = wave; nt * 16 < npx2; nt += NW) {
-            const int q = nt * 16 + r16;
-            const int qc = q < npx2 ? q : npx2 - 1;
-            const int r = qdiv(qc, t.inv_W), col = qc - r * W;
-            cb_f32x4 acc[MT];
+        for (int nt0 = wave; nt0 * 16 < npx2; nt0 += NW * NP) {
+          int qv[NP], rv[NP], cv[NP];
+          const unsigned char* xb[NP];
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) acc[mt] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
-            rb_mma<C>(tw + (r * TW + col) * PB, boff, wl2, wr2, r16, g, acc);
+          for (int p = 0; p < NP; ++p) {
+              qv[p] = (nt0 + p * NW) * 16 + r16;
+              const int qc = qv[p] < npx2 ? qv[p] : npx2 - 1;
+              rv[p] = qdiv(qc, t.inv_W); cv[p] = qc - rv[p] * W;
+              xb[p] = tw + (rv[p] * TW + cv[p]) * PB;
+          }
+          cb_f32x4 accs[NP][MT];
+#pragma unroll
+          for (int p = 0; p < NP; ++p)
+#pragma unroll
+              for (int mt = 0; mt < MT; ++mt) accs[p][mt] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+          rb_mma<C, NP>(xb, boff, twpb, wl2, wr2, r16, g, accs);
+#pragma unroll
+          for (int p = 0; p < NP; ++p) {
+            const int q = qv[p], r = rv[p], col = cv[p];
+            const cb_f32x4* acc = accs[p];
             if (q < npx2) {
                 uint16_t* yp = ybase + (uint32_t(h0 + r) * W + col) * C + g * 4;
                 const uint16_t* ap = reinterpret_cast<const uint16_t*>(xa) + q * C + g * 4;
@@ -226,6 +263,7 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_fwd_kernel(ResBlockArgs a
                            acc[mt][2] + b2.z + ad[2], acc[mt][3] + b2.w + ad[3]);
                 }
             }
+          }
         }
     }
 }
