@@ -71,7 +71,20 @@ def run_layer(P, key, n, steps):
         mode = P.X_U8 if "u8" in flags else (P.X_RELU if "relu" in flags else P.X_PLAIN)
         x = (torch.randint(0, 256, (n, h, w, 4), dtype=torch.uint8, device="cuda", generator=g)
              if mode == P.X_U8 else act(h, w, ci))
-        if fam == "conv_dgrad":   # key channels: dy (forward cout) x dx (forward cin)
+        if fam == "resblock_fwd":
+            w1, w2 = (torch.randn(3, 3, ci, ci, device="cuda", generator=g) * 0.1 for _ in range(2))
+            b1, b2 = torch.zeros(ci, device="cuda"), torch.zeros(ci, device="cuda")
+            x, tt, y = act(h, w, ci), act(h, w, ci), act(h, w, ci)
+            fn = lambda: P.impala_resblock_fwd(prec, n, h, w, ci, x, w1, b1, w2, b2, tt, y)  # noqa: E731
+        elif fam == "conv_bwd":     # key channels: forward cin x cout
+            dy, wt = act(h, w, co), torch.randn(3, 3, ci, co, device="cuda", generator=g) * 0.1
+            add = act(h, w, ci) if "add" in flags else None
+            dx = act(h, w, ci)
+            dw = torch.empty(3, 3, ci, co, device="cuda")
+            db = torch.empty(co, device="cuda")
+            ws = torch.empty(P.impala_conv3x3_bwd_workspace_bytes(prec, ci, co), dtype=torch.uint8, device="cuda")
+            fn = lambda: P.impala_conv3x3_bwd(prec, n, h, w, ci, co, dy, x, mode, wt, add, dx, dw, db, ws)  # noqa: E731
+        elif fam == "conv_dgrad":   # key channels: dy (forward cout) x dx (forward cin)
             wt = torch.randn(3, 3, co, ci, device="cuda", generator=g) * 0.1
             mask = act(h, w, co) if "mask" in flags else None
             add = act(h, w, co) if "add" in flags else None
@@ -181,6 +194,17 @@ def kernel_work(key, n, prec):
     parts = key.split("/")
     fam = parts[0]
     es = 2 if len(parts) > 1 and parts[1] == "bf16" else 4
+    if fam == "resblock_fwd":   # one pass: x in, t and y out
+        c = int(parts[2].split("x")[0])
+        h, w = map(int, parts[3].split("x"))
+        px = n * h * w
+        return "hbm", float(px * c * es * 3), "B", 2.0 * 2.0 * px * 9 * c * c
+    if fam == "conv_bwd":   # one pass: x, dy and the residual operand in, dx out
+        ci, co = map(int, parts[2].split("x"))
+        h, w = map(int, parts[3].split("x"))
+        px = n * h * w
+        b = px * es * (ci + co + ci + (ci if "add" in parts[4:] else 0))
+        return "hbm", float(b), "B", 2.0 * 2.0 * px * 9 * ci * co
     if fam in ("conv_fwd", "conv_dgrad", "wgrad", "conv_pool"):
         ci, co = map(int, parts[2].split("x"))
         h, w = map(int, parts[3].split("x"))
@@ -212,7 +236,8 @@ def kernel_work(key, n, prec):
 def source_digest(key):
     fam = key.split("/")[0]
     src = {"conv_fwd": "conv.hip", "conv_dgrad": "conv.hip", "conv_pool": "conv.hip", "wgrad": "wgrad.hip",
-           "gemm": "gemm.hip", "adam": "adam.hip", "pool_fwd": "pool.hip", "pool_bwd": "pool.hip"}.get(fam)
+           "gemm": "gemm.hip", "adam": "adam.hip", "pool_fwd": "pool.hip", "pool_bwd": "pool.hip",
+           "resblock_fwd": "resblock.hip", "conv_bwd": "convbwd.hip"}.get(fam)
     if not src:
         return None
     path = os.path.join(ROOT, "paper_2310_00036_amd", "csrc", src)

@@ -1,0 +1,394 @@
+// Backward pass of one 3x3 stride-1 SAME convolution in one kernel (bf16 storage, float32
+// accumulation on gfx950 MFMA). For y = conv(X, w) + b with X = relu(x) or x:
+//
+//   dx[p][ci]          = sum over taps and co of w[tap][ci][co] * dy[p - d(tap)][co]
+//                        (then * (x[p] > 0) when the conv read relu(x); then + add[p])
+//   dW[ky][kx][ci][co] = sum over pixels p of X[p + d(tap)][ci] * dy[p][co]
+//   db[co]             = sum over pixels p of dy[p][co]
+//
+// Computed separately, the input gradient and the weight gradient each read dy, and both
+// read x (once as the mask, once as the weight-gradient operand). Here one tile (FR frames x
+// TH rows x all W columns) stages the zero-padded windows of dy and of x in LDS once and both
+// gradients are formed from them, so each tensor crosses HBM once: dy, x and the optional
+// residual operand in, dx out. The weight gradient accumulates in registers over all tiles
+// of a workgroup and is written as one float32 partial per workgroup; a second kernel adds
+// the partials in a fixed order (deterministic, no atomics).
+//
+// Layouts in LDS:
+//   - dy window [FR][TH+2][W+2] pixels of CO/8 16-byte slots plus one zero slot: the input
+//     gradient reads 8 consecutive channels of one tap per lane (16 bytes) as its B
+//     fragment, an odd slot count spreads the 16 lanes over distinct banks, and the zero
+//     slot feeds the k-steps past the 9 taps;
+//   - x window [FR][TH+2][W+2] pixels of 2*CI bytes (+32 from 32 channels on); the weight
+//     gradient reads its fragments, pixel-consecutive, with the LDS transpose read
+//     (ds_read_b64_tr_b16), and the mask is read from it in the epilogue;
+//   - the residual operand for the tile's own pixels, [FR*TH*W][CI].
+// The input-gradient weights (taps rotated by 180 degrees, in/out channels swapped) live in
+// registers: each wave owns one 16-channel block of dx and holds its A fragments for all
+// k-steps, loaded once per workgroup.
+#include "common.h"
+#include "kernels.h"
+
+#include <algorithm>
+
+namespace cb {
+
+template <int CI, int CO>
+struct CbGeom {
+    static constexpr int DSL = CO / 8 + 1;               // dy window: 16-byte slots per pixel
+    static constexpr int DYP = DSL * 16;                 // dy window: bytes per pixel
+    static constexpr int XPB = CI * 2 + (CI >= 32 ? 32 : 0);   // x window: bytes per pixel
+    static constexpr int XSL = XPB / 16;
+    static constexpr int MTI = CI / 16, MTO = CO / 16;
+    static constexpr int KSD = (9 * CO + 31) / 32;       // input-gradient k-steps
+    static constexpr int NB = 9 * CI / 16;               // weight-gradient column blocks
+    static constexpr int NBB = NB + 1;                   // ... and the bias block
+    static constexpr int PSTRIDE = MTO * NBB * 256;      // floats per workgroup partial
+    // staging slots per lane (of an 8-wave workgroup) the tile planner stays within
+    static constexpr int MAXD = CO > CI ? 7 : 6, MAXX = 4, MAXA = 3;
+    __host__ __device__ static int blocks(int slots) { return (slots + 63) / 64; }
+};
+
+template <int CI, int CO, int MODE, int ADD, int NW>
+__global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbTile t) {
+    using G = CbGeom<CI, CO>;
+    constexpr int NT = 64 * NW;
+    constexpr int DSL = G::DSL, DYP = G::DYP, XPB = G::XPB, XSL = G::XSL;
+    constexpr int MTI = G::MTI, MTO = G::MTO, KSD = G::KSD, NB = G::NB, NBB = G::NBB;
+    constexpr int TPW = (NBB + NW - 1) / NW;   // weight-gradient column blocks per wave
+    constexpr int CB16 = CI / 16;
+    static_assert(NW % MTI == 0, "waves split evenly over the dx channel blocks");
+    static_assert(MODE == IN_PLAIN || MODE == IN_RELU, "bf16 activations");
+
+    extern __shared__ __align__(16) unsigned char smem[];
+    unsigned char* zero = smem;               // 64 zero bytes
+    unsigned char* dyw = smem + t.dy_off;
+    unsigned char* xw = smem + t.x_off + XPB;   // one zero guard pixel on either side
+    unsigned char* adt = smem + t.add_off;
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar branches
+    const int g = lane >> 4, r16 = lane & 15, jj = r16 >> 2, m = r16 & 3;
+    const int H = a.H, W = a.W, TH = t.TH, FR = t.FR;
+    const int TW = W + 2, TR = TH + 2;
+
+    if (tid < 16) reinterpret_cast<uint32_t*>(zero)[tid] = 0u;
+    // the x window's guard pixels (read only against zero dy padding, never staged)
+    if (tid < XPB / 4) {
+        reinterpret_cast<uint32_t*>(xw - XPB)[tid] = 0u;
+        reinterpret_cast<uint32_t*>(xw + t.x_guard)[tid] = 0u;
+    }
+
+    // ---- input gradient: this wave's dx channel block and its A fragments,
+    // A[o][k] = w[8 - tap][o][co] with k = tap * CO + co (zero past the 9 taps)
+    const int dmt = wave % MTI;
+    uint4 wf[KSD];
+#pragma unroll
+    for (int ks = 0; ks < KSD; ++ks) {
+        const int o = dmt * 16 + r16;
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int k = ks * 32 + g * 8 + j, tap = k / CO, co = k % CO;
+            v[j] = tap < 9 ? a.w[((8 - tap) * CI + o) * CO + co] : 0.f;
+        }
+        wf[ks] = make_uint4(pack2bf(v[0], v[1]), pack2bf(v[2], v[3]), pack2bf(v[4], v[5]), pack2bf(v[6], v[7]));
+    }
+    // its B fragments: byte offsets from the lane's tap-(0,0) dy-window pixel
+    int dboff[KSD];
+#pragma unroll
+    for (int ks = 0; ks < KSD; ++ks) {
+        const int k0 = ks * 32 + g * 8, tap = k0 / CO, slot = (k0 % CO) / 8;
+        dboff[ks] = tap < 9 ? ((tap / 3) * TW + tap % 3) * DYP + slot * 16 : (DSL - 1) * 16;
+    }
+    // ---- weight gradient: column blocks nb = wave + NW * i (16 input channels of one tap,
+    // or the bias block), each for all CO/16 output-channel blocks
+    int wboff[TPW];
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+        const int nb = wave + NW * i;
+        const int tap = nb / CB16, cb = nb % CB16;
+        wboff[i] = nb < NB ? ((tap / 3) * TW + tap % 3) * XPB + (cb * 16 + 4 * m) * 2 : 0;
+    }
+    cb_f32x4 wacc[TPW][MTO];
+#pragma unroll
+    for (int i = 0; i < TPW; ++i)
+#pragma unroll
+        for (int mo = 0; mo < MTO; ++mo) wacc[i][mo] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+    const uint4 ones = make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
+
+    // ---- staging offsets. Slot j of a window maps to the same frame / row / column of every
+    // tile, so each lane's byte offsets are formed once, relative to image row 0 of the tile's
+    // first frame; a tile adds h0 rows. Rows above the image come out negative and rows below
+    // it past the tile's frames: both fall outside the buffer resource and read as zero.
+    // Padding slots, padding columns and (multi-frame tiles) the halo rows between frames hold
+    // kOOB. Slot k of this wave is j = (wave + NW * k) * 64 + lane.
+    const int nsd = FR * TR * TW * DSL, nsx = FR * TR * TW * XSL, nsa = FR * TH * W * (CI / 8);
+    uint32_t od[G::MAXD], ox[G::MAXX], oa[ADD ? G::MAXA : 1];
+    auto win_off = [&](int j, int slots, int nreal, int cbytes) -> uint32_t {
+        const int p = j / slots, c = j - p * slots;
+        const int rowi = p / TW, col = p - rowi * TW;
+        const int f = rowi / TR, rr = rowi - f * TR;
+        if (j >= FR * TR * TW * slots || c >= nreal || col < 1 || col > W) return kOOB;
+        if (FR > 1 && (rr < 1 || rr > TH)) return kOOB;
+        return uint32_t(((f * H + rr - 1) * W + col - 1) * cbytes + c * 16);
+    };
+#pragma unroll
+    for (int k = 0; k < G::MAXD; ++k) od[k] = win_off((wave + NW * k) * 64 + lane, DSL, CO / 8, CO * 2);
+#pragma unroll
+    for (int k = 0; k < G::MAXX; ++k) ox[k] = win_off((wave + NW * k) * 64 + lane, XSL, CI / 8, CI * 2);
+    if constexpr (ADD) {
+#pragma unroll
+        for (int k = 0; k < G::MAXA; ++k) {
+            const int j = (wave + NW * k) * 64 + lane;
+            const int q = j / (CI / 8), c = j - q * (CI / 8);
+            const int rowi = q / W, col = q - rowi * W, f = rowi / TH, rr = rowi - f * TH;
+            oa[k] = j < nsa ? uint32_t(((f * H + rr) * W + col) * (CI * 2) + c * 16) : kOOB;
+        }
+    }
+
+    int lg = blockIdx.x;   // neighbouring tiles (which share halo rows) on one XCD
+    if ((gridDim.x & 7) == 0) lg = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+
+    for (int tile = lg; tile < t.ntiles; tile += gridDim.x) {
+        const int band = tile % t.nbands, fg = tile / t.nbands;
+        const int h0 = band * TH, f0 = fg * FR;
+        const int nf = a.n - f0 < FR ? a.n - f0 : FR;
+        const int the = H - h0 < TH ? H - h0 : TH;
+        const int npx = nf * the * W;   // FR > 1 only when a band is the whole frame
+        __syncthreads();   // the previous tile's LDS reads are done
+
+        // ---- stage the dy and x windows (rows h0-1 .. h0+TH) and the residual operand
+        {
+            const int64_t fpx = int64_t(f0) * H * W;
+            const auto rd = buf_rsrc(static_cast<const uint16_t*>(a.dy) + fpx * CO, uint32_t(nf) * H * W * CO * 2);
+            const auto rx = buf_rsrc(static_cast<const uint16_t*>(a.x) + fpx * CI, uint32_t(nf) * H * W * CI * 2);
+            const uint32_t hd = uint32_t(h0) * W * CO * 2, hx = uint32_t(h0) * W * CI * 2;
+#pragma unroll
+            for (int k = 0; k < G::MAXD; ++k)
+                if ((wave + NW * k) * 64 < nsd) dma16_to_lds(rd, dyw + (wave + NW * k) * 1024, od[k] + hd);
+#pragma unroll
+            for (int k = 0; k < G::MAXX; ++k)
+                if ((wave + NW * k) * 64 < nsx) dma16_to_lds(rx, xw + (wave + NW * k) * 1024, ox[k] + hx);
+            if constexpr (ADD) {
+                const auto ra = buf_rsrc(static_cast<const uint16_t*>(a.add) + fpx * CI, uint32_t(nf) * H * W * CI * 2);
+#pragma unroll
+                for (int k = 0; k < G::MAXA; ++k)
+                    if ((wave + NW * k) * 64 < nsa) dma16_to_lds(ra, adt + (wave + NW * k) * 1024, oa[k] + hx);
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0);   // this wave's loads have landed in LDS
+        __syncthreads();                 // ... and everyone else's
+        if constexpr (MODE == IN_RELU) {
+            // the conv read relu(x); relu(x) > 0 exactly where x > 0, so the mask reads it too
+            uint4* w4 = reinterpret_cast<uint4*>(xw);
+            for (int j = tid; j < FR * TR * TW * XSL; j += NT) {
+                uint4 v = w4[j];
+                v.x = relu_bf16x2(v.x); v.y = relu_bf16x2(v.y); v.z = relu_bf16x2(v.z); v.w = relu_bf16x2(v.w);
+                w4[j] = v;
+            }
+            __syncthreads();
+        }
+
+        // ---- weight gradient over the band's window rows, padding columns included (dy is
+        // zero there, so they add nothing): pixel p = TW + ks*32 + o of the dy window pairs with
+        // x-window pixel p - TW - 1 + tap, and every address advances by a constant per k-step.
+        // Lane (g, 4jj+m) takes pixels o = 16*half + 4g + jj (dy / x channels 4m.. of a block).
+        // Between frames of a multi-frame tile the two halo rows are outside the image: zero dy.
+        {
+            const int L = ((nf - 1) * TR + the) * TW;   // contracted window pixels
+            const int nfull = L >> 5;
+            const int o0 = 4 * g + jj;
+            const unsigned char* ap = dyw + (TW + o0) * DYP + 8 * m;
+            const unsigned char* bp = xw + (o0 - 1) * XPB;
+            auto kstep = [&](const unsigned char* a0, const unsigned char* a1, const unsigned char* b0,
+                             const unsigned char* b1) {
+                uint4 af[MTO];
+#pragma unroll
+                for (int mo = 0; mo < MTO; ++mo) {
+                    const uint2 lo = lds_read_tr16(a0 + mo * 32);   // a0, a1: zero for pixels past L
+                    const uint2 hi = lds_read_tr16(a1 + mo * 32);
+                    af[mo] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+                }
+#pragma unroll
+                for (int i = 0; i < TPW; ++i) {
+                    const int nb = wave + NW * i;
+                    if (nb >= NBB) continue;
+                    uint4 bf = ones;
+                    if (nb < NB) {
+                        const uint2 lo = lds_read_tr16(b0 + wboff[i]);
+                        const uint2 hi = lds_read_tr16(b1 + wboff[i]);
+                        bf = make_uint4(lo.x, lo.y, hi.x, hi.y);
+                    }
+#pragma unroll
+                    for (int mo = 0; mo < MTO; ++mo) wacc[i][mo] = PrecBF16::mma(af[mo], bf, wacc[i][mo]);
+                }
+            };
+#pragma unroll 2
+            for (int ks = 0; ks < nfull; ++ks) {
+                kstep(ap, ap + 16 * DYP, bp, bp + 16 * XPB);
+                ap += 32 * DYP;
+                bp += 32 * XPB;
+            }
+            if (L & 31) {   // the last, partial k-step: pixels past L read zero dy
+                const int o = nfull * 32 + o0;
+                const bool ok0 = o < L, ok1 = o + 16 < L;
+                kstep(ok0 ? ap : zero, ok1 ? ap + 16 * DYP : zero, ok0 ? bp : xw - XPB,
+                      ok1 ? bp + 16 * XPB : xw - XPB);
+            }
+        }
+
+        // ---- input gradient: 16-pixel column tiles of this wave's dx channel block. Band pixel
+        // q sits at window row q / W (+ 2 per earlier frame of a multi-frame tile), and dx and
+        // the residual operand are addressed by q itself from the tile's first pixel.
+        {
+            uint16_t* dxt = static_cast<uint16_t*>(a.dx) + (int64_t(f0) * H + h0) * W * CI;
+            const int ntl = (npx + 15) >> 4;
+            for (int nt = wave / MTI; nt < ntl; nt += NW / MTI) {
+                const int q = nt * 16 + r16;
+                const int qc = q < npx ? q : npx - 1;   // past npx: computed, not stored
+                const int row = qdiv(qc, t.inv_W), col = qc - row * W;
+                const int wrow = FR > 1 ? row + 2 * qdiv(row, t.inv_TH) : row;
+                const int wpx = wrow * TW + col;
+                const unsigned char* xb = dyw + wpx * DYP;
+                cb_f32x4 acc = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < KSD; ++ks)
+                    acc = PrecBF16::mma(wf[ks], *reinterpret_cast<const uint4*>(xb + dboff[ks]), acc);
+                if (q < npx) {
+                    const int ci0 = dmt * 16 + g * 4;
+                    float v[4] = {acc[0], acc[1], acc[2], acc[3]};
+                    if constexpr (MODE == IN_RELU) {
+                        float mk[4];
+                        load4(reinterpret_cast<const uint16_t*>(xw + (wpx + TW + 1) * XPB + ci0 * 2), mk);
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) v[j] = mk[j] > 0.f ? v[j] : 0.f;
+                    }
+                    if constexpr (ADD) {
+                        float ad[4];
+                        load4(reinterpret_cast<const uint16_t*>(adt + (q * CI + ci0) * 2), ad);
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) v[j] += ad[j];
+                    }
+                    store4(dxt + uint32_t(q * CI + ci0), v[0], v[1], v[2], v[3]);
+                }
+            }
+        }
+    }
+
+    // ---- this workgroup's weight-gradient partial: [mo*NBB + nb][row co 16][col ci 16]
+    float* part = a.partial + int64_t(blockIdx.x) * G::PSTRIDE;
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) {
+        const int nb = wave + NW * i;
+        if (nb < NBB) {
+#pragma unroll
+            for (int mo = 0; mo < MTO; ++mo)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) part[(mo * NBB + nb) * 256 + (4 * g + e) * 16 + r16] = wacc[i][mo][e];
+        }
+    }
+}
+
+namespace {
+
+constexpr int kCbWaves = 8;
+constexpr size_t kCbLdsTarget = 80 * 1024;   // two 8-wave workgroups per CU
+constexpr int kCbPixMax = 2048;
+constexpr size_t kCbPartBytes = 24u << 20;
+
+template <int CI, int CO>
+int cb_parts_cap() {
+    const size_t cap = kCbPartBytes / (size_t(CbGeom<CI, CO>::PSTRIDE) * sizeof(float));
+    return int(cap < 256 ? 256 : (cap > 1024 ? 1024 : cap));
+}
+
+template <int CI, int CO, int MODE, int ADD>
+hipError_t cb_launch(const ConvBwdArgs& a, hipStream_t s) {
+    using G = CbGeom<CI, CO>;
+    const int H = a.H, W = a.W;
+    auto regions = [&](int th, int fr, int& dyb, int& xb, int& ab) {
+        const int wp = fr * (th + 2) * (W + 2);
+        dyb = G::blocks(wp * G::DSL) * 1024;
+        xb = G::blocks(wp * G::XSL) * 1024 + 2 * G::XPB;   // + a guard pixel on either side
+        ab = ADD ? G::blocks(fr * th * W * (CI / 8)) * 1024 : 0;
+    };
+    auto lds = [&](int th, int fr) {
+        int dyb, xb, ab;
+        regions(th, fr, dyb, xb, ab);
+        return size_t(64 + dyb + xb + ab);
+    };
+    // staging slots per lane within the kernel's register tables
+    auto fits = [&](int th, int fr) {
+        const int per = kCbWaves * 64, wp = fr * (th + 2) * (W + 2);
+        return (wp * G::DSL + per - 1) / per <= G::MAXD && (wp * G::XSL + per - 1) / per <= G::MAXX &&
+               (!ADD || (fr * th * W * (CI / 8) + per - 1) / per <= G::MAXA);
+    };
+    const size_t limit = std::min<size_t>(lds_limit(), 160 * 1024);
+    int thmax = std::min(H, std::max(1, kCbPixMax / W));
+    while (thmax > 1 && (lds(thmax, 1) > kCbLdsTarget || !fits(thmax, 1))) --thmax;
+    if (lds(thmax, 1) > limit || !fits(thmax, 1)) return hipErrorInvalidValue;
+    int TH = 1, best = 1 << 30;   // band height staging the fewest window rows per frame
+    for (int th = 1; th <= thmax; ++th) {
+        const int rows = (H + th - 1) / th * (th + 2);
+        if (rows <= best) { best = rows; TH = th; }
+    }
+    const int nbands = (H + TH - 1) / TH;
+    int FR = 1;
+    if (nbands == 1)
+        while (FR < a.n && lds(TH, FR + 1) <= kCbLdsTarget && fits(TH, FR + 1) && (FR + 1) * H * W <= kCbPixMax) ++FR;
+    // 32-bit buffer offsets cover FR frames of each operand
+    if (int64_t(FR) * H * W * std::max(CI, CO) * 2 >= (int64_t(1) << 31)) return hipErrorInvalidValue;
+    CbTile t{};
+    t.TH = TH; t.FR = FR; t.nbands = nbands; t.ntiles = nbands * ((a.n + FR - 1) / FR);
+    int dyb, xb, ab;
+    regions(TH, FR, dyb, xb, ab);
+    t.dy_off = 64; t.x_off = t.dy_off + dyb; t.add_off = t.x_off + xb;
+    t.x_guard = xb - 2 * G::XPB;   // byte offset of the rear guard from the window start
+    t.inv_W = 1.f / float(W); t.inv_TW = 1.f / float(W + 2);
+    t.inv_TH = 1.f / float(TH); t.inv_TR = 1.f / float(TH + 2);
+    const size_t L = lds(TH, FR);
+    const void* fn = reinterpret_cast<const void*>(&conv_bwd_kernel<CI, CO, MODE, ADD, kCbWaves>);
+    int parts = std::min(resident_blocks(fn, 64 * kCbWaves, L), cb_parts_cap<CI, CO>());
+    if (parts > t.ntiles) parts = t.ntiles;
+    const std::string shape = cb_dims(CI, CO) + "/" + cb_dims(H, W) + cb_flags(MODE, false, ADD);
+    {
+        ProfScope ps(s, [&] { return cb_key("conv_bwd", 0, shape); });
+        hipLaunchKernelGGL((conv_bwd_kernel<CI, CO, MODE, ADD, kCbWaves>), dim3(unsigned(parts)), dim3(64 * kCbWaves),
+                           L, s, a, t);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    ProfScope ps(s, [&] { return cb_key("conv_bwd_reduce", 0, shape); });
+    return wgrad_reduce_tr(CI, CO, a.partial, parts, a.dw, a.db, 1.f, s);
+}
+
+}  // namespace
+
+bool conv3x3_bwd_supported(int cin, int cout, int mode, int add) {
+    if (mode == IN_RELU) return cin == cout && (cin == 16 || cin == 32);
+    if (mode == IN_PLAIN) return !add && ((cin == 16 && (cout == 16 || cout == 32)) || (cin == 32 && cout == 32));
+    return false;
+}
+
+size_t conv3x3_bwd_partial_floats(int cin, int cout) {
+    size_t best = 0;
+#define CB_PF(CI, CO) \
+    if (cin == CI && cout == CO) best = size_t(cb_parts_cap<CI, CO>()) * CbGeom<CI, CO>::PSTRIDE;
+    CB_PF(16, 16) CB_PF(16, 32) CB_PF(32, 32)
+#undef CB_PF
+    return best;
+}
+
+hipError_t conv3x3_bwd(int cin, int cout, int mode, const ConvBwdArgs& a, hipStream_t s) {
+    if (a.n <= 0) return hipSuccess;
+    const int add = a.add != nullptr;
+#define CB_B(CI, CO, MD, AD) \
+    if (cin == CI && cout == CO && mode == MD && add == AD) return cb_launch<CI, CO, MD, AD>(a, s);
+    CB_B(16, 16, IN_RELU, 0) CB_B(16, 16, IN_RELU, 1) CB_B(32, 32, IN_RELU, 0) CB_B(32, 32, IN_RELU, 1)
+    CB_B(16, 16, IN_PLAIN, 0) CB_B(16, 32, IN_PLAIN, 0) CB_B(32, 32, IN_PLAIN, 0)
+#undef CB_B
+    return hipErrorInvalidValue;
+}
+
+}  // namespace cb

@@ -61,6 +61,34 @@ hipError_t conv3x3_wgrad(int prec, int cin, int cout, int mode, const WgradArgs&
                          hipStream_t s);
 bool wgrad_supported(int cin, int cout, int mode);
 
+// ---- whole backward pass of one 3x3 SAME conv (bf16): input gradient and weight gradient
+//      from one staging of dy and x. Forward: y = conv(X, w) + b, X = relu(x) (IN_RELU) or x.
+struct ConvBwdArgs {
+    const void* dy;         // [n, H, W, cout] bf16
+    const void* x;          // [n, H, W, cin] bf16, the forward input as stored
+    const float* w;         // float32 HWIO [3,3,cin,cout]
+    const void* add;        // [n, H, W, cin] added to dx, or NULL
+    void* dx;               // [n, H, W, cin]: conv^T(dy) * (x > 0 if IN_RELU) + add
+    float* dw;              // float32 HWIO [3,3,cin,cout]
+    float* db;              // float32 [cout]
+    float* partial;         // workspace, conv3x3_bwd_partial_floats() floats
+    int n, H, W;
+};
+struct CbTile {
+    int TH, FR, nbands, ntiles;
+    int dy_off, x_off, add_off;   // LDS byte offsets; 64 zero bytes at offset 0
+    int x_guard;                  // x window: byte offset of its rear guard pixel
+    float inv_W, inv_TW, inv_TH, inv_TR;
+};
+bool conv3x3_bwd_supported(int cin, int cout, int mode, int add);
+size_t conv3x3_bwd_partial_floats(int cin, int cout);
+hipError_t conv3x3_bwd(int cin, int cout, int mode, const ConvBwdArgs& a, hipStream_t s);
+// Fixed-order sum of nparts bf16 weight-gradient partials laid out [mt*(9*cin/16+1) + nb]
+// [co 16][ci 16] (the last column block holds the bias sums), scattered to HWIO dw (times
+// scale) and db.
+hipError_t wgrad_reduce_tr(int cin, int cout, const float* partial, int nparts, float* dw, float* db,
+                           float scale, hipStream_t s);
+
 // ---- 3x3 stride-2 SAME max-pool (XLA padding split), first-max argmax in 0..8
 hipError_t maxpool_fwd(int prec, int n, int H, int W, int C, const void* x, void* y,
                        uint8_t* arg, hipStream_t s);

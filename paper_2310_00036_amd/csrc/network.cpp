@@ -113,6 +113,10 @@ NetPlan make_plan(const impala_net_t& net, int prec, int64_t cap, int training) 
         for (int s = 0; s < 3; ++s) {
             sc = std::max(sc, wgrad_partial_floats(prec, p.C[s], p.C[s + 1], p.H[s], p.W[s]));
             sc = std::max(sc, wgrad_partial_floats(prec, p.C[s + 1], p.C[s + 1], p.H[s + 1], p.W[s + 1]));
+            if (prec == BF16) {
+                sc = std::max(sc, conv3x3_bwd_partial_floats(p.C[s], p.C[s + 1]));
+                sc = std::max(sc, conv3x3_bwd_partial_floats(p.C[s + 1], p.C[s + 1]));
+            }
         }
         sc = std::max(sc, colsum_partial_floats(std::max(p.hidden, p.A + 1)));
     }
@@ -272,6 +276,21 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
             int fa, fb;
             others(gy, fa, fb);
             const int k0 = 1 + 2 * r, k1 = 2 + 2 * r;
+            if (p.prec == BF16 && conv3x3_bwd_supported(C, C, IN_RELU, 1)) {
+                // each conv's input and weight gradients from one staging of its dy and input
+                ConvBwdArgs c1{};
+                c1.dy = G[gy]; c1.x = ws + p.t[st][r]; c1.w = params + po.conv_w[st][k1]; c1.dx = G[fa];
+                c1.dw = grads + po.conv_w[st][k1]; c1.db = grads + po.conv_b[st][k1]; c1.partial = scratch;
+                c1.n = int(n); c1.H = Hs; c1.W = Ws;
+                CB_TRY(conv3x3_bwd(C, C, IN_RELU, c1, s));
+                ConvBwdArgs c0{};
+                c0.dy = G[fa]; c0.x = ws + p.x[st][r]; c0.w = params + po.conv_w[st][k0]; c0.add = G[gy];
+                c0.dx = G[fb]; c0.dw = grads + po.conv_w[st][k0]; c0.db = grads + po.conv_b[st][k0];
+                c0.partial = scratch; c0.n = int(n); c0.H = Hs; c0.W = Ws;
+                CB_TRY(conv3x3_bwd(C, C, IN_RELU, c0, s));
+                gy = fb;
+                continue;
+            }
             // y = x + conv1(relu(t)) + b1 with t = conv0(relu(x)) + b0
             WgradArgs w1{};
             w1.x = ws + p.t[st][r]; w1.dy = G[gy]; w1.dw = grads + po.conv_w[st][k1];
@@ -298,6 +317,15 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
         others(gy, fa, fb);
         CB_TRY(maxpool_bwd(p.prec, int(n), p.H[st], p.W[st], C,
                            reinterpret_cast<const uint8_t*>(ws + p.idx[st]), G[gy], G[fa], s));
+        if (st > 0 && p.prec == BF16 && conv3x3_bwd_supported(p.C[st], C, IN_PLAIN, 0)) {
+            ConvBwdArgs ce{};
+            ce.dy = G[fa]; ce.x = ws + p.x[st - 1][2]; ce.w = params + po.conv_w[st][0]; ce.dx = G[fb];
+            ce.dw = grads + po.conv_w[st][0]; ce.db = grads + po.conv_b[st][0]; ce.partial = scratch;
+            ce.n = int(n); ce.H = p.H[st]; ce.W = p.W[st];
+            CB_TRY(conv3x3_bwd(p.C[st], C, IN_PLAIN, ce, s));
+            gy = fb;
+            continue;
+        }
         WgradArgs we{};
         we.x = st == 0 ? static_cast<const void*>(obs) : static_cast<const void*>(ws + p.x[st - 1][2]);
         we.row_idx = st == 0 ? row_idx : nullptr;

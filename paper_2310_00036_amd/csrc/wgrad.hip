@@ -678,6 +678,20 @@ size_t pstride() { return WgGeom<PrecF32, CIN, COUT>::PSTRIDE; }
 
 }  // namespace
 
+hipError_t wgrad_reduce_tr(int cin, int cout, const float* partial, int nparts, float* dw, float* db,
+                           float scale, hipStream_t s) {
+#define CB_RT(CI, CO)                                                                                  \
+    if (cin == CI && cout == CO) {                                                                     \
+        hipLaunchKernelGGL((wgrad_tr_reduce_kernel<CI, CO, IN_PLAIN>),                                 \
+                           dim3((WgTr<CI, CO, IN_PLAIN>::PSTRIDE + 15) / 16), dim3(1024), 0, s, partial, \
+                           nparts, dw, db, scale);                                                     \
+        return hipGetLastError();                                                                      \
+    }
+    CB_RT(16, 16) CB_RT(16, 32) CB_RT(32, 32)
+#undef CB_RT
+    return hipErrorInvalidValue;
+}
+
 bool wgrad_supported(int cin, int cout, int mode) {
     auto ok = [](int c) { return c == 16 || c == 32 || c == 64; };
     if (mode == IN_U8) return cin == 4 && ok(cout);

@@ -200,6 +200,65 @@ def test_conv_input_gradient(case, prec, epi):
         G.assert_sum_close(G.host(out), want, absum, 1e-5, "dgrad")
 
 
+# (n, H, W, cin, cout, x_mode, add): the network's backward convs (residual convs read relu(x),
+# the second of a block adds the block's output gradient; stage entries read x as stored)
+# plus ragged shapes, many frames per tile and several bands per frame
+CONV_BWD_CASES = [
+    (3, 42, 42, 16, 16, P.X_RELU, 1), (2, 42, 42, 16, 16, P.X_RELU, 0), (4, 21, 21, 32, 32, P.X_RELU, 1),
+    (3, 21, 21, 32, 32, P.X_RELU, 0), (5, 11, 11, 32, 32, P.X_RELU, 1), (37, 11, 11, 32, 32, P.X_RELU, 0),
+    (3, 42, 42, 16, 32, P.X_PLAIN, 0), (2, 21, 21, 32, 32, P.X_PLAIN, 0), (2, 17, 23, 16, 16, P.X_RELU, 1),
+    (3, 9, 7, 32, 32, P.X_RELU, 1), (1, 84, 84, 16, 16, P.X_RELU, 1), (6, 5, 3, 16, 32, P.X_PLAIN, 0),
+]
+
+
+@pytest.mark.parametrize("case", CONV_BWD_CASES, ids=lambda c: "n%d_%dx%d_%d-%d_m%d_a%d" % c)
+def test_conv_backward_fused(case):
+    """One-pass conv backward (bf16): dx against the exact adjoint (masked by x > 0 for relu
+    inputs, plus the residual operand) to 1 bf16 ulp, dw and db against the exact sums."""
+    n, H, W, cin, cout, mode, has_add = case
+    rng = np.random.default_rng(41)
+    x = G.q(rng.standard_normal((n, H, W, cin)), G.BF16)
+    dy = G.q(rng.standard_normal((n, H, W, cout)), G.BF16)
+    add = G.q(rng.standard_normal((n, H, W, cin)), G.BF16) if has_add else None
+    w = (rng.standard_normal((3, 3, cin, cout)) * np.sqrt(2.0 / (9 * cin))).astype(np.float32)
+    wq = G.q(w, G.BF16)
+    xin = _relu(x) if mode == P.X_RELU else x
+    want = onet.conv3x3_dgrad(dy, wq)
+    absum = onet.conv3x3_dgrad(np.abs(dy), np.abs(wq))
+    if mode == P.X_RELU:
+        want, absum = want * (x > 0), absum * (x > 0)
+    if add is not None:
+        want, absum = want + add, absum + np.abs(add)
+    want_w, want_b = onet.conv3x3_wgrad(xin, dy)
+    abs_w, abs_b = onet.conv3x3_wgrad(np.abs(xin), np.abs(dy))
+    dx = G.empty_act((n, H, W, cin), G.BF16)
+    dw = G.dev_f32(np.full((3, 3, cin, cout), np.nan))
+    db = G.dev_f32(np.full(cout, np.nan))
+    ws = G.ws_bytes(P.impala_conv3x3_bwd_workspace_bytes(G.BF16, cin, cout))
+    P.impala_conv3x3_bwd(G.BF16, n, H, W, cin, cout, G.dev_act(dy, G.BF16), G.dev_act(x, G.BF16), mode,
+                         G.dev_f32(w), G.dev_act(add, G.BF16) if add is not None else None, dx, dw, db, ws)
+    G.sync()
+    G.assert_bf16_ulp(G.host(dx), want, absum, "conv_bwd dx")
+    G.assert_sum_close(G.host(dw), want_w, abs_w, 1e-5, "conv_bwd dw")
+    G.assert_sum_close(G.host(db), want_b, abs_b, 1e-5, "conv_bwd db")
+
+
+def test_conv_backward_fused_rejects_unsupported():
+    ws = G.ws_bytes(1 << 20)
+    z = G.dev_act(np.zeros((1, 8, 8, 64)), G.BF16)
+    w = G.dev_f32(np.zeros((3, 3, 64, 64)))
+    dw, db = G.dev_f32(np.zeros((3, 3, 64, 64))), G.dev_f32(np.zeros(64))
+    with pytest.raises(P.LibraryError):   # 64 channels: not in the fused set
+        P.impala_conv3x3_bwd(G.BF16, 1, 8, 8, 64, 64, z, z, P.X_RELU, w, None, z, dw, db, ws)
+    z16 = G.dev_act(np.zeros((1, 8, 8, 16)), G.FP32)
+    w16 = G.dev_f32(np.zeros((3, 3, 16, 16)))
+    with pytest.raises(P.LibraryError):   # float32 storage
+        P.impala_conv3x3_bwd(G.FP32, 1, 8, 8, 16, 16, z16, z16, P.X_RELU, w16, None, z16, dw, db, ws)
+    b16 = G.dev_act(np.zeros((1, 8, 8, 16)), G.BF16)
+    with pytest.raises(P.LibraryError):   # too small a workspace
+        P.impala_conv3x3_bwd(G.BF16, 1, 8, 8, 16, 16, b16, b16, P.X_RELU, w16, None, b16, dw, db, G.ws_bytes(16))
+
+
 @pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
 @pytest.mark.parametrize("case", CONV_CASES, ids=lambda c: "n%d_%dx%d_%d-%d_m%d" % c)
 def test_conv_weight_gradient(case, prec):
