@@ -71,7 +71,16 @@ def run_layer(P, key, n, steps):
         mode = P.X_U8 if "u8" in flags else (P.X_RELU if "relu" in flags else P.X_PLAIN)
         x = (torch.randint(0, 256, (n, h, w, 4), dtype=torch.uint8, device="cuda", generator=g)
              if mode == P.X_U8 else act(h, w, ci))
-        if fam == "resblock_fwd":
+        if fam == "pool_wgrad":
+            oh, ow = (h + 1) // 2, (w + 1) // 2
+            dp = act(oh, ow, co)
+            arg = torch.randint(0, 9, (n, oh, ow, co), dtype=torch.uint8, device="cuda", generator=g)
+            dw = torch.empty(3, 3, 4, co, device="cuda")
+            db = torch.empty(co, device="cuda")
+            ws = torch.empty(P.impala_conv3x3_pool_wgrad_u8_workspace_bytes(prec, co), dtype=torch.uint8,
+                             device="cuda")
+            fn = lambda: P.impala_conv3x3_pool_wgrad_u8(prec, n, h, w, co, x, None, dp, arg, dw, db, ws)  # noqa: E731
+        elif fam == "resblock_fwd":
             w1, w2 = (torch.randn(3, 3, ci, ci, device="cuda", generator=g) * 0.1 for _ in range(2))
             b1, b2 = torch.zeros(ci, device="cuda"), torch.zeros(ci, device="cuda")
             x, tt, y = act(h, w, ci), act(h, w, ci), act(h, w, ci)
@@ -199,6 +208,11 @@ def kernel_work(key, n, prec):
         h, w = map(int, parts[3].split("x"))
         px = n * h * w
         return "hbm", float(px * c * es * 3), "B", 2.0 * 2.0 * px * 9 * c * c
+    if fam == "pool_wgrad":   # one pass: frames, pooled gradient and argmax in
+        co = int(parts[2].split("x")[1])
+        h, w = map(int, parts[3].split("x"))
+        oh, ow = (h + 1) // 2, (w + 1) // 2
+        return "hbm", float(n * (h * w * 4 + oh * ow * co * (es + 1))), "B", 2.0 * n * h * w * 36 * co
     if fam == "conv_bwd":   # one pass: x, dy and the residual operand in, dx out
         ci, co = map(int, parts[2].split("x"))
         h, w = map(int, parts[3].split("x"))
@@ -237,7 +251,7 @@ def source_digest(key):
     fam = key.split("/")[0]
     src = {"conv_fwd": "conv.hip", "conv_dgrad": "conv.hip", "conv_pool": "conv.hip", "wgrad": "wgrad.hip",
            "gemm": "gemm.hip", "adam": "adam.hip", "pool_fwd": "pool.hip", "pool_bwd": "pool.hip",
-           "resblock_fwd": "resblock.hip", "conv_bwd": "convbwd.hip"}.get(fam)
+           "resblock_fwd": "resblock.hip", "conv_bwd": "convbwd.hip", "pool_wgrad": "poolwgrad.hip"}.get(fam)
     if not src:
         return None
     path = os.path.join(ROOT, "paper_2310_00036_amd", "csrc", src)

@@ -93,6 +93,23 @@ impala_status_t impala_conv3x3_bwd(impala_prec_t prec, int64_t n, int32_t H, int
                                    const float* w, const void* add, void* dx, float* dw, float* db,
                                    void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Backward of the first stage entry of Section 5's IMPALA-ResNet, y = maxpool3x3s2_same(
+ * conv3x3_same(frames / 255, w) + bias), in one pass, bf16 only (Algorithm 1's
+ * back-propagation; the frames need no input gradient): the max-pool's input gradient
+ * dC (as impala_maxpool_bwd forms it, rounded to bf16) is built on chip from the gradient
+ * at the pool output and the pool argmax, and feeds the weight gradient directly, so the
+ * result equals impala_maxpool_bwd followed by impala_conv3x3_wgrad (IMPALA_X_U8).
+ * obs: uint8 frames; frame i is obs[row_idx[i]] (row_idx may be NULL), [*, H, W, 4].
+ * dpool (bf16) and arg (uint8): [n, ceil(H/2), ceil(W/2), cout]. dw: float [3,3,4,cout];
+ * db: float [cout] (both overwritten). ws: device scratch of
+ * impala_conv3x3_pool_wgrad_u8_workspace_bytes() bytes. cout must be 16 or 32, else
+ * IMPALA_EUNSUPPORTED (as for IMPALA_PREC_FP32). */
+size_t impala_conv3x3_pool_wgrad_u8_workspace_bytes(impala_prec_t prec, int32_t cout);
+impala_status_t impala_conv3x3_pool_wgrad_u8(impala_prec_t prec, int64_t n, int32_t H, int32_t W,
+                                             int32_t cout, const uint8_t* obs, const int32_t* row_idx,
+                                             const void* dpool, const uint8_t* arg, float* dw, float* db,
+                                             void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* 3x3 stride-2 SAME max-pool with XLA's padding split (pad_lo = P/2) and -inf padding.
  * x: [n, H, W, C]; y: [n, ceil(H/2), ceil(W/2), C]; arg: uint8, same shape as y, the
  * row-major window index 0..8 of the first maximum. C % 4 == 0, C <= 256. */

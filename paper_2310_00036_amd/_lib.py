@@ -77,6 +77,9 @@ _SIGS = {
     "impala_conv3x3_bwd_workspace_bytes": (_SZ, [C.c_int, _I32, _I32]),
     "impala_conv3x3_bwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _I32, _P, _P, _I32, _P, _P, _P, _P, _P,
                                      _P, _SZ, _P]),
+    "impala_conv3x3_pool_wgrad_u8_workspace_bytes": (_SZ, [C.c_int, _I32]),
+    "impala_conv3x3_pool_wgrad_u8": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _SZ,
+                                               _P]),
     "impala_maxpool_fwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _P, _P, _P, _P]),
     "impala_maxpool_bwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _P, _P, _P, _P]),
     "impala_gumbel_sample": (C.c_int, [_I64, _I32, _P, _P, _P, _P, _P]),
@@ -306,6 +309,16 @@ def impala_conv3x3_bwd_workspace_bytes(prec, cin, cout) -> int:
 def impala_conv3x3_bwd(prec, n, H, W, cin, cout, dy, x, x_mode, w, add, dx, dw, db, ws, stream=None):
     _check("impala_conv3x3_bwd", lib.impala_conv3x3_bwd(
         prec, n, H, W, cin, cout, ptr(dy), ptr(x), x_mode, ptr(w), ptr(add), ptr(dx), ptr(dw), ptr(db), ptr(ws),
+        ws.numel() * ws.element_size(), stream_handle(stream)))
+
+
+def impala_conv3x3_pool_wgrad_u8_workspace_bytes(prec, cout) -> int:
+    return int(lib.impala_conv3x3_pool_wgrad_u8_workspace_bytes(prec, cout))
+
+
+def impala_conv3x3_pool_wgrad_u8(prec, n, H, W, cout, obs, row_idx, dpool, arg, dw, db, ws, stream=None):
+    _check("impala_conv3x3_pool_wgrad_u8", lib.impala_conv3x3_pool_wgrad_u8(
+        prec, n, H, W, cout, ptr(obs), ptr(row_idx), ptr(dpool), ptr(arg), ptr(dw), ptr(db), ptr(ws),
         ws.numel() * ws.element_size(), stream_handle(stream)))
 
 

@@ -581,6 +581,36 @@ impala_status_t impala_conv3x3_bwd(impala_prec_t prec, int64_t n, int32_t H, int
     return hip_status(conv3x3_bwd(cin, cout, x_mode, a, stream), "impala_conv3x3_bwd");
 }
 
+size_t impala_conv3x3_pool_wgrad_u8_workspace_bytes(impala_prec_t prec, int32_t cout) {
+    if (prec != IMPALA_PREC_BF16) return 0;
+    return pool_wgrad_u8_partial_floats(cout) * sizeof(float);
+}
+
+impala_status_t impala_conv3x3_pool_wgrad_u8(impala_prec_t prec, int64_t n, int32_t H, int32_t W,
+                                             int32_t cout, const uint8_t* obs, const int32_t* row_idx,
+                                             const void* dpool, const uint8_t* arg, float* dw, float* db,
+                                             void* ws, size_t ws_bytes, hipStream_t stream) {
+    impala_status_t st = check_layer(__func__, prec, n, H, W, 4, cout);
+    if (st) return st;
+    if (prec != IMPALA_PREC_BF16 || !pool_wgrad_u8_supported(cout))
+        return fail(IMPALA_EUNSUPPORTED, "impala_conv3x3_pool_wgrad_u8: bf16 with cout = 16 or 32 only (got prec=%d cout=%d)",
+                    int(prec), cout);
+    CHECK_PTR(dw); CHECK_PTR(db);
+    if (n == 0) {
+        hipError_t he = fill_zero(dw, int64_t(36) * cout, stream);
+        if (he == hipSuccess) he = fill_zero(db, cout, stream);
+        return hip_status(he, "impala_conv3x3_pool_wgrad_u8");
+    }
+    CHECK_PTR(obs); CHECK_PTR(dpool); CHECK_PTR(arg); CHECK_PTR(ws);
+    const size_t need = pool_wgrad_u8_partial_floats(cout) * sizeof(float);
+    if (ws_bytes < need)
+        return fail(IMPALA_EWORKSPACE, "impala_conv3x3_pool_wgrad_u8: workspace %zu < %zu", ws_bytes, need);
+    PoolWgArgs a{};
+    a.obs = obs; a.row_idx = row_idx; a.dp = dpool; a.arg = arg; a.dw = dw; a.db = db;
+    a.partial = static_cast<float*>(ws); a.n = int(n); a.H = H; a.W = W;
+    return hip_status(pool_wgrad_u8(cout, a, stream), "impala_conv3x3_pool_wgrad_u8");
+}
+
 impala_status_t impala_maxpool_fwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t C,
                                    const void* x, void* y, uint8_t* arg, hipStream_t stream) {
     impala_status_t st = check_layer(__func__, prec, n, H, W, C, C);

@@ -22,7 +22,8 @@
 //   - x window [FR][TH+2][W+2] pixels of 2*CI bytes (+32 from 32 channels on); the weight
 //     gradient reads its fragments, pixel-consecutive, with the LDS transpose read
 //     (ds_read_b64_tr_b16), and the mask is read from it in the epilogue;
-//   - the residual operand for the tile's own pixels, [FR*TH*W][CI].
+// The residual operand is read from global memory into registers before each 16-pixel
+// column tile's MFMAs (a wave's read covers whole pixels, so it stays coalesced).
 // The input-gradient weights (taps rotated by 180 degrees, in/out channels swapped) live in
 // registers: each wave owns one 16-channel block of dx and holds its A fragments for all
 // k-steps, loaded once per workgroup.
@@ -45,7 +46,8 @@ struct CbGeom {
     static constexpr int NBB = NB + 1;                   // ... and the bias block
     static constexpr int PSTRIDE = MTO * NBB * 256;      // floats per workgroup partial
     // staging slots per lane (of an 8-wave workgroup) the tile planner stays within
-    static constexpr int MAXD = CO > CI ? 7 : 6, MAXX = 4, MAXA = 3;
+    static constexpr int MAXD = CO > CI ? 7 : 6, MAXX = 4;
+    static constexpr int MAXT = CI >= 32 ? 4 : 6;   // dx column tiles per wave and tile (with a residual)
     __host__ __device__ static int blocks(int slots) { return (slots + 63) / 64; }
 };
 
@@ -64,7 +66,6 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
     unsigned char* zero = smem;               // 64 zero bytes
     unsigned char* dyw = smem + t.dy_off;
     unsigned char* xw = smem + t.x_off + XPB;   // one zero guard pixel on either side
-    unsigned char* adt = smem + t.add_off;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar branches
@@ -82,6 +83,7 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
     // ---- input gradient: this wave's dx channel block and its A fragments,
     // A[o][k] = w[8 - tap][o][co] with k = tap * CO + co (zero past the 9 taps)
     const int dmt = wave % MTI;
+    const int ci0 = dmt * 16 + g * 4;   // the lane's first dx channel
     uint4 wf[KSD];
 #pragma unroll
     for (int ks = 0; ks < KSD; ++ks) {
@@ -94,13 +96,22 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
         }
         wf[ks] = make_uint4(pack2bf(v[0], v[1]), pack2bf(v[2], v[3]), pack2bf(v[4], v[5]), pack2bf(v[6], v[7]));
     }
-    // its B fragments: byte offsets from the lane's tap-(0,0) dy-window pixel
-    int dboff[KSD];
+    // its B fragments: byte offsets from the lane's tap-(0,0) dy-window pixel; with 16
+    // channels a k-step spans two taps (a per-lane table), from 32 on the tap is the k-step's
+    // and only the 16-byte slot is the lane's (formed in place)
+    int dboff[CO < 32 ? KSD : 1];
+    if constexpr (CO < 32) {
 #pragma unroll
-    for (int ks = 0; ks < KSD; ++ks) {
-        const int k0 = ks * 32 + g * 8, tap = k0 / CO, slot = (k0 % CO) / 8;
-        dboff[ks] = tap < 9 ? ((tap / 3) * TW + tap % 3) * DYP + slot * 16 : (DSL - 1) * 16;
+        for (int ks = 0; ks < KSD; ++ks) {
+            const int k0 = ks * 32 + g * 8, tap = k0 / CO, slot = (k0 % CO) / 8;
+            dboff[ks] = tap < 9 ? ((tap / 3) * TW + tap % 3) * DYP + slot * 16 : (DSL - 1) * 16;
+        }
     }
+    const int twdy = TW * DYP;
+    auto dgrad_off = [&](int ks) -> int {
+        if constexpr (CO < 32) return dboff[ks];
+        else return (ks / (CO / 32) / 3) * twdy + (ks / (CO / 32) % 3) * DYP + ((ks % (CO / 32)) * 4 + g) * 16;
+    };
     // ---- weight gradient: column blocks nb = wave + NW * i (16 input channels of one tap,
     // or the bias block), each for all CO/16 output-channel blocks
     int wboff[TPW];
@@ -123,8 +134,8 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
     // it past the tile's frames: both fall outside the buffer resource and read as zero.
     // Padding slots, padding columns and (multi-frame tiles) the halo rows between frames hold
     // kOOB. Slot k of this wave is j = (wave + NW * k) * 64 + lane.
-    const int nsd = FR * TR * TW * DSL, nsx = FR * TR * TW * XSL, nsa = FR * TH * W * (CI / 8);
-    uint32_t od[G::MAXD], ox[G::MAXX], oa[ADD ? G::MAXA : 1];
+    const int nsd = FR * TR * TW * DSL, nsx = FR * TR * TW * XSL;
+    uint32_t od[G::MAXD], ox[G::MAXX];
     auto win_off = [&](int j, int slots, int nreal, int cbytes) -> uint32_t {
         const int p = j / slots, c = j - p * slots;
         const int rowi = p / TW, col = p - rowi * TW;
@@ -137,15 +148,6 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
     for (int k = 0; k < G::MAXD; ++k) od[k] = win_off((wave + NW * k) * 64 + lane, DSL, CO / 8, CO * 2);
 #pragma unroll
     for (int k = 0; k < G::MAXX; ++k) ox[k] = win_off((wave + NW * k) * 64 + lane, XSL, CI / 8, CI * 2);
-    if constexpr (ADD) {
-#pragma unroll
-        for (int k = 0; k < G::MAXA; ++k) {
-            const int j = (wave + NW * k) * 64 + lane;
-            const int q = j / (CI / 8), c = j - q * (CI / 8);
-            const int rowi = q / W, col = q - rowi * W, f = rowi / TH, rr = rowi - f * TH;
-            oa[k] = j < nsa ? uint32_t(((f * H + rr) * W + col) * (CI * 2) + c * 16) : kOOB;
-        }
-    }
 
     int lg = blockIdx.x;   // neighbouring tiles (which share halo rows) on one XCD
     if ((gridDim.x & 7) == 0) lg = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
@@ -158,7 +160,7 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
         const int npx = nf * the * W;   // FR > 1 only when a band is the whole frame
         __syncthreads();   // the previous tile's LDS reads are done
 
-        // ---- stage the dy and x windows (rows h0-1 .. h0+TH) and the residual operand
+        // ---- stage the dy and x windows (rows h0-1 .. h0+TH)
         {
             const int64_t fpx = int64_t(f0) * H * W;
             const auto rd = buf_rsrc(static_cast<const uint16_t*>(a.dy) + fpx * CO, uint32_t(nf) * H * W * CO * 2);
@@ -170,11 +172,17 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
 #pragma unroll
             for (int k = 0; k < G::MAXX; ++k)
                 if ((wave + NW * k) * 64 < nsx) dma16_to_lds(rx, xw + (wave + NW * k) * 1024, ox[k] + hx);
-            if constexpr (ADD) {
-                const auto ra = buf_rsrc(static_cast<const uint16_t*>(a.add) + fpx * CI, uint32_t(nf) * H * W * CI * 2);
+        }
+        // the residual operand of this wave's column tiles, fetched alongside the staging
+        const int64_t tpx = (int64_t(f0) * H + h0) * W * CI;   // the tile's first dx element
+        const int ntl = (npx + 15) >> 4;
+        uint2 addr[ADD ? G::MAXT : 1];
+        if constexpr (ADD) {
+            const uint16_t* adg = static_cast<const uint16_t*>(a.add) + tpx;
 #pragma unroll
-                for (int k = 0; k < G::MAXA; ++k)
-                    if ((wave + NW * k) * 64 < nsa) dma16_to_lds(ra, adt + (wave + NW * k) * 1024, oa[k] + hx);
+            for (int k = 0; k < G::MAXT; ++k) {
+                const int q = (wave / MTI + k * (NW / MTI)) * 16 + r16;
+                addr[k] = q < npx ? *reinterpret_cast<const uint2*>(adg + uint32_t(q * CI + ci0)) : make_uint2(0, 0);
             }
         }
         __builtin_amdgcn_s_waitcnt(0);   // this wave's loads have landed in LDS
@@ -242,9 +250,8 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
         // q sits at window row q / W (+ 2 per earlier frame of a multi-frame tile), and dx and
         // the residual operand are addressed by q itself from the tile's first pixel.
         {
-            uint16_t* dxt = static_cast<uint16_t*>(a.dx) + (int64_t(f0) * H + h0) * W * CI;
-            const int ntl = (npx + 15) >> 4;
-            for (int nt = wave / MTI; nt < ntl; nt += NW / MTI) {
+            uint16_t* dxt = static_cast<uint16_t*>(a.dx) + tpx;
+            auto column_tile = [&](int nt, uint2 addv) {
                 const int q = nt * 16 + r16;
                 const int qc = q < npx ? q : npx - 1;   // past npx: computed, not stored
                 const int row = qdiv(qc, t.inv_W), col = qc - row * W;
@@ -254,9 +261,8 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
                 cb_f32x4 acc = cb_f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int ks = 0; ks < KSD; ++ks)
-                    acc = PrecBF16::mma(wf[ks], *reinterpret_cast<const uint4*>(xb + dboff[ks]), acc);
+                    acc = PrecBF16::mma(wf[ks], *reinterpret_cast<const uint4*>(xb + dgrad_off(ks)), acc);
                 if (q < npx) {
-                    const int ci0 = dmt * 16 + g * 4;
                     float v[4] = {acc[0], acc[1], acc[2], acc[3]};
                     if constexpr (MODE == IN_RELU) {
                         float mk[4];
@@ -265,13 +271,20 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
                         for (int j = 0; j < 4; ++j) v[j] = mk[j] > 0.f ? v[j] : 0.f;
                     }
                     if constexpr (ADD) {
-                        float ad[4];
-                        load4(reinterpret_cast<const uint16_t*>(adt + (q * CI + ci0) * 2), ad);
-#pragma unroll
-                        for (int j = 0; j < 4; ++j) v[j] += ad[j];
+                        v[0] += __uint_as_float(addv.x << 16);
+                        v[1] += __uint_as_float(addv.x & 0xffff0000u);
+                        v[2] += __uint_as_float(addv.y << 16);
+                        v[3] += __uint_as_float(addv.y & 0xffff0000u);
                     }
                     store4(dxt + uint32_t(q * CI + ci0), v[0], v[1], v[2], v[3]);
                 }
+            };
+            if constexpr (ADD) {
+#pragma unroll
+                for (int k = 0; k < G::MAXT; ++k)
+                    if (wave / MTI + k * (NW / MTI) < ntl) column_tile(wave / MTI + k * (NW / MTI), addr[k]);
+            } else {
+                for (int nt = wave / MTI; nt < ntl; nt += NW / MTI) column_tile(nt, make_uint2(0, 0));
             }
         }
     }
@@ -307,22 +320,22 @@ template <int CI, int CO, int MODE, int ADD>
 hipError_t cb_launch(const ConvBwdArgs& a, hipStream_t s) {
     using G = CbGeom<CI, CO>;
     const int H = a.H, W = a.W;
-    auto regions = [&](int th, int fr, int& dyb, int& xb, int& ab) {
+    auto regions = [&](int th, int fr, int& dyb, int& xb) {
         const int wp = fr * (th + 2) * (W + 2);
         dyb = G::blocks(wp * G::DSL) * 1024;
         xb = G::blocks(wp * G::XSL) * 1024 + 2 * G::XPB;   // + a guard pixel on either side
-        ab = ADD ? G::blocks(fr * th * W * (CI / 8)) * 1024 : 0;
     };
     auto lds = [&](int th, int fr) {
-        int dyb, xb, ab;
-        regions(th, fr, dyb, xb, ab);
-        return size_t(64 + dyb + xb + ab);
+        int dyb, xb;
+        regions(th, fr, dyb, xb);
+        return size_t(64 + dyb + xb);
     };
     // staging slots per lane within the kernel's register tables
     auto fits = [&](int th, int fr) {
         const int per = kCbWaves * 64, wp = fr * (th + 2) * (W + 2);
+        const int tiles = (fr * th * W + 15) / 16, waves_per_block = kCbWaves / G::MTI;
         return (wp * G::DSL + per - 1) / per <= G::MAXD && (wp * G::XSL + per - 1) / per <= G::MAXX &&
-               (!ADD || (fr * th * W * (CI / 8) + per - 1) / per <= G::MAXA);
+               (!ADD || (tiles + waves_per_block - 1) / waves_per_block <= G::MAXT);
     };
     const size_t limit = std::min<size_t>(lds_limit(), 160 * 1024);
     int thmax = std::min(H, std::max(1, kCbPixMax / W));
@@ -341,9 +354,9 @@ hipError_t cb_launch(const ConvBwdArgs& a, hipStream_t s) {
     if (int64_t(FR) * H * W * std::max(CI, CO) * 2 >= (int64_t(1) << 31)) return hipErrorInvalidValue;
     CbTile t{};
     t.TH = TH; t.FR = FR; t.nbands = nbands; t.ntiles = nbands * ((a.n + FR - 1) / FR);
-    int dyb, xb, ab;
-    regions(TH, FR, dyb, xb, ab);
-    t.dy_off = 64; t.x_off = t.dy_off + dyb; t.add_off = t.x_off + xb;
+    int dyb, xb;
+    regions(TH, FR, dyb, xb);
+    t.dy_off = 64; t.x_off = t.dy_off + dyb;
     t.x_guard = xb - 2 * G::XPB;   // byte offset of the rear guard from the window start
     t.inv_W = 1.f / float(W); t.inv_TW = 1.f / float(W + 2);
     t.inv_TH = 1.f / float(TH); t.inv_TR = 1.f / float(TH + 2);

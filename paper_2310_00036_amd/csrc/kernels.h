@@ -76,18 +76,41 @@ struct ConvBwdArgs {
 };
 struct CbTile {
     int TH, FR, nbands, ntiles;
-    int dy_off, x_off, add_off;   // LDS byte offsets; 64 zero bytes at offset 0
+    int dy_off, x_off;            // LDS byte offsets; 64 zero bytes at offset 0
     int x_guard;                  // x window: byte offset of its rear guard pixel
     float inv_W, inv_TW, inv_TH, inv_TR;
 };
 bool conv3x3_bwd_supported(int cin, int cout, int mode, int add);
 size_t conv3x3_bwd_partial_floats(int cin, int cout);
 hipError_t conv3x3_bwd(int cin, int cout, int mode, const ConvBwdArgs& a, hipStream_t s);
-// Fixed-order sum of nparts bf16 weight-gradient partials laid out [mt*(9*cin/16+1) + nb]
-// [co 16][ci 16] (the last column block holds the bias sums), scattered to HWIO dw (times
-// scale) and db.
+// Fixed-order sum of nparts bf16 weight-gradient partials laid out [mt*(NB+1) + nb]
+// [co 16][col 16] (the last column block holds the bias sums), scattered to HWIO dw (times
+// scale) and db. NB = 9*cin/16 column blocks of 16 input channels of one tap; for uint8
+// frames (cin == 4) NB = 3 blocks of 4 taps x 4 channels.
 hipError_t wgrad_reduce_tr(int cin, int cout, const float* partial, int nparts, float* dw, float* db,
                            float scale, hipStream_t s);
+
+// ---- backward of the first stage entry, bf16: y = maxpool(conv3x3(frames / 255) + b); the
+//      max-pool backward feeds the conv's weight gradient on chip (the frames need no input
+//      gradient). Equals maxpool_bwd followed by conv3x3_wgrad(IN_U8).
+struct PoolWgArgs {
+    const uint8_t* obs;     // frames [*, H, W, 4]; frame i is obs[row_idx[i]] (NULL: i)
+    const int32_t* row_idx;
+    const void* dp;         // [n, OH, OW, cout] bf16 gradient at the pool output
+    const uint8_t* arg;     // [n, OH, OW, cout] pool argmax (0..8)
+    float* dw;              // float32 HWIO [3,3,4,cout]
+    float* db;              // float32 [cout]
+    float* partial;         // workspace, pool_wgrad_u8_partial_floats() floats
+    int n, H, W;
+};
+struct PwTile {
+    int TB, nbands, ntiles;         // 2x2 pixel-block rows per band
+    int OH, OW, ph, pw, BH, BW;     // pool geometry (padded-coordinate block grid BH x BW)
+    int raw_off, win_off, win_guard, dp_off, arg_off, dc_off;   // LDS layout (bytes)
+};
+bool pool_wgrad_u8_supported(int cout);
+size_t pool_wgrad_u8_partial_floats(int cout);
+hipError_t pool_wgrad_u8(int cout, const PoolWgArgs& a, hipStream_t s);
 
 // ---- 3x3 stride-2 SAME max-pool (XLA padding split), first-max argmax in 0..8
 hipError_t maxpool_fwd(int prec, int n, int H, int W, int C, const void* x, void* y,

@@ -1,7 +1,8 @@
 // Fused policy / value / entropy losses and their logit and value gradients, one thread per
 // minibatch row (A <= 64 logits per row), plus the actor's Gumbel-max sampler.
 //
-// PPO runs three launches: (1) one block computes the minibatch advantage mean and
+// Minibatches up to kFusedRows rows run as one single-workgroup launch. Larger ones run
+// PPO as three launches: (1) one block computes the minibatch advantage mean and
 // population std (float64 sums) into the caller's stats vector, (2) one thread per row
 // computes log-softmax, ratio, clipped surrogate, entropy and value terms and writes
 // dlogits / dvalue, (3) one block re-derives the row terms and sums them (float64, fixed
@@ -9,6 +10,8 @@
 // fixed order, so results are bit-reproducible.
 #include "common.h"
 #include "kernels.h"
+
+#include <algorithm>
 
 namespace cb {
 
@@ -65,11 +68,10 @@ struct PpoRow {
     int a;
 };
 
-CB_DEV PpoRow ppo_row(int64_t i, int64_t src, int A, const float* z, const int32_t* act,
+CB_DEV PpoRow ppo_row(const float* zr, int64_t src, int A, const int32_t* act,
                       const float* old_logp, const float* adv, int norm_adv, float clip,
                       float mean, float std) {
     PpoRow r;
-    const float* zr = z + i * A;
     r.s = row_log_softmax(zr, A);
     r.H = r.s.H;
     r.a = act[src];
@@ -95,7 +97,7 @@ __global__ __launch_bounds__(kLossRows) void ppo_rows_kernel(
     const int64_t i = int64_t(blockIdx.x) * kLossRows + threadIdx.x;
     if (i >= m) return;
     const int64_t src = rows ? rows[i] : i;
-    const PpoRow r = ppo_row(i, src, A, z, act, old_logp, adv, norm_adv, clip, stats[6], stats[7]);
+    const PpoRow r = ppo_row(z + i * A, src, A, act, old_logp, adv, norm_adv, clip, stats[6], stats[7]);
     const float inv_m = 1.f / float(m);
     const float coef = -r.kappa * r.A_hat * r.ratio;
     const float* zr = z + i * A;
@@ -118,7 +120,7 @@ __global__ __launch_bounds__(kStatThreads) void ppo_stats_kernel(
     double st[5] = {0, 0, 0, 0, 0};
     for (int64_t i = threadIdx.x; i < m; i += kStatThreads) {
         const int64_t src = rows ? rows[i] : i;
-        const PpoRow r = ppo_row(i, src, A, z, act, old_logp, adv, norm_adv, clip, mean, std);
+        const PpoRow r = ppo_row(z + i * A, src, A, act, old_logp, adv, norm_adv, clip, mean, std);
         const double dvl = double(val[i]) - double(ret[src]);
         st[0] += r.pg;
         st[1] += dvl * dvl;
@@ -190,6 +192,165 @@ __global__ __launch_bounds__(kStatThreads) void impala_stats_kernel(
     }
 }
 
+// ---- single-workgroup variants for minibatches up to kFusedRows rows: the advantage
+// statistics, the per-row gradients and the loss statistics in one launch (each row's terms
+// are computed once). Sums are float64: each wave adds its lanes in a fixed butterfly order,
+// then every thread adds the wave totals in wave order, so every thread holds the same
+// deterministic totals.
+constexpr int kFusedThreads = 512;
+constexpr int64_t kFusedRows = 16384;
+
+template <int K>
+CB_DEV void fused_block_sum(double (&v)[K], double* sh) {
+    constexpr int NWV = kFusedThreads / 64;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) v[k] += __shfl_xor(v[k], off);
+    if (lane == 0)
+#pragma unroll
+        for (int k = 0; k < K; ++k) sh[wave * K + k] = v[k];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        double t = 0.0;
+        for (int w = 0; w < NWV; ++w) t += sh[w * K + k];
+        v[k] = t;
+    }
+    __syncthreads();
+}
+
+// Rows are processed in chunks: the chunk's logits are read into LDS with coalesced loads,
+// each thread works on one row there (writing its logit gradients in place), and the chunk's
+// gradients leave with coalesced stores.
+CB_DEV int fused_chunk_rows(int A) { return (kFusedThreads * 64 / A) < kFusedThreads ? (kFusedThreads * 64 / A) : kFusedThreads; }
+
+// AC > 0 fixes the action count at compile time (the row loops unroll); 0 reads it from A_.
+template <int AC>
+__global__ __launch_bounds__(kFusedThreads) void ppo_fused_kernel(
+    int64_t m, int A_, const float* __restrict__ z, const float* __restrict__ val,
+    const int32_t* __restrict__ act, const float* __restrict__ old_logp,
+    const float* __restrict__ adv, const float* __restrict__ ret, const int32_t* __restrict__ rows,
+    int norm_adv, float clip, float vf, float ent, float* __restrict__ dz, float* __restrict__ dv,
+    float* __restrict__ stats) {
+    extern __shared__ float zs[];   // [chunk rows][A]
+    __shared__ double sh[(kFusedThreads / 64) * 5];
+    const int A = AC > 0 ? AC : A_;
+    const int tid = threadIdx.x;
+    // advantage mean and population std over the minibatch
+    double ms[2] = {0.0, 0.0};
+    for (int64_t i = tid; i < m; i += kFusedThreads) {
+        const double a = adv[rows ? rows[i] : i];
+        ms[0] += a;
+        ms[1] += a * a;
+    }
+    fused_block_sum<2>(ms, sh);
+    const double dmean = ms[0] / double(m), dvar = ms[1] / double(m) - dmean * dmean;
+    const float mean = float(dmean), std = float(sqrt(dvar > 0.0 ? dvar : 0.0));
+    // rows: gradients and loss terms
+    const float inv_m = 1.f / float(m);
+    const int CR = fused_chunk_rows(A);
+    double st[5] = {0, 0, 0, 0, 0};
+    for (int64_t c0 = 0; c0 < m; c0 += CR) {
+        const int nr = m - c0 < CR ? int(m - c0) : CR;
+        __syncthreads();   // the previous chunk's gradients have left LDS
+        for (int e = tid; e < nr * A; e += kFusedThreads) zs[e] = z[c0 * A + e];
+        __syncthreads();
+        if (tid < nr) {
+            const int64_t i = c0 + tid, src = rows ? rows[i] : i;
+            float* zr = zs + tid * A;
+            const PpoRow r = ppo_row(zr, src, A, act, old_logp, adv, norm_adv, clip, mean, std);
+            const float coef = -r.kappa * r.A_hat * r.ratio;
+            for (int j = 0; j < A; ++j) {
+                const float l = r.s.l(zr[j]);
+                const float p = expf(l);
+                zr[j] = (coef * ((j == r.a ? 1.f : 0.f) - p) + ent * p * (l + r.H)) * inv_m;
+            }
+            const float vi = val[i], ri = ret[src];
+            dv[i] = vf * (vi - ri) * inv_m;
+            const double dvl = double(vi) - double(ri);
+            st[0] += r.pg;
+            st[1] += dvl * dvl;
+            st[2] += r.H;
+            st[3] += double(r.ratio - 1.f) - double(logf(r.ratio));
+            st[4] += fabsf(r.ratio - 1.f) > clip ? 1.0 : 0.0;
+        }
+        __syncthreads();
+        for (int e = tid; e < nr * A; e += kFusedThreads) dz[c0 * A + e] = zs[e];
+    }
+    fused_block_sum<5>(st, sh);
+    if (tid == 0) {
+        const double inv = 1.0 / double(m);
+        const double pg = st[0] * inv, vl = 0.5 * st[1] * inv, H = st[2] * inv;
+        stats[0] = float(pg + vf * vl - ent * H);
+        stats[1] = float(pg); stats[2] = float(vl); stats[3] = float(H);
+        stats[4] = float(st[3] * inv); stats[5] = float(st[4] * inv);
+        stats[6] = mean; stats[7] = std;
+    }
+}
+
+template <int AC>
+__global__ __launch_bounds__(kFusedThreads) void impala_fused_kernel(
+    int64_t m, int A_, const float* __restrict__ z, const float* __restrict__ val,
+    const int32_t* __restrict__ act, const float* __restrict__ vs, const float* __restrict__ pgadv,
+    float pgc, float vf, float ent, float* __restrict__ dz, float* __restrict__ dv,
+    float* __restrict__ stats) {
+    extern __shared__ float zs[];   // [chunk rows][A]
+    __shared__ double sh[(kFusedThreads / 64) * 5];
+    const int A = AC > 0 ? AC : A_;
+    const int tid = threadIdx.x;
+    const float inv_m = 1.f / float(m);
+    const int CR = fused_chunk_rows(A);
+    double st[5] = {0, 0, 0, 0, 0};
+    for (int64_t c0 = 0; c0 < m; c0 += CR) {
+        const int nr = m - c0 < CR ? int(m - c0) : CR;
+        __syncthreads();
+        for (int e = tid; e < nr * A; e += kFusedThreads) zs[e] = z[c0 * A + e];
+        __syncthreads();
+        if (tid < nr) {
+            const int64_t i = c0 + tid;
+            float* zr = zs + tid * A;
+            const RowLsm rs = row_log_softmax(zr, A);
+            const float H = rs.H;
+            const int a = act[i];
+            const float adv = pgadv[i];
+            const bool a_ok = a >= 0 && a < A;
+            const double la = a_ok ? double(rs.l(zr[a])) : double(__builtin_nanf(""));
+            for (int j = 0; j < A; ++j) {
+                const float l = rs.l(zr[j]);
+                const float p = expf(l);
+                zr[j] = a_ok ? (-pgc * adv * ((j == a ? 1.f : 0.f) - p) + ent * p * (l + H)) * inv_m
+                             : __builtin_nanf("");
+            }
+            const float vi = val[i], vsi = vs[i];
+            dv[i] = vf * (vi - vsi) * inv_m;
+            const double dvl = double(vi) - double(vsi);
+            st[0] += -double(adv) * la;
+            st[1] += dvl * dvl;
+            st[2] += H;
+            st[3] += adv;
+            st[4] += vsi;
+        }
+        __syncthreads();
+        for (int e = tid; e < nr * A; e += kFusedThreads) dz[c0 * A + e] = zs[e];
+    }
+    fused_block_sum<5>(st, sh);
+    if (tid == 0) {
+        const double inv = 1.0 / double(m);
+        const double pg = st[0] * inv, vl = 0.5 * st[1] * inv, H = st[2] * inv;
+        stats[0] = float(pgc * pg + vf * vl - ent * H);
+        stats[1] = float(pg); stats[2] = float(vl); stats[3] = float(H);
+        stats[4] = float(st[3] * inv); stats[5] = float(st[4] * inv);
+        stats[6] = 0.f; stats[7] = 0.f;
+    }
+}
+
+static size_t fused_lds(int A) {
+    const int cr = std::min(kFusedThreads * 64 / A, kFusedThreads);
+    return size_t(cr) * A * sizeof(float);
+}
+
 hipError_t ppo_loss(int64_t m, int A, const float* z, const float* v, const int32_t* act,
                     const float* old_logp, const float* adv, const float* ret, const int32_t* rows,
                     int norm_adv, float clip, float vf, float ent, float* dz, float* dv, float* stats,
@@ -197,6 +358,12 @@ hipError_t ppo_loss(int64_t m, int A, const float* z, const float* v, const int3
     if (m <= 0) return hipSuccess;
     const int nb = int((m + kLossRows - 1) / kLossRows);
     ProfScope ps(s, [&] { return "ppo_loss/" + cb_dims(int(m), A); });
+    if (m <= kFusedRows) {
+        auto k = A == 18 ? ppo_fused_kernel<18> : (A == 6 ? ppo_fused_kernel<6> : ppo_fused_kernel<0>);
+        hipLaunchKernelGGL(k, dim3(1), dim3(kFusedThreads), fused_lds(A), s, m, A, z, v, act, old_logp, adv, ret, rows,
+                           norm_adv, clip, vf, ent, dz, dv, stats);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL(adv_stats_kernel, dim3(1), dim3(256), 0, s, m, adv, rows, stats);
     hipLaunchKernelGGL(ppo_rows_kernel, dim3(nb), dim3(kLossRows), 0, s, m, A, z, v, act, old_logp,
                        adv, ret, rows, norm_adv, clip, vf, ent, dz, dv, stats);
@@ -211,6 +378,12 @@ hipError_t impala_loss(int64_t m, int A, const float* z, const float* v, const i
     if (m <= 0) return hipSuccess;
     const int nb = int((m + kLossRows - 1) / kLossRows);
     ProfScope ps(s, [&] { return "impala_loss/" + cb_dims(int(m), A); });
+    if (m <= kFusedRows) {
+        auto k = A == 18 ? impala_fused_kernel<18> : (A == 6 ? impala_fused_kernel<6> : impala_fused_kernel<0>);
+        hipLaunchKernelGGL(k, dim3(1), dim3(kFusedThreads), fused_lds(A), s, m, A, z, v, act, vs, pg, pgc, vf, ent, dz,
+                           dv, stats);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL(impala_rows_kernel, dim3(nb), dim3(kLossRows), 0, s, m, A, z, v, act, vs, pg,
                        pgc, vf, ent, dz, dv);
     hipLaunchKernelGGL(impala_stats_kernel, dim3(1), dim3(kStatThreads), 0, s, m, A, z, v, act, vs, pg,

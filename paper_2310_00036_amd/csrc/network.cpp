@@ -114,6 +114,7 @@ NetPlan make_plan(const impala_net_t& net, int prec, int64_t cap, int training) 
             sc = std::max(sc, wgrad_partial_floats(prec, p.C[s], p.C[s + 1], p.H[s], p.W[s]));
             sc = std::max(sc, wgrad_partial_floats(prec, p.C[s + 1], p.C[s + 1], p.H[s + 1], p.W[s + 1]));
             if (prec == BF16) {
+                if (s == 0) sc = std::max(sc, pool_wgrad_u8_partial_floats(p.C[1]));
                 sc = std::max(sc, conv3x3_bwd_partial_floats(p.C[s], p.C[s + 1]));
                 sc = std::max(sc, conv3x3_bwd_partial_floats(p.C[s + 1], p.C[s + 1]));
             }
@@ -315,6 +316,16 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
         }
         int fa, fb;
         others(gy, fa, fb);
+        if (st == 0 && p.prec == BF16 && pool_wgrad_u8_supported(C)) {
+            // max-pool backward on chip, feeding the frames' conv weight gradient
+            PoolWgArgs pa{};
+            pa.obs = obs; pa.row_idx = row_idx; pa.dp = G[gy];
+            pa.arg = reinterpret_cast<const uint8_t*>(ws + p.idx[0]);
+            pa.dw = grads + po.conv_w[0][0]; pa.db = grads + po.conv_b[0][0]; pa.partial = scratch;
+            pa.n = int(n); pa.H = p.H[0]; pa.W = p.W[0];
+            CB_TRY(pool_wgrad_u8(C, pa, s));
+            continue;
+        }
         CB_TRY(maxpool_bwd(p.prec, int(n), p.H[st], p.W[st], C,
                            reinterpret_cast<const uint8_t*>(ws + p.idx[st]), G[gy], G[fa], s));
         if (st > 0 && p.prec == BF16 && conv3x3_bwd_supported(p.C[st], C, IN_PLAIN, 0)) {

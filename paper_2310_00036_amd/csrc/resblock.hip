@@ -6,16 +6,18 @@
 // for conv2; t written once); here it moves three (x read, t and y written). Each tile is a
 // band of TH output rows of one frame:
 //   - the input window, rows h0-2 .. h0+TH+1 of x, is staged HBM -> LDS (buffer loads, zero
-//     padding from out-of-range offsets) and ReLU'd in place; the band's own rows of x are
-//     staged a second time, unmodified, for the residual add;
+//     padding from out-of-range offsets) and ReLU'd in place;
 //   - conv1 computes t on the band's rows plus one halo row above and below (the halo rows
 //     are recomputed by the neighbouring bands); t is rounded to bf16, the band's own rows
 //     are stored (the backward pass reads them) and relu(t) goes to an LDS window with zero
 //     padding columns, exactly what conv2 would have read from HBM;
-//   - conv2 reads that window and writes y with the bias and the residual add fused.
-// The per-MFMA layout is that of the single convolution kernel: 16 output pixels per MFMA
-// column tile, weights as [out][tap*C + in] in LDS, one 16-byte B fragment per lane and
-// k-step from a window whose pixels are C/8 16-byte slots plus one zero slot.
+//   - conv2 reads that window and writes y with the bias and the residual add fused; the
+//     residual x comes from global memory into registers, fetched with the tile's staging.
+// Per MFMA: 16 output pixels per column tile, one 16-byte B fragment per lane and k-step
+// from a window whose pixels are C/8 16-byte slots plus one zero slot (an odd slot count
+// spreads a fragment read over the banks; the zero slot feeds k-steps past the 9 taps).
+// Each wave owns one 16-channel block of the outputs and holds both convolutions' A
+// fragments for it in registers, loaded once per workgroup, so LDS holds only the windows.
 #include "common.h"
 #include "kernels.h"
 
@@ -27,98 +29,66 @@ template <int C>
 struct RbGeom {
     static constexpr int K = 9 * C;
     static constexpr int KSTEPS = (K + 31) / 32;
-    static constexpr int KP = KSTEPS * 32;
-    static constexpr int KPITCH = KP + 8;                  // bf16 elements per weight row
     static constexpr int MT = C / 16;
     static constexpr int SPP = C / 8 + 1;                  // 16-byte slots per window pixel
     static constexpr int PB = SPP * 16;
-    static constexpr int OCH = C / 8;                      // 16-byte slots per add-tile pixel
-    static constexpr int WB = (C * KPITCH * 2 + 15) / 16 * 16;   // one weight set (bytes)
-    static constexpr bool HOIST = 2 * MT * KSTEPS <= 12;   // both convs' A fragments in VGPRs
+    static constexpr int MAXS = C >= 32 ? 4 : 5;           // x-window staging slots per lane
+    // conv2 column tiles per wave and tile whose residual is fetched with the staging (with 32
+    // channels the registers hold both weight sets, and the residual is read per column tile)
+    static constexpr int MAXT = C >= 32 ? 0 : 5;
     __host__ __device__ static int blocks(int slots) { return (slots + 63) / 64; }
     __host__ __device__ static int xwin_bytes(int TH, int W) { return blocks((TH + 4) * (W + 2) * SPP) * 1024; }
     __host__ __device__ static int twin_bytes(int TH, int W) { return ((TH + 2) * (W + 2) * PB + 15) / 16 * 16; }
-    __host__ __device__ static int add_bytes(int TH, int W) { return blocks(TH * W * OCH) * 1024; }
 };
 
 struct RbTile {
     int TH, nbands, ntiles;
-    int x_off, t_off, a_off, b_off;   // LDS byte offsets; the two weight sets sit at 0 and WB
+    int x_off, t_off;   // LDS byte offsets of the two windows
     float inv_W, inv_TW;
 };
-
-// The MFMAs of NP 16-pixel column tiles: acc[p][mt] += W[mt rows] * window(taps at xb[p]);
-// each A fragment read from LDS feeds all NP tiles.
-template <int C, int NP>
-CB_DEV void rb_mma(const unsigned char* const* xb, const int* boff, int twpb, const uint16_t* wl,
-                   const uint4* wreg, int r16, int g, cb_f32x4 (*acc)[C / 16]) {
-    using G = RbGeom<C>;
-#pragma unroll
-    for (int ks = 0; ks < G::KSTEPS; ++ks) {
-        // 16 channels: per-lane table (a k-step spans two taps); 32: tap ks, lane's slot g
-        const int bo = C < 32 ? boff[ks] : (ks / 3) * twpb + (ks % 3) * G::PB + g * 16;
-        uint4 b[NP];
-#pragma unroll
-        for (int p = 0; p < NP; ++p) b[p] = *reinterpret_cast<const uint4*>(xb[p] + bo);
-#pragma unroll
-        for (int mt = 0; mt < G::MT; ++mt) {
-            uint4 af;
-            if constexpr (G::HOIST) af = wreg[ks * G::MT + mt];
-            else af = PrecBF16::lds_frag(wl + (mt * 16 + r16) * G::KPITCH + ks * 32 + g * 8);
-#pragma unroll
-            for (int p = 0; p < NP; ++p) acc[p][mt] = PrecBF16::mma(af, b[p], acc[p][mt]);
-        }
-    }
-}
 
 template <int C, int NW>
 __global__ __launch_bounds__(64 * NW, 4) void resblock_fwd_kernel(ResBlockArgs a, RbTile t) {
     using G = RbGeom<C>;
-    constexpr int NT = 64 * NW, KSTEPS = G::KSTEPS, KPITCH = G::KPITCH, MT = G::MT;
-    constexpr int SPP = G::SPP, PB = G::PB, OCH = G::OCH;
-    constexpr int NP = 1;   // column tiles per pass (two would spill at 32 channels)
+    constexpr int NT = 64 * NW, KSTEPS = G::KSTEPS, MT = G::MT, SPP = G::SPP, PB = G::PB;
+    static_assert(NW % MT == 0, "waves split evenly over the output channel blocks");
 
     extern __shared__ __align__(16) unsigned char smem[];
-    uint16_t* wl1 = reinterpret_cast<uint16_t*>(smem);
-    uint16_t* wl2 = reinterpret_cast<uint16_t*>(smem + G::WB);
     unsigned char* xw = smem + t.x_off;   // relu(x) window [TH+4][W+2] pixels
     unsigned char* tw = smem + t.t_off;   // relu(t) window [TH+2][W+2] pixels
-    unsigned char* xa = smem + t.a_off;   // x of the band's rows [TH*W][C], for the add
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, r16 = lane & 15;
     const int H = a.H, W = a.W, TH = t.TH, TW = W + 2;
+    const int mt = wave % MT;                     // this wave's output channel block
+    const int co0 = mt * 16 + g * 4;              // the lane's first output channel
 
-    // ---- both weight sets -> LDS once ([out][tap*C + in], zero k padding); relu(t) window
-    // zeroed once (its padding columns and zero slots are never written afterwards)
-    for (int e = tid; e < 9 * C * C; e += NT) {
-        const int o = e % C, k = e / C;
-        wl1[o * KPITCH + k] = f2bf(a.w1[e]);
-        wl2[o * KPITCH + k] = f2bf(a.w2[e]);
-    }
-    if constexpr (G::KP > G::K) {
-        constexpr int PADK = G::KP - G::K;
-        for (int e = tid; e < C * PADK; e += NT) {
-            wl1[(e / PADK) * KPITCH + G::K + e % PADK] = 0;
-            wl2[(e / PADK) * KPITCH + G::K + e % PADK] = 0;
+    // ---- A fragments of both convolutions for rows mt*16 .. +15: A[o][k] = w[tap][i][o]
+    // with k = tap*C + i (zero past the 9 taps); biases of the lane's four output channels
+    uint4 wr1[KSTEPS], wr2[KSTEPS];
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+        const int o = mt * 16 + r16;
+        float v1[8], v2[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int k = ks * 32 + g * 8 + j;
+            v1[j] = k < G::K ? a.w1[k * C + o] : 0.f;
+            v2[j] = k < G::K ? a.w2[k * C + o] : 0.f;
         }
+        wr1[ks] = make_uint4(pack2bf(v1[0], v1[1]), pack2bf(v1[2], v1[3]), pack2bf(v1[4], v1[5]), pack2bf(v1[6], v1[7]));
+        wr2[ks] = make_uint4(pack2bf(v2[0], v2[1]), pack2bf(v2[2], v2[3]), pack2bf(v2[4], v2[5]), pack2bf(v2[6], v2[7]));
+        __builtin_amdgcn_sched_barrier(0);   // convert each k-step's weights before loading the next
     }
-    for (int j = tid; j < G::twin_bytes(TH, W) / 16; j += NT) reinterpret_cast<uint4*>(tw)[j] = make_uint4(0, 0, 0, 0);
-    float* bs = reinterpret_cast<float*>(smem + t.b_off);   // b1 then b2
-    for (int e = tid; e < 2 * C; e += NT) bs[e] = e < C ? (a.b1 ? a.b1[e] : 0.f) : (a.b2 ? a.b2[e - C] : 0.f);
-    __syncthreads();
-    uint4 wr1[G::HOIST ? MT * KSTEPS : 1], wr2[G::HOIST ? MT * KSTEPS : 1];
-    if constexpr (G::HOIST) {
+    float b1[4], b2[4];
 #pragma unroll
-        for (int ks = 0; ks < KSTEPS; ++ks)
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                wr1[ks * MT + mt] = PrecBF16::lds_frag(wl1 + (mt * 16 + r16) * KPITCH + ks * 32 + g * 8);
-                wr2[ks * MT + mt] = PrecBF16::lds_frag(wl2 + (mt * 16 + r16) * KPITCH + ks * 32 + g * 8);
-            }
+    for (int j = 0; j < 4; ++j) {
+        b1[j] = a.b1 ? a.b1[co0 + j] : 0.f;
+        b2[j] = a.b2 ? a.b2[co0 + j] : 0.f;
     }
     // per-lane B-fragment offsets from the tap-(0,0) pixel (both windows share the pitch);
-    // only 16 channels need the table
+    // only 16 channels need the table (a k-step spans two taps)
     int boff[C < 32 ? KSTEPS : 1];
     if constexpr (C < 32) {
 #pragma unroll
@@ -128,6 +98,34 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_fwd_kernel(ResBlockArgs a
         }
     }
     const int twpb = TW * PB;
+    auto mma = [&](const unsigned char* xb, const uint4* wr) {
+        cb_f32x4 acc = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KSTEPS; ++ks) {
+            const int bo = C < 32 ? boff[ks] : (ks / 3) * twpb + (ks % 3) * PB + g * 16;
+            acc = PrecBF16::mma(wr[ks], *reinterpret_cast<const uint4*>(xb + bo), acc);
+            // with both weight sets held, keep at most three B fragments in flight
+            if (C >= 32 && ks % 3 == 2) __builtin_amdgcn_sched_barrier(0);
+        }
+        return acc;
+    };
+
+    // ---- relu(t) window zeroed once (its padding columns and zero slots are never written)
+    for (int j = tid; j < G::twin_bytes(TH, W) / 16; j += NT) reinterpret_cast<uint4*>(tw)[j] = make_uint4(0, 0, 0, 0);
+
+    // ---- x-window staging offsets, tile-invariant per lane (slot k of this wave:
+    // j = (wave + NW*k)*64 + lane), relative to image row 0; a tile adds h0 - 2 rows. Rows
+    // off the frame fall outside the frame's buffer resource (negative, or past its end).
+    const int nsx = (TH + 4) * TW * SPP;
+    uint32_t ox[G::MAXS];
+#pragma unroll
+    for (int k = 0; k < G::MAXS; ++k) {
+        const int j = (wave + NW * k) * 64 + lane, p = j / SPP, c = j - p * SPP;
+        const int rr = p / TW, col = p - rr * TW;
+        ox[k] = (j < nsx && c < SPP - 1 && col >= 1 && col <= W) ? uint32_t(((rr * W + col - 1) * C + c * 8) * 2)
+                                                                   : kOOB;
+    }
+    __syncthreads();
 
     int lg = blockIdx.x;   // neighbouring bands on one XCD
     if ((gridDim.x & 7) == 0) lg = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
@@ -138,37 +136,28 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_fwd_kernel(ResBlockArgs a
         const int64_t fo = int64_t(f) * H * W * C;   // frame offset (elements)
         __syncthreads();   // the previous tile's LDS reads are done
 
-        // ---- stage: x window rows h0-2 .. h0+TH+1 and the band's own rows of x
+        // ---- stage the x window, rows h0-2 .. h0+TH+1
         {
             const auto rx = buf_rsrc(static_cast<const uint16_t*>(a.x) + fo, uint32_t(H) * W * C * 2);
-            const int ns = (TH + 4) * TW * SPP;
-            for (int b = wave; b * 64 < ns; b += NW) {
-                const int j = b * 64 + lane;
-                uint32_t off = kOOB;
-                if (j < ns) {
-                    const int p = j / SPP, c = j - p * SPP;
-                    const int rr = qdiv(p, t.inv_TW), col = p - rr * TW, h = h0 - 2 + rr;
-                    if (c < SPP - 1 && col >= 1 && col <= W && h >= 0 && h < H)
-                        off = ((uint32_t(h) * W + col - 1) * C + c * 8) * 2;
-                }
-                dma16_to_lds(rx, xw + b * 1024, off);
-            }
-            const int na = the * W * OCH;
-            for (int b = wave; b * 64 < na; b += NW) {
-                const int j = b * 64 + lane;
-                uint32_t off = kOOB;
-                if (j < na) {
-                    const int q = j / OCH, c = j - q * OCH;
-                    off = ((uint32_t(h0) * W + q) * C + c * 8) * 2;
-                }
-                dma16_to_lds(rx, xa + b * 1024, off);
-            }
+            const uint32_t hr = uint32_t((h0 - 2) * W * C * 2);   // wraps for h0 < 2: rows off the frame
+#pragma unroll
+            for (int k = 0; k < G::MAXS; ++k)
+                if ((wave + NW * k) * 64 < nsx) dma16_to_lds(rx, xw + (wave + NW * k) * 1024, ox[k] + hr);
+        }
+        // conv2's residual x for this wave's column tiles, fetched alongside the staging
+        const uint16_t* xbase = static_cast<const uint16_t*>(a.x) + fo + int64_t(h0) * W * C;
+        const int npx2 = the * W;
+        uint2 xres[G::MAXT > 0 ? G::MAXT : 1];
+#pragma unroll
+        for (int k = 0; k < G::MAXT; ++k) {
+            const int q = (wave / MT + k * (NW / MT)) * 16 + r16;
+            xres[k] = q < npx2 ? *reinterpret_cast<const uint2*>(xbase + uint32_t(q * C + co0)) : make_uint2(0, 0);
         }
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
         {
             uint4* w4 = reinterpret_cast<uint4*>(xw);
-            for (int j = tid; j < (TH + 4) * TW * SPP; j += NT) {
+            for (int j = tid; j < nsx; j += NT) {
                 uint4 v = w4[j];
                 v.x = relu_bf16x2(v.x); v.y = relu_bf16x2(v.y); v.z = relu_bf16x2(v.z); v.w = relu_bf16x2(v.w);
                 w4[j] = v;
@@ -189,81 +178,43 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_fwd_kernel(ResBlockArgs a
         // ---- conv1: t on rows [tr0, tr1)
         uint16_t* tbase = static_cast<uint16_t*>(a.t) + fo;
         const int npx1 = (tr1 - tr0) * W;
-        for (int nt0 = wave; nt0 * 16 < npx1; nt0 += NW * NP) {
-          int qv[NP], trv[NP], cv[NP];
-          const unsigned char* xb[NP];
-#pragma unroll
-          for (int p = 0; p < NP; ++p) {
-              qv[p] = (nt0 + p * NW) * 16 + r16;
-              const int qc = qv[p] < npx1 ? qv[p] : npx1 - 1;
-              const int rowi = qdiv(qc, t.inv_W);
-              cv[p] = qc - rowi * W; trv[p] = tr0 + rowi;
-              xb[p] = xw + (trv[p] * TW + cv[p]) * PB;
-          }
-          cb_f32x4 accs[NP][MT];
-#pragma unroll
-          for (int p = 0; p < NP; ++p)
-#pragma unroll
-              for (int mt = 0; mt < MT; ++mt) accs[p][mt] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
-          rb_mma<C, NP>(xb, boff, twpb, wl1, wr1, r16, g, accs);
-#pragma unroll
-          for (int p = 0; p < NP; ++p) {
-            const int q = qv[p], tr = trv[p], col = cv[p];
-            const cb_f32x4* acc = accs[p];
+        for (int nt = wave / MT; nt * 16 < npx1; nt += NW / MT) {
+            const int q = nt * 16 + r16;
+            const int qc = q < npx1 ? q : npx1 - 1;
+            const int rowi = qdiv(qc, t.inv_W), col = qc - rowi * W, tr = tr0 + rowi;
+            const cb_f32x4 acc = mma(xw + (tr * TW + col) * PB, wr1);
             if (q < npx1) {
                 const int h = h0 - 1 + tr;
-                const bool own = h >= h0 && h < h0 + the;
-                uint16_t* tp = tbase + (uint32_t(h) * W + col) * C + g * 4;
-                unsigned char* twp = tw + (tr * TW + col + 1) * PB + g * 8;
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    const float4 b1 = *reinterpret_cast<const float4*>(bs + mt * 16 + g * 4);
-                    const uint32_t u0 = pack2bf(acc[mt][0] + b1.x, acc[mt][1] + b1.y);
-                    const uint32_t u1 = pack2bf(acc[mt][2] + b1.z, acc[mt][3] + b1.w);
-                    if (own) *reinterpret_cast<uint2*>(tp + mt * 16) = make_uint2(u0, u1);
-                    *reinterpret_cast<uint2*>(twp + mt * 32) = make_uint2(relu_bf16x2(u0), relu_bf16x2(u1));
-                }
+                const uint32_t u0 = pack2bf(acc[0] + b1[0], acc[1] + b1[1]);
+                const uint32_t u1 = pack2bf(acc[2] + b1[2], acc[3] + b1[3]);
+                if (h >= h0 && h < h0 + the)
+                    *reinterpret_cast<uint2*>(tbase + (uint32_t(h) * W + col) * C + co0) = make_uint2(u0, u1);
+                *reinterpret_cast<uint2*>(tw + (tr * TW + col + 1) * PB + co0 * 2) =
+                    make_uint2(relu_bf16x2(u0), relu_bf16x2(u1));
             }
-          }
         }
         __syncthreads();
 
         // ---- conv2 + residual: y on the band's rows
-        uint16_t* ybase = static_cast<uint16_t*>(a.y) + fo;
-        const int npx2 = the * W;
-        for (int nt0 = wave; nt0 * 16 < npx2; nt0 += NW * NP) {
-          int qv[NP], rv[NP], cv[NP];
-          const unsigned char* xb[NP];
+        uint16_t* ybase = static_cast<uint16_t*>(a.y) + fo + int64_t(h0) * W * C;
+        auto conv2_tile = [&](int nt, const uint2* pre) {
+            const int q = nt * 16 + r16;
+            const int qc = q < npx2 ? q : npx2 - 1;
+            const uint2 xr = pre ? *pre : *reinterpret_cast<const uint2*>(xbase + uint32_t(qc * C + co0));
+            const int r = qdiv(qc, t.inv_W), col = qc - r * W;
+            const cb_f32x4 acc = mma(tw + (r * TW + col) * PB, wr2);
+            if (q < npx2)
+                store4(ybase + uint32_t(q * C + co0), acc[0] + b2[0] + __uint_as_float(xr.x << 16),
+                       acc[1] + b2[1] + __uint_as_float(xr.x & 0xffff0000u),
+                       acc[2] + b2[2] + __uint_as_float(xr.y << 16),
+                       acc[3] + b2[3] + __uint_as_float(xr.y & 0xffff0000u));
+        };
+        if constexpr (G::MAXT > 0) {
 #pragma unroll
-          for (int p = 0; p < NP; ++p) {
-              qv[p] = (nt0 + p * NW) * 16 + r16;
-              const int qc = qv[p] < npx2 ? qv[p] : npx2 - 1;
-              rv[p] = qdiv(qc, t.inv_W); cv[p] = qc - rv[p] * W;
-              xb[p] = tw + (rv[p] * TW + cv[p]) * PB;
-          }
-          cb_f32x4 accs[NP][MT];
-#pragma unroll
-          for (int p = 0; p < NP; ++p)
-#pragma unroll
-              for (int mt = 0; mt < MT; ++mt) accs[p][mt] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
-          rb_mma<C, NP>(xb, boff, twpb, wl2, wr2, r16, g, accs);
-#pragma unroll
-          for (int p = 0; p < NP; ++p) {
-            const int q = qv[p], r = rv[p], col = cv[p];
-            const cb_f32x4* acc = accs[p];
-            if (q < npx2) {
-                uint16_t* yp = ybase + (uint32_t(h0 + r) * W + col) * C + g * 4;
-                const uint16_t* ap = reinterpret_cast<const uint16_t*>(xa) + q * C + g * 4;
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    const float4 b2 = *reinterpret_cast<const float4*>(bs + C + mt * 16 + g * 4);
-                    float ad[4];
-                    load4(ap + mt * 16, ad);
-                    store4(yp + mt * 16, acc[mt][0] + b2.x + ad[0], acc[mt][1] + b2.y + ad[1],
-                           acc[mt][2] + b2.z + ad[2], acc[mt][3] + b2.w + ad[3]);
-                }
-            }
-          }
+            for (int k = 0; k < G::MAXT; ++k)
+                if ((wave / MT + k * (NW / MT)) * 16 < npx2) conv2_tile(wave / MT + k * (NW / MT), &xres[k]);
+        } else {
+            for (int nt = wave / MT; nt * 16 < npx2; nt += NW / MT) conv2_tile(nt, nullptr);
         }
     }
 }
@@ -277,12 +228,15 @@ template <int C>
 hipError_t rb_fwd_launch(const ResBlockArgs& a, hipStream_t s) {
     using G = RbGeom<C>;
     const int H = a.H, W = a.W;
-    auto lds = [&](int th) {
-        return size_t(2 * G::WB) + G::xwin_bytes(th, W) + G::twin_bytes(th, W) + G::add_bytes(th, W) + 2 * C * 4;
+    auto lds = [&](int th) { return size_t(G::xwin_bytes(th, W)) + G::twin_bytes(th, W); };
+    auto fits = [&](int th) {
+        const int tiles = (th * W + 15) / 16, per = kRbWaves / G::MT;
+        return ((th + 4) * (W + 2) * G::SPP + kRbWaves * 64 - 1) / (kRbWaves * 64) <= G::MAXS &&
+               (G::MAXT == 0 || (tiles + per - 1) / per <= G::MAXT);
     };
     int thmax = H;
-    while (thmax > 1 && lds(thmax) > kRbLdsTarget) --thmax;
-    if (lds(thmax) > std::min<size_t>(lds_limit(), 160 * 1024)) return hipErrorInvalidValue;
+    while (thmax > 1 && (lds(thmax) > kRbLdsTarget || !fits(thmax))) --thmax;
+    if (lds(thmax) > std::min<size_t>(lds_limit(), 160 * 1024) || !fits(thmax)) return hipErrorInvalidValue;
     if (int64_t(H) * W * C * 2 >= (int64_t(1) << 31)) return hipErrorInvalidValue;
     int TH = 1, best = 1 << 30;   // fewest staged window rows per frame
     for (int th = 1; th <= thmax; ++th) {
@@ -291,10 +245,8 @@ hipError_t rb_fwd_launch(const ResBlockArgs& a, hipStream_t s) {
     }
     RbTile t{};
     t.TH = TH; t.nbands = (H + TH - 1) / TH; t.ntiles = t.nbands * a.n;
-    t.x_off = 2 * G::WB;
-    t.t_off = t.x_off + G::xwin_bytes(TH, W);
-    t.a_off = t.t_off + G::twin_bytes(TH, W);
-    t.b_off = t.a_off + G::add_bytes(TH, W);
+    t.x_off = 0;
+    t.t_off = G::xwin_bytes(TH, W);
     t.inv_W = 1.f / float(W); t.inv_TW = 1.f / float(W + 2);
     const size_t L = lds(TH);
     const void* fn = reinterpret_cast<const void*>(&resblock_fwd_kernel<C, kRbWaves>);

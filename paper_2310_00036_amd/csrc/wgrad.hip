@@ -680,14 +680,15 @@ size_t pstride() { return WgGeom<PrecF32, CIN, COUT>::PSTRIDE; }
 
 hipError_t wgrad_reduce_tr(int cin, int cout, const float* partial, int nparts, float* dw, float* db,
                            float scale, hipStream_t s) {
-#define CB_RT(CI, CO)                                                                                  \
+#define CB_RT(CI, CO, MD)                                                                              \
     if (cin == CI && cout == CO) {                                                                     \
-        hipLaunchKernelGGL((wgrad_tr_reduce_kernel<CI, CO, IN_PLAIN>),                                 \
-                           dim3((WgTr<CI, CO, IN_PLAIN>::PSTRIDE + 15) / 16), dim3(1024), 0, s, partial, \
+        hipLaunchKernelGGL((wgrad_tr_reduce_kernel<CI, CO, MD>),                                       \
+                           dim3((WgTr<CI, CO, MD>::PSTRIDE + 15) / 16), dim3(1024), 0, s, partial,     \
                            nparts, dw, db, scale);                                                     \
         return hipGetLastError();                                                                      \
     }
-    CB_RT(16, 16) CB_RT(16, 32) CB_RT(32, 32)
+    CB_RT(16, 16, IN_PLAIN) CB_RT(16, 32, IN_PLAIN) CB_RT(32, 32, IN_PLAIN)
+    CB_RT(4, 16, IN_U8) CB_RT(4, 32, IN_U8)
 #undef CB_RT
     return hipErrorInvalidValue;
 }

@@ -259,6 +259,51 @@ def test_conv_backward_fused_rejects_unsupported():
         P.impala_conv3x3_bwd(G.BF16, 1, 8, 8, 16, 16, b16, b16, P.X_RELU, w16, None, b16, dw, db, G.ws_bytes(16))
 
 
+# (n, H, W, cout): the first stage entry (base and wide) plus ragged and odd-padding shapes
+POOL_WGRAD_CASES = [(3, 84, 84, 16), (2, 84, 84, 32), (4, 13, 9, 16), (3, 11, 11, 32), (2, 42, 42, 16),
+                    (5, 7, 5, 16), (2, 23, 17, 32)]
+
+
+@pytest.mark.parametrize("case", POOL_WGRAD_CASES, ids=lambda c: "n%d_%dx%d_c%d" % c)
+def test_pool_wgrad_u8_fused(case):
+    """First stage entry backward in one pass (bf16): the max-pool gradient dC (first-max rule,
+    many ties), rounded to bf16 as the stand-alone pool backward stores it, contracted with the
+    gathered frames / 255; dw and db against the exact sums."""
+    n, H, W, C = case
+    rng = np.random.default_rng(43)
+    frames = rng.integers(0, 256, size=(n + 2, H, W, 4), dtype=np.uint8)
+    rows = rng.permutation(n + 2)[:n].astype(np.int32)
+    conv_out = rng.integers(-4, 5, size=(n, H, W, C)).astype(np.float64) * 0.25
+    _, arg = onet.maxpool(conv_out)
+    OH, OW = arg.shape[1:3]
+    dp = G.q(rng.standard_normal((n, OH, OW, C)), G.BF16)
+    dc = G.q(onet.maxpool_backward(arg, dp, (n, H, W, C)), G.BF16)
+    xin = frames[rows].astype(np.float64) / 255.0
+    want_w, want_b = onet.conv3x3_wgrad(xin, dc)
+    abs_w, abs_b = onet.conv3x3_wgrad(xin, np.abs(dc))
+    dw = G.dev_f32(np.full((3, 3, 4, C), np.nan))
+    db = G.dev_f32(np.full(C, np.nan))
+    ws = G.ws_bytes(P.impala_conv3x3_pool_wgrad_u8_workspace_bytes(G.BF16, C))
+    P.impala_conv3x3_pool_wgrad_u8(G.BF16, n, H, W, C, G.dev_u8(frames), G.dev_i32(rows), G.dev_act(dp, G.BF16),
+                                   G.dev_u8(arg), dw, db, ws)
+    G.sync()
+    G.assert_sum_close(G.host(dw), want_w, abs_w, 1e-5, "pool_wgrad dw")
+    G.assert_sum_close(G.host(db), want_b, abs_b, 1e-5, "pool_wgrad db")
+
+
+def test_pool_wgrad_u8_rejects_unsupported():
+    z8 = G.dev_u8(np.zeros((1, 8, 8, 4)))
+    dp = G.dev_act(np.zeros((1, 4, 4, 64)), G.BF16)
+    ag = G.dev_u8(np.zeros((1, 4, 4, 64)))
+    dw, db = G.dev_f32(np.zeros((3, 3, 4, 64))), G.dev_f32(np.zeros(64))
+    with pytest.raises(P.LibraryError):   # 64 output channels
+        P.impala_conv3x3_pool_wgrad_u8(G.BF16, 1, 8, 8, 64, z8, None, dp, ag, dw, db, G.ws_bytes(1 << 22))
+    with pytest.raises(P.LibraryError):   # float32 storage
+        P.impala_conv3x3_pool_wgrad_u8(G.FP32, 1, 8, 8, 16, z8, None, dp, ag, dw, db, G.ws_bytes(1 << 22))
+    with pytest.raises(P.LibraryError):   # workspace too small
+        P.impala_conv3x3_pool_wgrad_u8(G.BF16, 1, 8, 8, 16, z8, None, dp, ag, dw, db, G.ws_bytes(16))
+
+
 @pytest.mark.parametrize("prec", PRECS, ids=lambda p: PNAME[p])
 @pytest.mark.parametrize("case", CONV_CASES, ids=lambda c: "n%d_%dx%d_%d-%d_m%d" % c)
 def test_conv_weight_gradient(case, prec):
