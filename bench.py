@@ -42,6 +42,7 @@ def parse():
     ap.add_argument("--layer", default=None,
                     help="replay one profiling key's launch (e.g. conv_dgrad/bf16/32x32/21x21/mask/add) "
                          "--steps times through the C-ABI on the minibatch size, for counter runs")
+    ap.add_argument("--kernels", type=int, default=24, help="launch keys listed in kernels_top")
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="time a plain device copy of this many MiB --steps times (counter calibration)")
     return ap.parse_args()
@@ -86,13 +87,18 @@ def run_layer(P, key, n, steps):
             x, tt, y = act(h, w, ci), act(h, w, ci), act(h, w, ci)
             fn = lambda: P.impala_resblock_fwd(prec, n, h, w, ci, x, w1, b1, w2, b2, tt, y)  # noqa: E731
         elif fam == "conv_bwd":     # key channels: forward cin x cout
-            dy, wt = act(h, w, co), torch.randn(3, 3, ci, co, device="cuda", generator=g) * 0.1
+            pooled = "pool" in flags
+            oh, ow = (h + 1) // 2, (w + 1) // 2
+            dy = act(oh, ow, co) if pooled else act(h, w, co)
+            parg = torch.randint(0, 9, (n, oh, ow, co), dtype=torch.uint8, device="cuda", generator=g) if pooled else None
+            wt = torch.randn(3, 3, ci, co, device="cuda", generator=g) * 0.1
             add = act(h, w, ci) if "add" in flags else None
             dx = act(h, w, ci)
             dw = torch.empty(3, 3, ci, co, device="cuda")
             db = torch.empty(co, device="cuda")
             ws = torch.empty(P.impala_conv3x3_bwd_workspace_bytes(prec, ci, co), dtype=torch.uint8, device="cuda")
-            fn = lambda: P.impala_conv3x3_bwd(prec, n, h, w, ci, co, dy, x, mode, wt, add, dx, dw, db, ws)  # noqa: E731
+            fn = lambda: P.impala_conv3x3_bwd(prec, n, h, w, ci, co, dy, x, mode, wt, add, dx, dw, db, ws,  # noqa: E731
+                                              pool_arg=parg)
         elif fam == "conv_dgrad":   # key channels: dy (forward cout) x dx (forward cin)
             wt = torch.randn(3, 3, co, ci, device="cuda", generator=g) * 0.1
             mask = act(h, w, co) if "mask" in flags else None
@@ -213,11 +219,12 @@ def kernel_work(key, n, prec):
         h, w = map(int, parts[3].split("x"))
         oh, ow = (h + 1) // 2, (w + 1) // 2
         return "hbm", float(n * (h * w * 4 + oh * ow * co * (es + 1))), "B", 2.0 * n * h * w * 36 * co
-    if fam == "conv_bwd":   # one pass: x, dy and the residual operand in, dx out
+    if fam == "conv_bwd":   # one pass: x, dy (or the pooled dy and argmax) and the residual in, dx out
         ci, co = map(int, parts[2].split("x"))
         h, w = map(int, parts[3].split("x"))
         px = n * h * w
-        b = px * es * (ci + co + ci + (ci if "add" in parts[4:] else 0))
+        dyb = (n * ((h + 1) // 2) * ((w + 1) // 2) * co * (es + 1)) if "pool" in parts[4:] else px * co * es
+        b = px * es * (ci + ci + (ci if "add" in parts[4:] else 0)) + dyb
         return "hbm", float(b), "B", 2.0 * 2.0 * px * 9 * ci * co
     if fam in ("conv_fwd", "conv_dgrad", "wgrad", "conv_pool"):
         ci, co = map(int, parts[2].split("x"))
@@ -398,7 +405,7 @@ def main():
                      "traffic": traffic, "algorithmic_bytes": work if unit == "B" else None,
                      "mfma_tflops": round(mfma_tflops, 2) if mfma_tflops else None,
                      "mfma_frac": round(mfma_tflops / PEAK[args.prec][0], 4) if mfma_tflops else None},
-        "kernels_top": [{"key": k, "ms_per_step": round(t, 3), "launches": c} for k, t, c in table[:24]],
+        "kernels_top": [{"key": k, "ms_per_step": round(t, 3), "launches": c} for k, t, c in table[:args.kernels]],
     }
     if args.cpu_sample_frames > 0:
         line["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_frames)

@@ -77,21 +77,26 @@ impala_status_t impala_conv3x3_wgrad(impala_prec_t prec, int64_t n, int32_t H, i
 /* The whole backward pass of y = conv3x3_same(X, w) + bias in one pass, bf16 only, with
  * X = x (IMPALA_X_PLAIN) or relu(x) (IMPALA_X_RELU); Algorithm 1's back-propagation through
  * one convolution of Section 5's IMPALA-ResNet:
- *   dx = conv3x3_same^T(dy, w), then dx *= (x > 0) when x_mode is IMPALA_X_RELU, then
+ *   dx = conv3x3_same^T(G, w), then dx *= (x > 0) when x_mode is IMPALA_X_RELU, then
  *   dx += add if add is not NULL;
- *   dw, db as impala_conv3x3_wgrad with the same x and x_mode.
- * dy and x are staged on chip once and both gradients are formed from them, so the result
- * equals impala_conv3x3_dgrad (mask = x) plus impala_conv3x3_wgrad.
- * dy: [n, H, W, cout]; x, add, dx: [n, H, W, cin] (all bf16); w: float HWIO [3,3,cin,cout];
- * dw: float [3,3,cin,cout]; db: float [cout] (both overwritten); ws: device scratch of
- * impala_conv3x3_bwd_workspace_bytes() bytes. Supported: IMPALA_X_RELU with cin == cout in
- * {16, 32}; IMPALA_X_PLAIN without add for (cin, cout) in {(16,16), (16,32), (32,32)};
- * anything else returns IMPALA_EUNSUPPORTED. */
+ *   dw, db as impala_conv3x3_wgrad with the same x and x_mode and gradient G.
+ * G = dy when pool_arg is NULL. Otherwise the conv feeds a stage's max-pool (a stage entry)
+ * and dy is the gradient at the pool output, [n, ceil(H/2), ceil(W/2), cout], with pool_arg
+ * its argmax as impala_maxpool_fwd returns it; G is then the pool's input gradient, formed
+ * on chip exactly as impala_maxpool_bwd forms and rounds it.
+ * dy (or G) and x are staged on chip once and both gradients are formed from them, so the
+ * result equals impala_maxpool_bwd (with pool_arg), impala_conv3x3_dgrad (mask = x) and
+ * impala_conv3x3_wgrad.
+ * dy: [n, H, W, cout] or pooled as above; x, add, dx: [n, H, W, cin] (all bf16); w: float
+ * HWIO [3,3,cin,cout]; dw: float [3,3,cin,cout]; db: float [cout] (both overwritten); ws:
+ * device scratch of impala_conv3x3_bwd_workspace_bytes() bytes. Supported: IMPALA_X_RELU
+ * without pool_arg with cin == cout in {16, 32}; IMPALA_X_PLAIN without add for (cin, cout)
+ * in {(16,16), (16,32), (32,32)}; anything else returns IMPALA_EUNSUPPORTED. */
 size_t impala_conv3x3_bwd_workspace_bytes(impala_prec_t prec, int32_t cin, int32_t cout);
 impala_status_t impala_conv3x3_bwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t cin,
-                                   int32_t cout, const void* dy, const void* x, int32_t x_mode,
-                                   const float* w, const void* add, void* dx, float* dw, float* db,
-                                   void* ws, size_t ws_bytes, hipStream_t stream);
+                                   int32_t cout, const void* dy, const uint8_t* pool_arg, const void* x,
+                                   int32_t x_mode, const float* w, const void* add, void* dx, float* dw,
+                                   float* db, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Backward of the first stage entry of Section 5's IMPALA-ResNet, y = maxpool3x3s2_same(
  * conv3x3_same(frames / 255, w) + bias), in one pass, bf16 only (Algorithm 1's

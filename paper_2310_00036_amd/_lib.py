@@ -75,8 +75,8 @@ _SIGS = {
     "impala_conv3x3_wgrad": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _I32, _P, _I32, _P, _P, _P, _P,
                                        _P, _SZ, _P]),
     "impala_conv3x3_bwd_workspace_bytes": (_SZ, [C.c_int, _I32, _I32]),
-    "impala_conv3x3_bwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _I32, _P, _P, _I32, _P, _P, _P, _P, _P,
-                                     _P, _SZ, _P]),
+    "impala_conv3x3_bwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _I32, _P, _P, _P, _P,
+                                     _P, _P, _SZ, _P]),
     "impala_conv3x3_pool_wgrad_u8_workspace_bytes": (_SZ, [C.c_int, _I32]),
     "impala_conv3x3_pool_wgrad_u8": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _SZ,
                                                _P]),
@@ -306,10 +306,11 @@ def impala_conv3x3_bwd_workspace_bytes(prec, cin, cout) -> int:
     return int(lib.impala_conv3x3_bwd_workspace_bytes(prec, cin, cout))
 
 
-def impala_conv3x3_bwd(prec, n, H, W, cin, cout, dy, x, x_mode, w, add, dx, dw, db, ws, stream=None):
+def impala_conv3x3_bwd(prec, n, H, W, cin, cout, dy, x, x_mode, w, add, dx, dw, db, ws, stream=None,
+                       pool_arg=None):
     _check("impala_conv3x3_bwd", lib.impala_conv3x3_bwd(
-        prec, n, H, W, cin, cout, ptr(dy), ptr(x), x_mode, ptr(w), ptr(add), ptr(dx), ptr(dw), ptr(db), ptr(ws),
-        ws.numel() * ws.element_size(), stream_handle(stream)))
+        prec, n, H, W, cin, cout, ptr(dy), ptr(pool_arg), ptr(x), x_mode, ptr(w), ptr(add), ptr(dx), ptr(dw),
+        ptr(db), ptr(ws), ws.numel() * ws.element_size(), stream_handle(stream)))
 
 
 def impala_conv3x3_pool_wgrad_u8_workspace_bytes(prec, cout) -> int:

@@ -558,14 +558,14 @@ size_t impala_conv3x3_bwd_workspace_bytes(impala_prec_t prec, int32_t cin, int32
 }
 
 impala_status_t impala_conv3x3_bwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t cin,
-                                   int32_t cout, const void* dy, const void* x, int32_t x_mode,
-                                   const float* w, const void* add, void* dx, float* dw, float* db,
-                                   void* ws, size_t ws_bytes, hipStream_t stream) {
+                                   int32_t cout, const void* dy, const uint8_t* pool_arg, const void* x,
+                                   int32_t x_mode, const float* w, const void* add, void* dx, float* dw,
+                                   float* db, void* ws, size_t ws_bytes, hipStream_t stream) {
     impala_status_t st = check_layer(__func__, prec, n, H, W, cin, cout);
     if (st) return st;
-    if (prec != IMPALA_PREC_BF16 || !conv3x3_bwd_supported(cin, cout, x_mode, add != nullptr))
-        return fail(IMPALA_EUNSUPPORTED, "impala_conv3x3_bwd: unsupported prec=%d cin=%d cout=%d x_mode=%d add=%d",
-                    int(prec), cin, cout, x_mode, int(add != nullptr));
+    if (prec != IMPALA_PREC_BF16 || !conv3x3_bwd_supported(cin, cout, x_mode, add != nullptr, pool_arg != nullptr))
+        return fail(IMPALA_EUNSUPPORTED, "impala_conv3x3_bwd: unsupported prec=%d cin=%d cout=%d x_mode=%d add=%d pooled=%d",
+                    int(prec), cin, cout, x_mode, int(add != nullptr), int(pool_arg != nullptr));
     CHECK_PTR(dw); CHECK_PTR(db);
     if (n == 0) {
         hipError_t he = fill_zero(dw, int64_t(9) * cin * cout, stream);
@@ -576,7 +576,7 @@ impala_status_t impala_conv3x3_bwd(impala_prec_t prec, int64_t n, int32_t H, int
     const size_t need = conv3x3_bwd_partial_floats(cin, cout) * sizeof(float);
     if (ws_bytes < need) return fail(IMPALA_EWORKSPACE, "impala_conv3x3_bwd: workspace %zu < %zu", ws_bytes, need);
     ConvBwdArgs a{};
-    a.dy = dy; a.x = x; a.w = w; a.add = add; a.dx = dx; a.dw = dw; a.db = db;
+    a.dy = dy; a.arg = pool_arg; a.x = x; a.w = w; a.add = add; a.dx = dx; a.dw = dw; a.db = db;
     a.partial = static_cast<float*>(ws); a.n = int(n); a.H = H; a.W = W;
     return hip_status(conv3x3_bwd(cin, cout, x_mode, a, stream), "impala_conv3x3_bwd");
 }

@@ -48,10 +48,11 @@ struct CbGeom {
     // staging slots per lane (of an 8-wave workgroup) the tile planner stays within
     static constexpr int MAXD = CO > CI ? 7 : 6, MAXX = 4;
     static constexpr int MAXT = CI >= 32 ? 4 : 6;   // dx column tiles per wave and tile (with a residual)
+    static constexpr int MAXP = 3, MAXG = 2;         // pooled-gradient / argmax staging slots per lane
     __host__ __device__ static int blocks(int slots) { return (slots + 63) / 64; }
 };
 
-template <int CI, int CO, int MODE, int ADD, int NW>
+template <int CI, int CO, int MODE, int ADD, int PDY, int NW>
 __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbTile t) {
     using G = CbGeom<CI, CO>;
     constexpr int NT = 64 * NW;
@@ -61,6 +62,7 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
     constexpr int CB16 = CI / 16;
     static_assert(NW % MTI == 0, "waves split evenly over the dx channel blocks");
     static_assert(MODE == IN_PLAIN || MODE == IN_RELU, "bf16 activations");
+    static_assert(!PDY || (!ADD && MODE == IN_PLAIN), "a pooled gradient feeds a stage-entry conv");
 
     extern __shared__ __align__(16) unsigned char smem[];
     unsigned char* zero = smem;               // 64 zero bytes
@@ -74,6 +76,10 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
     const int TW = W + 2, TR = TH + 2;
 
     if (tid < 16) reinterpret_cast<uint32_t*>(zero)[tid] = 0u;
+    if constexpr (PDY) {
+        // the dy window is built in LDS: its padding columns and zero slots are never written
+        for (int j = tid; j < (t.x_off - t.dy_off) / 16; j += NT) reinterpret_cast<uint4*>(dyw)[j] = make_uint4(0, 0, 0, 0);
+    }
     // the x window's guard pixels (read only against zero dy padding, never staged)
     if (tid < XPB / 4) {
         reinterpret_cast<uint32_t*>(xw - XPB)[tid] = 0u;
@@ -145,7 +151,26 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
         return uint32_t(((f * H + rr - 1) * W + col - 1) * cbytes + c * 16);
     };
 #pragma unroll
-    for (int k = 0; k < G::MAXD; ++k) od[k] = win_off((wave + NW * k) * 64 + lane, DSL, CO / 8, CO * 2);
+    for (int k = 0; k < G::MAXD; ++k) od[k] = PDY ? kOOB : win_off((wave + NW * k) * 64 + lane, DSL, CO / 8, CO * 2);
+    // pooled gradient / argmax rows (PDY): LDS row rr holds pooled row ib0 - 1 + rr with a zero
+    // column either side; offsets relative to pooled row -1, a tile adds ib0 rows
+    const int PW2 = t.OW + 2;
+    const int nsp = t.PR * PW2 * (CO / 8), nsg = t.PR * PW2 * (CO / 16);
+    uint32_t opd[PDY ? G::MAXP : 1], oag[PDY ? G::MAXG : 1];
+    if constexpr (PDY) {
+#pragma unroll
+        for (int k = 0; k < G::MAXP; ++k) {
+            const int j = (wave + NW * k) * 64 + lane, px = j / (CO / 8), c = j - px * (CO / 8);
+            const int rr = px / PW2, col = px - rr * PW2;
+            opd[k] = (j < nsp && col >= 1 && col <= t.OW) ? uint32_t((((rr - 1) * t.OW + col - 1) * CO + c * 8) * 2) : kOOB;
+        }
+#pragma unroll
+        for (int k = 0; k < G::MAXG; ++k) {
+            const int j = (wave + NW * k) * 64 + lane, px = j / (CO / 16), c = j - px * (CO / 16);
+            const int rr = px / PW2, col = px - rr * PW2;
+            oag[k] = (j < nsg && col >= 1 && col <= t.OW) ? uint32_t(((rr - 1) * t.OW + col - 1) * CO + c * 16) : kOOB;
+        }
+    }
 #pragma unroll
     for (int k = 0; k < G::MAXX; ++k) ox[k] = win_off((wave + NW * k) * 64 + lane, XSL, CI / 8, CI * 2);
 
@@ -166,9 +191,33 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
             const auto rd = buf_rsrc(static_cast<const uint16_t*>(a.dy) + fpx * CO, uint32_t(nf) * H * W * CO * 2);
             const auto rx = buf_rsrc(static_cast<const uint16_t*>(a.x) + fpx * CI, uint32_t(nf) * H * W * CI * 2);
             const uint32_t hd = uint32_t(h0) * W * CO * 2, hx = uint32_t(h0) * W * CI * 2;
+            if constexpr (PDY) {
+                // pooled rows ib0-1 .. ib1 (this frame's pooled gradient and argmax)
+                const int ib0 = (h0 - 1 + t.ph) >> 1;   // arithmetic shift: floor
+                const uint32_t pb = uint32_t(t.OH) * t.OW * CO;
+                const auto rp = buf_rsrc(static_cast<const uint16_t*>(a.dy) + int64_t(f0) * pb, pb * 2);
+                const auto rg = buf_rsrc(a.arg + int64_t(f0) * pb, pb);
+                const uint32_t pr = uint32_t(ib0 * t.OW * CO);   // wraps for ib0 < 0: rows off the grid
 #pragma unroll
-            for (int k = 0; k < G::MAXD; ++k)
-                if ((wave + NW * k) * 64 < nsd) dma16_to_lds(rd, dyw + (wave + NW * k) * 1024, od[k] + hd);
+                for (int k = 0; k < G::MAXP; ++k)
+                    if ((wave + NW * k) * 64 < nsp) dma16_to_lds(rp, smem + t.dp_off + (wave + NW * k) * 1024, opd[k] + 2 * pr);
+#pragma unroll
+                for (int k = 0; k < G::MAXG; ++k)
+                    if ((wave + NW * k) * 64 < nsg) dma16_to_lds(rg, smem + t.ag_off + (wave + NW * k) * 1024, oag[k] + pr);
+                // dy-window rows off the frame hold zero (no block covers every such row)
+                for (int j = tid; j < TR * TW; j += NT) {
+                    const int rr = j / TW, h = h0 - 1 + rr;
+                    if (h < 0 || h >= H) {
+                        uint4* p = reinterpret_cast<uint4*>(dyw + j * DYP);
+#pragma unroll
+                        for (int c = 0; c < CO / 8; ++c) p[c] = make_uint4(0, 0, 0, 0);
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < G::MAXD; ++k)
+                    if ((wave + NW * k) * 64 < nsd) dma16_to_lds(rd, dyw + (wave + NW * k) * 1024, od[k] + hd);
+            }
 #pragma unroll
             for (int k = 0; k < G::MAXX; ++k)
                 if ((wave + NW * k) * 64 < nsx) dma16_to_lds(rx, xw + (wave + NW * k) * 1024, ox[k] + hx);
@@ -187,6 +236,64 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
         }
         __builtin_amdgcn_s_waitcnt(0);   // this wave's loads have landed in LDS
         __syncthreads();                 // ... and everyone else's
+        if constexpr (PDY) {
+            // ---- max-pool backward into the dy window: 2x2 blocks of padded cells
+            // (2i + a, 2j + b), windows (i-1 | i, j-1 | j) at LDS rows i - ib0, i - ib0 + 1 and
+            // columns j, j + 1; the stand-alone pool backward's gather and summation order
+            const int ib0 = (h0 - 1 + t.ph) >> 1;
+            const int ib1 = min((h0 + the + t.ph) >> 1, t.BH - 1);
+            const int ilo = max(ib0, 0);
+            const int items = (ib1 - ilo + 1) * t.BW * (CO / 4);   // 4 channels per item
+            const unsigned char* dpl = smem + t.dp_off;
+            const unsigned char* agl = smem + t.ag_off;
+            for (int it = tid; it < items; it += NT) {
+                const int c4 = it % (CO / 4), blk = it / (CO / 4);
+                const int bi = blk / t.BW, j = blk - bi * t.BW;
+                const int i = ilo + bi, lr = i - ib0;
+                uint32_t ka[4];
+                float v[4][4];
+#pragma unroll
+                for (int w4 = 0; w4 < 4; ++w4) {
+                    const int px = (lr + (w4 >> 1)) * PW2 + j + (w4 & 1);
+                    ka[w4] = *reinterpret_cast<const uint32_t*>(agl + px * CO + c4 * 4);
+                    const uint2 d4 = *reinterpret_cast<const uint2*>(dpl + (px * CO + c4 * 4) * 2);
+                    v[w4][0] = __uint_as_float(d4.x << 16); v[w4][1] = __uint_as_float(d4.x & 0xffff0000u);
+                    v[w4][2] = __uint_as_float(d4.y << 16); v[w4][3] = __uint_as_float(d4.y & 0xffff0000u);
+                }
+                float c00[4], c01[4], c10[4], c11[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    uint32_t k[4];
+#pragma unroll
+                    for (int w4 = 0; w4 < 4; ++w4) k[w4] = (ka[w4] >> (8 * e)) & 0xffu;
+                    float s00 = 0.f, s01 = 0.f, s10 = 0.f, s11 = 0.f;
+                    s00 += k[0] == 8 ? v[0][e] : 0.f;
+                    s00 += k[1] == 6 ? v[1][e] : 0.f;
+                    s00 += k[2] == 2 ? v[2][e] : 0.f;
+                    s00 += k[3] == 0 ? v[3][e] : 0.f;
+                    s01 += k[1] == 7 ? v[1][e] : 0.f;
+                    s01 += k[3] == 1 ? v[3][e] : 0.f;
+                    s10 += k[2] == 5 ? v[2][e] : 0.f;
+                    s10 += k[3] == 3 ? v[3][e] : 0.f;
+                    s11 += k[3] == 4 ? v[3][e] : 0.f;
+                    c00[e] = s00; c01[e] = s01; c10[e] = s10; c11[e] = s11;
+                }
+                // cells -> dy-window row h - h0 + 1, column w + 1; off the frame: zero
+                const int h = 2 * i - t.ph, w = 2 * j - t.pw;
+                auto put = [&](int hh, int ww, const float* c) {
+                    const int rr = hh - h0 + 1;
+                    if (rr < 0 || rr >= the + 2) return;
+                    const bool in = hh >= 0 && hh < H && ww >= 0 && ww < W;
+                    *reinterpret_cast<uint2*>(dyw + (rr * TW + ww + 1) * DYP + c4 * 8) =
+                        in ? make_uint2(pack2bf(c[0], c[1]), pack2bf(c[2], c[3])) : make_uint2(0, 0);
+                };
+                put(h, w, c00);
+                put(h, w + 1, c01);
+                put(h + 1, w, c10);
+                put(h + 1, w + 1, c11);
+            }
+            __syncthreads();
+        }
         if constexpr (MODE == IN_RELU) {
             // the conv read relu(x); relu(x) > 0 exactly where x > 0, so the mask reads it too
             uint4* w4 = reinterpret_cast<uint4*>(xw);
@@ -316,26 +423,35 @@ int cb_parts_cap() {
     return int(cap < 256 ? 256 : (cap > 1024 ? 1024 : cap));
 }
 
-template <int CI, int CO, int MODE, int ADD>
+template <int CI, int CO, int MODE, int ADD, int PDY>
 hipError_t cb_launch(const ConvBwdArgs& a, hipStream_t s) {
     using G = CbGeom<CI, CO>;
     const int H = a.H, W = a.W;
-    auto regions = [&](int th, int fr, int& dyb, int& xb) {
+    // max-pool geometry of a pooled input gradient (PDY): XLA SAME padding split
+    const int OH = (H + 1) / 2, OW = (W + 1) / 2;
+    const int PH = (OH - 1) * 2 + 3 - H, PWd = (OW - 1) * 2 + 3 - W;
+    const int ph = (PH > 0 ? PH : 0) / 2, pw = (PWd > 0 ? PWd : 0) / 2;
+    auto prows = [](int th) { return (th + 1) / 2 + 3; };   // pooled rows a band reads
+    auto regions = [&](int th, int fr, int& dyb, int& xb, int& pb, int& gb) {
         const int wp = fr * (th + 2) * (W + 2);
         dyb = G::blocks(wp * G::DSL) * 1024;
         xb = G::blocks(wp * G::XSL) * 1024 + 2 * G::XPB;   // + a guard pixel on either side
+        pb = PDY ? G::blocks(prows(th) * (OW + 2) * (CO / 8)) * 1024 : 0;
+        gb = PDY ? G::blocks(prows(th) * (OW + 2) * (CO / 16)) * 1024 : 0;
     };
     auto lds = [&](int th, int fr) {
-        int dyb, xb;
-        regions(th, fr, dyb, xb);
-        return size_t(64 + dyb + xb);
+        int dyb, xb, pb, gb;
+        regions(th, fr, dyb, xb, pb, gb);
+        return size_t(64 + dyb + xb + pb + gb);
     };
     // staging slots per lane within the kernel's register tables
     auto fits = [&](int th, int fr) {
         const int per = kCbWaves * 64, wp = fr * (th + 2) * (W + 2);
         const int tiles = (fr * th * W + 15) / 16, waves_per_block = kCbWaves / G::MTI;
-        return (wp * G::DSL + per - 1) / per <= G::MAXD && (wp * G::XSL + per - 1) / per <= G::MAXX &&
-               (!ADD || (tiles + waves_per_block - 1) / waves_per_block <= G::MAXT);
+        return (PDY || (wp * G::DSL + per - 1) / per <= G::MAXD) && (wp * G::XSL + per - 1) / per <= G::MAXX &&
+               (!ADD || (tiles + waves_per_block - 1) / waves_per_block <= G::MAXT) &&
+               (!PDY || (fr == 1 && (prows(th) * (OW + 2) * (CO / 8) + per - 1) / per <= G::MAXP &&
+                         (prows(th) * (OW + 2) * (CO / 16) + per - 1) / per <= G::MAXG));
     };
     const size_t limit = std::min<size_t>(lds_limit(), 160 * 1024);
     int thmax = std::min(H, std::max(1, kCbPixMax / W));
@@ -348,26 +464,30 @@ hipError_t cb_launch(const ConvBwdArgs& a, hipStream_t s) {
     }
     const int nbands = (H + TH - 1) / TH;
     int FR = 1;
-    if (nbands == 1)
+    if (nbands == 1 && !PDY)
         while (FR < a.n && lds(TH, FR + 1) <= kCbLdsTarget && fits(TH, FR + 1) && (FR + 1) * H * W <= kCbPixMax) ++FR;
     // 32-bit buffer offsets cover FR frames of each operand
     if (int64_t(FR) * H * W * std::max(CI, CO) * 2 >= (int64_t(1) << 31)) return hipErrorInvalidValue;
     CbTile t{};
     t.TH = TH; t.FR = FR; t.nbands = nbands; t.ntiles = nbands * ((a.n + FR - 1) / FR);
-    int dyb, xb;
-    regions(TH, FR, dyb, xb);
+    int dyb, xb, pb, gb;
+    regions(TH, FR, dyb, xb, pb, gb);
     t.dy_off = 64; t.x_off = t.dy_off + dyb;
     t.x_guard = xb - 2 * G::XPB;   // byte offset of the rear guard from the window start
+    t.dp_off = t.x_off + xb; t.ag_off = t.dp_off + pb;
+    t.PR = PDY ? prows(TH) : 0;
+    t.OH = OH; t.OW = OW; t.ph = ph; t.pw = pw; t.BH = (H + ph + 1) / 2; t.BW = (W + pw + 1) / 2;
     t.inv_W = 1.f / float(W); t.inv_TW = 1.f / float(W + 2);
     t.inv_TH = 1.f / float(TH); t.inv_TR = 1.f / float(TH + 2);
     const size_t L = lds(TH, FR);
-    const void* fn = reinterpret_cast<const void*>(&conv_bwd_kernel<CI, CO, MODE, ADD, kCbWaves>);
+    if (PDY && int64_t(OH) * OW * CO * 2 >= (int64_t(1) << 31)) return hipErrorInvalidValue;
+    const void* fn = reinterpret_cast<const void*>(&conv_bwd_kernel<CI, CO, MODE, ADD, PDY, kCbWaves>);
     int parts = std::min(resident_blocks(fn, 64 * kCbWaves, L), cb_parts_cap<CI, CO>());
     if (parts > t.ntiles) parts = t.ntiles;
-    const std::string shape = cb_dims(CI, CO) + "/" + cb_dims(H, W) + cb_flags(MODE, false, ADD);
+    const std::string shape = cb_dims(CI, CO) + "/" + cb_dims(H, W) + cb_flags(MODE, false, ADD) + (PDY ? "/pool" : "");
     {
         ProfScope ps(s, [&] { return cb_key("conv_bwd", 0, shape); });
-        hipLaunchKernelGGL((conv_bwd_kernel<CI, CO, MODE, ADD, kCbWaves>), dim3(unsigned(parts)), dim3(64 * kCbWaves),
+        hipLaunchKernelGGL((conv_bwd_kernel<CI, CO, MODE, ADD, PDY, kCbWaves>), dim3(unsigned(parts)), dim3(64 * kCbWaves),
                            L, s, a, t);
     }
     hipError_t e = hipGetLastError();
@@ -378,8 +498,8 @@ hipError_t cb_launch(const ConvBwdArgs& a, hipStream_t s) {
 
 }  // namespace
 
-bool conv3x3_bwd_supported(int cin, int cout, int mode, int add) {
-    if (mode == IN_RELU) return cin == cout && (cin == 16 || cin == 32);
+bool conv3x3_bwd_supported(int cin, int cout, int mode, int add, int pooled) {
+    if (mode == IN_RELU) return !pooled && cin == cout && (cin == 16 || cin == 32);
     if (mode == IN_PLAIN) return !add && ((cin == 16 && (cout == 16 || cout == 32)) || (cin == 32 && cout == 32));
     return false;
 }
@@ -395,11 +515,12 @@ size_t conv3x3_bwd_partial_floats(int cin, int cout) {
 
 hipError_t conv3x3_bwd(int cin, int cout, int mode, const ConvBwdArgs& a, hipStream_t s) {
     if (a.n <= 0) return hipSuccess;
-    const int add = a.add != nullptr;
-#define CB_B(CI, CO, MD, AD) \
-    if (cin == CI && cout == CO && mode == MD && add == AD) return cb_launch<CI, CO, MD, AD>(a, s);
-    CB_B(16, 16, IN_RELU, 0) CB_B(16, 16, IN_RELU, 1) CB_B(32, 32, IN_RELU, 0) CB_B(32, 32, IN_RELU, 1)
-    CB_B(16, 16, IN_PLAIN, 0) CB_B(16, 32, IN_PLAIN, 0) CB_B(32, 32, IN_PLAIN, 0)
+    const int add = a.add != nullptr, pdy = a.arg != nullptr;
+#define CB_B(CI, CO, MD, AD, PD) \
+    if (cin == CI && cout == CO && mode == MD && add == AD && pdy == PD) return cb_launch<CI, CO, MD, AD, PD>(a, s);
+    CB_B(16, 16, IN_RELU, 0, 0) CB_B(16, 16, IN_RELU, 1, 0) CB_B(32, 32, IN_RELU, 0, 0) CB_B(32, 32, IN_RELU, 1, 0)
+    CB_B(16, 16, IN_PLAIN, 0, 0) CB_B(16, 32, IN_PLAIN, 0, 0) CB_B(32, 32, IN_PLAIN, 0, 0)
+    CB_B(16, 16, IN_PLAIN, 0, 1) CB_B(16, 32, IN_PLAIN, 0, 1) CB_B(32, 32, IN_PLAIN, 0, 1)
 #undef CB_B
     return hipErrorInvalidValue;
 }

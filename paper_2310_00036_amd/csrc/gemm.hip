@@ -9,6 +9,8 @@
 #include "common.h"
 #include "kernels.h"
 
+#include <algorithm>
+
 #include <type_traits>
 
 namespace cb {
@@ -44,6 +46,34 @@ CB_DEV void gemm_epilogue(const GemmArgs& a, int m, int n, float v) {
         if (a.out2_f32) static_cast<float*>(a.out2)[o] = v;
         else static_cast<T*>(a.out2)[o] = P::store(v);
     }
+}
+
+// Four consecutive rows m .. m+3 of output column n at once (bf16 storage): one 8-byte
+// mask load and one 8-byte store. Falls back to the per-element epilogue where the group
+// straddles the row split or the edge, or the output is not 8-byte addressable that way.
+CB_DEV bool gemm_epilogue4_ok(const GemmArgs& a) {
+    const bool mask_ok = !a.mask || ((a.ldmask & 3) == 0 && (reinterpret_cast<uintptr_t>(a.mask) & 7) == 0);
+    return !a.out1_f32 && (a.ld1 & 3) == 0 && (reinterpret_cast<uintptr_t>(a.out1) & 7) == 0 && mask_ok;
+}
+CB_DEV void gemm_epilogue4_bf16(const GemmArgs& a, bool vec_ok, int m, int n, cb_f32x4 v) {
+    if (!vec_ok || n >= a.N || m + 4 > a.M || m + 4 > a.msplit) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) gemm_epilogue<PrecBF16>(a, m + r, n, v[r]);
+        return;
+    }
+    float o[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        o[r] = v[r] * a.alpha + (a.bias1 ? a.bias1[m + r] : 0.f);
+        if (a.relu) o[r] = relu_f(o[r]);
+    }
+    if (a.mask) {
+        float mk[4];
+        load4(static_cast<const uint16_t*>(a.mask) + int64_t(n) * a.ldmask + m, mk);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) o[r] = mk[r] > 0.f ? o[r] : 0.f;
+    }
+    store4(static_cast<uint16_t*>(a.out1) + int64_t(n) * a.ld1 + m, o[0], o[1], o[2], o[3]);
 }
 
 // Loads one BM(or BN) x BK tile of an operand into LDS as tile[row][k] (k contiguous).
@@ -298,6 +328,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a, int kchunk) 
         gemm_block<AKC, BKC, BRELU>(cur, nxt, k0 + kGK < k_end, ra, rb, a, m0, n0, k0 + kGK, k_end, wave, lane, acc);
     }
 
+    const bool vec_ok = gemm_epilogue4_ok(a);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -305,8 +336,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a, int kchunk) 
             const int mb = m0 + wm * 64 + i * 16 + 4 * g;
             const int n = n0 + wn * 64 + j * 16 + r16;
             if (gridDim.z == 1) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) gemm_epilogue<PrecBF16>(a, mb + r, n, acc[i][j][r]);
+                gemm_epilogue4_bf16(a, vec_ok, mb, n, acc[i][j]);
             } else if (n < a.N && mb < a.M) {
                 float* pp = a.partial + (int64_t(blockIdx.z) * a.N + n) * a.M + mb;
                 if (mb + 4 <= a.M && (a.M & 3) == 0) {
@@ -319,14 +349,18 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a, int kchunk) 
         }
 }
 
+// Sums the split-K partials in split order; grid (ceil(M / 256), min(N, 65535)).
 template <class P>
 __global__ __launch_bounds__(256) void gemm_finish_kernel(GemmArgs a, int splits) {
-    const int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    const int m = blockIdx.x * 256 + threadIdx.x;
+    if (m >= a.M) return;
     const int64_t total = int64_t(a.M) * a.N;
-    if (e >= total) return;
-    float s = 0.f;
-    for (int z = 0; z < splits; ++z) s += a.partial[z * total + e];
-    gemm_epilogue<P>(a, int(e % a.M), int(e / a.M), s);
+    for (int n = blockIdx.y; n < a.N; n += gridDim.y) {
+        const float* p = a.partial + int64_t(n) * a.M + m;
+        float s = 0.f;
+        for (int z = 0; z < splits; ++z) s += p[z * total];
+        gemm_epilogue<P>(a, m, n, s);
+    }
 }
 
 // Split-K so the grid covers the chip (about two workgroups per CU), never below 256 k per
@@ -404,9 +438,8 @@ static hipError_t gemm_dma_launch(const GemmArgs& a, hipStream_t s) {
     }
     if (z > 1) {
         ProfScope ps(s, [&] { return cb_key("gemm_finish", 0, shape); });
-        const int64_t total = int64_t(a.M) * a.N;
-        hipLaunchKernelGGL(gemm_finish_kernel<PrecBF16>, dim3(unsigned((total + 255) / 256)), dim3(256), 0,
-                           s, a, z);
+        hipLaunchKernelGGL(gemm_finish_kernel<PrecBF16>, dim3(unsigned((a.M + 255) / 256), unsigned(std::min(a.N, 65535))),
+                           dim3(256), 0, s, a, z);
     }
     return hipGetLastError();
 }
@@ -435,9 +468,8 @@ static hipError_t gemm_launch(const GemmArgs& a, hipStream_t s) {
     }
     if (z > 1) {
         ProfScope ps(s, [&] { return cb_key("gemm_finish", pr, shape); });
-        const int64_t total = int64_t(a.M) * a.N;
-        hipLaunchKernelGGL(gemm_finish_kernel<P>, dim3(unsigned((total + 255) / 256)), dim3(256), 0,
-                           s, a, z);
+        hipLaunchKernelGGL(gemm_finish_kernel<P>, dim3(unsigned((a.M + 255) / 256), unsigned(std::min(a.N, 65535))), dim3(256),
+                           0, s, a, z);
     }
     return hipGetLastError();
 }

@@ -64,7 +64,9 @@ bool wgrad_supported(int cin, int cout, int mode);
 // ---- whole backward pass of one 3x3 SAME conv (bf16): input gradient and weight gradient
 //      from one staging of dy and x. Forward: y = conv(X, w) + b, X = relu(x) (IN_RELU) or x.
 struct ConvBwdArgs {
-    const void* dy;         // [n, H, W, cout] bf16
+    const void* dy;         // [n, H, W, cout] bf16; with arg: the max-pool output gradient
+                            // [n, ceil(H/2), ceil(W/2), cout] of the pool this conv feeds
+    const uint8_t* arg;     // that pool's argmax (same shape), or NULL: dy is the conv's own
     const void* x;          // [n, H, W, cin] bf16, the forward input as stored
     const float* w;         // float32 HWIO [3,3,cin,cout]
     const void* add;        // [n, H, W, cin] added to dx, or NULL
@@ -78,9 +80,11 @@ struct CbTile {
     int TH, FR, nbands, ntiles;
     int dy_off, x_off;            // LDS byte offsets; 64 zero bytes at offset 0
     int x_guard;                  // x window: byte offset of its rear guard pixel
+    int dp_off, ag_off, PR;       // pooled gradient / argmax rows in LDS (PR rows), pooled input
+    int OH, OW, ph, pw, BH, BW;   // max-pool geometry (2x2 block grid BH x BW)
     float inv_W, inv_TW, inv_TH, inv_TR;
 };
-bool conv3x3_bwd_supported(int cin, int cout, int mode, int add);
+bool conv3x3_bwd_supported(int cin, int cout, int mode, int add, int pooled);
 size_t conv3x3_bwd_partial_floats(int cin, int cout);
 hipError_t conv3x3_bwd(int cin, int cout, int mode, const ConvBwdArgs& a, hipStream_t s);
 // Fixed-order sum of nparts bf16 weight-gradient partials laid out [mt*(NB+1) + nb]

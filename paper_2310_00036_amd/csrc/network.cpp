@@ -277,7 +277,7 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
             int fa, fb;
             others(gy, fa, fb);
             const int k0 = 1 + 2 * r, k1 = 2 + 2 * r;
-            if (p.prec == BF16 && conv3x3_bwd_supported(C, C, IN_RELU, 1)) {
+            if (p.prec == BF16 && conv3x3_bwd_supported(C, C, IN_RELU, 1, 0)) {
                 // each conv's input and weight gradients from one staging of its dy and input
                 ConvBwdArgs c1{};
                 c1.dy = G[gy]; c1.x = ws + p.t[st][r]; c1.w = params + po.conv_w[st][k1]; c1.dx = G[fa];
@@ -326,17 +326,20 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
             CB_TRY(pool_wgrad_u8(C, pa, s));
             continue;
         }
-        CB_TRY(maxpool_bwd(p.prec, int(n), p.H[st], p.W[st], C,
-                           reinterpret_cast<const uint8_t*>(ws + p.idx[st]), G[gy], G[fa], s));
-        if (st > 0 && p.prec == BF16 && conv3x3_bwd_supported(p.C[st], C, IN_PLAIN, 0)) {
+        if (st > 0 && p.prec == BF16 && conv3x3_bwd_supported(p.C[st], C, IN_PLAIN, 0, 1)) {
+            // the stage entry's max-pool backward, input and weight gradients in one pass: the
+            // full-resolution conv-output gradient is formed on chip from the pooled one
             ConvBwdArgs ce{};
-            ce.dy = G[fa]; ce.x = ws + p.x[st - 1][2]; ce.w = params + po.conv_w[st][0]; ce.dx = G[fb];
+            ce.dy = G[gy]; ce.arg = reinterpret_cast<const uint8_t*>(ws + p.idx[st]);
+            ce.x = ws + p.x[st - 1][2]; ce.w = params + po.conv_w[st][0]; ce.dx = G[fa];
             ce.dw = grads + po.conv_w[st][0]; ce.db = grads + po.conv_b[st][0]; ce.partial = scratch;
             ce.n = int(n); ce.H = p.H[st]; ce.W = p.W[st];
             CB_TRY(conv3x3_bwd(p.C[st], C, IN_PLAIN, ce, s));
-            gy = fb;
+            gy = fa;
             continue;
         }
+        CB_TRY(maxpool_bwd(p.prec, int(n), p.H[st], p.W[st], C,
+                           reinterpret_cast<const uint8_t*>(ws + p.idx[st]), G[gy], G[fa], s));
         WgradArgs we{};
         we.x = st == 0 ? static_cast<const void*>(obs) : static_cast<const void*>(ws + p.x[st - 1][2]);
         we.row_idx = st == 0 ? row_idx : nullptr;

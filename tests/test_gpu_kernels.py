@@ -243,6 +243,42 @@ def test_conv_backward_fused(case):
     G.assert_sum_close(G.host(db), want_b, abs_b, 1e-5, "conv_bwd db")
 
 
+# (n, H, W, cin, cout): stage entries fed by a max-pool (base and ragged, odd and even padding)
+CONV_BWD_POOL_CASES = [(3, 42, 42, 16, 32), (2, 21, 21, 32, 32), (4, 42, 42, 16, 16), (2, 17, 23, 16, 32),
+                       (5, 9, 7, 32, 32), (1, 84, 84, 16, 16), (3, 11, 11, 32, 32), (6, 4, 5, 16, 16)]
+
+
+@pytest.mark.parametrize("case", CONV_BWD_POOL_CASES, ids=lambda c: "n%d_%dx%d_%d-%d" % c)
+def test_conv_backward_fused_pooled(case):
+    """Stage-entry backward in one pass (bf16): the conv-output gradient is the max-pool
+    backward of the pooled gradient (first-max rule, many ties), rounded to bf16 as the
+    stand-alone pool backward stores it; dx to 1 bf16 ulp, dw and db against the exact sums."""
+    n, H, W, cin, cout = case
+    rng = np.random.default_rng(47)
+    conv_out = rng.integers(-4, 5, size=(n, H, W, cout)).astype(np.float64) * 0.25
+    _, arg = onet.maxpool(conv_out)
+    OH, OW = arg.shape[1:3]
+    dp = G.q(rng.standard_normal((n, OH, OW, cout)), G.BF16)
+    dc = G.q(onet.maxpool_backward(arg, dp, (n, H, W, cout)), G.BF16)
+    x = G.q(rng.standard_normal((n, H, W, cin)), G.BF16)
+    w = (rng.standard_normal((3, 3, cin, cout)) * np.sqrt(2.0 / (9 * cin))).astype(np.float32)
+    wq = G.q(w, G.BF16)
+    want = onet.conv3x3_dgrad(dc, wq)
+    absum = onet.conv3x3_dgrad(np.abs(dc), np.abs(wq))
+    want_w, want_b = onet.conv3x3_wgrad(x, dc)
+    abs_w, abs_b = onet.conv3x3_wgrad(np.abs(x), np.abs(dc))
+    dx = G.empty_act((n, H, W, cin), G.BF16)
+    dw = G.dev_f32(np.full((3, 3, cin, cout), np.nan))
+    db = G.dev_f32(np.full(cout, np.nan))
+    ws = G.ws_bytes(P.impala_conv3x3_bwd_workspace_bytes(G.BF16, cin, cout))
+    P.impala_conv3x3_bwd(G.BF16, n, H, W, cin, cout, G.dev_act(dp, G.BF16), G.dev_act(x, G.BF16), P.X_PLAIN,
+                         G.dev_f32(w), None, dx, dw, db, ws, pool_arg=G.dev_u8(arg))
+    G.sync()
+    G.assert_bf16_ulp(G.host(dx), want, absum, "conv_bwd pooled dx")
+    G.assert_sum_close(G.host(dw), want_w, abs_w, 1e-5, "conv_bwd pooled dw")
+    G.assert_sum_close(G.host(db), want_b, abs_b, 1e-5, "conv_bwd pooled db")
+
+
 def test_conv_backward_fused_rejects_unsupported():
     ws = G.ws_bytes(1 << 20)
     z = G.dev_act(np.zeros((1, 8, 8, 64)), G.BF16)
@@ -257,6 +293,9 @@ def test_conv_backward_fused_rejects_unsupported():
     b16 = G.dev_act(np.zeros((1, 8, 8, 16)), G.BF16)
     with pytest.raises(P.LibraryError):   # too small a workspace
         P.impala_conv3x3_bwd(G.BF16, 1, 8, 8, 16, 16, b16, b16, P.X_RELU, w16, None, b16, dw, db, G.ws_bytes(16))
+    with pytest.raises(P.LibraryError):   # a pooled gradient feeds a plain (stage-entry) conv only
+        P.impala_conv3x3_bwd(G.BF16, 1, 8, 8, 16, 16, b16, b16, P.X_RELU, w16, None, b16, dw, db, ws,
+                             pool_arg=G.dev_u8(np.zeros((1, 4, 4, 16))))
 
 
 # (n, H, W, cout): the first stage entry (base and wide) plus ragged and odd-padding shapes
