@@ -881,6 +881,7 @@ bool conv3x3_supported(int cin, int cout, int mode, int flip) {
 
 hipError_t conv3x3_pool(int cin, int cout, int mode, const ConvArgs& a, hipStream_t s) {
     if (a.n <= 0) return hipSuccess;
+    if (conv_pool_fast_supported(cin, cout, mode)) return conv_pool_fast(cin, cout, mode, a, s);
 #define CB_CP(CI, CO, MD) \
     if (cin == CI && cout == CO && mode == MD) \
         return launch_bf16_pool<CI, conv_group<PrecBF16, CI, CO>(), MD>(a, CO, s);

@@ -35,6 +35,15 @@ bool conv3x3_supported(int cin, int cout, int mode, int flip);
 // output kept in LDS; OH = (H+1)/2, OW = (W+1)/2. Modes IN_U8 and IN_PLAIN.
 hipError_t conv3x3_pool(int cin, int cout, int mode, const ConvArgs& a, hipStream_t s);
 
+// Tile of the conv + max-pool kernel (conv_pool_fast): bands of PTH pooled rows.
+struct CpTile {
+    int PTH, nbands, ntiles, OH, OW, ph, pw, THmax;
+    int raw_off, win_off, win_guard, key_off;   // LDS layout (bytes)
+    float inv_OW, inv_TW;
+};
+bool conv_pool_fast_supported(int cin, int cout, int mode);
+hipError_t conv_pool_fast(int cin, int cout, int mode, const ConvArgs& a, hipStream_t s);
+
 // ---- a whole residual block, bf16 forward: t = conv1(relu(x)) + b1 (stored),
 //      y = x + conv2(relu(t)) + b2; all tensors [n, H, W, C], weights float32 HWIO [3,3,C,C].
 struct ResBlockArgs {

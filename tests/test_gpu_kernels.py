@@ -72,7 +72,9 @@ def test_conv_forward(case, prec):
 
 POOL_CASES = [(3, 84, 84, 4, 16, P.X_U8), (2, 84, 84, 4, 32, P.X_U8), (2, 13, 9, 4, 64, P.X_U8),
               (3, 42, 42, 16, 32, P.X_PLAIN), (2, 42, 42, 16, 16, P.X_PLAIN), (4, 21, 21, 32, 32, P.X_PLAIN),
-              (5, 11, 11, 32, 64, P.X_PLAIN), (2, 17, 23, 16, 64, P.X_PLAIN), (3, 21, 21, 64, 64, P.X_PLAIN)]
+              (5, 11, 11, 32, 64, P.X_PLAIN), (2, 17, 23, 16, 64, P.X_PLAIN), (3, 21, 21, 64, 64, P.X_PLAIN),
+              (3, 17, 23, 16, 32, P.X_PLAIN), (2, 13, 9, 4, 16, P.X_U8), (4, 9, 7, 32, 32, P.X_PLAIN),
+              (5, 11, 11, 32, 32, P.X_PLAIN), (1, 6, 5, 16, 16, P.X_PLAIN), (2, 23, 19, 4, 32, P.X_U8)]
 
 
 def _pool_windows(x, fill):
