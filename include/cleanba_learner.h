@@ -100,7 +100,8 @@ impala_status_t impala_cnn_fwd(const impala_net_t* net, impala_prec_t prec, cons
 
 /* Backward pass ("back-propagate" in Algorithm 1): the flat float32 gradient
  * grads [param_count] of sum(dlogits * logits) + sum(dvalue * value) w.r.t. every parameter,
- * reading the activations a training-mode impala_cnn_fwd left in `ws`.
+ * reading the activations a training-mode impala_cnn_fwd left in `ws` (in bf16 mode also
+ * its bf16 copy of the dense weights, so `params` must be the forward's).
  * dlogits: [n, A]; dvalue: [n]. */
 impala_status_t impala_cnn_bwd(const impala_net_t* net, impala_prec_t prec, const float* params,
                                const uint8_t* obs, const int32_t* row_idx, int64_t n, void* ws,

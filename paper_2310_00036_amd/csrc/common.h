@@ -167,3 +167,43 @@ CB_DEV double block_sum(double v, double* sh) {
     __syncthreads();
     return r;
 }
+
+// Entry-wise sum of `nparts` float32 partial vectors (stride `pstride` floats, a multiple of
+// 4, 16-byte aligned) in a fixed order: a 1024-thread block covers 64 entries as 16 float4
+// lanes x 64 slices; slice s adds the partials s, s + 64, s + 128, ... in turn (eight loads
+// in flight), then a fixed pairwise tree over the slices. emit(e, v) gets entries e..e+3.
+template <class F>
+CB_DEV void sum_partials_x4(const float* __restrict__ partial, int nparts, int pstride, F&& emit) {
+    __shared__ float4 sh[64][17];
+    const int q = threadIdx.x & 15, sl = threadIdx.x >> 4;
+    const int e = blockIdx.x * 64 + 4 * q;
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (e < pstride) {
+        const float4* p = reinterpret_cast<const float4*>(partial + e);
+        const int64_t st = pstride / 4;
+        int k = sl;
+        for (; k + 7 * 64 < nparts; k += 8 * 64) {
+            float4 v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = p[int64_t(k + 64 * u) * st];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) { s.x += v[u].x; s.y += v[u].y; s.z += v[u].z; s.w += v[u].w; }
+        }
+        for (; k < nparts; k += 64) {
+            const float4 v = p[int64_t(k) * st];
+            s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+        }
+    }
+    sh[sl][q] = s;
+    __syncthreads();
+#pragma unroll
+    for (int w = 32; w >= 1; w >>= 1) {
+        if (sl < w) {
+            const float4 o = sh[sl + w][q];
+            float4& m = sh[sl][q];
+            m.x += o.x; m.y += o.y; m.z += o.z; m.w += o.w;
+        }
+        __syncthreads();
+    }
+    if (sl == 0 && e < pstride) emit(e, sh[0][q]);
+}

@@ -329,6 +329,43 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a, int kchunk) 
     }
 
     const bool vec_ok = gemm_epilogue4_ok(a);
+    if (gridDim.z == 1 && vec_ok && m0 + kGB <= a.M && m0 + kGB <= a.msplit && n0 + kGB <= a.N) {
+        // whole tile inside the output: every bias and mask load is issued before the first
+        // use, so the epilogue waits for one load latency rather than sixteen
+        uint2 mk[4][4];
+        float bs[4][4];
+        const uint16_t* mask = static_cast<const uint16_t*>(a.mask);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int mb = m0 + wm * 64 + i * 16 + 4 * g;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) bs[i][r] = a.bias1 ? a.bias1[mb + r] : 0.f;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int n = n0 + wn * 64 + j * 16 + r16;
+                mk[i][j] = mask ? *reinterpret_cast<const uint2*>(mask + int64_t(n) * a.ldmask + mb) : make_uint2(0u, 0u);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int mb = m0 + wm * 64 + i * 16 + 4 * g;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int n = n0 + wn * 64 + j * 16 + r16;
+                float o[4];
+                const uint32_t mw[4] = {mk[i][j].x << 16, mk[i][j].x & 0xffff0000u, mk[i][j].y << 16,
+                                        mk[i][j].y & 0xffff0000u};
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    o[r] = acc[i][j][r] * a.alpha + bs[i][r];
+                    if (a.relu) o[r] = relu_f(o[r]);
+                    if (mask && !(__uint_as_float(mw[r]) > 0.f)) o[r] = 0.f;
+                }
+                store4(static_cast<uint16_t*>(a.out1) + int64_t(n) * a.ld1 + mb, o[0], o[1], o[2], o[3]);
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -358,7 +395,15 @@ __global__ __launch_bounds__(256) void gemm_finish_kernel(GemmArgs a, int splits
     for (int n = blockIdx.y; n < a.N; n += gridDim.y) {
         const float* p = a.partial + int64_t(n) * a.M + m;
         float s = 0.f;
-        for (int z = 0; z < splits; ++z) s += p[z * total];
+        int z = 0;
+        for (; z + 8 <= splits; z += 8) {   // eight loads in flight, added in split order
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = p[(z + u) * total];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; z < splits; ++z) s += p[z * total];
         gemm_epilogue<P>(a, m, n, s);
     }
 }
@@ -476,107 +521,6 @@ static hipError_t gemm_launch(const GemmArgs& a, hipStream_t s) {
 
 hipError_t gemm(int prec, const GemmArgs& a, hipStream_t s) {
     return prec == BF16 ? gemm_launch<PrecBF16>(a, s) : gemm_launch<PrecF32>(a, s);
-}
-
-// ------------------------------------------------------------------ column sums
-// out[c] = sum_r x[r*ld + c], two passes with a fixed order: 64 columns x 4 row lanes per
-// block and up to 64 row slabs, then one pass over the slabs.
-template <class T>
-__global__ __launch_bounds__(256) void colsum_kernel(const T* __restrict__ x, int64_t rows, int cols,
-                                                     int64_t ld, float* __restrict__ partial,
-                                                     int slabs) {
-    __shared__ float sh[4][64];
-    const int c = blockIdx.x * 64 + (threadIdx.x & 63);
-    const int rl = threadIdx.x >> 6;
-    const int64_t per = (rows + slabs - 1) / slabs;
-    const int64_t r0 = int64_t(blockIdx.y) * per, r1 = r0 + per < rows ? r0 + per : rows;
-    float s = 0.f;
-    if (c < cols)
-        for (int64_t r = r0 + rl; r < r1; r += 4) {
-            if constexpr (sizeof(T) == 2) s += bf2f(x[r * ld + c]);
-            else s += x[r * ld + c];
-        }
-    sh[rl][threadIdx.x & 63] = s;
-    __syncthreads();
-    if (rl == 0 && c < cols)
-        partial[int64_t(blockIdx.y) * cols + c] = ((sh[0][threadIdx.x] + sh[1][threadIdx.x]) + sh[2][threadIdx.x]) + sh[3][threadIdx.x];
-}
-
-__global__ void colsum_finish_kernel(const float* __restrict__ partial, int cols, int slabs,
-                                     float* __restrict__ out) {
-    const int c = blockIdx.x * 256 + threadIdx.x;
-    if (c >= cols) return;
-    float s = 0.f;
-    for (int z = 0; z < slabs; ++z) s += partial[int64_t(z) * cols + c];
-    out[c] = s;
-}
-
-constexpr int kColSlabs = 64;
-
-size_t colsum_partial_floats(int cols) { return size_t(kColSlabs) * cols; }
-
-hipError_t colsum(int prec_storage, const void* x, int64_t rows, int cols, int64_t ld, float* out,
-                  float* partial, hipStream_t s) {
-    if (cols <= 0) return hipSuccess;
-    int slabs = int(rows < kColSlabs ? (rows > 0 ? rows : 1) : kColSlabs);
-    ProfScope ps(s, [&] { return cb_key("colsum", prec_storage, std::to_string(cols)); });
-    dim3 grid((cols + 63) / 64, slabs);
-    if (prec_storage == BF16)
-        hipLaunchKernelGGL(colsum_kernel<uint16_t>, grid, dim3(256), 0, s,
-                           static_cast<const uint16_t*>(x), rows, cols, ld, partial, slabs);
-    else
-        hipLaunchKernelGGL(colsum_kernel<float>, grid, dim3(256), 0, s, static_cast<const float*>(x),
-                           rows, cols, ld, partial, slabs);
-    hipLaunchKernelGGL(colsum_finish_kernel, dim3((cols + 255) / 256), dim3(256), 0, s, partial, cols,
-                       slabs, out);
-    return hipGetLastError();
-}
-
-// ------------------------------------------------------------------ head packing
-// out[a][j]: rows 0..A-1 are the logit weights' columns, row A is the value weights.
-__global__ void pack_heads_w_kernel(const float* __restrict__ wl, const float* __restrict__ wv,
-                                    int hidden, int A, float* __restrict__ out) {
-    const int e = blockIdx.x * 256 + threadIdx.x;
-    if (e >= (A + 1) * hidden) return;
-    const int a = e / hidden, j = e % hidden;
-    out[e] = a < A ? wl[int64_t(j) * A + a] : wv[j];
-}
-
-hipError_t pack_heads_w(const float* wl, const float* wv, int hidden, int A, float* out,
-                        hipStream_t s) {
-    const int total = (A + 1) * hidden;
-    ProfScope ps(s, [&] { return std::string("pack_heads_w"); });
-    hipLaunchKernelGGL(pack_heads_w_kernel, dim3((total + 255) / 256), dim3(256), 0, s, wl, wv,
-                       hidden, A, out);
-    return hipGetLastError();
-}
-
-// out[i][a] = dlogits[i][a] (a < A), dvalue[i] (a == A), in the storage type.
-template <class T>
-__global__ void pack_dz_kernel(const float* __restrict__ dl, const float* __restrict__ dv,
-                               int64_t n, int A, T* __restrict__ out) {
-    const int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x;
-    if (e >= n * (A + 1)) return;
-    const int64_t i = e / (A + 1);
-    const int a = int(e % (A + 1));
-    const float v = a < A ? dl[i * A + a] : dv[i];
-    if constexpr (sizeof(T) == 2) out[e] = f2bf(v);
-    else out[e] = v;
-}
-
-hipError_t pack_dz(int prec, const float* dlogits, const float* dvalue, int64_t n, int A, void* out,
-                   hipStream_t s) {
-    const int64_t total = n * (A + 1);
-    if (total <= 0) return hipSuccess;
-    const dim3 grid(unsigned((total + 255) / 256));
-    ProfScope ps(s, [&] { return cb_key("pack_dz", prec, std::to_string(A)); });
-    if (prec == BF16)
-        hipLaunchKernelGGL(pack_dz_kernel<uint16_t>, grid, dim3(256), 0, s, dlogits, dvalue, n, A,
-                           static_cast<uint16_t*>(out));
-    else
-        hipLaunchKernelGGL(pack_dz_kernel<float>, grid, dim3(256), 0, s, dlogits, dvalue, n, A,
-                           static_cast<float*>(out));
-    return hipGetLastError();
 }
 
 }  // namespace cb

@@ -1,0 +1,354 @@
+// Policy-logit and value heads of the network (Section 5: the dense layer's output feeds a
+// linear policy head over the actions and a linear value head), forward and backward.
+//
+// Both heads together are one [J] -> [A + 1] linear map (column A is the value head). It is
+// a few MFLOP per minibatch, so these kernels use float32 FMAs with the weights staged in
+// LDS and make every pass over the hidden activations h count:
+//   forward:  logits and value for 16 rows per workgroup;
+//   backward: one pass over h and the head gradients dz produces the masked hidden
+//             gradient dh = (dz W^T) * (h > 0) in the storage type, and per-workgroup
+//             partial sums of the head weight gradient h^T dz, of the head bias gradient
+//             (column sums of dz) and of the dense-layer bias gradient (column sums of dh
+//             as stored); a second kernel adds the partials in a fixed order.
+#include "common.h"
+#include "kernels.h"
+
+#include <algorithm>
+
+namespace cb {
+
+namespace {
+
+constexpr int kHR = 16;    // rows per row group
+constexpr int kHJ = 256;   // hidden units per chunk: one per thread
+constexpr size_t kHeadsPartialCap = size_t(8) << 20;   // floats of partials at most
+
+template <class T>
+CB_DEV float ld_st(const T* p, int64_t i) {
+    if constexpr (sizeof(T) == 2) return bf2f(p[i]);
+    else return p[i];
+}
+
+// ws[jj][aa] (pitch MA | 1, odd: conflict-free column reads) = W(j0 + jj, aa) for the chunk:
+// the logit weights' row for aa < A, the value weight for aa == A, zero for aa > A and for
+// units past the chunk's nj, so the inner loops run over all MA columns and 256 units
+// without conditions. Thread t stages unit t's row; its loads are unconditional (clamped
+// indices) and all issued before the first store. AC > 0 fixes the action count at compile
+// time (MA = AC + 1: no padding columns, no uniform branches around the loads); 0 reads it
+// from the arguments.
+template <int AC, int MA>
+CB_DEV void stage_head_w(float* ws, const HeadsArgs& a, int j0, int nj) {
+    constexpr int PW = MA | 1;
+    const int A = AC > 0 ? AC : a.A;
+    const int t = threadIdx.x;
+    const int jc = j0 + min(t, nj - 1);
+    const float* wr = a.wl + int64_t(jc) * A;
+    const float wv = a.wv[jc];
+    float v[MA];
+#pragma unroll
+    for (int c = 0; c < MA; ++c) {
+        const float x = wr[min(c, A - 1)];
+        v[c] = c < A ? x : (c == A ? wv : 0.f);
+    }
+    const bool ok = t < nj;
+#pragma unroll
+    for (int c = 0; c < MA; ++c) ws[t * PW + c] = ok ? v[c] : 0.f;
+}
+
+// logits[i][a] = bl[a] + sum_j h[i][j] wl[j][a]; value[i] = bv + sum_j h[i][j] wv[j].
+// Thread (r, q) of the 16 x 16 layout takes row r and the units 16q .. 16q+15 of every
+// chunk (two 16-byte loads of h for bf16), accumulating all MA columns over them in order;
+// the 16 slices' sums are then added in slice order through LDS.
+template <class T, int AC, int MA>
+__global__ __launch_bounds__(256) void heads_fwd_kernel(HeadsArgs a, float* __restrict__ logits,
+                                                        float* __restrict__ value) {
+    extern __shared__ float sm[];
+    constexpr int PW = MA | 1;
+    const int A = AC > 0 ? AC : a.A;
+    float* ws = sm;   // [kHJ][PW]; reused as the slice sums [16 q][16 r][MA] at the end
+    const int tid = threadIdx.x, r = tid & 15, q = tid >> 4;
+    const int64_t row0 = int64_t(blockIdx.x) * kHR;
+    const int64_t rowc = std::min<int64_t>(row0 + r, a.n - 1);
+    const bool row_ok = row0 + r < a.n;
+    const T* h = static_cast<const T*>(a.h);
+    float acc[MA];
+#pragma unroll
+    for (int c = 0; c < MA; ++c) acc[c] = 0.f;
+    for (int j0 = 0; j0 < a.J; j0 += kHJ) {
+        const int nj = min(kHJ, a.J - j0);
+        float hv[16];
+        if (sizeof(T) == 2 && (a.J & 7) == 0 && j0 + 16 * q + 16 <= a.J) {
+            const uint4* p = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(a.h) + rowc * a.J + j0 + 16 * q);
+            const uint4 u0 = p[0], u1 = p[1];
+            const uint32_t w[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                hv[2 * k] = __uint_as_float(w[k] << 16);
+                hv[2 * k + 1] = __uint_as_float(w[k] & 0xffff0000u);
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < 16; ++k) {
+                const int jj = min(16 * q + k, nj - 1);
+                hv[k] = 16 * q + k < nj ? ld_st(h, rowc * a.J + j0 + jj) : 0.f;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < 16; ++k) hv[k] = row_ok ? hv[k] : 0.f;
+        __syncthreads();
+        stage_head_w<AC, MA>(ws, a, j0, nj);
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            const float* wr = ws + (16 * q + k) * PW;
+#pragma unroll
+            for (int c = 0; c < MA; ++c) acc[c] += hv[k] * wr[c];
+            if (k % 2 == 1) __builtin_amdgcn_sched_barrier(0);   // bounds the LDS reads in flight
+        }
+    }
+    __syncthreads();
+    float* red = sm;
+#pragma unroll
+    for (int c = 0; c < MA; ++c) red[(q * 16 + r) * MA + c] = acc[c];
+    __syncthreads();
+    const int A1 = A + 1;
+    for (int o = tid; o < 16 * A1; o += kHJ) {
+        const int rr = o / A1, aa = o - rr * A1;
+        float t = 0.f;
+#pragma unroll
+        for (int qq = 0; qq < 16; ++qq) t += red[(qq * 16 + rr) * MA + aa];
+        const int64_t row = row0 + rr;
+        if (row < a.n) {
+            if (aa < A) logits[row * A + aa] = t + a.bl[aa];
+            else value[row] = t + a.bv[0];
+        }
+    }
+}
+
+// Partial layout per workgroup (stride pstride):
+//   [aa * J + j]          sum over its rows of h[i][j] dz[i][aa]    (aa <= A)
+//   [(A + 1) * J + j]     sum over its rows of dh[i][j] (as stored)
+//   [(A + 2) * J + aa]    sum over its rows of dz[i][aa]            (aa <= A)
+// Workgroup b takes the row groups b, b + gridDim.x, ... in increasing order; thread t owns
+// hidden unit j0 + t of each chunk.
+template <class T, int AC, int MA>
+__global__ __launch_bounds__(256) void heads_bwd_kernel(HeadsArgs a, const float* __restrict__ dl,
+                                                        const float* __restrict__ dv, T* __restrict__ dh,
+                                                        float* __restrict__ partial, int pstride) {
+    extern __shared__ float sm[];
+    constexpr int PW = MA | 1;
+    const int A = AC > 0 ? AC : a.A;
+    const int A1 = A + 1;
+    float* ws = sm;               // [kHJ][PW]
+    float* dzs = sm + kHJ * PW;   // [MA][16]: the row group's dz, action-major, zero past A
+    const int tid = threadIdx.x;
+    const int64_t ngroups = (a.n + kHR - 1) / kHR;
+    float* part = partial + int64_t(blockIdx.x) * pstride;
+    const T* h = static_cast<const T*>(a.h);
+    float hb = 0.f;
+    for (int j0 = 0; j0 < a.J; j0 += kHJ) {
+        const int nj = min(kHJ, a.J - j0);
+        const int j = j0 + min(tid, nj - 1);
+        const bool own = tid < nj;
+        __syncthreads();
+        stage_head_w<AC, MA>(ws, a, j0, nj);
+        float pw[MA];
+#pragma unroll
+        for (int aa = 0; aa < MA; ++aa) pw[aa] = 0.f;
+        float pb = 0.f;
+        for (int64_t grp = blockIdx.x; grp < ngroups; grp += gridDim.x) {
+            const int64_t r0 = grp * kHR;
+            const int nr = int(std::min<int64_t>(kHR, a.n - r0));
+            float hv[kHR];
+#pragma unroll
+            for (int rr = 0; rr < kHR; ++rr) hv[rr] = ld_st(h, std::min<int64_t>(r0 + rr, a.n - 1) * a.J + j);
+            __syncthreads();
+            {
+                // the group's dz, action-major: thread (rr, g) stages actions g, g + 16, ...
+                // of row rr; zero past A and for rows past n
+                constexpr int U = (MA + 15) / 16;
+                const int rr = tid & 15, g = tid >> 4;
+                const int64_t rowc = r0 + min(rr, nr - 1);
+                const float dvr = dv[rowc];
+                float v[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int aa = g + 16 * u;
+                    const float x = dl[rowc * A + min(aa, A - 1)];
+                    v[u] = rr < nr ? (aa < A ? x : (aa == A ? dvr : 0.f)) : 0.f;
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    if (g + 16 * u < MA) dzs[(g + 16 * u) * kHR + rr] = v[u];
+            }
+            __syncthreads();
+            if (j0 == 0 && tid < A1) {
+#pragma unroll
+                for (int rr = 0; rr < kHR; ++rr) hb += dzs[tid * kHR + rr];
+            }
+#pragma unroll
+            for (int rr = 0; rr < kHR; ++rr) hv[rr] = rr < nr ? hv[rr] : 0.f;
+            float acc[kHR];
+#pragma unroll
+            for (int rr = 0; rr < kHR; ++rr) acc[rr] = 0.f;
+            const float* wr = ws + min(tid, nj - 1) * PW;
+#pragma unroll
+            for (int aa = 0; aa < MA; ++aa) {
+                const float w = wr[aa];
+                const float4* d4 = reinterpret_cast<const float4*>(dzs + aa * kHR);
+                float s = pw[aa];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const float4 d = d4[q];
+                    acc[4 * q] += d.x * w; s += hv[4 * q] * d.x;
+                    acc[4 * q + 1] += d.y * w; s += hv[4 * q + 1] * d.y;
+                    acc[4 * q + 2] += d.z * w; s += hv[4 * q + 2] * d.z;
+                    acc[4 * q + 3] += d.w * w; s += hv[4 * q + 3] * d.w;
+                }
+                pw[aa] = s;
+                if (aa % 4 == 3) __builtin_amdgcn_sched_barrier(0);   // bounds the LDS reads in flight
+            }
+            if (own) {
+#pragma unroll
+                for (int rr = 0; rr < kHR; ++rr) {
+                    if (rr < nr) {
+                        const int64_t row = r0 + rr;
+                        const float v = hv[rr] > 0.f ? acc[rr] : 0.f;
+                        if constexpr (sizeof(T) == 2) {
+                            const uint16_t b = f2bf(v);
+                            dh[row * a.J + j] = b;
+                            pb += bf2f(b);
+                        } else {
+                            dh[row * a.J + j] = v;
+                            pb += v;
+                        }
+                    }
+                }
+            }
+        }
+        if (own) {
+#pragma unroll
+            for (int aa = 0; aa < MA; ++aa)
+                if (aa < A1) part[int64_t(aa) * a.J + j] = pw[aa];
+            part[int64_t(A1) * a.J + j] = pb;
+        }
+    }
+    if (tid < A1) part[int64_t(A1 + 1) * a.J + tid] = hb;
+}
+
+struct HeadsOut {
+    float* dwl; float* dwv; float* dbl; float* dbv; float* db_dense;
+    int J, A;
+};
+
+__global__ __launch_bounds__(1024) void heads_reduce_kernel(const float* __restrict__ partial, int nparts,
+                                                            int pstride, HeadsOut o) {
+    const int A1 = o.A + 1;
+    const int64_t nw = int64_t(A1) * o.J, nd = nw + o.J, nt = nd + A1;
+    sum_partials_x4(partial, nparts, pstride, [&](int e0, float4 v) {
+        const float t[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int64_t e = e0 + u;
+            if (e < nw) {
+                const int aa = int(e / o.J), j = int(e - int64_t(aa) * o.J);
+                if (aa < o.A) o.dwl[int64_t(j) * o.A + aa] = t[u];
+                else o.dwv[j] = t[u];
+            } else if (e < nd) {
+                o.db_dense[e - nw] = t[u];
+            } else if (e < nt) {
+                const int aa = int(e - nd);
+                if (aa < o.A) o.dbl[aa] = t[u];
+                else o.dbv[0] = t[u];
+            }
+        }
+    });
+}
+
+int heads_pstride(int J, int A) {
+    const int64_t ps = int64_t(A + 2) * J + (A + 1);
+    return int((ps + 63) / 64 * 64);
+}
+
+int heads_bwd_blocks(int64_t n, int J, int A) {
+    const int64_t groups = (n + kHR - 1) / kHR;
+    const int64_t cap = std::max<int64_t>(1, int64_t(kHeadsPartialCap / size_t(heads_pstride(J, A))));
+    return int(std::max<int64_t>(1, std::min<int64_t>({groups, cap, 4096})));
+}
+
+std::string heads_shape(const HeadsArgs& a) {
+    return std::to_string(a.n) + "x" + std::to_string(a.J) + "x" + std::to_string(a.A);
+}
+
+}  // namespace
+
+size_t heads_bwd_partial_floats(int64_t n, int J, int A) {
+    return size_t(heads_bwd_blocks(n, J, A)) * size_t(heads_pstride(J, A));
+}
+
+namespace {
+// Column count of the staged weights: A + 1 when the action count has a compile-time
+// variant (18: the Atari action set; 6), else padded to 20 or 68.
+int heads_ma(int A) { return A == 18 || A == 6 ? A + 1 : (A + 1 <= 20 ? 20 : 68); }
+}  // namespace
+
+hipError_t heads_fwd(int prec, const HeadsArgs& a, float* logits, float* value, hipStream_t s) {
+    if (a.n <= 0) return hipSuccess;
+    if (a.A < 1 || a.A > 64 || a.J < 1) return hipErrorInvalidValue;
+    const int MA = heads_ma(a.A);
+    const size_t lds = std::max(size_t(kHJ) * (MA | 1), size_t(kHJ) * MA) * sizeof(float);
+    const dim3 grid(unsigned((a.n + kHR - 1) / kHR));
+    ProfScope ps(s, [&] { return cb_key("heads_fwd", prec, heads_shape(a)); });
+#define CB_HF(T, AC, MA) hipLaunchKernelGGL((heads_fwd_kernel<T, AC, MA>), grid, dim3(kHJ), lds, s, a, logits, value)
+#define CB_HF_ALL(T)                                 \
+    if (a.A == 18) CB_HF(T, 18, 19);                 \
+    else if (a.A == 6) CB_HF(T, 6, 7);               \
+    else if (a.A + 1 <= 20) CB_HF(T, 0, 20);         \
+    else CB_HF(T, 0, 68);
+    if (prec == BF16) {
+        CB_HF_ALL(uint16_t)
+    } else {
+        CB_HF_ALL(float)
+    }
+#undef CB_HF_ALL
+#undef CB_HF
+    return hipGetLastError();
+}
+
+hipError_t heads_bwd(int prec, const HeadsArgs& a, const float* dlogits, const float* dvalue, void* dh,
+                     float* dwl, float* dbl, float* dwv, float* dbv, float* db_dense, float* partial,
+                     size_t partial_floats, hipStream_t s) {
+    if (a.A < 1 || a.A > 64 || a.J < 1) return hipErrorInvalidValue;
+    const int pstride = heads_pstride(a.J, a.A);
+    const int nblk = heads_bwd_blocks(a.n > 0 ? a.n : 1, a.J, a.A);
+    if (size_t(nblk) * size_t(pstride) > partial_floats) return hipErrorInvalidValue;
+    const int MA = heads_ma(a.A);
+    const size_t lds = (size_t(kHJ) * (MA | 1) + size_t(MA) * kHR) * sizeof(float);
+    {
+        ProfScope ps(s, [&] { return cb_key("heads_bwd", prec, heads_shape(a)); });
+#define CB_HB(T, AC, MA) \
+        hipLaunchKernelGGL((heads_bwd_kernel<T, AC, MA>), dim3(unsigned(nblk)), dim3(kHJ), lds, s, a, dlogits, dvalue, \
+                           static_cast<T*>(dh), partial, pstride)
+#define CB_HB_ALL(T)                                 \
+        if (a.A == 18) CB_HB(T, 18, 19);             \
+        else if (a.A == 6) CB_HB(T, 6, 7);           \
+        else if (a.A + 1 <= 20) CB_HB(T, 0, 20);     \
+        else CB_HB(T, 0, 68);
+        if (prec == BF16) {
+            CB_HB_ALL(uint16_t)
+        } else {
+            CB_HB_ALL(float)
+        }
+#undef CB_HB_ALL
+#undef CB_HB
+    }
+    HeadsOut o{dwl, dwv, dbl, dbv, db_dense, a.J, a.A};
+    {
+        ProfScope ps(s, [&] { return cb_key("heads_reduce", prec, heads_shape(a)); });
+        hipLaunchKernelGGL(heads_reduce_kernel, dim3(unsigned((pstride + 63) / 64)), dim3(1024), 0, s, partial, nblk,
+                           pstride, o);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace cb

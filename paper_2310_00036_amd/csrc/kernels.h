@@ -156,14 +156,24 @@ hipError_t gemm(int prec, const GemmArgs& a, hipStream_t s);
 // y[i] = bf16(x[i]) (round to nearest even); y 4-byte aligned.
 hipError_t cast_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t s);
 
-// ---- small helpers
-hipError_t colsum(int prec_storage, const void* x, int64_t rows, int cols, int64_t ld,
-                  float* out, float* partial, hipStream_t s);   // out[c] = sum_r x[r*ld + c]
-size_t colsum_partial_floats(int cols);
-hipError_t pack_heads_w(const float* wl, const float* wv, int hidden, int A, float* out,
-                        hipStream_t s);   // out [A+1][hidden]
-hipError_t pack_dz(int prec, const float* dlogits, const float* dvalue, int64_t n, int A,
-                   void* out, hipStream_t s);   // out [n][A+1] storage type
+// ---- policy-logit and value heads (float32 FMAs; h and dh in the storage type)
+struct HeadsArgs {
+    const void* h;      // [n][J] dense-layer output (after relu), storage type
+    const float* wl;    // [J][A] logit weights
+    const float* bl;    // [A]
+    const float* wv;    // [J] value weights
+    const float* bv;    // [1]
+    int64_t n; int J, A;
+};
+// logits [n][A] and value [n], float32.
+hipError_t heads_fwd(int prec, const HeadsArgs& a, float* logits, float* value, hipStream_t s);
+// dh [n][J] (storage type) = (dz W^T) * (h > 0) with dz = [dlogits | dvalue]; the head weight
+// and bias gradients and the dense bias gradient (column sums of dh as stored) are
+// overwritten. `partial` holds heads_bwd_partial_floats(n, J, A) floats.
+hipError_t heads_bwd(int prec, const HeadsArgs& a, const float* dlogits, const float* dvalue, void* dh,
+                     float* dwl, float* dbl, float* dwv, float* dbv, float* db_dense, float* partial,
+                     size_t partial_floats, hipStream_t s);
+size_t heads_bwd_partial_floats(int64_t n, int J, int A);
 
 // ---- loss, targets, optimiser
 hipError_t gae(int T, int E, const float* r, const float* v, const uint8_t* d, const float* nv,

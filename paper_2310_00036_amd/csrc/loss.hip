@@ -68,23 +68,30 @@ struct PpoRow {
     int a;
 };
 
-CB_DEV PpoRow ppo_row(const float* zr, int64_t src, int A, const int32_t* act,
-                      const float* old_logp, const float* adv, int norm_adv, float clip,
-                      float mean, float std) {
+// One row's terms from its logits and the row's scalars (action, behaviour log-prob, raw
+// advantage).
+CB_DEV PpoRow ppo_row_v(const float* zr, int A, int a, float old_logp, float adv, int norm_adv, float clip,
+                        float mean, float std) {
     PpoRow r;
     r.s = row_log_softmax(zr, A);
     r.H = r.s.H;
-    r.a = act[src];
-    r.A_hat = adv[src];
+    r.a = a;
+    r.A_hat = adv;
     if (norm_adv) r.A_hat = (r.A_hat - mean) / (std + 1e-8f);
     // an action outside [0, A) poisons the row with NaN instead of reading past the row
     const float la = (r.a >= 0 && r.a < A) ? r.s.l(zr[r.a]) : __builtin_nanf("");
-    r.ratio = expf(la - old_logp[src]);
+    r.ratio = expf(la - old_logp);
     const float pg1 = -r.A_hat * r.ratio;
     const float pg2 = -r.A_hat * fminf(fmaxf(r.ratio, 1.f - clip), 1.f + clip);
     r.pg = fmaxf(pg1, pg2);
     r.kappa = pg2 > pg1 ? 0.f : 1.f;   // clipped branch strictly larger: no ratio gradient
     return r;
+}
+
+CB_DEV PpoRow ppo_row(const float* zr, int64_t src, int A, const int32_t* act,
+                      const float* old_logp, const float* adv, int norm_adv, float clip,
+                      float mean, float std) {
+    return ppo_row_v(zr, A, act[src], old_logp[src], adv[src], norm_adv, clip, mean, std);
 }
 
 // ---- (2) per-row PPO gradients
@@ -223,11 +230,96 @@ CB_DEV void fused_block_sum(double (&v)[K], double* sh) {
 
 // Rows are processed in chunks: the chunk's logits are read into LDS with coalesced loads,
 // each thread works on one row there (writing its logit gradients in place), and the chunk's
-// gradients leave with coalesced stores.
-CB_DEV int fused_chunk_rows(int A) { return (kFusedThreads * 64 / A) < kFusedThreads ? (kFusedThreads * 64 / A) : kFusedThreads; }
+// gradients leave with coalesced stores. With the action count fixed at compile time, the
+// next chunk's logits and row scalars are loaded into registers while the current chunk is
+// being worked on (and the first chunk's during the advantage statistics), so each chunk
+// costs its arithmetic rather than a chain of load latencies.
+CB_DEV constexpr int fused_chunk_rows(int A) { return (kFusedThreads * 64 / A) < kFusedThreads ? (kFusedThreads * 64 / A) : kFusedThreads; }
+
+// Thread t's share of a chunk's nr * A contiguous logits: elements t, t + 512, ...
+template <int LPT>
+struct ChunkRegs {
+    float v[LPT];
+    CB_DEV void load(const float* __restrict__ z, int64_t c0, int nr, int A) {
+        const int n = nr * A;
+        const float* p = z + c0 * A;
+#pragma unroll
+        for (int u = 0; u < LPT; ++u) {   // unconditional loads (clamped) keep all in flight
+            const int e = u * kFusedThreads + int(threadIdx.x);
+            v[u] = p[e < n ? e : n - 1];
+        }
+    }
+    CB_DEV void store(float* zs, int nr, int A) const {
+        const int n = nr * A;
+#pragma unroll
+        for (int u = 0; u < LPT; ++u) {
+            const int e = u * kFusedThreads + int(threadIdx.x);
+            if (e < n) zs[e] = v[u];
+        }
+    }
+};
+
+template <int AC>
+constexpr int fused_lpt() { return AC > 0 ? (fused_chunk_rows(AC) * AC + kFusedThreads - 1) / kFusedThreads : 1; }
+
+struct PpoScal {
+    int a;
+    float olp, adv, ret, val;
+};
+
+// Row i's source row (rows past m read row m - 1: unconditional loads stay in flight; such
+// rows are never used). Issued before a chunk's logits so that waiting for it does not wait
+// for them (loads complete in order).
+template <bool ROWS>
+CB_DEV int64_t ppo_src(int64_t i, int64_t m, const int32_t* __restrict__ rows) {
+    const int64_t ic = i < m ? i : m - 1;
+    if constexpr (ROWS) return rows[ic];
+    else return ic;
+}
+
+CB_DEV PpoScal ppo_scal(int64_t i, int64_t m, int64_t src, const int32_t* __restrict__ act,
+                        const float* __restrict__ old_logp, const float* __restrict__ adv,
+                        const float* __restrict__ ret, const float* __restrict__ val) {
+    const int64_t ic = i < m ? i : m - 1;
+    return PpoScal{act[src], old_logp[src], adv[src], ret[src], val[ic]};
+}
+
+// This thread's float64 sums of the minibatch advantages and their squares (rows tid,
+// tid + 512, ...), four rows' loads in flight. The block sum and the mean / population std
+// follow in adv_mean_std.
+template <bool ROWS>
+CB_DEV void adv_sums(int64_t m, const float* __restrict__ adv, const int32_t* __restrict__ rows, double (&ms)[2]) {
+    ms[0] = 0.0;
+    ms[1] = 0.0;
+    for (int64_t i0 = threadIdx.x; i0 < m; i0 += 4 * kFusedThreads) {
+        int64_t src[4];
+        float av[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            src[u] = ppo_src<ROWS>(i0 + u * kFusedThreads, m, rows);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) av[u] = adv[src[u]];
+        __builtin_amdgcn_sched_barrier(0);   // all four gathers in flight before the first use
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {   // rows past m add zero
+            const double a = i0 + u * kFusedThreads < m ? double(av[u]) : 0.0;
+            ms[0] += a;
+            ms[1] += a * a;
+        }
+    }
+}
+
+CB_DEV void adv_mean_std(int64_t m, double (&ms)[2], double* sh, float& mean, float& std) {
+    fused_block_sum<2>(ms, sh);
+    const double dmean = ms[0] / double(m), dvar = ms[1] / double(m) - dmean * dmean;
+    mean = float(dmean);
+    std = float(sqrt(dvar > 0.0 ? dvar : 0.0));
+}
 
 // AC > 0 fixes the action count at compile time (the row loops unroll); 0 reads it from A_.
-template <int AC>
+// ROWS: the rows are gathered through `rows` (else rows is NULL and row i is row i).
+template <int AC, bool ROWS>
 __global__ __launch_bounds__(kFusedThreads) void ppo_fused_kernel(
     int64_t m, int A_, const float* __restrict__ z, const float* __restrict__ val,
     const int32_t* __restrict__ act, const float* __restrict__ old_logp,
@@ -238,36 +330,52 @@ __global__ __launch_bounds__(kFusedThreads) void ppo_fused_kernel(
     __shared__ double sh[(kFusedThreads / 64) * 5];
     const int A = AC > 0 ? AC : A_;
     const int tid = threadIdx.x;
-    // advantage mean and population std over the minibatch
-    double ms[2] = {0.0, 0.0};
-    for (int64_t i = tid; i < m; i += kFusedThreads) {
-        const double a = adv[rows ? rows[i] : i];
-        ms[0] += a;
-        ms[1] += a * a;
+    const int CR = fused_chunk_rows(A);
+    // the advantage sums' loads first (loads complete in order), then the first chunk's
+    // prefetch, which the block sum overlaps
+    double ms[2];
+    adv_sums<ROWS>(m, adv, rows, ms);
+    ChunkRegs<fused_lpt<AC>()> cz;
+    PpoScal nx{};
+    if constexpr (AC > 0) {
+        const int64_t src = ppo_src<ROWS>(tid, m, rows);
+        cz.load(z, 0, int(m < CR ? m : CR), A);
+        nx = ppo_scal(tid, m, src, act, old_logp, adv, ret, val);
     }
-    fused_block_sum<2>(ms, sh);
-    const double dmean = ms[0] / double(m), dvar = ms[1] / double(m) - dmean * dmean;
-    const float mean = float(dmean), std = float(sqrt(dvar > 0.0 ? dvar : 0.0));
+    float mean, std;
+    adv_mean_std(m, ms, sh, mean, std);
     // rows: gradients and loss terms
     const float inv_m = 1.f / float(m);
-    const int CR = fused_chunk_rows(A);
     double st[5] = {0, 0, 0, 0, 0};
     for (int64_t c0 = 0; c0 < m; c0 += CR) {
         const int nr = m - c0 < CR ? int(m - c0) : CR;
         __syncthreads();   // the previous chunk's gradients have left LDS
-        for (int e = tid; e < nr * A; e += kFusedThreads) zs[e] = z[c0 * A + e];
+        PpoScal cur;
+        if constexpr (AC > 0) {
+            cz.store(zs, nr, A);
+            cur = nx;
+            if (c0 + CR < m) {
+                const int64_t c1 = c0 + CR;
+                const int64_t src = ppo_src<ROWS>(c1 + tid, m, rows);
+                cz.load(z, c1, int(m - c1 < CR ? m - c1 : CR), A);
+                nx = ppo_scal(c1 + tid, m, src, act, old_logp, adv, ret, val);
+            }
+        } else {
+            for (int e = tid; e < nr * A; e += kFusedThreads) zs[e] = z[c0 * A + e];
+            cur = ppo_scal(c0 + tid, m, ppo_src<ROWS>(c0 + tid, m, rows), act, old_logp, adv, ret, val);
+        }
         __syncthreads();
         if (tid < nr) {
-            const int64_t i = c0 + tid, src = rows ? rows[i] : i;
+            const int64_t i = c0 + tid;
             float* zr = zs + tid * A;
-            const PpoRow r = ppo_row(zr, src, A, act, old_logp, adv, norm_adv, clip, mean, std);
+            const PpoRow r = ppo_row_v(zr, A, cur.a, cur.olp, cur.adv, norm_adv, clip, mean, std);
             const float coef = -r.kappa * r.A_hat * r.ratio;
             for (int j = 0; j < A; ++j) {
                 const float l = r.s.l(zr[j]);
                 const float p = expf(l);
                 zr[j] = (coef * ((j == r.a ? 1.f : 0.f) - p) + ent * p * (l + r.H)) * inv_m;
             }
-            const float vi = val[i], ri = ret[src];
+            const float vi = cur.val, ri = cur.ret;
             dv[i] = vf * (vi - ri) * inv_m;
             const double dvl = double(vi) - double(ri);
             st[0] += r.pg;
@@ -290,6 +398,17 @@ __global__ __launch_bounds__(kFusedThreads) void ppo_fused_kernel(
     }
 }
 
+struct ImpScal {
+    int a;
+    float adv, val, vs;
+};
+
+CB_DEV ImpScal imp_scal(int64_t i, int64_t m, const int32_t* __restrict__ act, const float* __restrict__ pgadv,
+                        const float* __restrict__ val, const float* __restrict__ vs) {
+    const int64_t ic = i < m ? i : m - 1;
+    return ImpScal{act[ic], pgadv[ic], val[ic], vs[ic]};
+}
+
 template <int AC>
 __global__ __launch_bounds__(kFusedThreads) void impala_fused_kernel(
     int64_t m, int A_, const float* __restrict__ z, const float* __restrict__ val,
@@ -302,19 +421,37 @@ __global__ __launch_bounds__(kFusedThreads) void impala_fused_kernel(
     const int tid = threadIdx.x;
     const float inv_m = 1.f / float(m);
     const int CR = fused_chunk_rows(A);
+    ChunkRegs<fused_lpt<AC>()> cz;
+    ImpScal nx{};
+    if constexpr (AC > 0) {
+        cz.load(z, 0, int(m < CR ? m : CR), A);
+        nx = imp_scal(tid, m, act, pgadv, val, vs);
+    }
     double st[5] = {0, 0, 0, 0, 0};
     for (int64_t c0 = 0; c0 < m; c0 += CR) {
         const int nr = m - c0 < CR ? int(m - c0) : CR;
         __syncthreads();
-        for (int e = tid; e < nr * A; e += kFusedThreads) zs[e] = z[c0 * A + e];
+        ImpScal cur;
+        if constexpr (AC > 0) {
+            cz.store(zs, nr, A);
+            cur = nx;
+            if (c0 + CR < m) {
+                const int64_t c1 = c0 + CR;
+                cz.load(z, c1, int(m - c1 < CR ? m - c1 : CR), A);
+                nx = imp_scal(c1 + tid, m, act, pgadv, val, vs);
+            }
+        } else {
+            for (int e = tid; e < nr * A; e += kFusedThreads) zs[e] = z[c0 * A + e];
+            cur = imp_scal(c0 + tid, m, act, pgadv, val, vs);
+        }
         __syncthreads();
         if (tid < nr) {
             const int64_t i = c0 + tid;
             float* zr = zs + tid * A;
             const RowLsm rs = row_log_softmax(zr, A);
             const float H = rs.H;
-            const int a = act[i];
-            const float adv = pgadv[i];
+            const int a = cur.a;
+            const float adv = cur.adv;
             const bool a_ok = a >= 0 && a < A;
             const double la = a_ok ? double(rs.l(zr[a])) : double(__builtin_nanf(""));
             for (int j = 0; j < A; ++j) {
@@ -323,7 +460,7 @@ __global__ __launch_bounds__(kFusedThreads) void impala_fused_kernel(
                 zr[j] = a_ok ? (-pgc * adv * ((j == a ? 1.f : 0.f) - p) + ent * p * (l + H)) * inv_m
                              : __builtin_nanf("");
             }
-            const float vi = val[i], vsi = vs[i];
+            const float vi = cur.val, vsi = cur.vs;
             dv[i] = vf * (vi - vsi) * inv_m;
             const double dvl = double(vi) - double(vsi);
             st[0] += -double(adv) * la;
@@ -359,7 +496,9 @@ hipError_t ppo_loss(int64_t m, int A, const float* z, const float* v, const int3
     const int nb = int((m + kLossRows - 1) / kLossRows);
     ProfScope ps(s, [&] { return "ppo_loss/" + cb_dims(int(m), A); });
     if (m <= kFusedRows) {
-        auto k = A == 18 ? ppo_fused_kernel<18> : (A == 6 ? ppo_fused_kernel<6> : ppo_fused_kernel<0>);
+        auto k = rows ? (A == 18 ? ppo_fused_kernel<18, true> : (A == 6 ? ppo_fused_kernel<6, true> : ppo_fused_kernel<0, true>))
+                      : (A == 18 ? ppo_fused_kernel<18, false>
+                                 : (A == 6 ? ppo_fused_kernel<6, false> : ppo_fused_kernel<0, false>));
         hipLaunchKernelGGL(k, dim3(1), dim3(kFusedThreads), fused_lds(A), s, m, A, z, v, act, old_logp, adv, ret, rows,
                            norm_adv, clip, vf, ent, dz, dv, stats);
         return hipGetLastError();

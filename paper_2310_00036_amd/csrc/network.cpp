@@ -92,24 +92,20 @@ NetPlan make_plan(const impala_net_t& net, int prec, int64_t cap, int training) 
         for (int k = 0; k < 2; ++k) p.t[s][k] = take(size_t(cap * pool_el) * p.es);
     }
     p.h = take(size_t(cap) * p.hidden * p.es);
-    p.whp = take(size_t(p.A + 1) * p.hidden * sizeof(float));
     p.wdb = take(prec == BF16 ? size_t(p.flat) * p.hidden * 2 : 0);
     // split-K / column-sum / weight-gradient partials, shared by the launches in turn. The
     // GEMM launcher never splits beyond this capacity, so the sizing only affects speed.
     size_t sc = 0;
     for (int64_t nn = cap; nn >= 1; nn = nn > 64 ? nn / 2 : 0) {
         sc = std::max(sc, gemm_partial_floats(p.hidden, int(nn), p.flat));
-        sc = std::max(sc, gemm_partial_floats(p.A + 1, int(nn), p.hidden));
         if (training) {
-            sc = std::max(sc, gemm_partial_floats(p.A + 1, p.hidden, int(nn)));
-            sc = std::max(sc, gemm_partial_floats(p.hidden, int(nn), p.A + 1));
+            sc = std::max(sc, heads_bwd_partial_floats(nn, p.hidden, p.A));
             sc = std::max(sc, gemm_partial_floats(p.hidden, p.flat, int(nn)));
             sc = std::max(sc, gemm_partial_floats(p.flat, int(nn), p.hidden));
         }
     }
     if (training) {
         for (int k = 0; k < 3; ++k) p.g[k] = take(size_t(cap * maxact) * p.es);
-        p.dz = take(size_t(cap) * (p.A + 1) * p.es);
         for (int s = 0; s < 3; ++s) {
             sc = std::max(sc, wgrad_partial_floats(prec, p.C[s], p.C[s + 1], p.H[s], p.W[s]));
             sc = std::max(sc, wgrad_partial_floats(prec, p.C[s + 1], p.C[s + 1], p.H[s + 1], p.W[s + 1]));
@@ -119,7 +115,6 @@ NetPlan make_plan(const impala_net_t& net, int prec, int64_t cap, int training) 
                 sc = std::max(sc, conv3x3_bwd_partial_floats(p.C[s + 1], p.C[s + 1]));
             }
         }
-        sc = std::max(sc, colsum_partial_floats(std::max(p.hidden, p.A + 1)));
     }
     p.scratch_bytes = sc * sizeof(float);
     p.scratch = take(p.scratch_bytes);
@@ -198,17 +193,9 @@ hipError_t run_forward(const NetPlan& p, const float* params, const uint8_t* obs
     d.partial = reinterpret_cast<float*>(ws + p.scratch); d.partial_floats = p.scratch_bytes / sizeof(float);
     CB_TRY(gemm(p.prec, d, s));
     // heads: logits[i][a] = bl[a] + sum_j h[i][j] Wl[j][a]; value[i] = bv + sum_j h[i][j] Wv[j]
-    float* whp = reinterpret_cast<float*>(ws + p.whp);
-    CB_TRY(pack_heads_w(params + po.logits_w, params + po.value_w, p.hidden, p.A, whp, s));
-    GemmArgs hd{};
-    hd.a = whp; hd.a_f32 = 1; hd.a_kcontig = 1; hd.lda = p.hidden;
-    hd.b = ws + p.h; hd.b_f32 = p.prec == FP32; hd.b_kcontig = 1; hd.ldb = p.hidden;
-    hd.M = p.A + 1; hd.N = int(n); hd.K = p.hidden; hd.alpha = 1.f;
-    hd.bias1 = params + po.logits_b; hd.bias2 = params + po.value_b;
-    hd.out1 = logits; hd.ld1 = p.A; hd.out1_f32 = 1;
-    hd.out2 = value; hd.ld2 = 1; hd.out2_f32 = 1; hd.msplit = p.A;
-    hd.partial = reinterpret_cast<float*>(ws + p.scratch); hd.partial_floats = p.scratch_bytes / sizeof(float);
-    CB_TRY(gemm(p.prec, hd, s));
+    HeadsArgs hd{ws + p.h, params + po.logits_w, params + po.logits_b, params + po.value_w,
+                 params + po.value_b, n, p.hidden, p.A};
+    CB_TRY(heads_fwd(p.prec, hd, logits, value, s));
     return hipSuccess;
 }
 
@@ -217,36 +204,19 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
                         const float* dvalue, float* grads, hipStream_t s) {
     const ParamOffsets& po = p.po;
     if (n <= 0) return fill_zero(grads, po.total, s);
-    const int es = p.es, A = p.A;
+    const int A = p.A;
     const int st_f32 = p.prec == FP32;
     float* scratch = reinterpret_cast<float*>(ws + p.scratch);
-    char* dz = ws + p.dz;
     char* G[3] = {ws + p.g[0], ws + p.g[1], ws + p.g[2]};
 
-    CB_TRY(pack_dz(p.prec, dlogits, dvalue, n, A, dz, s));
-    // head weight gradients: dWl[j][a] = sum_i h[i][j] dz[i][a] (value column a == A)
-    GemmArgs hw{};
-    hw.a = dz; hw.a_f32 = st_f32; hw.a_kcontig = 0; hw.lda = A + 1;
-    hw.b = ws + p.h; hw.b_f32 = st_f32; hw.b_kcontig = 0; hw.ldb = p.hidden;
-    hw.M = A + 1; hw.N = p.hidden; hw.K = int(n); hw.alpha = 1.f;
-    hw.out1 = grads + po.logits_w; hw.ld1 = A; hw.out1_f32 = 1;
-    hw.out2 = grads + po.value_w; hw.ld2 = 1; hw.out2_f32 = 1; hw.msplit = A;
-    hw.partial = scratch; hw.partial_floats = p.scratch_bytes / sizeof(float);
-    CB_TRY(gemm(p.prec, hw, s));
-    CB_TRY(colsum(p.prec, dz, n, A, A + 1, grads + po.logits_b, scratch, s));
-    CB_TRY(colsum(p.prec, dz + size_t(A) * es, n, 1, A + 1, grads + po.value_b, scratch, s));
-    // dh = (dz Wh^T) * (h > 0)
-    float* whp = reinterpret_cast<float*>(ws + p.whp);
-    CB_TRY(pack_heads_w(params + po.logits_w, params + po.value_w, p.hidden, A, whp, s));
-    GemmArgs hg{};
-    hg.a = whp; hg.a_f32 = 1; hg.a_kcontig = 0; hg.lda = p.hidden;
-    hg.b = dz; hg.b_f32 = st_f32; hg.b_kcontig = 1; hg.ldb = A + 1;
-    hg.M = p.hidden; hg.N = int(n); hg.K = A + 1; hg.alpha = 1.f;
-    hg.mask = ws + p.h; hg.ldmask = p.hidden;
-    hg.out1 = G[0]; hg.ld1 = p.hidden; hg.out1_f32 = st_f32; hg.msplit = p.hidden;
-    hg.partial = scratch; hg.partial_floats = p.scratch_bytes / sizeof(float);
-    CB_TRY(gemm(p.prec, hg, s));
-    // dense weight gradient: dWd[k][j] = sum_i relu(x)[i][k] dh[i][j]; bias: column sums of dh
+    // heads: dh = (dz Wh^T) * (h > 0), the head weight / bias gradients and the dense bias
+    // gradient (column sums of dh) from one pass over h
+    HeadsArgs hd{ws + p.h, params + po.logits_w, params + po.logits_b, params + po.value_w,
+                 params + po.value_b, n, p.hidden, A};
+    CB_TRY(heads_bwd(p.prec, hd, dlogits, dvalue, G[0], grads + po.logits_w, grads + po.logits_b,
+                     grads + po.value_w, grads + po.value_b, grads + po.dense_b, scratch,
+                     p.scratch_bytes / sizeof(float), s));
+    // dense weight gradient: dWd[k][j] = sum_i relu(x)[i][k] dh[i][j]
     GemmArgs dw{};
     dw.a = G[0]; dw.a_f32 = st_f32; dw.a_kcontig = 0; dw.lda = p.hidden;
     dw.b = ws + p.x[2][2]; dw.b_f32 = st_f32; dw.b_kcontig = 0; dw.ldb = p.flat; dw.b_relu = 1;
@@ -254,11 +224,9 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
     dw.out1 = grads + po.dense_w; dw.ld1 = p.hidden; dw.out1_f32 = 1; dw.msplit = p.hidden;
     dw.partial = scratch; dw.partial_floats = p.scratch_bytes / sizeof(float);
     CB_TRY(gemm(p.prec, dw, s));
-    CB_TRY(colsum(p.prec, G[0], n, p.hidden, p.hidden, grads + po.dense_b, scratch, s));
     // dense input gradient: dx[i][k] = (sum_j Wd[k][j] dh[i][j]) * (x[i][k] > 0)
+    // bf16: the forward pass left the bf16 copy of the same dense weights in the workspace
     const bool wbf = p.prec == BF16;
-    if (wbf) CB_TRY(cast_bf16(params + po.dense_w, reinterpret_cast<uint16_t*>(ws + p.wdb),
-                              int64_t(p.flat) * p.hidden, s));
     GemmArgs dg{};
     dg.a = wbf ? static_cast<const void*>(ws + p.wdb) : static_cast<const void*>(params + po.dense_w);
     dg.a_f32 = !wbf; dg.a_kcontig = 1; dg.lda = p.hidden;

@@ -29,9 +29,8 @@ struct NetPlan {
     // workspace byte offsets (each region 256-byte aligned)
     size_t c[3], idx[3], x[3][3], t[3][2], h;
     size_t g[3];            // gradient ping-pong buffers (backward)
-    size_t dz, whp;         // packed head gradient [cap][A+1], packed head weights [A+1][hidden]
     size_t wdb;             // bf16 copy of the dense weights [flat][hidden] (bf16 mode)
-    size_t scratch;         // split-K / wgrad / column-sum partials
+    size_t scratch;         // split-K / weight-gradient / head-gradient partials
     size_t scratch_bytes;
     size_t total;
 };

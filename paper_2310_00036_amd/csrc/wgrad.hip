@@ -498,15 +498,21 @@ __global__ __launch_bounds__(1024) void wgrad_tr_reduce_kernel(const float* __re
                                                                int nparts, float* dw, float* db,
                                                                float scale) {
     using D = WgTr<CIN, COUT, MODE>;
-    sum_partials16(partial, nparts, D::PSTRIDE, [&](int e, float tot) {
-        const int tile = e >> 8, row = (e >> 4) & 15, col = e & 15;
+    static_assert(D::PSTRIDE % 64 == 0, "whole 64-entry blocks");
+    sum_partials_x4(partial, nparts, D::PSTRIDE, [&](int e0, float4 v) {
+        const float tv[4] = {v.x, v.y, v.z, v.w};
+        const int tile = e0 >> 8, row = (e0 >> 4) & 15;
         const int mt = tile / D::NBB, nb = tile % D::NBB, co = mt * 16 + row;
-        if (nb == D::NB) {
-            if (col == 0) db[co] = tot;
-        } else {
-            const int tap = D::U8 ? nb * 4 + col / 4 : nb / (CIN / 16 > 0 ? CIN / 16 : 1);
-            const int ci = D::U8 ? col % 4 : (nb % (CIN / 16 > 0 ? CIN / 16 : 1)) * 16 + col;
-            if (tap < 9) dw[(tap * CIN + ci) * COUT + co] = tot * scale;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int col = (e0 & 15) + u;
+            if (nb == D::NB) {
+                if (col == 0) db[co] = tv[u];
+            } else {
+                const int tap = D::U8 ? nb * 4 + col / 4 : nb / (CIN / 16 > 0 ? CIN / 16 : 1);
+                const int ci = D::U8 ? col % 4 : (nb % (CIN / 16 > 0 ? CIN / 16 : 1)) * 16 + col;
+                if (tap < 9) dw[(tap * CIN + ci) * COUT + co] = tv[u] * scale;
+            }
         }
     });
 }
@@ -647,7 +653,7 @@ hipError_t wg_tr_launch(const WgradArgs& a, hipStream_t s) {
     }
     {
         ProfScope ps(s, [&] { return cb_key("wgrad_reduce", 0, shape); });
-        hipLaunchKernelGGL((wgrad_tr_reduce_kernel<CIN, COUT, MODE>), dim3((D::PSTRIDE + 15) / 16), dim3(1024),
+        hipLaunchKernelGGL((wgrad_tr_reduce_kernel<CIN, COUT, MODE>), dim3(D::PSTRIDE / 64), dim3(1024),
                            0, s, a.partial, parts, a.dw, a.db, a.scale);
     }
     return hipGetLastError();
@@ -683,7 +689,7 @@ hipError_t wgrad_reduce_tr(int cin, int cout, const float* partial, int nparts, 
 #define CB_RT(CI, CO, MD)                                                                              \
     if (cin == CI && cout == CO) {                                                                     \
         hipLaunchKernelGGL((wgrad_tr_reduce_kernel<CI, CO, MD>),                                       \
-                           dim3((WgTr<CI, CO, MD>::PSTRIDE + 15) / 16), dim3(1024), 0, s, partial,     \
+                           dim3(WgTr<CI, CO, MD>::PSTRIDE / 64), dim3(1024), 0, s, partial,            \
                            nparts, dw, db, scale);                                                     \
         return hipGetLastError();                                                                      \
     }
