@@ -53,11 +53,20 @@ def run_layer(P, key, n, steps):
     the minibatch's shape; prints the average launch time."""
     import torch
     parts = key.split("/")
-    fam, prec = parts[0], (P.PREC_BF16 if parts[1] == "bf16" else P.PREC_FP32)
+    fam, prec = parts[0], (P.PREC_BF16 if parts[1] != "fp32" else P.PREC_FP32)
     dt = torch.bfloat16 if prec == P.PREC_BF16 else torch.float32
     g = torch.Generator(device="cuda").manual_seed(7)
     act = lambda h, w, c: (torch.randn(n, h, w, c, device="cuda", generator=g) * 0.5).to(dt)  # noqa: E731
-    if fam in ("pool_fwd", "pool_bwd"):
+    if fam == "ppo_loss":   # key: ppo_loss/<rows>x<actions>
+        m, A = map(int, parts[1].split("x"))
+        z = torch.randn(m, A, device="cuda", generator=g)
+        v, ret, adv = (torch.randn(m, device="cuda", generator=g) for _ in range(3))
+        a = torch.randint(0, A, (m,), dtype=torch.int32, device="cuda", generator=g)
+        olp = torch.log_softmax(z, 1).gather(1, a.long()[:, None])[:, 0] + 0.1 * torch.randn(m, device="cuda", generator=g)
+        dz, dv = torch.empty_like(z), torch.empty_like(v)
+        st = torch.empty(8, device="cuda")
+        fn = lambda: P.ppo_loss_grad(m, A, z, v, a, olp, adv, ret, 1, 0.1, 0.5, 0.01, dz, dv, st)  # noqa: E731
+    elif fam in ("pool_fwd", "pool_bwd"):
         c = int(parts[2])
         h, w = map(int, parts[3].split("x"))
         oh, ow = (h + 1) // 2, (w + 1) // 2
@@ -241,7 +250,16 @@ def kernel_work(key, n, prec):
         else:
             b = px * (ci * xb + co * es * (1 + ("mask" in flags) + ("add" in flags)))
         return "hbm", float(b), "B", flop
-    if fam in ("pool_fwd", "pool_bwd"):
+    if fam == "ppo_loss":   # key: ppo_loss/<rows>x<actions>
+        m, A = map(int, parts[1].split("x"))
+        z = torch.randn(m, A, device="cuda", generator=g)
+        v, ret, adv = (torch.randn(m, device="cuda", generator=g) for _ in range(3))
+        a = torch.randint(0, A, (m,), dtype=torch.int32, device="cuda", generator=g)
+        olp = torch.log_softmax(z, 1).gather(1, a.long()[:, None])[:, 0] + 0.1 * torch.randn(m, device="cuda", generator=g)
+        dz, dv = torch.empty_like(z), torch.empty_like(v)
+        st = torch.empty(8, device="cuda")
+        fn = lambda: P.ppo_loss_grad(m, A, z, v, a, olp, adv, ret, 1, 0.1, 0.5, 0.01, dz, dv, st)  # noqa: E731
+    elif fam in ("pool_fwd", "pool_bwd"):
         c = int(parts[2])
         h, w = map(int, parts[3].split("x"))
         oh, ow = (h + 1) // 2, (w + 1) // 2

@@ -170,7 +170,21 @@ impala_status_t adam_step(int64_t n_params, float* params, const float* grads, f
                           float max_grad_norm, float* stats, void* ws, size_t ws_bytes,
                           hipStream_t stream);
 
+/* Global-norm clip then RMSprop over the flat buffers (Algorithm 1: clip the gradient norm,
+ * step the optimiser; Appendix B's IMPALA table: RMSprop with epsilon 0.01, decay 0.99):
+ *   g as adam_step's clip;  nu <- decay nu + (1 - decay) g^2;  p <- p - lr g / sqrt(nu + eps).
+ * The paper does not place epsilon. Reading: inside the square root, with nu starting at zero,
+ * the convention of optax's RMSprop (the paper's learner is written in JAX).
+ * params and nu are updated in place (nu zero before the first step); grads is read only.
+ * stats (device, float [2] or NULL) and ws (rmsprop_workspace_bytes()) as adam_step.
+ * EINVAL for n_params < 0, decay outside [0, 1) or eps < 0. */
+size_t rmsprop_workspace_bytes(int64_t n_params);
+impala_status_t rmsprop_step(int64_t n_params, float* params, const float* grads, float* nu,
+                             float lr, float decay, float eps, float max_grad_norm, float* stats,
+                             void* ws, size_t ws_bytes, hipStream_t stream);
+
 typedef enum { LEARNER_PPO = 0, LEARNER_IMPALA = 1 } learner_algo_t;
+typedef enum { LEARNER_OPT_ADAM = 0, LEARNER_OPT_RMSPROP = 1 } learner_opt_t;
 
 /* One learning phase's hyperparameters (Appendix A nomenclature; Appendix B values). */
 typedef struct learner_cfg {
@@ -188,6 +202,9 @@ typedef struct learner_cfg {
     float rho_bar, c_bar, pg_rho_bar; /* IMPALA importance-weight clips */
     float lr, beta1, beta2, adam_eps;
     float max_grad_norm;      /* omega; <= 0 disables clipping */
+    int32_t optimizer;        /* learner_opt_t: Adam (Appendix B's PPO table) or RMSprop (its
+                                 IMPALA table) */
+    float rms_decay, rms_eps; /* RMSprop (Appendix B: 0.99, 0.01) */
 } learner_cfg_t;
 
 /* The rollout one learning phase consumes (Algorithm 1's D plus the bootstrap state). */
@@ -207,10 +224,11 @@ typedef struct rollout {
 size_t learner_workspace_bytes(const impala_net_t* net, const learner_cfg_t* cfg);
 
 /* One learning phase. PPO: GAE once, then for epoch j and minibatch k the rows
- * perm[j*T*E + k*m .. +m]: forward, loss, backward, clip, Adam (step incremented per update).
- * IMPALA: forward over (T+1)*E frames, target log-probs, V-trace, loss over the T*E rows,
- * backward (bootstrap rows get no gradient), clip, Adam.
- * params, m, v: float [param_count], updated in place. step: HOST int32, 1-based count of
+ * perm[j*T*E + k*m .. +m]: forward, loss, backward, clip, optimiser step (step incremented
+ * per update). IMPALA: forward over (T+1)*E frames, target log-probs, V-trace, loss over the
+ * T*E rows, backward (bootstrap rows get no gradient), clip, optimiser step.
+ * params, m, v: float [param_count], updated in place (RMSprop: v holds its nu, m is unused and
+ * may be NULL). step: HOST int32, 1-based count of
  * updates done so far (incremented). perm: int32 [update_epochs, T*E] (PPO; NULL for IMPALA).
  * stats: float [n_updates, 8] rows [L, policy, value, entropy, approx_kl or mean pg_adv,
  * clipfrac or mean vs, pre-clip grad norm, nonfinite]. */

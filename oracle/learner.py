@@ -12,15 +12,20 @@ import numpy as np
 from . import losses, net as netmod, optim, targets
 
 
-def _adam_update(params, g, m, v, step, cfg, dtype):
+def _opt_update(params, g, m, v, step, cfg, dtype):
+    """Clip the gradient's global norm, then the configured optimiser: Adam (m, v) or
+    RMSprop (v holds its second-moment estimate; m passes through)."""
     g, gnorm = optim.clip_by_global_norm(g, cfg.max_grad_norm, dtype)
+    if getattr(cfg, "optimizer", "adam") == "rmsprop":
+        p, v = optim.rmsprop(params, g, v, cfg.lr, cfg.rms_decay, cfg.rms_eps, dtype)
+        return p, m, v, gnorm
     p, m, v = optim.adam(params, g, m, v, step, cfg.lr, cfg.beta1, cfg.beta2, cfg.adam_eps, dtype)
     return p, m, v, gnorm
 
 
 def ppo_learner_step(net, cfg, ro, params, m, v, step, perm, prec="fp64"):
     """GAE once over the rollout, then update_epochs x num_minibatches updates, each:
-    normalise advantages -> losses -> back-propagate -> clip grad norm -> Adam.
+    normalise advantages -> losses -> back-propagate -> clip grad norm -> optimiser step.
 
     ro: dict with obs [T*E, H, W, C] u8, actions [T*E], logp [T*E] (behaviour), rewards,
     values, dones [T, E], next_value [E], next_done [E].
@@ -43,7 +48,7 @@ def ppo_learner_step(net, cfg, ro, params, m, v, step, perm, prec="fp64"):
                                                  cfg.ent_coef, bool(cfg.norm_adv), dtype=dtype)
             g = netmod.backward(net, cache, dz, dv)
             step += 1
-            p, m_, v_, gn = _adam_update(p, g, m_, v_, step, cfg, dtype)
+            p, m_, v_, gn = _opt_update(p, g, m_, v_, step, cfg, dtype)
             out.append(list(st[:6]) + [gn, float(not np.isfinite(gn))])
     return p, m_, v_, step, np.array(out)
 
@@ -51,7 +56,7 @@ def ppo_learner_step(net, cfg, ro, params, m, v, step, perm, prec="fp64"):
 def impala_learner_step(net, cfg, ro, params, m, v, step, prec="fp64"):
     """Forward over the T*E rollout frames plus E bootstrap frames (rows T*E..), V-trace from
     the current policy's log-probs and values (constants), IMPALA loss, backward over the
-    T*E rollout rows (the bootstrap rows get zero gradient), clip, Adam.
+    T*E rollout rows (the bootstrap rows get zero gradient), clip, optimiser step.
 
     ro: obs [(T+1)*E, H, W, C] u8, actions [T*E], logp [T*E] (behaviour mu), rewards, dones
     [T, E], next_done [E].
@@ -74,7 +79,7 @@ def impala_learner_step(net, cfg, ro, params, m, v, step, prec="fp64"):
     dv_all[:n] = dv
     g = netmod.backward(net, cache, dz_all, dv_all)
     step += 1
-    p, m_, v_, gn = _adam_update(p, g, m_, v_, step, cfg, dtype)
+    p, m_, v_, gn = _opt_update(p, g, m_, v_, step, cfg, dtype)
     stats = np.array([list(st[:6]) + [gn, float(not np.isfinite(gn))]])
     return p, m_, v_, step, stats
 

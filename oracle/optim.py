@@ -1,9 +1,15 @@
-"""Global gradient-norm clipping and Adam, over the flat parameter buffer.
+"""Global gradient-norm clipping, Adam and RMSprop, over the flat parameter buffer.
+
+Test infrastructure: only the tests, the smoke check and the benchmark's CPU baseline use
+this package.
 
 Algorithm 1 clips the maximum gradient norm of all parameters (policy and value share the
 trunk) before the optimiser step; Appendix B sets the threshold (PPO 0.5, IMPALA 40) and
 Adam's epsilon (1e-5). beta1 = 0.9, beta2 = 0.999 and bias correction are the standard Adam
-(Kingma and Ba, 2015) values, as used by optax.
+(Kingma and Ba, 2015) values, as used by optax. Appendix B's IMPALA table gives RMSprop with
+epsilon 0.01 and decay 0.99; where epsilon sits is not stated, and it is read as optax's
+RMSprop does it: inside the square root, with the second-moment estimate starting at zero
+(the paper's learner is written in JAX).
 """
 from __future__ import annotations
 
@@ -36,3 +42,14 @@ def adam(p, g, m, v, step, lr, beta1=0.9, beta2=0.999, eps=1e-5, dtype=np.float6
     mhat = m / (1 - beta1 ** step)
     vhat = v / (1 - beta2 ** step)
     return p - lr * mhat / (np.sqrt(vhat) + eps), m, v
+
+
+def rmsprop(p, g, nu, lr, decay=0.99, eps=0.01, dtype=np.float64):
+    """One RMSprop update; returns new (p, nu).
+
+    nu <- decay nu + (1 - decay) g^2
+    p  <- p - lr * g / sqrt(nu + eps)
+    """
+    p, g, nu = (np.asarray(a, dtype) for a in (p, g, nu))
+    nu = decay * nu + (1 - decay) * g * g
+    return p - lr * g / np.sqrt(nu + eps), nu

@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(HERE, "libcleanba_learner.so")
 
 PREC_BF16, PREC_FP32 = 0, 1
 LEARNER_PPO, LEARNER_IMPALA = 0, 1
+LEARNER_OPT_ADAM, LEARNER_OPT_RMSPROP = 0, 1
 X_PLAIN, X_RELU, X_U8 = 0, 1, 2
 STATUS = {0: "OK", -1: "EINVAL", -2: "EWORKSPACE", -3: "EUNSUPPORTED", -4: "EHIP"}
 
@@ -37,7 +38,8 @@ class LearnerCfg(C.Structure):
                 ("vf_coef", C.c_float), ("ent_coef", C.c_float), ("pg_coef", C.c_float),
                 ("rho_bar", C.c_float), ("c_bar", C.c_float), ("pg_rho_bar", C.c_float),
                 ("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float),
-                ("adam_eps", C.c_float), ("max_grad_norm", C.c_float)]
+                ("adam_eps", C.c_float), ("max_grad_norm", C.c_float),
+                ("optimizer", C.c_int32), ("rms_decay", C.c_float), ("rms_eps", C.c_float)]
 
 
 class Rollout(C.Structure):
@@ -62,6 +64,8 @@ _SIGS = {
     "impala_loss_grad": (C.c_int, [_I64, _I32, _P, _P, _P, _P, _P, _F, _F, _F, _P, _P, _P, _P]),
     "adam_workspace_bytes": (_SZ, [_I64]),
     "adam_step": (C.c_int, [_I64, _P, _P, _P, _P, _I32, _F, _F, _F, _F, _F, _P, _P, _SZ, _P]),
+    "rmsprop_workspace_bytes": (_SZ, [_I64]),
+    "rmsprop_step": (C.c_int, [_I64, _P, _P, _P, _F, _F, _F, _F, _P, _P, _SZ, _P]),
     "learner_workspace_bytes": (_SZ, [_NETP, C.POINTER(LearnerCfg)]),
     "learner_step": (C.c_int, [_NETP, C.POINTER(LearnerCfg), C.POINTER(Rollout), _P, _P, _P,
                                C.POINTER(_I32), _P, _P, _SZ, _P, _P]),
@@ -223,6 +227,16 @@ def adam_step(n_params, params, grads, m, v, step, lr, beta1, beta2, eps, max_gr
         max_grad_norm, ptr(stats), ptr(ws), ws.numel() * ws.element_size(), stream_handle(stream)))
 
 
+def rmsprop_workspace_bytes(n_params: int) -> int:
+    return int(lib.rmsprop_workspace_bytes(n_params))
+
+
+def rmsprop_step(n_params, params, grads, nu, lr, decay, eps, max_grad_norm, stats, ws, stream=None):
+    _check("rmsprop_step", lib.rmsprop_step(
+        n_params, ptr(params), ptr(grads), ptr(nu), lr, decay, eps, max_grad_norm, ptr(stats), ptr(ws),
+        ws.numel() * ws.element_size(), stream_handle(stream)))
+
+
 def learner_cfg(wl, prec: int) -> LearnerCfg:
     """LearnerCfg from a workload description (synth.Workload or anything alike)."""
     c = LearnerCfg()
@@ -236,6 +250,8 @@ def learner_cfg(wl, prec: int) -> LearnerCfg:
     c.rho_bar, c.c_bar, c.pg_rho_bar = wl.rho_bar, wl.c_bar, wl.pg_rho_bar
     c.lr, c.beta1, c.beta2, c.adam_eps = wl.lr, wl.beta1, wl.beta2, wl.adam_eps
     c.max_grad_norm = wl.max_grad_norm
+    c.optimizer = LEARNER_OPT_RMSPROP if getattr(wl, "optimizer", "adam") == "rmsprop" else LEARNER_OPT_ADAM
+    c.rms_decay, c.rms_eps = getattr(wl, "rms_decay", 0.99), getattr(wl, "rms_eps", 0.01)
     return c
 
 

@@ -1,10 +1,11 @@
-// Global-norm gradient clipping and Adam over the flat float32 parameter buffer.
+// Global-norm gradient clipping, then Adam or RMSprop, over the flat float32 parameter buffer.
 //
 // Pass 1: each of up to 1024 blocks sums the squares of a fixed strided share of the
 // gradient in float64 and writes one partial. Pass 2: every block first re-adds all
 // partials in the same fixed order (so every block sees the identical norm), derives the
-// clip scale, then updates params, m and v with 16-byte vector accesses. The update is
-// HBM-bound: per parameter it reads p, g, m, v and writes p, m, v (28 bytes).
+// clip scale, then updates the parameters and the optimiser state with 16-byte vector
+// accesses. The update is HBM-bound: per parameter Adam reads p, g, m, v and writes p, m, v
+// (28 bytes); RMSprop reads p, g, nu and writes p, nu (20 bytes).
 #include "common.h"
 #include "kernels.h"
 
@@ -33,66 +34,123 @@ __global__ __launch_bounds__(256) void sumsq_kernel(int64_t n, const float* __re
 // omb1 = 1 - b1 and omb2 = 1 - b2 arrive precomputed in double precision on the host:
 // forming them from the float betas would carry the betas' representation error
 // (1 - 0.999f differs from 0.001 by 1.3e-5 relative).
-CB_DEV void adam_one(float& p, float g, float& m, float& v, float scale, float lr, float b1,
-                     float b2, float omb1, float omb2, float bc1, float bc2, float eps) {
+CB_DEV void adam_one(float& p, float g, float& m, float& v, float scale, const OptArgs& a) {
     g *= scale;
-    m = b1 * m + omb1 * g;
-    v = b2 * v + omb2 * g * g;
-    const float mhat = m / bc1, vhat = v / bc2;
-    p = p - lr * mhat / (sqrtf(vhat) + eps);
+    m = a.b1 * m + a.omb1 * g;
+    v = a.b2 * v + a.omb2 * g * g;
+    const float mhat = m / a.bc1, vhat = v / a.bc2;
+    p = p - a.lr * mhat / (sqrtf(vhat) + a.eps);
 }
 
-__global__ __launch_bounds__(256) void adam_kernel(int64_t n, float* __restrict__ p,
-                                                   const float* __restrict__ g, float* __restrict__ m,
-                                                   float* __restrict__ v, float lr, float b1, float b2,
-                                                   float omb1, float omb2, float bc1, float bc2,
-                                                   float eps, float max_norm,
-                                                   const double* __restrict__ part, int nparts,
-                                                   float* __restrict__ stats) {
-    __shared__ double sh[256];
+// RMSprop with the decay in b2 and 1 - decay in omb2: nu <- decay nu + (1 - decay) g^2;
+// p <- p - lr g / sqrt(nu + eps) (epsilon inside the root; nu starts at zero).
+CB_DEV void rms_one(float& p, float g, float& nu, float scale, const OptArgs& a) {
+    g *= scale;
+    nu = a.b2 * nu + a.omb2 * g * g;
+    p = p - a.lr * g / sqrtf(nu + a.eps);
+}
+
+template <int OPT>
+CB_DEV void opt_one(float& p, float g, float& m, float& v, float scale, const OptArgs& a) {
+    if constexpr (OPT == OPT_ADAM) adam_one(p, g, m, v, scale, a);
+    else rms_one(p, g, v, scale, a);
+}
+
+template <int OPT>
+CB_DEV void opt_four(float4& p, const float4& g, float4& m, float4& v, float scale, const OptArgs& a) {
+    opt_one<OPT>(p.x, g.x, m.x, v.x, scale, a);
+    opt_one<OPT>(p.y, g.y, m.y, v.y, scale, a);
+    opt_one<OPT>(p.z, g.z, m.z, v.z, scale, a);
+    opt_one<OPT>(p.w, g.w, m.w, v.w, scale, a);
+}
+
+// Clip scale from the norm partials (every block re-adds them in the same order); block 0's
+// thread 0 records [norm, nonfinite]. pv: this thread's partials (indices t, t + 256, ...).
+CB_DEV float clip_scale(const double (&pv)[4], int nparts, float max_norm, double* sh, float* stats) {
     double s = 0.0;
-    for (int i = threadIdx.x; i < nparts; i += 256) s += part[i];
-    const double tot = block_sum<256>(s, sh);
-    const double norm = sqrt(tot);
-    const float scale = (max_norm > 0.f && norm > double(max_norm)) ? float(double(max_norm) / norm) : 1.f;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+        if (int(threadIdx.x) + 256 * u < nparts) s += pv[u];
+    const double norm = sqrt(block_sum<256>(s, sh));
     if (blockIdx.x == 0 && threadIdx.x == 0 && stats) {
         stats[0] = float(norm);
         stats[1] = isfinite(norm) ? 0.f : 1.f;
     }
-    const int64_t n4 = n / 4;
-    float4* p4 = reinterpret_cast<float4*>(p);
-    float4* m4 = reinterpret_cast<float4*>(m);
-    float4* v4 = reinterpret_cast<float4*>(v);
-    const float4* g4 = reinterpret_cast<const float4*>(g);
-    for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n4; i += int64_t(gridDim.x) * 256) {
-        float4 pp = p4[i], mm = m4[i], vv = v4[i];
-        const float4 gg = g4[i];
-        adam_one(pp.x, gg.x, mm.x, vv.x, scale, lr, b1, b2, omb1, omb2, bc1, bc2, eps);
-        adam_one(pp.y, gg.y, mm.y, vv.y, scale, lr, b1, b2, omb1, omb2, bc1, bc2, eps);
-        adam_one(pp.z, gg.z, mm.z, vv.z, scale, lr, b1, b2, omb1, omb2, bc1, bc2, eps);
-        adam_one(pp.w, gg.w, mm.w, vv.w, scale, lr, b1, b2, omb1, omb2, bc1, bc2, eps);
-        p4[i] = pp; m4[i] = mm; v4[i] = vv;
-    }
-    if (blockIdx.x == 0)
-        for (int64_t i = n4 * 4 + threadIdx.x; i < n; i += 256)
-            adam_one(p[i], g[i], m[i], v[i], scale, lr, b1, b2, omb1, omb2, bc1, bc2, eps);
+    return (max_norm > 0.f && norm > double(max_norm)) ? float(double(max_norm) / norm) : 1.f;
 }
 
-hipError_t adam(int64_t n, float* p, const float* g, float* m, float* v, float lr, float b1,
-                float b2, float omb1, float omb2, float bc1, float bc2, float eps, float max_norm,
-                float* stats, float* partial, hipStream_t s) {
-    if (n <= 0) return hipSuccess;
+// Each thread's first float4 of p, g, m, v is loaded before the norm is known (clamped
+// index, so the loads are unconditional): their latency overlaps the re-addition of the
+// norm partials, which are loaded before them (loads complete in order, so waiting for the
+// partials does not wait for the parameters).
+template <int OPT>
+__global__ __launch_bounds__(256) void opt_kernel(OptArgs a, const double* __restrict__ part, int nparts,
+                                                  float* __restrict__ stats) {
+    __shared__ double sh[256];
+    static_assert(kAdamBlocks <= 4 * 256, "four partials per thread");
+    double pv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int i = int(threadIdx.x) + 256 * u;
+        pv[u] = part[i < nparts ? i : 0];
+    }
+    const int64_t n4 = a.n / 4;
+    if (n4 == 0) {   // fewer than four parameters: block 0 alone, element by element
+        const float scale = clip_scale(pv, nparts, a.max_norm, sh, stats);
+        if (blockIdx.x == 0)
+            for (int64_t i = threadIdx.x; i < a.n; i += 256) {
+                float mt = OPT == OPT_ADAM ? a.m[i] : 0.f;
+                opt_one<OPT>(a.p[i], a.g[i], mt, a.v[i], scale, a);
+                if constexpr (OPT == OPT_ADAM) a.m[i] = mt;
+            }
+        return;
+    }
+    float4* p4 = reinterpret_cast<float4*>(a.p);
+    float4* m4 = reinterpret_cast<float4*>(a.m);
+    float4* v4 = reinterpret_cast<float4*>(a.v);
+    const float4* g4 = reinterpret_cast<const float4*>(a.g);
+    const int64_t i0 = int64_t(blockIdx.x) * 256 + threadIdx.x, stride = int64_t(gridDim.x) * 256;
+    const int64_t ic = i0 < n4 ? i0 : n4 - 1;
+    float4 pp = p4[ic], gg = g4[ic], vv = v4[ic];
+    float4 mm = make_float4(0.f, 0.f, 0.f, 0.f);
+    if constexpr (OPT == OPT_ADAM) mm = m4[ic];
+    const float scale = clip_scale(pv, nparts, a.max_norm, sh, stats);
+    if (i0 < n4) {
+        opt_four<OPT>(pp, gg, mm, vv, scale, a);
+        p4[i0] = pp; v4[i0] = vv;
+        if constexpr (OPT == OPT_ADAM) m4[i0] = mm;
+    }
+    for (int64_t i = i0 + stride; i < n4; i += stride) {
+        pp = p4[i]; gg = g4[i]; vv = v4[i];
+        if constexpr (OPT == OPT_ADAM) mm = m4[i];
+        opt_four<OPT>(pp, gg, mm, vv, scale, a);
+        p4[i] = pp; v4[i] = vv;
+        if constexpr (OPT == OPT_ADAM) m4[i] = mm;
+    }
+    if (blockIdx.x == 0)
+        for (int64_t i = n4 * 4 + threadIdx.x; i < a.n; i += 256) {
+            float mt = OPT == OPT_ADAM ? a.m[i] : 0.f;
+            opt_one<OPT>(a.p[i], a.g[i], mt, a.v[i], scale, a);
+            if constexpr (OPT == OPT_ADAM) a.m[i] = mt;
+        }
+}
+
+hipError_t clip_opt_step(int opt, const OptArgs& a, float* stats, float* partial, hipStream_t s) {
+    if (a.n <= 0) return hipSuccess;
     double* part = reinterpret_cast<double*>(partial);
-    int64_t blocks = (n / 4 + 255) / 256;
+    int64_t blocks = (a.n / 4 + 255) / 256;
     if (blocks < 1) blocks = 1;
     if (blocks > kAdamBlocks) blocks = kAdamBlocks;
     {
-        ProfScope ps(s, [&] { return "grad_sumsq/" + std::to_string(n); });
-        hipLaunchKernelGGL(sumsq_kernel, dim3(unsigned(blocks)), dim3(256), 0, s, n, g, part);
+        ProfScope ps(s, [&] { return "grad_sumsq/" + std::to_string(a.n); });
+        hipLaunchKernelGGL(sumsq_kernel, dim3(unsigned(blocks)), dim3(256), 0, s, a.n, a.g, part);
     }
-    ProfScope ps(s, [&] { return "adam/" + std::to_string(n); });
-    hipLaunchKernelGGL(adam_kernel, dim3(unsigned(blocks)), dim3(256), 0, s, n, p, g, m, v, lr, b1, b2,
-                       omb1, omb2, bc1, bc2, eps, max_norm, part, int(blocks), stats);
+    ProfScope ps(s, [&] { return std::string(opt == OPT_ADAM ? "adam/" : "rmsprop/") + std::to_string(a.n); });
+    if (opt == OPT_ADAM)
+        hipLaunchKernelGGL(opt_kernel<OPT_ADAM>, dim3(unsigned(blocks)), dim3(256), 0, s, a, part, int(blocks), stats);
+    else
+        hipLaunchKernelGGL(opt_kernel<OPT_RMSPROP>, dim3(unsigned(blocks)), dim3(256), 0, s, a, part, int(blocks),
+                           stats);
     return hipGetLastError();
 }
 

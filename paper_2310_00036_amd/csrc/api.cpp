@@ -66,9 +66,14 @@ std::string check_cfg(const learner_cfg_t* c) {
         if (int64_t(c->num_minibatches) * c->minibatch_size > int64_t(c->T) * c->E)
             return "num_minibatches * minibatch_size exceeds T * E";
     }
-    if (!(c->lr >= 0.f) || !(c->adam_eps >= 0.f) || !(c->beta1 >= 0.f && c->beta1 < 1.f) ||
-        !(c->beta2 >= 0.f && c->beta2 < 1.f))
+    if (c->optimizer != LEARNER_OPT_ADAM && c->optimizer != LEARNER_OPT_RMSPROP)
+        return "cfg.optimizer must be ADAM or RMSPROP";
+    if (!(c->lr >= 0.f)) return "cfg.lr must be >= 0";
+    if (c->optimizer == LEARNER_OPT_ADAM &&
+        (!(c->adam_eps >= 0.f) || !(c->beta1 >= 0.f && c->beta1 < 1.f) || !(c->beta2 >= 0.f && c->beta2 < 1.f)))
         return "cfg Adam hyperparameters out of range";
+    if (c->optimizer == LEARNER_OPT_RMSPROP && (!(c->rms_eps >= 0.f) || !(c->rms_decay >= 0.f && c->rms_decay < 1.f)))
+        return "cfg RMSprop hyperparameters out of range";
     return "";
 }
 
@@ -299,17 +304,28 @@ impala_status_t impala_loss_grad(int64_t m, int32_t A, const float* logits, cons
 }
 
 namespace {
-struct AdamConsts { float omb1, omb2, bc1, bc2; };
+// Adam's constants from the caller's float betas: 1 - beta and the bias corrections
+// 1 - beta^t formed in double (in float, 1 - beta would lose the low bits of beta: for
+// 0.999f about 1e-5 relative).
+OptArgs adam_args(int64_t n, float* p, const float* g, float* m, float* v, int32_t step, float lr, float b1,
+                  float b2, float eps, float max_norm) {
+    OptArgs a{};
+    a.n = n; a.p = p; a.g = g; a.m = m; a.v = v;
+    a.lr = lr; a.b1 = b1; a.b2 = b2; a.eps = eps; a.max_norm = max_norm;
+    a.omb1 = float(1.0 - double(b1));
+    a.omb2 = float(1.0 - double(b2));
+    a.bc1 = float(1.0 - std::pow(double(b1), double(step)));
+    a.bc2 = float(1.0 - std::pow(double(b2), double(step)));
+    return a;
+}
 
-// 1 - beta and the bias corrections 1 - beta^t of the caller's float betas, formed in double
-// (in float, 1 - beta would lose the low bits of beta: for 0.999f about 1e-5 relative).
-AdamConsts adam_consts(int32_t step, float b1, float b2) {
-    AdamConsts c;
-    c.omb1 = float(1.0 - double(b1));
-    c.omb2 = float(1.0 - double(b2));
-    c.bc1 = float(1.0 - std::pow(double(b1), double(step)));
-    c.bc2 = float(1.0 - std::pow(double(b2), double(step)));
-    return c;
+// RMSprop's: decay in b2, 1 - decay (formed in double) in omb2.
+OptArgs rmsprop_args(int64_t n, float* p, const float* g, float* nu, float lr, float decay, float eps,
+                     float max_norm) {
+    OptArgs a{};
+    a.n = n; a.p = p; a.g = g; a.m = nullptr; a.v = nu;
+    a.lr = lr; a.b2 = decay; a.omb2 = float(1.0 - double(decay)); a.eps = eps; a.max_norm = max_norm;
+    return a;
 }
 }  // namespace
 
@@ -329,10 +345,24 @@ impala_status_t adam_step(int64_t n_params, float* params, const float* grads, f
     CHECK_PTR(params); CHECK_PTR(grads); CHECK_PTR(m); CHECK_PTR(v); CHECK_PTR(ws);
     const size_t need = adam_workspace_bytes(n_params);
     if (ws_bytes < need) return fail(IMPALA_EWORKSPACE, "adam_step: workspace %zu < %zu bytes", ws_bytes, need);
-    const AdamConsts ac = adam_consts(step, beta1, beta2);
-    return hip_status(adam(n_params, params, grads, m, v, lr, beta1, beta2, ac.omb1, ac.omb2, ac.bc1, ac.bc2,
-                           eps, max_grad_norm, stats, static_cast<float*>(ws), stream),
-                      "adam_step");
+    const OptArgs a = adam_args(n_params, params, grads, m, v, step, lr, beta1, beta2, eps, max_grad_norm);
+    return hip_status(clip_opt_step(OPT_ADAM, a, stats, static_cast<float*>(ws), stream), "adam_step");
+}
+
+size_t rmsprop_workspace_bytes(int64_t n_params) { return adam_workspace_bytes(n_params); }
+
+impala_status_t rmsprop_step(int64_t n_params, float* params, const float* grads, float* nu, float lr,
+                             float decay, float eps, float max_grad_norm, float* stats, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
+    if (n_params < 0) return fail(IMPALA_EINVAL, "rmsprop_step: n_params < 0");
+    if (!(decay >= 0.f && decay < 1.f)) return fail(IMPALA_EINVAL, "rmsprop_step: decay must be in [0, 1)");
+    if (!(eps >= 0.f)) return fail(IMPALA_EINVAL, "rmsprop_step: eps must be >= 0");
+    if (n_params == 0) return ok();
+    CHECK_PTR(params); CHECK_PTR(grads); CHECK_PTR(nu); CHECK_PTR(ws);
+    const size_t need = rmsprop_workspace_bytes(n_params);
+    if (ws_bytes < need) return fail(IMPALA_EWORKSPACE, "rmsprop_step: workspace %zu < %zu bytes", ws_bytes, need);
+    const OptArgs a = rmsprop_args(n_params, params, grads, nu, lr, decay, eps, max_grad_norm);
+    return hip_status(clip_opt_step(OPT_RMSPROP, a, stats, static_cast<float*>(ws), stream), "rmsprop_step");
 }
 
 size_t learner_workspace_bytes(const impala_net_t* net, const learner_cfg_t* cfg) {
@@ -350,8 +380,9 @@ impala_status_t learner_step(const impala_net_t* net, const learner_cfg_t* cfg,
     std::string e = check_net(net);
     if (e.empty()) e = check_cfg(cfg);
     if (!e.empty()) return fail(IMPALA_EINVAL, "learner_step: %s", e.c_str());
-    CHECK_PTR(ro); CHECK_PTR(params); CHECK_PTR(m); CHECK_PTR(v); CHECK_PTR(step); CHECK_PTR(ws);
+    CHECK_PTR(ro); CHECK_PTR(params); CHECK_PTR(v); CHECK_PTR(step); CHECK_PTR(ws);
     CHECK_PTR(stats);
+    if (cfg->optimizer == LEARNER_OPT_ADAM) CHECK_PTR(m);
     CHECK_PTR(ro->obs); CHECK_PTR(ro->actions); CHECK_PTR(ro->behav_logp); CHECK_PTR(ro->rewards);
     CHECK_PTR(ro->dones); CHECK_PTR(ro->next_done);
     if (*step < 0) return fail(IMPALA_EINVAL, "learner_step: *step must be >= 0");
@@ -376,6 +407,16 @@ impala_status_t learner_step(const impala_net_t* net, const learner_cfg_t* cfg,
     hipError_t he;
 #define LS_TRY(x, what) \
     if ((he = (x)) != hipSuccess) return hip_status(he, what)
+    // clip, then the configured optimiser (Adam: m, v; RMSprop: v holds nu), at step *step
+    auto opt_step = [&](float* st) {
+        if (c.optimizer == LEARNER_OPT_ADAM)
+            return clip_opt_step(OPT_ADAM, adam_args(P.po.total, params, grads, m, v, *step, c.lr, c.beta1, c.beta2,
+                                                     c.adam_eps, c.max_grad_norm),
+                                 st, apart, stream);
+        return clip_opt_step(OPT_RMSPROP, rmsprop_args(P.po.total, params, grads, v, c.lr, c.rms_decay, c.rms_eps,
+                                                       c.max_grad_norm),
+                             st, apart, stream);
+    };
 
     if (c.algo == LEARNER_PPO) {
         float* adv = reinterpret_cast<float*>(w + L.adv);
@@ -395,10 +436,7 @@ impala_status_t learner_step(const impala_net_t* net, const learner_cfg_t* cfg,
                 LS_TRY(run_backward(P, params, ro->obs, rows, mb, cnn, dlogits, dvalue, grads, stream),
                        "learner_step: backward");
                 *step += 1;
-                const AdamConsts ac = adam_consts(*step, c.beta1, c.beta2);
-                LS_TRY(adam(P.po.total, params, grads, m, v, c.lr, c.beta1, c.beta2, ac.omb1, ac.omb2, ac.bc1,
-                            ac.bc2, c.adam_eps, c.max_grad_norm, stats + 8 * u + 6, apart, stream),
-                       "learner_step: adam");
+                LS_TRY(opt_step(stats + 8 * u + 6), "learner_step: optimiser");
             }
         }
     } else {
@@ -417,9 +455,7 @@ impala_status_t learner_step(const impala_net_t* net, const learner_cfg_t* cfg,
         LS_TRY(run_backward(P, params, ro->obs, nullptr, TE, cnn, dlogits, dvalue, grads, stream),
                "learner_step: backward");
         *step += 1;
-        const AdamConsts ac = adam_consts(*step, c.beta1, c.beta2);
-        LS_TRY(adam(P.po.total, params, grads, m, v, c.lr, c.beta1, c.beta2, ac.omb1, ac.omb2, ac.bc1, ac.bc2,
-                    c.adam_eps, c.max_grad_norm, stats + 6, apart, stream), "learner_step: adam");
+        LS_TRY(opt_step(stats + 6), "learner_step: optimiser");
     }
 #undef LS_TRY
     return ok();

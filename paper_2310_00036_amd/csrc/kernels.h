@@ -196,9 +196,16 @@ hipError_t gumbel_max(int64_t m, int A, const float* z, const float* g, int32_t*
                       float* logp, hipStream_t s);
 size_t adam_partial_floats(int64_t n);
 // omb1 = 1 - b1, omb2 = 1 - b2, bc1 = 1 - b1^t, bc2 = 1 - b2^t, all formed in double.
-hipError_t adam(int64_t n, float* p, const float* g, float* m, float* v, float lr, float b1,
-                float b2, float omb1, float omb2, float bc1, float bc2, float eps, float max_norm,
-                float* stats, float* partial, hipStream_t s);
+enum { OPT_ADAM = 0, OPT_RMSPROP = 1 };
+// Adam: b1, b2, omb1 = 1 - b1, omb2 = 1 - b2 (formed in double), bc1 = 1 - b1^t, bc2 = 1 - b2^t.
+// RMSprop: b2 = decay, omb2 = 1 - decay; m unused; v holds nu.
+struct OptArgs {
+    int64_t n;
+    float* p; const float* g; float* m; float* v;
+    float lr, b1, b2, omb1, omb2, bc1, bc2, eps, max_norm;
+};
+// Global-norm clip then one optimiser step; stats [2] = [pre-clip norm, nonfinite] or NULL.
+hipError_t clip_opt_step(int opt, const OptArgs& a, float* stats, float* partial, hipStream_t s);
 // Largest dynamic LDS allocation per workgroup on the current device (bytes).
 size_t lds_limit();
 // Workgroups of kernel `fn` (with `threads` threads and `lds` bytes of dynamic LDS) that are

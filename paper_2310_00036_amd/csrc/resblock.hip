@@ -130,20 +130,22 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_fwd_kernel(ResBlockArgs a
     int lg = blockIdx.x;   // neighbouring bands on one XCD
     if ((gridDim.x & 7) == 0) lg = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
 
+    // x window of a tile, rows h0-2 .. h0+TH+1. The next tile's window is issued as soon as
+    // conv1 has finished reading this one, so its latency overlaps conv2.
+    auto stage_x = [&](int tile) {
+        const int band = tile % t.nbands, f = tile / t.nbands;
+        const auto rx = buf_rsrc(static_cast<const uint16_t*>(a.x) + int64_t(f) * H * W * C, uint32_t(H) * W * C * 2);
+        const uint32_t hr = uint32_t((band * TH - 2) * W * C * 2);   // wraps for h0 < 2: rows off the frame
+#pragma unroll
+        for (int k = 0; k < G::MAXS; ++k)
+            if ((wave + NW * k) * 64 < nsx) dma16_to_lds(rx, xw + (wave + NW * k) * 1024, ox[k] + hr);
+    };
+    if (lg < t.ntiles) stage_x(lg);
+
     for (int tile = lg; tile < t.ntiles; tile += gridDim.x) {
         const int band = tile % t.nbands, f = tile / t.nbands;
         const int h0 = band * TH, the = H - h0 < TH ? H - h0 : TH;
         const int64_t fo = int64_t(f) * H * W * C;   // frame offset (elements)
-        __syncthreads();   // the previous tile's LDS reads are done
-
-        // ---- stage the x window, rows h0-2 .. h0+TH+1
-        {
-            const auto rx = buf_rsrc(static_cast<const uint16_t*>(a.x) + fo, uint32_t(H) * W * C * 2);
-            const uint32_t hr = uint32_t((h0 - 2) * W * C * 2);   // wraps for h0 < 2: rows off the frame
-#pragma unroll
-            for (int k = 0; k < G::MAXS; ++k)
-                if ((wave + NW * k) * 64 < nsx) dma16_to_lds(rx, xw + (wave + NW * k) * 1024, ox[k] + hr);
-        }
         // conv2's residual x for this wave's column tiles, fetched alongside the staging
         const uint16_t* xbase = static_cast<const uint16_t*>(a.x) + fo + int64_t(h0) * W * C;
         const int npx2 = the * W;
@@ -153,7 +155,7 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_fwd_kernel(ResBlockArgs a
             const int q = (wave / MT + k * (NW / MT)) * 16 + r16;
             xres[k] = q < npx2 ? *reinterpret_cast<const uint2*>(xbase + uint32_t(q * C + co0)) : make_uint2(0, 0);
         }
-        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_s_waitcnt(0);   // this tile's window (and the residual) have landed
         __syncthreads();
         {
             uint4* w4 = reinterpret_cast<uint4*>(xw);
@@ -193,7 +195,8 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_fwd_kernel(ResBlockArgs a
                     make_uint2(relu_bf16x2(u0), relu_bf16x2(u1));
             }
         }
-        __syncthreads();
+        __syncthreads();   // conv1 has read the x window: the next tile's may land there
+        if (tile + int(gridDim.x) < t.ntiles) stage_x(tile + gridDim.x);
 
         // ---- conv2 + residual: y on the band's rows
         uint16_t* ybase = static_cast<uint16_t*>(a.y) + fo + int64_t(h0) * W * C;

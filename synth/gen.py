@@ -52,6 +52,9 @@ class Workload:
     beta2: float = 0.999
     adam_eps: float = 1e-5
     max_grad_norm: float = 0.5
+    optimizer: str = "adam"      # "adam" | "rmsprop"
+    rms_decay: float = 0.99
+    rms_eps: float = 0.01
     norm_adv: int = 1
     reward_probs: tuple = (0.05, 0.9, 0.05)   # P(r=-1), P(r=0), P(r=+1)
     done_prob: float = 0.02

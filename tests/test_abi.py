@@ -80,6 +80,12 @@ def test_null_pointers_and_small_workspace_fail_before_hip():
     assert lib.adam_step(10, 1, 1, 1, 1, 0, 1e-3, .9, .999, 1e-5, .5, None, 1, 1 << 20, None) == -1
     assert lib.adam_step(10, 1, 1, 1, 1, 1, 1e-3, 1.0, .999, 1e-5, .5, None, 1, 1 << 20, None) == -1
     assert lib.adam_step(10, 1, 1, 1, 1, 1, 1e-3, .9, .999, 1e-5, .5, None, 1, 8, None) == -2
+    # rmsprop
+    assert lib.rmsprop_step(10, 1, 1, 1, 6e-4, 1.0, .01, 40., None, 1, 1 << 20, None) == -1
+    assert lib.rmsprop_step(10, 1, 1, 1, 6e-4, .99, -1., 40., None, 1, 1 << 20, None) == -1
+    assert lib.rmsprop_step(10, 1, 1, None, 6e-4, .99, .01, 40., None, 1, 1 << 20, None) == -1
+    assert lib.rmsprop_step(10, 1, 1, 1, 6e-4, .99, .01, 40., None, 1, 8, None) == -2
+    assert lib.rmsprop_step(0, None, None, None, 6e-4, .99, .01, 40., None, None, 0, None) == 0
     # layers
     assert lib.impala_conv3x3_fwd(0, 4, 84, 84, 4, 24, 1, 2, None, 1, None, None, 1, None) == -3
     assert lib.impala_conv3x3_dgrad(0, 4, 42, 42, 32, 16, 1, 1, None, None, 1, None) == -3
@@ -101,6 +107,11 @@ def test_learner_cfg_validation():
     r = P.lib.learner_step(C.byref(P.net_struct(wl.net)), C.byref(cfg), C.byref(ro), 1, 1, 1,
                            C.byref(st), 1, 1, 1 << 40, 1, None)
     assert r == -1 and b"obs" in P.lib.impala_last_error()
+    bad = P.learner_cfg(wl.replace(optimizer="rmsprop", rms_decay=1.0), P.PREC_BF16)
+    assert P.lib.learner_workspace_bytes(C.byref(P.net_struct(wl.net)), C.byref(bad)) == 0
+    assert b"RMSprop" in P.lib.impala_last_error()
+    bad.optimizer = 7
+    assert P.lib.learner_workspace_bytes(C.byref(P.net_struct(wl.net)), C.byref(bad)) == 0
 
 
 def test_workspace_grows_with_frames_and_precision():

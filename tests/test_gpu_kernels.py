@@ -502,6 +502,36 @@ def test_adam_matches_oracle(n, scale, max_norm, step):
     assert abs(s[0] - norm) <= 1e-5 * norm and s[1] == 0
 
 
+@pytest.mark.parametrize("n,scale,max_norm", [(1_094_115, 1e-3, 40.0), (1_094_115, 100.0, 40.0),
+                                             (4_364_211, 1.0, 0.5), (1001, 1.0, 0.0), (3, 1.0, 40.0)])
+def test_rmsprop_matches_oracle(n, scale, max_norm):
+    """Appendix B's IMPALA optimiser (decay 0.99, eps 0.01) after the global-norm clip."""
+    rng = np.random.default_rng(n + 17)
+    p = rng.standard_normal(n).astype(np.float32)
+    g = (rng.standard_normal(n) * scale / np.sqrt(n) * 30).astype(np.float32)
+    nu = (rng.random(n) * 1e-3).astype(np.float32)
+    f = lambda x: float(np.float32(x))  # noqa: E731
+    gc, norm = ooptim.clip_by_global_norm(g, f(max_norm))
+    pw, nuw = ooptim.rmsprop(p, gc, nu, f(6e-4), f(0.99), f(0.01))
+    dp, dg, dnu = G.dev_f32(p), G.dev_f32(g), G.dev_f32(nu)
+    st = G.dev_f32(np.zeros(2))
+    ws = G.ws_bytes(P.rmsprop_workspace_bytes(n))
+    P.rmsprop_step(n, dp, dg, dnu, 6e-4, 0.99, 0.01, max_norm, st, ws)
+    G.sync()
+    G.assert_close(G.host(dnu), nuw, 1e-5, "nu")
+    got_p = G.host(dp)
+    ulp = np.spacing(np.abs(pw).astype(np.float32)).astype(np.float64)
+    assert (np.abs(got_p - pw) <= 2 * ulp + 1e-5 * np.abs(pw - p)).all()
+    # the step is proportional to g while g^2 << eps: for small gradients it is a few ulps of
+    # the parameter, so the step itself is compared where it spans at least 1024 ulps (the
+    # result's own rounding then stays below 5e-4 of the step)
+    big = np.abs(pw - p) >= 1024 * ulp
+    if big.sum() >= 16:
+        G.assert_close(got_p[big] - p[big], (pw - p)[big], 1e-3, "param update")
+    s = G.host(st)
+    assert abs(s[0] - norm) <= 1e-5 * norm and s[1] == 0
+
+
 @pytest.mark.parametrize("n,A", [(128, 18), (1000, 6), (7, 64)])
 def test_gumbel_sample_bit_exact(n, A):
     rng = np.random.default_rng(n)

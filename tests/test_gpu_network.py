@@ -220,8 +220,12 @@ def _compare_learner(wl, prec, p0, out_gpu, want, label, tier, emu=None):
     assert step == want[3]
     net = wl.net
     got_m, got_v, got_p = G.host(m), G.host(v), G.host(p)
-    # m after the updates is a weighted sum of the (clipped) gradients: per-tensor parity
-    _check_grads(got_m, want[1], net, prec, label + " adam-m", tier, None if emu is None else emu[1])
+    # Adam's m after the updates is a weighted sum of the (clipped) gradients: per-tensor
+    # parity (RMSprop keeps no first moment; its nu is checked below like Adam's v)
+    if wl.optimizer == "adam":
+        _check_grads(got_m, want[1], net, prec, label + " adam-m", tier, None if emu is None else emu[1])
+    else:
+        assert (got_m == 0).all()   # untouched
     if prec == G.FP32:
         tol = FP32_TOL if tier == "A" else FP32_FLIP_TOL
         assert G.rel_l2(got_v, want[2]) <= 2 * tol
@@ -318,6 +322,18 @@ def test_learner_step_impala_small(prec):
     want, emu = _oracle_learner(wl, params, ro, None, prec)
     got = _learner_gpu(wl, prec, params, ro, None)
     _compare_learner(wl, prec, params.astype(np.float64), got, want, "impala", "B", emu)
+
+
+@pytest.mark.parametrize("prec", [G.BF16, G.FP32], ids=lambda p: PNAME[p])
+def test_learner_step_impala_rmsprop(prec):
+    """Tier B: IMPALA with Appendix B's RMSprop (decay 0.99, eps 0.01), 8 envs x 5 steps."""
+    wl = WORKLOADS[2].replace(T=5, E=8, seed=23, optimizer="rmsprop")
+    params = draw_params(wl.net, wl.seed)
+    raw = draw_rollout(wl)
+    ro = olearner.behaviour_rollout(wl, params, raw)
+    want, emu = _oracle_learner(wl, params, ro, None, prec)
+    got = _learner_gpu(wl, prec, params, ro, None)
+    _compare_learner(wl, prec, params.astype(np.float64), got, want, "impala-rmsprop", "B", emu)
 
 
 def _c1_like_inputs(seed=1):

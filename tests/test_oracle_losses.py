@@ -120,6 +120,37 @@ def test_adam_second_step_by_hand():
     assert np.isclose(p[0], -1.0 - mhat / np.sqrt(vhat), rtol=1e-14)
 
 
+def test_rmsprop_first_step_by_hand():
+    # Appendix B's IMPALA values (decay 0.99, eps 0.01), g = 3, lr = 1, nu0 = 0:
+    # nu = 0.01 * 9 = 0.09; step = 3 / sqrt(0.09 + 0.01) = 3 / sqrt(0.1) = 9.486832980505138
+    # (epsilon outside the root would give 3 / 0.31 = 9.677...)
+    p, nu = optim.rmsprop(np.array([0.0]), np.array([3.0]), np.zeros(1), 1.0, 0.99, 0.01)
+    assert np.isclose(nu[0], 0.09, rtol=1e-14)
+    assert np.isclose(p[0], -9.486832980505138, rtol=1e-14)
+
+
+def test_rmsprop_constant_gradient_closed_form():
+    # with a constant gradient from nu0 = 0 the recurrence sums a geometric series:
+    # nu_t = (1 - decay^t) g^2, so the t-th step is g / sqrt((1 - decay^t) g^2 + eps)
+    rng = np.random.default_rng(8)
+    g = rng.standard_normal(40) * 3
+    p0 = rng.standard_normal(40)
+    p, nu = p0.copy(), np.zeros(40)
+    lr, decay, eps = 6e-4, 0.99, 0.01
+    for _ in range(25):
+        p, nu = optim.rmsprop(p, g, nu, lr, decay, eps)
+    np.testing.assert_allclose(nu, (1 - decay ** 25) * g * g, rtol=1e-12)
+    want = p0 - lr * sum(g / np.sqrt((1 - decay ** t) * g * g + eps) for t in range(1, 26))
+    np.testing.assert_allclose(p, want, rtol=1e-12, atol=1e-15)
+
+
+def test_rmsprop_without_decay_or_eps_steps_by_the_sign():
+    # decay 0, eps 0: nu = g^2 and the step is lr * g / |g| = lr * sign(g)
+    g = np.array([-2.5, 0.125, 7.0, -1e-3])
+    p, _ = optim.rmsprop(np.zeros(4), g, np.full(4, 5.0), 0.1, 0.0, 0.0)
+    np.testing.assert_allclose(p, -0.1 * np.sign(g), rtol=1e-15)
+
+
 @pytest.mark.parametrize("scale,max_norm", [(0.1, 0.5), (10.0, 0.5), (3.0, 40.0), (100.0, 40.0), (5.0, 0.0)])
 def test_clip_norm_is_min_of_norm_and_threshold(scale, max_norm):
     g = np.random.default_rng(5).standard_normal(1000) * scale
