@@ -27,7 +27,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK = {"bf16": (2500.0, "TFLOP/s"), "fp32": (157.3, "TFLOP/s"), "hbm": (8000.0, "GB/s")}
-WORKLOAD_NAMES = {1: "ppo_64x128_mb2048x4_e2", 2: "impala_vtrace_64x20", 4: "ppo_wide_128x128_mb8192"}
+WORKLOAD_NAMES = {1: "ppo_64x128_mb2048x4_e2", 2: "impala_vtrace_64x20", 4: "ppo_wide_128x128_mb8192",
+                  5: "ppo_paper_128x128_mb4096x4_e4", 6: "impala_paper_128x20_mb4"}
 
 
 def parse():
@@ -353,7 +354,7 @@ def main():
     stats = torch.zeros((wl.n_updates, 8), dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
     step = 0
-    mb = wl.mb if wl.algo == "ppo" else wl.T * wl.E
+    mb = wl.mb if wl.algo == "ppo" else wl.T * wl.E // wl.num_minibatches   # rollout rows per update
     frames_per_step = wl.n_updates * mb
 
     def run(k):
@@ -414,6 +415,7 @@ def main():
         "config": {"workload": WORKLOAD_NAMES[args.workload], "algo": wl.algo, "envs": wl.E,
                    "steps_per_env": wl.T, "minibatch": mb, "updates_per_step": wl.n_updates,
                    "frame_passes_per_step": frames_per_step, "net": f"{net.ch}/{net.hidden}/A{net.num_actions}",
+                   "optimizer": wl.optimizer,
                    "rollout_frames_per_s": round(wl.T * wl.E * args.steps / (gpu_ms / 1e3), 1),
                    "wall_s": round(wall, 3)},
         "roofline": {"bound": bound, "kernel": dominant[0], "achieved": round(achieved, 2), "peak": peak,

@@ -191,8 +191,8 @@ typedef struct learner_cfg {
     int32_t algo;             /* learner_algo_t */
     int32_t prec;             /* impala_prec_t */
     int32_t T, E;             /* num_steps, local_num_envs */
-    int32_t update_epochs;    /* PPO; IMPALA does one update */
-    int32_t num_minibatches;  /* PPO */
+    int32_t update_epochs;    /* PPO; IMPALA takes each minibatch once */
+    int32_t num_minibatches;  /* PPO: row minibatches; IMPALA: env blocks (divides E) */
     int32_t minibatch_size;   /* PPO m; num_minibatches * m <= T * E */
     int32_t norm_adv;         /* PPO: normalise advantages per minibatch */
     float gamma, lambda;      /* discount; GAE lambda / V-trace lambda */
@@ -225,12 +225,15 @@ size_t learner_workspace_bytes(const impala_net_t* net, const learner_cfg_t* cfg
 
 /* One learning phase. PPO: GAE once, then for epoch j and minibatch k the rows
  * perm[j*T*E + k*m .. +m]: forward, loss, backward, clip, optimiser step (step incremented
- * per update). IMPALA: forward over (T+1)*E frames, target log-probs, V-trace, loss over the
- * T*E rows, backward (bootstrap rows get no gradient), clip, optimiser step.
+ * per update). IMPALA: for minibatch k, the env block [k*E/N, (k+1)*E/N) (N = num_minibatches;
+ * V-trace runs along time, so a minibatch keeps whole trajectories): forward over its T*E/N
+ * rollout frames and E/N bootstrap frames, target log-probs, V-trace, loss over the rollout
+ * rows, backward (bootstrap rows get no gradient), clip, optimiser step.
  * params, m, v: float [param_count], updated in place (RMSprop: v holds its nu, m is unused and
  * may be NULL). step: HOST int32, 1-based count of
  * updates done so far (incremented). perm: int32 [update_epochs, T*E] (PPO; NULL for IMPALA).
- * stats: float [n_updates, 8] rows [L, policy, value, entropy, approx_kl or mean pg_adv,
+ * stats: float [n_updates, 8] (n_updates = update_epochs * num_minibatches for PPO,
+ * num_minibatches for IMPALA) rows [L, policy, value, entropy, approx_kl or mean pg_adv,
  * clipfrac or mean vs, pre-clip grad norm, nonfinite]. */
 impala_status_t learner_step(const impala_net_t* net, const learner_cfg_t* cfg,
                              const rollout_t* rollout, float* params, float* m, float* v,

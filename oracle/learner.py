@@ -54,34 +54,45 @@ def ppo_learner_step(net, cfg, ro, params, m, v, step, perm, prec="fp64"):
 
 
 def impala_learner_step(net, cfg, ro, params, m, v, step, prec="fp64"):
-    """Forward over the T*E rollout frames plus E bootstrap frames (rows T*E..), V-trace from
-    the current policy's log-probs and values (constants), IMPALA loss, backward over the
-    T*E rollout rows (the bootstrap rows get zero gradient), clip, optimiser step.
+    """num_minibatches updates, minibatch k being the env block [k*E/N, (k+1)*E/N) over all T
+    steps (V-trace runs along time, so a minibatch keeps whole trajectories). Each update:
+    forward over the block's T*Eb rollout frames plus its Eb bootstrap frames, V-trace from the
+    current policy's log-probs and values (constants), IMPALA loss, backward over the rollout
+    rows (the bootstrap rows get zero gradient), clip, optimiser step.
 
-    ro: obs [(T+1)*E, H, W, C] u8, actions [T*E], logp [T*E] (behaviour mu), rewards, dones
-    [T, E], next_done [E].
+    ro: obs [(T+1)*E, H, W, C] u8 (row t*E + e; rows T*E.. are the bootstrap frames), actions
+    [T*E], logp [T*E] (behaviour mu), rewards, dones [T, E], next_done [E].
     """
     dtype = np.float64 if prec == "fp64" else np.float32
     T, E = ro["rewards"].shape
-    n = T * E
+    nmb = getattr(cfg, "num_minibatches", 1) or 1
+    if E % nmb:
+        raise ValueError("IMPALA minibatches split the envs evenly")
+    Eb = E // nmb
     p, m_, v_ = (np.asarray(a, dtype) for a in (params, m, v))
-    z, val, cache = netmod.forward(net, p, ro["obs"], prec)
-    tlogp = losses.log_softmax(z[:n])[np.arange(n), ro["actions"]]
-    vs, pg_adv = targets.vtrace(ro["logp"].reshape(T, E), tlogp.reshape(T, E), ro["rewards"],
-                                val[:n].reshape(T, E), ro["dones"], val[n:], ro["next_done"],
-                                cfg.gamma, cfg.lam, cfg.rho_bar, cfg.c_bar, cfg.pg_rho_bar, dtype)
-    _, dz, dv, st = losses.impala_loss_grad(z[:n], val[:n], ro["actions"], vs.ravel(),
-                                            pg_adv.ravel(), cfg.pg_coef, cfg.vf_coef,
-                                            cfg.ent_coef, dtype)
-    dz_all = np.zeros_like(z)
-    dz_all[:n] = dz
-    dv_all = np.zeros_like(val)
-    dv_all[:n] = dv
-    g = netmod.backward(net, cache, dz_all, dv_all)
-    step += 1
-    p, m_, v_, gn = _opt_update(p, g, m_, v_, step, cfg, dtype)
-    stats = np.array([list(st[:6]) + [gn, float(not np.isfinite(gn))]])
-    return p, m_, v_, step, stats
+    out = []
+    for k in range(nmb):
+        envs = np.arange(k * Eb, (k + 1) * Eb)
+        rows = (np.arange(T + 1)[:, None] * E + envs[None, :]).ravel()   # (t, e) order, t = T: bootstrap
+        n = T * Eb
+        z, val, cache = netmod.forward(net, p, ro["obs"][rows], prec)
+        act = ro["actions"][rows[:n]]
+        tlogp = losses.log_softmax(z[:n])[np.arange(n), act]
+        vs, pg_adv = targets.vtrace(ro["logp"][rows[:n]].reshape(T, Eb), tlogp.reshape(T, Eb),
+                                    ro["rewards"][:, envs], val[:n].reshape(T, Eb), ro["dones"][:, envs],
+                                    val[n:], ro["next_done"][envs], cfg.gamma, cfg.lam, cfg.rho_bar,
+                                    cfg.c_bar, cfg.pg_rho_bar, dtype)
+        _, dz, dv, st = losses.impala_loss_grad(z[:n], val[:n], act, vs.ravel(), pg_adv.ravel(),
+                                                cfg.pg_coef, cfg.vf_coef, cfg.ent_coef, dtype)
+        dz_all = np.zeros_like(z)
+        dz_all[:n] = dz
+        dv_all = np.zeros_like(val)
+        dv_all[:n] = dv
+        g = netmod.backward(net, cache, dz_all, dv_all)
+        step += 1
+        p, m_, v_, gn = _opt_update(p, g, m_, v_, step, cfg, dtype)
+        out.append(list(st[:6]) + [gn, float(not np.isfinite(gn))])
+    return p, m_, v_, step, np.array(out)
 
 
 def actor_step(net, params, obs, gumbel, prec="fp64"):

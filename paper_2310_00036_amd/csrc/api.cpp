@@ -48,6 +48,7 @@ bool valid_prec(int p) { return p == IMPALA_PREC_BF16 || p == IMPALA_PREC_FP32; 
 struct LearnerLayout {
     NetPlan plan;
     size_t cnn, adv, ret, tlogp, logits, value, dlogits, dvalue, grads, apart;
+    size_t rows, gact, gmu, grew, gdone, gnd;   // IMPALA minibatch gathers (more than one)
     size_t total;
     int64_t fwd_rows, mb;
 };
@@ -65,6 +66,9 @@ std::string check_cfg(const learner_cfg_t* c) {
             return "PPO needs update_epochs, num_minibatches, minibatch_size >= 1";
         if (int64_t(c->num_minibatches) * c->minibatch_size > int64_t(c->T) * c->E)
             return "num_minibatches * minibatch_size exceeds T * E";
+    } else {
+        if (c->num_minibatches < 1 || c->E % c->num_minibatches)
+            return "IMPALA needs num_minibatches >= 1 dividing E (minibatches are env blocks)";
     }
     if (c->optimizer != LEARNER_OPT_ADAM && c->optimizer != LEARNER_OPT_RMSPROP)
         return "cfg.optimizer must be ADAM or RMSPROP";
@@ -81,8 +85,10 @@ LearnerLayout learner_layout(const impala_net_t& net, const learner_cfg_t& c) {
     LearnerLayout L;
     const int64_t TE = int64_t(c.T) * c.E;
     const int A = net.num_actions;
-    L.mb = c.algo == LEARNER_PPO ? c.minibatch_size : TE;
-    L.fwd_rows = c.algo == LEARNER_PPO ? c.minibatch_size : TE + c.E;
+    const int nmb = c.algo == LEARNER_PPO ? 1 : c.num_minibatches;
+    const int64_t Eb = c.E / nmb;   // IMPALA: envs per minibatch
+    L.mb = c.algo == LEARNER_PPO ? c.minibatch_size : int64_t(c.T) * Eb;
+    L.fwd_rows = c.algo == LEARNER_PPO ? c.minibatch_size : int64_t(c.T) * Eb + Eb;
     L.plan = make_plan(net, c.prec, L.fwd_rows, 1);
     size_t off = 0;
     auto take = [&](size_t bytes) { const size_t o = off; off += a256(bytes); return o; };
@@ -96,6 +102,13 @@ LearnerLayout learner_layout(const impala_net_t& net, const learner_cfg_t& c) {
     L.dvalue = take(size_t(L.mb) * sizeof(float));
     L.grads = take(size_t(L.plan.po.total) * sizeof(float));
     L.apart = take(adam_partial_floats(L.plan.po.total) * sizeof(float));
+    const bool gather = c.algo == LEARNER_IMPALA && nmb > 1;
+    L.rows = take(gather ? size_t(L.fwd_rows) * sizeof(int32_t) : 0);
+    L.gact = take(gather ? size_t(L.mb) * sizeof(int32_t) : 0);
+    L.gmu = take(gather ? size_t(L.mb) * sizeof(float) : 0);
+    L.grew = take(gather ? size_t(L.mb) * sizeof(float) : 0);
+    L.gdone = take(gather ? size_t(L.mb) : 0);
+    L.gnd = take(gather ? size_t(Eb) : 0);
     L.total = off;
     return L;
 }
@@ -440,22 +453,41 @@ impala_status_t learner_step(const impala_net_t* net, const learner_cfg_t* cfg,
             }
         }
     } else {
+        // minibatch k: the env block [k*Eb, (k+1)*Eb) over all T steps plus its bootstrap frames
         float* tlogp = reinterpret_cast<float*>(w + L.tlogp);
         float* vs = reinterpret_cast<float*>(w + L.adv);
         float* pg = reinterpret_cast<float*>(w + L.ret);
-        const int64_t n1 = TE + c.E;
-        LS_TRY(run_forward(P, params, ro->obs, nullptr, n1, cnn, logits, value, stream),
-               "learner_step: forward");
-        LS_TRY(action_logp(TE, A, logits, ro->actions, tlogp, stream), "learner_step: logp");
-        LS_TRY(vtrace(c.T, c.E, ro->behav_logp, tlogp, ro->rewards, value, ro->dones, value + TE,
-                      ro->next_done, c.gamma, c.lambda, c.rho_bar, c.c_bar, c.pg_rho_bar, vs, pg, stream),
-               "learner_step: vtrace");
-        LS_TRY(impala_loss(TE, A, logits, value, ro->actions, vs, pg, c.pg_coef, c.vf_coef, c.ent_coef,
-                           dlogits, dvalue, stats, stream), "learner_step: impala loss");
-        LS_TRY(run_backward(P, params, ro->obs, nullptr, TE, cnn, dlogits, dvalue, grads, stream),
-               "learner_step: backward");
-        *step += 1;
-        LS_TRY(opt_step(stats + 6), "learner_step: optimiser");
+        const int nmb = c.num_minibatches, Eb = c.E / nmb;
+        const int64_t n = int64_t(c.T) * Eb, n1 = n + Eb;
+        for (int k = 0; k < nmb; ++k) {
+            const int32_t* rows = nullptr;
+            const int32_t* act = ro->actions;
+            const float* mu = ro->behav_logp;
+            const float* rw = ro->rewards;
+            const uint8_t* dn = ro->dones;
+            const uint8_t* nd = ro->next_done;
+            if (nmb > 1) {
+                EnvBlock b{reinterpret_cast<int32_t*>(w + L.rows), reinterpret_cast<int32_t*>(w + L.gact),
+                           reinterpret_cast<float*>(w + L.gmu), reinterpret_cast<float*>(w + L.grew),
+                           reinterpret_cast<uint8_t*>(w + L.gdone), reinterpret_cast<uint8_t*>(w + L.gnd)};
+                LS_TRY(env_block_gather(c.T, c.E, k * Eb, Eb, ro->actions, ro->behav_logp, ro->rewards, ro->dones,
+                                        ro->next_done, b, stream), "learner_step: minibatch gather");
+                rows = b.rows; act = b.act; mu = b.mu; rw = b.r; dn = b.d; nd = b.nd;
+            }
+            LS_TRY(run_forward(P, params, ro->obs, rows, n1, cnn, logits, value, stream),
+                   "learner_step: forward");
+            LS_TRY(action_logp(n, A, logits, act, tlogp, stream), "learner_step: logp");
+            LS_TRY(vtrace(c.T, Eb, mu, tlogp, rw, value, dn, value + n, nd, c.gamma, c.lambda, c.rho_bar, c.c_bar,
+                          c.pg_rho_bar, vs, pg, stream),
+                   "learner_step: vtrace");
+            LS_TRY(impala_loss(n, A, logits, value, act, vs, pg, c.pg_coef, c.vf_coef, c.ent_coef, dlogits, dvalue,
+                               stats + 8 * k, stream),
+                   "learner_step: impala loss");
+            LS_TRY(run_backward(P, params, ro->obs, rows, n, cnn, dlogits, dvalue, grads, stream),
+                   "learner_step: backward");
+            *step += 1;
+            LS_TRY(opt_step(stats + 8 * k + 6), "learner_step: optimiser");
+        }
     }
 #undef LS_TRY
     return ok();

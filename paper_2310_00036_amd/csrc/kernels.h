@@ -190,6 +190,13 @@ hipError_t ppo_loss(int64_t m, int A, const float* z, const float* v, const int3
 hipError_t impala_loss(int64_t m, int A, const float* z, const float* v, const int32_t* act,
                        const float* vs, const float* pg, float pgc, float vf, float ent,
                        float* dz, float* dv, float* stats, hipStream_t s);
+// IMPALA minibatch gather (env block [e0, e0 + Eb) of a [T, E] rollout): rows [(T+1)*Eb]
+// rollout row indices (the last Eb are the bootstrap frames), act, mu, r, d [T*Eb], nd [Eb].
+struct EnvBlock {
+    int32_t* rows; int32_t* act; float* mu; float* r; uint8_t* d; uint8_t* nd;
+};
+hipError_t env_block_gather(int T, int E, int e0, int Eb, const int32_t* act, const float* mu, const float* r,
+                            const uint8_t* d, const uint8_t* nd, const EnvBlock& b, hipStream_t s);
 hipError_t action_logp(int64_t m, int A, const float* z, const int32_t* act, float* logp,
                        hipStream_t s);
 hipError_t gumbel_max(int64_t m, int A, const float* z, const float* g, int32_t* act,

@@ -141,4 +141,40 @@ hipError_t vtrace(int T, int E, const float* mu, const float* pi, const float* r
     return hipGetLastError();
 }
 
+// ---- IMPALA minibatch k: the env block [e0, e0 + Eb) over all T steps. rows[i] for
+// i = t*Eb + e' is the rollout row t*E + e0 + e' (t = T: the bootstrap frames, rows T*E..);
+// the block's actions, behaviour log-probs, rewards and dones are gathered to [T, Eb], and
+// its next_done to [Eb].
+__global__ __launch_bounds__(256) void env_block_gather_kernel(int T, int E, int e0, int Eb,
+                                                               const int32_t* __restrict__ act,
+                                                               const float* __restrict__ mu,
+                                                               const float* __restrict__ r,
+                                                               const uint8_t* __restrict__ d,
+                                                               const uint8_t* __restrict__ nd,
+                                                               EnvBlock b) {
+    const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= int64_t(T + 1) * Eb) return;
+    const int t = int(i / Eb), e = e0 + int(i - int64_t(t) * Eb);
+    const int64_t src = int64_t(t) * E + e;
+    b.rows[i] = int32_t(src);
+    if (t < T) {
+        b.act[i] = act[src];
+        b.mu[i] = mu[src];
+        b.r[i] = r[src];
+        b.d[i] = d[src];
+    } else {
+        b.nd[i - int64_t(T) * Eb] = nd[e];
+    }
+}
+
+hipError_t env_block_gather(int T, int E, int e0, int Eb, const int32_t* act, const float* mu, const float* r,
+                            const uint8_t* d, const uint8_t* nd, const EnvBlock& b, hipStream_t s) {
+    const int64_t n = int64_t(T + 1) * Eb;
+    if (n <= 0) return hipSuccess;
+    ProfScope ps(s, [&] { return "env_block_gather/" + cb_dims(T, Eb); });
+    hipLaunchKernelGGL(env_block_gather_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, T, E, e0, Eb, act,
+                       mu, r, d, nd, b);
+    return hipGetLastError();
+}
+
 }  // namespace cb

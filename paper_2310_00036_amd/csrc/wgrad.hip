@@ -305,14 +305,22 @@ struct WgTr {
     static constexpr int NB = U8 ? 3 : 9 * CIN / 16;                  // weight column blocks
     static constexpr int NBB = NB + 1;                                 // + the bias block
     static constexpr int TILES = MT * NBB;
-    // waves splitting k: as many as leave each wave at most 12 accumulator tiles
-    static constexpr int kw_fits(int kw) { return (4 / kw) % MT == 0 && (NBB + (4 / kw) / MT - 1) / ((4 / kw) / MT) <= 12; }
+    // Row blocks per wave. One row block each while a wave's column blocks fit in 12
+    // accumulator tiles; with 64 output channels and at least 32 input channels (19 or 37
+    // column blocks) a wave keeps all four row blocks of a quarter of the column blocks, so
+    // one B fragment read from LDS feeds four MFMAs (accumulators in AGPRs, one wave per SIMD).
+    static constexpr int MTW = (MT == 4 && NBB > 12) ? 4 : 1;
+    static constexpr int MTG = MT / MTW;                               // row-block groups
+    // waves splitting k: as many as leave each wave at most 12 accumulator tiles (MTW = 1)
+    static constexpr int kw_fits(int kw) {
+        return MTW > 1 ? kw == 1 : ((4 / kw) % MT == 0 && (NBB + (4 / kw) / MT - 1) / ((4 / kw) / MT) <= 12);
+    }
     static constexpr int KW = kw_fits(4) ? 4 : (kw_fits(2) ? 2 : 1);
     static constexpr int TG = 4 / KW;                                  // waves splitting tiles
-    static constexpr int NPW = TG / MT;                                // waves per row block
+    static constexpr int NPW = TG / MTG;                               // waves per row-block group
     static constexpr int TPW = (NBB + NPW - 1) / NPW;                  // column blocks per wave
     static constexpr int PSTRIDE = TILES * 256;                        // floats per partial
-    static_assert(TG % MT == 0, "row blocks spread over whole wave groups");
+    static_assert(TG % MTG == 0, "row-block groups spread over whole wave groups");
 };
 
 struct WgTrRun {
@@ -324,8 +332,8 @@ struct WgTrRun {
 template <int CIN, int COUT, int MODE>
 __global__ __launch_bounds__(256) void wgrad_tr_kernel(WgradArgs a, WgTrRun t) {
     using D = WgTr<CIN, COUT, MODE>;
-    constexpr int XPB = D::XPB, DPB = D::DPB, MT = D::MT, NB = D::NB, NBB = D::NBB;
-    constexpr int KW = D::KW, TG = D::TG, NPW = D::NPW, TPW = D::TPW;
+    constexpr int XPB = D::XPB, DPB = D::DPB, NB = D::NB, NBB = D::NBB;
+    constexpr int KW = D::KW, TG = D::TG, NPW = D::NPW, TPW = D::TPW, MTW = D::MTW, MTG = D::MTG;
     constexpr bool U8 = D::U8;
     constexpr int XSL = XPB / 16, DSL = DPB / 16;   // 16-byte DMA slots per pixel
 
@@ -338,7 +346,7 @@ __global__ __launch_bounds__(256) void wgrad_tr_kernel(WgradArgs a, WgTrRun t) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, r16 = lane & 15, jj = r16 >> 2, m = r16 & 3;
     const int kgrp = wave % KW, tgrp = wave / KW;
-    const int mt = tgrp % MT, nbw = tgrp / MT;
+    const int mt0 = (tgrp % MTG) * MTW, nbw = tgrp / MTG;   // row blocks mt0 .. mt0+MTW-1
     const int H = a.H, W = a.W, TH = t.TH, FR = t.FR;
     const int TW = W + 2, TR = TH + 2;
 
@@ -354,9 +362,11 @@ __global__ __launch_bounds__(256) void wgrad_tr_kernel(WgradArgs a, WgTrRun t) {
         const int ci = U8 ? 0 : (nb % (CIN / 16 > 0 ? CIN / 16 : 1)) * 16 + 4 * m;
         boff[i] = (nb < NB && tap < 9) ? ((tap / 3) * TW + tap % 3) * XPB + ci * 2 : -1;
     }
-    cb_f32x4 acc[TPW];
+    cb_f32x4 acc[TPW][MTW];
 #pragma unroll
-    for (int i = 0; i < TPW; ++i) acc[i] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < TPW; ++i)
+#pragma unroll
+        for (int w = 0; w < MTW; ++w) acc[i][w] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
     const uint4 ones = make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
 
     int lg = blockIdx.x;   // neighbouring tiles (which share halo rows) on one XCD
@@ -438,7 +448,7 @@ __global__ __launch_bounds__(256) void wgrad_tr_kernel(WgradArgs a, WgTrRun t) {
         const int nks = (npx + 31) >> 5;
 #pragma unroll 2
         for (int ks = kgrp; ks < nks; ks += KW) {
-            uint2 av[2];
+            uint2 av[2][MTW];
             int bp[2];
 #pragma unroll
             for (int half = 0; half < 2; ++half) {
@@ -448,9 +458,13 @@ __global__ __launch_bounds__(256) void wgrad_tr_kernel(WgradArgs a, WgTrRun t) {
                 const int rowi = qdiv(qc, t.inv_W), col = qc - rowi * W;
                 const int f = qdiv(rowi, t.inv_TH), r = rowi - f * TH;
                 bp[half] = ((f * TR + r) * TW + col) * XPB;
-                av[half] = lds_read_tr16(ok ? dyt + q * DPB + (mt * 16 + 4 * m) * 2 : zero);
+#pragma unroll
+                for (int w = 0; w < MTW; ++w)
+                    av[half][w] = lds_read_tr16(ok ? dyt + q * DPB + ((mt0 + w) * 16 + 4 * m) * 2 : zero);
             }
-            const uint4 af = make_uint4(av[0].x, av[0].y, av[1].x, av[1].y);
+            uint4 af[MTW];
+#pragma unroll
+            for (int w = 0; w < MTW; ++w) af[w] = make_uint4(av[0][w].x, av[0][w].y, av[1][w].x, av[1][w].y);
 #pragma unroll
             for (int i = 0; i < TPW; ++i) {
                 const int nb = nbw + NPW * i;
@@ -461,22 +475,23 @@ __global__ __launch_bounds__(256) void wgrad_tr_kernel(WgradArgs a, WgTrRun t) {
                     const uint2 hi = lds_read_tr16(boff[i] >= 0 ? win + bp[1] + boff[i] : zero);
                     bf = make_uint4(lo.x, lo.y, hi.x, hi.y);
                 }
-                acc[i] = PrecBF16::mma(af, bf, acc[i]);
+#pragma unroll
+                for (int w = 0; w < MTW; ++w) acc[i][w] = PrecBF16::mma(af[w], bf, acc[i][w]);
             }
         }
     }
 
     // ---- this workgroup's partial: [mt*NBB + nb][row 16][col 16]
-    if constexpr (KW > 1) {
+    if constexpr (KW > 1) {   // (MTW == 1 here)
         __syncthreads();   // tile LDS is free
         cb_f32x4* red = reinterpret_cast<cb_f32x4*>(smem);   // [KW][TG][TPW][64]
 #pragma unroll
-        for (int i = 0; i < TPW; ++i) red[((kgrp * TG + tgrp) * TPW + i) * 64 + lane] = acc[i];
+        for (int i = 0; i < TPW; ++i) red[((kgrp * TG + tgrp) * TPW + i) * 64 + lane] = acc[i][0];
         __syncthreads();
         if (kgrp == 0) {
 #pragma unroll
             for (int i = 0; i < TPW; ++i)
-                for (int k = 1; k < KW; ++k) acc[i] += red[((k * TG + tgrp) * TPW + i) * 64 + lane];
+                for (int k = 1; k < KW; ++k) acc[i][0] += red[((k * TG + tgrp) * TPW + i) * 64 + lane];
         }
     }
     if (kgrp == 0) {
@@ -486,7 +501,10 @@ __global__ __launch_bounds__(256) void wgrad_tr_kernel(WgradArgs a, WgTrRun t) {
             const int nb = nbw + NPW * i;
             if (nb < NBB) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) part[(mt * NBB + nb) * 256 + (4 * g + e) * 16 + r16] = acc[i][e];
+                for (int w = 0; w < MTW; ++w)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        part[((mt0 + w) * NBB + nb) * 256 + (4 * g + e) * 16 + r16] = acc[i][w][e];
             }
         }
     }
@@ -592,12 +610,13 @@ constexpr int kWgTrPixMax = 2048;
 
 static int wg_tr_parts_cap(size_t pstride) {
     const size_t cap = kWgTrPartBytes / (pstride * sizeof(float));
-    return int(cap < 256 ? 256 : (cap > 1024 ? 1024 : cap));
+    return int(cap < 256 ? 256 : (cap > 1024 ? 1024 : cap));   // at least one workgroup per CU
 }
 
 // Channel pairs the transpose-read kernel takes (its accumulators fit in registers).
 static bool wg_tr_ok(int cin, int cout) {
-    return cin == 4 || (cin == 16 && (cout == 16 || cout == 32 || cout == 64)) || (cin == 32 && cout == 32);
+    return cin == 4 || (cin == 16 && (cout == 16 || cout == 32 || cout == 64)) ||
+           (cin == 32 && (cout == 32 || cout == 64)) || (cin == 64 && cout == 64);
 }
 static size_t wg_tr_pstride(int cin, int cout) {
     const int nb = cin == 4 ? 3 : 9 * cin / 16;
@@ -621,8 +640,10 @@ hipError_t wg_tr_launch(const WgradArgs& a, hipStream_t s) {
         return size_t(16 + raw + win + dyb);
     };
     const size_t limit = std::min<size_t>(lds_limit(), 160 * 1024);
+    // four row blocks per wave hold one workgroup per CU: it may use most of the CU's LDS
+    const size_t budget = D::MTW > 1 ? std::min<size_t>(limit, 144 * 1024) : size_t(kWgTrLds);
     int thmax = std::min(H, std::max(1, kWgTrPixMax / W));
-    while (thmax > 1 && lds(thmax, 1) > size_t(kWgTrLds)) --thmax;
+    while (thmax > 1 && lds(thmax, 1) > budget) --thmax;
     if (lds(thmax, 1) > limit) return hipErrorInvalidValue;
     int TH = 1, best = 1 << 30;
     for (int th = 1; th <= thmax; ++th) {
@@ -632,7 +653,7 @@ hipError_t wg_tr_launch(const WgradArgs& a, hipStream_t s) {
     const int nbands = (H + TH - 1) / TH;
     int FR = 1;
     if (nbands == 1 && !D::U8)
-        while (FR < a.n && lds(TH, FR + 1) <= size_t(kWgTrLds) && (FR + 1) * H * W <= kWgTrPixMax) ++FR;
+        while (FR < a.n && lds(TH, FR + 1) <= budget && (FR + 1) * H * W <= kWgTrPixMax) ++FR;
     if (int64_t(FR) * H * W * std::max(CIN, COUT) * 2 >= (int64_t(1) << 31)) return hipErrorInvalidValue;
     WgTrRun r{};
     r.TH = TH; r.FR = FR; r.nbands = nbands; r.ntiles = nbands * ((a.n + FR - 1) / FR);
@@ -666,7 +687,8 @@ hipError_t wg_dispatch(int cin, int cout, int mode, const WgradArgs& a, hipStrea
         if (cin == CI && cout == CO && mode == MD) return wg_tr_launch<CI, CO, MD>(a, s);
         CB_WGT(4, 16, IN_U8) CB_WGT(4, 32, IN_U8) CB_WGT(4, 64, IN_U8)
         CB_WGT(16, 16, IN_PLAIN) CB_WGT(16, 32, IN_PLAIN) CB_WGT(16, 64, IN_PLAIN) CB_WGT(32, 32, IN_PLAIN)
-        CB_WGT(16, 16, IN_RELU) CB_WGT(32, 32, IN_RELU)
+        CB_WGT(32, 64, IN_PLAIN) CB_WGT(64, 64, IN_PLAIN)
+        CB_WGT(16, 16, IN_RELU) CB_WGT(32, 32, IN_RELU) CB_WGT(64, 64, IN_RELU)
 #undef CB_WGT
     }
 #define CB_WG(CI, CO, MD) \

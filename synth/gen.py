@@ -72,7 +72,7 @@ class Workload:
 
     @property
     def n_updates(self) -> int:
-        return self.epochs * self.num_minibatches if self.algo == "ppo" else 1
+        return self.epochs * self.num_minibatches if self.algo == "ppo" else self.num_minibatches
 
     def replace(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)
@@ -96,6 +96,15 @@ WORKLOADS = {
     # Widened learner: (32,64,64)/512, 128 envs x 128 steps, one minibatch of 8192.
     4: Workload("ppo_wide_128x128_mb8192", "ppo", T=128, E=128, net=WIDE_NET, epochs=1,
                 num_minibatches=1, minibatch_size=8192, seed=4),
+    # The paper's PPO shape (Appendix B, PPO table): 128 envs x 128 steps, 4 minibatches of
+    # 4096, 4 epochs (16 updates); fixed learning rate (no annealing).
+    5: Workload("ppo_paper_128x128_mb4096x4_e4", "ppo", T=128, E=128, epochs=4, num_minibatches=4,
+                seed=5),
+    # The paper's IMPALA shape (Appendix B, IMPALA table): 128 envs x 20 steps, 4 minibatches
+    # of 32 envs, RMSprop (decay 0.99, eps 0.01), lr 6e-4, omega 40.
+    6: Workload("impala_paper_128x20_mb4", "impala", T=20, E=128, num_minibatches=4, lam=1.0, lr=6e-4,
+                max_grad_norm=40.0, optimizer="rmsprop", behav_logp_noise=0.0, behav_logit_noise=0.3,
+                seed=6),
 }
 
 

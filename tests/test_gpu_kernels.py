@@ -30,6 +30,7 @@ CONV_CASES = [
     (3, 42, 42, 16, 16, P.X_RELU), (3, 42, 42, 16, 32, P.X_PLAIN), (2, 21, 21, 32, 32, P.X_PLAIN),
     (5, 21, 21, 32, 32, P.X_RELU), (7, 11, 11, 32, 32, P.X_RELU), (3, 42, 42, 32, 64, P.X_PLAIN),
     (3, 21, 21, 64, 64, P.X_RELU), (5, 11, 11, 64, 64, P.X_PLAIN), (2, 17, 23, 16, 64, P.X_PLAIN),
+    (4, 9, 13, 32, 64, P.X_PLAIN), (6, 7, 5, 64, 64, P.X_RELU),
 ]
 
 

@@ -23,7 +23,7 @@ import pytest
 
 pytestmark = pytest.mark.gpu
 
-from oracle import learner as olearner, losses as olosses, net as onet  # noqa: E402
+from oracle import learner as olearner, losses as olosses, net as onet, targets as otargets  # noqa: E402
 from synth import NetShape, Workload, WORKLOADS, draw_params, draw_rollout, draw_actor_batch  # noqa: E402
 from tests import certify, gpu_util as G  # noqa: E402
 
@@ -336,10 +336,61 @@ def test_learner_step_impala_rmsprop(prec):
     _compare_learner(wl, prec, params.astype(np.float64), got, want, "impala-rmsprop", "B", emu)
 
 
-def _c1_like_inputs(seed=1):
-    """PPO 64 x 128 rollout with minibatches of 2048 (Cleanba-like shape); behaviour data
-    are drawn without the network (this test compares GPU against GPU)."""
-    wl = WORKLOADS[1]
+@pytest.mark.parametrize("prec", [G.BF16, G.FP32], ids=lambda p: PNAME[p])
+def test_learner_step_impala_env_block_minibatches(prec):
+    """Tier B: Appendix B's IMPALA setting (4 minibatches = env blocks, RMSprop decay 0.99 /
+    eps 0.01, omega 40) on 8 envs x 5 steps: four updates against the oracle's. With 10 rows
+    per minibatch the paper's lr (6e-4) drives the network into a different regime by the
+    third update depending on rounding (all ReLUs dead in float64, not in bf16), so this
+    small case runs at lr 1e-5, where four updates stay comparable."""
+    wl = WORKLOADS[6].replace(T=5, E=8, seed=24, lr=1e-5)
+    params = draw_params(wl.net, wl.seed)
+    raw = draw_rollout(wl)
+    ro = olearner.behaviour_rollout(wl, params, raw)
+    want, emu = _oracle_learner(wl, params, ro, None, prec)
+    got = _learner_gpu(wl, prec, params, ro, None)
+    assert got[4].shape == (4, 8)
+    _compare_learner(wl, prec, params.astype(np.float64), got, want, "impala-mb", "B", emu)
+
+
+def test_paper_impala_shape_first_update_matches_oracle():
+    """The paper's IMPALA shape (128 envs x 20 steps, 4 minibatches of 32 envs, RMSprop): the
+    first update's loss statistics, taken at the initial parameters over env block 0 (672
+    frames with its bootstrap frames), against the oracle's; fp32 mode. All four updates'
+    statistics finite. Behaviour data are drawn without the network."""
+    wl = WORKLOADS[6]
+    T, E, A = wl.T, wl.E, wl.net.num_actions
+    raw = draw_rollout(wl)
+    rng = np.random.default_rng(60)
+    ro = dict(obs=raw["obs"].reshape((T + 1) * E, 84, 84, 4), actions=rng.integers(0, A, T * E).astype(np.int32),
+              logp=(np.log(1.0 / A) + 0.3 * rng.standard_normal(T * E)).astype(np.float32),
+              rewards=raw["rewards"], dones=raw["dones"], next_done=raw["next_done"])
+    params = draw_params(wl.net, wl.seed)
+    got = _learner_gpu(wl, G.FP32, params, ro, None)
+    s = G.host(got[4])
+    assert s.shape == (4, 8) and np.isfinite(s).all() and (s[:, 7] == 0).all()
+    # the oracle's first update, up to its statistics (a forward over block 0 at params p0)
+    Eb = E // 4
+    envs = np.arange(Eb)
+    rows = (np.arange(T + 1)[:, None] * E + envs[None, :]).ravel()
+    n = T * Eb
+    z, val, _ = onet.forward(wl.net, params, ro["obs"][rows])
+    act = ro["actions"][rows[:n]]
+    tlogp = olosses.log_softmax(z[:n])[np.arange(n), act]
+    vs, pg = otargets.vtrace(ro["logp"][rows[:n]].reshape(T, Eb), tlogp.reshape(T, Eb), ro["rewards"][:, envs],
+                             val[:n].reshape(T, Eb), ro["dones"][:, envs], val[n:], ro["next_done"][envs],
+                             wl.gamma, wl.lam, wl.rho_bar, wl.c_bar, wl.pg_rho_bar)
+    _, _, _, st = olosses.impala_loss_grad(z[:n], val[:n], act, vs.ravel(), pg.ravel(), wl.pg_coef, wl.vf_coef,
+                                           wl.ent_coef)
+    for col in range(6):
+        assert abs(s[0, col] - st[col]) <= 1e-4 * (abs(st[col]) + 1e-2), (col, s[0, col], st[col])
+
+
+def _c1_like_inputs(seed=1, wid=1):
+    """PPO rollout of workload `wid` (default: 64 x 128 with minibatches of 2048, the
+    Cleanba-like shape); behaviour data are drawn without the network (the tests using it
+    compare GPU against GPU)."""
+    wl = WORKLOADS[wid]
     raw = draw_rollout(wl)
     rng = np.random.default_rng(seed)
     T, E, A = wl.T, wl.E, wl.net.num_actions
@@ -369,12 +420,16 @@ def test_learner_step_is_deterministic_and_resumable():
         assert torch.equal(x, y)
 
 
-def test_learner_step_equals_its_abi_calls():
+@pytest.mark.parametrize("wid", [1, 5], ids=["cleanba_like_2_updates", "paper_ppo_shape_16_updates"])
+def test_learner_step_equals_its_abi_calls(wid):
     """learner_step (PPO) is exactly GAE, then per minibatch impala_cnn_fwd with the permuted
-    rows, ppo_loss_grad on the gathered rows, impala_cnn_bwd and adam_step."""
+    rows, ppo_loss_grad on the gathered rows, impala_cnn_bwd and adam_step: two updates of the
+    Cleanba-like shape, and all 16 updates of the paper's shape (128 envs x 128 steps, 4
+    minibatches of 4096, 4 epochs)."""
     torch = G.torch()
-    wl, params, ro, perm = _c1_like_inputs()
-    wl = wl.replace(epochs=1, num_minibatches=2)
+    wl, params, ro, perm = _c1_like_inputs(wid=wid)
+    if wid == 1:
+        wl = wl.replace(epochs=1, num_minibatches=2)
     net, prec = wl.net, G.BF16
     got = _learner_gpu(wl, prec, params, ro, perm)
     d = _gpu_rollout(ro, wl)

@@ -84,6 +84,36 @@ def test_impala_learner_runs_and_moves_params(tiny_net):
     assert moved.max() <= 6e-4 * 1.0001
 
 
+def test_impala_minibatches_are_env_blocks_in_order(tiny_net):
+    """N IMPALA minibatches are N updates on the env blocks of the rollout, one after the
+    other: equal to single-minibatch learner steps on each block's own sub-rollout (its
+    trajectories and bootstrap frames), chained through params and optimiser state."""
+    from synth import Workload
+    wl = Workload("tiny_impala_mb", "impala", T=4, E=4, net=tiny_net, num_minibatches=2, lam=1.0,
+                  lr=6e-4, max_grad_norm=40.0, optimizer="rmsprop", behav_logp_noise=0.0,
+                  behav_logit_noise=0.3, seed=9)
+    p0 = draw_params(wl.net, 5).astype(np.float64)
+    raw = draw_rollout(wl)
+    ro = learner.behaviour_rollout(wl, p0, raw)
+    z = np.zeros_like(p0)
+    got = learner.impala_learner_step(wl.net, wl, ro, p0, z, z, 0)
+    T, E, Eb = wl.T, wl.E, 2
+    state = (p0, z, z, 0)
+    rows_all = []
+    for k in range(2):
+        envs = np.arange(k * Eb, (k + 1) * Eb)
+        rows = (np.arange(T + 1)[:, None] * E + envs[None, :]).ravel()
+        sub = dict(obs=ro["obs"][rows], actions=ro["actions"][rows[:T * Eb]], logp=ro["logp"][rows[:T * Eb]],
+                   rewards=ro["rewards"][:, envs], dones=ro["dones"][:, envs], next_done=ro["next_done"][envs])
+        out = learner.impala_learner_step(wl.net, wl.replace(E=Eb, num_minibatches=1), sub, *state)
+        state = out[:4]
+        rows_all.append(out[4])
+    assert got[3] == state[3] == 2
+    for x, y in zip(got[:3], state[:3]):
+        np.testing.assert_array_equal(x, y)
+    np.testing.assert_array_equal(got[4], np.concatenate(rows_all))
+
+
 def test_bf16_emulation_floor_on_tiny_ppo_batch():
     """Measure the intrinsic bf16 error floor (bf16-emulating oracle vs float64 oracle) on 8
     Atari-shaped frames with the full-size network. Parity unpinned against the paper.
