@@ -549,6 +549,9 @@ __global__ __launch_bounds__(64 * NW, (conv_min_waves<CIN, COUT, MODE>())) void 
         };
         const int ntl = (npx + 15) >> 4;
         for (int nt0 = wave; nt0 < ntl; nt0 += NW * NP) {
+            // with many weight fragments (more than 18: 64 input channels), those read
+            // from LDS stay inside the loop: hoisted out of it they would all take registers
+            if constexpr (!HOIST && MT * KSTEPS > 18) asm volatile("" ::: "memory");
             int qv[NP], fv[NP], rv[NP], cv[NP];
             const unsigned char* xb[NP];
 #pragma unroll
@@ -736,9 +739,19 @@ constexpr int conv_group() {
 // stages the fewest window rows per frame; whole frames batch up to kDmaPixMax pixels.
 constexpr int kDmaLdsTarget = 40 * 1024;
 constexpr int kDmaPixMax = 2048;
+// Layers whose full weight tile is large (64 output channels from 32 or more inputs) keep all
+// output channels in one 8-wave workgroup per CU, with most of the CU's LDS: every staged
+// window is read once and each weight fragment feeds two column tiles, where 16-channel
+// groups would stage each window once per group and feed one MFMA per fragment pair.
+constexpr int kDmaWideLdsTarget = 150 * 1024;
+template <int CIN, int COUT>
+constexpr bool conv_wide_tile() { return COUT * ConvGeom<PrecBF16, CIN>::KPITCH * 2 > 24 * 1024; }
 
 template <int CIN, int COUT, int MODE, int FLIP>
 hipError_t launch_bf16(const ConvArgs& a, int cout_total, hipStream_t s) {
+    constexpr bool WIDE = conv_wide_tile<CIN, COUT>();
+    constexpr int NW = WIDE ? 8 : 4;
+    const int target = WIDE ? kDmaWideLdsTarget : kDmaLdsTarget;
     using D = DmaGeom<CIN, COUT, MODE>;
     const int H = a.H, W = a.W;
     const int nops = (a.mask ? 1 : 0) + (a.add ? 1 : 0);
@@ -747,7 +760,7 @@ hipError_t launch_bf16(const ConvArgs& a, int cout_total, hipStream_t s) {
     };
     const size_t limit = std::min<size_t>(lds_limit(), 160 * 1024);
     int thmax = std::min(H, std::max(1, kDmaPixMax / W));
-    while (thmax > 1 && lds(thmax, 1) > size_t(kDmaLdsTarget)) --thmax;
+    while (thmax > 1 && lds(thmax, 1) > size_t(target)) --thmax;
     if (lds(thmax, 1) > limit) return hipErrorInvalidValue;
     int TH = 1, best = 1 << 30;
     for (int th = 1; th <= thmax; ++th) {
@@ -757,7 +770,7 @@ hipError_t launch_bf16(const ConvArgs& a, int cout_total, hipStream_t s) {
     const int nbands = (H + TH - 1) / TH;
     int FR = 1;
     if (nbands == 1 && MODE != IN_U8)
-        while (FR < a.n && lds(TH, FR + 1) <= size_t(kDmaLdsTarget) && (FR + 1) * H * W <= kDmaPixMax) ++FR;
+        while (FR < a.n && lds(TH, FR + 1) <= size_t(target) && (FR + 1) * H * W <= kDmaPixMax) ++FR;
     // 32-bit buffer offsets cover FR frames of input and of each operand
     if (int64_t(FR) * H * W * std::max(MODE == IN_U8 ? 2 : CIN, cout_total) * 2 >= (int64_t(1) << 31))
         return hipErrorInvalidValue;
@@ -771,15 +784,15 @@ hipError_t launch_bf16(const ConvArgs& a, int cout_total, hipStream_t s) {
     t.inv_W = 1.f / float(W); t.inv_TW = 1.f / float(W + 2);
     t.inv_TH = 1.f / float(TH); t.inv_TR = 1.f / float(TH + 2);
     const int groups = cout_total / COUT;
-    const void* fn = reinterpret_cast<const void*>(&conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP, 0, 4>);
-    int gx = std::max(1, resident_blocks(fn, 256, L) / groups);
+    const void* fn = reinterpret_cast<const void*>(&conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP, 0, NW>);
+    int gx = std::max(1, resident_blocks(fn, 64 * NW, L) / groups);
     if (gx > ntiles) gx = ntiles;
     const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(groups));
     ProfScope ps(s, [&] {
         return cb_key(FLIP ? "conv_dgrad" : "conv_fwd", 0,
                       cb_dims(CIN, cout_total) + "/" + cb_dims(H, W) + cb_flags(MODE, a.mask, a.add));
     });
-    hipLaunchKernelGGL((conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP, 0, 4>), grid, dim3(256), L, s, a, t);
+    hipLaunchKernelGGL((conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP, 0, NW>), grid, dim3(64 * NW), L, s, a, t);
     return hipGetLastError();
 }
 
@@ -803,15 +816,17 @@ hipError_t launch_bf16_pool(const ConvArgs& a, int cout_total, hipStream_t s) {
         return size_t(D::WLB) + size_t(D::win_bytes(th, fr, W)) + size_t(fr) * th * W * COUT * 2 + 16;
     };
     const size_t limit = std::min<size_t>(lds_limit(), 160 * 1024);
+    // the wide budget only where the weights alone would crowd two workgroups per CU
+    const int target = D::WLB > 40 * 1024 ? kDmaWideLdsTarget : kPoolLdsTarget;
     int pmax = OH;
-    while (pmax > 1 && (lds(pmax, 1) > size_t(kPoolLdsTarget) || cap(pmax, 1) * W > kPoolPixMax)) --pmax;
+    while (pmax > 1 && (lds(pmax, 1) > size_t(target) || cap(pmax, 1) * W > kPoolPixMax)) --pmax;
     if (lds(pmax, 1) > limit) return hipErrorInvalidValue;
     const int nbands0 = (OH + pmax - 1) / pmax;
     const int PTH = (OH + nbands0 - 1) / nbands0;
     const int nbands = (OH + PTH - 1) / PTH;
     int FR = 1;
     if (nbands == 1 && MODE != IN_U8)
-        while (FR < a.n && lds(PTH, FR + 1) <= size_t(kPoolLdsTarget) && (FR + 1) * H * W <= kPoolPixMax) ++FR;
+        while (FR < a.n && lds(PTH, FR + 1) <= size_t(target) && (FR + 1) * H * W <= kPoolPixMax) ++FR;
     const int TH = cap(PTH, FR);
     if (int64_t(FR) * H * W * std::max(MODE == IN_U8 ? 2 : CIN, cout_total) * 2 >= (int64_t(1) << 31))
         return hipErrorInvalidValue;
@@ -843,7 +858,7 @@ hipError_t launch_bf16_pool(const ConvArgs& a, int cout_total, hipStream_t s) {
 template <class P, int CIN, int COUT, int MODE, int FLIP>
 hipError_t launch_split(const ConvArgs& a, hipStream_t s) {
     if constexpr (std::is_same_v<P, PrecBF16>)
-        return launch_bf16<CIN, conv_group<P, CIN, COUT>(), MODE, FLIP>(a, COUT, s);
+        return launch_bf16<CIN, COUT, MODE, FLIP>(a, COUT, s);   // all output channels per workgroup
     else
         return launch<P, CIN, conv_group<P, CIN, COUT>(), MODE, FLIP>(a, COUT, s);
 }
@@ -882,9 +897,11 @@ bool conv3x3_supported(int cin, int cout, int mode, int flip) {
 hipError_t conv3x3_pool(int cin, int cout, int mode, const ConvArgs& a, hipStream_t s) {
     if (a.n <= 0) return hipSuccess;
     if (conv_pool_fast_supported(cin, cout, mode)) return conv_pool_fast(cin, cout, mode, a, s);
+    // all output channels per workgroup from 64 input channels; below that, 16/32-channel
+    // groups (measured faster there: the conv tile shares LDS with the weights)
 #define CB_CP(CI, CO, MD) \
     if (cin == CI && cout == CO && mode == MD) \
-        return launch_bf16_pool<CI, conv_group<PrecBF16, CI, CO>(), MD>(a, CO, s);
+        return launch_bf16_pool<CI, (CI >= 64 ? CO : conv_group<PrecBF16, CI, CO>()), MD>(a, CO, s);
     CB_CP(4, 16, IN_U8) CB_CP(4, 32, IN_U8) CB_CP(4, 64, IN_U8)
     CB_CP(16, 16, IN_PLAIN) CB_CP(16, 32, IN_PLAIN) CB_CP(16, 64, IN_PLAIN)
     CB_CP(32, 32, IN_PLAIN) CB_CP(32, 64, IN_PLAIN) CB_CP(64, 64, IN_PLAIN)
