@@ -148,6 +148,42 @@ def test_cnn_forward_backward_with_gather(prec, netname):
     _check_grads(g, g_w, net, prec, netname, "B", emu)
 
 
+ODD_NETS = {
+    # hidden sizes that are not multiples of the heads' 256-unit chunk, and action counts
+    # without a compile-time head variant (padded to 20 and 68 head columns, or exactly 20)
+    "h300_a3": NetShape(in_h=12, in_w=10, ch=(16, 16, 32), hidden=300, num_actions=3),
+    "h40_a64": NetShape(in_h=9, in_w=13, ch=(16, 32, 32), hidden=40, num_actions=64),
+    "h513_a19": NetShape(in_h=20, in_w=20, ch=(16, 32, 64), hidden=513, num_actions=19),
+}
+
+
+@pytest.mark.parametrize("prec", [G.BF16, G.FP32], ids=lambda p: PNAME[p])
+@pytest.mark.parametrize("netname", sorted(ODD_NETS))
+def test_cnn_odd_head_shapes(prec, netname):
+    """Tier B on small frames: forward outputs and every parameter gradient of nets whose
+    head shapes take the generic head-kernel paths, 5 gathered frames (a ragged row group)."""
+    net = ODD_NETS[netname]
+    rng = np.random.default_rng(11)
+    params = draw_params(net, 5)
+    obs = rng.integers(0, 256, size=(8, net.in_h, net.in_w, 4), dtype=np.uint8)
+    rows = np.array([6, 1, 3, 7, 0], np.int32)
+    n = len(rows)
+    dz = (rng.standard_normal((n, net.num_actions)) * 0.1).astype(np.float32)
+    dv = rng.standard_normal(n).astype(np.float32)
+    z_w, v_w, cache = onet.forward(net, params, obs[rows], "fp64")
+    g_w = onet.backward(net, cache, dz, dv)
+    emu = None
+    if prec == G.BF16:
+        z_e, v_e, cache_e = onet.forward(net, params, obs[rows], "bf16")
+        emu = onet.backward(net, cache_e, dz, dv)
+        z_w, v_w = z_e, v_e
+    z, v, g = _run_fwd_bwd(net, prec, params, obs, rows, n, dz, dv)
+    tol = FP32_TOL if prec == G.FP32 else BF16_OUT_TOL
+    G.assert_close(z, z_w, tol, "logits")
+    G.assert_close(v, v_w, tol, "value")
+    _check_grads(g, g_w, net, prec, netname, "B", emu)
+
+
 @pytest.mark.parametrize("prec", [G.BF16, G.FP32], ids=lambda p: PNAME[p])
 def test_cnn_full_minibatch_sampled_rows(prec):
     """At the PPO minibatch size (2048 frames) in the launch configuration the learner uses:
