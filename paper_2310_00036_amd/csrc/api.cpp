@@ -49,6 +49,7 @@ struct LearnerLayout {
     NetPlan plan;
     size_t cnn, adv, ret, tlogp, logits, value, dlogits, dvalue, grads, apart;
     size_t rows, gact, gmu, grew, gdone, gnd;   // IMPALA minibatch gathers (more than one)
+    size_t lossws;                               // the loss kernels' statistics and row terms
     size_t total;
     int64_t fwd_rows, mb;
 };
@@ -109,6 +110,7 @@ LearnerLayout learner_layout(const impala_net_t& net, const learner_cfg_t& c) {
     L.grew = take(gather ? size_t(L.mb) * sizeof(float) : 0);
     L.gdone = take(gather ? size_t(L.mb) : 0);
     L.gnd = take(gather ? size_t(Eb) : 0);
+    L.lossws = take(loss_ws_bytes(L.mb));
     L.total = off;
     return L;
 }
@@ -443,9 +445,9 @@ impala_status_t learner_step(const impala_net_t* net, const learner_cfg_t* cfg,
                 const int64_t mb = c.minibatch_size;
                 LS_TRY(run_forward(P, params, ro->obs, rows, mb, cnn, logits, value, stream),
                        "learner_step: forward");
-                LS_TRY(ppo_loss(mb, A, logits, value, ro->actions, ro->behav_logp, adv, ret, rows,
-                                c.norm_adv, c.clip_eps, c.vf_coef, c.ent_coef, dlogits, dvalue,
-                                stats + 8 * u, stream), "learner_step: ppo loss");
+                LS_TRY(ppo_loss_ws(mb, A, logits, value, ro->actions, ro->behav_logp, adv, ret, rows,
+                                   c.norm_adv, c.clip_eps, c.vf_coef, c.ent_coef, dlogits, dvalue,
+                                   stats + 8 * u, w + L.lossws, stream), "learner_step: ppo loss");
                 LS_TRY(run_backward(P, params, ro->obs, rows, mb, cnn, dlogits, dvalue, grads, stream),
                        "learner_step: backward");
                 *step += 1;
@@ -480,8 +482,8 @@ impala_status_t learner_step(const impala_net_t* net, const learner_cfg_t* cfg,
             LS_TRY(vtrace(c.T, Eb, mu, tlogp, rw, value, dn, value + n, nd, c.gamma, c.lambda, c.rho_bar, c.c_bar,
                           c.pg_rho_bar, vs, pg, stream),
                    "learner_step: vtrace");
-            LS_TRY(impala_loss(n, A, logits, value, act, vs, pg, c.pg_coef, c.vf_coef, c.ent_coef, dlogits, dvalue,
-                               stats + 8 * k, stream),
+            LS_TRY(impala_loss_ws(n, A, logits, value, act, vs, pg, c.pg_coef, c.vf_coef, c.ent_coef, dlogits,
+                                  dvalue, stats + 8 * k, w + L.lossws, stream),
                    "learner_step: impala loss");
             LS_TRY(run_backward(P, params, ro->obs, rows, n, cnn, dlogits, dvalue, grads, stream),
                    "learner_step: backward");

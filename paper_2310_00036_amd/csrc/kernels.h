@@ -190,6 +190,16 @@ hipError_t ppo_loss(int64_t m, int A, const float* z, const float* v, const int3
 hipError_t impala_loss(int64_t m, int A, const float* z, const float* v, const int32_t* act,
                        const float* vs, const float* pg, float pgc, float vf, float ent,
                        float* dz, float* dv, float* stats, hipStream_t s);
+// The same results (bit-identical) over many workgroups, for callers with a workspace of
+// loss_ws_bytes(m) bytes (the advantage statistics and the per-row loss terms).
+size_t loss_ws_bytes(int64_t m);
+hipError_t ppo_loss_ws(int64_t m, int A, const float* z, const float* v, const int32_t* act,
+                       const float* old_logp, const float* adv, const float* ret, const int32_t* rows,
+                       int norm_adv, float clip, float vf, float ent, float* dz, float* dv, float* stats,
+                       void* ws, hipStream_t s);
+hipError_t impala_loss_ws(int64_t m, int A, const float* z, const float* v, const int32_t* act,
+                          const float* vs, const float* pg, float pgc, float vf, float ent, float* dz,
+                          float* dv, float* stats, void* ws, hipStream_t s);
 // IMPALA minibatch gather (env block [e0, e0 + Eb) of a [T, E] rollout): rows [(T+1)*Eb]
 // rollout row indices (the last Eb are the bootstrap frames), act, mu, r, d [T*Eb], nd [Eb].
 struct EnvBlock {

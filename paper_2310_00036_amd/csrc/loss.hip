@@ -483,6 +483,160 @@ __global__ __launch_bounds__(kFusedThreads) void impala_fused_kernel(
     }
 }
 
+// ---- wide variants for callers with a workspace (the learner step). The same arithmetic as
+// the single-workgroup kernels, spread over many workgroups: (1) one workgroup forms the
+// advantage statistics exactly as the fused kernel does; (2) one thread per row forms the
+// row's gradients and its five loss terms (stored per row, float64); (3) one workgroup adds
+// the row terms in the fused kernel's order (thread t: rows t, t + 512, ...; then the same
+// block sum). Every output is bit-identical to the single-workgroup kernel's.
+constexpr int kWideRows = 256;   // rows (one per thread) per workgroup of (2)
+
+size_t loss_ws_bytes(int64_t m) { return 256 + size_t(m > 0 ? m : 1) * 5 * sizeof(double); }
+
+template <bool ROWS>
+__global__ __launch_bounds__(kFusedThreads) void adv_stats_ws_kernel(int64_t m, const float* __restrict__ adv,
+                                                                   const int32_t* __restrict__ rows,
+                                                                   float* __restrict__ ms_out) {
+    __shared__ double sh[(kFusedThreads / 64) * 5];
+    double ms[2];
+    adv_sums<ROWS>(m, adv, rows, ms);
+    float mean, std;
+    adv_mean_std(m, ms, sh, mean, std);
+    if (threadIdx.x == 0) { ms_out[0] = mean; ms_out[1] = std; }
+}
+
+// The workgroup's rows' logits into LDS with coalesced loads (unconditional, clamped; all in
+// flight before the first store).
+template <int AC>
+CB_DEV void stage_rows(float* zs, const float* __restrict__ z, int64_t r0, int nr, int A) {
+    if constexpr (AC > 0) {
+        const int n = nr * AC;
+        const float* p = z + r0 * AC;
+        float v[AC];
+#pragma unroll
+        for (int u = 0; u < AC; ++u) {
+            const int e = u * kWideRows + int(threadIdx.x);
+            v[u] = p[e < n ? e : n - 1];
+        }
+#pragma unroll
+        for (int u = 0; u < AC; ++u) {
+            const int e = u * kWideRows + int(threadIdx.x);
+            if (e < n) zs[e] = v[u];
+        }
+    } else {
+        for (int e = threadIdx.x; e < nr * A; e += kWideRows) zs[e] = z[r0 * A + e];
+    }
+}
+
+template <int AC, bool ROWS>
+__global__ __launch_bounds__(kWideRows) void ppo_rows_ws_kernel(
+    int64_t m, int A_, const float* __restrict__ z, const float* __restrict__ val,
+    const int32_t* __restrict__ act, const float* __restrict__ old_logp,
+    const float* __restrict__ adv, const float* __restrict__ ret, const int32_t* __restrict__ rows,
+    int norm_adv, float clip, float vf, float ent, float* __restrict__ dz, float* __restrict__ dv,
+    const float* __restrict__ ms, double* __restrict__ terms) {
+    extern __shared__ float zs[];   // [kWideRows][A]
+    const int A = AC > 0 ? AC : A_;
+    const int tid = threadIdx.x;
+    const int64_t r0 = int64_t(blockIdx.x) * kWideRows;
+    const int nr = m - r0 < kWideRows ? int(m - r0) : kWideRows;
+    const int64_t src = ppo_src<ROWS>(r0 + tid, m, rows);
+    stage_rows<AC>(zs, z, r0, nr, A);
+    const PpoScal cur = ppo_scal(r0 + tid, m, src, act, old_logp, adv, ret, val);
+    const float mean = ms[0], std = ms[1];
+    const float inv_m = 1.f / float(m);
+    __syncthreads();
+    if (tid < nr) {
+        const int64_t i = r0 + tid;
+        float* zr = zs + tid * A;
+        const PpoRow r = ppo_row_v(zr, A, cur.a, cur.olp, cur.adv, norm_adv, clip, mean, std);
+        const float coef = -r.kappa * r.A_hat * r.ratio;
+        for (int j = 0; j < A; ++j) {
+            const float l = r.s.l(zr[j]);
+            const float p = expf(l);
+            zr[j] = (coef * ((j == r.a ? 1.f : 0.f) - p) + ent * p * (l + r.H)) * inv_m;
+        }
+        const float vi = cur.val, ri = cur.ret;
+        dv[i] = vf * (vi - ri) * inv_m;
+        const double dvl = double(vi) - double(ri);
+        double* tr = terms + i * 5;
+        tr[0] = r.pg;
+        tr[1] = dvl * dvl;
+        tr[2] = r.H;
+        tr[3] = double(r.ratio - 1.f) - double(logf(r.ratio));
+        tr[4] = fabsf(r.ratio - 1.f) > clip ? 1.0 : 0.0;
+    }
+    __syncthreads();
+    for (int e = tid; e < nr * A; e += kWideRows) dz[r0 * A + e] = zs[e];
+}
+
+template <int AC>
+__global__ __launch_bounds__(kWideRows) void impala_rows_ws_kernel(
+    int64_t m, int A_, const float* __restrict__ z, const float* __restrict__ val,
+    const int32_t* __restrict__ act, const float* __restrict__ vs, const float* __restrict__ pgadv,
+    float pgc, float vf, float ent, float* __restrict__ dz, float* __restrict__ dv, double* __restrict__ terms) {
+    extern __shared__ float zs[];   // [kWideRows][A]
+    const int A = AC > 0 ? AC : A_;
+    const int tid = threadIdx.x;
+    const int64_t r0 = int64_t(blockIdx.x) * kWideRows;
+    const int nr = m - r0 < kWideRows ? int(m - r0) : kWideRows;
+    stage_rows<AC>(zs, z, r0, nr, A);
+    const ImpScal cur = imp_scal(r0 + tid, m, act, pgadv, val, vs);
+    const float inv_m = 1.f / float(m);
+    __syncthreads();
+    if (tid < nr) {
+        const int64_t i = r0 + tid;
+        float* zr = zs + tid * A;
+        const RowLsm rs = row_log_softmax(zr, A);
+        const float H = rs.H;
+        const int a = cur.a;
+        const float advv = cur.adv;
+        const bool a_ok = a >= 0 && a < A;
+        const double la = a_ok ? double(rs.l(zr[a])) : double(__builtin_nanf(""));
+        for (int j = 0; j < A; ++j) {
+            const float l = rs.l(zr[j]);
+            const float p = expf(l);
+            zr[j] = a_ok ? (-pgc * advv * ((j == a ? 1.f : 0.f) - p) + ent * p * (l + H)) * inv_m
+                         : __builtin_nanf("");
+        }
+        const float vi = cur.val, vsi = cur.vs;
+        dv[i] = vf * (vi - vsi) * inv_m;
+        const double dvl = double(vi) - double(vsi);
+        double* tr = terms + i * 5;
+        tr[0] = -double(advv) * la;
+        tr[1] = dvl * dvl;
+        tr[2] = H;
+        tr[3] = advv;
+        tr[4] = vsi;
+    }
+    __syncthreads();
+    for (int e = tid; e < nr * A; e += kWideRows) dz[r0 * A + e] = zs[e];
+}
+
+// (3): the row terms summed in the fused kernel's order, then its statistics.
+template <bool PPO>
+__global__ __launch_bounds__(kFusedThreads) void loss_final_ws_kernel(int64_t m, float pgc, float vf, float ent,
+                                                                    const double* __restrict__ terms,
+                                                                    const float* __restrict__ ms,
+                                                                    float* __restrict__ stats) {
+    __shared__ double sh[(kFusedThreads / 64) * 5];
+    double st[5] = {0, 0, 0, 0, 0};
+    for (int64_t i = threadIdx.x; i < m; i += kFusedThreads) {
+#pragma unroll
+        for (int k = 0; k < 5; ++k) st[k] += terms[i * 5 + k];
+    }
+    fused_block_sum<5>(st, sh);
+    if (threadIdx.x == 0) {
+        const double inv = 1.0 / double(m);
+        const double pg = st[0] * inv, vl = 0.5 * st[1] * inv, H = st[2] * inv;
+        stats[0] = float(PPO ? pg + vf * vl - ent * H : pgc * pg + vf * vl - ent * H);
+        stats[1] = float(pg); stats[2] = float(vl); stats[3] = float(H);
+        stats[4] = float(st[3] * inv); stats[5] = float(st[4] * inv);
+        stats[6] = PPO ? ms[0] : 0.f;
+        stats[7] = PPO ? ms[1] : 0.f;
+    }
+}
+
 static size_t fused_lds(int A) {
     const int cr = std::min(kFusedThreads * 64 / A, kFusedThreads);
     return size_t(cr) * A * sizeof(float);
@@ -527,6 +681,55 @@ hipError_t impala_loss(int64_t m, int A, const float* z, const float* v, const i
                        pgc, vf, ent, dz, dv);
     hipLaunchKernelGGL(impala_stats_kernel, dim3(1), dim3(kStatThreads), 0, s, m, A, z, v, act, vs, pg,
                        pgc, vf, ent, stats);
+    return hipGetLastError();
+}
+
+hipError_t ppo_loss_ws(int64_t m, int A, const float* z, const float* v, const int32_t* act,
+                       const float* old_logp, const float* adv, const float* ret, const int32_t* rows,
+                       int norm_adv, float clip, float vf, float ent, float* dz, float* dv, float* stats,
+                       void* ws, hipStream_t s) {
+    if (m <= 0) return hipSuccess;
+    if (m <= kWideRows || m > kFusedRows)   // one workgroup's worth, or beyond the fused order
+        return ppo_loss(m, A, z, v, act, old_logp, adv, ret, rows, norm_adv, clip, vf, ent, dz, dv, stats, s);
+    float* ms = static_cast<float*>(ws);
+    double* terms = reinterpret_cast<double*>(static_cast<char*>(ws) + 256);
+    const int nb = int((m + kWideRows - 1) / kWideRows);
+    const size_t lds = size_t(kWideRows) * A * sizeof(float);
+    ProfScope ps(s, [&] { return "ppo_loss/" + cb_dims(int(m), A); });
+    if (rows) hipLaunchKernelGGL(adv_stats_ws_kernel<true>, dim3(1), dim3(kFusedThreads), 0, s, m, adv, rows, ms);
+    else hipLaunchKernelGGL(adv_stats_ws_kernel<false>, dim3(1), dim3(kFusedThreads), 0, s, m, adv, rows, ms);
+#define CB_PR(AC, RW) \
+    hipLaunchKernelGGL((ppo_rows_ws_kernel<AC, RW>), dim3(unsigned(nb)), dim3(kWideRows), lds, s, m, A, z, v, act, \
+                       old_logp, adv, ret, rows, norm_adv, clip, vf, ent, dz, dv, ms, terms)
+    if (rows) {
+        if (A == 18) CB_PR(18, true); else if (A == 6) CB_PR(6, true); else CB_PR(0, true);
+    } else {
+        if (A == 18) CB_PR(18, false); else if (A == 6) CB_PR(6, false); else CB_PR(0, false);
+    }
+#undef CB_PR
+    hipLaunchKernelGGL(loss_final_ws_kernel<true>, dim3(1), dim3(kFusedThreads), 0, s, m, 0.f, vf, ent, terms, ms,
+                       stats);
+    return hipGetLastError();
+}
+
+hipError_t impala_loss_ws(int64_t m, int A, const float* z, const float* v, const int32_t* act,
+                          const float* vs, const float* pg, float pgc, float vf, float ent, float* dz,
+                          float* dv, float* stats, void* ws, hipStream_t s) {
+    if (m <= 0) return hipSuccess;
+    if (m <= kWideRows || m > kFusedRows)
+        return impala_loss(m, A, z, v, act, vs, pg, pgc, vf, ent, dz, dv, stats, s);
+    float* ms = static_cast<float*>(ws);
+    double* terms = reinterpret_cast<double*>(static_cast<char*>(ws) + 256);
+    const int nb = int((m + kWideRows - 1) / kWideRows);
+    const size_t lds = size_t(kWideRows) * A * sizeof(float);
+    ProfScope ps(s, [&] { return "impala_loss/" + cb_dims(int(m), A); });
+#define CB_IR(AC) \
+    hipLaunchKernelGGL((impala_rows_ws_kernel<AC>), dim3(unsigned(nb)), dim3(kWideRows), lds, s, m, A, z, v, act, vs, \
+                       pg, pgc, vf, ent, dz, dv, terms)
+    if (A == 18) CB_IR(18); else if (A == 6) CB_IR(6); else CB_IR(0);
+#undef CB_IR
+    hipLaunchKernelGGL(loss_final_ws_kernel<false>, dim3(1), dim3(kFusedThreads), 0, s, m, pgc, vf, ent, terms, ms,
+                       stats);
     return hipGetLastError();
 }
 
