@@ -207,3 +207,64 @@ CB_DEV void sum_partials_x4(const float* __restrict__ partial, int nparts, int p
     }
     if (sl == 0 && e < pstride) emit(e, sh[0][q]);
 }
+
+// A pending weight-gradient reduce (PendingReduce, see kernels.h) done by the first work of a
+// kernel with NT threads: blocks of 64 entries (16 float4 lanes x NT/16 slices, each slice
+// adding the partials s, s + NT/16, ... in turn, then a fixed pairwise tree) spread over the
+// grid, scattered to HWIO weights (times scale) and the bias. `lds` holds NT/16 x 17 float4.
+// Ends with a barrier, so the caller may reuse the LDS.
+template <int NT, class R>
+CB_DEV void pending_reduce(const R& r, unsigned char* lds) {
+    constexpr int SL = NT / 16;
+    float4* sh = reinterpret_cast<float4*>(lds);
+    const int q = threadIdx.x & 15, sl = threadIdx.x >> 4;
+    const int NB = r.u8 ? 3 : 9 * r.cin / 16, NBB = NB + 1, cb16 = r.cin / 16 > 0 ? r.cin / 16 : 1;
+    const int nrb = r.pstride / 64;
+    const int64_t st = r.pstride / 4;
+    for (int rb = blockIdx.x; rb < nrb; rb += gridDim.x) {
+        const int e = rb * 64 + 4 * q;
+        const float4* p = reinterpret_cast<const float4*>(r.partial + e);
+        float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+        int k = sl;
+        for (; k + 7 * SL < r.nparts; k += 8 * SL) {
+            float4 v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = p[int64_t(k + SL * u) * st];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) { s.x += v[u].x; s.y += v[u].y; s.z += v[u].z; s.w += v[u].w; }
+        }
+        for (; k < r.nparts; k += SL) {
+            const float4 v = p[int64_t(k) * st];
+            s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+        }
+        sh[sl * 17 + q] = s;
+        __syncthreads();
+#pragma unroll
+        for (int w = SL / 2; w >= 1; w >>= 1) {
+            if (sl < w) {
+                const float4 o = sh[(sl + w) * 17 + q];
+                float4& m = sh[sl * 17 + q];
+                m.x += o.x; m.y += o.y; m.z += o.z; m.w += o.w;
+            }
+            __syncthreads();
+        }
+        if (sl == 0) {
+            const float4 v = sh[q];
+            const float tv[4] = {v.x, v.y, v.z, v.w};
+            const int tile = e >> 8, row = (e >> 4) & 15;
+            const int mt = tile / NBB, nb = tile - mt * NBB, co = mt * 16 + row;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int col = (e & 15) + u;
+                if (nb == NB) {
+                    if (col == 0) r.db[co] = tv[u];
+                } else {
+                    const int tap = r.u8 ? nb * 4 + col / 4 : nb / cb16;
+                    const int ci = r.u8 ? col % 4 : (nb % cb16) * 16 + col;
+                    if (tap < 9) r.dw[(tap * r.cin + ci) * r.cout + co] = tv[u] * r.scale;
+                }
+            }
+        }
+        __syncthreads();
+    }
+}

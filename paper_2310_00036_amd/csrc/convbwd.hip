@@ -75,6 +75,8 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
     const int H = a.H, W = a.W, TH = t.TH, FR = t.FR;
     const int TW = W + 2, TR = TH + 2;
 
+    // an earlier launch's weight-gradient partials, summed first (LDS is free until staging)
+    if (a.pend.nparts > 0) pending_reduce<NT>(a.pend, smem);
     if (tid < 16) reinterpret_cast<uint32_t*>(zero)[tid] = 0u;
     if constexpr (PDY) {
         // the dy window is built in LDS: its padding columns and zero slots are never written
@@ -424,7 +426,7 @@ int cb_parts_cap() {
 }
 
 template <int CI, int CO, int MODE, int ADD, int PDY>
-hipError_t cb_launch(const ConvBwdArgs& a, hipStream_t s) {
+hipError_t cb_launch(const ConvBwdArgs& a, hipStream_t s, PendingReduce* deferred) {
     using G = CbGeom<CI, CO>;
     const int H = a.H, W = a.W;
     // max-pool geometry of a pooled input gradient (PDY): XLA SAME padding split
@@ -479,7 +481,7 @@ hipError_t cb_launch(const ConvBwdArgs& a, hipStream_t s) {
     t.OH = OH; t.OW = OW; t.ph = ph; t.pw = pw; t.BH = (H + ph + 1) / 2; t.BW = (W + pw + 1) / 2;
     t.inv_W = 1.f / float(W); t.inv_TW = 1.f / float(W + 2);
     t.inv_TH = 1.f / float(TH); t.inv_TR = 1.f / float(TH + 2);
-    const size_t L = lds(TH, FR);
+    const size_t L = std::max(lds(TH, FR), size_t(kCbWaves * 4) * 17 * 16);   // (pending reduce)
     if (PDY && int64_t(OH) * OW * CO * 2 >= (int64_t(1) << 31)) return hipErrorInvalidValue;
     const void* fn = reinterpret_cast<const void*>(&conv_bwd_kernel<CI, CO, MODE, ADD, PDY, kCbWaves>);
     int parts = std::min(resident_blocks(fn, 64 * kCbWaves, L), cb_parts_cap<CI, CO>());
@@ -492,6 +494,10 @@ hipError_t cb_launch(const ConvBwdArgs& a, hipStream_t s) {
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (deferred) {
+        *deferred = PendingReduce{a.partial, a.dw, a.db, parts, G::PSTRIDE, CI, CO, 0, 1.f};
+        return hipSuccess;
+    }
     ProfScope ps(s, [&] { return cb_key("conv_bwd_reduce", 0, shape); });
     return wgrad_reduce_tr(CI, CO, a.partial, parts, a.dw, a.db, 1.f, s);
 }
@@ -513,11 +519,12 @@ size_t conv3x3_bwd_partial_floats(int cin, int cout) {
     return best;
 }
 
-hipError_t conv3x3_bwd(int cin, int cout, int mode, const ConvBwdArgs& a, hipStream_t s) {
-    if (a.n <= 0) return hipSuccess;
+hipError_t conv3x3_bwd(int cin, int cout, int mode, const ConvBwdArgs& a, hipStream_t s, PendingReduce* deferred) {
+    if (deferred) deferred->nparts = 0;
+    if (a.n <= 0) return flush_pending_reduce(a.pend, s);
     const int add = a.add != nullptr, pdy = a.arg != nullptr;
 #define CB_B(CI, CO, MD, AD, PD) \
-    if (cin == CI && cout == CO && mode == MD && add == AD && pdy == PD) return cb_launch<CI, CO, MD, AD, PD>(a, s);
+    if (cin == CI && cout == CO && mode == MD && add == AD && pdy == PD) return cb_launch<CI, CO, MD, AD, PD>(a, s, deferred);
     CB_B(16, 16, IN_RELU, 0, 0) CB_B(16, 16, IN_RELU, 1, 0) CB_B(32, 32, IN_RELU, 0, 0) CB_B(32, 32, IN_RELU, 1, 0)
     CB_B(16, 16, IN_PLAIN, 0, 0) CB_B(16, 32, IN_PLAIN, 0, 0) CB_B(32, 32, IN_PLAIN, 0, 0)
     CB_B(16, 16, IN_PLAIN, 0, 1) CB_B(16, 32, IN_PLAIN, 0, 1) CB_B(32, 32, IN_PLAIN, 0, 1)

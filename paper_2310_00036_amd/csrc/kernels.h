@@ -72,6 +72,19 @@ bool wgrad_supported(int cin, int cout, int mode);
 
 // ---- whole backward pass of one 3x3 SAME conv (bf16): input gradient and weight gradient
 //      from one staging of dy and x. Forward: y = conv(X, w) + b, X = relu(x) (IN_RELU) or x.
+// A weight-gradient partial sum deferred to the next kernel on the stream: nparts float32
+// partials (stride pstride floats) laid out [mt*(NB+1) + nb][co 16][col 16] (NB = 9*cin/16
+// column blocks, 3 for uint8 frames; the last block holds the bias sums), to be scattered to
+// HWIO dw (times scale) and db. nparts == 0: none.
+struct PendingReduce {
+    const float* partial;
+    float* dw; float* db;
+    int nparts, pstride, cin, cout, u8;
+    float scale;
+};
+// Launches the standalone fixed-order reduce of a pending partial sum (no-op if none).
+hipError_t flush_pending_reduce(const PendingReduce& r, hipStream_t s);
+
 struct ConvBwdArgs {
     const void* dy;         // [n, H, W, cout] bf16; with arg: the max-pool output gradient
                             // [n, ceil(H/2), ceil(W/2), cout] of the pool this conv feeds
@@ -84,6 +97,7 @@ struct ConvBwdArgs {
     float* db;              // float32 [cout]
     float* partial;         // workspace, conv3x3_bwd_partial_floats() floats
     int n, H, W;
+    PendingReduce pend;     // an earlier launch's partials, summed by this kernel first
 };
 struct CbTile {
     int TH, FR, nbands, ntiles;
@@ -95,7 +109,10 @@ struct CbTile {
 };
 bool conv3x3_bwd_supported(int cin, int cout, int mode, int add, int pooled);
 size_t conv3x3_bwd_partial_floats(int cin, int cout);
-hipError_t conv3x3_bwd(int cin, int cout, int mode, const ConvBwdArgs& a, hipStream_t s);
+// deferred: when non-NULL the launch's own partial sum is not reduced; it is described there
+// for a later launch (conv3x3_bwd / pool_wgrad_u8 via .pend, or flush_pending_reduce).
+hipError_t conv3x3_bwd(int cin, int cout, int mode, const ConvBwdArgs& a, hipStream_t s,
+                       PendingReduce* deferred = nullptr);
 // Fixed-order sum of nparts bf16 weight-gradient partials laid out [mt*(NB+1) + nb]
 // [co 16][col 16] (the last column block holds the bias sums), scattered to HWIO dw (times
 // scale) and db. NB = 9*cin/16 column blocks of 16 input channels of one tap; for uint8
@@ -115,6 +132,7 @@ struct PoolWgArgs {
     float* db;              // float32 [cout]
     float* partial;         // workspace, pool_wgrad_u8_partial_floats() floats
     int n, H, W;
+    PendingReduce pend;     // an earlier launch's partials, summed by this kernel first
 };
 struct PwTile {
     int TB, nbands, ntiles;         // 2x2 pixel-block rows per band

@@ -116,7 +116,17 @@ NetPlan make_plan(const impala_net_t& net, int prec, int64_t cap, int training) 
             }
         }
     }
-    p.scratch_bytes = sc * sizeof(float);
+    // the trunk backward's fused kernels defer each weight-gradient reduce to the next launch,
+    // alternating between two partial buffers: the second one follows the shared scratch
+    size_t sc2 = 0;
+    if (training && prec == BF16)
+        for (int s = 0; s < 3; ++s) {
+            if (s == 0) sc2 = std::max(sc2, pool_wgrad_u8_partial_floats(p.C[1]));
+            sc2 = std::max(sc2, conv3x3_bwd_partial_floats(p.C[s], p.C[s + 1]));
+            sc2 = std::max(sc2, conv3x3_bwd_partial_floats(p.C[s + 1], p.C[s + 1]));
+        }
+    p.scratch_floats = sc;
+    p.scratch_bytes = (sc + sc2) * sizeof(float);
     p.scratch = take(p.scratch_bytes);
     p.total = off;
     return p;
@@ -239,6 +249,26 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
 
     int gy = 1;
     auto others = [](int k, int& a, int& b) { a = (k + 1) % 3; b = (k + 2) % 3; };
+    // fused conv backward launches: each one's weight-gradient reduce runs at the start of the
+    // next fused launch (or a standalone reduce before any other launch), the partials
+    // alternating between two buffers
+    float* pbuf[2] = {scratch, scratch + p.scratch_floats};
+    PendingReduce pend{};
+    int pb = 0;
+    auto fused_bwd = [&](int ci, int co, int mode, ConvBwdArgs c) -> hipError_t {
+        c.partial = pbuf[pb];
+        c.pend = pend;
+        PendingReduce nx{};
+        const hipError_t e = conv3x3_bwd(ci, co, mode, c, s, &nx);
+        pend = nx;
+        pb ^= 1;
+        return e;
+    };
+    auto flush = [&]() -> hipError_t {
+        const hipError_t e = flush_pending_reduce(pend, s);
+        pend.nparts = 0;
+        return e;
+    };
     for (int st = 2; st >= 0; --st) {
         const int C = p.C[st + 1], Hs = p.H[st + 1], Ws = p.W[st + 1];
         for (int r = 1; r >= 0; --r) {
@@ -249,18 +279,19 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
                 // each conv's input and weight gradients from one staging of its dy and input
                 ConvBwdArgs c1{};
                 c1.dy = G[gy]; c1.x = ws + p.t[st][r]; c1.w = params + po.conv_w[st][k1]; c1.dx = G[fa];
-                c1.dw = grads + po.conv_w[st][k1]; c1.db = grads + po.conv_b[st][k1]; c1.partial = scratch;
+                c1.dw = grads + po.conv_w[st][k1]; c1.db = grads + po.conv_b[st][k1];
                 c1.n = int(n); c1.H = Hs; c1.W = Ws;
-                CB_TRY(conv3x3_bwd(C, C, IN_RELU, c1, s));
+                CB_TRY(fused_bwd(C, C, IN_RELU, c1));
                 ConvBwdArgs c0{};
                 c0.dy = G[fa]; c0.x = ws + p.x[st][r]; c0.w = params + po.conv_w[st][k0]; c0.add = G[gy];
                 c0.dx = G[fb]; c0.dw = grads + po.conv_w[st][k0]; c0.db = grads + po.conv_b[st][k0];
-                c0.partial = scratch; c0.n = int(n); c0.H = Hs; c0.W = Ws;
-                CB_TRY(conv3x3_bwd(C, C, IN_RELU, c0, s));
+                c0.n = int(n); c0.H = Hs; c0.W = Ws;
+                CB_TRY(fused_bwd(C, C, IN_RELU, c0));
                 gy = fb;
                 continue;
             }
             // y = x + conv1(relu(t)) + b1 with t = conv0(relu(x)) + b0
+            CB_TRY(flush());
             WgradArgs w1{};
             w1.x = ws + p.t[st][r]; w1.dy = G[gy]; w1.dw = grads + po.conv_w[st][k1];
             w1.db = grads + po.conv_b[st][k1]; w1.partial = scratch;
@@ -289,8 +320,10 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
             PoolWgArgs pa{};
             pa.obs = obs; pa.row_idx = row_idx; pa.dp = G[gy];
             pa.arg = reinterpret_cast<const uint8_t*>(ws + p.idx[0]);
-            pa.dw = grads + po.conv_w[0][0]; pa.db = grads + po.conv_b[0][0]; pa.partial = scratch;
+            pa.dw = grads + po.conv_w[0][0]; pa.db = grads + po.conv_b[0][0]; pa.partial = pbuf[pb];
             pa.n = int(n); pa.H = p.H[0]; pa.W = p.W[0];
+            pa.pend = pend;   // the previous fused launch's reduce runs first in this kernel
+            pend.nparts = 0;
             CB_TRY(pool_wgrad_u8(C, pa, s));
             continue;
         }
@@ -300,12 +333,13 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
             ConvBwdArgs ce{};
             ce.dy = G[gy]; ce.arg = reinterpret_cast<const uint8_t*>(ws + p.idx[st]);
             ce.x = ws + p.x[st - 1][2]; ce.w = params + po.conv_w[st][0]; ce.dx = G[fa];
-            ce.dw = grads + po.conv_w[st][0]; ce.db = grads + po.conv_b[st][0]; ce.partial = scratch;
+            ce.dw = grads + po.conv_w[st][0]; ce.db = grads + po.conv_b[st][0];
             ce.n = int(n); ce.H = p.H[st]; ce.W = p.W[st];
-            CB_TRY(conv3x3_bwd(p.C[st], C, IN_PLAIN, ce, s));
+            CB_TRY(fused_bwd(p.C[st], C, IN_PLAIN, ce));
             gy = fa;
             continue;
         }
+        CB_TRY(flush());
         CB_TRY(maxpool_bwd(p.prec, int(n), p.H[st], p.W[st], C,
                            reinterpret_cast<const uint8_t*>(ws + p.idx[st]), G[gy], G[fa], s));
         WgradArgs we{};
@@ -323,6 +357,7 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
             gy = fb;
         }
     }
+    CB_TRY(flush());
     return hipSuccess;
 }
 

@@ -32,6 +32,7 @@ struct NetPlan {
     size_t wdb;             // bf16 copy of the dense weights [flat][hidden] (bf16 mode)
     size_t scratch;         // split-K / weight-gradient / head-gradient partials
     size_t scratch_bytes;
+    size_t scratch_floats;  // the shared part; a second partial buffer for deferred reduces follows
     size_t total;
 };
 

@@ -56,6 +56,8 @@ __global__ __launch_bounds__(64 * NW, 4) void pool_wgrad_u8_kernel(PoolWgArgs a,
     unsigned char* agl = smem + t.arg_off;          // argmax [TB+1][OW+2] x CO
     unsigned char* dcl = smem + t.dc_off;           // dC [2TB][TW] x DPB
 
+    // an earlier launch's weight-gradient partials, summed first (LDS is free until staging)
+    if (a.pend.nparts > 0) pending_reduce<NT>(a.pend, smem);
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, r16 = lane & 15, jj = r16 >> 2, m = r16 & 3;
@@ -304,7 +306,7 @@ hipError_t pw_launch(const PoolWgArgs& a, hipStream_t s) {
         return hipErrorInvalidValue;
     const int nb0 = (BH + tbmax - 1) / tbmax;
     const int TB = (BH + nb0 - 1) / nb0;   // balanced bands
-    const size_t L = layout(TB, t);
+    const size_t L = std::max(layout(TB, t), size_t(kPwWaves * 4) * 17 * 16);   // (pending reduce)
     t.TB = TB; t.nbands = (BH + TB - 1) / TB; t.ntiles = t.nbands * a.n;
     t.OH = OH; t.OW = OW; t.ph = ph; t.pw = pw; t.BH = BH; t.BW = BW;
     const void* fn = reinterpret_cast<const void*>(&pool_wgrad_u8_kernel<CO, kPwWaves>);
@@ -333,7 +335,7 @@ size_t pool_wgrad_u8_partial_floats(int cout) {
 }
 
 hipError_t pool_wgrad_u8(int cout, const PoolWgArgs& a, hipStream_t s) {
-    if (a.n <= 0) return hipSuccess;
+    if (a.n <= 0) return flush_pending_reduce(a.pend, s);
     if (cout == 16) return pw_launch<16>(a, s);
     if (cout == 32) return pw_launch<32>(a, s);
     return hipErrorInvalidValue;

@@ -746,4 +746,16 @@ hipError_t conv3x3_wgrad(int prec, int cin, int cout, int mode, const WgradArgs&
                         : wg_dispatch<PrecF32>(cin, cout, mode, a, s);
 }
 
+__global__ __launch_bounds__(1024) void pending_reduce_kernel(PendingReduce r) {
+    __shared__ __align__(16) unsigned char sh[64 * 17 * 16];
+    pending_reduce<1024>(r, sh);
+}
+
+hipError_t flush_pending_reduce(const PendingReduce& r, hipStream_t s) {
+    if (r.nparts <= 0) return hipSuccess;
+    ProfScope ps(s, [&] { return "wgrad_reduce_pending/" + cb_dims(r.cin, r.cout); });
+    hipLaunchKernelGGL(pending_reduce_kernel, dim3(unsigned(r.pstride / 64)), dim3(1024), 0, s, r);
+    return hipGetLastError();
+}
+
 }  // namespace cb
