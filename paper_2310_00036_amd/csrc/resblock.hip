@@ -32,7 +32,13 @@ struct RbGeom {
     static constexpr int MT = C / 16;
     static constexpr int SPP = C / 8 + 1;                  // 16-byte slots per window pixel
     static constexpr int PB = SPP * 16;
-    static constexpr int MAXS = C >= 32 ? 4 : 5;           // x-window staging slots per lane
+    // Workgroup shape: 16 channels hold both weight sets in 8-wave workgroups at 4 waves per
+    // SIMD (128 registers); 32 channels need about 170 registers, so 4-wave workgroups at 3
+    // waves per SIMD (three workgroups per CU) instead of spilling.
+    static constexpr int NW = C >= 32 ? 4 : 8;
+    static constexpr int WPS = C >= 32 ? 3 : 4;            // waves per SIMD (register budget)
+    static constexpr int WGS = WPS * 4 / NW;               // workgroups per CU
+    static constexpr int MAXS = C >= 32 ? 8 : 5;           // x-window staging slots per lane
     // conv2 column tiles per wave and tile whose residual is fetched with the staging (with 32
     // channels the registers hold both weight sets, and the residual is read per column tile)
     static constexpr int MAXT = C >= 32 ? 0 : 5;
@@ -48,7 +54,7 @@ struct RbTile {
 };
 
 template <int C, int NW>
-__global__ __launch_bounds__(64 * NW, 4) void resblock_fwd_kernel(ResBlockArgs a, RbTile t) {
+__global__ __launch_bounds__(64 * NW, RbGeom<C>::WPS) void resblock_fwd_kernel(ResBlockArgs a, RbTile t) {
     using G = RbGeom<C>;
     constexpr int NT = 64 * NW, KSTEPS = G::KSTEPS, MT = G::MT, SPP = G::SPP, PB = G::PB;
     static_assert(NW % MT == 0, "waves split evenly over the output channel blocks");
@@ -224,12 +230,13 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_fwd_kernel(ResBlockArgs a
 
 namespace {
 
-constexpr int kRbWaves = 8;
-constexpr size_t kRbLdsTarget = 80 * 1024;
+constexpr size_t kRbLds = 160 * 1024;   // per CU, shared by the resident workgroups
 
 template <int C>
 hipError_t rb_fwd_launch(const ResBlockArgs& a, hipStream_t s) {
     using G = RbGeom<C>;
+    constexpr int kRbWaves = G::NW;
+    constexpr size_t kRbLdsTarget = kRbLds / G::WGS;
     const int H = a.H, W = a.W;
     auto lds = [&](int th) { return size_t(G::xwin_bytes(th, W)) + G::twin_bytes(th, W); };
     auto fits = [&](int th) {
