@@ -96,6 +96,12 @@ def run_layer(P, key, n, steps):
             b1, b2 = torch.zeros(ci, device="cuda"), torch.zeros(ci, device="cuda")
             x, tt, y = act(h, w, ci), act(h, w, ci), act(h, w, ci)
             fn = lambda: P.impala_resblock_fwd(prec, n, h, w, ci, x, w1, b1, w2, b2, tt, y)  # noqa: E731
+        elif fam == "resblock_bwd":
+            wa, wb = (torch.randn(3, 3, ci, ci, device="cuda", generator=g) * 0.1 for _ in range(2))
+            dy, tt, x, dx = act(h, w, ci), act(h, w, ci), act(h, w, ci), act(h, w, ci)
+            gw = [torch.empty(shape, device="cuda") for shape in ((3, 3, ci, ci), (ci,), (3, 3, ci, ci), (ci,))]
+            ws = torch.empty(P.impala_resblock_bwd_workspace_bytes(prec, ci), dtype=torch.uint8, device="cuda")
+            fn = lambda: P.impala_resblock_bwd(prec, n, h, w, ci, dy, tt, x, wa, wb, dx, *gw, ws)  # noqa: E731
         elif fam == "conv_bwd":     # key channels: forward cin x cout
             pooled = "pool" in flags
             oh, ow = (h + 1) // 2, (w + 1) // 2
@@ -224,6 +230,11 @@ def kernel_work(key, n, prec):
         h, w = map(int, parts[3].split("x"))
         px = n * h * w
         return "hbm", float(px * c * es * 3), "B", 2.0 * 2.0 * px * 9 * c * c
+    if fam == "resblock_bwd":   # one pass: dy, t and x in, dx out (dt stays on chip)
+        c = int(parts[2].split("x")[0])
+        h, w = map(int, parts[3].split("x"))
+        px = n * h * w
+        return "hbm", float(px * c * es * 4), "B", 4.0 * 2.0 * px * 9 * c * c
     if fam == "pool_wgrad":   # one pass: frames, pooled gradient and argmax in
         co = int(parts[2].split("x")[1])
         h, w = map(int, parts[3].split("x"))
@@ -277,7 +288,8 @@ def source_digest(key):
     fam = key.split("/")[0]
     src = {"conv_fwd": "conv.hip", "conv_dgrad": "conv.hip", "conv_pool": "conv.hip", "wgrad": "wgrad.hip",
            "gemm": "gemm.hip", "adam": "adam.hip", "pool_fwd": "pool.hip", "pool_bwd": "pool.hip",
-           "resblock_fwd": "resblock.hip", "conv_bwd": "convbwd.hip", "pool_wgrad": "poolwgrad.hip"}.get(fam)
+           "resblock_fwd": "resblock.hip", "resblock_bwd": "resbwd.hip", "conv_bwd": "convbwd.hip",
+           "pool_wgrad": "poolwgrad.hip"}.get(fam)
     if not src:
         return None
     path = os.path.join(ROOT, "paper_2310_00036_amd", "csrc", src)

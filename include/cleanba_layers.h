@@ -98,6 +98,25 @@ impala_status_t impala_conv3x3_bwd(impala_prec_t prec, int64_t n, int32_t H, int
                                    int32_t x_mode, const float* w, const void* add, void* dx, float* dw,
                                    float* db, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* The backward pass of one residual block of Section 5's IMPALA-ResNet in one pass, bf16
+ * only (C = 16), Algorithm 1's back-propagation through the block that impala_resblock_fwd
+ * computes: with t = conv3x3_same(relu(x), wa) + ba, y = x + conv3x3_same(relu(t), wb) + bb
+ * (wa, wb are that call's w1, w2) and dy the gradient at y:
+ *   dt = conv3x3_same^T(dy, wb) * (t > 0), rounded to bf16;
+ *   dx = conv3x3_same^T(dt, wa) * (x > 0) + dy;
+ *   dwb, dbb as impala_conv3x3_wgrad of relu(t) against dy; dwa, dba of relu(x) against dt.
+ * The result equals impala_conv3x3_bwd for the second conv (IMPALA_X_RELU with x = t)
+ * followed by impala_conv3x3_bwd for the first (IMPALA_X_RELU with add = dy); dt never
+ * leaves the chip. dy, t, x, dx: [n, H, W, C] bf16 (dx must not overlap the inputs); wa, wb:
+ * float HWIO [3,3,C,C]; dwa, dwb: float [3,3,C,C] and dba, dbb: float [C] (all overwritten);
+ * ws: device scratch of impala_resblock_bwd_workspace_bytes() bytes. Other precisions or
+ * channel counts return IMPALA_EUNSUPPORTED. */
+size_t impala_resblock_bwd_workspace_bytes(impala_prec_t prec, int32_t C);
+impala_status_t impala_resblock_bwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t C,
+                                    const void* dy, const void* t, const void* x, const float* wa,
+                                    const float* wb, void* dx, float* dwa, float* dba, float* dwb,
+                                    float* dbb, void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Backward of the first stage entry of Section 5's IMPALA-ResNet, y = maxpool3x3s2_same(
  * conv3x3_same(frames / 255, w) + bias), in one pass, bf16 only (Algorithm 1's
  * back-propagation; the frames need no input gradient): the max-pool's input gradient

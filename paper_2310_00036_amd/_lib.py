@@ -81,6 +81,9 @@ _SIGS = {
     "impala_conv3x3_bwd_workspace_bytes": (_SZ, [C.c_int, _I32, _I32]),
     "impala_conv3x3_bwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _I32, _P, _P, _P, _P,
                                      _P, _P, _SZ, _P]),
+    "impala_resblock_bwd_workspace_bytes": (_SZ, [C.c_int, _I32]),
+    "impala_resblock_bwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                      _P, _SZ, _P]),
     "impala_conv3x3_pool_wgrad_u8_workspace_bytes": (_SZ, [C.c_int, _I32]),
     "impala_conv3x3_pool_wgrad_u8": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _SZ,
                                                _P]),
@@ -327,6 +330,16 @@ def impala_conv3x3_bwd(prec, n, H, W, cin, cout, dy, x, x_mode, w, add, dx, dw, 
     _check("impala_conv3x3_bwd", lib.impala_conv3x3_bwd(
         prec, n, H, W, cin, cout, ptr(dy), ptr(pool_arg), ptr(x), x_mode, ptr(w), ptr(add), ptr(dx), ptr(dw),
         ptr(db), ptr(ws), ws.numel() * ws.element_size(), stream_handle(stream)))
+
+
+def impala_resblock_bwd_workspace_bytes(prec, C_) -> int:
+    return int(lib.impala_resblock_bwd_workspace_bytes(prec, C_))
+
+
+def impala_resblock_bwd(prec, n, H, W, C_, dy, t, x, wa, wb, dx, dwa, dba, dwb, dbb, ws, stream=None):
+    _check("impala_resblock_bwd", lib.impala_resblock_bwd(
+        prec, n, H, W, C_, ptr(dy), ptr(t), ptr(x), ptr(wa), ptr(wb), ptr(dx), ptr(dwa), ptr(dba), ptr(dwb),
+        ptr(dbb), ptr(ws), ws.numel() * ws.element_size(), stream_handle(stream)))
 
 
 def impala_conv3x3_pool_wgrad_u8_workspace_bytes(prec, cout) -> int:

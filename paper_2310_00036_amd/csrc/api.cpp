@@ -651,6 +651,41 @@ impala_status_t impala_conv3x3_bwd(impala_prec_t prec, int64_t n, int32_t H, int
     return hip_status(conv3x3_bwd(cin, cout, x_mode, a, stream), "impala_conv3x3_bwd");
 }
 
+size_t impala_resblock_bwd_workspace_bytes(impala_prec_t prec, int32_t C) {
+    if (prec != IMPALA_PREC_BF16) return 0;
+    return resblock_bwd_partial_floats(C) * sizeof(float);
+}
+
+impala_status_t impala_resblock_bwd(impala_prec_t prec, int64_t n, int32_t H, int32_t W, int32_t C,
+                                    const void* dy, const void* t, const void* x, const float* wa,
+                                    const float* wb, void* dx, float* dwa, float* dba, float* dwb,
+                                    float* dbb, void* ws, size_t ws_bytes, hipStream_t stream) {
+    impala_status_t st = check_layer(__func__, prec, n, H, W, C, C);
+    if (st) return st;
+    if (prec != IMPALA_PREC_BF16 || !resblock_bwd_supported(C))
+        return fail(IMPALA_EUNSUPPORTED, "impala_resblock_bwd: bf16 with C = 16 only (got prec=%d C=%d)", int(prec), C);
+    CHECK_PTR(dwa); CHECK_PTR(dba); CHECK_PTR(dwb); CHECK_PTR(dbb);
+    if (n == 0) {
+        hipError_t he = fill_zero(dwa, int64_t(9) * C * C, stream);
+        if (he == hipSuccess) he = fill_zero(dba, C, stream);
+        if (he == hipSuccess) he = fill_zero(dwb, int64_t(9) * C * C, stream);
+        if (he == hipSuccess) he = fill_zero(dbb, C, stream);
+        return hip_status(he, "impala_resblock_bwd");
+    }
+    CHECK_PTR(dy); CHECK_PTR(t); CHECK_PTR(x); CHECK_PTR(wa); CHECK_PTR(wb); CHECK_PTR(dx); CHECK_PTR(ws);
+    const size_t need = resblock_bwd_partial_floats(C) * sizeof(float);
+    if (ws_bytes < need) return fail(IMPALA_EWORKSPACE, "impala_resblock_bwd: workspace %zu < %zu", ws_bytes, need);
+    ResBwdArgs a{};
+    a.dy = dy; a.t = t; a.x = x; a.wa = wa; a.wb = wb; a.dx = dx;
+    a.dwa = dwa; a.dba = dba; a.dwb = dwb; a.dbb = dbb;
+    a.partial = static_cast<float*>(ws); a.n = int(n); a.H = H; a.W = W;
+    PendingReduce out[2];
+    hipError_t he = resblock_bwd(C, a, stream, out);
+    if (he == hipSuccess) he = flush_pending_reduce(out[0], stream);
+    if (he == hipSuccess) he = flush_pending_reduce(out[1], stream);
+    return hip_status(he, "impala_resblock_bwd");
+}
+
 size_t impala_conv3x3_pool_wgrad_u8_workspace_bytes(impala_prec_t prec, int32_t cout) {
     if (prec != IMPALA_PREC_BF16) return 0;
     return pool_wgrad_u8_partial_floats(cout) * sizeof(float);

@@ -77,6 +77,7 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
 
     // an earlier launch's weight-gradient partials, summed first (LDS is free until staging)
     if (a.pend.nparts > 0) pending_reduce<NT>(a.pend, smem);
+    if (a.pend2.nparts > 0) pending_reduce<NT>(a.pend2, smem);
     if (tid < 16) reinterpret_cast<uint32_t*>(zero)[tid] = 0u;
     if constexpr (PDY) {
         // the dy window is built in LDS: its padding columns and zero slots are never written
@@ -521,7 +522,10 @@ size_t conv3x3_bwd_partial_floats(int cin, int cout) {
 
 hipError_t conv3x3_bwd(int cin, int cout, int mode, const ConvBwdArgs& a, hipStream_t s, PendingReduce* deferred) {
     if (deferred) deferred->nparts = 0;
-    if (a.n <= 0) return flush_pending_reduce(a.pend, s);
+    if (a.n <= 0) {
+        const hipError_t e = flush_pending_reduce(a.pend, s);
+        return e != hipSuccess ? e : flush_pending_reduce(a.pend2, s);
+    }
     const int add = a.add != nullptr, pdy = a.arg != nullptr;
 #define CB_B(CI, CO, MD, AD, PD) \
     if (cin == CI && cout == CO && mode == MD && add == AD && pdy == PD) return cb_launch<CI, CO, MD, AD, PD>(a, s, deferred);

@@ -85,6 +85,32 @@ struct PendingReduce {
 // Launches the standalone fixed-order reduce of a pending partial sum (no-op if none).
 hipError_t flush_pending_reduce(const PendingReduce& r, hipStream_t s);
 
+// ---- backward of a whole residual block, t = conv_a(relu(x)) + b_a, y = x + conv_b(relu(t)) + b_b
+// (bf16): dx = conv_a^T(conv_b^T(dy) * [t > 0]) * [x > 0] + dy and both weight gradients
+struct ResBwdArgs {
+    const void* dy;         // [n, H, W, C] gradient at the block output
+    const void* t;          // [n, H, W, C] conv_a's output as the forward stored it
+    const void* x;          // [n, H, W, C] block input
+    const float* wa; const float* wb;   // float32 HWIO [3,3,C,C]
+    void* dx;               // [n, H, W, C]
+    float* dwa; float* dba; float* dwb; float* dbb;
+    float* partial;         // workspace, resblock_bwd_partial_floats() floats
+    int n, H, W;
+    PendingReduce pend, pend2;   // earlier launches' partials, summed by this kernel first
+};
+struct RbbTile {
+    int TH, nbands, ntiles;
+    int dy_off, t_off, x_off, dt_off;   // LDS byte offsets; 64 zero bytes at offset 0
+    int tx_guard;                       // t / x windows: byte offset of the rear guard pixel
+    int dt_bytes;                       // dt window bytes
+    int pset;                           // floats per partial set (one per conv)
+    float inv_W;
+};
+bool resblock_bwd_supported(int C);
+size_t resblock_bwd_partial_floats(int C);
+// out[0] / out[1]: conv_b's / conv_a's weight-gradient partials, left for a later launch to sum
+hipError_t resblock_bwd(int C, const ResBwdArgs& a, hipStream_t s, PendingReduce out[2]);
+
 struct ConvBwdArgs {
     const void* dy;         // [n, H, W, cout] bf16; with arg: the max-pool output gradient
                             // [n, ceil(H/2), ceil(W/2), cout] of the pool this conv feeds
@@ -97,7 +123,7 @@ struct ConvBwdArgs {
     float* db;              // float32 [cout]
     float* partial;         // workspace, conv3x3_bwd_partial_floats() floats
     int n, H, W;
-    PendingReduce pend;     // an earlier launch's partials, summed by this kernel first
+    PendingReduce pend, pend2;   // earlier launches' partials, summed by this kernel first
 };
 struct CbTile {
     int TH, FR, nbands, ntiles;
@@ -132,7 +158,7 @@ struct PoolWgArgs {
     float* db;              // float32 [cout]
     float* partial;         // workspace, pool_wgrad_u8_partial_floats() floats
     int n, H, W;
-    PendingReduce pend;     // an earlier launch's partials, summed by this kernel first
+    PendingReduce pend, pend2;   // earlier launches' partials, summed by this kernel first
 };
 struct PwTile {
     int TB, nbands, ntiles;         // 2x2 pixel-block rows per band

@@ -113,6 +113,7 @@ NetPlan make_plan(const impala_net_t& net, int prec, int64_t cap, int training) 
                 if (s == 0) sc = std::max(sc, pool_wgrad_u8_partial_floats(p.C[1]));
                 sc = std::max(sc, conv3x3_bwd_partial_floats(p.C[s], p.C[s + 1]));
                 sc = std::max(sc, conv3x3_bwd_partial_floats(p.C[s + 1], p.C[s + 1]));
+                sc = std::max(sc, resblock_bwd_partial_floats(p.C[s + 1]));
             }
         }
     }
@@ -124,6 +125,7 @@ NetPlan make_plan(const impala_net_t& net, int prec, int64_t cap, int training) 
             if (s == 0) sc2 = std::max(sc2, pool_wgrad_u8_partial_floats(p.C[1]));
             sc2 = std::max(sc2, conv3x3_bwd_partial_floats(p.C[s], p.C[s + 1]));
             sc2 = std::max(sc2, conv3x3_bwd_partial_floats(p.C[s + 1], p.C[s + 1]));
+            sc2 = std::max(sc2, resblock_bwd_partial_floats(p.C[s + 1]));
         }
     p.scratch_floats = sc;
     p.scratch_bytes = (sc + sc2) * sizeof(float);
@@ -252,21 +254,26 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
     // fused conv backward launches: each one's weight-gradient reduce runs at the start of the
     // next fused launch (or a standalone reduce before any other launch), the partials
     // alternating between two buffers
+    // (a residual block's backward leaves two: one per conv)
     float* pbuf[2] = {scratch, scratch + p.scratch_floats};
-    PendingReduce pend{};
+    PendingReduce pend[2] = {};
     int pb = 0;
     auto fused_bwd = [&](int ci, int co, int mode, ConvBwdArgs c) -> hipError_t {
         c.partial = pbuf[pb];
-        c.pend = pend;
+        c.pend = pend[0];
+        c.pend2 = pend[1];
         PendingReduce nx{};
         const hipError_t e = conv3x3_bwd(ci, co, mode, c, s, &nx);
-        pend = nx;
+        pend[0] = nx;
+        pend[1].nparts = 0;
         pb ^= 1;
         return e;
     };
     auto flush = [&]() -> hipError_t {
-        const hipError_t e = flush_pending_reduce(pend, s);
-        pend.nparts = 0;
+        hipError_t e = flush_pending_reduce(pend[0], s);
+        if (e == hipSuccess) e = flush_pending_reduce(pend[1], s);
+        pend[0].nparts = 0;
+        pend[1].nparts = 0;
         return e;
     };
     for (int st = 2; st >= 0; --st) {
@@ -275,6 +282,20 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
             int fa, fb;
             others(gy, fa, fb);
             const int k0 = 1 + 2 * r, k1 = 2 + 2 * r;
+            if (p.prec == BF16 && resblock_bwd_supported(C)) {
+                // the whole block in one pass: dt stays on chip
+                ResBwdArgs rb{};
+                rb.dy = G[gy]; rb.t = ws + p.t[st][r]; rb.x = ws + p.x[st][r];
+                rb.wa = params + po.conv_w[st][k0]; rb.wb = params + po.conv_w[st][k1]; rb.dx = G[fa];
+                rb.dwa = grads + po.conv_w[st][k0]; rb.dba = grads + po.conv_b[st][k0];
+                rb.dwb = grads + po.conv_w[st][k1]; rb.dbb = grads + po.conv_b[st][k1];
+                rb.partial = pbuf[pb]; rb.pend = pend[0]; rb.pend2 = pend[1];
+                rb.n = int(n); rb.H = Hs; rb.W = Ws;
+                CB_TRY(resblock_bwd(C, rb, s, pend));
+                pb ^= 1;
+                gy = fa;
+                continue;
+            }
             if (p.prec == BF16 && conv3x3_bwd_supported(C, C, IN_RELU, 1, 0)) {
                 // each conv's input and weight gradients from one staging of its dy and input
                 ConvBwdArgs c1{};
@@ -322,8 +343,10 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
             pa.arg = reinterpret_cast<const uint8_t*>(ws + p.idx[0]);
             pa.dw = grads + po.conv_w[0][0]; pa.db = grads + po.conv_b[0][0]; pa.partial = pbuf[pb];
             pa.n = int(n); pa.H = p.H[0]; pa.W = p.W[0];
-            pa.pend = pend;   // the previous fused launch's reduce runs first in this kernel
-            pend.nparts = 0;
+            pa.pend = pend[0];   // the previous fused launch's reduces run first in this kernel
+            pa.pend2 = pend[1];
+            pend[0].nparts = 0;
+            pend[1].nparts = 0;
             CB_TRY(pool_wgrad_u8(C, pa, s));
             continue;
         }

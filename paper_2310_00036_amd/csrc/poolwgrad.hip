@@ -58,6 +58,7 @@ __global__ __launch_bounds__(64 * NW, 4) void pool_wgrad_u8_kernel(PoolWgArgs a,
 
     // an earlier launch's weight-gradient partials, summed first (LDS is free until staging)
     if (a.pend.nparts > 0) pending_reduce<NT>(a.pend, smem);
+    if (a.pend2.nparts > 0) pending_reduce<NT>(a.pend2, smem);
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, r16 = lane & 15, jj = r16 >> 2, m = r16 & 3;
@@ -335,7 +336,10 @@ size_t pool_wgrad_u8_partial_floats(int cout) {
 }
 
 hipError_t pool_wgrad_u8(int cout, const PoolWgArgs& a, hipStream_t s) {
-    if (a.n <= 0) return flush_pending_reduce(a.pend, s);
+    if (a.n <= 0) {
+        const hipError_t e = flush_pending_reduce(a.pend, s);
+        return e != hipSuccess ? e : flush_pending_reduce(a.pend2, s);
+    }
     if (cout == 16) return pw_launch<16>(a, s);
     if (cout == 32) return pw_launch<32>(a, s);
     return hipErrorInvalidValue;

@@ -246,6 +246,92 @@ def test_conv_backward_fused(case):
     G.assert_sum_close(G.host(db), want_b, abs_b, 1e-5, "conv_bwd db")
 
 
+# (n, H, W, C): the residual blocks' backward, base and ragged bands, tiny frames
+RES_BWD_CASES = [(3, 42, 42, 16), (2, 17, 23, 16), (4, 9, 7, 16), (1, 84, 84, 16), (5, 3, 4, 16), (2, 43, 11, 16)]
+
+
+def _resblock_bwd(n, H, W, C, dy, t, x, wa, wb):
+    dx = G.empty_act((n, H, W, C), G.BF16)
+    out = [G.dev_f32(np.full(shape, np.nan)) for shape in ((3, 3, C, C), (C,), (3, 3, C, C), (C,))]
+    ws = G.ws_bytes(P.impala_resblock_bwd_workspace_bytes(G.BF16, C))
+    P.impala_resblock_bwd(G.BF16, n, H, W, C, dy, t, x, wa, wb, dx, *out, ws)
+    G.sync()
+    return G.host(dx), [G.host(o) for o in out]
+
+
+@pytest.mark.parametrize("case", RES_BWD_CASES, ids=lambda c: "n%d_%dx%d_c%d" % c)
+def test_resblock_backward_fused(case):
+    """Whole residual-block backward in one pass (bf16) against the exact sums. dy and conv_b's
+    weights are small integers, so dt = conv_b^T(dy) * [t > 0] is an integer below 256: exact in
+    float32 and in bf16 on both sides, and dx, the weight and bias gradients are checked to the
+    usual bounds (dx to 1 bf16 ulp of the exact value, the sums to float32 accumulation)."""
+    n, H, W, C = case
+    rng = np.random.default_rng(53)
+    x = G.q(rng.standard_normal((n, H, W, C)), G.BF16)
+    t = G.q(rng.standard_normal((n, H, W, C)), G.BF16)
+    dy = rng.choice([-1.0, 0.0, 0.0, 1.0], size=(n, H, W, C))
+    wb = rng.choice([-1.0, 0.0, 0.0, 1.0], size=(3, 3, C, C)).astype(np.float32)
+    wa = (rng.standard_normal((3, 3, C, C)) * np.sqrt(2.0 / (9 * C))).astype(np.float32)
+    waq = G.q(wa, G.BF16)
+    dt = onet.conv3x3_dgrad(dy, wb.astype(np.float64)) * (t > 0)
+    assert np.array_equal(G.q(dt, G.BF16), dt) and np.abs(dt).max() < 256
+    want_dx = onet.conv3x3_dgrad(dt, waq) * (x > 0) + dy
+    abs_dx = onet.conv3x3_dgrad(np.abs(dt), np.abs(waq)) * (x > 0) + np.abs(dy)
+    rt, rx = _relu(t), _relu(x)
+    want_wb, want_bb = onet.conv3x3_wgrad(rt, dy)
+    abs_wb, abs_bb = onet.conv3x3_wgrad(np.abs(rt), np.abs(dy))
+    want_wa, want_ba = onet.conv3x3_wgrad(rx, dt)
+    abs_wa, abs_ba = onet.conv3x3_wgrad(np.abs(rx), np.abs(dt))
+    got_dx, (dwa, dba, dwb, dbb) = _resblock_bwd(n, H, W, C, G.dev_act(dy, G.BF16), G.dev_act(t, G.BF16),
+                                                 G.dev_act(x, G.BF16), G.dev_f32(wa), G.dev_f32(wb))
+    G.assert_bf16_ulp(got_dx, want_dx, abs_dx, "resblock_bwd dx")
+    G.assert_sum_close(dwb, want_wb, abs_wb, 1e-5, "resblock_bwd dwb")
+    G.assert_sum_close(dbb, want_bb, abs_bb, 1e-5, "resblock_bwd dbb")
+    G.assert_sum_close(dwa, want_wa, abs_wa, 1e-5, "resblock_bwd dwa")
+    G.assert_sum_close(dba, want_ba, abs_ba, 1e-5, "resblock_bwd dba")
+
+
+@pytest.mark.parametrize("case", [(3, 42, 42, 16), (2, 17, 23, 16), (5, 3, 4, 16)], ids=lambda c: "n%d_%dx%d_c%d" % c)
+def test_resblock_backward_matches_two_conv_backwards(case):
+    """On real-valued data the fused block backward equals the two single-conv backward passes
+    it replaces: dt is rounded from the same float32 sums, so dx is bit-identical; the weight
+    gradients are the same float32 sums in another order."""
+    n, H, W, C = case
+    rng = np.random.default_rng(59)
+    x, t, dy = (G.q(rng.standard_normal((n, H, W, C)), G.BF16) for _ in range(3))
+    wa, wb = (rng.standard_normal((2, 3, 3, C, C)) * np.sqrt(2.0 / (9 * C))).astype(np.float32)
+    dyd, td, xd, wad, wbd = (G.dev_act(dy, G.BF16), G.dev_act(t, G.BF16), G.dev_act(x, G.BF16), G.dev_f32(wa),
+                             G.dev_f32(wb))
+    got_dx, (dwa, dba, dwb, dbb) = _resblock_bwd(n, H, W, C, dyd, td, xd, wad, wbd)
+    ws = G.ws_bytes(P.impala_conv3x3_bwd_workspace_bytes(G.BF16, C, C))
+    dt = G.empty_act((n, H, W, C), G.BF16)
+    dx2 = G.empty_act((n, H, W, C), G.BF16)
+    ref = [G.dev_f32(np.zeros(shape)) for shape in ((3, 3, C, C), (C,), (3, 3, C, C), (C,))]
+    P.impala_conv3x3_bwd(G.BF16, n, H, W, C, C, dyd, td, P.X_RELU, wbd, None, dt, ref[2], ref[3], ws)
+    P.impala_conv3x3_bwd(G.BF16, n, H, W, C, C, dt, xd, P.X_RELU, wad, dyd, dx2, ref[0], ref[1], ws)
+    G.sync()
+    np.testing.assert_array_equal(got_dx, G.host(dx2))
+    dt_h = G.host(dt)
+    abs_wa, abs_ba = onet.conv3x3_wgrad(np.abs(_relu(x)), np.abs(dt_h))
+    abs_wb, abs_bb = onet.conv3x3_wgrad(np.abs(_relu(t)), np.abs(dy))
+    for got, want, ab, what in ((dwa, ref[0], abs_wa, "dwa"), (dba, ref[1], abs_ba, "dba"),
+                                (dwb, ref[2], abs_wb, "dwb"), (dbb, ref[3], abs_bb, "dbb")):
+        G.assert_sum_close(got, G.host(want), 2.0 * ab, 1e-5, "resblock_bwd vs two launches " + what)
+
+
+def test_resblock_backward_rejects_unsupported():
+    z = G.dev_act(np.zeros((1, 8, 8, 32)), G.BF16)
+    w = G.dev_f32(np.zeros((3, 3, 32, 32)))
+    g = [G.dev_f32(np.zeros(shape)) for shape in ((3, 3, 32, 32), (32,), (3, 3, 32, 32), (32,))]
+    with pytest.raises(P.LibraryError):   # 32 channels: not in the fused set
+        P.impala_resblock_bwd(G.BF16, 1, 8, 8, 32, z, z, z, w, w, z, *g, G.ws_bytes(1 << 22))
+    b16 = G.dev_act(np.zeros((1, 8, 8, 16)), G.BF16)
+    w16 = G.dev_f32(np.zeros((3, 3, 16, 16)))
+    g16 = [G.dev_f32(np.zeros(shape)) for shape in ((3, 3, 16, 16), (16,), (3, 3, 16, 16), (16,))]
+    with pytest.raises(P.LibraryError):   # too small a workspace
+        P.impala_resblock_bwd(G.BF16, 1, 8, 8, 16, b16, b16, b16, w16, w16, b16, *g16, G.ws_bytes(16))
+
+
 # (n, H, W, cin, cout): stage entries fed by a max-pool (base and ragged, odd and even padding)
 CONV_BWD_POOL_CASES = [(3, 42, 42, 16, 32), (2, 21, 21, 32, 32), (4, 42, 42, 16, 16), (2, 17, 23, 16, 32),
                        (5, 9, 7, 32, 32), (1, 84, 84, 16, 16), (3, 11, 11, 32, 32), (6, 4, 5, 16, 16)]
