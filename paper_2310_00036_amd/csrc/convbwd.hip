@@ -31,6 +31,7 @@
 #include "kernels.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace cb {
 
@@ -313,46 +314,84 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
         // x-window pixel p - TW - 1 + tap, and every address advances by a constant per k-step.
         // Lane (g, 4jj+m) takes pixels o = 16*half + 4g + jj (dy / x channels 4m.. of a block).
         // Between frames of a multi-frame tile the two halo rows are outside the image: zero dy.
+        // With 16 output channels, specialised per wave, so that each column block's kind
+        // (loaded or bias) is known at compile time and the k-step loop carries no branches.
         {
             const int L = ((nf - 1) * TR + the) * TW;   // contracted window pixels
-            const int nfull = L >> 5;
-            const int o0 = 4 * g + jj;
-            const unsigned char* ap = dyw + (TW + o0) * DYP + 8 * m;
-            const unsigned char* bp = xw + (o0 - 1) * XPB;
-            auto kstep = [&](const unsigned char* a0, const unsigned char* a1, const unsigned char* b0,
-                             const unsigned char* b1) {
-                uint4 af[MTO];
+            auto run = [&](auto wv) {
+                const int WV = wv;   // a compile-time constant when specialised
+                const int nfull = L >> 5;
+                const int o0 = 4 * g + jj;
+                const unsigned char* ap = dyw + (TW + o0) * DYP + 8 * m;
+                const unsigned char* bp = xw + (o0 - 1) * XPB;
+                auto kstep = [&](const unsigned char* a0, const unsigned char* a1, const unsigned char* b0,
+                                 const unsigned char* b1) {
+                    uint4 af[MTO];
 #pragma unroll
-                for (int mo = 0; mo < MTO; ++mo) {
-                    const uint2 lo = lds_read_tr16(a0 + mo * 32);   // a0, a1: zero for pixels past L
-                    const uint2 hi = lds_read_tr16(a1 + mo * 32);
-                    af[mo] = make_uint4(lo.x, lo.y, hi.x, hi.y);
-                }
-#pragma unroll
-                for (int i = 0; i < TPW; ++i) {
-                    const int nb = wave + NW * i;
-                    if (nb >= NBB) continue;
-                    uint4 bf = ones;
-                    if (nb < NB) {
-                        const uint2 lo = lds_read_tr16(b0 + wboff[i]);
-                        const uint2 hi = lds_read_tr16(b1 + wboff[i]);
-                        bf = make_uint4(lo.x, lo.y, hi.x, hi.y);
+                    for (int mo = 0; mo < MTO; ++mo) {
+                        const uint2 lo = lds_read_tr16(a0 + mo * 32);   // a0, a1: zero for pixels past L
+                        const uint2 hi = lds_read_tr16(a1 + mo * 32);
+                        af[mo] = make_uint4(lo.x, lo.y, hi.x, hi.y);
                     }
 #pragma unroll
-                    for (int mo = 0; mo < MTO; ++mo) wacc[i][mo] = PrecBF16::mma(af[mo], bf, wacc[i][mo]);
+                    for (int i = 0; i < TPW; ++i) {
+                        const int nb = WV + NW * i;
+                        if constexpr (MTO == 1) {
+                            if (nb < NB) {
+                                const uint2 lo = lds_read_tr16(b0 + wboff[i]);
+                                const uint2 hi = lds_read_tr16(b1 + wboff[i]);
+                                wacc[i][0] = PrecBF16::mma(af[0], make_uint4(lo.x, lo.y, hi.x, hi.y), wacc[i][0]);
+                            } else if (nb == NB) {   // the bias block: a column of ones
+                                wacc[i][0] = PrecBF16::mma(af[0], ones, wacc[i][0]);
+                            }
+                        } else {
+                            if (nb >= NBB) continue;
+                            uint4 bf = ones;   // the bias block: a column of ones
+                            if (nb < NB) {
+                                const uint2 lo = lds_read_tr16(b0 + wboff[i]);
+                                const uint2 hi = lds_read_tr16(b1 + wboff[i]);
+                                bf = make_uint4(lo.x, lo.y, hi.x, hi.y);
+                            }
+#pragma unroll
+                            for (int mo = 0; mo < MTO; ++mo) wacc[i][mo] = PrecBF16::mma(af[mo], bf, wacc[i][mo]);
+                        }
+                    }
+                };
+                int ks = 0;
+                if constexpr (MTO == 1) {   // two k-steps per trip: half the pointer updates
+                    for (; ks + 2 <= nfull; ks += 2) {
+                        kstep(ap, ap + 16 * DYP, bp, bp + 16 * XPB);
+                        kstep(ap + 32 * DYP, ap + 48 * DYP, bp + 32 * XPB, bp + 48 * XPB);
+                        ap += 64 * DYP;
+                        bp += 64 * XPB;
+                    }
+                }
+                for (; ks < nfull; ++ks) {
+                    kstep(ap, ap + 16 * DYP, bp, bp + 16 * XPB);
+                    ap += 32 * DYP;
+                    bp += 32 * XPB;
+                }
+                if (L & 31) {   // the last, partial k-step: pixels past L read zero dy
+                    const int o = nfull * 32 + o0;
+                    const bool ok0 = o < L, ok1 = o + 16 < L;
+                    kstep(ok0 ? ap : zero, ok1 ? ap + 16 * DYP : zero, ok0 ? bp : xw - XPB,
+                          ok1 ? bp + 16 * XPB : xw - XPB);
                 }
             };
-#pragma unroll 2
-            for (int ks = 0; ks < nfull; ++ks) {
-                kstep(ap, ap + 16 * DYP, bp, bp + 16 * XPB);
-                ap += 32 * DYP;
-                bp += 32 * XPB;
-            }
-            if (L & 31) {   // the last, partial k-step: pixels past L read zero dy
-                const int o = nfull * 32 + o0;
-                const bool ok0 = o < L, ok1 = o + 16 < L;
-                kstep(ok0 ? ap : zero, ok1 ? ap + 16 * DYP : zero, ok0 ? bp : xw - XPB,
-                      ok1 ? bp + 16 * XPB : xw - XPB);
+            if constexpr (MTO == 1) {
+                static_assert(NW == 8, "one specialisation per wave");
+                switch (wave) {
+                    case 0: run(std::integral_constant<int, 0>{}); break;
+                    case 1: run(std::integral_constant<int, 1>{}); break;
+                    case 2: run(std::integral_constant<int, 2>{}); break;
+                    case 3: run(std::integral_constant<int, 3>{}); break;
+                    case 4: run(std::integral_constant<int, 4>{}); break;
+                    case 5: run(std::integral_constant<int, 5>{}); break;
+                    case 6: run(std::integral_constant<int, 6>{}); break;
+                    default: run(std::integral_constant<int, 7>{}); break;
+                }
+            } else {
+                run(wave);   // 32 output channels: the registers afford no specialised copies
             }
         }
 

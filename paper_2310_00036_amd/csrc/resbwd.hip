@@ -25,6 +25,7 @@
 #include "kernels.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace cb {
 
@@ -154,43 +155,66 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_bwd_kernel(ResBwdArgs a, 
     // o = 16*half + 4g + jj (channels 4m.. of a 16-channel block).
     auto wgrad = [&](const unsigned char* dwin, int drow0, const unsigned char* bwin, const unsigned char* bguard,
                      int L, cb_f32x4 (&wacc)[TPW][MT]) {
-        const int nfull = L >> 5;
-        const int o0 = 4 * g + jj;
-        const unsigned char* ap = dwin + (drow0 * TW + o0) * DYP + 8 * m;
-        const unsigned char* bp = bwin + (o0 - 1) * XPB;
-        auto kstep = [&](const unsigned char* a0, const unsigned char* a1, const unsigned char* b0,
-                         const unsigned char* b1) {
-            uint4 af[MT];
+        // specialised per wave, so that each column block's kind (loaded or bias) is known at
+        // compile time and the k-step loop carries no branches
+        auto run = [&](auto wv) {
+            constexpr int WV = decltype(wv)::value;
+            const int nfull = L >> 5;
+            const int o0 = 4 * g + jj;
+            const unsigned char* ap = dwin + (drow0 * TW + o0) * DYP + 8 * m;
+            const unsigned char* bp = bwin + (o0 - 1) * XPB;
+            auto kstep = [&](const unsigned char* a0, const unsigned char* a1, const unsigned char* b0,
+                             const unsigned char* b1) {
+                uint4 af[MT];
 #pragma unroll
-            for (int mo = 0; mo < MT; ++mo) {
-                const uint2 lo = lds_read_tr16(a0 + mo * 32);   // a0, a1: zero past L
-                const uint2 hi = lds_read_tr16(a1 + mo * 32);
-                af[mo] = make_uint4(lo.x, lo.y, hi.x, hi.y);
-            }
-#pragma unroll
-            for (int i = 0; i < TPW; ++i) {
-                const int nb = wave + NW * i;
-                if (nb >= NBB) continue;
-                uint4 bf = ones;
-                if (nb < NB) {
-                    const uint2 lo = lds_read_tr16(b0 + wboff[i]);
-                    const uint2 hi = lds_read_tr16(b1 + wboff[i]);
-                    bf = make_uint4(lo.x, lo.y, hi.x, hi.y);
+                for (int mo = 0; mo < MT; ++mo) {
+                    const uint2 lo = lds_read_tr16(a0 + mo * 32);   // a0, a1: zero past L
+                    const uint2 hi = lds_read_tr16(a1 + mo * 32);
+                    af[mo] = make_uint4(lo.x, lo.y, hi.x, hi.y);
                 }
 #pragma unroll
-                for (int mo = 0; mo < MT; ++mo) wacc[i][mo] = PrecBF16::mma(af[mo], bf, wacc[i][mo]);
+                for (int i = 0; i < TPW; ++i) {
+                    const int nb = WV + NW * i;
+                    if (nb < NB) {
+                        const uint2 lo = lds_read_tr16(b0 + wboff[i]);
+                        const uint2 hi = lds_read_tr16(b1 + wboff[i]);
+                        const uint4 bf = make_uint4(lo.x, lo.y, hi.x, hi.y);
+#pragma unroll
+                        for (int mo = 0; mo < MT; ++mo) wacc[i][mo] = PrecBF16::mma(af[mo], bf, wacc[i][mo]);
+                    } else if (nb == NB) {   // the bias block: a column of ones
+#pragma unroll
+                        for (int mo = 0; mo < MT; ++mo) wacc[i][mo] = PrecBF16::mma(af[mo], ones, wacc[i][mo]);
+                    }
+                }
+            };
+            int ks = 0;
+            for (; ks + 2 <= nfull; ks += 2) {   // two k-steps per trip: half the pointer updates
+                kstep(ap, ap + 16 * DYP, bp, bp + 16 * XPB);
+                kstep(ap + 32 * DYP, ap + 48 * DYP, bp + 32 * XPB, bp + 48 * XPB);
+                ap += 64 * DYP;
+                bp += 64 * XPB;
+            }
+            if (ks < nfull) {
+                kstep(ap, ap + 16 * DYP, bp, bp + 16 * XPB);
+                ap += 32 * DYP;
+                bp += 32 * XPB;
+            }
+            if (L & 31) {   // the last, partial k-step
+                const int o = nfull * 32 + o0;
+                const bool ok0 = o < L, ok1 = o + 16 < L;
+                kstep(ok0 ? ap : zero, ok1 ? ap + 16 * DYP : zero, ok0 ? bp : bguard, ok1 ? bp + 16 * XPB : bguard);
             }
         };
-#pragma unroll 2
-        for (int ks = 0; ks < nfull; ++ks) {
-            kstep(ap, ap + 16 * DYP, bp, bp + 16 * XPB);
-            ap += 32 * DYP;
-            bp += 32 * XPB;
-        }
-        if (L & 31) {   // the last, partial k-step
-            const int o = nfull * 32 + o0;
-            const bool ok0 = o < L, ok1 = o + 16 < L;
-            kstep(ok0 ? ap : zero, ok1 ? ap + 16 * DYP : zero, ok0 ? bp : bguard, ok1 ? bp + 16 * XPB : bguard);
+        static_assert(NW == 8, "one specialisation per wave");
+        switch (wave) {
+            case 0: run(std::integral_constant<int, 0>{}); break;
+            case 1: run(std::integral_constant<int, 1>{}); break;
+            case 2: run(std::integral_constant<int, 2>{}); break;
+            case 3: run(std::integral_constant<int, 3>{}); break;
+            case 4: run(std::integral_constant<int, 4>{}); break;
+            case 5: run(std::integral_constant<int, 5>{}); break;
+            case 6: run(std::integral_constant<int, 6>{}); break;
+            default: run(std::integral_constant<int, 7>{}); break;
         }
     };
 
