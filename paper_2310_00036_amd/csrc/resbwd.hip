@@ -49,7 +49,10 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_bwd_kernel(ResBwdArgs a, 
     constexpr int NT = 64 * NW;
     constexpr int DSL = G::DSL, DYP = G::DYP, XPB = G::XPB, XSL = G::XSL;
     constexpr int MT = G::MT, KSD = G::KSD, NB = G::NB, NBB = G::NBB;
-    constexpr int TPW = (NBB + NW - 1) / NW;   // weight-gradient column blocks per wave
+    // weight gradients: waves 0 .. NW/2-1 form conv_b's, the others conv_a's, each wave TPW
+    // column blocks, so each dy / dt fragment is read by half the waves
+    constexpr int NWG = NW / 2;
+    constexpr int TPW = (NBB + NWG - 1) / NWG;   // weight-gradient column blocks per wave
     constexpr int CB16 = C / 16;
     static_assert(NW % MT == 0, "waves split evenly over the channel blocks");
 
@@ -113,23 +116,21 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_bwd_kernel(ResBwdArgs a, 
         if constexpr (C < 32) return dboff[ks];
         else return (ks / (C / 32) / 3) * twdy + (ks / (C / 32) % 3) * DYP + ((ks % (C / 32)) * 4 + g) * 16;
     };
-    // weight-gradient column blocks nb = wave + NW * i (16 input channels of one tap, or the
-    // bias block), each for all C/16 output-channel blocks
+    // weight-gradient column blocks nb = wg + NWG * i (16 input channels of one tap, or the
+    // bias block), each for all C/16 output-channel blocks, of conv_b (grp 0) or conv_a (grp 1)
+    const int wg = wave % NWG, grp = wave / NWG;
     int wboff[TPW];
 #pragma unroll
     for (int i = 0; i < TPW; ++i) {
-        const int nb = wave + NW * i;
+        const int nb = wg + NWG * i;
         const int tap = nb / CB16, cb = nb % CB16;
         wboff[i] = nb < NB ? ((tap / 3) * TW + tap % 3) * XPB + (cb * 16 + 4 * m) * 2 : 0;
     }
-    cb_f32x4 wacc_a[TPW][MT], wacc_b[TPW][MT];
+    cb_f32x4 wacc[TPW][MT];
 #pragma unroll
     for (int i = 0; i < TPW; ++i)
 #pragma unroll
-        for (int mo = 0; mo < MT; ++mo) {
-            wacc_a[i][mo] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
-            wacc_b[i][mo] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
-        }
+        for (int mo = 0; mo < MT; ++mo) wacc[i][mo] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
     const uint4 ones = make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
 
     // ---- staging offsets, tile-invariant per lane (slot k of this wave: j = (wave + NW*k)*64
@@ -154,11 +155,11 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_bwd_kernel(ResBwdArgs a, 
     // the own rows pairs with bwin pixel idx - 1 + tap offset. Lane (g, 4jj+m) takes pixels
     // o = 16*half + 4g + jj (channels 4m.. of a 16-channel block).
     auto wgrad = [&](const unsigned char* dwin, int drow0, const unsigned char* bwin, const unsigned char* bguard,
-                     int L, cb_f32x4 (&wacc)[TPW][MT]) {
+                     int L) {
         // specialised per wave, so that each column block's kind (loaded or bias) is known at
         // compile time and the k-step loop carries no branches
         auto run = [&](auto wv) {
-            constexpr int WV = decltype(wv)::value;
+            constexpr int WG = decltype(wv)::value;
             const int nfull = L >> 5;
             const int o0 = 4 * g + jj;
             const unsigned char* ap = dwin + (drow0 * TW + o0) * DYP + 8 * m;
@@ -174,7 +175,7 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_bwd_kernel(ResBwdArgs a, 
                 }
 #pragma unroll
                 for (int i = 0; i < TPW; ++i) {
-                    const int nb = WV + NW * i;
+                    const int nb = WG + NWG * i;
                     if (nb < NB) {
                         const uint2 lo = lds_read_tr16(b0 + wboff[i]);
                         const uint2 hi = lds_read_tr16(b1 + wboff[i]);
@@ -205,16 +206,12 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_bwd_kernel(ResBwdArgs a, 
                 kstep(ok0 ? ap : zero, ok1 ? ap + 16 * DYP : zero, ok0 ? bp : bguard, ok1 ? bp + 16 * XPB : bguard);
             }
         };
-        static_assert(NW == 8, "one specialisation per wave");
-        switch (wave) {
+        static_assert(NWG == 4, "one specialisation per wave of a group");
+        switch (wg) {
             case 0: run(std::integral_constant<int, 0>{}); break;
             case 1: run(std::integral_constant<int, 1>{}); break;
             case 2: run(std::integral_constant<int, 2>{}); break;
-            case 3: run(std::integral_constant<int, 3>{}); break;
-            case 4: run(std::integral_constant<int, 4>{}); break;
-            case 5: run(std::integral_constant<int, 5>{}); break;
-            case 6: run(std::integral_constant<int, 6>{}); break;
-            default: run(std::integral_constant<int, 7>{}); break;
+            default: run(std::integral_constant<int, 3>{}); break;
         }
     };
 
@@ -289,8 +286,6 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_bwd_kernel(ResBwdArgs a, 
                 }
             }
         }
-        // ---- conv_b's weight gradient: dy (own rows from dy-window row 2) against relu(t)
-        wgrad(dyw, 2, tw, tw - XPB, the * TW, wacc_b);
         __syncthreads();   // the dt window is complete
 
         // ---- dx = conv_a^T(dt) * [x > 0] + dy on the band's rows
@@ -317,24 +312,23 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_bwd_kernel(ResBwdArgs a, 
                 }
             }
         }
-        // ---- conv_a's weight gradient: dt (own rows from dt-window row 1) against relu(x)
-        wgrad(dtw, 1, xw, xw - XPB, the * TW, wacc_a);
+        // ---- the weight gradients: conv_b's, dy (own rows from dy-window row 2) against
+        // relu(t), by the first half of the waves; conv_a's, dt (own rows from dt-window row
+        // 1) against relu(x), by the second
+        if (grp == 0) wgrad(dyw, 2, tw, tw - XPB, the * TW);
+        else wgrad(dtw, 1, xw, xw - XPB, the * TW);
     }
 
     // ---- this workgroup's partials: conv_b's set, then conv_a's, each [mo*NBB + nb][co 16][ci 16]
-    float* pb = a.partial + int64_t(blockIdx.x) * G::PSTRIDE;
-    float* pa = a.partial + t.pset + int64_t(blockIdx.x) * G::PSTRIDE;
+    float* part = a.partial + (grp == 0 ? 0 : t.pset) + int64_t(blockIdx.x) * G::PSTRIDE;
 #pragma unroll
     for (int i = 0; i < TPW; ++i) {
-        const int nb = wave + NW * i;
+        const int nb = wg + NWG * i;
         if (nb < NBB) {
 #pragma unroll
             for (int mo = 0; mo < MT; ++mo)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    pb[(mo * NBB + nb) * 256 + (4 * g + e) * 16 + r16] = wacc_b[i][mo][e];
-                    pa[(mo * NBB + nb) * 256 + (4 * g + e) * 16 + r16] = wacc_a[i][mo][e];
-                }
+                for (int e = 0; e < 4; ++e) part[(mo * NBB + nb) * 256 + (4 * g + e) * 16 + r16] = wacc[i][mo][e];
         }
     }
 }
