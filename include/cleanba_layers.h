@@ -99,7 +99,7 @@ impala_status_t impala_conv3x3_bwd(impala_prec_t prec, int64_t n, int32_t H, int
                                    float* db, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* The backward pass of one residual block of Section 5's IMPALA-ResNet in one pass, bf16
- * only (C = 16), Algorithm 1's back-propagation through the block that impala_resblock_fwd
+ * only (C = 16 or 32), Algorithm 1's back-propagation through the block that impala_resblock_fwd
  * computes: with t = conv3x3_same(relu(x), wa) + ba, y = x + conv3x3_same(relu(t), wb) + bb
  * (wa, wb are that call's w1, w2) and dy the gradient at y:
  *   dt = conv3x3_same^T(dy, wb) * (t > 0), rounded to bf16;

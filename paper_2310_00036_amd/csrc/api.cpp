@@ -663,7 +663,7 @@ impala_status_t impala_resblock_bwd(impala_prec_t prec, int64_t n, int32_t H, in
     impala_status_t st = check_layer(__func__, prec, n, H, W, C, C);
     if (st) return st;
     if (prec != IMPALA_PREC_BF16 || !resblock_bwd_supported(C))
-        return fail(IMPALA_EUNSUPPORTED, "impala_resblock_bwd: bf16 with C = 16 only (got prec=%d C=%d)", int(prec), C);
+        return fail(IMPALA_EUNSUPPORTED, "impala_resblock_bwd: bf16 with C = 16 or 32 only (got prec=%d C=%d)", int(prec), C);
     CHECK_PTR(dwa); CHECK_PTR(dba); CHECK_PTR(dwb); CHECK_PTR(dbb);
     if (n == 0) {
         hipError_t he = fill_zero(dwa, int64_t(9) * C * C, stream);

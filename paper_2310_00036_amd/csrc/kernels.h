@@ -107,6 +107,7 @@ struct RbbTile {
     float inv_W;
 };
 bool resblock_bwd_supported(int C);
+bool resblock_bwd_preferred(int C, int H, int W);   // over two fused conv backward launches
 size_t resblock_bwd_partial_floats(int C);
 // out[0] / out[1]: conv_b's / conv_a's weight-gradient partials, left for a later launch to sum
 hipError_t resblock_bwd(int C, const ResBwdArgs& a, hipStream_t s, PendingReduce out[2]);

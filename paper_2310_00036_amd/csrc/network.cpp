@@ -282,7 +282,7 @@ hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* ob
             int fa, fb;
             others(gy, fa, fb);
             const int k0 = 1 + 2 * r, k1 = 2 + 2 * r;
-            if (p.prec == BF16 && resblock_bwd_supported(C)) {
+            if (p.prec == BF16 && resblock_bwd_preferred(C, Hs, Ws)) {
                 // the whole block in one pass: dt stays on chip
                 ResBwdArgs rb{};
                 rb.dy = G[gy]; rb.t = ws + p.t[st][r]; rb.x = ws + p.x[st][r];

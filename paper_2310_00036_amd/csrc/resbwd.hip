@@ -39,12 +39,17 @@ struct RbbGeom {
     static constexpr int KSD = (9 * C + 31) / 32;          // input-gradient k-steps
     static constexpr int NB = 9 * C / 16, NBB = NB + 1;    // weight-gradient column blocks (+ bias)
     static constexpr int PSTRIDE = MT * NBB * 256;         // floats per workgroup partial, one conv
-    static constexpr int MAXD = 4, MAXX = 4;               // staging slots per lane (8 waves)
+    static constexpr int MAXD = C >= 32 ? 6 : 4, MAXX = C >= 32 ? 6 : 4;   // staging slots per lane (8 waves)
+    // 16 channels: two workgroups per CU (4 waves per SIMD, 128 registers); 32 channels hold
+    // both convs' input-gradient weights (72 registers) and wider accumulators: one
+    // workgroup per CU with 256 registers and all of the LDS
+    static constexpr int WPS = C >= 32 ? 2 : 4;
+    static constexpr size_t LDS_TARGET = C >= 32 ? 160 * 1024 : 80 * 1024;
     __host__ __device__ static int blocks(int slots) { return (slots + 63) / 64; }
 };
 
 template <int C, int NW>
-__global__ __launch_bounds__(64 * NW, 4) void resblock_bwd_kernel(ResBwdArgs a, RbbTile t) {
+__global__ __launch_bounds__(64 * NW, RbbGeom<C>::WPS) void resblock_bwd_kernel(ResBwdArgs a, RbbTile t) {
     using G = RbbGeom<C>;
     constexpr int NT = 64 * NW;
     constexpr int DSL = G::DSL, DYP = G::DYP, XPB = G::XPB, XSL = G::XSL;
@@ -336,7 +341,6 @@ __global__ __launch_bounds__(64 * NW, 4) void resblock_bwd_kernel(ResBwdArgs a, 
 namespace {
 
 constexpr int kRbbWaves = 8;
-constexpr size_t kRbbLdsTarget = 80 * 1024;   // two 8-wave workgroups per CU
 constexpr size_t kRbbPartBytes = 24u << 20;   // both partial sets
 
 template <int C>
@@ -365,7 +369,7 @@ hipError_t rbb_launch(const ResBwdArgs& a, hipStream_t s, PendingReduce out[2]) 
     };
     const size_t limit = std::min<size_t>(lds_limit(), 160 * 1024);
     int thmax = H;
-    while (thmax > 1 && (lds(thmax) > kRbbLdsTarget || !fits(thmax))) --thmax;
+    while (thmax > 1 && (lds(thmax) > G::LDS_TARGET || !fits(thmax))) --thmax;
     if (lds(thmax) > limit || !fits(thmax)) return hipErrorInvalidValue;
     if (int64_t(H) * W * C * 2 >= (int64_t(1) << 31)) return hipErrorInvalidValue;
     const int nb0 = (H + thmax - 1) / thmax;
@@ -395,10 +399,16 @@ hipError_t rbb_launch(const ResBwdArgs& a, hipStream_t s, PendingReduce out[2]) 
 
 }  // namespace
 
-bool resblock_bwd_supported(int C) { return C == 16; }
+bool resblock_bwd_supported(int C) { return C == 16 || C == 32; }
+
+// With 32 channels the block backward runs one workgroup per CU, which exposes each tile's
+// staging: it beats the two conv backward launches on whole-frame tiles (11x11: 63 against
+// 69 us for 2048 frames) but not on banded ones (21x21: 159 against 152 us).
+bool resblock_bwd_preferred(int C, int H, int W) { return C == 16 || (C == 32 && H * W <= 256); }
 
 size_t resblock_bwd_partial_floats(int C) {
     if (C == 16) return 2 * size_t(rbb_parts_cap<16>()) * RbbGeom<16>::PSTRIDE;
+    if (C == 32) return 2 * size_t(rbb_parts_cap<32>()) * RbbGeom<32>::PSTRIDE;
     return 0;
 }
 
@@ -410,6 +420,7 @@ hipError_t resblock_bwd(int C, const ResBwdArgs& a, hipStream_t s, PendingReduce
         return e != hipSuccess ? e : flush_pending_reduce(a.pend2, s);
     }
     if (C == 16) return rbb_launch<16>(a, s, out);
+    if (C == 32) return rbb_launch<32>(a, s, out);
     return hipErrorInvalidValue;
 }
 

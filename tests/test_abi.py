@@ -90,11 +90,12 @@ def test_null_pointers_and_small_workspace_fail_before_hip():
     assert lib.impala_conv3x3_fwd(0, 4, 84, 84, 4, 24, 1, 2, None, 1, None, None, 1, None) == -3
     assert lib.impala_conv3x3_dgrad(0, 4, 42, 42, 32, 16, 1, 1, None, None, 1, None) == -3
     assert lib.impala_maxpool_fwd(0, 4, 42, 42, 6, 1, 1, 1, None) == -3
-    # the fused residual-block backward: 16 channels in bf16 only, a workspace, no NULLs
+    # the fused residual-block backward: 16 or 32 channels in bf16 only, a workspace, no NULLs
     rb_ws = lib.impala_resblock_bwd_workspace_bytes(P.PREC_BF16, 16)
     assert rb_ws > 0 and lib.impala_resblock_bwd_workspace_bytes(P.PREC_FP32, 16) == 0
+    assert lib.impala_resblock_bwd_workspace_bytes(P.PREC_BF16, 32) > 0
     rb = (1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1)
-    assert lib.impala_resblock_bwd(P.PREC_BF16, 4, 42, 42, 32, *rb, 1 << 40, None) == -3
+    assert lib.impala_resblock_bwd(P.PREC_BF16, 4, 42, 42, 64, *rb, 1 << 40, None) == -3
     assert lib.impala_resblock_bwd(P.PREC_FP32, 4, 42, 42, 16, *rb, 1 << 40, None) == -3
     assert lib.impala_resblock_bwd(P.PREC_BF16, 4, 42, 42, 16, *rb, rb_ws - 1, None) == -2
     assert lib.impala_resblock_bwd(P.PREC_BF16, 4, 42, 42, 16, None, *rb[1:], rb_ws, None) == -1

@@ -247,7 +247,8 @@ def test_conv_backward_fused(case):
 
 
 # (n, H, W, C): the residual blocks' backward, base and ragged bands, tiny frames
-RES_BWD_CASES = [(3, 42, 42, 16), (2, 17, 23, 16), (4, 9, 7, 16), (1, 84, 84, 16), (5, 3, 4, 16), (2, 43, 11, 16)]
+RES_BWD_CASES = [(3, 42, 42, 16), (2, 17, 23, 16), (4, 9, 7, 16), (1, 84, 84, 16), (5, 3, 4, 16), (2, 43, 11, 16),
+                 (4, 21, 21, 32), (5, 11, 11, 32), (3, 9, 7, 32), (2, 23, 17, 32), (1, 42, 42, 32)]
 
 
 def _resblock_bwd(n, H, W, C, dy, t, x, wa, wb):
@@ -291,7 +292,8 @@ def test_resblock_backward_fused(case):
     G.assert_sum_close(dba, want_ba, abs_ba, 1e-5, "resblock_bwd dba")
 
 
-@pytest.mark.parametrize("case", [(3, 42, 42, 16), (2, 17, 23, 16), (5, 3, 4, 16)], ids=lambda c: "n%d_%dx%d_c%d" % c)
+@pytest.mark.parametrize("case", [(3, 42, 42, 16), (2, 17, 23, 16), (5, 3, 4, 16), (2, 21, 21, 32), (3, 11, 11, 32)],
+                         ids=lambda c: "n%d_%dx%d_c%d" % c)
 def test_resblock_backward_matches_two_conv_backwards(case):
     """On real-valued data the fused block backward equals the two single-conv backward passes
     it replaces: dt is rounded from the same float32 sums, so dx is bit-identical; the weight
@@ -320,11 +322,11 @@ def test_resblock_backward_matches_two_conv_backwards(case):
 
 
 def test_resblock_backward_rejects_unsupported():
-    z = G.dev_act(np.zeros((1, 8, 8, 32)), G.BF16)
-    w = G.dev_f32(np.zeros((3, 3, 32, 32)))
-    g = [G.dev_f32(np.zeros(shape)) for shape in ((3, 3, 32, 32), (32,), (3, 3, 32, 32), (32,))]
-    with pytest.raises(P.LibraryError):   # 32 channels: not in the fused set
-        P.impala_resblock_bwd(G.BF16, 1, 8, 8, 32, z, z, z, w, w, z, *g, G.ws_bytes(1 << 22))
+    z = G.dev_act(np.zeros((1, 8, 8, 64)), G.BF16)
+    w = G.dev_f32(np.zeros((3, 3, 64, 64)))
+    g = [G.dev_f32(np.zeros(shape)) for shape in ((3, 3, 64, 64), (64,), (3, 3, 64, 64), (64,))]
+    with pytest.raises(P.LibraryError):   # 64 channels: not in the fused set
+        P.impala_resblock_bwd(G.BF16, 1, 8, 8, 64, z, z, z, w, w, z, *g, G.ws_bytes(1 << 22))
     b16 = G.dev_act(np.zeros((1, 8, 8, 16)), G.BF16)
     w16 = G.dev_f32(np.zeros((3, 3, 16, 16)))
     g16 = [G.dev_f32(np.zeros(shape)) for shape in ((3, 3, 16, 16), (16,), (3, 3, 16, 16), (16,))]
