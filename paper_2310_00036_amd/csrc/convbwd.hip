@@ -247,54 +247,77 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
             const int ib0 = (h0 - 1 + t.ph) >> 1;
             const int ib1 = min((h0 + the + t.ph) >> 1, t.BH - 1);
             const int ilo = max(ib0, 0);
-            const int items = (ib1 - ilo + 1) * t.BW * (CO / 4);   // 4 channels per item
+            // an item is RPI block rows of one block column and 4 channels; with two, the
+            // windows of the shared middle row are loaded once for both (with 32 input channels
+            // the registers afford one)
+            constexpr int RPI = CI < 32 ? 2 : 1;
+            const int nbr = ib1 - ilo + 1;
+            const int items = ((nbr + RPI - 1) / RPI) * t.BW * (CO / 4);
             const unsigned char* dpl = smem + t.dp_off;
             const unsigned char* agl = smem + t.ag_off;
             for (int it = tid; it < items; it += NT) {
                 const int c4 = it % (CO / 4), blk = it / (CO / 4);
-                const int bi = blk / t.BW, j = blk - bi * t.BW;
-                const int i = ilo + bi, lr = i - ib0;
-                uint32_t ka[4];
-                float v[4][4];
+                const int bp2 = qdiv(blk, t.inv_BW), j = blk - bp2 * t.BW;
+                const int i0 = ilo + RPI * bp2, lr0 = i0 - ib0;
+                // window rows lr0, lr0+1 (the first block row), then lr0+2 replaces lr0 (the
+                // second): the middle row is loaded once for both
+                uint32_t ka[2][2];
+                uint2 dg[2][2];   // 4 bf16 gradients, unpacked where used
+                auto load_row = [&](int slot, int lr) {
 #pragma unroll
-                for (int w4 = 0; w4 < 4; ++w4) {
-                    const int px = (lr + (w4 >> 1)) * PW2 + j + (w4 & 1);
-                    ka[w4] = *reinterpret_cast<const uint32_t*>(agl + px * CO + c4 * 4);
-                    const uint2 d4 = *reinterpret_cast<const uint2*>(dpl + (px * CO + c4 * 4) * 2);
-                    v[w4][0] = __uint_as_float(d4.x << 16); v[w4][1] = __uint_as_float(d4.x & 0xffff0000u);
-                    v[w4][2] = __uint_as_float(d4.y << 16); v[w4][3] = __uint_as_float(d4.y & 0xffff0000u);
-                }
-                float c00[4], c01[4], c10[4], c11[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    uint32_t k[4];
-#pragma unroll
-                    for (int w4 = 0; w4 < 4; ++w4) k[w4] = (ka[w4] >> (8 * e)) & 0xffu;
-                    float s00 = 0.f, s01 = 0.f, s10 = 0.f, s11 = 0.f;
-                    s00 += k[0] == 8 ? v[0][e] : 0.f;
-                    s00 += k[1] == 6 ? v[1][e] : 0.f;
-                    s00 += k[2] == 2 ? v[2][e] : 0.f;
-                    s00 += k[3] == 0 ? v[3][e] : 0.f;
-                    s01 += k[1] == 7 ? v[1][e] : 0.f;
-                    s01 += k[3] == 1 ? v[3][e] : 0.f;
-                    s10 += k[2] == 5 ? v[2][e] : 0.f;
-                    s10 += k[3] == 3 ? v[3][e] : 0.f;
-                    s11 += k[3] == 4 ? v[3][e] : 0.f;
-                    c00[e] = s00; c01[e] = s01; c10[e] = s10; c11[e] = s11;
-                }
-                // cells -> dy-window row h - h0 + 1, column w + 1; off the frame: zero
-                const int h = 2 * i - t.ph, w = 2 * j - t.pw;
-                auto put = [&](int hh, int ww, const float* c) {
-                    const int rr = hh - h0 + 1;
-                    if (rr < 0 || rr >= the + 2) return;
-                    const bool in = hh >= 0 && hh < H && ww >= 0 && ww < W;
-                    *reinterpret_cast<uint2*>(dyw + (rr * TW + ww + 1) * DYP + c4 * 8) =
-                        in ? make_uint2(pack2bf(c[0], c[1]), pack2bf(c[2], c[3])) : make_uint2(0, 0);
+                    for (int q = 0; q < 2; ++q) {
+                        const int px = lr * PW2 + j + q;
+                        ka[slot][q] = *reinterpret_cast<const uint32_t*>(agl + px * CO + c4 * 4);
+                        dg[slot][q] = *reinterpret_cast<const uint2*>(dpl + (px * CO + c4 * 4) * 2);
+                    }
                 };
-                put(h, w, c00);
-                put(h, w + 1, c01);
-                put(h + 1, w, c10);
-                put(h + 1, w + 1, c11);
+                load_row(0, lr0);
+                load_row(1, lr0 + 1);
+#pragma unroll
+                for (int sb = 0; sb < RPI; ++sb) {
+                    const int i = i0 + sb;
+                    if (i > ib1) break;
+                    if (sb == 1) load_row(0, lr0 + 2);   // rows: slot 1 = lr0+1 (top), slot 0 = lr0+2
+                    const int top = sb == 0 ? 0 : 1, bot = sb == 0 ? 1 : 0;
+                    float c00[4], c01[4], c10[4], c11[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        uint32_t k[4];
+                        float g4[4];
+#pragma unroll
+                        for (int w4 = 0; w4 < 4; ++w4) {
+                            const int rs = (w4 >> 1) ? bot : top;
+                            k[w4] = (ka[rs][w4 & 1] >> (8 * e)) & 0xffu;
+                            const uint2 d = dg[rs][w4 & 1];
+                            const uint32_t u = e < 2 ? d.x : d.y;
+                            g4[w4] = __uint_as_float((e & 1) ? (u & 0xffff0000u) : (u << 16));
+                        }
+                        float s00 = 0.f, s01 = 0.f, s10 = 0.f, s11 = 0.f;
+                        s00 += k[0] == 8 ? g4[0] : 0.f;
+                        s00 += k[1] == 6 ? g4[1] : 0.f;
+                        s00 += k[2] == 2 ? g4[2] : 0.f;
+                        s00 += k[3] == 0 ? g4[3] : 0.f;
+                        s01 += k[1] == 7 ? g4[1] : 0.f;
+                        s01 += k[3] == 1 ? g4[3] : 0.f;
+                        s10 += k[2] == 5 ? g4[2] : 0.f;
+                        s10 += k[3] == 3 ? g4[3] : 0.f;
+                        s11 += k[3] == 4 ? g4[3] : 0.f;
+                        c00[e] = s00; c01[e] = s01; c10[e] = s10; c11[e] = s11;
+                    }
+                    // cells -> dy-window row h - h0 + 1, column w + 1; off the frame: zero
+                    const int h = 2 * i - t.ph, w = 2 * j - t.pw;
+                    auto put = [&](int hh, int ww, const float* c) {
+                        const int rr = hh - h0 + 1;
+                        if (rr < 0 || rr >= the + 2) return;
+                        const bool in = hh >= 0 && hh < H && ww >= 0 && ww < W;
+                        *reinterpret_cast<uint2*>(dyw + (rr * TW + ww + 1) * DYP + c4 * 8) =
+                            in ? make_uint2(pack2bf(c[0], c[1]), pack2bf(c[2], c[3])) : make_uint2(0, 0);
+                    };
+                    put(h, w, c00);
+                    put(h, w + 1, c01);
+                    put(h + 1, w, c10);
+                    put(h + 1, w + 1, c11);
+                }
             }
             __syncthreads();
         }
@@ -520,7 +543,7 @@ hipError_t cb_launch(const ConvBwdArgs& a, hipStream_t s, PendingReduce* deferre
     t.PR = PDY ? prows(TH) : 0;
     t.OH = OH; t.OW = OW; t.ph = ph; t.pw = pw; t.BH = (H + ph + 1) / 2; t.BW = (W + pw + 1) / 2;
     t.inv_W = 1.f / float(W); t.inv_TW = 1.f / float(W + 2);
-    t.inv_TH = 1.f / float(TH); t.inv_TR = 1.f / float(TH + 2);
+    t.inv_TH = 1.f / float(TH); t.inv_TR = 1.f / float(TH + 2); t.inv_BW = 1.f / float(t.BW);
     const size_t L = std::max(lds(TH, FR), size_t(kCbWaves * 4) * 17 * 16);   // (pending reduce)
     if (PDY && int64_t(OH) * OW * CO * 2 >= (int64_t(1) << 31)) return hipErrorInvalidValue;
     const void* fn = reinterpret_cast<const void*>(&conv_bwd_kernel<CI, CO, MODE, ADD, PDY, kCbWaves>);

@@ -132,7 +132,7 @@ struct CbTile {
     int x_guard;                  // x window: byte offset of its rear guard pixel
     int dp_off, ag_off, PR;       // pooled gradient / argmax rows in LDS (PR rows), pooled input
     int OH, OW, ph, pw, BH, BW;   // max-pool geometry (2x2 block grid BH x BW)
-    float inv_W, inv_TW, inv_TH, inv_TR;
+    float inv_W, inv_TW, inv_TH, inv_TR, inv_BW;
 };
 bool conv3x3_bwd_supported(int cin, int cout, int mode, int add, int pooled);
 size_t conv3x3_bwd_partial_floats(int cin, int cout);
