@@ -228,28 +228,49 @@ constexpr int kGStage = 2 * kGTile;            // A and B
 static_assert(kGK * kPM == kGTile, "both layouts fill the same tile");
 }  // namespace
 
-// DMA one operand tile: rows [r0, r0+128) of `nrows`, k [k0, k0+64) of `kend`.
+// DMA of one operand tile: rows [r0, r0+128) of `nrows`, k [k0, k0+64) of `kend`. A lane's
+// slots map to the same row and column of every k-block, so their offsets are formed once
+// per workgroup (rows past `nrows` and padding slots: kOOB); a k-block adds k0 (k-contiguous)
+// or k0 rows, and a slot past `kend` reads zero.
 template <int KC>
-CB_DEV void gemm_stage(__amdgpu_buffer_rsrc_t rs, unsigned char* __restrict__ dst, int ld, int r0, int nrows,
-                       int k0, int kend, int wave, int lane) {
-    constexpr int SPR = KC ? kPK / 16 : kPM / 16;   // slots per LDS row
-    constexpr int DATA = KC ? 8 : 16;               // data slots per row
-    constexpr int NS = (KC ? kGB : kGK) * SPR;      // slots per tile (multiple of 64)
+struct GemmStage {
+    static constexpr int SPR = KC ? kPK / 16 : kPM / 16;   // slots per LDS row
+    static constexpr int DATA = KC ? 8 : 16;               // data slots per row
+    static constexpr int NS = (KC ? kGB : kGK) * SPR;      // slots per tile (multiple of 64)
+    static constexpr int NB = (NS / 64 + 3) / 4;           // DMA blocks per wave (at most)
     static_assert(NS % 64 == 0, "whole DMA blocks");
-    for (int b = wave; b < NS / 64; b += 4) {
-        const int j = b * 64 + lane;
-        const int row = j / SPR, c = j - row * SPR;
-        uint32_t off = kOOB;
-        if (KC) {
-            if (c < DATA && r0 + row < nrows && k0 + c * 8 < kend)
-                off = (uint32_t(r0 + row) * uint32_t(ld) + uint32_t(k0 + c * 8)) * 2u;
-        } else {
-            if (c < DATA && k0 + row < kend && r0 + c * 8 < nrows)
-                off = (uint32_t(k0 + row) * uint32_t(ld) + uint32_t(r0 + c * 8)) * 2u;
+    uint32_t base[NB];   // byte offset at k0 = 0, or kOOB
+    int kx[NB];          // the slot's k (k-contiguous: column, else row) within the block
+    CB_DEV GemmStage(int ld, int r0, int nrows, int wave, int lane) {
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int b = wave + 4 * i;
+            const int j = b * 64 + lane;
+            const int row = j / SPR, c = j - row * SPR;
+            bool ok = b < NS / 64 && c < DATA;
+            if (KC) {
+                ok = ok && r0 + row < nrows;
+                base[i] = ok ? (uint32_t(r0 + row) * uint32_t(ld) + uint32_t(c * 8)) * 2u : kOOB;
+                kx[i] = c * 8;
+            } else {
+                ok = ok && r0 + c * 8 < nrows;
+                base[i] = ok ? (uint32_t(row) * uint32_t(ld) + uint32_t(r0 + c * 8)) * 2u : kOOB;
+                kx[i] = row;
+            }
         }
-        dma16_to_lds(rs, dst + b * 1024, off);
     }
-}
+    CB_DEV void issue(__amdgpu_buffer_rsrc_t rs, unsigned char* __restrict__ dst, int ld, int k0, int kend, int wave) const {
+        const uint32_t kadd = KC ? uint32_t(k0) * 2u : uint32_t(k0) * uint32_t(ld) * 2u;
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int b = wave + 4 * i;
+            if (b < NS / 64) {
+                const uint32_t off = (base[i] != kOOB && k0 + kx[i] < kend) ? base[i] + kadd : kOOB;
+                dma16_to_lds(rs, dst + b * 1024, off);
+            }
+        }
+    }
+};
 
 // Fragment of 8 consecutive k (k-step ks, lane group g) of tile row `row`.
 template <int KC>
@@ -271,11 +292,12 @@ CB_DEV uint4 gemm_frag(const unsigned char* __restrict__ t, int row, int ks, int
 // write what the MFMAs read and does not wait for them.
 template <int AKC, int BKC, int BRELU>
 CB_DEV void gemm_block(const unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt, bool more,
-                       __amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb, const GemmArgs& a, int m0, int n0,
-                       int k1, int k_end, int wave, int lane, cb_f32x4 (&acc)[4][4]) {
+                       __amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb, const GemmStage<AKC>& sa,
+                       const GemmStage<BKC>& sb, const GemmArgs& a, int k1, int k_end, int wave, int lane,
+                       cb_f32x4 (&acc)[4][4]) {
     if (more) {
-        gemm_stage<AKC>(ra, nxt, int(a.lda), m0, a.M, k1, k_end, wave, lane);
-        gemm_stage<BKC>(rb, nxt + kGTile, int(a.ldb), n0, a.N, k1, k_end, wave, lane);
+        sa.issue(ra, nxt, int(a.lda), k1, k_end, wave);
+        sb.issue(rb, nxt + kGTile, int(a.ldb), k1, k_end, wave);
     }
     const int g = (lane >> 4) & 3, r16 = lane & 15;
     const int wm = wave >> 1, wn = wave & 1;
@@ -317,15 +339,17 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a, int kchunk) 
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
 
-    gemm_stage<AKC>(ra, smem, int(a.lda), m0, a.M, k_begin, k_end, wave, lane);
-    gemm_stage<BKC>(rb, smem + kGTile, int(a.ldb), n0, a.N, k_begin, k_end, wave, lane);
+    const GemmStage<AKC> sa(int(a.lda), m0, a.M, wave, lane);
+    const GemmStage<BKC> sb(int(a.ldb), n0, a.N, wave, lane);
+    sa.issue(ra, smem, int(a.lda), k_begin, k_end, wave);
+    sb.issue(rb, smem + kGTile, int(a.ldb), k_begin, k_end, wave);
     int it = 0;
     for (int k0 = k_begin; k0 < k_end; k0 += kGK, ++it) {
         __builtin_amdgcn_s_waitcnt(0);   // this block's loads (this wave's) are in LDS
         __syncthreads();                 // all waves' loads in; the other buffer is free
         unsigned char* cur = smem + (it & 1) * kGStage;
         unsigned char* nxt = smem + ((it + 1) & 1) * kGStage;
-        gemm_block<AKC, BKC, BRELU>(cur, nxt, k0 + kGK < k_end, ra, rb, a, m0, n0, k0 + kGK, k_end, wave, lane, acc);
+        gemm_block<AKC, BKC, BRELU>(cur, nxt, k0 + kGK < k_end, ra, rb, sa, sb, a, k0 + kGK, k_end, wave, lane, acc);
     }
 
     const bool vec_ok = gemm_epilogue4_ok(a);
