@@ -45,9 +45,13 @@ struct RbGeom {
     static constexpr int WPS = C >= 32 ? 3 : 4;            // waves per SIMD (register budget)
     static constexpr int WGS = WPS * 4 / NW;               // workgroups per CU
     static constexpr int MAXS = C >= 32 ? 8 : 5;           // x-window staging slots per lane
-    // conv2 column tiles per wave and tile whose residual is fetched with the staging (with 32
-    // channels the registers hold both weight sets, and the residual is read per column tile)
-    static constexpr int MAXT = C >= 32 ? 0 : 5;
+    // conv2 column tiles per wave and tile whose residual is fetched at the tile's start; with 16
+    // channels that covers all of them, with 32 (whose registers hold both weight sets) the
+    // first two, and the rest are read per column tile
+    static constexpr int MAXT = C >= 32 ? 2 : 5;
+    static constexpr bool ALLPRE = C < 32;
+    // x-window staging offsets kept in registers (with 32 channels, recomputed per tile)
+    static constexpr bool OXREG = C < 32;
     __host__ __device__ static int blocks(int slots) { return (slots + 63) / 64; }
     // x window: MT planes of (TH+4) x (W+2) pixels, in whole 1 KB staging blocks
     __host__ __device__ static int xwin_bytes(int TH, int W) { return blocks(MT * (TH + 4) * (W + 2) * 2) * 1024; }
@@ -140,14 +144,16 @@ __global__ __launch_bounds__(64 * NW, RbGeom<C>::WPS) void resblock_fwd_kernel(R
     // tile adds h0 - 2 rows. Rows off the frame fall outside the frame's buffer resource
     // (negative, or past its end); padding columns read zero (kOOB).
     const int npx = (TH + 4) * TW, nsx = MT * npx * 2;
-    uint32_t ox[G::MAXS];
-#pragma unroll
-    for (int k = 0; k < G::MAXS; ++k) {
+    auto x_off = [&](int k) {
         const int j = (wave + NW * k) * 64 + lane, pl = j / (npx * 2), rem = j - pl * npx * 2;
         const int p = rem >> 1, half = rem & 1;
         const int rr = p / TW, col = p - rr * TW;
-        ox[k] = (j < nsx && col >= 1 && col <= W) ? uint32_t(((rr * W + col - 1) * C + pl * 16 + half * 8) * 2)
-                                                   : kOOB;
+        return (j < nsx && col >= 1 && col <= W) ? uint32_t(((rr * W + col - 1) * C + pl * 16 + half * 8) * 2) : kOOB;
+    };
+    uint32_t ox[G::OXREG ? G::MAXS : 1];
+    if constexpr (G::OXREG) {
+#pragma unroll
+        for (int k = 0; k < G::MAXS; ++k) ox[k] = x_off(k);
     }
     __syncthreads();
 
@@ -162,7 +168,7 @@ __global__ __launch_bounds__(64 * NW, RbGeom<C>::WPS) void resblock_fwd_kernel(R
         const uint32_t hr = uint32_t((band * TH - 2) * W * C * 2);   // wraps for h0 < 2: rows off the frame
 #pragma unroll
         for (int k = 0; k < G::MAXS; ++k)
-            if ((wave + NW * k) * 64 < nsx) dma16_to_lds(rx, dst + (wave + NW * k) * 1024, ox[k] + hr);
+            if ((wave + NW * k) * 64 < nsx) dma16_to_lds(rx, dst + (wave + NW * k) * 1024, (G::OXREG ? ox[k] : x_off(k)) + hr);
     };
     if (lg < t.ntiles) stage_x(xw, lg);
 
@@ -187,7 +193,7 @@ __global__ __launch_bounds__(64 * NW, RbGeom<C>::WPS) void resblock_fwd_kernel(R
         __builtin_amdgcn_s_waitcnt(0);   // this tile's window has landed
         __syncthreads();
         // conv2's residual for this wave's column tiles, in flight during the ReLU pass and conv1
-        uint2 xres[G::MAXT > 0 ? G::MAXT : 1];
+        uint2 xres[G::MAXT];
 #pragma unroll
         for (int k = 0; k < G::MAXT; ++k) {
             const int q = (wave / MT + k * (NW / MT)) * 16 + r16;
@@ -255,13 +261,11 @@ __global__ __launch_bounds__(64 * NW, RbGeom<C>::WPS) void resblock_fwd_kernel(R
                            acc[2] + b2[2] + __uint_as_float(xr.y << 16),
                            acc[3] + b2[3] + __uint_as_float(xr.y & 0xffff0000u));
             };
-            if constexpr (G::MAXT > 0) {
 #pragma unroll
-                for (int k = 0; k < G::MAXT; ++k)
-                    if ((wave / MT + k * (NW / MT)) * 16 < npx2) conv2_tile(wave / MT + k * (NW / MT), &xres[k]);
-            } else {
-                for (int nt = wave / MT; nt * 16 < npx2; nt += NW / MT) conv2_tile(nt, nullptr);
-            }
+            for (int k = 0; k < G::MAXT; ++k)
+                if ((wave / MT + k * (NW / MT)) * 16 < npx2) conv2_tile(wave / MT + k * (NW / MT), &xres[k]);
+            if constexpr (!G::ALLPRE)
+                for (int nt = wave / MT + G::MAXT * (NW / MT); nt * 16 < npx2; nt += NW / MT) conv2_tile(nt, nullptr);
         };
         stage_conv2(xw, tw);
     }
@@ -281,7 +285,7 @@ hipError_t rb_fwd_launch(const ResBlockArgs& a, hipStream_t s) {
     auto fits = [&](int th) {
         const int tiles = (th * (W + 2) - 2 + 15) / 16, per = kRbWaves / G::MT;
         return G::blocks(G::MT * (th + 4) * (W + 2) * 2) <= G::MAXS * kRbWaves &&
-               (G::MAXT == 0 || (tiles + per - 1) / per <= G::MAXT);
+               (!G::ALLPRE || (tiles + per - 1) / per <= G::MAXT);
     };
     int thmax = H;
     while (thmax > 1 && (lds(thmax) > kRbLdsTarget || !fits(thmax))) --thmax;
