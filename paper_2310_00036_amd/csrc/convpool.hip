@@ -131,14 +131,13 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_pool_kernel(ConvArgs a, CpTil
     int lg = blockIdx.x;   // neighbouring bands on one XCD
     if ((gridDim.x & 7) == 0) lg = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
 
-    for (int tile = lg; tile < t.ntiles; tile += gridDim.x) {
+    // input window of a tile, image rows hc0-1 .. hc0+THmax (uint8 frames: the raw bytes). The
+    // next tile's window is issued as soon as the conv has read this one, so its latency
+    // overlaps the max-pool.
+    unsigned char* const sdst = U8 ? raw : win;
+    auto stage = [&](unsigned char* dst, int tile) {
         const int band = tile % t.nbands, f = tile / t.nbands;
-        const int p0 = band * t.PTH, p1 = min(p0 + t.PTH, t.OH);
-        const int hc0 = max(2 * p0 - t.ph, 0), hc1 = min(2 * (p1 - 1) - t.ph + 3, H);
-        const int TH = hc1 - hc0;
-        __syncthreads();   // the previous tile's LDS reads are done
-
-        // ---- stage the input window, image rows hc0-1 .. hc0+THmax
+        const int hc0 = max(2 * band * t.PTH - t.ph, 0);
         if constexpr (U8) {
             const int64_t row = a.row_idx ? a.row_idx[f] : f;
             const uint32_t fb = uint32_t(H) * W * 4;
@@ -146,17 +145,25 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_pool_kernel(ConvArgs a, CpTil
             const uint32_t hr = uint32_t(hc0 * W * 4);
 #pragma unroll
             for (int k = 0; k < G::MAXS; ++k)
-                if ((wave + NW * k) * 64 < ns) dma4_to_lds(rx, raw + (wave + NW * k) * 256, ox[k] + hr);
+                if ((wave + NW * k) * 64 < ns) dma4_to_lds(rx, dst + (wave + NW * k) * 256, ox[k] + hr);
         } else {
             const uint32_t fb = uint32_t(H) * W * CIN * 2;
             const auto rx = buf_rsrc(static_cast<const uint16_t*>(a.x) + int64_t(f) * H * W * CIN, fb);
             const uint32_t hr = uint32_t(hc0 * W * CIN * 2);
 #pragma unroll
             for (int k = 0; k < G::MAXS; ++k)
-                if ((wave + NW * k) * 64 < ns) dma16_to_lds(rx, win + (wave + NW * k) * 1024, ox[k] + hr);
+                if ((wave + NW * k) * 64 < ns) dma16_to_lds(rx, dst + (wave + NW * k) * 1024, ox[k] + hr);
         }
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
+    };
+    if (lg < t.ntiles) stage(sdst, lg);
+
+    for (int tile = lg; tile < t.ntiles; tile += gridDim.x) {
+        const int band = tile % t.nbands, f = tile / t.nbands;
+        const int p0 = band * t.PTH, p1 = min(p0 + t.PTH, t.OH);
+        const int hc0 = max(2 * p0 - t.ph, 0), hc1 = min(2 * (p1 - 1) - t.ph + 3, H);
+        const int TH = hc1 - hc0;
+        __builtin_amdgcn_s_waitcnt(0);   // this tile's window has landed
+        __syncthreads();                 // ... everyone's, and the previous max-pool is done
         if constexpr (U8) {
             for (int p = tid; p < ns; p += NT)
                 *reinterpret_cast<uint2*>(win + p * 8) = u8x4_to_bf16(*reinterpret_cast<const uint32_t*>(raw + p * 4));
@@ -187,52 +194,59 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_pool_kernel(ConvArgs a, CpTil
                 if (c >= TW) c -= TW;
             }
         }
-        __syncthreads();
+        __syncthreads();   // the conv has read the window: the next tile's may land there
 
-        // ---- 3x3 stride-2 max-pool of the key tile, 8 channels per item
-        {
-            const int prows = p1 - p0, items = prows * t.OW * C8;
-            uint16_t* ybase = static_cast<uint16_t*>(a.y) + (int64_t(f) * t.OH + p0) * t.OW * COUT;
-            uint8_t* abase = a.arg + (int64_t(f) * t.OH + p0) * t.OW * COUT;
-            for (int it = tid; it < items; it += NT) {
-                const int c8 = it % C8, pp = it / C8;
-                const int ohl = qdiv(pp, t.inv_OW), ow = pp - ohl * t.OW;
-                const int hc = 2 * (p0 + ohl) - t.ph, wc = 2 * ow - t.pw;
-                // window cell (dy, dx): key-tile row hc + dy - hc0, column wc + dx + 1 (the
-                // padding columns hold zero keys); rows off the frame read the zero area
-                const unsigned char* kb = keys + ((hc - hc0) * TW + wc + 1) * KPB + c8 * 16;
-                const bool rv[3] = {hc >= 0, true, hc + 2 < H};
-                uint4 cell[9];
+        // ---- next tile's window, then the 3x3 stride-2 max-pool of the key tile, 8 channels per
+        // item. The window and the key tile are restrict parameters of one call, so the compiler
+        // knows that the loads in flight do not write what the max-pool reads.
+        auto stage_pool = [&](unsigned char* __restrict__ dst, const unsigned char* __restrict__ kt,
+                              const unsigned char* __restrict__ zr) {
+            if (tile + int(gridDim.x) < t.ntiles) stage(dst, tile + gridDim.x);
+            {
+                const int prows = p1 - p0, items = prows * t.OW * C8;
+                uint16_t* ybase = static_cast<uint16_t*>(a.y) + (int64_t(f) * t.OH + p0) * t.OW * COUT;
+                uint8_t* abase = a.arg + (int64_t(f) * t.OH + p0) * t.OW * COUT;
+                for (int it = tid; it < items; it += NT) {
+                    const int c8 = it % C8, pp = it / C8;
+                    const int ohl = qdiv(pp, t.inv_OW), ow = pp - ohl * t.OW;
+                    const int hc = 2 * (p0 + ohl) - t.ph, wc = 2 * ow - t.pw;
+                    // window cell (dy, dx): key-tile row hc + dy - hc0, column wc + dx + 1 (the
+                    // padding columns hold zero keys); rows off the frame read the zero area
+                    const unsigned char* kb = kt + ((hc - hc0) * TW + wc + 1) * KPB + c8 * 16;
+                    const bool rv[3] = {hc >= 0, true, hc + 2 < H};
+                    uint4 cell[9];
 #pragma unroll
-                for (int dy = 0; dy < 3; ++dy)
+                    for (int dy = 0; dy < 3; ++dy)
 #pragma unroll
-                    for (int dx = 0; dx < 3; ++dx)
-                        cell[dy * 3 + dx] = *reinterpret_cast<const uint4*>(rv[dy] ? kb + (dy * TW + dx) * KPB : zero);
-                uint32_t best[8];
+                        for (int dx = 0; dx < 3; ++dx)
+                            cell[dy * 3 + dx] = *reinterpret_cast<const uint4*>(rv[dy] ? kb + (dy * TW + dx) * KPB : zr);
+                    uint32_t best[8];
 #pragma unroll
-                for (int j = 0; j < 8; ++j) best[j] = 0u;
+                    for (int j = 0; j < 8; ++j) best[j] = 0u;
 #pragma unroll
-                for (int cidx = 0; cidx < 9; ++cidx) {
-                    const uint32_t tag = 15u - uint32_t(cidx);
-                    const uint32_t kk[4] = {cell[cidx].x, cell[cidx].y, cell[cidx].z, cell[cidx].w};
+                    for (int cidx = 0; cidx < 9; ++cidx) {
+                        const uint32_t tag = 15u - uint32_t(cidx);
+                        const uint32_t kk[4] = {cell[cidx].x, cell[cidx].y, cell[cidx].z, cell[cidx].w};
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        best[2 * j] = max(best[2 * j], (kk[j] << 16) | tag);
-                        best[2 * j + 1] = max(best[2 * j + 1], (kk[j] & 0xffff0000u) | tag);
+                        for (int j = 0; j < 4; ++j) {
+                            best[2 * j] = max(best[2 * j], (kk[j] << 16) | tag);
+                            best[2 * j + 1] = max(best[2 * j + 1], (kk[j] & 0xffff0000u) | tag);
+                        }
                     }
+                    uint32_t vals[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        vals[j] = bf16x2_unkey((best[2 * j] >> 16) | (best[2 * j + 1] & 0xffff0000u));
+                    uint32_t idx[2] = {0u, 0u};
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) idx[j >> 2] |= (15u - (best[j] & 15u)) << (8 * (j & 3));
+                    const uint32_t o = (uint32_t(ohl) * t.OW + ow) * COUT + c8 * 8;
+                    *reinterpret_cast<uint4*>(ybase + o) = make_uint4(vals[0], vals[1], vals[2], vals[3]);
+                    *reinterpret_cast<uint2*>(abase + o) = make_uint2(idx[0], idx[1]);
                 }
-                uint32_t vals[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    vals[j] = bf16x2_unkey((best[2 * j] >> 16) | (best[2 * j + 1] & 0xffff0000u));
-                uint32_t idx[2] = {0u, 0u};
-#pragma unroll
-                for (int j = 0; j < 8; ++j) idx[j >> 2] |= (15u - (best[j] & 15u)) << (8 * (j & 3));
-                const uint32_t o = (uint32_t(ohl) * t.OW + ow) * COUT + c8 * 8;
-                *reinterpret_cast<uint4*>(ybase + o) = make_uint4(vals[0], vals[1], vals[2], vals[3]);
-                *reinterpret_cast<uint2*>(abase + o) = make_uint2(idx[0], idx[1]);
             }
-        }
+        };
+        stage_pool(sdst, keys, zero);
     }
 }
 
