@@ -115,34 +115,38 @@ __global__ __launch_bounds__(64 * NW, 4) void pool_wgrad_u8_kernel(PoolWgArgs a,
     int lg = blockIdx.x;   // neighbouring bands on one XCD
     if ((gridDim.x & 7) == 0) lg = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
 
-    for (int tile = lg; tile < t.ntiles; tile += gridDim.x) {
+    // a tile's inputs: frame rows hw0 .. of the window, pooled rows i0-1 .. of the gradient and the
+    // argmax. The next tile's are issued once the max-pool backward has read this one's, so
+    // their latency overlaps the weight gradient.
+    auto stage = [&](unsigned char* rdst, unsigned char* pdst, unsigned char* gdst, int tile) {
         const int band = tile % t.nbands, f = tile / t.nbands;
         const int i0 = band * TB;
-        const int nbr = t.BH - i0 < TB ? t.BH - i0 : TB;   // block rows in this band
-        const int hw0 = 2 * i0 - t.ph - 1;                 // image row of window row 0
-        __syncthreads();   // the previous tile's LDS reads are done
+        const int hw0 = 2 * i0 - t.ph - 1;
+        const int64_t row = a.row_idx ? a.row_idx[f] : f;
+        const uint32_t fb = uint32_t(H) * W * 4;
+        const auto rf = buf_rsrc(a.obs + row * fb, fb);
+        const uint32_t hr = uint32_t(hw0 * W * 4);   // wraps for hw0 = -1: reads zero
+#pragma unroll
+        for (int k = 0; k < G::MAXR; ++k)
+            if ((wave + NW * k) * 64 < nsr) dma4_to_lds(rf, rdst + (wave + NW * k) * 256, orw[k] + hr);
+        const uint32_t pb = uint32_t(OH) * OW * CO;   // pooled elements per frame
+        const auto rp = buf_rsrc(static_cast<const uint16_t*>(a.dp) + int64_t(f) * pb, pb * 2);
+        const auto rg = buf_rsrc(a.arg + int64_t(f) * pb, pb);
+        const uint32_t pr = uint32_t((i0 - 1) * OW * CO);   // pooled row i0-1 (wraps at i0 = 0)
+#pragma unroll
+        for (int k = 0; k < G::MAXP; ++k)
+            if ((wave + NW * k) * 64 < nsp) dma16_to_lds(rp, pdst + (wave + NW * k) * 1024, opd[k] + 2 * pr);
+#pragma unroll
+        for (int k = 0; k < G::MAXG; ++k)
+            if ((wave + NW * k) * 64 < nsg) dma16_to_lds(rg, gdst + (wave + NW * k) * 1024, oag[k] + pr);
+    };
+    if (lg < t.ntiles) stage(raw, dpl, agl, lg);
 
-        {
-            const int64_t row = a.row_idx ? a.row_idx[f] : f;
-            const uint32_t fb = uint32_t(H) * W * 4;
-            const auto rf = buf_rsrc(a.obs + row * fb, fb);
-            const uint32_t hr = uint32_t(hw0 * W * 4);   // wraps for hw0 = -1: reads zero
-#pragma unroll
-            for (int k = 0; k < G::MAXR; ++k)
-                if ((wave + NW * k) * 64 < nsr) dma4_to_lds(rf, raw + (wave + NW * k) * 256, orw[k] + hr);
-            const uint32_t pb = uint32_t(OH) * OW * CO;   // pooled elements per frame
-            const auto rp = buf_rsrc(static_cast<const uint16_t*>(a.dp) + int64_t(f) * pb, pb * 2);
-            const auto rg = buf_rsrc(a.arg + int64_t(f) * pb, pb);
-            const uint32_t pr = uint32_t((i0 - 1) * OW * CO);   // pooled row i0-1 (wraps at i0 = 0)
-#pragma unroll
-            for (int k = 0; k < G::MAXP; ++k)
-                if ((wave + NW * k) * 64 < nsp) dma16_to_lds(rp, dpl + (wave + NW * k) * 1024, opd[k] + 2 * pr);
-#pragma unroll
-            for (int k = 0; k < G::MAXG; ++k)
-                if ((wave + NW * k) * 64 < nsg) dma16_to_lds(rg, agl + (wave + NW * k) * 1024, oag[k] + pr);
-        }
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
+    for (int tile = lg; tile < t.ntiles; tile += gridDim.x) {
+        const int i0 = (tile % t.nbands) * TB;
+        const int nbr = t.BH - i0 < TB ? t.BH - i0 : TB;   // block rows in this band
+        __builtin_amdgcn_s_waitcnt(0);   // this tile's inputs have landed
+        __syncthreads();                 // ... everyone's, and the previous weight gradient is done
 
         // ---- frames -> bf16 window (4 channels per pixel)
         for (int p = tid; p < nsr; p += NT)
@@ -204,10 +208,15 @@ __global__ __launch_bounds__(64 * NW, 4) void pool_wgrad_u8_kernel(PoolWgArgs a,
                 put(cp + (TW + 1) * DPB, r1 && q1, c11);
             }
         }
-        __syncthreads();
+        __syncthreads();   // the max-pool backward has read the inputs: the next tile's may land
 
-        // ---- weight gradient over dC's window pixels; wave w takes k-steps w, w+NW, ...
-        {
+        // ---- next tile's inputs, then the weight gradient over dC's window pixels (wave w takes
+        // k-steps w, w+NW, ...). The staging buffers and the windows the weight gradient reads are
+        // restrict parameters of one call, so the compiler does not wait for the loads in flight.
+        auto stage_wgrad = [&](unsigned char* __restrict__ rdst, unsigned char* __restrict__ pdst,
+                               unsigned char* __restrict__ gdst, const unsigned char* __restrict__ dc,
+                               const unsigned char* __restrict__ wn, const unsigned char* __restrict__ zr) {
+            if (tile + int(gridDim.x) < t.ntiles) stage(rdst, pdst, gdst, tile + gridDim.x);
             const int L = 2 * nbr * TW;
             const int nks = (L + 31) >> 5;
             const int o0 = 4 * g + jj;
@@ -221,14 +230,14 @@ __global__ __launch_bounds__(64 * NW, 4) void pool_wgrad_u8_kernel(PoolWgArgs a,
                     pb[half] = ok ? p : L - 1;
 #pragma unroll
                     for (int mt = 0; mt < MT; ++mt) {
-                        const uint2 u = lds_read_tr16(ok ? dcl + p * DPB + mt * 32 + 8 * m : zero);
+                        const uint2 u = lds_read_tr16(ok ? dc + p * DPB + mt * 32 + 8 * m : zr);
                         if (half == 0) { af[mt].x = u.x; af[mt].y = u.y; } else { af[mt].z = u.x; af[mt].w = u.y; }
                     }
                 }
 #pragma unroll
                 for (int nb = 0; nb < 3; ++nb) {
-                    const uint2 lo = lds_read_tr16(win + pb[0] * 8 + boff[nb]);
-                    const uint2 hi = lds_read_tr16(win + pb[1] * 8 + boff[nb]);
+                    const uint2 lo = lds_read_tr16(wn + pb[0] * 8 + boff[nb]);
+                    const uint2 hi = lds_read_tr16(wn + pb[1] * 8 + boff[nb]);
                     const uint4 bf = make_uint4(lo.x, lo.y, hi.x, hi.y);
 #pragma unroll
                     for (int mt = 0; mt < MT; ++mt) acc[mt][nb] = PrecBF16::mma(af[mt], bf, acc[mt][nb]);
@@ -236,7 +245,8 @@ __global__ __launch_bounds__(64 * NW, 4) void pool_wgrad_u8_kernel(PoolWgArgs a,
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) acc[mt][3] = PrecBF16::mma(af[mt], ones, acc[mt][3]);
             }
-        }
+        };
+        stage_wgrad(raw, dpl, agl, dcl, win, zero);
     }
 
     // ---- add the waves' accumulators in wave order; wave 0 writes the partial
