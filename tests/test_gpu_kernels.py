@@ -94,8 +94,22 @@ def test_conv_pool_forward(case):
     the exact conv: the pooled value is within 1 bf16 ulp of the exact conv at the chosen
     cell, that cell is a maximum up to rounding, and wherever the window's maximum is clear
     by more than 4 ulps the argmax is the oracle's."""
+    _conv_pool_check(case)
+
+
+@pytest.mark.parametrize("case", [(1024, 84, 84, 4, 16, P.X_U8), (1024, 42, 42, 16, 32, P.X_PLAIN)],
+                         ids=lambda c: "n%d_%dx%d_%d-%d_m%d" % c)
+def test_conv_pool_forward_many_tiles_per_workgroup(case):
+    """The same checks at a frame count where every workgroup runs several tiles (each tile's
+    window is staged during the previous tile's max-pool), on frames spread over the launch."""
+    _conv_pool_check(case, sample=[0, 1, 517, case[0] - 1])
+
+
+def _conv_pool_check(case, sample=None):
     n, H, W, cin, cout, mode = case
     x, rows, xin, w, b = _conv_inputs(n, H, W, cin, cout, mode, G.BF16, 13)
+    fs = slice(None) if sample is None else np.asarray(sample)   # frames checked
+    xin = xin[fs]
     wq = G.q(w, G.BF16)
     conv = onet.conv3x3(xin, wq, b.astype(np.float64))
     absum = onet.conv3x3(np.abs(xin), np.abs(wq), np.abs(b).astype(np.float64))
@@ -108,11 +122,11 @@ def test_conv_pool_forward(case):
     P.impala_conv3x3_pool_fwd(G.BF16, n, H, W, cin, cout, dx, mode, G.dev_i32(rows) if rows is not None else None,
                               G.dev_f32(w), G.dev_f32(b), y, arg)
     G.sync()
-    got_arg = arg.cpu().numpy().astype(np.int64)
+    got_arg = arg.cpu().numpy().astype(np.int64)[fs]
     assert got_arg.max() <= 8
     sel = np.take_along_axis(win, got_arg[None], 0)[0]
     assert np.isfinite(sel).all(), "argmax points at a padded cell"
-    G.assert_bf16_ulp(G.host(y), sel, np.take_along_axis(wabs, got_arg[None], 0)[0], "pooled value")
+    G.assert_bf16_ulp(G.host(y)[fs], sel, np.take_along_axis(wabs, got_arg[None], 0)[0], "pooled value")
     best = win.max(0)
     amax = wabs.max(0)
     spacing = np.maximum(np.abs(best), 1e-30) * 2.0 ** -7
@@ -138,7 +152,19 @@ RES_CASES = [(3, 42, 42, 16), (4, 21, 21, 32), (5, 11, 11, 32), (2, 17, 23, 16),
 def test_resblock_forward(case):
     """Fused residual block (bf16): t against the exact conv1 of relu(x), y against the exact
     conv2 of relu(t) using the t the kernel returned (so t's rounding does not propagate)."""
+    _resblock_fwd_check(case)
+
+
+@pytest.mark.parametrize("case", [(1024, 42, 42, 16), (2048, 21, 21, 32)], ids=lambda c: "n%d_%dx%d_c%d" % c)
+def test_resblock_forward_many_tiles_per_workgroup(case):
+    """The same checks at a frame count where every workgroup runs several tiles (each tile's
+    window is staged during the previous tile's conv2), on frames spread over the launch."""
+    _resblock_fwd_check(case, sample=[0, 1, 517, case[0] - 1])
+
+
+def _resblock_fwd_check(case, sample=None):
     n, H, W, C = case
+    fs = slice(None) if sample is None else np.asarray(sample)   # frames checked
     rng = np.random.default_rng(17)
     x = G.q(rng.standard_normal((n, H, W, C)), G.BF16)
     w1, w2 = (rng.standard_normal((2, 3, 3, C, C)) * np.sqrt(2.0 / (9 * C))).astype(np.float32)
@@ -149,15 +175,16 @@ def test_resblock_forward(case):
     P.impala_resblock_fwd(G.BF16, n, H, W, C, G.dev_act(x, G.BF16), G.dev_f32(w1), G.dev_f32(b1), G.dev_f32(w2),
                           G.dev_f32(b2), t, y)
     G.sync()
+    x = x[fs]
     rx = _relu(x)
     t_want = onet.conv3x3(rx, w1q, b1.astype(np.float64))
     t_abs = onet.conv3x3(np.abs(rx), np.abs(w1q), np.abs(b1).astype(np.float64))
-    got_t = G.host(t)
+    got_t = G.host(t)[fs]
     G.assert_bf16_ulp(got_t, t_want, t_abs, "resblock t")
     rt = _relu(got_t)
     y_want = onet.conv3x3(rt, w2q, b2.astype(np.float64)) + x
     y_abs = onet.conv3x3(np.abs(rt), np.abs(w2q), np.abs(b2).astype(np.float64)) + np.abs(x)
-    G.assert_bf16_ulp(G.host(y), y_want, y_abs, "resblock y")
+    G.assert_bf16_ulp(G.host(y)[fs], y_want, y_abs, "resblock y")
 
 
 def test_resblock_rejects_unsupported():
