@@ -448,6 +448,37 @@ def test_pool_wgrad_u8_fused(case):
     G.assert_sum_close(G.host(db), want_b, abs_b, 1e-5, "pool_wgrad db")
 
 
+
+def test_pool_wgrad_u8_many_tiles_per_workgroup():
+    """The first stage entry backward at a frame count where every workgroup runs several
+    tiles (each tile's inputs are staged during the previous tile's weight gradient): the
+    pooled gradient is non-zero on three frames spread over the launch only, so dw and db are
+    those frames' exact sums."""
+    n, H, W, C = 1024, 84, 84, 16
+    pick = np.array([0, 517, n - 1])
+    rng = np.random.default_rng(47)
+    frames = rng.integers(0, 256, size=(n + 2, H, W, 4), dtype=np.uint8)
+    rows = rng.permutation(n + 2)[:n].astype(np.int32)
+    _, arg_p = onet.maxpool(rng.integers(-4, 5, size=(len(pick), H, W, C)).astype(np.float64) * 0.25)
+    OH, OW = arg_p.shape[1:3]
+    dp_p = G.q(rng.standard_normal((len(pick), OH, OW, C)), G.BF16)
+    arg = np.zeros((n, OH, OW, C), np.uint8)
+    arg[pick] = arg_p
+    dp = np.zeros((n, OH, OW, C), np.float32)
+    dp[pick] = dp_p
+    dc = G.q(onet.maxpool_backward(arg_p, dp_p, (len(pick), H, W, C)), G.BF16)
+    xin = frames[rows[pick]].astype(np.float64) / 255.0
+    want_w, want_b = onet.conv3x3_wgrad(xin, dc)
+    abs_w, abs_b = onet.conv3x3_wgrad(xin, np.abs(dc))
+    dw = G.dev_f32(np.full((3, 3, 4, C), np.nan))
+    db = G.dev_f32(np.full(C, np.nan))
+    ws = G.ws_bytes(P.impala_conv3x3_pool_wgrad_u8_workspace_bytes(G.BF16, C))
+    P.impala_conv3x3_pool_wgrad_u8(G.BF16, n, H, W, C, G.dev_u8(frames), G.dev_i32(rows), G.dev_act(dp, G.BF16),
+                                   G.dev_u8(arg), dw, db, ws)
+    G.sync()
+    G.assert_sum_close(G.host(dw), want_w, abs_w, 1e-5, "pool_wgrad dw")
+    G.assert_sum_close(G.host(db), want_b, abs_b, 1e-5, "pool_wgrad db")
+
 def test_pool_wgrad_u8_rejects_unsupported():
     z8 = G.dev_u8(np.zeros((1, 8, 8, 4)))
     dp = G.dev_act(np.zeros((1, 4, 4, 64)), G.BF16)
