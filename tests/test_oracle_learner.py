@@ -144,3 +144,189 @@ def test_bf16_emulation_floor_on_tiny_ppo_batch():
     for name in ("logits.w", "logits.b", "value.w", "value.b"):
         assert errs[name] < 2e-2, (name, errs[name])
     assert max(errs.values()) < 0.3, errs
+
+
+# ----------------------------------------------------------------------------- learning-phase
+# composition pins: which rows each update sees, where the advantages come from, how the
+# optimiser step is counted, and the first update's closed form. The oracle's parts are pinned
+# elsewhere; these pin how Algorithm 1's learning phase strings them together.
+
+
+def _row_coded_obs(n, net):
+    """Frames whose first two bytes spell their own row index (row = 256 * b0 + b1), the rest
+    seeded noise, so a spy on the forward pass can tell which rollout rows it was given."""
+    rng = np.random.default_rng(17)
+    obs = rng.integers(0, 256, size=(n, net.in_h, net.in_w, net.in_c), dtype=np.uint8)
+    obs[:, 0, 0, 0] = np.arange(n) // 256
+    obs[:, 0, 0, 1] = np.arange(n) % 256
+    return obs
+
+
+def _spy(monkeypatch, module, name, log, keep):
+    """Wrap module.name so each call appends keep(*args) to log, then runs the original."""
+    orig = getattr(module, name)
+
+    def wrapped(*args, **kw):
+        log.append(keep(*args, **kw))
+        return orig(*args, **kw)
+    monkeypatch.setattr(module, name, wrapped)
+
+
+def _ppo_rollout(wl, net, values=None, dones=None, next_done=None, seed=5):
+    rng = np.random.default_rng(seed)
+    T, E, n = wl.T, wl.E, wl.T * wl.E
+    return dict(obs=_row_coded_obs(n, net), actions=rng.integers(0, net.num_actions, n).astype(np.int32),
+                logp=(np.log(1.0 / net.num_actions) + 0.05 * rng.standard_normal(n)).astype(np.float32),
+                rewards=rng.choice(np.array([-1.0, 0.0, 1.0], np.float32), size=(T, E)),
+                values=(rng.standard_normal((T, E)) if values is None else values).astype(np.float32),
+                dones=(rng.random((T, E)) < 0.1).astype(np.uint8) if dones is None else dones,
+                next_value=rng.standard_normal(E).astype(np.float32),
+                next_done=np.zeros(E, np.uint8) if next_done is None else next_done)
+
+
+def test_ppo_phase_is_appendix_a_worked_example(tiny_net, monkeypatch):
+    """Appendix A's worked example: 8 envs x 128 steps give 1024 rows; 4 minibatches of 256;
+    K = 4 epochs give 16 gradient updates. Update (j, k) reads exactly the rows
+    perm[j, 256k : 256(k+1)] in that order, so every row is read once per epoch, 4 times in all,
+    and the optimiser step runs 16 times with t = 1..16."""
+    from oracle import cfg as ocfg
+    from synth import Workload
+    from oracle import optim as ooptim
+    d = ocfg.derive(world_size=1, local_num_envs=8, num_steps=128, num_minibatches=4, update_epochs=4)
+    assert (d["local_batch_size"], d["local_minibatch_size"], d["updates"]) == (1024, 256, 16)
+    wl = Workload("appA", "ppo", T=128, E=8, net=tiny_net, epochs=4, num_minibatches=4, seed=3)
+    assert wl.mb == 256 and wl.n_updates == 16
+    ro = _ppo_rollout(wl, tiny_net)
+    perm = np.stack([np.random.default_rng(40 + j).permutation(1024) for j in range(4)]).astype(np.int32)
+    seen, steps = [], []
+    _spy(monkeypatch, onet, "forward", seen,
+         lambda net, p, obs, prec="fp64": 256 * obs[:, 0, 0, 0].astype(np.int64) + obs[:, 0, 0, 1])
+    _spy(monkeypatch, ooptim, "adam", steps, lambda p, g, m, v, step, *a, **k: step)
+    p0 = draw_params(tiny_net, 2).astype(np.float64)
+    z = np.zeros_like(p0)
+    _, _, _, step, stats = learner.ppo_learner_step(tiny_net, wl, ro, p0, z, z, 0, perm)
+    assert step == 16 and stats.shape == (16, 8)
+    assert steps == list(range(1, 17))
+    assert len(seen) == 16
+    for u, rows in enumerate(seen):
+        j, k = divmod(u, 4)
+        np.testing.assert_array_equal(rows, perm[j, 256 * k:256 * (k + 1)])
+    for j in range(4):
+        np.testing.assert_array_equal(np.sort(np.concatenate(seen[4 * j:4 * j + 4])), np.arange(1024))
+    np.testing.assert_array_equal(np.bincount(np.concatenate(seen), minlength=1024), np.full(1024, 4))
+
+
+def test_ppo_advantages_are_taken_once_from_the_rollout(tiny_net, monkeypatch):
+    """Algorithm 1 computes the advantages and returns once, from the stored values, before the
+    epochs; each minibatch then takes its rows of them. With every transition terminal
+    (all d = 1) GAE reduces to A = r - V and R = r for any lambda, whatever the network now
+    predicts: every update of a 2-epoch phase with a non-zero learning rate must be handed
+    exactly those values at its rows (a recomputation from the current network, or a slice
+    that does not follow perm, fails)."""
+    from synth import Workload
+    from oracle import losses as olosses
+    wl = Workload("once", "ppo", T=6, E=4, net=tiny_net, epochs=2, num_minibatches=3, lam=0.95,
+                  lr=1e-2, seed=3)
+    T, E = wl.T, wl.E
+    ro = _ppo_rollout(wl, tiny_net, dones=np.ones((T, E), np.uint8), next_done=np.ones(E, np.uint8))
+    perm = np.stack([np.random.default_rng(50 + j).permutation(T * E) for j in range(2)]).astype(np.int32)
+    got = []
+    _spy(monkeypatch, olosses, "ppo_loss_grad", got,
+         lambda z, v, a, old, adv, ret, *rest, **kw: (np.array(adv), np.array(ret), np.array(a), np.array(old)))
+    p0 = draw_params(tiny_net, 2).astype(np.float64)
+    zero = np.zeros_like(p0)
+    p1 = learner.ppo_learner_step(tiny_net, wl, ro, p0, zero, zero, 0, perm)[0]
+    assert np.abs(p1 - p0).max() > 1e-3          # the network did move between updates
+    a_want = (ro["rewards"].astype(np.float64) - ro["values"]).ravel()
+    r_want = ro["rewards"].astype(np.float64).ravel()
+    assert len(got) == 6
+    for u, (adv, ret, act, old) in enumerate(got):
+        j, k = divmod(u, 3)
+        rows = perm[j, 8 * k:8 * (k + 1)]
+        np.testing.assert_allclose(adv, a_want[rows], rtol=0, atol=1e-6)
+        np.testing.assert_allclose(ret, r_want[rows], rtol=0, atol=1e-6)
+        np.testing.assert_array_equal(act, ro["actions"][rows])
+        np.testing.assert_array_equal(old, ro["logp"][rows])
+
+
+def test_ppo_first_update_is_clipped_adam_step_one(tiny_net):
+    """The first update of a phase started at step 0 is Adam at t = 1, where the bias
+    corrections give m_hat = g and v_hat = g^2, so p1 = p0 - lr g_c / (|g_c| + eps), with g_c
+    the minibatch gradient scaled to norm min(||g||, omega). The gradient is formed here from
+    the oracle's forward, loss and backward on the minibatch rows; omega is set below ||g||
+    so the clip acts. A phase entered at step s continues at t = s + 1."""
+    from synth import Workload
+    wl = Workload("first", "ppo", T=4, E=3, net=tiny_net, epochs=1, num_minibatches=2, lr=1e-3, seed=3)
+    ro = _ppo_rollout(wl, tiny_net)
+    perm = np.random.default_rng(7).permutation(12).astype(np.int32)[None]
+    p0 = draw_params(tiny_net, 2).astype(np.float64)
+    rows = perm[0, :6]
+    from oracle import losses as olosses, targets as otargets
+    adv, ret = otargets.gae(ro["rewards"], ro["values"], ro["dones"], ro["next_value"], ro["next_done"],
+                            wl.gamma, wl.lam)
+    zz, vv, cache = onet.forward(tiny_net, p0, ro["obs"][rows])
+    _, dz, dv, _ = olosses.ppo_loss_grad(zz, vv, ro["actions"][rows], ro["logp"][rows], adv.ravel()[rows],
+                                         ret.ravel()[rows], wl.clip_eps, wl.vf_coef, wl.ent_coef)
+    g = onet.backward(tiny_net, cache, dz, dv)
+    gn = np.linalg.norm(g)
+    wl = wl.replace(max_grad_norm=0.5 * gn, num_minibatches=1, minibatch_size=6)
+    gc = g * 0.5
+    zero = np.zeros_like(p0)
+    p1, m1, v1, step, stats = learner.ppo_learner_step(tiny_net, wl, ro, p0, zero, zero, 0, perm)
+    assert step == 1
+    np.testing.assert_allclose(stats[0, 6], gn, rtol=1e-12)
+    np.testing.assert_allclose(p1, p0 - wl.lr * gc / (np.abs(gc) + wl.adam_eps), rtol=0, atol=1e-15)
+    np.testing.assert_allclose(m1, 0.1 * gc, rtol=1e-12, atol=0)
+    np.testing.assert_allclose(v1, 0.001 * gc * gc, rtol=1e-12, atol=0)
+    # entered at step 4 with the same zero moments: t = 5, m_hat = 0.1 g / (1 - 0.9^5)
+    p5, _, _, step5, _ = learner.ppo_learner_step(tiny_net, wl, ro, p0, zero, zero, 4, perm)
+    assert step5 == 5
+    mh = 0.1 * gc / (1 - 0.9 ** 5)
+    vh = 0.001 * gc * gc / (1 - 0.999 ** 5)
+    np.testing.assert_allclose(p5, p0 - wl.lr * mh / (np.sqrt(vh) + wl.adam_eps), rtol=0, atol=1e-15)
+
+
+def test_impala_updates_read_their_env_block_and_fresh_targets(tiny_net, monkeypatch):
+    """IMPALA with N env-block minibatches: update k runs the forward over block k's T*Eb
+    rollout frames in (t, e) order followed by its Eb bootstrap frames, and V-trace reads the
+    log-probabilities and values of that same forward (the current parameters, not the
+    behaviour policy's), the block's rewards and dones, and the bootstrap frames' values.
+    Steps are counted t = 1..N."""
+    from synth import Workload
+    from oracle import optim as ooptim, targets as otargets, losses as olosses
+    wl = Workload("blocks", "impala", T=3, E=6, net=tiny_net, num_minibatches=3, lam=1.0, lr=1e-2,
+                  max_grad_norm=40.0, behav_logp_noise=0.0, behav_logit_noise=0.3, seed=9)
+    T, E, Eb = 3, 6, 2
+    rng = np.random.default_rng(8)
+    n = T * E
+    ro = dict(obs=_row_coded_obs((T + 1) * E, tiny_net), actions=rng.integers(0, 3, n).astype(np.int32),
+              logp=np.log(np.full(n, 1 / 3)).astype(np.float32) + 0.1 * rng.standard_normal(n).astype(np.float32),
+              rewards=rng.choice(np.array([-1.0, 0.0, 1.0], np.float32), size=(T, E)),
+              dones=(rng.random((T, E)) < 0.2).astype(np.uint8), next_done=np.array([0, 1, 0, 0, 1, 0], np.uint8))
+    fwd, vt, steps = [], [], []
+    plain_forward = onet.forward
+    _spy(monkeypatch, onet, "forward", fwd,
+         lambda net, p, obs, prec="fp64": (256 * obs[:, 0, 0, 0].astype(np.int64) + obs[:, 0, 0, 1], np.array(p)))
+    _spy(monkeypatch, otargets, "vtrace", vt, lambda *a, **k: [np.array(x) for x in a[:7]])
+    _spy(monkeypatch, ooptim, "adam", steps, lambda p, g, m, v, step, *a, **k: step)
+    p0 = draw_params(tiny_net, 2).astype(np.float64)
+    zero = np.zeros_like(p0)
+    learner.impala_learner_step(tiny_net, wl, ro, p0, zero, zero, 0)
+    assert steps == [1, 2, 3] and len(fwd) == 3 and len(vt) == 3
+    for k in range(3):
+        envs = np.arange(k * Eb, (k + 1) * Eb)
+        want_rows = np.concatenate([(t * E + envs) for t in range(T + 1)])
+        rows, p = fwd[k]
+        np.testing.assert_array_equal(rows, want_rows)
+        if k:
+            assert np.abs(p - fwd[k - 1][1]).max() > 0      # parameters moved in between
+        z, val, _ = plain_forward(tiny_net, p, ro["obs"][want_rows])
+        behav, tgt, rew, values, dones, boot, nd = vt[k]
+        np.testing.assert_array_equal(behav.ravel(), ro["logp"][want_rows[:T * Eb]])
+        lp = olosses.log_softmax(z[:T * Eb])[np.arange(T * Eb), ro["actions"][want_rows[:T * Eb]]]
+        np.testing.assert_allclose(tgt.ravel(), lp, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(values.ravel(), val[:T * Eb], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(boot, val[T * Eb:], rtol=0, atol=1e-12)
+        np.testing.assert_array_equal(rew, ro["rewards"][:, envs])
+        np.testing.assert_array_equal(dones, ro["dones"][:, envs])
+        np.testing.assert_array_equal(nd, ro["next_done"][envs])
