@@ -145,6 +145,47 @@ impala_status_t impala_maxpool_bwd(impala_prec_t prec, int64_t n, int32_t H, int
                                    const uint8_t* arg, const void* dy, void* dx,
                                    hipStream_t stream);
 
+/* Where a training-mode impala_cnn_fwd on n_frames frames (workspace laid out by
+ * impala_workspace_bytes(net, n_frames, prec, 1)) leaves the activations that impala_cnn_bwd
+ * reads, so a caller can inspect them or replace them between the two calls: the backward
+ * pass (Algorithm 1's back-propagation) then differentiates the network at the activations it
+ * finds there, taking every ReLU decision from the stored x and t and every max-pool routing
+ * from the stored argmax. Tests use this to evaluate the backward pass at a reference
+ * forward's activations.
+ * Regions, each frame-major ([n_frames, ...], frame i at offset + i * bytes / n_frames):
+ *   "s<k>.arg"  uint8 [n, ceil(H_k/2), ceil(W_k/2), C_k]  stage k's max-pool argmax, the
+ *               row-major window index 0..8 as impala_maxpool_fwd returns it;
+ *   "s<k>.x0"   the pooled output of stage k (input of its residual block 0);
+ *   "s<k>.x1", "s<k>.x2"  the outputs of residual blocks 0 and 1 (x2 feeds stage k+1's
+ *               entry conv, or for k = 2 the flatten);
+ *   "s<k>.t0", "s<k>.t1"  the inner activation t = conv(relu(x)) + b of blocks 0 and 1;
+ *   "h"         [n, hidden], the dense layer's output after its ReLU;
+ *   "s<k>.conv" (IMPALA_PREC_FP32 only) [n, H_k, W_k, C_k], the stage entry's conv output
+ *               before pooling (the bf16 path pools on chip and never stores it).
+ * x, t, h and conv are bf16 bit patterns in IMPALA_PREC_BF16 and float32 otherwise; stage k
+ * reads [H_k, W_k] (the frame for k = 0, halved, rounded up, per stage). The first stage's
+ * input is the uint8 frames themselves, read through row_idx. Writes `cap` descriptors at most
+ * into `out` (host memory) and returns the number of regions (19 bf16, 22 float32), or a
+ * negative status. */
+typedef enum { IMPALA_DT_U8 = 0, IMPALA_DT_BF16 = 1, IMPALA_DT_F32 = 2 } impala_dtype_t;
+typedef struct impala_activation_desc {
+    char name[32];
+    int64_t offset;    /* bytes from the start of the workspace */
+    int64_t bytes;     /* bytes of the region's n_frames frames */
+    int32_t dtype;     /* impala_dtype_t */
+    int32_t ndim;
+    int64_t shape[4];  /* [n_frames, H, W, C] or [n_frames, hidden] */
+} impala_activation_desc_t;
+int impala_activation_layout(const impala_net_t* net, impala_prec_t prec, int64_t n_frames,
+                             impala_activation_desc_t* out, int cap);
+
+/* Log-probability of given actions under given logits, the target log-probs that V-trace
+ * reads (log pi(a_t|s_t) in Espeholt et al.'s importance weights, which Appendix B's rlax
+ * V-trace takes): logp[i] = log_softmax(logits[i])[actions[i]], NaN where actions[i] is
+ * outside [0, A). logits: float [n, A]; actions: int32 [n]; logp: float [n]. */
+impala_status_t impala_action_logp(int64_t n, int32_t A, const float* logits, const int32_t* actions,
+                                   float* logp, hipStream_t stream);
+
 /* Gumbel-max sampling on given logits: actions[i] = argmax_j (logits[i][j] + gumbel[i][j])
  * (float32 sums, ties to the lowest index) and logp[i] = log_softmax(logits[i])[actions[i]]. */
 impala_status_t impala_gumbel_sample(int64_t n, int32_t A, const float* logits,

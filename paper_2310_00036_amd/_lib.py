@@ -30,6 +30,14 @@ class TensorDesc(C.Structure):
                 ("shape", C.c_int32 * 4)]
 
 
+class ActivationDesc(C.Structure):
+    _fields_ = [("name", C.c_char * 32), ("offset", C.c_int64), ("bytes", C.c_int64), ("dtype", C.c_int32),
+                ("ndim", C.c_int32), ("shape", C.c_int64 * 4)]
+
+
+DT_U8, DT_BF16, DT_F32 = 0, 1, 2
+
+
 class LearnerCfg(C.Structure):
     _fields_ = [("algo", C.c_int32), ("prec", C.c_int32), ("T", C.c_int32), ("E", C.c_int32),
                 ("update_epochs", C.c_int32), ("num_minibatches", C.c_int32),
@@ -55,6 +63,7 @@ _SIGS = {
     "impala_param_count": (_I64, [_NETP]),
     "impala_param_layout": (C.c_int, [_NETP, C.POINTER(TensorDesc), C.c_int]),
     "impala_workspace_bytes": (_SZ, [_NETP, _I64, C.c_int, C.c_int]),
+    "impala_activation_layout": (C.c_int, [_NETP, C.c_int, _I64, C.POINTER(ActivationDesc), C.c_int]),
     "impala_last_error": (C.c_char_p, []),
     "impala_cnn_fwd": (C.c_int, [_NETP, C.c_int, _P, _P, _P, _I64, _P, _SZ, C.c_int, _P, _P, _P]),
     "impala_cnn_bwd": (C.c_int, [_NETP, C.c_int, _P, _P, _P, _I64, _P, _SZ, _P, _P, _P, _P]),
@@ -90,6 +99,7 @@ _SIGS = {
     "impala_maxpool_fwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _P, _P, _P, _P]),
     "impala_maxpool_bwd": (C.c_int, [C.c_int, _I64, _I32, _I32, _I32, _P, _P, _P, _P]),
     "impala_gumbel_sample": (C.c_int, [_I64, _I32, _P, _P, _P, _P, _P]),
+    "impala_action_logp": (C.c_int, [_I64, _I32, _P, _P, _P, _P]),
     "impala_profile_begin": (C.c_int, [C.c_char_p, _I32]),
     "impala_profile_end": (C.c_int, []),
     "impala_profile_key": (C.c_int, [_I32, C.c_char_p, _SZ, C.POINTER(C.c_double), C.POINTER(_I32)]),
@@ -176,6 +186,17 @@ def impala_param_layout(net) -> list:
 
 def impala_workspace_bytes(net, n_frames: int, prec: int, training: int) -> int:
     return int(lib.impala_workspace_bytes(C.byref(net_struct(net)), n_frames, prec, training))
+
+
+def impala_activation_layout(net, prec: int, n_frames: int) -> list:
+    """[(name, byte offset, bytes, dtype, shape)] of the activations a training-mode forward on
+    n_frames frames leaves in its workspace (dtype: DT_U8, DT_BF16 or DT_F32)."""
+    descs = (ActivationDesc * 64)()
+    k = lib.impala_activation_layout(C.byref(net_struct(net)), prec, n_frames, descs, 64)
+    if k < 0:
+        raise LibraryError("impala_activation_layout", k)
+    return [(d.name.decode(), int(d.offset), int(d.bytes), int(d.dtype), tuple(d.shape[i] for i in range(d.ndim)))
+            for d in descs[:k]]
 
 
 def impala_cnn_fwd(net, prec, params, obs, row_idx, n, ws, training, logits, value, stream=None):
@@ -365,6 +386,11 @@ def impala_maxpool_bwd(prec, n, H, W, C_, arg, dy, dx, stream=None):
 def impala_gumbel_sample(n, A, logits, gumbel, actions, logp, stream=None):
     _check("impala_gumbel_sample", lib.impala_gumbel_sample(n, A, ptr(logits), ptr(gumbel), ptr(actions),
                                                             ptr(logp), stream_handle(stream)))
+
+
+def impala_action_logp(n, A, logits, actions, logp, stream=None):
+    _check("impala_action_logp", lib.impala_action_logp(n, A, ptr(logits), ptr(actions), ptr(logp),
+                                                        stream_handle(stream)))
 
 
 def impala_profile_begin(only_key: str | None = None, max_launches: int = 1 << 16) -> None:

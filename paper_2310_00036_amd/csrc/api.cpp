@@ -219,6 +219,53 @@ int impala_param_layout(const impala_net_t* net, impala_tensor_desc_t* out, int 
     return k;
 }
 
+int impala_activation_layout(const impala_net_t* net, impala_prec_t prec, int64_t n_frames,
+                             impala_activation_desc_t* out, int cap) {
+    const std::string e = check_net(net);
+    if (!e.empty()) return fail(IMPALA_EINVAL, "impala_activation_layout: %s", e.c_str());
+    if (!valid_prec(prec)) return fail(IMPALA_EINVAL, "impala_activation_layout: bad prec %d", int(prec));
+    if (n_frames < 1 || n_frames > (int64_t(1) << 24))
+        return fail(IMPALA_EINVAL, "impala_activation_layout: n_frames out of range");
+    if (!out && cap > 0) return fail(IMPALA_EINVAL, "impala_activation_layout: out is NULL");
+    const NetPlan p = make_plan(*net, prec, n_frames, 1);
+    const int act = prec == IMPALA_PREC_BF16 ? IMPALA_DT_BF16 : IMPALA_DT_F32;
+    int k = 0;
+    auto put = [&](const char* name, size_t off, int dtype, int es, int64_t s1, int64_t s2, int64_t s3) {
+        if (k < cap) {
+            impala_activation_desc_t& d = out[k];
+            std::memset(&d, 0, sizeof(d));
+            std::snprintf(d.name, sizeof(d.name), "%s", name);
+            d.offset = int64_t(off);
+            d.dtype = dtype;
+            d.ndim = s3 > 0 ? 4 : 2;
+            d.shape[0] = n_frames; d.shape[1] = s1; d.shape[2] = s3 > 0 ? s2 : 0; d.shape[3] = s3;
+            d.bytes = n_frames * s1 * (s3 > 0 ? s2 * s3 : 1) * es;
+        }
+        ++k;
+    };
+    char nm[32];
+    for (int s = 0; s < 3; ++s) {
+        const int C = p.C[s + 1], OH = p.H[s + 1], OW = p.W[s + 1];
+        if (prec == IMPALA_PREC_FP32) {
+            std::snprintf(nm, sizeof(nm), "s%d.conv", s);
+            put(nm, p.c[s], act, p.es, p.H[s], p.W[s], C);
+        }
+        std::snprintf(nm, sizeof(nm), "s%d.arg", s);
+        put(nm, p.idx[s], IMPALA_DT_U8, 1, OH, OW, C);
+        for (int r = 0; r < 3; ++r) {
+            std::snprintf(nm, sizeof(nm), "s%d.x%d", s, r);
+            put(nm, p.x[s][r], act, p.es, OH, OW, C);
+        }
+        for (int r = 0; r < 2; ++r) {
+            std::snprintf(nm, sizeof(nm), "s%d.t%d", s, r);
+            put(nm, p.t[s][r], act, p.es, OH, OW, C);
+        }
+    }
+    put("h", p.h, act, p.es, p.hidden, 0, 0);
+    ok();
+    return k;
+}
+
 size_t impala_workspace_bytes(const impala_net_t* net, int64_t n_frames, impala_prec_t prec,
                               int training) {
     const std::string e = check_net(net);
@@ -734,6 +781,15 @@ impala_status_t impala_maxpool_bwd(impala_prec_t prec, int64_t n, int32_t H, int
     if (n == 0) return ok();
     CHECK_PTR(arg); CHECK_PTR(dy); CHECK_PTR(dx);
     return hip_status(maxpool_bwd(prec, int(n), H, W, C, arg, dy, dx, stream), "impala_maxpool_bwd");
+}
+
+impala_status_t impala_action_logp(int64_t n, int32_t A, const float* logits, const int32_t* actions,
+                                   float* logp, hipStream_t stream) {
+    if (n < 0 || n > (int64_t(1) << 26) || A < 1 || A > 64)
+        return fail(IMPALA_EINVAL, "impala_action_logp: bad n or A");
+    if (n == 0) return ok();
+    CHECK_PTR(logits); CHECK_PTR(actions); CHECK_PTR(logp);
+    return hip_status(action_logp(n, A, logits, actions, logp, stream), "impala_action_logp");
 }
 
 impala_status_t impala_gumbel_sample(int64_t n, int32_t A, const float* logits, const float* gumbel,

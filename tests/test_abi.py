@@ -4,6 +4,7 @@ import ctypes as C
 import os
 import re
 
+import numpy as np
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -134,3 +135,42 @@ def test_workspace_grows_with_frames_and_precision():
     d = P.impala_workspace_bytes(net, 256, P.PREC_BF16, 0)
     assert b > a and abs((e - b) - 2 * (b - a)) <= 0.02 * (e - b)
     assert c > 1.5 * a and d < a
+
+
+@pytest.mark.parametrize("prec", [0, 1], ids=["bf16", "fp32"])
+@pytest.mark.parametrize("net", [NetShape(), NetShape(ch=(32, 64, 64), hidden=512),
+                                 NetShape(in_h=12, in_w=10, ch=(16, 16, 32), hidden=8, num_actions=3)])
+def test_activation_layout_is_disjoint_and_inside_the_workspace(net, prec):
+    """The saved-activation regions of a training forward: the names and shapes of the network's
+    stages, disjoint, inside impala_workspace_bytes(net, n, prec, 1), element sizes per dtype."""
+    n = 37
+    lay = P.impala_activation_layout(net, prec, n)
+    total = P.impala_workspace_bytes(net, n, prec, 1)
+    es = {P.DT_U8: 1, P.DT_BF16: 2, P.DT_F32: 4}
+    act = P.DT_BF16 if prec == 0 else P.DT_F32
+    names = [d[0] for d in lay]
+    want = []
+    h, w = net.in_h, net.in_w
+    shapes = {}
+    for s, c in enumerate(net.ch):
+        oh, ow = -(-h // 2), -(-w // 2)
+        if prec == 1:
+            want.append(f"s{s}.conv")
+            shapes[f"s{s}.conv"] = ((n, h, w, c), act)
+        for k in ("arg", "x0", "x1", "x2", "t0", "t1"):
+            want.append(f"s{s}.{k}")
+            shapes[f"s{s}.{k}"] = ((n, oh, ow, c), P.DT_U8 if k == "arg" else act)
+        h, w = oh, ow
+    want.append("h")
+    shapes["h"] = ((n, net.hidden), act)
+    assert names == want and len(lay) == (22 if prec == 1 else 19)
+    spans = []
+    for name, off, nbytes, dt, shape in lay:
+        assert (shape, dt) == shapes[name], name
+        assert nbytes == int(np.prod(shape)) * es[dt]
+        assert off % 256 == 0 and off + nbytes <= total
+        spans.append((off, off + nbytes))
+    spans.sort()
+    assert all(a[1] <= b[0] for a, b in zip(spans, spans[1:]))
+    with pytest.raises(P.LibraryError):
+        P.impala_activation_layout(net, prec, 0)

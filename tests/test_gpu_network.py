@@ -456,17 +456,22 @@ def test_learner_step_is_deterministic_and_resumable():
         assert torch.equal(x, y)
 
 
-@pytest.mark.parametrize("wid", [1, 5], ids=["cleanba_like_2_updates", "paper_ppo_shape_16_updates"])
-def test_learner_step_equals_its_abi_calls(wid):
+@pytest.mark.parametrize("wid,prec", [(0, G.BF16), (0, G.FP32), (1, G.BF16), (4, G.BF16), (5, G.BF16)],
+                         ids=["tiny_ppo_bf16", "tiny_ppo_fp32", "cleanba_like_2_updates", "wide_mb8192",
+                              "paper_ppo_shape_16_updates"])
+def test_learner_step_equals_its_abi_calls(wid, prec):
     """learner_step (PPO) is exactly GAE, then per minibatch impala_cnn_fwd with the permuted
-    rows, ppo_loss_grad on the gathered rows, impala_cnn_bwd and adam_step: two updates of the
-    Cleanba-like shape, and all 16 updates of the paper's shape (128 envs x 128 steps, 4
-    minibatches of 4096, 4 epochs)."""
+    rows, ppo_loss_grad on the gathered rows, impala_cnn_bwd and adam_step: the tiny workload's
+    full-batch update in both precisions, two updates of the Cleanba-like shape, the wide net's
+    8192-frame minibatch of a 16384-frame rollout, and all 16 updates of the paper's shape (128
+    envs x 128 steps, 4 minibatches of 4096, 4 epochs). With each of those calls checked against
+    the oracle at the oracle's activations (test_gpu_forced.py), this carries that parity to
+    learner_step."""
     torch = G.torch()
     wl, params, ro, perm = _c1_like_inputs(wid=wid)
     if wid == 1:
         wl = wl.replace(epochs=1, num_minibatches=2)
-    net, prec = wl.net, G.BF16
+    net = wl.net
     got = _learner_gpu(wl, prec, params, ro, perm)
     d = _gpu_rollout(ro, wl)
     T, E, A, mb = wl.T, wl.E, net.num_actions, wl.mb
@@ -500,6 +505,94 @@ def test_learner_step_equals_its_abi_calls(wid):
     G.sync()
     assert torch.equal(got[0], p) and torch.equal(got[1], m) and torch.equal(got[2], v)
     assert torch.equal(got[4], stats)
+
+
+def _impala_inputs(wl, seed):
+    """IMPALA rollout with behaviour data drawn without the network (GPU-against-GPU tests)."""
+    raw = draw_rollout(wl)
+    T, E, A = wl.T, wl.E, wl.net.num_actions
+    rng = np.random.default_rng(seed)
+    ro = dict(obs=raw["obs"].reshape((T + 1) * E, 84, 84, 4), actions=rng.integers(0, A, T * E).astype(np.int32),
+              logp=(np.log(1.0 / A) + 0.3 * rng.standard_normal(T * E)).astype(np.float32),
+              rewards=raw["rewards"], dones=raw["dones"], next_done=raw["next_done"])
+    return ro, draw_params(wl.net, wl.seed)
+
+
+def test_impala_learner_step_equals_its_abi_calls():
+    """learner_step (IMPALA / V-trace, 64 envs x 20 steps + 64 bootstrap frames) is
+    impala_cnn_fwd over the 1344 frames, impala_action_logp of the rollout rows, vtrace_targets
+    (the bootstrap frames' values as V_T), impala_loss_grad, the backward pass and adam_step.
+    learner_step runs its backward over the 1280 rollout frames of the forward's workspace;
+    through the C-ABI the backward takes the forward's 1344 frames, the bootstrap rows with zero
+    gradient, which sums the same terms in another grouping: the targets and loss outputs are
+    bit-identical, the gradient (Adam's first moment) within 1e-5 per tensor."""
+    torch = G.torch()
+    wl = WORKLOADS[2]
+    net, prec = wl.net, G.BF16
+    T, E, A = wl.T, wl.E, net.num_actions
+    n, n1 = T * E, (T + 1) * E
+    ro, params = _impala_inputs(wl, 7)
+    got = _learner_gpu(wl, prec, params, ro, None)
+    d = _gpu_rollout(ro, wl)
+    p = G.dev_f32(params)
+    m, v = torch.zeros_like(p), torch.zeros_like(p)
+    ws = G.ws_bytes(P.impala_workspace_bytes(net, n1, prec, 1))
+    aws = G.ws_bytes(P.adam_workspace_bytes(p.numel()))
+    logits = torch.empty((n1, A), dtype=torch.float32, device="cuda:0")
+    value = torch.empty(n1, dtype=torch.float32, device="cuda:0")
+    P.impala_cnn_fwd(net, prec, p, d["obs"], None, n1, ws, 1, logits, value)
+    tlogp = torch.empty(n, dtype=torch.float32, device="cuda:0")
+    P.impala_action_logp(n, A, logits, d["actions"], tlogp)
+    vs, pg = torch.empty(n, dtype=torch.float32, device="cuda:0"), torch.empty(n, dtype=torch.float32, device="cuda:0")
+    P.vtrace_targets(T, E, d["logp"], tlogp, d["rewards"], value[:n], d["dones"], value[n:], d["next_done"],
+                     wl.gamma, wl.lam, wl.rho_bar, wl.c_bar, wl.pg_rho_bar, vs, pg)
+    dz, dv = torch.zeros((n1, A), dtype=torch.float32, device="cuda:0"), torch.zeros(n1, dtype=torch.float32,
+                                                                                     device="cuda:0")
+    stats = torch.zeros((1, 8), dtype=torch.float32, device="cuda:0")
+    P.impala_loss_grad(n, A, logits, value, d["actions"], vs, pg, wl.pg_coef, wl.vf_coef, wl.ent_coef, dz, dv,
+                       stats[0])
+    grads = torch.empty_like(p)
+    P.impala_cnn_bwd(net, prec, p, d["obs"], None, n1, ws, dz, dv, grads)
+    P.adam_step(p.numel(), p, grads, m, v, 1, wl.lr, wl.beta1, wl.beta2, wl.adam_eps, wl.max_grad_norm,
+                stats[0, 6:], aws)
+    G.sync()
+    assert got[3] == 1
+    assert torch.equal(got[4][:, :6], stats[:, :6])          # loss statistics: bit-identical
+    gm, cm = G.host(got[1]), G.host(m)
+    errs = _tensor_errs(gm, cm, net)
+    assert max(errs.values()) <= 1e-5, max(errs.items(), key=lambda kv: kv[1])
+    assert G.rel_l2(G.host(got[2]), G.host(v)) <= 2e-5
+    assert G.rel_l2(G.host(got[0]) - params, G.host(p) - params) <= 1e-4
+    assert abs(float(got[4][0, 6]) - float(stats[0, 6])) <= 1e-5 * float(stats[0, 6])
+
+
+def test_impala_env_block_minibatches_equal_chained_sub_rollouts():
+    """The paper's IMPALA shape (128 envs x 20 steps, 4 env-block minibatches, RMSprop): one
+    learner_step equals four single-minibatch learner_steps on the blocks' own sub-rollouts
+    (each block's 20 x 32 frames and 32 bootstrap frames copied out, with its actions,
+    behaviour log-probs, rewards and done flags), chained through the parameters, the RMSprop
+    state and the step count, bit for bit."""
+    torch = G.torch()
+    wl = WORKLOADS[6]
+    T, E, nmb = wl.T, wl.E, wl.num_minibatches
+    Eb = E // nmb
+    ro, params = _impala_inputs(wl, 8)
+    got = _learner_gpu(wl, G.BF16, params, ro, None)
+    state = None
+    rows_stats = []
+    for k in range(nmb):
+        envs = np.arange(k * Eb, (k + 1) * Eb)
+        rows = (np.arange(T + 1)[:, None] * E + envs[None, :]).ravel()
+        sub = dict(obs=ro["obs"][rows], actions=ro["actions"][rows[:T * Eb]], logp=ro["logp"][rows[:T * Eb]],
+                   rewards=np.ascontiguousarray(ro["rewards"][:, envs]),
+                   dones=np.ascontiguousarray(ro["dones"][:, envs]), next_done=ro["next_done"][envs])
+        out = _learner_gpu(wl.replace(E=Eb, num_minibatches=1), G.BF16, params, sub, None, state=state)
+        state = (out[0], out[1], out[2], out[3])
+        rows_stats.append(out[4])
+    assert got[3] == state[3] == nmb
+    for x, y in zip(got[:3], state[:3]):
+        assert torch.equal(x, y)
+    assert torch.equal(got[4], torch.cat(rows_stats))
 
 
 @pytest.mark.parametrize("prec", [G.BF16, G.FP32], ids=lambda p: PNAME[p])
