@@ -170,6 +170,18 @@ impala_status_t adam_step(int64_t n_params, float* params, const float* grads, f
                           float max_grad_norm, float* stats, void* ws, size_t ws_bytes,
                           hipStream_t stream);
 
+/* adam_step without a workspace, for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the same kernels
+ * and results as adam_step (bit for bit), with the norm's partial sums in a buffer the library
+ * holds on each GPU it runs on (8 KB per device, kept until the process ends). It calls no
+ * allocating routine. Calls that overlap on one GPU share that buffer and race: order them on
+ * one stream, or use adam_step with a workspace each. Arguments and errors as adam_step;
+ * IMPALA_EINVAL if the partial sums would outgrow the buffer (they never do: their count is
+ * capped at 1024 for every n_params), IMPALA_EHIP if the buffer's address cannot be found. */
+impala_status_t adam_step_noalloc(int64_t n_params, float* params, const float* grads, float* m,
+                                  float* v, int32_t step, float lr, float beta1, float beta2,
+                                  float eps, float max_grad_norm, float* stats, hipStream_t stream);
+
 /* Global-norm clip then RMSprop over the flat buffers (Algorithm 1: clip the gradient norm,
  * step the optimiser; Appendix B's IMPALA table: RMSprop with epsilon 0.01, decay 0.99):
  *   g as adam_step's clip;  nu <- decay nu + (1 - decay) g^2;  p <- p - lr g / sqrt(nu + eps).

@@ -73,6 +73,7 @@ _SIGS = {
     "impala_loss_grad": (C.c_int, [_I64, _I32, _P, _P, _P, _P, _P, _F, _F, _F, _P, _P, _P, _P]),
     "adam_workspace_bytes": (_SZ, [_I64]),
     "adam_step": (C.c_int, [_I64, _P, _P, _P, _P, _I32, _F, _F, _F, _F, _F, _P, _P, _SZ, _P]),
+    "adam_step_noalloc": (C.c_int, [_I64, _P, _P, _P, _P, _I32, _F, _F, _F, _F, _F, _P, _P]),
     "rmsprop_workspace_bytes": (_SZ, [_I64]),
     "rmsprop_step": (C.c_int, [_I64, _P, _P, _P, _F, _F, _F, _F, _P, _P, _SZ, _P]),
     "learner_workspace_bytes": (_SZ, [_NETP, C.POINTER(LearnerCfg)]),
@@ -249,6 +250,13 @@ def adam_step(n_params, params, grads, m, v, step, lr, beta1, beta2, eps, max_gr
     _check("adam_step", lib.adam_step(
         n_params, ptr(params), ptr(grads), ptr(m), ptr(v), step, lr, beta1, beta2, eps,
         max_grad_norm, ptr(stats), ptr(ws), ws.numel() * ws.element_size(), stream_handle(stream)))
+
+
+def adam_step_noalloc(n_params, params, grads, m, v, step, lr, beta1, beta2, eps, max_grad_norm, stats,
+                      stream=None):
+    _check("adam_step_noalloc", lib.adam_step_noalloc(
+        n_params, ptr(params), ptr(grads), ptr(m), ptr(v), step, lr, beta1, beta2, eps, max_grad_norm,
+        ptr(stats), stream_handle(stream)))
 
 
 def rmsprop_workspace_bytes(n_params: int) -> int:

@@ -6,6 +6,8 @@
 // clip scale, then updates the parameters and the optimiser state with 16-byte vector
 // accesses. The update is HBM-bound: per parameter Adam reads p, g, m, v and writes p, m, v
 // (28 bytes); RMSprop reads p, g, nu and writes p, nu (20 bytes).
+#include <mutex>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -14,6 +16,35 @@ namespace cb {
 constexpr int kAdamBlocks = 1024;
 
 size_t adam_partial_floats(int64_t) { return 2 * kAdamBlocks; }
+
+// Norm partials of the allocation-free optimiser entry point: one file-scope buffer per GPU
+// (each device holds its own copy until the process ends). Host code never passes the name
+// `scratch` to a kernel: on the host it is only a stand-in for the symbol, so its device
+// address is looked up per device with hipGetSymbolAddress and used instead.
+constexpr size_t kNoAllocScratchBytes = size_t(2 * kAdamBlocks) * sizeof(float);
+static __device__ __align__(256) double scratch[kNoAllocScratchBytes / sizeof(double)];
+
+size_t noalloc_scratch_bytes() { return kNoAllocScratchBytes; }
+
+hipError_t noalloc_scratch(float** out) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!ptr) return hipErrorInvalidSymbol;
+        addr[dev] = ptr;
+    }
+    *out = static_cast<float*>(addr[dev]);
+    return hipSuccess;
+}
 
 __global__ __launch_bounds__(256) void sumsq_kernel(int64_t n, const float* __restrict__ g,
                                                     double* __restrict__ part) {

@@ -411,6 +411,26 @@ impala_status_t adam_step(int64_t n_params, float* params, const float* grads, f
     return hip_status(clip_opt_step(OPT_ADAM, a, stats, static_cast<float*>(ws), stream), "adam_step");
 }
 
+impala_status_t adam_step_noalloc(int64_t n_params, float* params, const float* grads, float* m, float* v,
+                                  int32_t step, float lr, float beta1, float beta2, float eps,
+                                  float max_grad_norm, float* stats, hipStream_t stream) {
+    if (n_params < 0) return fail(IMPALA_EINVAL, "adam_step_noalloc: n_params < 0");
+    if (step < 1) return fail(IMPALA_EINVAL, "adam_step_noalloc: step is 1-based");
+    if (!(beta1 >= 0.f && beta1 < 1.f && beta2 >= 0.f && beta2 < 1.f))
+        return fail(IMPALA_EINVAL, "adam_step_noalloc: betas must be in [0, 1)");
+    if (n_params == 0) return ok();
+    CHECK_PTR(params); CHECK_PTR(grads); CHECK_PTR(m); CHECK_PTR(v);
+    const size_t need = adam_workspace_bytes(n_params);
+    if (need > noalloc_scratch_bytes())
+        return fail(IMPALA_EINVAL, "adam_step_noalloc: needs %zu bytes of scratch, the built-in buffer holds %zu",
+                    need, noalloc_scratch_bytes());
+    float* part = nullptr;
+    const hipError_t e = noalloc_scratch(&part);
+    if (e != hipSuccess) return hip_status(e, "adam_step_noalloc: scratch address");
+    const OptArgs a = adam_args(n_params, params, grads, m, v, step, lr, beta1, beta2, eps, max_grad_norm);
+    return hip_status(clip_opt_step(OPT_ADAM, a, stats, part, stream), "adam_step_noalloc");
+}
+
 size_t rmsprop_workspace_bytes(int64_t n_params) { return adam_workspace_bytes(n_params); }
 
 impala_status_t rmsprop_step(int64_t n_params, float* params, const float* grads, float* nu, float lr,

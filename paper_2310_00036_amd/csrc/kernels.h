@@ -257,6 +257,10 @@ hipError_t action_logp(int64_t m, int A, const float* z, const int32_t* act, flo
 hipError_t gumbel_max(int64_t m, int A, const float* z, const float* g, int32_t* act,
                       float* logp, hipStream_t s);
 size_t adam_partial_floats(int64_t n);
+// The allocation-free optimiser's per-device norm-partial buffer (a file-scope device array):
+// its size, and its address on the current device (looked up once per device).
+size_t noalloc_scratch_bytes();
+hipError_t noalloc_scratch(float** out);
 // omb1 = 1 - b1, omb2 = 1 - b2, bc1 = 1 - b1^t, bc2 = 1 - b2^t, all formed in double.
 enum { OPT_ADAM = 0, OPT_RMSPROP = 1 };
 // Adam: b1, b2, omb1 = 1 - b1, omb2 = 1 - b2 (formed in double), bc1 = 1 - b1^t, bc2 = 1 - b2^t.

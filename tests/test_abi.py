@@ -174,3 +174,15 @@ def test_activation_layout_is_disjoint_and_inside_the_workspace(net, prec):
     assert all(a[1] <= b[0] for a, b in zip(spans, spans[1:]))
     with pytest.raises(P.LibraryError):
         P.impala_activation_layout(net, prec, 0)
+
+
+def test_noalloc_adam_validates_before_hip():
+    """adam_step_noalloc rejects bad arguments on the host and returns OK for an empty buffer
+    before touching the GPU."""
+    lib = P.lib
+    assert lib.adam_step_noalloc(-1, 1, 1, 1, 1, 1, 1e-3, 0.9, 0.999, 1e-5, 0.5, None, None) == -1
+    assert lib.adam_step_noalloc(10, 1, 1, 1, 1, 0, 1e-3, 0.9, 0.999, 1e-5, 0.5, None, None) == -1
+    assert b"1-based" in lib.impala_last_error()
+    assert lib.adam_step_noalloc(10, 1, 1, 1, 1, 1, 1e-3, 1.0, 0.999, 1e-5, 0.5, None, None) == -1
+    assert lib.adam_step_noalloc(10, None, 1, 1, 1, 1, 1e-3, 0.9, 0.999, 1e-5, 0.5, None, None) == -1
+    assert lib.adam_step_noalloc(0, None, None, None, None, 1, 1e-3, 0.9, 0.999, 1e-5, 0.5, None, None) == 0
