@@ -531,12 +531,13 @@ def hbm_sweep(P, reps=20):
         old = torch.log_softmax(z, 1).gather(1, a.long()[:, None])[:, 0] + 0.1 * torch.randn(m, generator=g, **dev)
         dz, dv = torch.empty_like(z), torch.empty_like(v)
         st = torch.empty(8, **dev)
+        lws = torch.empty(P.loss_workspace_bytes(m), dtype=torch.uint8, **dev)
         if fam == "ppo_loss":
-            sec = timed(lambda: P.ppo_loss_grad(m, A, z, v, a, old, adv, ret, 1, 0.1, 0.5, 0.01, dz, dv, st))
+            sec = timed(lambda: P.ppo_loss_grad(m, A, z, v, a, old, adv, ret, 1, 0.1, 0.5, 0.01, dz, dv, st, lws))
         else:
-            sec = timed(lambda: P.impala_loss_grad(m, A, z, v, a, ret, adv, 1.0, 0.5, 0.01, dz, dv, st))
+            sec = timed(lambda: P.impala_loss_grad(m, A, z, v, a, ret, adv, 1.0, 0.5, 0.01, dz, dv, st, lws))
         add(fam, label, f"{m}x{A}", kernel_work(f"{fam}/{m}x{A}", 0)["bytes"], sec)
-        del z, v, ret, adv, a, old, dz, dv
+        del z, v, ret, adv, a, old, dz, dv, lws
     for n, label in ((1_094_115, "config"), (4_364_211, "config"), (1 << 26, "scaled")):
         p = torch.randn(n, generator=g, **dev)
         gr = torch.randn(n, generator=g, **dev) * 1e-3

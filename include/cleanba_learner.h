@@ -141,20 +141,26 @@ impala_status_t vtrace_targets(int32_t T, int32_t E, const float* behav_logp,
  *   L = mean(pg) + vf_coef * 0.5 mean((V - ret)^2) - ent_coef mean(entropy).
  * logits, dlogits: [m, A]; value, old_logp, adv, ret, dvalue: [m]; actions: int32 [m].
  * stats (device, float [8]): [L, policy, value, entropy, approx_kl, clipfrac, adv mean,
- * adv std]. */
+ * adv std].
+ * ws: optional device scratch of loss_workspace_bytes(m) bytes (NULL: none). With it the rows
+ * are spread over many workgroups in one pass over the logits; without it, up to 16384 rows
+ * run in one workgroup, and larger minibatches keep their partial sums in dvalue's memory
+ * and pass over the logits twice. Every output is the same bit for bit either way. */
+size_t loss_workspace_bytes(int64_t m);
 impala_status_t ppo_loss_grad(int64_t m, int32_t A, const float* logits, const float* value,
                               const int32_t* actions, const float* old_logp, const float* adv,
                               const float* ret, int32_t norm_adv, float clip_eps, float vf_coef,
-                              float ent_coef, float* dlogits, float* dvalue, float* stats,
-                              hipStream_t stream);
+                              float ent_coef, float* dlogits, float* dvalue, float* stats, void* ws,
+                              size_t ws_bytes, hipStream_t stream);
 
 /* IMPALA loss and its gradient over m rows (Appendix B's IMPALA table):
  *   L = pg_coef mean(-pg_adv log pi(a)) + vf_coef * 0.5 mean((V - vs)^2) - ent_coef mean(H).
- * Shapes as ppo_loss_grad; stats: [L, policy, value, entropy, mean pg_adv, mean vs, 0, 0]. */
+ * Shapes and ws as ppo_loss_grad; stats: [L, policy, value, entropy, mean pg_adv, mean vs, 0, 0]. */
 impala_status_t impala_loss_grad(int64_t m, int32_t A, const float* logits, const float* value,
                                  const int32_t* actions, const float* vs, const float* pg_adv,
                                  float pg_coef, float vf_coef, float ent_coef, float* dlogits,
-                                 float* dvalue, float* stats, hipStream_t stream);
+                                 float* dvalue, float* stats, void* ws, size_t ws_bytes,
+                                 hipStream_t stream);
 
 /* Global-norm clip then Adam over the flat buffers (Algorithm 1: clip the gradient norm,
  * step the optimiser; Appendix B: Adam epsilon 1e-5):

@@ -69,8 +69,9 @@ _SIGS = {
     "impala_cnn_bwd": (C.c_int, [_NETP, C.c_int, _P, _P, _P, _I64, _P, _SZ, _P, _P, _P, _P]),
     "gae_advantages": (C.c_int, [_I32, _I32, _P, _P, _P, _P, _P, _F, _F, _P, _P, _P]),
     "vtrace_targets": (C.c_int, [_I32, _I32, _P, _P, _P, _P, _P, _P, _P, _F, _F, _F, _F, _F, _P, _P, _P]),
-    "ppo_loss_grad": (C.c_int, [_I64, _I32, _P, _P, _P, _P, _P, _P, _I32, _F, _F, _F, _P, _P, _P, _P]),
-    "impala_loss_grad": (C.c_int, [_I64, _I32, _P, _P, _P, _P, _P, _F, _F, _F, _P, _P, _P, _P]),
+    "loss_workspace_bytes": (_SZ, [_I64]),
+    "ppo_loss_grad": (C.c_int, [_I64, _I32, _P, _P, _P, _P, _P, _P, _I32, _F, _F, _F, _P, _P, _P, _P, _SZ, _P]),
+    "impala_loss_grad": (C.c_int, [_I64, _I32, _P, _P, _P, _P, _P, _F, _F, _F, _P, _P, _P, _P, _SZ, _P]),
     "adam_workspace_bytes": (_SZ, [_I64]),
     "adam_step": (C.c_int, [_I64, _P, _P, _P, _P, _I32, _F, _F, _F, _F, _F, _P, _P, _SZ, _P]),
     "adam_step_noalloc": (C.c_int, [_I64, _P, _P, _P, _P, _I32, _F, _F, _F, _F, _F, _P, _P]),
@@ -227,18 +228,27 @@ def vtrace_targets(T, E, behav_logp, target_logp, rewards, values, dones, bootst
         ptr(pg_adv), stream_handle(stream)))
 
 
+def loss_workspace_bytes(m: int) -> int:
+    return int(lib.loss_workspace_bytes(m))
+
+
+def _ws_args(ws):
+    return (ptr(ws), ws.numel() * ws.element_size()) if ws is not None else (None, 0)
+
+
 def ppo_loss_grad(m, A, logits, value, actions, old_logp, adv, ret, norm_adv, clip_eps, vf_coef,
-                  ent_coef, dlogits, dvalue, stats, stream=None):
+                  ent_coef, dlogits, dvalue, stats, ws=None, stream=None):
     _check("ppo_loss_grad", lib.ppo_loss_grad(
         m, A, ptr(logits), ptr(value), ptr(actions), ptr(old_logp), ptr(adv), ptr(ret), norm_adv,
-        clip_eps, vf_coef, ent_coef, ptr(dlogits), ptr(dvalue), ptr(stats), stream_handle(stream)))
+        clip_eps, vf_coef, ent_coef, ptr(dlogits), ptr(dvalue), ptr(stats), *_ws_args(ws),
+        stream_handle(stream)))
 
 
 def impala_loss_grad(m, A, logits, value, actions, vs, pg_adv, pg_coef, vf_coef, ent_coef,
-                     dlogits, dvalue, stats, stream=None):
+                     dlogits, dvalue, stats, ws=None, stream=None):
     _check("impala_loss_grad", lib.impala_loss_grad(
         m, A, ptr(logits), ptr(value), ptr(actions), ptr(vs), ptr(pg_adv), pg_coef, vf_coef,
-        ent_coef, ptr(dlogits), ptr(dvalue), ptr(stats), stream_handle(stream)))
+        ent_coef, ptr(dlogits), ptr(dvalue), ptr(stats), *_ws_args(ws), stream_handle(stream)))
 
 
 def adam_workspace_bytes(n_params: int) -> int:

@@ -338,31 +338,41 @@ impala_status_t vtrace_targets(int32_t T, int32_t E, const float* behav_logp,
                       "vtrace_targets");
 }
 
+size_t loss_workspace_bytes(int64_t m) { return loss_ws_bytes(m > 0 ? m : 1); }
+
 impala_status_t ppo_loss_grad(int64_t m, int32_t A, const float* logits, const float* value,
                               const int32_t* actions, const float* old_logp, const float* adv,
                               const float* ret, int32_t norm_adv, float clip_eps, float vf_coef,
-                              float ent_coef, float* dlogits, float* dvalue, float* stats,
-                              hipStream_t stream) {
+                              float ent_coef, float* dlogits, float* dvalue, float* stats, void* ws,
+                              size_t ws_bytes, hipStream_t stream) {
     if (m < 1 || m > (int64_t(1) << 26)) return fail(IMPALA_EINVAL, "ppo_loss_grad: m out of range");
     if (A < 1 || A > 64) return fail(IMPALA_EINVAL, "ppo_loss_grad: A must be in [1, 64]");
     CHECK_PTR(logits); CHECK_PTR(value); CHECK_PTR(actions); CHECK_PTR(old_logp); CHECK_PTR(adv);
     CHECK_PTR(ret); CHECK_PTR(dlogits); CHECK_PTR(dvalue); CHECK_PTR(stats);
-    return hip_status(ppo_loss(m, A, logits, value, actions, old_logp, adv, ret, nullptr, norm_adv,
-                               clip_eps, vf_coef, ent_coef, dlogits, dvalue, stats, stream),
-                      "ppo_loss_grad");
+    if (ws && ws_bytes < loss_ws_bytes(m))
+        return fail(IMPALA_EWORKSPACE, "ppo_loss_grad: workspace %zu < %zu bytes", ws_bytes, loss_ws_bytes(m));
+    const hipError_t e = ws ? ppo_loss_ws(m, A, logits, value, actions, old_logp, adv, ret, nullptr, norm_adv,
+                                          clip_eps, vf_coef, ent_coef, dlogits, dvalue, stats, ws, stream)
+                            : ppo_loss(m, A, logits, value, actions, old_logp, adv, ret, nullptr, norm_adv,
+                                       clip_eps, vf_coef, ent_coef, dlogits, dvalue, stats, stream);
+    return hip_status(e, "ppo_loss_grad");
 }
 
 impala_status_t impala_loss_grad(int64_t m, int32_t A, const float* logits, const float* value,
                                  const int32_t* actions, const float* vs, const float* pg_adv,
                                  float pg_coef, float vf_coef, float ent_coef, float* dlogits,
-                                 float* dvalue, float* stats, hipStream_t stream) {
+                                 float* dvalue, float* stats, void* ws, size_t ws_bytes, hipStream_t stream) {
     if (m < 1 || m > (int64_t(1) << 26)) return fail(IMPALA_EINVAL, "impala_loss_grad: m out of range");
     if (A < 1 || A > 64) return fail(IMPALA_EINVAL, "impala_loss_grad: A must be in [1, 64]");
     CHECK_PTR(logits); CHECK_PTR(value); CHECK_PTR(actions); CHECK_PTR(vs); CHECK_PTR(pg_adv);
     CHECK_PTR(dlogits); CHECK_PTR(dvalue); CHECK_PTR(stats);
-    return hip_status(impala_loss(m, A, logits, value, actions, vs, pg_adv, pg_coef, vf_coef, ent_coef,
-                                  dlogits, dvalue, stats, stream),
-                      "impala_loss_grad");
+    if (ws && ws_bytes < loss_ws_bytes(m))
+        return fail(IMPALA_EWORKSPACE, "impala_loss_grad: workspace %zu < %zu bytes", ws_bytes, loss_ws_bytes(m));
+    const hipError_t e = ws ? impala_loss_ws(m, A, logits, value, actions, vs, pg_adv, pg_coef, vf_coef, ent_coef,
+                                             dlogits, dvalue, stats, ws, stream)
+                            : impala_loss(m, A, logits, value, actions, vs, pg_adv, pg_coef, vf_coef, ent_coef,
+                                          dlogits, dvalue, stats, stream);
+    return hip_status(e, "impala_loss_grad");
 }
 
 namespace {

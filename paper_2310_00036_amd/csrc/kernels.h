@@ -227,7 +227,9 @@ hipError_t vtrace(int T, int E, const float* mu, const float* pi, const float* r
                   const uint8_t* d, const float* bv, const uint8_t* nd, float gamma, float lam,
                   float rho_bar, float c_bar, float pg_rho_bar, float* vs, float* pg,
                   hipStream_t s);
-// stats [8] doubles as the advantage-statistics scratch (entries 6, 7) of ppo_loss.
+// Losses without a workspace. stats [8] holds the advantage statistics (entries 6, 7) between
+// launches; above 16384 rows dv holds the per-workgroup partial sums until the gradients are
+// written there.
 hipError_t ppo_loss(int64_t m, int A, const float* z, const float* v, const int32_t* act,
                     const float* old_logp, const float* adv, const float* ret,
                     const int32_t* rows, int norm_adv, float clip, float vf, float ent,
@@ -236,7 +238,8 @@ hipError_t impala_loss(int64_t m, int A, const float* z, const float* v, const i
                        const float* vs, const float* pg, float pgc, float vf, float ent,
                        float* dz, float* dv, float* stats, hipStream_t s);
 // The same results (bit-identical) over many workgroups, for callers with a workspace of
-// loss_ws_bytes(m) bytes (the advantage statistics and the per-row loss terms).
+// loss_ws_bytes(m) bytes (the advantage statistics and the per-row loss terms, or above 16384
+// rows the per-workgroup partial sums).
 size_t loss_ws_bytes(int64_t m);
 hipError_t ppo_loss_ws(int64_t m, int A, const float* z, const float* v, const int32_t* act,
                        const float* old_logp, const float* adv, const float* ret, const int32_t* rows,

@@ -1,13 +1,12 @@
 // Fused policy / value / entropy losses and their logit and value gradients, one thread per
 // minibatch row (A <= 64 logits per row), plus the actor's Gumbel-max sampler.
 //
-// Minibatches up to kFusedRows rows run as one single-workgroup launch. Larger ones run
-// PPO as three launches: (1) one block computes the minibatch advantage mean and
-// population std (float64 sums) into the caller's stats vector, (2) one thread per row
-// computes log-softmax, ratio, clipped surrogate, entropy and value terms and writes
-// dlogits / dvalue, (3) one block re-derives the row terms and sums them (float64, fixed
-// order) into the stats vector. No scratch memory is needed and every reduction has a
-// fixed order, so results are bit-reproducible.
+// Minibatches up to kFusedRows rows run as one single-workgroup launch (advantage
+// statistics, row gradients and loss statistics); callers with a workspace (the learner
+// step) spread the row work of such minibatches over many workgroups with results bit-
+// identical to the single launch. Larger minibatches reduce over workgroups: per-workgroup
+// partial sums in a fixed order, then one workgroup adds them in a fixed order. Every sum is
+// float64 and every reduction order is fixed, so results are bit-reproducible.
 #include "common.h"
 #include "kernels.h"
 
@@ -15,30 +14,7 @@
 
 namespace cb {
 
-constexpr int kLossRows = 256;   // rows per block in the gradient kernels
 constexpr int kStatThreads = 1024;
-
-// ---- (1) advantage statistics over the minibatch (single block, fixed order), written to
-//          stats[6] (mean) and stats[7] (population std)
-__global__ __launch_bounds__(256) void adv_stats_kernel(int64_t m, const float* __restrict__ adv,
-                                                        const int32_t* __restrict__ rows,
-                                                        float* __restrict__ stats) {
-    __shared__ double sh[256];
-    double s = 0.0, s2 = 0.0;
-    for (int64_t i = threadIdx.x; i < m; i += 256) {
-        const double a = adv[rows ? rows[i] : i];
-        s += a;
-        s2 += a * a;
-    }
-    const double tot = block_sum<256>(s, sh);
-    const double tot2 = block_sum<256>(s2, sh);
-    if (threadIdx.x == 0) {
-        const double mean = tot / double(m);
-        const double var = tot2 / double(m) - mean * mean;
-        stats[6] = float(mean);
-        stats[7] = float(sqrt(var > 0.0 ? var : 0.0));
-    }
-}
 
 // Log-softmax of one row, kept as (zmax, lse): log pi_j = (z_j - zmax) - lse, recomputed from
 // the logits where needed (no per-row array, so nothing spills to scratch). Also the entropy.
@@ -86,117 +62,6 @@ CB_DEV PpoRow ppo_row_v(const float* zr, int A, int a, float old_logp, float adv
     r.pg = fmaxf(pg1, pg2);
     r.kappa = pg2 > pg1 ? 0.f : 1.f;   // clipped branch strictly larger: no ratio gradient
     return r;
-}
-
-CB_DEV PpoRow ppo_row(const float* zr, int64_t src, int A, const int32_t* act,
-                      const float* old_logp, const float* adv, int norm_adv, float clip,
-                      float mean, float std) {
-    return ppo_row_v(zr, A, act[src], old_logp[src], adv[src], norm_adv, clip, mean, std);
-}
-
-// ---- (2) per-row PPO gradients
-__global__ __launch_bounds__(kLossRows) void ppo_rows_kernel(
-    int64_t m, int A, const float* __restrict__ z, const float* __restrict__ val,
-    const int32_t* __restrict__ act, const float* __restrict__ old_logp,
-    const float* __restrict__ adv, const float* __restrict__ ret, const int32_t* __restrict__ rows,
-    int norm_adv, float clip, float vf, float ent, float* __restrict__ dz, float* __restrict__ dv,
-    const float* __restrict__ stats) {
-    const int64_t i = int64_t(blockIdx.x) * kLossRows + threadIdx.x;
-    if (i >= m) return;
-    const int64_t src = rows ? rows[i] : i;
-    const PpoRow r = ppo_row(z + i * A, src, A, act, old_logp, adv, norm_adv, clip, stats[6], stats[7]);
-    const float inv_m = 1.f / float(m);
-    const float coef = -r.kappa * r.A_hat * r.ratio;
-    const float* zr = z + i * A;
-    for (int j = 0; j < A; ++j) {
-        const float l = r.s.l(zr[j]);
-        const float p = expf(l);
-        dz[i * A + j] = (coef * ((j == r.a ? 1.f : 0.f) - p) + ent * p * (l + r.H)) * inv_m;
-    }
-    dv[i] = vf * (val[i] - ret[src]) * inv_m;
-}
-
-// ---- (3) PPO stats: one block re-derives the row terms and sums them in a fixed order
-__global__ __launch_bounds__(kStatThreads) void ppo_stats_kernel(
-    int64_t m, int A, const float* __restrict__ z, const float* __restrict__ val,
-    const int32_t* __restrict__ act, const float* __restrict__ old_logp,
-    const float* __restrict__ adv, const float* __restrict__ ret, const int32_t* __restrict__ rows,
-    int norm_adv, float clip, float vf, float ent, float* __restrict__ stats) {
-    __shared__ double sh[kStatThreads];
-    const float mean = stats[6], std = stats[7];
-    double st[5] = {0, 0, 0, 0, 0};
-    for (int64_t i = threadIdx.x; i < m; i += kStatThreads) {
-        const int64_t src = rows ? rows[i] : i;
-        const PpoRow r = ppo_row(z + i * A, src, A, act, old_logp, adv, norm_adv, clip, mean, std);
-        const double dvl = double(val[i]) - double(ret[src]);
-        st[0] += r.pg;
-        st[1] += dvl * dvl;
-        st[2] += r.H;
-        st[3] += double(r.ratio - 1.f) - double(logf(r.ratio));
-        st[4] += fabsf(r.ratio - 1.f) > clip ? 1.0 : 0.0;
-    }
-    double tot[5];
-    for (int k = 0; k < 5; ++k) tot[k] = block_sum<kStatThreads>(st[k], sh);
-    if (threadIdx.x == 0) {
-        const double inv = 1.0 / double(m);
-        const double pg = tot[0] * inv, vl = 0.5 * tot[1] * inv, H = tot[2] * inv;
-        stats[0] = float(pg + vf * vl - ent * H);
-        stats[1] = float(pg); stats[2] = float(vl); stats[3] = float(H);
-        stats[4] = float(tot[3] * inv); stats[5] = float(tot[4] * inv);
-    }
-}
-
-// ---- IMPALA: per-row gradients, then one stats block
-__global__ __launch_bounds__(kLossRows) void impala_rows_kernel(
-    int64_t m, int A, const float* __restrict__ z, const float* __restrict__ val,
-    const int32_t* __restrict__ act, const float* __restrict__ vs, const float* __restrict__ pgadv,
-    float pgc, float vf, float ent, float* __restrict__ dz, float* __restrict__ dv) {
-    const int64_t i = int64_t(blockIdx.x) * kLossRows + threadIdx.x;
-    if (i >= m) return;
-    const float* zr = z + i * A;
-    const RowLsm rs = row_log_softmax(zr, A);
-    const float H = rs.H;
-    const int a = act[i];
-    const float adv = pgadv[i];
-    const float inv_m = 1.f / float(m);
-    const bool a_ok = a >= 0 && a < A;
-    for (int j = 0; j < A; ++j) {
-        const float l = rs.l(zr[j]);
-        const float p = expf(l);
-        dz[i * A + j] = a_ok ? (-pgc * adv * ((j == a ? 1.f : 0.f) - p) + ent * p * (l + H)) * inv_m
-                             : __builtin_nanf("");
-    }
-    dv[i] = vf * (val[i] - vs[i]) * inv_m;
-}
-
-__global__ __launch_bounds__(kStatThreads) void impala_stats_kernel(
-    int64_t m, int A, const float* __restrict__ z, const float* __restrict__ val,
-    const int32_t* __restrict__ act, const float* __restrict__ vs, const float* __restrict__ pgadv,
-    float pgc, float vf, float ent, float* __restrict__ stats) {
-    __shared__ double sh[kStatThreads];
-    double st[5] = {0, 0, 0, 0, 0};
-    for (int64_t i = threadIdx.x; i < m; i += kStatThreads) {
-        const float* zr = z + i * A;
-        const RowLsm rs = row_log_softmax(zr, A);
-        const float H = rs.H;
-        const double dvl = double(val[i]) - double(vs[i]);
-        const int a = act[i];
-        st[0] += -double(pgadv[i]) * ((a >= 0 && a < A) ? double(rs.l(zr[a])) : double(__builtin_nanf("")));
-        st[1] += dvl * dvl;
-        st[2] += H;
-        st[3] += pgadv[i];
-        st[4] += vs[i];
-    }
-    double tot[5];
-    for (int k = 0; k < 5; ++k) tot[k] = block_sum<kStatThreads>(st[k], sh);
-    if (threadIdx.x == 0) {
-        const double inv = 1.0 / double(m);
-        const double pg = tot[0] * inv, vl = 0.5 * tot[1] * inv, H = tot[2] * inv;
-        stats[0] = float(pgc * pg + vf * vl - ent * H);
-        stats[1] = float(pg); stats[2] = float(vl); stats[3] = float(H);
-        stats[4] = float(tot[3] * inv); stats[5] = float(tot[4] * inv);
-        stats[6] = 0.f; stats[7] = 0.f;
-    }
 }
 
 // ---- single-workgroup variants for minibatches up to kFusedRows rows: the advantage
@@ -637,6 +502,231 @@ __global__ __launch_bounds__(kFusedThreads) void loss_final_ws_kernel(int64_t m,
     }
 }
 
+// ---- minibatches beyond kFusedRows rows: every reduction over workgroups. Each workgroup
+// (kWideRows rows, one per thread) reduces its rows' advantage sums or loss terms in a fixed
+// order into one partial; a single workgroup then adds the partials in a fixed order. The
+// partials live in the caller's workspace when there is one; without it they live in dvalue
+// before the gradients are written there (its m floats hold the 5 doubles per 256 rows).
+// With a workspace the row kernel forms the gradients and the loss partials in one pass over
+// the logits; without it a first pass forms the partials and a second one the gradients.
+template <bool ROWS>
+__global__ __launch_bounds__(kWideRows) void adv_part_kernel(int64_t m, const float* __restrict__ adv,
+                                                           const int32_t* __restrict__ rows,
+                                                           double* __restrict__ part) {
+    __shared__ double sh[kWideRows];
+    const int64_t i = int64_t(blockIdx.x) * kWideRows + threadIdx.x;
+    const double a = i < m ? double(adv[ppo_src<ROWS>(i, m, rows)]) : 0.0;
+    const double s = block_sum<kWideRows>(a, sh);
+    const double s2 = block_sum<kWideRows>(a * a, sh);
+    if (threadIdx.x == 0) {
+        part[2 * blockIdx.x] = s;
+        part[2 * blockIdx.x + 1] = s2;
+    }
+}
+
+// One workgroup adds nb partials of K doubles (thread t: partials t, t + kStatThreads, ...;
+// then a fixed tree) and writes the statistics. KIND 0: advantage mean and population std
+// into stats[6], stats[7]; 1: PPO loss statistics into stats[0..5]; 2: IMPALA's into
+// stats[0..7].
+template <int K, int KIND>
+__global__ __launch_bounds__(kStatThreads) void part_final_kernel(int64_t m, int nb, float pgc, float vf,
+                                                                  float ent, const double* __restrict__ part,
+                                                                  float* __restrict__ stats) {
+    __shared__ double sh[kStatThreads];
+    double st[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) st[k] = 0.0;
+    for (int b = threadIdx.x; b < nb; b += kStatThreads)
+#pragma unroll
+        for (int k = 0; k < K; ++k) st[k] += part[int64_t(b) * K + k];
+    double tot[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) tot[k] = block_sum<kStatThreads>(st[k], sh);
+    if (threadIdx.x != 0) return;
+    const double inv = 1.0 / double(m);
+    if constexpr (KIND == 0) {
+        const double mean = tot[0] * inv, var = tot[1] * inv - mean * mean;
+        stats[6] = float(mean);
+        stats[7] = float(sqrt(var > 0.0 ? var : 0.0));
+    } else {
+        const double pg = tot[0] * inv, vl = 0.5 * tot[1] * inv, H = tot[2] * inv;
+        stats[0] = float(KIND == 1 ? pg + vf * vl - ent * H : pgc * pg + vf * vl - ent * H);
+        stats[1] = float(pg); stats[2] = float(vl); stats[3] = float(H);
+        stats[4] = float(tot[3] * inv); stats[5] = float(tot[4] * inv);
+        if constexpr (KIND == 2) { stats[6] = 0.f; stats[7] = 0.f; }
+    }
+}
+
+// This workgroup's five loss terms, reduced in a fixed order into part[5 * blockIdx.x ..].
+CB_DEV void block_terms(const double (&t)[5], double* sh, double* __restrict__ part) {
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+        const double s = block_sum<kWideRows>(t[k], sh);
+        if (threadIdx.x == 0) part[5 * int64_t(blockIdx.x) + k] = s;
+    }
+}
+
+// PPO rows of a large minibatch: GRAD writes dlogits / dvalue, PART the loss partials; the
+// advantage statistics come from stats[6], stats[7].
+template <int AC, bool ROWS, bool GRAD, bool PART>
+__global__ __launch_bounds__(kWideRows) void ppo_big_rows_kernel(
+    int64_t m, int A_, const float* __restrict__ z, const float* __restrict__ val,
+    const int32_t* __restrict__ act, const float* __restrict__ old_logp,
+    const float* __restrict__ adv, const float* __restrict__ ret, const int32_t* __restrict__ rows,
+    int norm_adv, float clip, float vf, float ent, float* __restrict__ dz, float* __restrict__ dv,
+    const float* __restrict__ stats, double* __restrict__ part) {
+    extern __shared__ float zs[];   // [kWideRows][A]
+    __shared__ double sh[kWideRows];
+    const int A = AC > 0 ? AC : A_;
+    const int tid = threadIdx.x;
+    const int64_t r0 = int64_t(blockIdx.x) * kWideRows;
+    const int nr = m - r0 < kWideRows ? int(m - r0) : kWideRows;
+    const int64_t src = ppo_src<ROWS>(r0 + tid, m, rows);
+    stage_rows<AC>(zs, z, r0, nr, A);
+    const PpoScal cur = ppo_scal(r0 + tid, m, src, act, old_logp, adv, ret, val);
+    const float mean = stats[6], std = stats[7];
+    const float inv_m = 1.f / float(m);
+    __syncthreads();
+    double t[5] = {0, 0, 0, 0, 0};
+    if (tid < nr) {
+        const int64_t i = r0 + tid;
+        float* zr = zs + tid * A;
+        const PpoRow r = ppo_row_v(zr, A, cur.a, cur.olp, cur.adv, norm_adv, clip, mean, std);
+        if constexpr (GRAD) {
+            const float coef = -r.kappa * r.A_hat * r.ratio;
+            for (int j = 0; j < A; ++j) {
+                const float l = r.s.l(zr[j]);
+                const float p = expf(l);
+                zr[j] = (coef * ((j == r.a ? 1.f : 0.f) - p) + ent * p * (l + r.H)) * inv_m;
+            }
+            dv[i] = vf * (cur.val - cur.ret) * inv_m;
+        }
+        const double dvl = double(cur.val) - double(cur.ret);
+        t[0] = r.pg;
+        t[1] = dvl * dvl;
+        t[2] = r.H;
+        t[3] = double(r.ratio - 1.f) - double(logf(r.ratio));
+        t[4] = fabsf(r.ratio - 1.f) > clip ? 1.0 : 0.0;
+    }
+    if constexpr (PART) block_terms(t, sh, part);
+    if constexpr (GRAD) {
+        __syncthreads();
+        for (int e = tid; e < nr * A; e += kWideRows) dz[r0 * A + e] = zs[e];
+    }
+}
+
+template <int AC, bool GRAD, bool PART>
+__global__ __launch_bounds__(kWideRows) void impala_big_rows_kernel(
+    int64_t m, int A_, const float* __restrict__ z, const float* __restrict__ val,
+    const int32_t* __restrict__ act, const float* __restrict__ vs, const float* __restrict__ pgadv,
+    float pgc, float vf, float ent, float* __restrict__ dz, float* __restrict__ dv, double* __restrict__ part) {
+    extern __shared__ float zs[];   // [kWideRows][A]
+    __shared__ double sh[kWideRows];
+    const int A = AC > 0 ? AC : A_;
+    const int tid = threadIdx.x;
+    const int64_t r0 = int64_t(blockIdx.x) * kWideRows;
+    const int nr = m - r0 < kWideRows ? int(m - r0) : kWideRows;
+    stage_rows<AC>(zs, z, r0, nr, A);
+    const ImpScal cur = imp_scal(r0 + tid, m, act, pgadv, val, vs);
+    const float inv_m = 1.f / float(m);
+    __syncthreads();
+    double t[5] = {0, 0, 0, 0, 0};
+    if (tid < nr) {
+        const int64_t i = r0 + tid;
+        float* zr = zs + tid * A;
+        const RowLsm rs = row_log_softmax(zr, A);
+        const int a = cur.a;
+        const bool a_ok = a >= 0 && a < A;
+        const double la = a_ok ? double(rs.l(zr[a])) : double(__builtin_nanf(""));
+        if constexpr (GRAD) {
+            for (int j = 0; j < A; ++j) {
+                const float l = rs.l(zr[j]);
+                const float p = expf(l);
+                zr[j] = a_ok ? (-pgc * cur.adv * ((j == a ? 1.f : 0.f) - p) + ent * p * (l + rs.H)) * inv_m
+                             : __builtin_nanf("");
+            }
+            dv[i] = vf * (cur.val - cur.vs) * inv_m;
+        }
+        const double dvl = double(cur.val) - double(cur.vs);
+        t[0] = -double(cur.adv) * la;
+        t[1] = dvl * dvl;
+        t[2] = rs.H;
+        t[3] = cur.adv;
+        t[4] = cur.vs;
+    }
+    if constexpr (PART) block_terms(t, sh, part);
+    if constexpr (GRAD) {
+        __syncthreads();
+        for (int e = tid; e < nr * A; e += kWideRows) dz[r0 * A + e] = zs[e];
+    }
+}
+
+// The partial buffer: the workspace's, else dvalue's memory (8-byte aligned within it).
+static double* big_part(void* ws, float* dv) {
+    if (ws) return reinterpret_cast<double*>(static_cast<char*>(ws) + 256);
+    const uintptr_t p = reinterpret_cast<uintptr_t>(dv);
+    return reinterpret_cast<double*>(p & 7 ? p + 4 : p);
+}
+
+static hipError_t ppo_loss_big(int64_t m, int A, const float* z, const float* v, const int32_t* act,
+                               const float* old_logp, const float* adv, const float* ret, const int32_t* rows,
+                               int norm_adv, float clip, float vf, float ent, float* dz, float* dv, float* stats,
+                               void* ws, hipStream_t s) {
+    const int nb = int((m + kWideRows - 1) / kWideRows);
+    const size_t lds = size_t(kWideRows) * A * sizeof(float);
+    double* part = big_part(ws, dv);
+    if (rows) hipLaunchKernelGGL(adv_part_kernel<true>, dim3(nb), dim3(kWideRows), 0, s, m, adv, rows, part);
+    else hipLaunchKernelGGL(adv_part_kernel<false>, dim3(nb), dim3(kWideRows), 0, s, m, adv, rows, part);
+    hipLaunchKernelGGL((part_final_kernel<2, 0>), dim3(1), dim3(kStatThreads), 0, s, m, nb, 0.f, vf, ent, part, stats);
+#define CB_PB(AC, RW, GR, PT) \
+    hipLaunchKernelGGL((ppo_big_rows_kernel<AC, RW, GR, PT>), dim3(nb), dim3(kWideRows), lds, s, m, A, z, v, act, \
+                       old_logp, adv, ret, rows, norm_adv, clip, vf, ent, dz, dv, stats, part)
+#define CB_PBA(RW, GR, PT) \
+    if (A == 18) CB_PB(18, RW, GR, PT); else if (A == 6) CB_PB(6, RW, GR, PT); else CB_PB(0, RW, GR, PT)
+#define CB_PBR(GR, PT) \
+    if (rows) { CB_PBA(true, GR, PT); } else { CB_PBA(false, GR, PT); }
+    if (ws) {
+        CB_PBR(true, true);
+        hipLaunchKernelGGL((part_final_kernel<5, 1>), dim3(1), dim3(kStatThreads), 0, s, m, nb, 0.f, vf, ent, part,
+                           stats);
+    } else {
+        CB_PBR(false, true);
+        hipLaunchKernelGGL((part_final_kernel<5, 1>), dim3(1), dim3(kStatThreads), 0, s, m, nb, 0.f, vf, ent, part,
+                           stats);
+        CB_PBR(true, false);
+    }
+#undef CB_PBR
+#undef CB_PBA
+#undef CB_PB
+    return hipGetLastError();
+}
+
+static hipError_t impala_loss_big(int64_t m, int A, const float* z, const float* v, const int32_t* act,
+                                  const float* vs, const float* pg, float pgc, float vf, float ent, float* dz,
+                                  float* dv, float* stats, void* ws, hipStream_t s) {
+    const int nb = int((m + kWideRows - 1) / kWideRows);
+    const size_t lds = size_t(kWideRows) * A * sizeof(float);
+    double* part = big_part(ws, dv);
+#define CB_IB(AC, GR, PT) \
+    hipLaunchKernelGGL((impala_big_rows_kernel<AC, GR, PT>), dim3(nb), dim3(kWideRows), lds, s, m, A, z, v, act, vs, \
+                       pg, pgc, vf, ent, dz, dv, part)
+#define CB_IBA(GR, PT) \
+    if (A == 18) CB_IB(18, GR, PT); else if (A == 6) CB_IB(6, GR, PT); else CB_IB(0, GR, PT)
+    if (ws) {
+        CB_IBA(true, true);
+        hipLaunchKernelGGL((part_final_kernel<5, 2>), dim3(1), dim3(kStatThreads), 0, s, m, nb, pgc, vf, ent, part,
+                           stats);
+    } else {
+        CB_IBA(false, true);
+        hipLaunchKernelGGL((part_final_kernel<5, 2>), dim3(1), dim3(kStatThreads), 0, s, m, nb, pgc, vf, ent, part,
+                           stats);
+        CB_IBA(true, false);
+    }
+#undef CB_IBA
+#undef CB_IB
+    return hipGetLastError();
+}
+
 static size_t fused_lds(int A) {
     const int cr = std::min(kFusedThreads * 64 / A, kFusedThreads);
     return size_t(cr) * A * sizeof(float);
@@ -647,7 +737,6 @@ hipError_t ppo_loss(int64_t m, int A, const float* z, const float* v, const int3
                     int norm_adv, float clip, float vf, float ent, float* dz, float* dv, float* stats,
                     hipStream_t s) {
     if (m <= 0) return hipSuccess;
-    const int nb = int((m + kLossRows - 1) / kLossRows);
     ProfScope ps(s, [&] { return "ppo_loss/" + cb_dims(int(m), A); });
     if (m <= kFusedRows) {
         auto k = rows ? (A == 18 ? ppo_fused_kernel<18, true> : (A == 6 ? ppo_fused_kernel<6, true> : ppo_fused_kernel<0, true>))
@@ -657,19 +746,14 @@ hipError_t ppo_loss(int64_t m, int A, const float* z, const float* v, const int3
                            norm_adv, clip, vf, ent, dz, dv, stats);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL(adv_stats_kernel, dim3(1), dim3(256), 0, s, m, adv, rows, stats);
-    hipLaunchKernelGGL(ppo_rows_kernel, dim3(nb), dim3(kLossRows), 0, s, m, A, z, v, act, old_logp,
-                       adv, ret, rows, norm_adv, clip, vf, ent, dz, dv, stats);
-    hipLaunchKernelGGL(ppo_stats_kernel, dim3(1), dim3(kStatThreads), 0, s, m, A, z, v, act, old_logp,
-                       adv, ret, rows, norm_adv, clip, vf, ent, stats);
-    return hipGetLastError();
+    return ppo_loss_big(m, A, z, v, act, old_logp, adv, ret, rows, norm_adv, clip, vf, ent, dz, dv, stats, nullptr,
+                        s);
 }
 
 hipError_t impala_loss(int64_t m, int A, const float* z, const float* v, const int32_t* act,
                        const float* vs, const float* pg, float pgc, float vf, float ent, float* dz,
                        float* dv, float* stats, hipStream_t s) {
     if (m <= 0) return hipSuccess;
-    const int nb = int((m + kLossRows - 1) / kLossRows);
     ProfScope ps(s, [&] { return "impala_loss/" + cb_dims(int(m), A); });
     if (m <= kFusedRows) {
         auto k = A == 18 ? impala_fused_kernel<18> : (A == 6 ? impala_fused_kernel<6> : impala_fused_kernel<0>);
@@ -677,11 +761,7 @@ hipError_t impala_loss(int64_t m, int A, const float* z, const float* v, const i
                            dv, stats);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL(impala_rows_kernel, dim3(nb), dim3(kLossRows), 0, s, m, A, z, v, act, vs, pg,
-                       pgc, vf, ent, dz, dv);
-    hipLaunchKernelGGL(impala_stats_kernel, dim3(1), dim3(kStatThreads), 0, s, m, A, z, v, act, vs, pg,
-                       pgc, vf, ent, stats);
-    return hipGetLastError();
+    return impala_loss_big(m, A, z, v, act, vs, pg, pgc, vf, ent, dz, dv, stats, nullptr, s);
 }
 
 hipError_t ppo_loss_ws(int64_t m, int A, const float* z, const float* v, const int32_t* act,
@@ -689,8 +769,12 @@ hipError_t ppo_loss_ws(int64_t m, int A, const float* z, const float* v, const i
                        int norm_adv, float clip, float vf, float ent, float* dz, float* dv, float* stats,
                        void* ws, hipStream_t s) {
     if (m <= 0) return hipSuccess;
-    if (m <= kWideRows || m > kFusedRows)   // one workgroup's worth, or beyond the fused order
+    if (m <= kWideRows)   // one workgroup's worth
         return ppo_loss(m, A, z, v, act, old_logp, adv, ret, rows, norm_adv, clip, vf, ent, dz, dv, stats, s);
+    if (m > kFusedRows) {
+        ProfScope ps(s, [&] { return "ppo_loss/" + cb_dims(int(m), A); });
+        return ppo_loss_big(m, A, z, v, act, old_logp, adv, ret, rows, norm_adv, clip, vf, ent, dz, dv, stats, ws, s);
+    }
     float* ms = static_cast<float*>(ws);
     double* terms = reinterpret_cast<double*>(static_cast<char*>(ws) + 256);
     const int nb = int((m + kWideRows - 1) / kWideRows);
@@ -716,8 +800,12 @@ hipError_t impala_loss_ws(int64_t m, int A, const float* z, const float* v, cons
                           const float* vs, const float* pg, float pgc, float vf, float ent, float* dz,
                           float* dv, float* stats, void* ws, hipStream_t s) {
     if (m <= 0) return hipSuccess;
-    if (m <= kWideRows || m > kFusedRows)
+    if (m <= kWideRows)
         return impala_loss(m, A, z, v, act, vs, pg, pgc, vf, ent, dz, dv, stats, s);
+    if (m > kFusedRows) {
+        ProfScope ps(s, [&] { return "impala_loss/" + cb_dims(int(m), A); });
+        return impala_loss_big(m, A, z, v, act, vs, pg, pgc, vf, ent, dz, dv, stats, ws, s);
+    }
     float* ms = static_cast<float*>(ws);
     double* terms = reinterpret_cast<double*>(static_cast<char*>(ws) + 256);
     const int nb = int((m + kWideRows - 1) / kWideRows);

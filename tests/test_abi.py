@@ -74,9 +74,13 @@ def test_null_pointers_and_small_workspace_fail_before_hip():
     assert lib.gae_advantages(-1, 4, 1, 1, 1, 1, 1, 0.99, 0.95, 1, 1, None) == -1
     assert lib.gae_advantages(8, 4, None, 1, 1, 1, 1, 0.99, 0.95, 1, 1, None) == -1
     assert lib.vtrace_targets(8, 4, 1, 1, 1, 1, 1, 1, None, .99, 1, 1, 1, 1, 1, 1, None) == -1
-    assert lib.ppo_loss_grad(16, 0, 1, 1, 1, 1, 1, 1, 1, .1, .5, .01, 1, 1, 1, None) == -1
-    assert lib.ppo_loss_grad(16, 65, 1, 1, 1, 1, 1, 1, 1, .1, .5, .01, 1, 1, 1, None) == -1
-    assert lib.impala_loss_grad(0, 6, 1, 1, 1, 1, 1, 1., .5, .01, 1, 1, 1, None) == -1
+    assert lib.ppo_loss_grad(16, 0, 1, 1, 1, 1, 1, 1, 1, .1, .5, .01, 1, 1, 1, None, 0, None) == -1
+    assert lib.ppo_loss_grad(16, 65, 1, 1, 1, 1, 1, 1, 1, .1, .5, .01, 1, 1, 1, None, 0, None) == -1
+    assert lib.impala_loss_grad(0, 6, 1, 1, 1, 1, 1, 1., .5, .01, 1, 1, 1, None, 0, None) == -1
+    need = lib.loss_workspace_bytes(4096)
+    assert need >= 4096 * 40
+    assert lib.ppo_loss_grad(4096, 18, 1, 1, 1, 1, 1, 1, 1, .1, .5, .01, 1, 1, 1, 1, need - 1, None) == -2
+    assert lib.impala_loss_grad(4096, 18, 1, 1, 1, 1, 1, 1., .5, .01, 1, 1, 1, 1, need - 1, None) == -2
     # adam
     assert lib.adam_step(10, 1, 1, 1, 1, 0, 1e-3, .9, .999, 1e-5, .5, None, 1, 1 << 20, None) == -1
     assert lib.adam_step(10, 1, 1, 1, 1, 1, 1e-3, 1.0, .999, 1e-5, .5, None, 1, 1 << 20, None) == -1

@@ -589,34 +589,50 @@ def _loss_batch(m, A, seed):
                 pg=rng.standard_normal(m).astype(np.float32))
 
 
-@pytest.mark.parametrize("m,A,norm", [(2048, 18, 1), (32, 6, 1), (8192, 18, 1), (1000, 7, 0), (1, 18, 0)])
+@pytest.mark.parametrize("m,A,norm", [(2048, 18, 1), (32, 6, 1), (8192, 18, 1), (1000, 7, 0), (1, 18, 0),
+                                      (16385, 18, 1), (70001, 7, 1), (262144, 18, 1), (40000, 6, 0)])
 def test_ppo_loss_matches_oracle(m, A, norm):
+    """Against the oracle without a workspace; with one, the same outputs bit for bit."""
     b = _loss_batch(m, A, m + A)
     L, dz_w, dv_w, st_w = olosses.ppo_loss_grad(b["z"], b["v"], b["a"], b["old"], b["adv"], b["ret"],
                                                 0.1, 0.5, 0.01, bool(norm))
-    dz, dv, st = G.dev_f32(np.zeros((m, A))), G.dev_f32(np.zeros(m)), G.dev_f32(np.zeros(8))
-    P.ppo_loss_grad(m, A, G.dev_f32(b["z"]), G.dev_f32(b["v"]), G.dev_i32(b["a"]), G.dev_f32(b["old"]),
-                    G.dev_f32(b["adv"]), G.dev_f32(b["ret"]), norm, 0.1, 0.5, 0.01, dz, dv, st)
-    G.sync()
+    outs = []
+    for ws in (None, G.ws_bytes(P.loss_workspace_bytes(m))):
+        dz, dv, st = G.dev_f32(np.zeros((m, A))), G.dev_f32(np.zeros(m)), G.dev_f32(np.zeros(8))
+        P.ppo_loss_grad(m, A, G.dev_f32(b["z"]), G.dev_f32(b["v"]), G.dev_i32(b["a"]), G.dev_f32(b["old"]),
+                        G.dev_f32(b["adv"]), G.dev_f32(b["ret"]), norm, 0.1, 0.5, 0.01, dz, dv, st, ws)
+        G.sync()
+        outs.append((dz, dv, st))
+    dz, dv, st = outs[0]
     G.assert_close(G.host(dz), dz_w, 1e-5, "dlogits")
     G.assert_close(G.host(dv), dv_w, 1e-5, "dvalue")
     got = G.host(st)
     idx = [0, 1, 2, 3, 4, 6, 7] if m > 1 else [0, 1, 2, 3, 4, 6]
     G.assert_close(got[idx], st_w[idx], 1e-5, "stats")
     assert abs(got[5] - st_w[5]) <= 1.0 / m   # clip fraction: a count over rows
+    torch = G.torch()
+    assert all(torch.equal(x, y) for x, y in zip(outs[0], outs[1]))
 
 
-@pytest.mark.parametrize("m,A", [(1280, 18), (37, 6), (4096, 64)])
+@pytest.mark.parametrize("m,A", [(1280, 18), (37, 6), (4096, 64), (16385, 18), (50001, 6), (262144, 18),
+                                 (20000, 64)])
 def test_impala_loss_matches_oracle(m, A):
+    """Against the oracle without a workspace; with one, the same outputs bit for bit."""
     b = _loss_batch(m, A, 3 * m + A)
     L, dz_w, dv_w, st_w = olosses.impala_loss_grad(b["z"], b["v"], b["a"], b["vs"], b["pg"], 1.0, 0.5, 0.01)
-    dz, dv, st = G.dev_f32(np.zeros((m, A))), G.dev_f32(np.zeros(m)), G.dev_f32(np.zeros(8))
-    P.impala_loss_grad(m, A, G.dev_f32(b["z"]), G.dev_f32(b["v"]), G.dev_i32(b["a"]), G.dev_f32(b["vs"]),
-                       G.dev_f32(b["pg"]), 1.0, 0.5, 0.01, dz, dv, st)
-    G.sync()
+    outs = []
+    for ws in (None, G.ws_bytes(P.loss_workspace_bytes(m))):
+        dz, dv, st = G.dev_f32(np.zeros((m, A))), G.dev_f32(np.zeros(m)), G.dev_f32(np.zeros(8))
+        P.impala_loss_grad(m, A, G.dev_f32(b["z"]), G.dev_f32(b["v"]), G.dev_i32(b["a"]), G.dev_f32(b["vs"]),
+                           G.dev_f32(b["pg"]), 1.0, 0.5, 0.01, dz, dv, st, ws)
+        G.sync()
+        outs.append((dz, dv, st))
+    dz, dv, st = outs[0]
     G.assert_close(G.host(dz), dz_w, 1e-5, "dlogits")
     G.assert_close(G.host(dv), dv_w, 1e-5, "dvalue")
     G.assert_close(G.host(st)[:6], st_w[:6], 1e-5, "stats")
+    torch = G.torch()
+    assert all(torch.equal(x, y) for x, y in zip(outs[0], outs[1]))
 
 
 @pytest.mark.parametrize("n,scale,max_norm,step", [(1_094_115, 1e-3, 0.5, 1), (1_094_115, 10.0, 0.5, 7),

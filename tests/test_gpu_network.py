@@ -507,6 +507,54 @@ def test_learner_step_equals_its_abi_calls(wid, prec):
     assert torch.equal(got[4], stats)
 
 
+def test_learner_step_large_minibatch_equals_its_abi_calls():
+    """A minibatch above 16384 rows (the loss then reduces over workgroups; learner_step forms
+    the gradients and the loss partials in one pass with its workspace, ppo_loss_grad in two
+    passes without one): learner_step on small frames (12 x 10, stages (16,16,32)) with one
+    20000-row minibatch of a 160 x 128 rollout equals GAE, impala_cnn_fwd, ppo_loss_grad,
+    impala_cnn_bwd and adam_step bit for bit."""
+    torch = G.torch()
+    net = NetShape(in_h=12, in_w=10, ch=(16, 16, 32), hidden=64, num_actions=7)
+    wl = Workload("ppo_bigmb", "ppo", T=160, E=128, net=net, epochs=1, num_minibatches=1, minibatch_size=20000,
+                  seed=31)
+    raw = draw_rollout(wl)
+    rng = np.random.default_rng(31)
+    T, E, A, mb = wl.T, wl.E, net.num_actions, wl.mb
+    ro = dict(obs=raw["obs"][:T].reshape(T * E, net.in_h, net.in_w, 4),
+              actions=rng.integers(0, A, T * E).astype(np.int32),
+              logp=(np.log(1.0 / A) + 0.05 * rng.standard_normal(T * E)).astype(np.float32),
+              rewards=raw["rewards"], dones=raw["dones"], values=(0.1 * rng.standard_normal((T, E))).astype(np.float32),
+              next_value=(0.1 * rng.standard_normal(E)).astype(np.float32), next_done=raw["next_done"])
+    params = draw_params(net, wl.seed)
+    got = _learner_gpu(wl, G.BF16, params, ro, raw["perm"])
+    d = _gpu_rollout(ro, wl)
+    adv = torch.empty((T, E), dtype=torch.float32, device="cuda:0")
+    ret = torch.empty_like(adv)
+    P.gae_advantages(T, E, d["rewards"], d["values"], d["dones"], d["next_value"], d["next_done"], wl.gamma, wl.lam,
+                     adv, ret)
+    p = G.dev_f32(params)
+    m, v = torch.zeros_like(p), torch.zeros_like(p)
+    ws = G.ws_bytes(P.impala_workspace_bytes(net, mb, G.BF16, 1))
+    aws = G.ws_bytes(P.adam_workspace_bytes(p.numel()))
+    rows = G.dev_i32(raw["perm"][0, :mb])
+    logits = torch.empty((mb, A), dtype=torch.float32, device="cuda:0")
+    value = torch.empty(mb, dtype=torch.float32, device="cuda:0")
+    P.impala_cnn_fwd(net, G.BF16, p, d["obs"], rows, mb, ws, 1, logits, value)
+    rl = rows.long()
+    dz, dv = torch.empty_like(logits), torch.empty_like(value)
+    stats = torch.zeros((1, 8), dtype=torch.float32, device="cuda:0")
+    P.ppo_loss_grad(mb, A, logits, value, d["actions"][rl].contiguous(), d["logp"][rl].contiguous(),
+                    adv.view(-1)[rl].contiguous(), ret.view(-1)[rl].contiguous(), 1, wl.clip_eps, wl.vf_coef,
+                    wl.ent_coef, dz, dv, stats[0])
+    grads = torch.empty_like(p)
+    P.impala_cnn_bwd(net, G.BF16, p, d["obs"], rows, mb, ws, dz, dv, grads)
+    P.adam_step(p.numel(), p, grads, m, v, 1, wl.lr, wl.beta1, wl.beta2, wl.adam_eps, wl.max_grad_norm,
+                stats[0, 6:], aws)
+    G.sync()
+    assert torch.equal(got[4], stats)
+    assert torch.equal(got[0], p) and torch.equal(got[1], m) and torch.equal(got[2], v)
+
+
 def _impala_inputs(wl, seed):
     """IMPALA rollout with behaviour data drawn without the network (GPU-against-GPU tests)."""
     raw = draw_rollout(wl)
