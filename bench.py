@@ -447,8 +447,8 @@ def actor_latency(P, wl, prec_name, calls):
     obs = torch.from_numpy(b["obs"]).cuda()
     gumbel = torch.from_numpy(b["gumbel"]).cuda()
     # without a logits output the call keeps the logits in its workspace: n * A floats more
-    ws = torch.empty(P.impala_workspace_bytes(net, n, prec, 0) + n * net.num_actions * 4, dtype=torch.uint8,
-                     device="cuda")
+    ws = torch.empty(P.impala_workspace_bytes(net, n, prec, 0) + (n * net.num_actions * 4 + 255) // 256 * 256,
+                     dtype=torch.uint8, device="cuda")
     act = torch.empty(n, dtype=torch.int32, device="cuda")
     logp, value = (torch.empty(n, dtype=torch.float32, device="cuda") for _ in range(2))
     stream = torch.cuda.current_stream()

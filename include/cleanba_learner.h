@@ -261,7 +261,9 @@ impala_status_t learner_step(const impala_net_t* net, const learner_cfg_t* cfg,
 /* Actor inference (Algorithm 1: a_t ~ pi(.|s_t) and v_t = v(s_t)): forward on n frames,
  * then Gumbel-max sampling a = argmax_j(z_j + gumbel_j) with ties to the lowest index, and
  * log pi(a). gumbel: float [n, A] caller-drawn standard Gumbel noise. actions: int32 [n];
- * logp, value: float [n]; logits: float [n, A] or NULL. ws sized with training = 0. */
+ * logp, value: float [n]; logits: float [n, A] or NULL. ws: impala_workspace_bytes(net, n,
+ * prec, 0) bytes, plus n*A*4 rounded up to a multiple of 256 when logits is NULL (the logits
+ * are then kept there). */
 impala_status_t impala_actor_step(const impala_net_t* net, impala_prec_t prec, const float* params,
                                   const uint8_t* obs, int64_t n, const float* gumbel, void* ws,
                                   size_t ws_bytes, int32_t* actions, float* logp, float* value,
