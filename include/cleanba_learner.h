@@ -90,7 +90,9 @@ const char* impala_last_error(void);
 
 /* Forward pass: logits [n, A] and value [n] of frames obs[row_idx[i]] (or obs[i] when
  * row_idx is NULL; gathering the minibatch rows of Algorithm 1 in the first conv's load).
- * obs: uint8 [*, H, W, C]; row_idx: int32 [n] or NULL. Pixels are scaled by 1/255.
+ * obs: uint8 [*, H, W, C]; row_idx: int32 [n] or NULL, every entry a row of obs (0 <= r <
+ * rows of obs; the call cannot check this without reading device memory, and an entry outside
+ * the buffer makes the kernels read outside it). Pixels are scaled by 1/255.
  * training != 0 keeps the activations in `ws` for a following impala_cnn_bwd with the same
  * (params, obs, row_idx, n, ws). */
 impala_status_t impala_cnn_fwd(const impala_net_t* net, impala_prec_t prec, const float* params,
@@ -249,7 +251,9 @@ size_t learner_workspace_bytes(const impala_net_t* net, const learner_cfg_t* cfg
  * rows, backward (bootstrap rows get no gradient), clip, optimiser step.
  * params, m, v: float [param_count], updated in place (RMSprop: v holds its nu, m is unused and
  * may be NULL). step: HOST int32, 1-based count of
- * updates done so far (incremented). perm: int32 [update_epochs, T*E] (PPO; NULL for IMPALA).
+ * updates done so far (incremented). perm: int32 [update_epochs, T*E] (PPO; NULL for IMPALA),
+ * every entry in [0, T*E) (not checked: it indexes the frames and the rollout arrays on the
+ * device; each row of perm is normally a permutation).
  * stats: float [n_updates, 8] (n_updates = update_epochs * num_minibatches for PPO,
  * num_minibatches for IMPALA) rows [L, policy, value, entropy, approx_kl or mean pg_adv,
  * clipfrac or mean vs, pre-clip grad norm, nonfinite]. */
