@@ -31,8 +31,11 @@ namespace cb {
 
 template <int C>
 struct RbbGeom {
-    static constexpr int DSL = C / 8 + 1;                  // dy / dt windows: 16-byte slots per pixel
-    static constexpr int DYP = DSL * 16;                   // ... the last slot is zero
+    // dy / dt windows: 16-byte slots per pixel. 16 channels: 32 bytes, for which the 16 lanes
+    // of a fragment read on consecutive pixels cover every bank; 32: an extra slot (never
+    // read) makes the pitch odd in 16-byte units
+    static constexpr int DSL = C >= 32 ? C / 8 + 1 : C / 8;
+    static constexpr int DYP = DSL * 16;
     static constexpr int XPB = C * 2 + (C >= 32 ? 32 : 0);    // t / x windows: bytes per pixel
     static constexpr int XSL = XPB / 16;
     static constexpr int MT = C / 16;
@@ -107,13 +110,16 @@ __global__ __launch_bounds__(64 * NW, RbbGeom<C>::WPS) void resblock_bwd_kernel(
         wfb[ks] = make_uint4(pack2bf(vb[0], vb[1]), pack2bf(vb[2], vb[3]), pack2bf(vb[4], vb[5]), pack2bf(vb[6], vb[7]));
     }
     // B-fragment byte offsets from the lane's tap-(0,0) pixel of a dy-like window; with 16
-    // channels a k-step spans two taps (a per-lane table), from 32 on only the slot is the lane's
+    // channels a k-step spans two taps (a per-lane table), from 32 on only the slot is the lane's.
+    // Past the ninth tap the weights are zero, so those lanes re-read tap 8 (a value that
+    // already enters the sum through tap 8 itself)
     int dboff[C < 32 ? KSD : 1];
     if constexpr (C < 32) {
 #pragma unroll
         for (int ks = 0; ks < KSD; ++ks) {
             const int k0 = ks * 32 + g * 8, tap = k0 / C, slot = (k0 % C) / 8;
-            dboff[ks] = tap < 9 ? ((tap / 3) * TW + tap % 3) * DYP + slot * 16 : (DSL - 1) * 16;
+            const int tp = tap < 9 ? tap : 8;
+            dboff[ks] = ((tp / 3) * TW + tp % 3) * DYP + slot * 16;
         }
     }
     const int twdy = TW * DYP;
