@@ -46,15 +46,21 @@ struct CbGeom {
     static constexpr int NB = 9 * CI / 16;               // weight-gradient column blocks
     static constexpr int NBB = NB + 1;                   // ... and the bias block
     static constexpr int PSTRIDE = MTO * NBB * 256;      // floats per workgroup partial
+    // 64 channels: the input-gradient weights (72 registers) and the weight-gradient
+    // accumulators (up to 80) take the registers of two waves per SIMD, so one workgroup per CU
+    // with all of the LDS (taller bands); otherwise two per CU
+    static constexpr bool WIDE = CI >= 64 || CO >= 64;
+    static constexpr int WPS = WIDE ? 2 : 4;
+    static constexpr size_t LDS_TARGET = WIDE ? 160 * 1024 : 80 * 1024;
     // staging slots per lane (of an 8-wave workgroup) the tile planner stays within
-    static constexpr int MAXD = CO > CI ? 7 : 6, MAXX = 4;
-    static constexpr int MAXT = CI >= 32 ? 4 : 6;   // dx column tiles per wave and tile (with a residual)
-    static constexpr int MAXP = 3, MAXG = 2;         // pooled-gradient / argmax staging slots per lane
+    static constexpr int MAXD = WIDE ? 8 : (CO > CI ? 7 : 6), MAXX = WIDE || CO > CI ? (CI >= 32 ? 8 : 4) : 4;
+    static constexpr int MAXT = WIDE ? 5 : (CI >= 32 ? 4 : 6);   // dx column tiles per wave and tile (with a residual)
+    static constexpr int MAXP = CO >= 64 ? 4 : 3, MAXG = 2;      // pooled-gradient / argmax staging slots per lane
     __host__ __device__ static int blocks(int slots) { return (slots + 63) / 64; }
 };
 
 template <int CI, int CO, int MODE, int ADD, int PDY, int NW>
-__global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbTile t) {
+__global__ __launch_bounds__(64 * NW, (CbGeom<CI, CO>::WPS)) void conv_bwd_kernel(ConvBwdArgs a, CbTile t) {
     using G = CbGeom<CI, CO>;
     constexpr int NT = 64 * NW;
     constexpr int DSL = G::DSL, DYP = G::DYP, XPB = G::XPB, XSL = G::XSL;
@@ -478,7 +484,6 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_bwd_kernel(ConvBwdArgs a, CbT
 namespace {
 
 constexpr int kCbWaves = 8;
-constexpr size_t kCbLdsTarget = 80 * 1024;   // two 8-wave workgroups per CU
 constexpr int kCbPixMax = 2048;
 constexpr size_t kCbPartBytes = 24u << 20;
 
@@ -520,7 +525,7 @@ hipError_t cb_launch(const ConvBwdArgs& a, hipStream_t s, PendingReduce* deferre
     };
     const size_t limit = std::min<size_t>(lds_limit(), 160 * 1024);
     int thmax = std::min(H, std::max(1, kCbPixMax / W));
-    while (thmax > 1 && (lds(thmax, 1) > kCbLdsTarget || !fits(thmax, 1))) --thmax;
+    while (thmax > 1 && (lds(thmax, 1) > G::LDS_TARGET || !fits(thmax, 1))) --thmax;
     if (lds(thmax, 1) > limit || !fits(thmax, 1)) return hipErrorInvalidValue;
     int TH = 1, best = 1 << 30;   // band height staging the fewest window rows per frame
     for (int th = 1; th <= thmax; ++th) {
@@ -530,7 +535,7 @@ hipError_t cb_launch(const ConvBwdArgs& a, hipStream_t s, PendingReduce* deferre
     const int nbands = (H + TH - 1) / TH;
     int FR = 1;
     if (nbands == 1 && !PDY)
-        while (FR < a.n && lds(TH, FR + 1) <= kCbLdsTarget && fits(TH, FR + 1) && (FR + 1) * H * W <= kCbPixMax) ++FR;
+        while (FR < a.n && lds(TH, FR + 1) <= G::LDS_TARGET && fits(TH, FR + 1) && (FR + 1) * H * W <= kCbPixMax) ++FR;
     // 32-bit buffer offsets cover FR frames of each operand
     if (int64_t(FR) * H * W * std::max(CI, CO) * 2 >= (int64_t(1) << 31)) return hipErrorInvalidValue;
     CbTile t{};
@@ -568,8 +573,10 @@ hipError_t cb_launch(const ConvBwdArgs& a, hipStream_t s, PendingReduce* deferre
 }  // namespace
 
 bool conv3x3_bwd_supported(int cin, int cout, int mode, int add, int pooled) {
-    if (mode == IN_RELU) return !pooled && cin == cout && (cin == 16 || cin == 32);
-    if (mode == IN_PLAIN) return !add && ((cin == 16 && (cout == 16 || cout == 32)) || (cin == 32 && cout == 32));
+    if (mode == IN_RELU) return !pooled && cin == cout && (cin == 16 || cin == 32 || cin == 64);
+    if (mode == IN_PLAIN)
+        return !add && ((cin == 16 && (cout == 16 || cout == 32)) || (cin == 32 && (cout == 32 || cout == 64)) ||
+                        (cin == 64 && cout == 64));
     return false;
 }
 
@@ -577,7 +584,7 @@ size_t conv3x3_bwd_partial_floats(int cin, int cout) {
     size_t best = 0;
 #define CB_PF(CI, CO) \
     if (cin == CI && cout == CO) best = size_t(cb_parts_cap<CI, CO>()) * CbGeom<CI, CO>::PSTRIDE;
-    CB_PF(16, 16) CB_PF(16, 32) CB_PF(32, 32)
+    CB_PF(16, 16) CB_PF(16, 32) CB_PF(32, 32) CB_PF(32, 64) CB_PF(64, 64)
 #undef CB_PF
     return best;
 }
@@ -592,8 +599,11 @@ hipError_t conv3x3_bwd(int cin, int cout, int mode, const ConvBwdArgs& a, hipStr
 #define CB_B(CI, CO, MD, AD, PD) \
     if (cin == CI && cout == CO && mode == MD && add == AD && pdy == PD) return cb_launch<CI, CO, MD, AD, PD>(a, s, deferred);
     CB_B(16, 16, IN_RELU, 0, 0) CB_B(16, 16, IN_RELU, 1, 0) CB_B(32, 32, IN_RELU, 0, 0) CB_B(32, 32, IN_RELU, 1, 0)
+    CB_B(64, 64, IN_RELU, 0, 0) CB_B(64, 64, IN_RELU, 1, 0)
     CB_B(16, 16, IN_PLAIN, 0, 0) CB_B(16, 32, IN_PLAIN, 0, 0) CB_B(32, 32, IN_PLAIN, 0, 0)
+    CB_B(32, 64, IN_PLAIN, 0, 0) CB_B(64, 64, IN_PLAIN, 0, 0)
     CB_B(16, 16, IN_PLAIN, 0, 1) CB_B(16, 32, IN_PLAIN, 0, 1) CB_B(32, 32, IN_PLAIN, 0, 1)
+    CB_B(32, 64, IN_PLAIN, 0, 1) CB_B(64, 64, IN_PLAIN, 0, 1)
 #undef CB_B
     return hipErrorInvalidValue;
 }

@@ -715,8 +715,8 @@ hipError_t wgrad_reduce_tr(int cin, int cout, const float* partial, int nparts, 
                            nparts, dw, db, scale);                                                     \
         return hipGetLastError();                                                                      \
     }
-    CB_RT(16, 16, IN_PLAIN) CB_RT(16, 32, IN_PLAIN) CB_RT(32, 32, IN_PLAIN)
-    CB_RT(4, 16, IN_U8) CB_RT(4, 32, IN_U8)
+    CB_RT(16, 16, IN_PLAIN) CB_RT(16, 32, IN_PLAIN) CB_RT(32, 32, IN_PLAIN) CB_RT(32, 64, IN_PLAIN)
+    CB_RT(64, 64, IN_PLAIN) CB_RT(4, 16, IN_U8) CB_RT(4, 32, IN_U8)
 #undef CB_RT
     return hipErrorInvalidValue;
 }

@@ -238,6 +238,10 @@ CONV_BWD_CASES = [
     (3, 21, 21, 32, 32, P.X_RELU, 0), (5, 11, 11, 32, 32, P.X_RELU, 1), (37, 11, 11, 32, 32, P.X_RELU, 0),
     (3, 42, 42, 16, 32, P.X_PLAIN, 0), (2, 21, 21, 32, 32, P.X_PLAIN, 0), (2, 17, 23, 16, 16, P.X_RELU, 1),
     (3, 9, 7, 32, 32, P.X_RELU, 1), (1, 84, 84, 16, 16, P.X_RELU, 1), (6, 5, 3, 16, 32, P.X_PLAIN, 0),
+    # the wide net's 64-channel layers: bands of 21x21 frames, multi-frame 11x11 tiles, ragged
+    (3, 21, 21, 64, 64, P.X_RELU, 1), (2, 21, 21, 64, 64, P.X_RELU, 0), (7, 11, 11, 64, 64, P.X_RELU, 1),
+    (5, 11, 11, 64, 64, P.X_RELU, 0), (2, 13, 9, 64, 64, P.X_RELU, 1), (2, 21, 21, 64, 64, P.X_PLAIN, 0),
+    (2, 42, 42, 32, 64, P.X_PLAIN, 0), (3, 7, 5, 32, 64, P.X_PLAIN, 0),
 ]
 
 
@@ -363,7 +367,8 @@ def test_resblock_backward_rejects_unsupported():
 
 # (n, H, W, cin, cout): stage entries fed by a max-pool (base and ragged, odd and even padding)
 CONV_BWD_POOL_CASES = [(3, 42, 42, 16, 32), (2, 21, 21, 32, 32), (4, 42, 42, 16, 16), (2, 17, 23, 16, 32),
-                       (5, 9, 7, 32, 32), (1, 84, 84, 16, 16), (3, 11, 11, 32, 32), (6, 4, 5, 16, 16)]
+                       (5, 9, 7, 32, 32), (1, 84, 84, 16, 16), (3, 11, 11, 32, 32), (6, 4, 5, 16, 16),
+                       (2, 42, 42, 32, 64), (3, 21, 21, 64, 64), (4, 9, 11, 32, 64), (5, 11, 11, 64, 64)]
 
 
 @pytest.mark.parametrize("case", CONV_BWD_POOL_CASES, ids=lambda c: "n%d_%dx%d_%d-%d" % c)
@@ -402,8 +407,9 @@ def test_conv_backward_fused_rejects_unsupported():
     z = G.dev_act(np.zeros((1, 8, 8, 64)), G.BF16)
     w = G.dev_f32(np.zeros((3, 3, 64, 64)))
     dw, db = G.dev_f32(np.zeros((3, 3, 64, 64))), G.dev_f32(np.zeros(64))
-    with pytest.raises(P.LibraryError):   # 64 channels: not in the fused set
-        P.impala_conv3x3_bwd(G.BF16, 1, 8, 8, 64, 64, z, z, P.X_RELU, w, None, z, dw, db, ws)
+    z16 = G.dev_act(np.zeros((1, 8, 8, 16)), G.BF16)
+    with pytest.raises(P.LibraryError):   # 16 -> 64 channels: not in the fused set
+        P.impala_conv3x3_bwd(G.BF16, 1, 8, 8, 16, 64, z, z16, P.X_PLAIN, w, None, z16, dw, db, ws)
     z16 = G.dev_act(np.zeros((1, 8, 8, 16)), G.FP32)
     w16 = G.dev_f32(np.zeros((3, 3, 16, 16)))
     with pytest.raises(P.LibraryError):   # float32 storage
