@@ -31,10 +31,14 @@ struct CpGeom {
     static constexpr int KPB = COUT * 2 + 16;              // key-tile bytes per pixel (odd slots)
     static constexpr int C8 = COUT / 8;
     static constexpr int MAXS = 6;                         // input staging slots per lane
+    // 64 input channels: the weight fragments (72 registers) take the registers of two waves
+    // per SIMD, so one workgroup per CU with most of the LDS; otherwise four waves per SIMD
+    static constexpr int WPS = CIN >= 64 ? 2 : 4;
+    static constexpr size_t LDS_TARGET = CIN >= 64 ? 150 * 1024 : 80 * 1024;
 };
 
 template <int CIN, int COUT, int MODE, int NW>
-__global__ __launch_bounds__(64 * NW, 4) void conv_pool_kernel(ConvArgs a, CpTile t) {
+__global__ __launch_bounds__(64 * NW, (CpGeom<CIN, COUT, MODE>::WPS)) void conv_pool_kernel(ConvArgs a, CpTile t) {
     using G = CpGeom<CIN, COUT, MODE>;
     constexpr int NT = 64 * NW, KSTEPS = G::KSTEPS, MT = G::MT, PB = G::PB, KPB = G::KPB, C8 = G::C8;
     constexpr bool U8 = G::U8;
@@ -96,8 +100,10 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_pool_kernel(ConvArgs a, CpTil
             return make_uint4(t8.x, t8.y, t8.x, t8.y);
         } else if constexpr (CIN < 32) {
             return *reinterpret_cast<const uint4*>(xb + boff[ks]);
-        } else {
-            return *reinterpret_cast<const uint4*>(xb + (ks / 3) * twpb + (ks % 3) * PB + g * 16);
+        } else {   // from 32 channels a tap spans CIN / 32 k-steps; the lane's slot within it
+            constexpr int TPK = CIN / 32;
+            const int tap = ks / TPK, cs = (ks % TPK) * 4;
+            return *reinterpret_cast<const uint4*>(xb + (tap / 3) * twpb + (tap % 3) * PB + (cs + g) * 16);
         }
     };
 
@@ -253,7 +259,6 @@ __global__ __launch_bounds__(64 * NW, 4) void conv_pool_kernel(ConvArgs a, CpTil
 namespace {
 
 constexpr int kCpWaves = 8;
-constexpr size_t kCpLdsTarget = 80 * 1024;
 constexpr int kCpPixMax = 4096;
 
 template <int CIN, int COUT, int MODE>
@@ -281,7 +286,7 @@ hipError_t cp_launch(const ConvArgs& a, hipStream_t s) {
     };
     CpTile t{};
     int pmax = OH;
-    while (pmax > 1 && (layout(pmax, t) > kCpLdsTarget || !fits(pmax))) --pmax;
+    while (pmax > 1 && (layout(pmax, t) > G::LDS_TARGET || !fits(pmax))) --pmax;
     if (layout(pmax, t) > std::min<size_t>(lds_limit(), 160 * 1024) || !fits(pmax)) return hipErrorInvalidValue;
     if (int64_t(H) * W * std::max(CIN, 2) * 2 >= (int64_t(1) << 31)) return hipErrorInvalidValue;
     const int nb0 = (OH + pmax - 1) / pmax;
@@ -305,7 +310,8 @@ hipError_t cp_launch(const ConvArgs& a, hipStream_t s) {
 
 bool conv_pool_fast_supported(int cin, int cout, int mode) {
     if (mode == IN_U8) return cin == 4 && (cout == 16 || cout == 32);
-    return mode == IN_PLAIN && ((cin == 16 && (cout == 16 || cout == 32)) || (cin == 32 && cout == 32));
+    return mode == IN_PLAIN && ((cin == 16 && (cout == 16 || cout == 32)) || (cin == 32 && (cout == 32 || cout == 64)) ||
+                                (cin == 64 && cout == 64));
 }
 
 hipError_t conv_pool_fast(int cin, int cout, int mode, const ConvArgs& a, hipStream_t s) {
@@ -313,6 +319,7 @@ hipError_t conv_pool_fast(int cin, int cout, int mode, const ConvArgs& a, hipStr
 #define CB_CPF(CI, CO, MD) \
     if (cin == CI && cout == CO && mode == MD) return cp_launch<CI, CO, MD>(a, s);
     CB_CPF(4, 16, IN_U8) CB_CPF(4, 32, IN_U8) CB_CPF(16, 16, IN_PLAIN) CB_CPF(16, 32, IN_PLAIN) CB_CPF(32, 32, IN_PLAIN)
+    CB_CPF(32, 64, IN_PLAIN) CB_CPF(64, 64, IN_PLAIN)
 #undef CB_CPF
     return hipErrorInvalidValue;
 }

@@ -75,7 +75,8 @@ POOL_CASES = [(3, 84, 84, 4, 16, P.X_U8), (2, 84, 84, 4, 32, P.X_U8), (2, 13, 9,
               (3, 42, 42, 16, 32, P.X_PLAIN), (2, 42, 42, 16, 16, P.X_PLAIN), (4, 21, 21, 32, 32, P.X_PLAIN),
               (5, 11, 11, 32, 64, P.X_PLAIN), (2, 17, 23, 16, 64, P.X_PLAIN), (3, 21, 21, 64, 64, P.X_PLAIN),
               (3, 17, 23, 16, 32, P.X_PLAIN), (2, 13, 9, 4, 16, P.X_U8), (4, 9, 7, 32, 32, P.X_PLAIN),
-              (5, 11, 11, 32, 32, P.X_PLAIN), (1, 6, 5, 16, 16, P.X_PLAIN), (2, 23, 19, 4, 32, P.X_U8)]
+              (5, 11, 11, 32, 32, P.X_PLAIN), (1, 6, 5, 16, 16, P.X_PLAIN), (2, 23, 19, 4, 32, P.X_U8),
+              (2, 42, 42, 32, 64, P.X_PLAIN), (3, 9, 11, 64, 64, P.X_PLAIN), (2, 11, 11, 64, 64, P.X_PLAIN)]
 
 
 def _pool_windows(x, fill):
@@ -97,7 +98,8 @@ def test_conv_pool_forward(case):
     _conv_pool_check(case)
 
 
-@pytest.mark.parametrize("case", [(1024, 84, 84, 4, 16, P.X_U8), (1024, 42, 42, 16, 32, P.X_PLAIN)],
+@pytest.mark.parametrize("case", [(1024, 84, 84, 4, 16, P.X_U8), (1024, 42, 42, 16, 32, P.X_PLAIN),
+                                  (1024, 42, 42, 32, 64, P.X_PLAIN), (1024, 21, 21, 64, 64, P.X_PLAIN)],
                          ids=lambda c: "n%d_%dx%d_%d-%d_m%d" % c)
 def test_conv_pool_forward_many_tiles_per_workgroup(case):
     """The same checks at a frame count where every workgroup runs several tiles (each tile's
