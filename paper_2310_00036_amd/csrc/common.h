@@ -134,8 +134,46 @@ CB_DEV void dma16_to_lds(__amdgpu_buffer_rsrc_t r, unsigned char* lds, uint32_t 
 
 // Order-preserving 16-bit keys of two packed bf16 values: as unsigned integers the keys
 // compare like the values (-0 sorts just below +0; NaNs sort beyond the infinities).
-CB_DEV uint32_t bf16x2_key(uint32_t u) { return u ^ ((((u >> 15) & 0x10001u) * 0x7fffu) | 0x80008000u); }
-CB_DEV uint32_t bf16x2_unkey(uint32_t k) { return k ^ (((((~k) >> 15) & 0x10001u) * 0x7fffu) | 0x80008000u); }
+// A negative half is complemented, a positive one has its sign bit set; the sign masks come
+// from one packed 16-bit arithmetic shift.
+CB_DEV uint32_t sign_mask16x2(uint32_t u) {
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(cb_s16x2, u) >> cb_s16x2{15, 15});
+}
+CB_DEV uint32_t bf16x2_key(uint32_t u) { return u ^ (sign_mask16x2(u) | 0x80008000u); }
+CB_DEV uint32_t bf16x2_unkey(uint32_t k) { return k ^ (~sign_mask16x2(k) | 0x80008000u); }
+
+// Max-pool backward gathers. ka holds the argmax cells (0..8) of four channels, one per
+// byte; d their bf16 gradients (channels 0, 1 in d.x, 2, 3 in d.y). arg_pick<T> keeps the
+// gradients of the channels whose cell is T and makes the others +0. arg_sel gives byte
+// selectors that name each channel's cell twice ([k0 k0 k1 k1], [k2 k2 k3 k3]): v_perm with
+// such a selector looks up each cell in an 8-byte table (0xff at byte T) and widens the
+// result to the channel's 16 bits. Cell 8 selects v_perm's sign-of-byte-1 entry, which is
+// zero in every table but T = 1's; T = 1 therefore looks up cell ^ 1 in T = 0's table (cell
+// 8 then selects the zero sign of byte 3), and T = 8, the only cell with bit 3 set, widens
+// that bit with the sign-byte selectors.
+CB_DEV uint32_t arg_sel01(uint32_t ka) { return __builtin_amdgcn_perm(0u, ka, 0x01010000u); }
+CB_DEV uint32_t arg_sel23(uint32_t ka) { return __builtin_amdgcn_perm(0u, ka, 0x03030202u); }
+template <int T>
+CB_DEV uint2 arg_pick(uint2 d, uint32_t ka, uint32_t s01, uint32_t s23) {
+    static_assert(T >= 0 && T <= 8, "a 3x3 window has cells 0..8");
+    uint32_t m01, m23;
+    if constexpr (T == 8) {
+        const uint32_t a = ka << 4, b = ka << 12;   // bit 3 of cells 1, 3 at bits 15, 31 of a; 0, 2 of b
+        m01 = __builtin_amdgcn_perm(b, a, 0x08080a0au);
+        m23 = __builtin_amdgcn_perm(b, a, 0x09090b0bu);
+    } else if constexpr (T == 1) {
+        const uint32_t kb = ka ^ 0x01010101u;
+        m01 = __builtin_amdgcn_perm(0u, 0xffu, arg_sel01(kb));
+        m23 = __builtin_amdgcn_perm(0u, 0xffu, arg_sel23(kb));
+    } else {
+        constexpr uint32_t lo = T < 4 ? 0xffu << (8 * T) : 0u, hi = T < 4 ? 0u : 0xffu << (8 * (T - 4));
+        m01 = __builtin_amdgcn_perm(hi, lo, s01);
+        m23 = __builtin_amdgcn_perm(hi, lo, s23);
+    }
+    return make_uint2(d.x & m01, d.y & m23);
+}
+CB_DEV float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
+CB_DEV float bf_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
 
 typedef short cb_s16x4 __attribute__((ext_vector_type(4)));
 // LDS transpose read of 16-bit data (ds_read_b64_tr_b16). Every lane addresses an 8-byte

@@ -267,14 +267,16 @@ __global__ __launch_bounds__(64 * NW, (CbGeom<CI, CO>::WPS)) void conv_bwd_kerne
                 const int i0 = ilo + RPI * bp2, lr0 = i0 - ib0;
                 // window rows lr0, lr0+1 (the first block row), then lr0+2 replaces lr0 (the
                 // second): the middle row is loaded once for both
-                uint32_t ka[2][2];
-                uint2 dg[2][2];   // 4 bf16 gradients, unpacked where used
+                uint32_t ka[2][2], s01[2][2], s23[2][2];
+                uint2 dg[2][2];   // 4 bf16 gradients
                 auto load_row = [&](int slot, int lr) {
 #pragma unroll
                     for (int q = 0; q < 2; ++q) {
                         const int px = lr * PW2 + j + q;
                         ka[slot][q] = *reinterpret_cast<const uint32_t*>(agl + px * CO + c4 * 4);
                         dg[slot][q] = *reinterpret_cast<const uint2*>(dpl + (px * CO + c4 * 4) * 2);
+                        s01[slot][q] = arg_sel01(ka[slot][q]);
+                        s23[slot][q] = arg_sel23(ka[slot][q]);
                     }
                 };
                 load_row(0, lr0);
@@ -285,39 +287,34 @@ __global__ __launch_bounds__(64 * NW, (CbGeom<CI, CO>::WPS)) void conv_bwd_kerne
                     if (i > ib1) break;
                     if (sb == 1) load_row(0, lr0 + 2);   // rows: slot 1 = lr0+1 (top), slot 0 = lr0+2
                     const int top = sb == 0 ? 0 : 1, bot = sb == 0 ? 1 : 0;
-                    float c00[4], c01[4], c10[4], c11[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        uint32_t k[4];
-                        float g4[4];
-#pragma unroll
-                        for (int w4 = 0; w4 < 4; ++w4) {
-                            const int rs = (w4 >> 1) ? bot : top;
-                            k[w4] = (ka[rs][w4 & 1] >> (8 * e)) & 0xffu;
-                            const uint2 d = dg[rs][w4 & 1];
-                            const uint32_t u = e < 2 ? d.x : d.y;
-                            g4[w4] = __uint_as_float((e & 1) ? (u & 0xffff0000u) : (u << 16));
-                        }
-                        float s00 = 0.f, s01 = 0.f, s10 = 0.f, s11 = 0.f;
-                        s00 += k[0] == 8 ? g4[0] : 0.f;
-                        s00 += k[1] == 6 ? g4[1] : 0.f;
-                        s00 += k[2] == 2 ? g4[2] : 0.f;
-                        s00 += k[3] == 0 ? g4[3] : 0.f;
-                        s01 += k[1] == 7 ? g4[1] : 0.f;
-                        s01 += k[3] == 1 ? g4[3] : 0.f;
-                        s10 += k[2] == 5 ? g4[2] : 0.f;
-                        s10 += k[3] == 3 ? g4[3] : 0.f;
-                        s11 += k[3] == 4 ? g4[3] : 0.f;
-                        c00[e] = s00; c01[e] = s01; c10[e] = s10; c11[e] = s11;
-                    }
+                    // window w4's gradients where its cell is T, else +0; each cell adds its
+                    // windows in (oh, ow) order, the lower-right cell has one and keeps its bf16
+                    // gradient as it is
+#define CB_PICK(T, w4)                                                                                 \
+    arg_pick<T>(dg[((w4) >> 1) ? bot : top][(w4) & 1], ka[((w4) >> 1) ? bot : top][(w4) & 1], \
+                s01[((w4) >> 1) ? bot : top][(w4) & 1], s23[((w4) >> 1) ? bot : top][(w4) & 1])
+                    const uint2 a0 = CB_PICK(8, 0), a1 = CB_PICK(6, 1), a2 = CB_PICK(2, 2), a3 = CB_PICK(0, 3);
+                    const uint2 b1 = CB_PICK(7, 1), b3 = CB_PICK(1, 3);
+                    const uint2 e2 = CB_PICK(5, 2), e3 = CB_PICK(3, 3);
+                    const uint2 c11 = CB_PICK(4, 3);
+#undef CB_PICK
+                    auto sum4 = [](uint32_t u0, uint32_t u1, uint32_t u2, uint32_t u3) {
+                        return pack2bf(bf_lo(u0) + bf_lo(u1) + bf_lo(u2) + bf_lo(u3),
+                                       bf_hi(u0) + bf_hi(u1) + bf_hi(u2) + bf_hi(u3));
+                    };
+                    auto sum2 = [](uint32_t u0, uint32_t u1) {
+                        return pack2bf(bf_lo(u0) + bf_lo(u1), bf_hi(u0) + bf_hi(u1));
+                    };
+                    const uint2 c00 = make_uint2(sum4(a0.x, a1.x, a2.x, a3.x), sum4(a0.y, a1.y, a2.y, a3.y));
+                    const uint2 c01 = make_uint2(sum2(b1.x, b3.x), sum2(b1.y, b3.y));
+                    const uint2 c10 = make_uint2(sum2(e2.x, e3.x), sum2(e2.y, e3.y));
                     // cells -> dy-window row h - h0 + 1, column w + 1; off the frame: zero
                     const int h = 2 * i - t.ph, w = 2 * j - t.pw;
-                    auto put = [&](int hh, int ww, const float* c) {
+                    auto put = [&](int hh, int ww, uint2 c) {
                         const int rr = hh - h0 + 1;
                         if (rr < 0 || rr >= the + 2) return;
                         const bool in = hh >= 0 && hh < H && ww >= 0 && ww < W;
-                        *reinterpret_cast<uint2*>(dyw + (rr * TW + ww + 1) * DYP + c4 * 8) =
-                            in ? make_uint2(pack2bf(c[0], c[1]), pack2bf(c[2], c[3])) : make_uint2(0, 0);
+                        *reinterpret_cast<uint2*>(dyw + (rr * TW + ww + 1) * DYP + c4 * 8) = in ? c : make_uint2(0, 0);
                     };
                     put(h, w, c00);
                     put(h, w + 1, c01);

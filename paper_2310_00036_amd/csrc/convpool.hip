@@ -96,8 +96,11 @@ __global__ __launch_bounds__(64 * NW, (CpGeom<CIN, COUT, MODE>::WPS)) void conv_
                 const uint2 hi = *reinterpret_cast<const uint2*>(xb + boff[1]);
                 return make_uint4(lo.x, lo.y, hi.x, hi.y);
             }
+            // tap 8 and the next pixel (a finite value against zero weights; the window ends
+            // in a guard pixel)
             const uint2 t8 = *reinterpret_cast<const uint2*>(xb + boff[2]);
-            return make_uint4(t8.x, t8.y, t8.x, t8.y);
+            const uint2 t9 = *reinterpret_cast<const uint2*>(xb + boff[2] + 8);
+            return make_uint4(t8.x, t8.y, t9.x, t9.y);
         } else if constexpr (CIN < 32) {
             return *reinterpret_cast<const uint4*>(xb + boff[ks]);
         } else {   // from 32 channels a tap spans CIN / 32 k-steps; the lane's slot within it
@@ -177,30 +180,35 @@ __global__ __launch_bounds__(64 * NW, (CpGeom<CIN, COUT, MODE>::WPS)) void conv_
         }
 
         // ---- conv over window pixels p in [TW, (TH+1)*TW): output (image row hc0 + p/TW - 1,
-        // column p%TW - 1), tap (0,0) at window pixel p - TW - 1; its key at key-tile pixel p - TW
+        // column p%TW - 1), tap (0,0) at window pixel p - TW - 1; its key at key-tile pixel
+        // p - TW. The padding columns get keys too (of wrapped windows); they are zeroed after.
         {
             constexpr int STEP = NW / MT;               // column tiles between a wave's passes
-            const int S = 16 * STEP, dS = S % TW;       // pixels per pass, column advance
+            const int S = 16 * STEP;                    // pixels per pass
             const int pend = (TH + 1) * TW;
             int p = TW + (wave / MT) * 16 + r16;
-            int c = p - qdiv(p, t.inv_TW) * TW;
             const unsigned char* xb = win + (p - TW - 1) * PB;
             unsigned char* kp = keys + (p - TW) * KPB + co0 * 2;
             for (int nt = wave / MT; nt * 16 < TH * TW; nt += STEP) {
                 cb_f32x4 acc = cb_f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int ks = 0; ks < KSTEPS; ++ks) acc = PrecBF16::mma(wr[ks], bfrag(xb, ks), acc);
-                if (p < pend && c >= 1 && c <= W) {
+                if (p < pend) {
                     const uint32_t u0 = pack2bf(acc[0] * a.scale + bias[0], acc[1] * a.scale + bias[1]);
                     const uint32_t u1 = pack2bf(acc[2] * a.scale + bias[2], acc[3] * a.scale + bias[3]);
                     *reinterpret_cast<uint2*>(kp) = make_uint2(bf16x2_key(u0), bf16x2_key(u1));
                 }
                 p += S; xb += S * PB; kp += S * KPB;
-                c += dS;
-                if (c >= TW) c -= TW;
             }
         }
-        __syncthreads();   // the conv has read the window: the next tile's may land there
+        __syncthreads();   // the conv has read the window (the next tile's may land there) and
+                           // written the key tile
+        // the key tile's padding columns back to zero keys (below every value)
+        for (int j = tid; j < TH * 2 * C8; j += NT) {
+            const int c8 = j % C8, e = j / C8, row = e >> 1;
+            *reinterpret_cast<uint4*>(keys + (row * TW + (e & 1) * (TW - 1)) * KPB + c8 * 16) = make_uint4(0, 0, 0, 0);
+        }
+        __syncthreads();
 
         // ---- next tile's window, then the 3x3 stride-2 max-pool of the key tile, 8 channels per
         // item. The window and the key tile are restrict parameters of one call, so the compiler
@@ -294,7 +302,7 @@ hipError_t cp_launch(const ConvArgs& a, hipStream_t s) {
     const size_t L = layout(PTH, t);
     t.PTH = PTH; t.nbands = (OH + PTH - 1) / PTH; t.ntiles = t.nbands * a.n;
     t.OH = OH; t.OW = OW; t.ph = ph; t.pw = pw; t.THmax = thmax(PTH);
-    t.inv_OW = 1.f / float(OW); t.inv_TW = 1.f / float(TW);
+    t.inv_OW = 1.f / float(OW);
     const void* fn = reinterpret_cast<const void*>(&conv_pool_kernel<CIN, COUT, MODE, kCpWaves>);
     int gx = std::max(1, resident_blocks(fn, 64 * kCpWaves, L));
     if (gx > t.ntiles) gx = t.ntiles;

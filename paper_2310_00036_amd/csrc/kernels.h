@@ -39,7 +39,7 @@ hipError_t conv3x3_pool(int cin, int cout, int mode, const ConvArgs& a, hipStrea
 struct CpTile {
     int PTH, nbands, ntiles, OH, OW, ph, pw, THmax;
     int raw_off, win_off, win_guard, key_off;   // LDS layout (bytes)
-    float inv_OW, inv_TW;
+    float inv_OW;
 };
 bool conv_pool_fast_supported(int cin, int cout, int mode);
 hipError_t conv_pool_fast(int cin, int cout, int mode, const ConvArgs& a, hipStream_t s);

@@ -158,49 +158,48 @@ __global__ __launch_bounds__(64 * NW, 4) void pool_wgrad_u8_kernel(PoolWgArgs a,
                 const int c8 = it % CG, blk = it / CG;
                 const int bi = blk / t.BW, j = blk - bi * t.BW;
                 // windows (bi-1+u, j-1+v) at LDS rows bi+u, columns j+v
-                uint32_t ka[4][2];
-                float v[4][8];
+                uint32_t ka[4][2], s01[4][2], s23[4][2];
+                uint4 dv[4];
 #pragma unroll
                 for (int w4 = 0; w4 < 4; ++w4) {
                     const int px = (bi + (w4 >> 1)) * PW2 + j + (w4 & 1);
                     const uint2 k8 = *reinterpret_cast<const uint2*>(agl + px * CO + c8 * 8);
                     ka[w4][0] = k8.x; ka[w4][1] = k8.y;
-                    const uint4 d8 = *reinterpret_cast<const uint4*>(dpl + (px * CO + c8 * 8) * 2);
-                    const uint32_t d[4] = {d8.x, d8.y, d8.z, d8.w};
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        v[w4][2 * e] = __uint_as_float(d[e] << 16);
-                        v[w4][2 * e + 1] = __uint_as_float(d[e] & 0xffff0000u);
+                    for (int wd = 0; wd < 2; ++wd) { s01[w4][wd] = arg_sel01(ka[w4][wd]); s23[w4][wd] = arg_sel23(ka[w4][wd]); }
+                    dv[w4] = *reinterpret_cast<const uint4*>(dpl + (px * CO + c8 * 8) * 2);
+                }
+                // window w4's gradients of channels 4wd .. 4wd+3 where its cell is T, else +0
+#define CB_PICK(T, w4, wd) \
+    arg_pick<T>((wd) ? make_uint2(dv[w4].z, dv[w4].w) : make_uint2(dv[w4].x, dv[w4].y), ka[w4][wd], s01[w4][wd], s23[w4][wd])
+                // each cell adds its windows in (oh, ow) order; the lower-right cell has one
+                // window, whose bf16 gradient it keeps as it is
+                uint32_t c00[4], c01[4], c10[4], c11[4];
+#pragma unroll
+                for (int wd = 0; wd < 2; ++wd) {
+                    const uint2 a0 = CB_PICK(8, 0, wd), a1 = CB_PICK(6, 1, wd), a2 = CB_PICK(2, 2, wd), a3 = CB_PICK(0, 3, wd);
+                    const uint2 b1 = CB_PICK(7, 1, wd), b3 = CB_PICK(1, 3, wd);
+                    const uint2 e2 = CB_PICK(5, 2, wd), e3 = CB_PICK(3, 3, wd);
+                    const uint2 f3 = CB_PICK(4, 3, wd);
+                    const uint32_t A0[2] = {a0.x, a0.y}, A1[2] = {a1.x, a1.y}, A2[2] = {a2.x, a2.y}, A3[2] = {a3.x, a3.y};
+                    const uint32_t B1[2] = {b1.x, b1.y}, B3[2] = {b3.x, b3.y}, E2[2] = {e2.x, e2.y}, E3[2] = {e3.x, e3.y};
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        c00[2 * wd + h] = pack2bf(bf_lo(A0[h]) + bf_lo(A1[h]) + bf_lo(A2[h]) + bf_lo(A3[h]),
+                                                  bf_hi(A0[h]) + bf_hi(A1[h]) + bf_hi(A2[h]) + bf_hi(A3[h]));
+                        c01[2 * wd + h] = pack2bf(bf_lo(B1[h]) + bf_lo(B3[h]), bf_hi(B1[h]) + bf_hi(B3[h]));
+                        c10[2 * wd + h] = pack2bf(bf_lo(E2[h]) + bf_lo(E3[h]), bf_hi(E2[h]) + bf_hi(E3[h]));
                     }
+                    c11[2 * wd] = f3.x; c11[2 * wd + 1] = f3.y;
                 }
-                float c00[8], c01[8], c10[8], c11[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    uint32_t k[4];
-#pragma unroll
-                    for (int w4 = 0; w4 < 4; ++w4) k[w4] = (ka[w4][e >> 2] >> (8 * (e & 3))) & 0xffu;
-                    // each cell adds its windows in (oh, ow) order
-                    float s00 = 0.f, s01 = 0.f, s10 = 0.f, s11 = 0.f;
-                    s00 += k[0] == 8 ? v[0][e] : 0.f;
-                    s00 += k[1] == 6 ? v[1][e] : 0.f;
-                    s00 += k[2] == 2 ? v[2][e] : 0.f;
-                    s00 += k[3] == 0 ? v[3][e] : 0.f;
-                    s01 += k[1] == 7 ? v[1][e] : 0.f;
-                    s01 += k[3] == 1 ? v[3][e] : 0.f;
-                    s10 += k[2] == 5 ? v[2][e] : 0.f;
-                    s10 += k[3] == 3 ? v[3][e] : 0.f;
-                    s11 += k[3] == 4 ? v[3][e] : 0.f;
-                    c00[e] = s00; c01[e] = s01; c10[e] = s10; c11[e] = s11;
-                }
+#undef CB_PICK
                 // cells (2bi + a, 2j + b) in padded coordinates -> dC row 2bi + a, window column
                 // 2j + b - pw + 1; cells off the frame hold zero
                 const int h = 2 * (i0 + bi) - t.ph, w = 2 * j - t.pw;
                 const bool r0 = h >= 0 && h < a.H, r1 = h + 1 < a.H, q0 = w >= 0, q1 = w + 1 < W;
                 unsigned char* cp = dcl + ((2 * bi) * TW + w + 1) * DPB + c8 * 16;
-                auto put = [&](unsigned char* p, bool ok, const float* c) {
-                    *reinterpret_cast<uint4*>(p) = ok ? make_uint4(pack2bf(c[0], c[1]), pack2bf(c[2], c[3]),
-                                                                   pack2bf(c[4], c[5]), pack2bf(c[6], c[7]))
-                                                      : make_uint4(0, 0, 0, 0);
+                auto put = [&](unsigned char* p, bool ok, const uint32_t* c) {
+                    *reinterpret_cast<uint4*>(p) = ok ? make_uint4(c[0], c[1], c[2], c[3]) : make_uint4(0, 0, 0, 0);
                 };
                 put(cp, r0 && q0, c00);
                 put(cp + DPB, r0 && q1, c01);
