@@ -189,16 +189,35 @@ __global__ __launch_bounds__(64 * NW, (CpGeom<CIN, COUT, MODE>::WPS)) void conv_
             int p = TW + (wave / MT) * 16 + r16;
             const unsigned char* xb = win + (p - TW - 1) * PB;
             unsigned char* kp = keys + (p - TW) * KPB + co0 * 2;
-            for (int nt = wave / MT; nt * 16 < TH * TW; nt += STEP) {
-                cb_f32x4 acc = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+            auto put = [&](const cb_f32x4& acc, unsigned char* k) {
+                const uint32_t u0 = pack2bf(acc[0] * a.scale + bias[0], acc[1] * a.scale + bias[1]);
+                const uint32_t u1 = pack2bf(acc[2] * a.scale + bias[2], acc[3] * a.scale + bias[3]);
+                *reinterpret_cast<uint2*>(k) = make_uint2(bf16x2_key(u0), bf16x2_key(u1));
+            };
+            if constexpr (U8) {
+                // two column tiles per pass, so that each one's fragment reads and MFMAs overlap
+                // the other's (a missing second tile repeats the first and is not stored)
+                for (int nt = wave / MT; nt * 16 < TH * TW; nt += 2 * STEP) {
+                    const bool two = (nt + STEP) * 16 < TH * TW;
+                    const unsigned char* xb2 = two ? xb + S * PB : xb;
+                    cb_f32x4 acc = cb_f32x4{0.f, 0.f, 0.f, 0.f}, acc2 = acc;
 #pragma unroll
-                for (int ks = 0; ks < KSTEPS; ++ks) acc = PrecBF16::mma(wr[ks], bfrag(xb, ks), acc);
-                if (p < pend) {
-                    const uint32_t u0 = pack2bf(acc[0] * a.scale + bias[0], acc[1] * a.scale + bias[1]);
-                    const uint32_t u1 = pack2bf(acc[2] * a.scale + bias[2], acc[3] * a.scale + bias[3]);
-                    *reinterpret_cast<uint2*>(kp) = make_uint2(bf16x2_key(u0), bf16x2_key(u1));
+                    for (int ks = 0; ks < KSTEPS; ++ks) {
+                        acc = PrecBF16::mma(wr[ks], bfrag(xb, ks), acc);
+                        acc2 = PrecBF16::mma(wr[ks], bfrag(xb2, ks), acc2);
+                    }
+                    if (p < pend) put(acc, kp);
+                    if (two && p + S < pend) put(acc2, kp + S * KPB);
+                    p += 2 * S; xb += 2 * S * PB; kp += 2 * S * KPB;
                 }
-                p += S; xb += S * PB; kp += S * KPB;
+            } else {
+                for (int nt = wave / MT; nt * 16 < TH * TW; nt += STEP) {
+                    cb_f32x4 acc = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int ks = 0; ks < KSTEPS; ++ks) acc = PrecBF16::mma(wr[ks], bfrag(xb, ks), acc);
+                    if (p < pend) put(acc, kp);
+                    p += S; xb += S * PB; kp += S * KPB;
+                }
             }
         }
         __syncthreads();   // the conv has read the window (the next tile's may land there) and
