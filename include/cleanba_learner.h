@@ -31,6 +31,11 @@
  *             calling thread. Non-finite numbers propagate; adam_step flags them.
  * Determinism No floating-point atomics: every reduction runs in a fixed order, so a
  *             call repeated on the same inputs returns bit-identical outputs.
+ * Threads     Calls may run concurrently from several host threads on different streams
+ *             when their workspaces and outputs are distinct (the actor-learner pipeline
+ *             does this); the library keeps no state between calls besides a per-device
+ *             occupancy cache and adam_step_noalloc's buffer. The per-launch profiler of
+ *             cleanba_profile.h is the exception: one host thread.
  */
 #ifndef CLEANBA_LEARNER_H
 #define CLEANBA_LEARNER_H
