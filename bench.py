@@ -552,6 +552,26 @@ def hbm_sweep(P, reps=20):
     return out
 
 
+def mfma_loop_peak(P, reps=5):
+    """The achievable bf16 matrix-core rate of this device: impala_probe_mfma_bf16 (register-only
+    loops of independent MFMAs, four 4-wave workgroups per CU), timed with HIP events."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks, iters = 4 * cus, 4096
+    sink = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    flop = P.impala_probe_mfma_bf16(blocks, iters, sink)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        P.impala_probe_mfma_bf16(blocks, iters, sink)
+    e1.record()
+    torch.cuda.synchronize()
+    tf = flop / (e0.elapsed_time(e1) / 1e3 / reps) / 1e12
+    return {"achieved": round(tf, 1), "unit": "TFLOP/s", "published": PEAK["bf16"][0],
+            "frac_of_published": round(tf / PEAK["bf16"][0], 4), "blocks": blocks, "iters": iters}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -575,6 +595,9 @@ def main():
     head = time_learner(P, wl, args.prec, args.steps, args.warmup)
     rl = head["roofline"]
     rl["traffic"] = traffic_for(rl["kernel"], head["dominant_n"])
+    loop_peak = mfma_loop_peak(P)
+    if rl.get("bound") == "mfma" and args.prec == "bf16":
+        rl["frac_of_loop_peak"] = round(rl["achieved"] / loop_peak["achieved"], 4)
     line = {
         "metric": "learner frames/sec (fwd+bwd+loss+Adam), IMPALA-CNN; % MFMA peak",
         "value": round(head["value"], 1),
@@ -595,6 +618,7 @@ def main():
                    "net": f"{net.ch}/{net.hidden}/A{net.num_actions}", "optimizer": wl.optimizer,
                    "rollout_frames_per_s": round(head["rollout_fps"], 1), "wall_s": round(head["wall"], 3)},
         "roofline": rl,
+        "mfma_loop_peak": loop_peak,
         "kernels_top": head["kernels"][:args.kernels],
     }
     if args.extras:

@@ -38,6 +38,15 @@ impala_status_t impala_profile_key(int32_t i, char* key, size_t key_cap, double*
 /* Launches that were not recorded because max_launches was reached in the last profile. */
 int32_t impala_profile_dropped(void);
 
+/* The achievable matrix-core rate, for reporting kernels against it beside the published
+ * dense peak: `blocks` workgroups of 4 waves, each wave `iters` rounds of 8 independent
+ * v_mfma_f32_16x16x32_bf16 on operands held in registers (no memory traffic in the loop).
+ * sink: device float32 [blocks * 256], written with one checksum per thread. *flop receives
+ * the matrix-core flop of the launch (2 per multiply-add). 1 <= blocks <= 65536,
+ * 1 <= iters <= 1<<20; the caller times the launch (for example with HIP events). */
+impala_status_t impala_probe_mfma_bf16(int32_t blocks, int32_t iters, float* sink, int64_t* flop,
+                                       hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

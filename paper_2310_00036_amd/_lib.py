@@ -106,6 +106,7 @@ _SIGS = {
     "impala_profile_end": (C.c_int, []),
     "impala_profile_key": (C.c_int, [_I32, C.c_char_p, _SZ, C.POINTER(C.c_double), C.POINTER(_I32)]),
     "impala_profile_dropped": (_I32, []),
+    "impala_probe_mfma_bf16": (C.c_int, [_I32, _I32, _P, C.POINTER(_I64), _P]),
 }
 
 
@@ -409,6 +410,14 @@ def impala_gumbel_sample(n, A, logits, gumbel, actions, logp, stream=None):
 def impala_action_logp(n, A, logits, actions, logp, stream=None):
     _check("impala_action_logp", lib.impala_action_logp(n, A, ptr(logits), ptr(actions), ptr(logp),
                                                         stream_handle(stream)))
+
+
+def impala_probe_mfma_bf16(blocks, iters, sink, stream=None) -> int:
+    """Launch the register-only MFMA loop (cleanba_profile.h); returns its matrix-core flop."""
+    flop = C.c_int64()
+    _check("impala_probe_mfma_bf16", lib.impala_probe_mfma_bf16(blocks, iters, ptr(sink), C.byref(flop),
+                                                                stream_handle(stream)))
+    return flop.value
 
 
 def impala_profile_begin(only_key: str | None = None, max_launches: int = 1 << 16) -> None:

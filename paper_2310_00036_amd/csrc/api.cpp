@@ -10,6 +10,7 @@
 
 #include "../../include/cleanba_layers.h"
 #include "../../include/cleanba_learner.h"
+#include "../../include/cleanba_profile.h"
 #include "kernels.h"
 #include "plan.h"
 
@@ -828,6 +829,15 @@ impala_status_t impala_gumbel_sample(int64_t n, int32_t A, const float* logits, 
     if (n == 0) return ok();
     CHECK_PTR(logits); CHECK_PTR(gumbel); CHECK_PTR(actions); CHECK_PTR(logp);
     return hip_status(gumbel_max(n, A, logits, gumbel, actions, logp, stream), "impala_gumbel_sample");
+}
+
+impala_status_t impala_probe_mfma_bf16(int32_t blocks, int32_t iters, float* sink, int64_t* flop,
+                                       hipStream_t stream) {
+    if (blocks < 1 || blocks > 65536 || iters < 1 || iters > (1 << 20))
+        return fail(IMPALA_EINVAL, "impala_probe_mfma_bf16: bad blocks or iters");
+    CHECK_PTR(sink); CHECK_PTR(flop);
+    *flop = mfma_probe_flop(blocks, iters);
+    return hip_status(mfma_probe(blocks, iters, sink, stream), "impala_probe_mfma_bf16");
 }
 
 }  // extern "C"

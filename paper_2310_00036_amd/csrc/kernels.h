@@ -281,4 +281,9 @@ size_t lds_limit();
 // resident at once on the whole current device; sizes persistent grids (cached).
 int resident_blocks(const void* fn, int threads, size_t lds);
 
+// ---- achievable MFMA throughput: `blocks` workgroups of 4 waves, each wave `iters` rounds of
+// 8 independent 16x16x32 bf16 MFMAs on register operands; one float per thread to `sink`
+hipError_t mfma_probe(int blocks, int iters, float* sink, hipStream_t s);
+int64_t mfma_probe_flop(int blocks, int iters);
+
 }  // namespace cb

@@ -16,7 +16,7 @@ from synth import NetShape, WORKLOADS  # noqa: E402
 
 def _declared_functions():
     names = set()
-    for h in ("cleanba_learner.h", "cleanba_layers.h"):
+    for h in ("cleanba_learner.h", "cleanba_layers.h", "cleanba_profile.h"):
         src = open(os.path.join(ROOT, "include", h)).read()
         src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
         for m in re.finditer(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\*?\s*([a-z_][a-z0-9_]*)\s*\(",
@@ -190,3 +190,17 @@ def test_noalloc_adam_validates_before_hip():
     assert lib.adam_step_noalloc(10, 1, 1, 1, 1, 1, 1e-3, 1.0, 0.999, 1e-5, 0.5, None, None) == -1
     assert lib.adam_step_noalloc(10, None, 1, 1, 1, 1, 1e-3, 0.9, 0.999, 1e-5, 0.5, None, None) == -1
     assert lib.adam_step_noalloc(0, None, None, None, None, 1, 1e-3, 0.9, 0.999, 1e-5, 0.5, None, None) == 0
+
+
+def test_mfma_probe_validates_before_hip():
+    """impala_probe_mfma_bf16 rejects bad sizes and NULL pointers on the host (no launch)."""
+    lib = P.lib
+    flop = C.c_int64()
+    fake = C.c_void_p(16)   # never dereferenced: every call below fails validation first
+    assert lib.impala_probe_mfma_bf16(0, 1, fake, C.byref(flop), None) == -1
+    assert lib.impala_probe_mfma_bf16(1, 0, fake, C.byref(flop), None) == -1
+    assert lib.impala_probe_mfma_bf16(65537, 1, fake, C.byref(flop), None) == -1
+    assert lib.impala_probe_mfma_bf16(1, (1 << 20) + 1, fake, C.byref(flop), None) == -1
+    assert lib.impala_probe_mfma_bf16(1, 1, None, C.byref(flop), None) == -1
+    assert lib.impala_probe_mfma_bf16(1, 1, fake, None, None) == -1
+    assert b"NULL" in lib.impala_last_error()

@@ -716,3 +716,30 @@ def test_gumbel_sample_bit_exact(n, A):
     G.sync()
     np.testing.assert_array_equal(act.cpu().numpy(), a_w)
     G.assert_close(G.host(lp), olosses.log_softmax(z.astype(np.float64))[np.arange(n), a_w], 1e-5, "logp")
+
+
+def test_mfma_probe_runs_its_matrix_products():
+    """The matrix-core probe does the MFMAs it counts: every thread's checksum equals the sum,
+    written out, of its lane's accumulator rows (16x16x32 products of the per-lane bf16
+    operands it builds, exact in float32), and two launches agree bit for bit."""
+    import torch
+    blocks, iters = 8, 16
+    sink = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    flop = P.impala_probe_mfma_bf16(blocks, iters, sink)
+    assert flop == blocks * 4 * iters * 8 * (16 * 16 * 32 * 2)
+    G.sync()
+    first = sink.cpu().numpy().copy()
+    P.impala_probe_mfma_bf16(blocks, iters, sink)
+    G.sync()
+    np.testing.assert_array_equal(first, sink.cpu().numpy())
+    # A[i][8g+m] = x[i+16g] (m even) or 1, B[8g+m][n] = y[n+16g] (m even) or 0.5, lane l
+    # supplying row / column l % 16 for k = 8(l // 16) .. +7 and receiving rows 4(l // 16) .. +3
+    x = 1.0 + np.arange(64) / 128.0
+    y = 1.0 - np.arange(64) / 256.0
+    D = np.zeros((16, 16))
+    for g in range(4):
+        D += 4.0 * np.outer(x[16 * g:16 * g + 16], y[16 * g:16 * g + 16]) + 2.0
+    lane = np.arange(256) % 64
+    want = np.array([8 * iters * D[4 * (l // 16):4 * (l // 16) + 4, l % 16].sum() for l in lane])
+    # the MFMA sums are exact (15 fractional bits, below 2^9); the 32-term float32 checksum rounds
+    np.testing.assert_allclose(first.reshape(blocks, 256), np.broadcast_to(want, (blocks, 256)), rtol=1e-5)
