@@ -132,6 +132,10 @@ CB_DEV void dma16_to_lds(__amdgpu_buffer_rsrc_t r, unsigned char* lds, uint32_t 
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_t*)(lds), 16, off, 0, 0, 0);
 }
 
+// Workgroup barrier that waits for this wave's LDS operations only: buffer -> LDS loads
+// staging a later tile (and global stores) stay in flight across it.
+CB_DEV void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // Order-preserving 16-bit keys of two packed bf16 values: as unsigned integers the keys
 // compare like the values (-0 sorts just below +0; NaNs sort beyond the infinities).
 // A negative half is complemented, a positive one has its sign bit set; the sign masks come

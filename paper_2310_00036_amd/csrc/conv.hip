@@ -290,6 +290,7 @@ struct DmaTile {
     // fused max-pool: PTH pooled rows per band, pooled size OH x OW, pads ph/pw, conv tile
     int PTH, OH, OW, ph, pw, ct_off, zero_off;   // zero_off: 16 zero bytes
     float inv_OW, inv_ppf;   // 1/OW, 1/(OH*OW)
+    int buf_off;             // double-buffered tiles: LDS byte offset of the second buffer
 };
 
 template <int CIN, int COUT, int MODE>
@@ -664,6 +665,251 @@ __global__ __launch_bounds__(64 * NW, (conv_min_waves<CIN, COUT, MODE>())) void 
     }
 }
 
+// ------------------------------------------------------------------ register-weight kernel
+//
+// 64 output channels from 32 or 64 bf16 input channels (the wide net's residual convolutions
+// and their input gradients). Their weight tile (up to 72 KB) leaves room for one window per
+// workgroup beside it, and read from LDS it costs an A-fragment read for every MFMA pair.
+// Here the 8 waves of a workgroup split the output channels in two halves and each wave holds
+// its half's A fragments in registers for the whole launch (2 x 18 x 4 = 144 registers at 64
+// input channels), so every B-fragment read feeds two MFMAs and LDS holds only tiles. One
+// workgroup per CU double-buffers them: the next tile's window and epilogue operands are
+// staged by buffer -> LDS loads while this tile's MFMAs run. (Two workgroups per CU with one
+// buffer each fall into step, staging together and computing together, so their phases add
+// up instead of overlapping.) Tile shapes, window layout and epilogue are those of
+// conv3x3_bf16_kernel.
+constexpr int kRegwWaves = 8;
+constexpr int kRegwMaxW = 10, kRegwMaxQ = 4;   // staging slots per lane: window, operands
+
+// Epilogue operand tiles hold per output pixel q its 8 slots of 8 channels, slot c of pixel q
+// at position c ^ ((q >> 1) & 7): the 8-byte reads of 16 consecutive pixels' same channels
+// then fall on distinct bank quadruples (pixel q starts 32 q (mod 64) banks in, plus 4 x its
+// position), where unswizzled every pixel pair 2 apart would share them.
+CB_DEV int op_slot(int q, int c) { return c ^ ((q >> 1) & 7); }
+
+// Window layout of these tiles. gfx950's LDS serves a 16-byte read of a wave in four passes of
+// 16 lanes, each pass conflict-free when its reads land on distinct 16-byte bank groups (64
+// four-byte banks). A B fragment is 16 consecutive output pixels (one 16-byte slot each) of
+// two adjacent lane groups; a pixel pitch of P slots spreads such a pass over distinct groups
+// when P = 2 (mod 4), so a pixel holds CIN/8 data slots plus two zero slots (10 or 6). A run
+// of pixels that wraps to the next row jumps over the two padding columns; extra slots at the
+// end of every row (row pitch = W*P (mod 16) slots) keep the wrapped run's groups as they would
+// be without the jump.
+template <int CIN>
+struct RegwGeom {
+    static constexpr int SPP = CIN / 8 + 2;   // 16-byte slots per window pixel
+    static constexpr int PB = SPP * 16;
+    static_assert(SPP % 4 == 2, "pixel pitch = 2 (mod 4) slots");
+    __host__ __device__ static int row_slots(int W) {
+        const int base = (W + 2) * SPP;
+        return base + ((W * SPP - base) % 16 + 16) % 16;
+    }
+    __host__ __device__ static int win_bytes(int TH, int FR, int W) {
+        return (FR * (TH + 2) * row_slots(W) + 63) / 64 * 1024;
+    }
+};
+
+template <int CIN, int COUT, int MODE, int FLIP>
+__global__ __launch_bounds__(64 * kRegwWaves, 2) void conv3x3_regw_kernel(ConvArgs a, DmaTile t) {
+    using D = DmaGeom<CIN, COUT, MODE>;
+    using G = ConvGeom<PrecBF16, CIN>;
+    using P = PrecBF16;
+    constexpr int NW = kRegwWaves, NT = 64 * NW;
+    constexpr int KSTEPS = G::KSTEPS, KPITCH = G::KPITCH, MT = COUT / 16;
+    using R = RegwGeom<CIN>;
+    constexpr int SPP = R::SPP, PB = R::PB, OCH = D::OCH;
+    constexpr int OS = 2, MTW = MT / OS, NWC = NW / OS;   // output halves, waves per half
+    constexpr int TPK = CIN / 32;                         // k-steps per tap
+    constexpr int KPD = 6;                                // B fragments read ahead of their MFMAs
+    static_assert(MODE != IN_U8 && CIN % 32 == 0 && MT % OS == 0 && G::KP == G::K && OCH == 8,
+                  "bf16 inputs in 32-channel multiples (k-steps never straddle a tap)");
+
+    extern __shared__ __align__(16) unsigned char smem[];
+    uint16_t* wl = reinterpret_cast<uint16_t*>(smem);   // weight loading area, then the tiles
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, r16 = lane & 15;
+    const int og = blockIdx.y * COUT;
+    const int mt0 = (wave % OS) * MTW;   // the wave's first 16-channel output block
+    const int H = a.H, W = a.W, TH = t.TH, FR = t.FR;
+    const int TR = TH + 2;
+    const int RS = R::row_slots(W), RB = RS * 16;        // window row pitch (slots, bytes)
+    const float inv_RS = 1.f / float(RS);
+    const bool has_mask = a.mask != nullptr, has_add = a.add != nullptr;
+
+    // ---- weights -> LDS as wl[o][tap*CIN + i] (bf16) -> this wave's A fragments
+    if (FLIP) {
+        for (int e = tid; e < 9 * COUT * CIN; e += NT) {
+            const int i = e % CIN, o = (e / CIN) % COUT, tap = e / (CIN * COUT);
+            wl[o * KPITCH + (8 - tap) * CIN + i] = P::store(a.w[(int64_t(tap) * t.cout_total + og + o) * CIN + i]);
+        }
+    } else {
+        for (int e = tid; e < 9 * CIN * COUT; e += NT) {
+            const int o = e % COUT, k = e / COUT;
+            wl[o * KPITCH + k] = P::store(a.w[int64_t(k) * t.cout_total + og + o]);
+        }
+    }
+    float bias[MTW][4];
+#pragma unroll
+    for (int m = 0; m < MTW; ++m)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) bias[m][j] = a.bias ? a.bias[og + (mt0 + m) * 16 + g * 4 + j] : 0.f;
+    __syncthreads();
+    uint4 wreg[MTW * KSTEPS];
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks)
+#pragma unroll
+        for (int m = 0; m < MTW; ++m)
+            wreg[ks * MTW + m] = P::lds_frag(wl + ((mt0 + m) * 16 + r16) * KPITCH + ks * 32 + g * 8);
+    __syncthreads();   // every wave holds its fragments: the tiles may overwrite the weights
+
+    // ---- staging of a tile's zero-padded input window and epilogue operands into a buffer.
+    // A lane's slots are the same in every tile, so their source offsets are formed once,
+    // relative to the tile's first frame and row 0; a tile adds its first row h0. Window rows
+    // above the frame come out negative and wrap past the end of the buffer resource (one
+    // frame's bytes when bands split frames), as do rows below it, so they read zero; with
+    // several frames per tile (whole frames, h0 = 0) the padding rows are marked here, and
+    // frames past n lie beyond the resource. Padding columns and zero slots never load.
+    uint32_t woff[kRegwMaxW], qoff[kRegwMaxQ];
+#pragma unroll
+    for (int k = 0; k < kRegwMaxW; ++k) {
+        const int j = (wave + NW * k) * 64 + lane;
+        const int rowi = qdiv(j, inv_RS), rem = j - rowi * RS;
+        const int col = rem / SPP, c = rem - col * SPP;
+        const int f = qdiv(rowi, t.inv_TR), rr = rowi - f * TR;
+        const bool ok = j < FR * TR * RS && c < CIN / 8 && col >= 1 && col <= W && (FR == 1 || (rr >= 1 && rr <= H));
+        woff[k] = ok ? uint32_t(((f * H + rr - 1) * W + col - 1) * (CIN * 2) + c * 16) : kOOB;
+    }
+#pragma unroll
+    for (int k = 0; k < kRegwMaxQ; ++k) {
+        const int j = (wave + NW * k) * 64 + lane;
+        const int q = j / OCH, c = op_slot(q, j - q * OCH);
+        const int rowi = qdiv(q, t.inv_W), col = q - rowi * W;
+        const int f = qdiv(rowi, t.inv_TH), rr = rowi - f * TH;
+        qoff[k] = uint32_t(((f * H + rr) * W + col) * (t.cout_total * 2) + (og + c * 8) * 2);
+    }
+    auto stage = [&](unsigned char* dst, int tile) {
+        const int band = tile % t.nbands, fg = tile / t.nbands;
+        const int f0 = fg * FR, nf = a.n - f0 < FR ? a.n - f0 : FR;
+        const int h0 = band * TH, the = H - h0 < TH ? H - h0 : TH;
+        const uint32_t fb = uint32_t(H) * W * CIN * 2;
+        const auto rx = buf_rsrc(static_cast<const uint16_t*>(a.x) + int64_t(f0) * H * W * CIN, uint32_t(nf) * fb);
+        const uint32_t hx = uint32_t(h0) * W * CIN * 2;   // (kOOB + hx stays past every resource)
+        const int ns = FR * TR * RS;
+#pragma unroll
+        for (int k = 0; k < kRegwMaxW; ++k)
+            if ((wave + NW * k) * 64 < ns) dma16_to_lds(rx, dst + (wave + NW * k) * 1024, woff[k] + hx);
+        if (has_mask || has_add) {
+            const uint32_t ob = uint32_t(H) * W * t.cout_total * 2;
+            const int64_t fo = int64_t(f0) * H * W * t.cout_total;
+            const auto rm = buf_rsrc(has_mask ? static_cast<const uint16_t*>(a.mask) + fo : nullptr, has_mask ? uint32_t(nf) * ob : 0);
+            const auto ra = buf_rsrc(has_add ? static_cast<const uint16_t*>(a.add) + fo : nullptr, has_add ? uint32_t(nf) * ob : 0);
+            const uint32_t ho = uint32_t(h0) * W * t.cout_total * 2;
+            const int ns2 = nf * the * W * OCH;
+#pragma unroll
+            for (int k = 0; k < kRegwMaxQ; ++k) {
+                const int b = wave + NW * k;
+                if (b * 64 < ns2) {
+                    const uint32_t off = b * 64 + lane < ns2 ? qoff[k] + ho : kOOB;
+                    if (has_mask) dma16_to_lds(rm, dst + t.mask_off + b * 1024, off);
+                    if (has_add) dma16_to_lds(ra, dst + t.add_off + b * 1024, off);
+                }
+            }
+        }
+    };
+
+    // ---- one tile out of `cur` while the next one lands in `nxt`. The buffers are restrict
+    // parameters, so the compiler knows the loads in flight into nxt do not write what this
+    // tile reads and does not wait for them before its LDS reads.
+    auto run_tile = [&](unsigned char* __restrict__ cur, unsigned char* __restrict__ nxt, int tile) {
+        if (tile + int(gridDim.x) < t.ntiles) stage(nxt, tile + gridDim.x);
+        const int band = tile % t.nbands, fg = tile / t.nbands;
+        const int f0 = fg * FR, nf = a.n - f0 < FR ? a.n - f0 : FR;
+        const int h0 = band * TH, the = H - h0 < TH ? H - h0 : TH;
+        const int npx = nf * the * W;
+        uint16_t* ybase = static_cast<uint16_t*>(a.y) + (int64_t(f0) * H + h0) * W * t.cout_total + og;
+        if constexpr (MODE == IN_RELU) {
+            // (unrolled over the lane's slots, so their LDS reads are in flight together)
+            uint4* w4 = reinterpret_cast<uint4*>(cur);
+            const int ns = FR * TR * RS;
+#pragma unroll
+            for (int k = 0; k < kRegwMaxW; ++k) {
+                const int j = tid + NT * k;
+                if (j < ns) {
+                    uint4 v = w4[j];
+                    v.x = relu_bf16x2(v.x); v.y = relu_bf16x2(v.y); v.z = relu_bf16x2(v.z); v.w = relu_bf16x2(v.w);
+                    w4[j] = v;
+                }
+            }
+            lds_barrier();
+        }
+        const unsigned char* opm = cur + t.mask_off;
+        const unsigned char* opa = cur + t.add_off;
+        const int ntl = (npx + 15) >> 4;
+        for (int nt = wave / OS; nt < ntl; nt += NWC) {
+            const int q = nt * 16 + r16;   // past npx: clamped, computed, not stored
+            const int qc = q < npx ? q : npx - 1;
+            const int rowi = qdiv(qc, t.inv_W), col = qc - rowi * W;
+            int f = 0, r = rowi;
+            if (FR > 1) { f = qdiv(rowi, t.inv_TH); r = rowi - f * TH; }
+            const unsigned char* xb = cur + (f * TR + r) * RB + col * PB;
+            // k-step ks: tap ks / TPK (window pixel offset), channels (ks % TPK) * 32 + 8g
+            auto bfrag = [&](int ks) {
+                const int tap = ks / TPK;
+                return *reinterpret_cast<const uint4*>(xb + (tap / 3) * RB + (tap % 3) * PB + ((ks % TPK) * 4 + g) * 16);
+            };
+            cb_f32x4 acc[MTW];
+#pragma unroll
+            for (int m = 0; m < MTW; ++m) acc[m] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+            uint4 bq[KSTEPS];
+#pragma unroll
+            for (int ks = 0; ks < KPD && ks < KSTEPS; ++ks) bq[ks] = bfrag(ks);
+#pragma unroll
+            for (int ks = 0; ks < KSTEPS; ++ks) {
+                if (ks + KPD < KSTEPS) bq[ks + KPD] = bfrag(ks + KPD);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int m = 0; m < MTW; ++m) acc[m] = P::mma(wreg[ks * MTW + m], bq[ks], acc[m]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            if (q < npx) {
+                uint16_t* yp = ybase + ((uint32_t(f) * H + r) * W + col) * uint32_t(t.cout_total) + g * 4;
+                const int oq = q * OCH * 16 + (g & 1) * 8;
+#pragma unroll
+                for (int m = 0; m < MTW; ++m) {
+                    const int mt = mt0 + m;
+                    const int os = oq + op_slot(q, 2 * mt + (g >> 1)) * 16;   // channels mt*16 + 4g .. +3
+                    float v[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) v[j] = acc[m][j] * a.scale + bias[m][j];
+                    if (has_mask) {
+                        float mk[4];
+                        load4(reinterpret_cast<const uint16_t*>(opm + os), mk);
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) v[j] = mk[j] > 0.f ? v[j] : 0.f;
+                    }
+                    if (has_add) {
+                        float ad[4];
+                        load4(reinterpret_cast<const uint16_t*>(opa + os), ad);
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) v[j] += ad[j];
+                    }
+                    store4(yp + mt * 16, v[0], v[1], v[2], v[3]);
+                }
+            }
+        }
+    };
+
+    int lg = blockIdx.x;   // neighbouring tiles (which share halo rows) on one XCD
+    if ((gridDim.x & 7) == 0) lg = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+    if (lg < t.ntiles) stage(smem, lg);
+    int it = 0;
+    for (int tile = lg; tile < t.ntiles; tile += gridDim.x, ++it) {
+        __builtin_amdgcn_s_waitcnt(0);   // this wave's loads of the tile have landed in LDS
+        __syncthreads();                 // ... and everyone else's; the other buffer is free
+        run_tile(smem + (it & 1) * t.buf_off, smem + ((it + 1) & 1) * t.buf_off, tile);
+    }
+}
+
 // ------------------------------------------------------------------ launcher
 
 namespace {
@@ -739,8 +985,9 @@ constexpr int conv_group() {
 // stages the fewest window rows per frame; whole frames batch up to kDmaPixMax pixels.
 constexpr int kDmaLdsTarget = 40 * 1024;
 constexpr int kDmaPixMax = 2048;
-// Layers whose full weight tile is large (64 output channels from 32 or more inputs) keep all
-// output channels in one 8-wave workgroup per CU, with most of the CU's LDS: every staged
+// Layers whose full weight tile is large (here the input gradient of 32 -> 64, whose kernel
+// maps 64 channels to 32; 64 output channels go to conv3x3_regw_kernel) keep all output
+// channels in one 8-wave workgroup per CU, with most of the CU's LDS: every staged
 // window is read once and each weight fragment feeds two column tiles, where 16-channel
 // groups would stage each window once per group and feed one MFMA per fragment pair.
 constexpr int kDmaWideLdsTarget = 150 * 1024;
@@ -793,6 +1040,60 @@ hipError_t launch_bf16(const ConvArgs& a, int cout_total, hipStream_t s) {
                       cb_dims(CIN, cout_total) + "/" + cb_dims(H, W) + cb_flags(MODE, a.mask, a.add));
     });
     hipLaunchKernelGGL((conv3x3_bf16_kernel<CIN, COUT, MODE, FLIP, 0, NW>), grid, dim3(64 * NW), L, s, a, t);
+    return hipGetLastError();
+}
+
+// Register-weight tiles: two buffers per workgroup, each within half of the CU's LDS.
+template <int CIN, int COUT, int MODE>
+constexpr bool conv_regw() { return MODE != IN_U8 && COUT == 64 && CIN >= 32 && CIN % 32 == 0; }
+constexpr int kRegwBufTarget = 80 * 1024;
+
+template <int CIN, int COUT, int MODE, int FLIP>
+hipError_t launch_regw(const ConvArgs& a, int cout_total, hipStream_t s) {
+    using D = DmaGeom<CIN, COUT, MODE>;
+    const int H = a.H, W = a.W;
+    const int nops = (a.mask ? 1 : 0) + (a.add ? 1 : 0);
+    using R = RegwGeom<CIN>;
+    // (tiles whose staging slots exceed the per-lane offset registers count as too large)
+    auto buf = [&](int th, int fr) {
+        const bool fits = fr * (th + 2) * R::row_slots(W) <= kRegwMaxW * 64 * kRegwWaves &&
+                          fr * th * W * D::OCH <= kRegwMaxQ * 64 * kRegwWaves;
+        return fits ? size_t(R::win_bytes(th, fr, W)) + size_t(nops) * D::op_bytes(th, fr, W) : size_t(1) << 30;
+    };
+    int thmax = std::min(H, std::max(1, kDmaPixMax / W));
+    while (thmax > 1 && buf(thmax, 1) > size_t(kRegwBufTarget)) --thmax;
+    if (buf(thmax, 1) > size_t(kRegwBufTarget)) return hipErrorInvalidValue;
+    int TH = 1, best = 1 << 30;   // fewest staged window rows per frame
+    for (int th = 1; th <= thmax; ++th) {
+        const int rows = (H + th - 1) / th * (th + 2);
+        if (rows <= best) { best = rows; TH = th; }
+    }
+    const int nbands = (H + TH - 1) / TH;
+    int FR = 1;
+    if (nbands == 1)
+        while (FR < a.n && buf(TH, FR + 1) <= size_t(kRegwBufTarget) && (FR + 1) * H * W <= kDmaPixMax) ++FR;
+    // 32-bit buffer offsets cover FR frames of input and of each operand
+    if (int64_t(FR) * H * W * std::max(CIN, cout_total) * 2 >= (int64_t(1) << 31)) return hipErrorInvalidValue;
+    DmaTile t{};
+    t.TH = TH; t.FR = FR; t.nbands = nbands; t.ntiles = nbands * ((a.n + FR - 1) / FR); t.cout_total = cout_total;
+    t.win_off = 0;
+    t.mask_off = R::win_bytes(TH, FR, W);
+    t.add_off = t.mask_off + (a.mask ? D::op_bytes(TH, FR, W) : 0);
+    t.buf_off = int(buf(TH, FR));
+    t.inv_W = 1.f / float(W); t.inv_TW = 1.f / float(W + 2);
+    t.inv_TH = 1.f / float(TH); t.inv_TR = 1.f / float(TH + 2);
+    const size_t L = std::max(size_t(D::WLB), 2 * buf(TH, FR));
+    if (L > std::min<size_t>(lds_limit(), 160 * 1024)) return hipErrorInvalidValue;
+    const int groups = cout_total / COUT;
+    const void* fn = reinterpret_cast<const void*>(&conv3x3_regw_kernel<CIN, COUT, MODE, FLIP>);
+    int gx = std::max(1, resident_blocks(fn, 64 * kRegwWaves, L) / groups);
+    if (gx > t.ntiles) gx = t.ntiles;
+    const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(groups));
+    ProfScope ps(s, [&] {
+        return cb_key(FLIP ? "conv_dgrad" : "conv_fwd", 0,
+                      cb_dims(CIN, cout_total) + "/" + cb_dims(H, W) + cb_flags(MODE, a.mask, a.add));
+    });
+    hipLaunchKernelGGL((conv3x3_regw_kernel<CIN, COUT, MODE, FLIP>), grid, dim3(64 * kRegwWaves), L, s, a, t);
     return hipGetLastError();
 }
 
@@ -857,7 +1158,9 @@ hipError_t launch_bf16_pool(const ConvArgs& a, int cout_total, hipStream_t s) {
 
 template <class P, int CIN, int COUT, int MODE, int FLIP>
 hipError_t launch_split(const ConvArgs& a, hipStream_t s) {
-    if constexpr (std::is_same_v<P, PrecBF16>)
+    if constexpr (std::is_same_v<P, PrecBF16> && conv_regw<CIN, COUT, MODE>())
+        return launch_regw<CIN, COUT, MODE, FLIP>(a, COUT, s);
+    else if constexpr (std::is_same_v<P, PrecBF16>)
         return launch_bf16<CIN, COUT, MODE, FLIP>(a, COUT, s);   // all output channels per workgroup
     else
         return launch<P, CIN, conv_group<P, CIN, COUT>(), MODE, FLIP>(a, COUT, s);

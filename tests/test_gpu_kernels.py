@@ -202,6 +202,30 @@ def test_resblock_rejects_unsupported():
                               G.empty_act((1, 8, 8, 16), G.FP32))
 
 
+@pytest.mark.parametrize("case", [(1024, 21, 21, 64, 64, 1), (1024, 21, 21, 64, 64, 0), (1027, 11, 11, 64, 64, 1),
+                                  (1026, 11, 11, 64, 64, 0), (300, 42, 42, 32, 64, 0)],
+                         ids=lambda c: "n%d_%dx%d_%d-%d_add%d" % c)
+def test_conv_forward_many_tiles_per_workgroup(case):
+    """bf16 forward conv at frame counts where every workgroup of the persistent grid runs many
+    tiles (the wide net's 64-channel residual convs, relu(x) in, with and without the residual
+    add; several frames per tile at 11x11 with a ragged last tile), checked on frames spread
+    over the launch."""
+    n, H, W, cin, cout, with_add = case
+    mode = P.X_RELU if cin == cout else P.X_PLAIN
+    fs = np.asarray([0, 1, n // 2 + 5, n - 2, n - 1])
+    x, rows, xin, w, b = _conv_inputs(n, H, W, cin, cout, mode, G.BF16, 17)
+    wq = G.q(w, G.BF16)
+    add = G.q(np.random.default_rng(6).standard_normal((n, H, W, cout)), G.BF16) if with_add else None
+    want = onet.conv3x3(xin[fs], wq, b.astype(np.float64)) + (add[fs] if with_add else 0)
+    absum = onet.conv3x3(np.abs(xin[fs]), np.abs(wq), np.abs(b).astype(np.float64)) + \
+        (np.abs(add[fs]) if with_add else 0)
+    y = G.empty_act((n, H, W, cout), G.BF16)
+    P.impala_conv3x3_fwd(G.BF16, n, H, W, cin, cout, G.dev_act(x, G.BF16), mode, None, G.dev_f32(w),
+                         G.dev_f32(b), G.dev_act(add, G.BF16) if with_add else None, y)
+    G.sync()
+    G.assert_bf16_ulp(G.host(y)[fs], want, absum, "conv fwd (many tiles)")
+
+
 DGRAD_CASES = [(3, 42, 42, 16, 16), (3, 42, 42, 16, 32), (4, 21, 21, 32, 32), (7, 11, 11, 32, 32),
                (2, 42, 42, 32, 64), (3, 21, 21, 64, 64), (2, 17, 23, 16, 64)]
 
