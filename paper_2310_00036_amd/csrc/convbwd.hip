@@ -15,10 +15,9 @@
 // the partials in a fixed order (deterministic, no atomics).
 //
 // Layouts in LDS:
-//   - dy window [FR][TH+2][W+2] pixels of CO/8 16-byte slots plus one zero slot: the input
-//     gradient reads 8 consecutive channels of one tap per lane (16 bytes) as its B
-//     fragment, an odd slot count spreads the 16 lanes over distinct banks, and the zero
-//     slot feeds the k-steps past the 9 taps;
+//   - dy window [FR][TH+2][W+2] pixels of CO/8 16-byte slots plus zero slots (CbGeom::DSL):
+//     the input gradient reads 8 consecutive channels of one tap per lane (16 bytes) as its
+//     B fragment, and with 16 channels the zero slot feeds the k-steps past the 9 taps;
 //   - x window [FR][TH+2][W+2] pixels of 2*CI bytes (+32 from 32 channels on); the weight
 //     gradient reads its fragments, pixel-consecutive, with the LDS transpose read
 //     (ds_read_b64_tr_b16), and the mask is read from it in the epilogue;
@@ -37,7 +36,10 @@ namespace cb {
 
 template <int CI, int CO>
 struct CbGeom {
-    static constexpr int DSL = CO / 8 + 1;               // dy window: 16-byte slots per pixel
+    // dy window: 16-byte slots per pixel, the data and one zero slot (16 channels: the k-steps
+    // past the 9 taps read it), or two from 32 channels on, where a pitch of 2 (mod 4) slots
+    // keeps the 16 pixels of a B-fragment read on distinct bank groups
+    static constexpr int DSL = CO >= 32 ? CO / 8 + 2 : CO / 8 + 1;
     static constexpr int DYP = DSL * 16;                 // dy window: bytes per pixel
     static constexpr int XPB = CI * 2 + (CI >= 32 ? 32 : 0);   // x window: bytes per pixel
     static constexpr int XSL = XPB / 16;

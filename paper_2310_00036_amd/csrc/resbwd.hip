@@ -31,10 +31,10 @@ namespace cb {
 
 template <int C>
 struct RbbGeom {
-    // dy / dt windows: 16-byte slots per pixel. 16 channels: 32 bytes, for which the 16 lanes
-    // of a fragment read on consecutive pixels cover every bank; 32: an extra slot (never
-    // read) makes the pitch odd in 16-byte units
-    static constexpr int DSL = C >= 32 ? C / 8 + 1 : C / 8;
+    // dy / dt windows: 16-byte slots per pixel. A 16-lane B-fragment read on consecutive
+    // pixels lands on distinct bank groups when the pitch is 2 (mod 4) slots: 16 channels fill
+    // 2; 32 channels take two extra slots (never read) for 6
+    static constexpr int DSL = C >= 32 ? C / 8 + 2 : C / 8;
     static constexpr int DYP = DSL * 16;
     static constexpr int XPB = C * 2 + (C >= 32 ? 32 : 0);    // t / x windows: bytes per pixel
     static constexpr int XSL = XPB / 16;
