@@ -5,10 +5,10 @@
 // A tile is a band of pooled rows of one frame; it needs conv rows hc0 .. hc1-1 and input
 // rows hc0-1 .. hc1. Staged in LDS: the zero-padded input window (uint8 frames as bytes,
 // then converted once to bf16, exact for 0..255; bf16 inputs as C/8 16-byte slots per pixel
-// plus a zero slot), with a zero guard pixel either side. The conv runs over the window's
-// pixels padding columns included, 16 per MFMA column tile, so a fragment's address is the
-// tile base plus a constant per k-step and the lane only tracks its column to skip the
-// padding outputs. Each wave owns one 16-channel block of the outputs with its weight
+// plus, from 32 channels on, two zero slots), with a zero guard pixel either side. The conv
+// runs over the window's pixels padding columns included, 16 per MFMA column tile, so a
+// fragment's address is the tile base plus a constant per k-step and the lane only tracks
+// its column to skip the padding outputs. Each wave owns one 16-channel block of the outputs with its weight
 // fragments in registers. Conv outputs (scale, bias, rounded to bf16) are kept as
 // order-preserving 16-bit keys in an LDS tile whose padding columns stay zero (a zero key is
 // below every finite value, so padding never wins). The pool compares (key << 16 | 15 - cell)
@@ -24,7 +24,10 @@ namespace cb {
 template <int CIN, int COUT, int MODE>
 struct CpGeom {
     static constexpr bool U8 = MODE == IN_U8;
-    static constexpr int SPP = U8 ? 1 : CIN / 8 + 1;      // bf16 input: 16-byte slots per pixel
+    // bf16 input: 16-byte slots per pixel. A 16-lane B-fragment read on consecutive window
+    // pixels lands on distinct bank groups when the pitch is 2 (mod 4) slots: 16 channels fill
+    // 2, from 32 on two zero slots are added (6, 10)
+    static constexpr int SPP = U8 ? 1 : (CIN >= 32 ? CIN / 8 + 2 : CIN / 8);
     static constexpr int PB = U8 ? 8 : SPP * 16;           // window bytes per pixel
     static constexpr int K = 9 * CIN, KSTEPS = (K + 31) / 32;
     static constexpr int MT = COUT / 16;
@@ -75,7 +78,7 @@ __global__ __launch_bounds__(64 * NW, (CpGeom<CIN, COUT, MODE>::WPS)) void conv_
     for (int j = 0; j < 4; ++j) bias[j] = a.bias ? a.bias[co0 + j] : 0.f;
     // B-fragment offsets from the lane's tap-(0,0) pixel. uint8: k-step 0 holds taps 2g, 2g+1
     // (4 channels each), k-step 1 tap 8 (its other k have zero weights, so any finite value
-    // serves); 16 channels: a k-step spans two taps (table; past the ninth the zero slot);
+    // serves); 16 channels: a k-step spans two taps (table; past the ninth, zeros);
     // 32: the k-step's tap, the lane's slot
     auto tapoff = [&](int tap) { return ((tap / 3) * TW + tap % 3) * PB; };
     int boff[U8 ? 3 : (CIN < 32 ? KSTEPS : 1)];
@@ -85,7 +88,7 @@ __global__ __launch_bounds__(64 * NW, (CpGeom<CIN, COUT, MODE>::WPS)) void conv_
 #pragma unroll
         for (int ks = 0; ks < KSTEPS; ++ks) {
             const int k0 = ks * 32 + g * 8, tap = k0 / CIN, c = (k0 % CIN) / 8;
-            boff[ks] = tap < 9 ? tapoff(tap) + c * 16 : (G::SPP - 1) * 16;
+            boff[ks] = tap < 9 ? tapoff(tap) + c * 16 : 0;   // past the taps: zeroed below
         }
     }
     const int twpb = TW * PB;
@@ -102,7 +105,9 @@ __global__ __launch_bounds__(64 * NW, (CpGeom<CIN, COUT, MODE>::WPS)) void conv_
             const uint2 t9 = *reinterpret_cast<const uint2*>(xb + boff[2] + 8);
             return make_uint4(t8.x, t8.y, t9.x, t9.y);
         } else if constexpr (CIN < 32) {
-            return *reinterpret_cast<const uint4*>(xb + boff[ks]);
+            // 16 channels: lanes g >= 2 of the last k-step are past the 9 taps
+            const uint4 v = *reinterpret_cast<const uint4*>(xb + boff[ks]);
+            return ks == KSTEPS - 1 && g >= 2 ? make_uint4(0, 0, 0, 0) : v;
         } else {   // from 32 channels a tap spans CIN / 32 k-steps; the lane's slot within it
             constexpr int TPK = CIN / 32;
             const int tap = ks / TPK, cs = (ks % TPK) * 4;
