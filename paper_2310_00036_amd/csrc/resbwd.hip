@@ -408,9 +408,12 @@ hipError_t rbb_launch(const ResBwdArgs& a, hipStream_t s, PendingReduce out[2]) 
 bool resblock_bwd_supported(int C) { return C == 16 || C == 32; }
 
 // With 32 channels the block backward runs one workgroup per CU, which exposes each tile's
-// staging: it beats the two conv backward launches on whole-frame tiles (11x11: 63 against
-// 69 us for 2048 frames) but not on banded ones (21x21: 159 against 152 us).
-bool resblock_bwd_preferred(int C, int H, int W) { return C == 16 || (C == 32 && H * W <= 256); }
+// staging; measured against the two conv backward launches it wins on whole-frame tiles
+// (11x11: 67 against 75 us for 2048 frames) and on the wide net's 42x42 bands (1.89 against
+// 1.97 ms for 8192 frames), but not at 21x21 (153 against 148 us in the learner step).
+bool resblock_bwd_preferred(int C, int H, int W) {
+    return C == 16 || (C == 32 && (H * W <= 256 || H * W >= 1024));
+}
 
 size_t resblock_bwd_partial_floats(int C) {
     if (C == 16) return 2 * size_t(rbb_parts_cap<16>()) * RbbGeom<16>::PSTRIDE;
