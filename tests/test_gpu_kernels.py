@@ -268,6 +268,8 @@ CONV_BWD_CASES = [
     (3, 21, 21, 64, 64, P.X_RELU, 1), (2, 21, 21, 64, 64, P.X_RELU, 0), (7, 11, 11, 64, 64, P.X_RELU, 1),
     (5, 11, 11, 64, 64, P.X_RELU, 0), (2, 13, 9, 64, 64, P.X_RELU, 1), (2, 21, 21, 64, 64, P.X_PLAIN, 0),
     (2, 42, 42, 32, 64, P.X_PLAIN, 0), (3, 7, 5, 32, 64, P.X_PLAIN, 0),
+    # frame counts at which each workgroup runs several tiles (weight gradients accumulating)
+    (300, 21, 21, 64, 64, P.X_RELU, 1), (400, 11, 11, 64, 64, P.X_RELU, 0), (300, 21, 21, 32, 32, P.X_RELU, 1),
 ]
 
 
@@ -303,9 +305,12 @@ def test_conv_backward_fused(case):
     G.assert_sum_close(G.host(db), want_b, abs_b, 1e-5, "conv_bwd db")
 
 
-# (n, H, W, C): the residual blocks' backward, base and ragged bands, tiny frames
+# (n, H, W, C): the residual blocks' backward, base and ragged bands, tiny frames, and frame
+# counts at which every workgroup of the persistent grid runs several tiles (its weight
+# gradients accumulating over them)
 RES_BWD_CASES = [(3, 42, 42, 16), (2, 17, 23, 16), (4, 9, 7, 16), (1, 84, 84, 16), (5, 3, 4, 16), (2, 43, 11, 16),
-                 (4, 21, 21, 32), (5, 11, 11, 32), (3, 9, 7, 32), (2, 23, 17, 32), (1, 42, 42, 32)]
+                 (4, 21, 21, 32), (5, 11, 11, 32), (3, 9, 7, 32), (2, 23, 17, 32), (1, 42, 42, 32),
+                 (150, 42, 42, 16), (600, 11, 11, 32), (300, 21, 21, 32), (96, 42, 42, 32)]
 
 
 def _resblock_bwd(n, H, W, C, dy, t, x, wa, wb):
@@ -394,7 +399,8 @@ def test_resblock_backward_rejects_unsupported():
 # (n, H, W, cin, cout): stage entries fed by a max-pool (base and ragged, odd and even padding)
 CONV_BWD_POOL_CASES = [(3, 42, 42, 16, 32), (2, 21, 21, 32, 32), (4, 42, 42, 16, 16), (2, 17, 23, 16, 32),
                        (5, 9, 7, 32, 32), (1, 84, 84, 16, 16), (3, 11, 11, 32, 32), (6, 4, 5, 16, 16),
-                       (2, 42, 42, 32, 64), (3, 21, 21, 64, 64), (4, 9, 11, 32, 64), (5, 11, 11, 64, 64)]
+                       (2, 42, 42, 32, 64), (3, 21, 21, 64, 64), (4, 9, 11, 32, 64), (5, 11, 11, 64, 64),
+                       (80, 42, 42, 32, 64), (300, 21, 21, 64, 64), (200, 42, 42, 16, 32)]
 
 
 @pytest.mark.parametrize("case", CONV_BWD_POOL_CASES, ids=lambda c: "n%d_%dx%d_%d-%d" % c)
