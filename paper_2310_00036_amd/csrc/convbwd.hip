@@ -61,8 +61,10 @@ struct CbGeom {
     // 64 channels: the waves specialise (of 8, the first half form input gradients, two dx
     // channel blocks per wave so that each B-fragment read feeds two MFMAs, the second half
     // the weight gradients), each half holding only its own registers, and run concurrently
-    // on every tile; otherwise every wave forms both, one dx block each
-    static constexpr bool SPEC = WIDE;
+    // on every tile. The 16 -> 32 stage entry specialises too (measured 190 -> 181 us for its
+    // pooled backward at 2048 frames: the halves overlap); otherwise every wave forms both, one
+    // dx block each (specialised, the 32-channel ones spill at four waves per SIMD)
+    static constexpr bool SPEC = WIDE || (CI == 16 && CO == 32);
     static constexpr int NWD = SPEC ? 4 : 8;               // waves forming input gradients
     static constexpr int NWW = SPEC ? 4 : 8;               // ... and weight gradients
     static constexpr int DB = SPEC && MTI >= 2 ? 2 : 1;    // dx channel blocks per input-gradient wave
@@ -489,13 +491,14 @@ __global__ __launch_bounds__(64 * NW, (CbGeom<CI, CO>::WPS)) void conv_bwd_kerne
     }
 }
 
-// The same backward with specialised waves, for 64 channels (one workgroup per CU). There
-// every wave forming both gradients reads each input-gradient B fragment for one dx channel
-// block (1 KB of LDS per MFMA, more than the LDS delivers at the matrix cores' rate) and
-// holds the weight-gradient accumulators beside the input-gradient weights. Here the first
-// half of the waves forms the input gradient, two dx channel blocks per wave (144 registers
-// of weights, each B fragment feeding two MFMAs), and the second half the weight gradients,
-// each for a quarter of the column blocks against all output channels; the halves run
+// The same backward with specialised waves, for 64 channels (one workgroup per CU) and the
+// 16 -> 32 stage entry (two per CU). There every wave forming both gradients reads each
+// input-gradient B fragment for one dx channel block (1 KB of LDS per MFMA, more than the LDS
+// delivers at the matrix cores' rate) and holds the weight-gradient accumulators beside the
+// input-gradient weights. Here the first half of the waves forms the input gradient, two dx
+// channel blocks per wave where there are two or more (at 64 channels 144 registers of
+// weights, each B fragment feeding two MFMAs), and the second half the weight gradients, each
+// for a quarter of the column blocks against all output channels; the halves run
 // concurrently on every tile, in two loops, so each keeps only its own registers live.
 // Staging, the max-pool backward and the relu pass are shared, with the same barriers.
 template <int CI, int CO, int MODE, int ADD, int PDY, int NW>
