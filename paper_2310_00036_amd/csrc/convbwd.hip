@@ -34,7 +34,7 @@
 
 namespace cb {
 
-template <int CI, int CO>
+template <int CI, int CO, bool SP = false>
 struct CbGeom {
     // dy window: 16-byte slots per pixel, the data and one zero slot (16 channels: the k-steps
     // past the 9 taps read it), or two from 32 channels on, where a pitch of 2 (mod 4) slots
@@ -61,20 +61,26 @@ struct CbGeom {
     // 64 channels: the waves specialise (of 8, the first half form input gradients, two dx
     // channel blocks per wave so that each B-fragment read feeds two MFMAs, the second half
     // the weight gradients), each half holding only its own registers, and run concurrently
-    // on every tile. The 16 -> 32 stage entry specialises too (measured 190 -> 181 us for its
-    // pooled backward at 2048 frames: the halves overlap); otherwise every wave forms both, one
-    // dx block each (specialised, the 32-channel ones spill at four waves per SIMD)
-    static constexpr bool SPEC = WIDE || (CI == 16 && CO == 32);
+    // on every tile. The stage entries from the pooled gradient at 16 -> 32 and 32 -> 32 (SP)
+    // specialise too, one dx block per wave: their halves overlap (measured at 2048 frames:
+    // 190 -> 181 us and 81 -> 76 us); otherwise every wave forms both, one dx block each (the
+    // 32-channel relu/residual variants specialised were 3% slower; with two dx blocks per wave
+    // they spill at four waves per SIMD)
+    static constexpr bool SPEC = WIDE || (CI == 16 && CO == 32) || SP;
     static constexpr int NWD = SPEC ? 4 : 8;               // waves forming input gradients
     static constexpr int NWW = SPEC ? 4 : 8;               // ... and weight gradients
-    static constexpr int DB = SPEC && MTI >= 2 ? 2 : 1;    // dx channel blocks per input-gradient wave
+    static constexpr int DB = SPEC && WIDE && MTI >= 2 ? 2 : 1;   // dx channel blocks per input-gradient wave
     static constexpr int NCG = NWD / (MTI / DB);           // waves sharing a block group (column groups)
     __host__ __device__ static int blocks(int slots) { return (slots + 63) / 64; }
 };
 
+// the geometry of a launch: the 32 -> 32 stage entry from the pooled gradient specialises
+template <int CI, int CO, int PDY>
+using CbG = CbGeom<CI, CO, PDY && CI == 32 && CO == 32>;
+
 template <int CI, int CO, int MODE, int ADD, int PDY, int NW>
 __global__ __launch_bounds__(64 * NW, (CbGeom<CI, CO>::WPS)) void conv_bwd_kernel(ConvBwdArgs a, CbTile t) {
-    using G = CbGeom<CI, CO>;
+    using G = CbG<CI, CO, PDY>;
     constexpr int NT = 64 * NW;
     constexpr int DSL = G::DSL, DYP = G::DYP, XPB = G::XPB, XSL = G::XSL;
     constexpr int MTI = G::MTI, MTO = G::MTO, KSD = G::KSD, NB = G::NB, NBB = G::NBB;
@@ -503,7 +509,7 @@ __global__ __launch_bounds__(64 * NW, (CbGeom<CI, CO>::WPS)) void conv_bwd_kerne
 // Staging, the max-pool backward and the relu pass are shared, with the same barriers.
 template <int CI, int CO, int MODE, int ADD, int PDY, int NW>
 __global__ __launch_bounds__(64 * NW, (CbGeom<CI, CO>::WPS)) void conv_bwd_spec_kernel(ConvBwdArgs a, CbTile t) {
-    using G = CbGeom<CI, CO>;
+    using G = CbG<CI, CO, PDY>;
     constexpr int NT = 64 * NW;
     constexpr int DSL = G::DSL, DYP = G::DYP, XPB = G::XPB, XSL = G::XSL;
     constexpr int MTI = G::MTI, MTO = G::MTO, KSD = G::KSD, NB = G::NB, NBB = G::NBB;
@@ -1004,7 +1010,7 @@ int cb_parts_cap() {
 
 template <int CI, int CO, int MODE, int ADD, int PDY>
 hipError_t cb_launch(const ConvBwdArgs& a, hipStream_t s, PendingReduce* deferred) {
-    using G = CbGeom<CI, CO>;
+    using G = CbG<CI, CO, PDY>;
     const int H = a.H, W = a.W;
     // max-pool geometry of a pooled input gradient (PDY): XLA SAME padding split
     const int OH = (H + 1) / 2, OW = (W + 1) / 2;
