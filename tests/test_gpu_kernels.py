@@ -157,10 +157,13 @@ def test_resblock_forward(case):
     _resblock_fwd_check(case)
 
 
-@pytest.mark.parametrize("case", [(1024, 42, 42, 16), (2048, 21, 21, 32)], ids=lambda c: "n%d_%dx%d_c%d" % c)
+@pytest.mark.parametrize("case", [(1024, 42, 42, 16), (2048, 21, 21, 32), (2053, 42, 42, 32)],
+                         ids=lambda c: "n%d_%dx%d_c%d" % c)
 def test_resblock_forward_many_tiles_per_workgroup(case):
     """The same checks at a frame count where every workgroup runs several tiles (each tile's
-    window is staged during the previous tile's conv2), on frames spread over the launch."""
+    window is staged during the previous tile's conv2), on frames spread over the launch. At
+    2053 frames of 42x42 with 32 channels every workgroup runs 32 or 33 tiles, which selects the
+    kernel whose two wave roles run conv1 and conv2 of neighbouring tiles at once."""
     _resblock_fwd_check(case, sample=[0, 1, 517, case[0] - 1])
 
 
