@@ -327,8 +327,22 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a, int kchunk) 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, r16 = lane & 15;
     const int wm = wave >> 1, wn = wave & 1;
-    const int m0 = blockIdx.x * kGB, n0 = blockIdx.y * kGB;
-    const int k_begin = blockIdx.z * kchunk;
+    // Workgroups go to the XCDs in turn (linear id mod 8), each XCD with its own L2. With split
+    // k, a run of consecutive linear ids is given to one XCD, and within it the output tiles
+    // advance along n first, so an XCD's workgroups share a few A tiles and the B tiles of one
+    // k-split (dense forward 21.6 -> 19.0 us, weight gradient 24.7 -> 22.5 us at 2048 frames;
+    // without split k this order measured no better).
+    int tm = int(blockIdx.x), tn = int(blockIdx.y), tz = int(blockIdx.z);
+    const int nwg = int(gridDim.x * gridDim.y * gridDim.z);
+    if (gridDim.z > 1 && (nwg & 7) == 0) {
+        const int bid = int(blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z));
+        const int b2 = (bid & 7) * (nwg >> 3) + (bid >> 3);
+        tn = b2 % int(gridDim.y);
+        tm = (b2 / int(gridDim.y)) % int(gridDim.x);
+        tz = b2 / int(gridDim.y * gridDim.x);
+    }
+    const int m0 = tm * kGB, n0 = tn * kGB;
+    const int k_begin = tz * kchunk;
     const int k_end = min(a.K, k_begin + kchunk);
     const auto ra = buf_rsrc(a.a, uint32_t((AKC ? int64_t(a.M) : int64_t(a.K)) * a.lda * 2));
     const auto rb = buf_rsrc(a.b, uint32_t((BKC ? int64_t(a.N) : int64_t(a.K)) * a.ldb * 2));
@@ -399,7 +413,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs a, int kchunk) 
             if (gridDim.z == 1) {
                 gemm_epilogue4_bf16(a, vec_ok, mb, n, acc[i][j]);
             } else if (n < a.N && mb < a.M) {
-                float* pp = a.partial + (int64_t(blockIdx.z) * a.N + n) * a.M + mb;
+                float* pp = a.partial + (int64_t(tz) * a.N + n) * a.M + mb;
                 if (mb + 4 <= a.M && (a.M & 3) == 0) {
                     *reinterpret_cast<float4*>(pp) = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
                 } else {
