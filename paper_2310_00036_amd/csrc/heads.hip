@@ -280,6 +280,75 @@ std::string heads_shape(const HeadsArgs& a) {
     return std::to_string(a.n) + "x" + std::to_string(a.J) + "x" + std::to_string(a.A);
 }
 
+// ---- bf16 forward on the matrix cores: [logits | value] = h Wh + [bl | bv] as an MFMA product
+// D[o][i] = sum_j Wh[j][o] h[i][j] with the A + 1 <= 32 outputs in two 16-row blocks (rows past
+// A zero) and k = hidden units, 32 per k-step. The workgroup stages Wh rounded to bf16 in LDS
+// as [o][j] rows (pitch J + 8 elements: an odd count of 16-byte slots, so the 16 rows of a
+// fragment read land on distinct bank groups); each wave takes 16 rows i of h, whose
+// B fragments (8 consecutive hidden units of one row) are plain 16-byte loads from h.
+constexpr int kHmWaves = 4;
+constexpr int kHmOut = 32;
+
+__global__ __launch_bounds__(64 * kHmWaves) void heads_fwd_mfma_kernel(HeadsArgs a, float* __restrict__ logits,
+                                                                      float* __restrict__ value) {
+    extern __shared__ __align__(16) uint16_t wsh[];   // [kHmOut][J + 8]
+    const int J = a.J, A = a.A, P = J + 8, nk = J / 32;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, r16 = lane & 15;
+    const int64_t i0 = (int64_t(blockIdx.x) * kHmWaves + wave) * 16;
+    const bool live = i0 < a.n;
+    const int64_t ir = live ? std::min<int64_t>(i0 + r16, a.n - 1) : 0;   // rows past n: computed, not stored
+    const uint16_t* hrow = static_cast<const uint16_t*>(a.h) + ir * J + g * 8;
+    // B fragments of up to eight k-steps in flight at once; the first eight are issued before
+    // the weights are staged, so their latencies overlap
+    constexpr int KC = 8;
+    uint4 bfr[KC];
+#pragma unroll
+    for (int u = 0; u < KC; ++u)
+        if (u < nk) bfr[u] = *reinterpret_cast<const uint4*>(hrow + u * 32);
+    for (int j = tid; j < J; j += 64 * kHmWaves) {   // unit j's row: clamped, unconditional loads in flight at once
+        const float* wr = a.wl + int64_t(j) * A;
+        const float wv = a.wv[j];
+        float v[kHmOut];
+#pragma unroll
+        for (int o = 0; o < kHmOut; ++o) {
+            const float x = wr[o < A ? o : A - 1];
+            v[o] = o < A ? x : (o == A ? wv : 0.f);
+        }
+#pragma unroll
+        for (int o = 0; o < kHmOut; ++o) wsh[o * P + j] = f2bf(v[o]);
+    }
+    __syncthreads();
+    if (!live) return;
+    cb_f32x4 acc[2] = {cb_f32x4{0.f, 0.f, 0.f, 0.f}, cb_f32x4{0.f, 0.f, 0.f, 0.f}};
+    for (int c0 = 0; c0 < nk; c0 += KC) {
+        if (c0 > 0) {
+#pragma unroll
+            for (int u = 0; u < KC; ++u)
+                if (c0 + u < nk) bfr[u] = *reinterpret_cast<const uint4*>(hrow + (c0 + u) * 32);
+        }
+#pragma unroll
+        for (int u = 0; u < KC; ++u)
+            if (c0 + u < nk) {
+#pragma unroll
+                for (int ob = 0; ob < 2; ++ob) {
+                    const uint4 af = *reinterpret_cast<const uint4*>(wsh + (ob * 16 + r16) * P + (c0 + u) * 32 + g * 8);
+                    acc[ob] = PrecBF16::mma(af, bfr[u], acc[ob]);
+                }
+            }
+    }
+    if (i0 + r16 >= a.n) return;
+    const int64_t i = i0 + r16;
+#pragma unroll
+    for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int o = ob * 16 + 4 * g + e;
+            if (o < A) logits[i * A + o] = acc[ob][e] + (a.bl ? a.bl[o] : 0.f);
+            else if (o == A) value[i] = acc[ob][e] + (a.bv ? a.bv[0] : 0.f);
+        }
+}
+
 }  // namespace
 
 size_t heads_bwd_partial_floats(int64_t n, int J, int A) {
@@ -295,10 +364,18 @@ int heads_ma(int A) { return A == 18 || A == 6 ? A + 1 : (A + 1 <= 20 ? 20 : 68)
 hipError_t heads_fwd(int prec, const HeadsArgs& a, float* logits, float* value, hipStream_t s) {
     if (a.n <= 0) return hipSuccess;
     if (a.A < 1 || a.A > 64 || a.J < 1) return hipErrorInvalidValue;
+    ProfScope ps(s, [&] { return cb_key("heads_fwd", prec, heads_shape(a)); });
+    if (prec == BF16 && a.A + 1 <= kHmOut && a.J % 32 == 0 && a.J <= 2048 &&
+        (reinterpret_cast<uintptr_t>(a.h) & 15) == 0) {
+        const int64_t waves = (a.n + 15) / 16;
+        const size_t lds = size_t(kHmOut) * (a.J + 8) * sizeof(uint16_t);
+        hipLaunchKernelGGL(heads_fwd_mfma_kernel, dim3(unsigned((waves + kHmWaves - 1) / kHmWaves)),
+                           dim3(64 * kHmWaves), lds, s, a, logits, value);
+        return hipGetLastError();
+    }
     const int MA = heads_ma(a.A);
     const size_t lds = std::max(size_t(kHJ) * (MA | 1), size_t(kHJ) * MA) * sizeof(float);
     const dim3 grid(unsigned((a.n + kHR - 1) / kHR));
-    ProfScope ps(s, [&] { return cb_key("heads_fwd", prec, heads_shape(a)); });
 #define CB_HF(T, AC, MA) hipLaunchKernelGGL((heads_fwd_kernel<T, AC, MA>), grid, dim3(kHJ), lds, s, a, logits, value)
 #define CB_HF_ALL(T)                                 \
     if (a.A == 18) CB_HF(T, 18, 19);                 \
