@@ -22,6 +22,8 @@ namespace {
 constexpr int kHR = 16;    // rows per row group
 constexpr int kHJ = 256;   // hidden units per chunk: one per thread
 constexpr size_t kHeadsPartialCap = size_t(8) << 20;   // floats of partials at most
+constexpr int kHmWaves = 4;                              // MFMA forward: waves per workgroup
+constexpr int kHmOut = 32;                               // MFMA kernels: head outputs (A + 1) at most
 
 template <class T>
 CB_DEV float ld_st(const T* p, int64_t i) {
@@ -236,6 +238,160 @@ __global__ __launch_bounds__(256) void heads_bwd_kernel(HeadsArgs a, const float
     if (tid < A1) part[int64_t(A1 + 1) * a.J + tid] = hb;
 }
 
+// ---- bf16 backward on the matrix cores, for A + 1 <= 32 outputs and J = 64 * NJB hidden units.
+// Per group of 32 rows (the workgroup's groups in turn), with dz = [dlogits | dvalue] rounded to
+// bf16 (zero past A and for rows past n) and the head weights Wh (bf16) in LDS:
+//   dh[i][j] = (sum_o Wh[j][o] dz[i][o]) * (h[i][j] > 0)      MFMA D[j][i], k = o (one k-step);
+//   gW[j][o] += sum_i h[i][j] dz[i][o]                         MFMA D[j][o], k = the 32 rows;
+//   dense bias += sum_i dh[i][j] as stored; head bias += sum_i dz[i][o].
+// Wave w takes the 16-unit blocks jb = w + 4 u (u < NJB). The h and dz tiles are row-major in
+// LDS; the weight-gradient fragments, which run along rows, are read with the transpose read.
+// Each workgroup writes the partial layout heads_reduce_kernel sums (the float32 kernel's).
+constexpr int kHbRows = 32;
+constexpr int kHzP = 40;   // dz tile and weight rows: 32 outputs + 8 (80 bytes, an odd count of 16-byte slots)
+
+// Stages a group of 32 rows for the MFMA head backward: h rows (clamped past n: their dz is
+// zero) into the h tile, dz = [dlogits | dvalue] rounded to bf16 (zero past A and for rows past
+// n) into the dz tile, thread (rr, c) taking outputs 4c .. 4c+3 of row rr.
+template <int NJB>
+CB_DEV void hb_stage(const HeadsArgs& a, const float* __restrict__ dl, const float* __restrict__ dv,
+                     const uint16_t* __restrict__ h, int64_t r0, int tid, uint16_t* hs, uint16_t* zs) {
+    constexpr int J = 64 * NJB, PH = J + 8;
+    const int A = a.A;
+#pragma unroll
+    for (int u = 0; u < NJB; ++u) {
+        const int e = tid + 256 * u, rr = e / (J / 8), c = e - rr * (J / 8);
+        const int64_t row = std::min<int64_t>(r0 + rr, a.n - 1);
+        *reinterpret_cast<uint4*>(hs + rr * PH + c * 8) = *reinterpret_cast<const uint4*>(h + row * J + c * 8);
+    }
+    const int rr = tid >> 3, c = tid & 7;
+    const int64_t rowc = std::min<int64_t>(r0 + rr, a.n - 1);
+    const bool live = r0 + rr < a.n;
+    const float dvr = dv[rowc];
+    float v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int o = 4 * c + e;
+        const float x = dl[rowc * A + (o < A ? o : A - 1)];
+        v[e] = live ? (o < A ? x : (o == A ? dvr : 0.f)) : 0.f;
+    }
+    *reinterpret_cast<uint2*>(zs + rr * kHzP + 4 * c) = make_uint2(pack2bf(v[0], v[1]), pack2bf(v[2], v[3]));
+}
+
+template <int NJB>
+__global__ __launch_bounds__(256) void heads_bwd_mfma_kernel(HeadsArgs a, const float* __restrict__ dl,
+                                                             const float* __restrict__ dv, uint16_t* __restrict__ dh,
+                                                             float* __restrict__ partial, int pstride) {
+    constexpr int J = 64 * NJB, PH = J + 8;   // h tile pitch (elements)
+    extern __shared__ __align__(16) uint16_t hsm[];
+    uint16_t* wsh = hsm;                       // [J][kHzP]   Wh[j][o]
+    uint16_t* hs = wsh + J * kHzP;             // [32][PH]    h rows of the group
+    uint16_t* zs = hs + kHbRows * PH;          // [32][kHzP]  dz rows of the group
+    const int A = a.A, A1 = A + 1;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, r16 = lane & 15, jj = r16 >> 2, m = r16 & 3;
+    const uint16_t* h = static_cast<const uint16_t*>(a.h);
+
+    // the first group's tiles are staged before the weights, so the two load latencies overlap
+    const int64_t ngroups = (a.n + kHbRows - 1) / kHbRows;
+    if (blockIdx.x < ngroups) hb_stage<NJB>(a, dl, dv, h, int64_t(blockIdx.x) * kHbRows, tid, hs, zs);
+
+    for (int j = tid; j < J; j += 256) {   // unit j's weights: clamped, unconditional loads
+        const float* wr = a.wl + int64_t(j) * A;
+        const float wv = a.wv[j];
+        float v[kHmOut];
+#pragma unroll
+        for (int o = 0; o < kHmOut; ++o) {
+            const float x = wr[o < A ? o : A - 1];
+            v[o] = o < A ? x : (o == A ? wv : 0.f);
+        }
+#pragma unroll
+        for (int c = 0; c < kHmOut / 8; ++c)
+            *reinterpret_cast<uint4*>(wsh + j * kHzP + c * 8) =
+                make_uint4(pack2bf(v[8 * c], v[8 * c + 1]), pack2bf(v[8 * c + 2], v[8 * c + 3]),
+                           pack2bf(v[8 * c + 4], v[8 * c + 5]), pack2bf(v[8 * c + 6], v[8 * c + 7]));
+    }
+
+    cb_f32x4 gw[NJB][2];
+    float pb[NJB][4];
+#pragma unroll
+    for (int u = 0; u < NJB; ++u) {
+        gw[u][0] = gw[u][1] = cb_f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) pb[u][e] = 0.f;
+    }
+    float hb = 0.f;   // thread o < A1: head bias partial
+    __syncthreads();
+    for (int64_t grp = blockIdx.x; grp < ngroups; grp += gridDim.x) {
+        const int64_t r0 = grp * kHbRows;
+        if (grp != int64_t(blockIdx.x)) {
+            __syncthreads();   // the previous group's tiles are read
+            hb_stage<NJB>(a, dl, dv, h, r0, tid, hs, zs);
+            __syncthreads();
+        }
+        if (tid < A1) {
+#pragma unroll 8
+            for (int rr = 0; rr < kHbRows; ++rr) hb += bf2f(zs[rr * kHzP + tid]);
+        }
+        // dz fragments (k = outputs) of the two 16-row tiles; transposed (k = rows) of the two
+        // 16-output blocks
+        uint4 zf[2], zt[2];
+#pragma unroll
+        for (int t2 = 0; t2 < 2; ++t2) {
+            zf[t2] = *reinterpret_cast<const uint4*>(zs + (t2 * 16 + r16) * kHzP + g * 8);
+            const uint2 lo = lds_read_tr16(reinterpret_cast<const unsigned char*>(zs + (g * 8 + jj) * kHzP + t2 * 16 + 4 * m));
+            const uint2 hi = lds_read_tr16(reinterpret_cast<const unsigned char*>(zs + (g * 8 + 4 + jj) * kHzP + t2 * 16 + 4 * m));
+            zt[t2] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        }
+#pragma unroll
+        for (int u = 0; u < NJB; ++u) {
+            const int jb = wave + 4 * u;
+            // dh on the two row tiles
+            const uint4 wf = *reinterpret_cast<const uint4*>(wsh + (jb * 16 + r16) * kHzP + g * 8);
+#pragma unroll
+            for (int t2 = 0; t2 < 2; ++t2) {
+                const cb_f32x4 d = PrecBF16::mma(wf, zf[t2], cb_f32x4{0.f, 0.f, 0.f, 0.f});
+                const int rr = t2 * 16 + r16, j0 = jb * 16 + 4 * g;
+                const uint2 hm = *reinterpret_cast<const uint2*>(hs + rr * PH + j0);
+                const uint32_t u0 = pack2bf(bf_lo(hm.x) > 0.f ? d[0] : 0.f, bf_hi(hm.x) > 0.f ? d[1] : 0.f);
+                const uint32_t u1 = pack2bf(bf_lo(hm.y) > 0.f ? d[2] : 0.f, bf_hi(hm.y) > 0.f ? d[3] : 0.f);
+                if (r0 + rr < a.n) *reinterpret_cast<uint2*>(dh + (r0 + rr) * J + j0) = make_uint2(u0, u1);
+                pb[u][0] += bf_lo(u0); pb[u][1] += bf_hi(u0); pb[u][2] += bf_lo(u1); pb[u][3] += bf_hi(u1);
+            }
+            // head weight gradient: h^T fragments (k = rows) against dz
+            const uint2 lo = lds_read_tr16(reinterpret_cast<const unsigned char*>(hs + (g * 8 + jj) * PH + jb * 16 + 4 * m));
+            const uint2 hi = lds_read_tr16(reinterpret_cast<const unsigned char*>(hs + (g * 8 + 4 + jj) * PH + jb * 16 + 4 * m));
+            const uint4 hf = make_uint4(lo.x, lo.y, hi.x, hi.y);
+#pragma unroll
+            for (int ob = 0; ob < 2; ++ob) gw[u][ob] = PrecBF16::mma(hf, zt[ob], gw[u][ob]);
+        }
+    }
+    // ---- partials: [A1][J] weight gradient, [J] dense bias, [A1] head bias
+    float* part = partial + int64_t(blockIdx.x) * pstride;
+#pragma unroll
+    for (int u = 0; u < NJB; ++u) {
+        const int j0 = (wave + 4 * u) * 16 + 4 * g;
+#pragma unroll
+        for (int ob = 0; ob < 2; ++ob) {
+            const int o = ob * 16 + r16;
+            if (o < A1)
+                *reinterpret_cast<float4*>(part + int64_t(o) * J + j0) =
+                    make_float4(gw[u][ob][0], gw[u][ob][1], gw[u][ob][2], gw[u][ob][3]);
+        }
+        // the dense bias: this lane's four units summed over its 16 row lanes, in a fixed order
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            float v = pb[u][e];
+#pragma unroll
+            for (int sh = 1; sh < 16; sh <<= 1) v += __shfl_xor(v, sh, 64);
+            pb[u][e] = v;
+        }
+        if (r16 == 0)
+            *reinterpret_cast<float4*>(part + int64_t(A1) * J + j0) = make_float4(pb[u][0], pb[u][1], pb[u][2], pb[u][3]);
+    }
+    if (tid < A1) part[int64_t(A1 + 1) * J + tid] = hb;
+}
+
 struct HeadsOut {
     float* dwl; float* dwv; float* dbl; float* dbv; float* db_dense;
     int J, A;
@@ -286,8 +442,6 @@ std::string heads_shape(const HeadsArgs& a) {
 // as [o][j] rows (pitch J + 8 elements: an odd count of 16-byte slots, so the 16 rows of a
 // fragment read land on distinct bank groups); each wave takes 16 rows i of h, whose
 // B fragments (8 consecutive hidden units of one row) are plain 16-byte loads from h.
-constexpr int kHmWaves = 4;
-constexpr int kHmOut = 32;
 
 __global__ __launch_bounds__(64 * kHmWaves) void heads_fwd_mfma_kernel(HeadsArgs a, float* __restrict__ logits,
                                                                       float* __restrict__ value) {
@@ -401,6 +555,27 @@ hipError_t heads_bwd(int prec, const HeadsArgs& a, const float* dlogits, const f
     if (size_t(nblk) * size_t(pstride) > partial_floats) return hipErrorInvalidValue;
     const int MA = heads_ma(a.A);
     const size_t lds = (size_t(kHJ) * (MA | 1) + size_t(MA) * kHR) * sizeof(float);
+    const bool mfma = prec == BF16 && a.A + 1 <= kHmOut && (a.J == 256 || a.J == 512) &&
+                      (reinterpret_cast<uintptr_t>(a.h) & 15) == 0 && (reinterpret_cast<uintptr_t>(dh) & 7) == 0;
+    if (mfma) {
+        const int64_t groups = (std::max<int64_t>(a.n, 1) + kHbRows - 1) / kHbRows;
+        const int nb = int(std::min<int64_t>({groups, int64_t(nblk), 256}));
+        const size_t lm = (size_t(a.J) * kHzP + size_t(kHbRows) * (a.J + 8) + size_t(kHbRows) * kHzP) * sizeof(uint16_t);
+        {
+            ProfScope ps(s, [&] { return cb_key("heads_bwd", prec, heads_shape(a)); });
+            if (a.J == 256)
+                hipLaunchKernelGGL(heads_bwd_mfma_kernel<4>, dim3(unsigned(nb)), dim3(256), lm, s, a, dlogits, dvalue,
+                                   static_cast<uint16_t*>(dh), partial, pstride);
+            else
+                hipLaunchKernelGGL(heads_bwd_mfma_kernel<8>, dim3(unsigned(nb)), dim3(256), lm, s, a, dlogits, dvalue,
+                                   static_cast<uint16_t*>(dh), partial, pstride);
+        }
+        HeadsOut o{dwl, dwv, dbl, dbv, db_dense, a.J, a.A};
+        ProfScope ps(s, [&] { return cb_key("heads_reduce", prec, heads_shape(a)); });
+        hipLaunchKernelGGL(heads_reduce_kernel, dim3(unsigned((pstride + 63) / 64)), dim3(1024), 0, s, partial, nb,
+                           pstride, o);
+        return hipGetLastError();
+    }
     {
         ProfScope ps(s, [&] { return cb_key("heads_bwd", prec, heads_shape(a)); });
 #define CB_HB(T, AC, MA) \
