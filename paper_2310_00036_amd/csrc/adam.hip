@@ -110,6 +110,14 @@ CB_DEV float clip_scale(const double (&pv)[4], int nparts, float max_norm, doubl
     return (max_norm > 0.f && norm > double(max_norm)) ? float(double(max_norm) / norm) : 1.f;
 }
 
+// The bf16 mirror of updated parameters i .. i+k-1 (those inside the mirrored range).
+CB_DEV void mirror_store(const OptArgs& a, int64_t i, const float* v, int k) {
+    for (int e = 0; e < k; ++e) {
+        const int64_t d = i + e - a.mir_off;
+        if (d >= 0 && d < a.mir_len) a.mir[d] = f2bf(v[e]);
+    }
+}
+
 // Each thread's first float4 of p, g, m, v is loaded before the norm is known (clamped
 // index, so the loads are unconditional): their latency overlaps the re-addition of the
 // norm partials, which are loaded before them (loads complete in order, so waiting for the
@@ -133,6 +141,7 @@ __global__ __launch_bounds__(256) void opt_kernel(OptArgs a, const double* __res
                 float mt = OPT == OPT_ADAM ? a.m[i] : 0.f;
                 opt_one<OPT>(a.p[i], a.g[i], mt, a.v[i], scale, a);
                 if constexpr (OPT == OPT_ADAM) a.m[i] = mt;
+                if (a.mir) mirror_store(a, i, &a.p[i], 1);
             }
         return;
     }
@@ -146,10 +155,28 @@ __global__ __launch_bounds__(256) void opt_kernel(OptArgs a, const double* __res
     float4 mm = make_float4(0.f, 0.f, 0.f, 0.f);
     if constexpr (OPT == OPT_ADAM) mm = m4[ic];
     const float scale = clip_scale(pv, nparts, a.max_norm, sh, stats);
+    // the mirror takes 8-byte stores where its range and address are 4-element aligned
+    const bool mvec = a.mir && (a.mir_off & 3) == 0 && (reinterpret_cast<uintptr_t>(a.mir) & 7) == 0;
+    auto mirror4 = [&](int64_t i, const float4& q) {
+        if (!a.mir) return;
+        const int64_t d = 4 * i - a.mir_off;
+        if (mvec) {
+            if (d >= 0 && d + 4 <= a.mir_len)
+                *reinterpret_cast<uint2*>(a.mir + d) = make_uint2(pack2bf(q.x, q.y), pack2bf(q.z, q.w));
+            else if (d + 4 > 0 && d < a.mir_len) {
+                const float t[4] = {q.x, q.y, q.z, q.w};
+                mirror_store(a, 4 * i, t, 4);
+            }
+        } else if (d + 4 > 0 && d < a.mir_len) {
+            const float t[4] = {q.x, q.y, q.z, q.w};
+            mirror_store(a, 4 * i, t, 4);
+        }
+    };
     if (i0 < n4) {
         opt_four<OPT>(pp, gg, mm, vv, scale, a);
         p4[i0] = pp; v4[i0] = vv;
         if constexpr (OPT == OPT_ADAM) m4[i0] = mm;
+        mirror4(i0, pp);
     }
     for (int64_t i = i0 + stride; i < n4; i += stride) {
         pp = p4[i]; gg = g4[i]; vv = v4[i];
@@ -157,12 +184,14 @@ __global__ __launch_bounds__(256) void opt_kernel(OptArgs a, const double* __res
         opt_four<OPT>(pp, gg, mm, vv, scale, a);
         p4[i] = pp; v4[i] = vv;
         if constexpr (OPT == OPT_ADAM) m4[i] = mm;
+        mirror4(i, pp);
     }
     if (blockIdx.x == 0)
         for (int64_t i = n4 * 4 + threadIdx.x; i < a.n; i += 256) {
             float mt = OPT == OPT_ADAM ? a.m[i] : 0.f;
             opt_one<OPT>(a.p[i], a.g[i], mt, a.v[i], scale, a);
             if constexpr (OPT == OPT_ADAM) a.m[i] = mt;
+            if (a.mir) mirror_store(a, i, &a.p[i], 1);
         }
 }
 

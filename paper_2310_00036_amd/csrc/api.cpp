@@ -501,14 +501,24 @@ impala_status_t learner_step(const impala_net_t* net, const learner_cfg_t* cfg,
 #define LS_TRY(x, what) \
     if ((he = (x)) != hipSuccess) return hip_status(he, what)
     // clip, then the configured optimiser (Adam: m, v; RMSprop: v holds nu), at step *step
+    // bf16: the optimiser also writes the bf16 copy of the updated dense weights that the next
+    // forward's dense GEMMs read (the rounding the forward's own cast applies), so only the
+    // first forward of the call casts them
+    bool dense_ready = false;
     auto opt_step = [&](float* st) {
-        if (c.optimizer == LEARNER_OPT_ADAM)
-            return clip_opt_step(OPT_ADAM, adam_args(P.po.total, params, grads, m, v, *step, c.lr, c.beta1, c.beta2,
-                                                     c.adam_eps, c.max_grad_norm),
-                                 st, apart, stream);
-        return clip_opt_step(OPT_RMSPROP, rmsprop_args(P.po.total, params, grads, v, c.lr, c.rms_decay, c.rms_eps,
-                                                       c.max_grad_norm),
-                             st, apart, stream);
+        OptArgs oa = c.optimizer == LEARNER_OPT_ADAM
+                         ? adam_args(P.po.total, params, grads, m, v, *step, c.lr, c.beta1, c.beta2, c.adam_eps,
+                                     c.max_grad_norm)
+                         : rmsprop_args(P.po.total, params, grads, v, c.lr, c.rms_decay, c.rms_eps, c.max_grad_norm);
+        if (P.prec == BF16) {
+            oa.mir = reinterpret_cast<uint16_t*>(cnn + P.wdb);
+            oa.mir_off = P.po.dense_w;
+            oa.mir_len = int64_t(P.flat) * P.hidden;
+        }
+        const hipError_t e = clip_opt_step(c.optimizer == LEARNER_OPT_ADAM ? OPT_ADAM : OPT_RMSPROP, oa, st, apart,
+                                           stream);
+        dense_ready = e == hipSuccess && P.prec == BF16;
+        return e;
     };
 
     if (c.algo == LEARNER_PPO) {
@@ -521,7 +531,7 @@ impala_status_t learner_step(const impala_net_t* net, const learner_cfg_t* cfg,
             for (int k = 0; k < c.num_minibatches; ++k, ++u) {
                 const int32_t* rows = perm + int64_t(j) * TE + int64_t(k) * c.minibatch_size;
                 const int64_t mb = c.minibatch_size;
-                LS_TRY(run_forward(P, params, ro->obs, rows, mb, cnn, logits, value, stream),
+                LS_TRY(run_forward(P, params, ro->obs, rows, mb, cnn, logits, value, stream, dense_ready),
                        "learner_step: forward");
                 LS_TRY(ppo_loss_ws(mb, A, logits, value, ro->actions, ro->behav_logp, adv, ret, rows,
                                    c.norm_adv, c.clip_eps, c.vf_coef, c.ent_coef, dlogits, dvalue,
@@ -554,7 +564,7 @@ impala_status_t learner_step(const impala_net_t* net, const learner_cfg_t* cfg,
                                         ro->next_done, b, stream), "learner_step: minibatch gather");
                 rows = b.rows; act = b.act; mu = b.mu; rw = b.r; dn = b.d; nd = b.nd;
             }
-            LS_TRY(run_forward(P, params, ro->obs, rows, n1, cnn, logits, value, stream),
+            LS_TRY(run_forward(P, params, ro->obs, rows, n1, cnn, logits, value, stream, dense_ready),
                    "learner_step: forward");
             LS_TRY(action_logp(n, A, logits, act, tlogp, stream), "learner_step: logp");
             LS_TRY(vtrace(c.T, Eb, mu, tlogp, rw, value, dn, value + n, nd, c.gamma, c.lambda, c.rho_bar, c.c_bar,

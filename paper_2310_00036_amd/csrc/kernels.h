@@ -272,6 +272,9 @@ struct OptArgs {
     int64_t n;
     float* p; const float* g; float* m; float* v;
     float lr, b1, b2, omb1, omb2, bc1, bc2, eps, max_norm;
+    // optional bf16 mirror of p[mir_off, mir_off + mir_len): mir[i - mir_off] = bf16(p[i]) as
+    // updated (the copy the bf16 forward's dense GEMMs read); NULL for none
+    uint16_t* mir; int64_t mir_off, mir_len;
 };
 // Global-norm clip then one optimiser step; stats [2] = [pre-clip norm, nonfinite] or NULL.
 hipError_t clip_opt_step(int opt, const OptArgs& a, float* stats, float* partial, hipStream_t s);

@@ -142,7 +142,7 @@ NetPlan make_plan(const impala_net_t& net, int prec, int64_t cap, int training) 
 
 hipError_t run_forward(const NetPlan& p, const float* params, const uint8_t* obs,
                        const int32_t* row_idx, int64_t n, char* ws, float* logits, float* value,
-                       hipStream_t s) {
+                       hipStream_t s, bool dense_bf16_ready) {
     if (n <= 0) return hipSuccess;
     const ParamOffsets& po = p.po;
     for (int st = 0; st < 3; ++st) {
@@ -191,9 +191,10 @@ hipError_t run_forward(const NetPlan& p, const float* params, const uint8_t* obs
         }
     }
     // dense: h[i][j] = relu(b[j] + sum_k relu(x)[i][k] W[k][j])
-    // bf16: the dense weights are cast once per pass, so both dense GEMMs read bf16 operands
+    // bf16: the dense weights are cast once per pass (or were written by the optimiser step
+    // that produced them), so both dense GEMMs read bf16 operands
     const bool wbf = p.prec == BF16;
-    if (wbf) CB_TRY(cast_bf16(params + po.dense_w, reinterpret_cast<uint16_t*>(ws + p.wdb),
+    if (wbf && !dense_bf16_ready) CB_TRY(cast_bf16(params + po.dense_w, reinterpret_cast<uint16_t*>(ws + p.wdb),
                               int64_t(p.flat) * p.hidden, s));
     GemmArgs d{};
     d.a = wbf ? static_cast<const void*>(ws + p.wdb) : static_cast<const void*>(params + po.dense_w);

@@ -42,9 +42,11 @@ ParamOffsets param_offsets(const impala_net_t& net);
 NetPlan make_plan(const impala_net_t& net, int prec, int64_t cap, int training);
 
 // Launch sequences (argument validation done by the caller). n <= plan.cap frames.
+// dense_bf16_ready: the bf16 copy of the dense weights in ws already holds params' values (an
+// optimiser step wrote it), so the forward does not cast them again.
 hipError_t run_forward(const NetPlan& p, const float* params, const uint8_t* obs,
                        const int32_t* row_idx, int64_t n, char* ws, float* logits, float* value,
-                       hipStream_t s);
+                       hipStream_t s, bool dense_bf16_ready = false);
 hipError_t run_backward(const NetPlan& p, const float* params, const uint8_t* obs,
                         const int32_t* row_idx, int64_t n, char* ws, const float* dlogits,
                         const float* dvalue, float* grads, hipStream_t s);
