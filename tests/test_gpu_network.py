@@ -157,12 +157,31 @@ ODD_NETS = {
 }
 
 
+# head shapes at the edges of the bf16 matrix-core head kernels: A + 1 = 32 outputs (both
+# 16-row output blocks full, the value head in the last row) and 512 hidden units
+MFMA_HEAD_NETS = {
+    "h256_a31": NetShape(in_h=12, in_w=10, ch=(16, 16, 32), hidden=256, num_actions=31),
+    "h512_a5": NetShape(in_h=9, in_w=13, ch=(16, 32, 32), hidden=512, num_actions=5),
+}
+
+
 @pytest.mark.parametrize("prec", [G.BF16, G.FP32], ids=lambda p: PNAME[p])
 @pytest.mark.parametrize("netname", sorted(ODD_NETS))
 def test_cnn_odd_head_shapes(prec, netname):
     """Tier B on small frames: forward outputs and every parameter gradient of nets whose
     head shapes take the generic head-kernel paths, 5 gathered frames (a ragged row group)."""
-    net = ODD_NETS[netname]
+    _odd_head_check(ODD_NETS[netname], prec, netname)
+
+
+@pytest.mark.parametrize("netname", sorted(MFMA_HEAD_NETS))
+def test_cnn_mfma_head_edge_shapes(netname):
+    """The same checks (bf16) for head shapes at the edges of the matrix-core head kernels,
+    on 5 gathered frames: one ragged row group of the forward and of the backward's 32-row
+    groups."""
+    _odd_head_check(MFMA_HEAD_NETS[netname], G.BF16, netname)
+
+
+def _odd_head_check(net, prec, netname):
     rng = np.random.default_rng(11)
     params = draw_params(net, 5)
     obs = rng.integers(0, 256, size=(8, net.in_h, net.in_w, 4), dtype=np.uint8)
