@@ -51,6 +51,7 @@ struct LearnerLayout {
     size_t cnn, adv, ret, tlogp, logits, value, dlogits, dvalue, grads, apart;
     size_t rows, gact, gmu, grew, gdone, gnd;   // IMPALA minibatch gathers (more than one)
     size_t lossws;                               // the loss kernels' statistics and row terms
+    size_t advms;                                // PPO: every update's advantage mean / std
     size_t total;
     int64_t fwd_rows, mb;
 };
@@ -112,6 +113,7 @@ LearnerLayout learner_layout(const impala_net_t& net, const learner_cfg_t& c) {
     L.gdone = take(gather ? size_t(L.mb) : 0);
     L.gnd = take(gather ? size_t(Eb) : 0);
     L.lossws = take(loss_ws_bytes(L.mb));
+    L.advms = take(c.algo == LEARNER_PPO ? size_t(2) * c.update_epochs * c.num_minibatches * sizeof(float) : 0);
     L.total = off;
     return L;
 }
@@ -526,6 +528,14 @@ impala_status_t learner_step(const impala_net_t* net, const learner_cfg_t* cfg,
         float* ret = reinterpret_cast<float*>(w + L.ret);
         LS_TRY(gae(c.T, c.E, ro->rewards, ro->values, ro->dones, ro->next_value, ro->next_done, c.gamma,
                    c.lambda, adv, ret, stream), "learner_step: gae");
+        // the advantages are fixed for the whole phase: every update's minibatch statistics in
+        // one launch (update u = j * num_minibatches + k reads rows perm + j * T * E + k * minibatch_size)
+        float* advms = reinterpret_cast<float*>(w + L.advms);
+        const bool pre = ppo_adv_stats_batched(c.minibatch_size);
+        if (pre)
+            LS_TRY(ppo_adv_stats(c.minibatch_size, c.update_epochs * c.num_minibatches, adv, perm, c.minibatch_size,
+                                 c.num_minibatches, TE, advms, stream),
+                   "learner_step: advantage statistics");
         int u = 0;
         for (int j = 0; j < c.update_epochs; ++j) {
             for (int k = 0; k < c.num_minibatches; ++k, ++u) {
@@ -535,7 +545,8 @@ impala_status_t learner_step(const impala_net_t* net, const learner_cfg_t* cfg,
                        "learner_step: forward");
                 LS_TRY(ppo_loss_ws(mb, A, logits, value, ro->actions, ro->behav_logp, adv, ret, rows,
                                    c.norm_adv, c.clip_eps, c.vf_coef, c.ent_coef, dlogits, dvalue,
-                                   stats + 8 * u, w + L.lossws, stream), "learner_step: ppo loss");
+                                   stats + 8 * u, w + L.lossws, stream, pre ? advms + 2 * u : nullptr),
+                       "learner_step: ppo loss");
                 LS_TRY(run_backward(P, params, ro->obs, rows, mb, cnn, dlogits, dvalue, grads, stream),
                        "learner_step: backward");
                 *step += 1;

@@ -244,7 +244,14 @@ size_t loss_ws_bytes(int64_t m);
 hipError_t ppo_loss_ws(int64_t m, int A, const float* z, const float* v, const int32_t* act,
                        const float* old_logp, const float* adv, const float* ret, const int32_t* rows,
                        int norm_adv, float clip, float vf, float ent, float* dz, float* dv, float* stats,
-                       void* ws, hipStream_t s);
+                       void* ws, hipStream_t s, const float* ms_pre = nullptr);
+// PPO advantage mean / std of nmb minibatches of m rows each (minibatch u: rows + (u / per) *
+// stride2 + (u % per) * stride) into ms[2u], ms[2u + 1], in one launch; ppo_loss_ws takes
+// minibatch u's pair as ms_pre (bit-identical to the statistics it forms itself) where
+// ppo_adv_stats_batched(m).
+bool ppo_adv_stats_batched(int64_t m);
+hipError_t ppo_adv_stats(int64_t m, int nmb, const float* adv, const int32_t* rows, int64_t stride, int per,
+                         int64_t stride2, float* ms, hipStream_t s);
 hipError_t impala_loss_ws(int64_t m, int A, const float* z, const float* v, const int32_t* act,
                           const float* vs, const float* pg, float pgc, float vf, float ent, float* dz,
                           float* dv, float* stats, void* ws, hipStream_t s);

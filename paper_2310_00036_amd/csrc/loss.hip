@@ -358,16 +358,36 @@ constexpr int kWideRows = 256;   // rows (one per thread) per workgroup of (2)
 
 size_t loss_ws_bytes(int64_t m) { return 256 + size_t(m > 0 ? m : 1) * 5 * sizeof(double); }
 
+// Workgroup u: the statistics of the minibatch at rows + (u / per) * stride2 + (u % per) *
+// stride (one launch can serve every minibatch of a learning phase; each workgroup's
+// arithmetic is the single minibatch's).
 template <bool ROWS>
 __global__ __launch_bounds__(kFusedThreads) void adv_stats_ws_kernel(int64_t m, const float* __restrict__ adv,
-                                                                   const int32_t* __restrict__ rows,
+                                                                   const int32_t* __restrict__ rows, int64_t stride,
+                                                                   int per, int64_t stride2,
                                                                    float* __restrict__ ms_out) {
     __shared__ double sh[(kFusedThreads / 64) * 5];
     double ms[2];
-    adv_sums<ROWS>(m, adv, rows, ms);
+    const int u = int(blockIdx.x);
+    adv_sums<ROWS>(m, adv, ROWS ? rows + int64_t(u / per) * stride2 + int64_t(u % per) * stride : rows, ms);
     float mean, std;
     adv_mean_std(m, ms, sh, mean, std);
-    if (threadIdx.x == 0) { ms_out[0] = mean; ms_out[1] = std; }
+    if (threadIdx.x == 0) { ms_out[2 * blockIdx.x] = mean; ms_out[2 * blockIdx.x + 1] = std; }
+}
+
+bool ppo_adv_stats_batched(int64_t m) { return m > kWideRows && m <= kFusedRows; }
+
+hipError_t ppo_adv_stats(int64_t m, int nmb, const float* adv, const int32_t* rows, int64_t stride, int per,
+                         int64_t stride2, float* ms, hipStream_t s) {
+    if (m <= 0 || nmb <= 0 || per <= 0) return hipSuccess;
+    ProfScope ps(s, [&] { return "ppo_adv_stats/" + std::to_string(m) + "x" + std::to_string(nmb); });
+    if (rows)
+        hipLaunchKernelGGL(adv_stats_ws_kernel<true>, dim3(unsigned(nmb)), dim3(kFusedThreads), 0, s, m, adv, rows,
+                           stride, per, stride2, ms);
+    else
+        hipLaunchKernelGGL(adv_stats_ws_kernel<false>, dim3(unsigned(nmb)), dim3(kFusedThreads), 0, s, m, adv, rows,
+                           stride, per, stride2, ms);
+    return hipGetLastError();
 }
 
 // The workgroup's rows' logits into LDS with coalesced loads (unconditional, clamped; all in
@@ -767,7 +787,7 @@ hipError_t impala_loss(int64_t m, int A, const float* z, const float* v, const i
 hipError_t ppo_loss_ws(int64_t m, int A, const float* z, const float* v, const int32_t* act,
                        const float* old_logp, const float* adv, const float* ret, const int32_t* rows,
                        int norm_adv, float clip, float vf, float ent, float* dz, float* dv, float* stats,
-                       void* ws, hipStream_t s) {
+                       void* ws, hipStream_t s, const float* ms_pre) {
     if (m <= 0) return hipSuccess;
     if (m <= kWideRows)   // one workgroup's worth
         return ppo_loss(m, A, z, v, act, old_logp, adv, ret, rows, norm_adv, clip, vf, ent, dz, dv, stats, s);
@@ -775,13 +795,18 @@ hipError_t ppo_loss_ws(int64_t m, int A, const float* z, const float* v, const i
         ProfScope ps(s, [&] { return "ppo_loss/" + cb_dims(int(m), A); });
         return ppo_loss_big(m, A, z, v, act, old_logp, adv, ret, rows, norm_adv, clip, vf, ent, dz, dv, stats, ws, s);
     }
-    float* ms = static_cast<float*>(ws);
+    const float* ms = ms_pre ? ms_pre : static_cast<const float*>(ws);
     double* terms = reinterpret_cast<double*>(static_cast<char*>(ws) + 256);
     const int nb = int((m + kWideRows - 1) / kWideRows);
     const size_t lds = size_t(kWideRows) * A * sizeof(float);
     ProfScope ps(s, [&] { return "ppo_loss/" + cb_dims(int(m), A); });
-    if (rows) hipLaunchKernelGGL(adv_stats_ws_kernel<true>, dim3(1), dim3(kFusedThreads), 0, s, m, adv, rows, ms);
-    else hipLaunchKernelGGL(adv_stats_ws_kernel<false>, dim3(1), dim3(kFusedThreads), 0, s, m, adv, rows, ms);
+    if (!ms_pre) {
+        float* mo = static_cast<float*>(ws);
+        if (rows)
+            hipLaunchKernelGGL(adv_stats_ws_kernel<true>, dim3(1), dim3(kFusedThreads), 0, s, m, adv, rows, 0, 1, 0, mo);
+        else
+            hipLaunchKernelGGL(adv_stats_ws_kernel<false>, dim3(1), dim3(kFusedThreads), 0, s, m, adv, rows, 0, 1, 0, mo);
+    }
 #define CB_PR(AC, RW) \
     hipLaunchKernelGGL((ppo_rows_ws_kernel<AC, RW>), dim3(unsigned(nb)), dim3(kWideRows), lds, s, m, A, z, v, act, \
                        old_logp, adv, ret, rows, norm_adv, clip, vf, ent, dz, dv, ms, terms)
